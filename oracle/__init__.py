@@ -1,0 +1,198 @@
+"""ORACLE -- test infrastructure only.
+
+numpy front end of ``oracle.c``: a plain, slow, destination-centric CPU
+reference for layer-wise GNN inference (Taurus, arXiv 2607.17374), in fp64.
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the GPU library
+in ``paper_2607_17374_amd``; the only common code is the seeded input
+generator in ``fixtures``.
+
+Every function is pinned by the CPU tests in ``tests/test_oracle_pins.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "liboracle.so")
+_SRC = os.path.join(_HERE, "oracle.c")
+
+F32, BF16, F16 = 0, 1, 2
+SAGE_MEAN, GCN_SYM = 0, 1
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_SO):
+        tmp = _SO + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _SO)
+    return _SO
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        _lib = load(_SO)
+    return _lib
+
+
+def load(path: str):
+    """Open a compiled oracle library and declare its entry points."""
+    L = ctypes.CDLL(path)
+    i64, u64, i32, vp = ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p
+    L.or_build_csr.restype = i32
+    L.or_build_csr.argtypes = [i64, i64, vp, vp, vp, vp]
+    L.or_build_in_lists.restype = i32
+    L.or_build_in_lists.argtypes = [i64, vp, vp, vp, vp, vp]
+    L.or_hash.restype = u64
+    L.or_hash.argtypes = [u64, u64, i32, vp]
+    L.or_sample.restype = None
+    L.or_sample.argtypes = [i64, vp, vp, vp, vp, u64, i64, i64, vp, vp, vp]
+    L.or_round_store.restype = None
+    L.or_round_store.argtypes = [i64, vp, i32, vp]
+    L.or_widen.restype = None
+    L.or_widen.argtypes = [i64, vp, i32, vp]
+    L.or_layer.restype = i32
+    L.or_layer.argtypes = [i32, i64, vp, vp, vp, vp, vp, i32, i64, vp, vp, i64, i32, i64, vp, vp]
+    L.or_reorder_bfs.restype = i32
+    L.or_reorder_bfs.argtypes = [i64, vp, vp, vp]
+    L.or_total_span.restype = i64
+    L.or_total_span.argtypes = [i64, vp, vp, vp]
+    return L
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Graph:
+    """CSR by source plus in-neighbour lists, built by the oracle."""
+
+    def __init__(self, n: int, src: np.ndarray, dst: np.ndarray, check_simple: bool = True):
+        src = np.ascontiguousarray(src, np.int32)
+        dst = np.ascontiguousarray(dst, np.int32)
+        e = src.size
+        self.n, self.e = n, e
+        self.row_off = np.empty(n + 1, np.int64)
+        self.col_dst = np.empty(e, np.int32)
+        rc = lib().or_build_csr(n, e, _p(src), _p(dst), _p(self.row_off), _p(self.col_dst))
+        if rc == -2 or rc == -3 or (rc == -1 and check_simple):
+            raise ValueError(f"or_build_csr: {rc}")
+        self.simple = rc == 0
+        self.in_off = np.empty(n + 1, np.int64)
+        self.in_src = np.empty(e, np.int32)
+        self.in_pos = np.empty(e, np.int64)
+        rc = lib().or_build_in_lists(n, _p(self.row_off), _p(self.col_dst), _p(self.in_off),
+                                     _p(self.in_src), _p(self.in_pos))
+        if rc:
+            raise MemoryError("or_build_in_lists")
+        self.deg_out = np.diff(self.row_off).astype(np.int32)
+        self.deg_in = np.diff(self.in_off).astype(np.int32)
+
+
+def hash_u64(seed: int, tag: int, *args: int) -> int:
+    a = np.array(args, dtype=np.uint64) if args else np.zeros(1, np.uint64)
+    return int(lib().or_hash(seed & (2**64 - 1), tag, len(args), _p(a)))
+
+
+def sample(g: Graph, seed: int, layer: int, k: int):
+    """Fanout mask of one layer -> (mask_words uint64[ceil(e/64)], keep_in uint8[e], m int32[n])."""
+    words = np.zeros((g.e + 63) // 64, np.uint64)
+    keep_in = np.zeros(g.e, np.uint8)
+    m = np.zeros(g.n, np.int32)
+    lib().or_sample(g.n, _p(g.row_off), _p(g.in_off), _p(g.in_src), _p(g.in_pos),
+                    seed & (2**64 - 1), layer, k, _p(words), _p(keep_in), _p(m))
+    return words, keep_in, m
+
+
+def layer(agg: int, g: Graph, H: np.ndarray, h_dtype: int, W: np.ndarray, b: np.ndarray | None,
+          relu: bool, keep_in: np.ndarray | None = None, dst_ids: np.ndarray | None = None) -> np.ndarray:
+    """One layer in fp64 for ``dst_ids`` (all vertices if None).
+
+    ``W`` in the paper's orientation (rows = d_out; SAGE cols = 2 d_in =
+    [W_agg | W_self]); ``H`` is the layer input in its storage dtype (16-bit
+    types as uint16 bit patterns)."""
+    H = np.ascontiguousarray(H)
+    d_in = H.shape[1]
+    W = np.ascontiguousarray(W, np.float64)
+    d_out = W.shape[0]
+    cols = 2 * d_in if agg == SAGE_MEAN else d_in
+    assert W.shape[1] == cols, (W.shape, cols)
+    bb = None if b is None else np.ascontiguousarray(b, np.float64)
+    ids = None if dst_ids is None else np.ascontiguousarray(dst_ids, np.int64)
+    count = g.n if ids is None else ids.size
+    out = np.empty((count, d_out), np.float64)
+    kin = None if keep_in is None else np.ascontiguousarray(keep_in, np.uint8)
+    rc = lib().or_layer(agg, g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(g.deg_out),
+                        _p(H), h_dtype, d_in, _p(W), _p(bb), d_out, int(relu),
+                        count, _p(ids), _p(out))
+    if rc:
+        raise RuntimeError(f"or_layer: {rc}")
+    return out
+
+
+def round_store(x: np.ndarray, dtype: int) -> np.ndarray:
+    """fp64 -> fp32 -> (bf16 | fp16), round to nearest even; 16-bit as uint16 bits."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, np.float32 if dtype == F32 else np.uint16)
+    lib().or_round_store(x.size, _p(x), dtype, _p(out))
+    return out
+
+
+def widen(x: np.ndarray, dtype: int) -> np.ndarray:
+    x = np.ascontiguousarray(x)
+    out = np.empty(x.shape, np.float64)
+    lib().or_widen(x.size, _p(x), dtype, _p(out))
+    return out
+
+
+def reorder_bfs(g: Graph) -> np.ndarray:
+    out = np.empty(g.n, np.int32)
+    if lib().or_reorder_bfs(g.n, _p(g.in_off), _p(g.in_src), _p(out)):
+        raise MemoryError("or_reorder_bfs")
+    return out
+
+
+def total_span(g: Graph, pi: np.ndarray) -> int:
+    pi = np.ascontiguousarray(pi, np.int32)
+    return int(lib().or_total_span(g.n, _p(g.in_off), _p(g.in_src), _p(pi)))
+
+
+def mask_bits(words: np.ndarray, e: int) -> np.ndarray:
+    """Unpack a little-endian bit mask (bit i of word i//64) into a bool array of length e."""
+    b = np.unpackbits(np.ascontiguousarray(words, np.uint64).view(np.uint8), bitorder="little")
+    return b[:e].astype(bool)
+
+
+def run_model(w, g: Graph, X: np.ndarray, params):
+    """Full-graph layer-wise inference through every layer of workload ``w``.
+
+    Returns the list of per-layer outputs in storage dtype (hidden layers in
+    the workload's feature dtype, last layer fp32), and the fp64 outputs of
+    the last layer.  Sampled layers draw their fanout masks with the oracle's
+    own sampler."""
+    H, h_dtype = X, w.feat_dtype
+    outs = []
+    z = None
+    for li in range(1, w.layers + 1):
+        p = params[li - 1]
+        keep = None
+        if w.fanout(li) > 0:
+            _, keep, _ = sample(g, w.seed, li, w.fanout(li))
+        relu = li < w.layers
+        z = layer(w.agg, g, H, h_dtype, p.W, p.b, relu, keep_in=keep)
+        _, out_dtype = w.layer_dtypes(li)
+        H = round_store(z, out_dtype)
+        h_dtype = out_dtype
+        outs.append(H)
+    return outs, z

@@ -1,0 +1,381 @@
+/*
+ * ORACLE -- test infrastructure only.
+ *
+ * A plain, slow, destination-centric CPU reference for layer-wise GNN
+ * inference (Taurus, arXiv 2607.17374).  Only the test-suite, the smoke
+ * check and the benchmark's CPU-baseline leg may load this file; the GPU
+ * library never does, and the two share no code.  Everything here is written
+ * to be checked by eye against the paper:
+ *
+ *   - graph storage: CSR by source (Sec. 3.2, "Data Layout"), built by
+ *     sorting the (u, v) pairs, plus in-neighbour lists for the gather;
+ *   - one layer = Aggregate over in-neighbours then Update and activation
+ *     (Background, Eqs. gnn-1 and gnn-2), evaluated per destination in fp64
+ *     with in-neighbours visited in ascending source ID.  The paper states
+ *     that source-centric broadcast is semantically equal to this gather for
+ *     the same message set, Aggregate and Update (Sec. 3.1), so the gather is
+ *     the plain definition of what the GPU path must reach;
+ *   - GraphSAGE with mean aggregation and the concatenated update
+ *     W [h_agg || h_v] (Sec. 3.9, "SAGEConv");
+ *   - GCN with the symmetric normalisation of Kipf and Welling, one self
+ *     loop per vertex (the paper cites the model in Sec. 4.1 without
+ *     writing its formula; the directed-graph reading is documented below);
+ *   - fanout sampling: up to k incoming edges kept per vertex, per layer
+ *     (Sec. 3.9, "Sampling-based Inference"), ranked by a counter-based
+ *     hash;
+ *   - the degree/BFS vertex ordering used as a topology-aware bootstrap
+ *     (Sec. 3.8 discusses bandwidth-style bootstraps; the exact ordering
+ *     rule is this build's reading and is stated at or_reorder_bfs).
+ *
+ * Parity status: every function here is pinned by CPU tests (dense
+ * adjacency-matrix products, closed forms, hand-worked small graphs,
+ * brute force and the published SplitMix64 outputs); none is unpinned.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------ helpers ---- */
+
+typedef struct { int32_t a, b; } or_pair;
+
+static int or_pair_cmp(const void* x, const void* y) {
+    const or_pair* p = (const or_pair*)x; const or_pair* q = (const or_pair*)y;
+    if (p->a != q->a) return p->a < q->a ? -1 : 1;
+    if (p->b != q->b) return p->b < q->b ? -1 : 1;
+    return 0;
+}
+
+/*
+ * CSR by source.  Sort the pairs by (u, v); row u then lists the
+ * destinations of u's out-edges in ascending order.  Returns 0, or -1 if the
+ * list holds a self loop or a repeated pair (the graph must be simple), or
+ * -2 on an ID out of range.
+ */
+int or_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
+                 int64_t* row_off, int32_t* col_dst) {
+    or_pair* p = (or_pair*)malloc((size_t)(e > 0 ? e : 1) * sizeof(or_pair));
+    if (!p) return -3;
+    for (int64_t i = 0; i < e; i++) {
+        if (src[i] < 0 || src[i] >= n || dst[i] < 0 || dst[i] >= n) { free(p); return -2; }
+        p[i].a = src[i]; p[i].b = dst[i];
+    }
+    qsort(p, (size_t)e, sizeof(or_pair), or_pair_cmp);
+    int rc = 0;
+    for (int64_t i = 0; i <= n; i++) row_off[i] = 0;
+    for (int64_t i = 0; i < e; i++) {
+        if (p[i].a == p[i].b) rc = -1;
+        if (i > 0 && p[i].a == p[i - 1].a && p[i].b == p[i - 1].b) rc = -1;
+        row_off[p[i].a + 1]++;
+        col_dst[i] = p[i].b;
+    }
+    for (int64_t u = 0; u < n; u++) row_off[u + 1] += row_off[u];
+    free(p);
+    return rc;
+}
+
+/*
+ * In-neighbour lists: for every destination v, the sources u of its
+ * in-edges (u, v) in ascending order, with in_pos[k] = the CSR position of
+ * that edge (so per-edge flags can be mapped between the two orders).
+ */
+int or_build_in_lists(int64_t n, const int64_t* row_off, const int32_t* col_dst,
+                      int64_t* in_off, int32_t* in_src, int64_t* in_pos) {
+    int64_t e = row_off[n];
+    for (int64_t v = 0; v <= n; v++) in_off[v] = 0;
+    for (int64_t i = 0; i < e; i++) in_off[col_dst[i] + 1]++;
+    for (int64_t v = 0; v < n; v++) in_off[v + 1] += in_off[v];
+    int64_t* fill = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    if (!fill) return -3;
+    for (int64_t v = 0; v < n; v++) fill[v] = in_off[v];
+    /* walking CSR rows in ascending u appends sources in ascending order */
+    for (int64_t u = 0; u < n; u++)
+        for (int64_t i = row_off[u]; i < row_off[u + 1]; i++) {
+            int64_t k = fill[col_dst[i]]++;
+            in_src[k] = (int32_t)u;
+            if (in_pos) in_pos[k] = i;
+        }
+    free(fill);
+    return 0;
+}
+
+/* --------------------------------------------------- counter-based hash -- */
+/*
+ * H(s, t, x1..xk): h = s; for x in (t, x1..xk): h = mix64(h + G + x), with
+ * mix64 the SplitMix64 finaliser and G its golden-ratio increment (Steele,
+ * Lea and Flood, OOPSLA 2014).  The fanout sampler draws with tag 4.
+ */
+static uint64_t or_mix64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+uint64_t or_hash(uint64_t seed, uint64_t tag, int nargs, const uint64_t* args) {
+    uint64_t h = or_mix64(seed + 0x9e3779b97f4a7c15ULL + tag);
+    for (int i = 0; i < nargs; i++) h = or_mix64(h + 0x9e3779b97f4a7c15ULL + args[i]);
+    return h;
+}
+
+/* ------------------------------------------------------ fanout sampler -- */
+typedef struct { uint64_t key; int32_t u; int64_t pos; } or_cand;
+
+static int or_cand_cmp(const void* x, const void* y) {
+    const or_cand* p = (const or_cand*)x; const or_cand* q = (const or_cand*)y;
+    if (p->key != q->key) return p->key < q->key ? -1 : 1;
+    return (p->u > q->u) - (p->u < q->u);
+}
+
+/*
+ * Per-layer fanout mask (Sec. 3.9, "Sampling-based Inference": for fanout k
+ * keep up to k incoming edges per vertex and suppress the rest).  In-edge
+ * (u, v) of layer `layer` gets the rank key (H(seed, 4, layer, v, u), u); for
+ * every v the min(d_in(v), k) smallest keys are kept.  Outputs:
+ *   mask_words  ceil(e/64) words, bit i of the CSR edge order set if kept;
+ *   keep_in     per in-list entry, 1 if kept (may be NULL);
+ *   m_out       |M_layer(v)|, the kept in-degree.
+ * k <= 0 keeps everything (exact inference).
+ */
+void or_sample(int64_t n, const int64_t* row_off, const int64_t* in_off, const int32_t* in_src,
+               const int64_t* in_pos, uint64_t seed, int64_t layer, int64_t k,
+               uint64_t* mask_words, uint8_t* keep_in, int32_t* m_out) {
+    int64_t e = row_off[n];
+    memset(mask_words, 0, (size_t)((e + 63) / 64) * sizeof(uint64_t));
+#pragma omp parallel
+    {
+        or_cand* buf = NULL;
+        int64_t cap = 0;
+#pragma omp for schedule(dynamic, 1024)
+        for (int64_t v = 0; v < n; v++) {
+            int64_t d = in_off[v + 1] - in_off[v];
+            int64_t keep = (k <= 0 || d <= k) ? d : k;
+            m_out[v] = (int32_t)keep;
+            if (d > cap) { cap = d; buf = (or_cand*)realloc(buf, (size_t)cap * sizeof(or_cand)); }
+            for (int64_t j = 0; j < d; j++) {
+                int32_t u = in_src[in_off[v] + j];
+                uint64_t args[3] = {(uint64_t)layer, (uint64_t)v, (uint64_t)u};
+                buf[j].key = or_hash(seed, 4, 3, args);
+                buf[j].u = u;
+                buf[j].pos = in_off[v] + j;
+            }
+            if (keep < d) qsort(buf, (size_t)d, sizeof(or_cand), or_cand_cmp);
+            for (int64_t j = 0; j < d; j++) {
+                int kept = j < keep;
+                int64_t idx = buf[j].pos;            /* in-list index */
+                if (keep_in) keep_in[idx] = (uint8_t)kept;
+                if (kept) {
+                    int64_t p = in_pos[idx];         /* CSR position */
+                    __atomic_fetch_or(&mask_words[p >> 6], 1ULL << (p & 63), __ATOMIC_RELAXED);
+                }
+            }
+        }
+        free(buf);
+    }
+}
+
+/* -------------------------------------------------- precision handling -- */
+/* storage dtypes: 0 fp32, 1 bf16, 2 fp16 (16-bit ones as raw bit patterns) */
+static double or_load(const void* H, int dtype, int64_t idx) {
+    if (dtype == 0) return (double)((const float*)H)[idx];
+    uint16_t b = ((const uint16_t*)H)[idx];
+    if (dtype == 1) {
+        uint32_t x = (uint32_t)b << 16; float f; memcpy(&f, &x, 4); return (double)f;
+    }
+    /* fp16: sign, 5-bit exponent (bias 15), 10-bit fraction */
+    int s = b >> 15, ex = (b >> 10) & 31, fr = b & 1023;
+    double mag;
+    if (ex == 0) mag = ldexp((double)fr, -24);
+    else if (ex == 31) mag = fr ? NAN : INFINITY;
+    else mag = ldexp((double)(1024 + fr), ex - 25);
+    return s ? -mag : mag;
+}
+
+/*
+ * fp64 -> fp32 (round to nearest even, the C conversion) -> optionally the
+ * 16-bit storage type, also round to nearest even.  Written from the IEEE 754
+ * definitions: bf16 keeps the top 16 bits of the fp32 pattern; fp16 keeps 10
+ * fraction bits with exponent bias 15.
+ */
+static uint16_t or_to_bf16(float f) {
+    uint32_t x; memcpy(&x, &f, 4);
+    if ((x & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((x >> 16) | 0x40u);
+    uint32_t lower = x & 0xffffu, upper = x >> 16;
+    if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper++;
+    return (uint16_t)upper;
+}
+static uint16_t or_to_f16(float f) {
+    double a = fabs((double)f);
+    uint16_t sign = signbit(f) ? 0x8000 : 0;
+    if (isnan(f)) return 0x7e00;
+    if (a >= 65520.0) return sign | 0x7c00;                /* rounds past the largest finite */
+    if (a < ldexp(1.0, -14)) {                              /* subnormal: units of 2^-24 */
+        double q = a * ldexp(1.0, 24);
+        double r = nearbyint(q);                            /* ties to even */
+        return sign | (uint16_t)r;
+    }
+    int ex; double m = frexp(a, &ex);                       /* a = m * 2^ex, m in [0.5, 1) */
+    double q = ldexp(m, 11);                                /* 11 significant bits in [1024, 2048) */
+    double r = nearbyint(q);
+    if (r >= 2048.0) { r = 1024.0; ex += 1; }
+    int bexp = ex - 1 + 15;                                 /* value = (r/1024) * 2^(ex-1) */
+    return sign | (uint16_t)(bexp << 10) | (uint16_t)((int)r - 1024);
+}
+void or_round_store(int64_t count, const double* in, int dtype, void* out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; i++) {
+        float f = (float)in[i];
+        if (dtype == 0) ((float*)out)[i] = f;
+        else if (dtype == 1) ((uint16_t*)out)[i] = or_to_bf16(f);
+        else ((uint16_t*)out)[i] = or_to_f16(f);
+    }
+}
+void or_widen(int64_t count, const void* in, int dtype, double* out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; i++) out[i] = or_load(in, dtype, i);
+}
+
+/* ------------------------------------------------------------- layers ---- */
+/*
+ * One GNN layer for the destinations listed in dst_ids (all if NULL), in
+ * fp64.  H is the layer input (n rows of width d_in, storage dtype h_dtype);
+ * W has the paper's orientation (rows = d_out, it maps an input vector to an
+ * output vector) and is given in fp64; bias may be NULL.  keep_in selects the
+ * propagated in-edges (NULL = all, exact inference).
+ *
+ * agg 0, GraphSAGE-mean (Sec. 3.9): with M(v) the propagated in-neighbours,
+ *     a    = (1/|M(v)|) * sum_{u in M(v)} h_u   (0 when M(v) is empty),
+ *     z    = W [a || h_v] + b,  W = [W_agg  W_self],  cols = 2 d_in.
+ * agg 1, GCN, symmetric normalisation with one self loop per vertex on the
+ *     directed graph: d^_out(u) = d_out(u) + 1, d^_in(v) = d_in(v) + 1,
+ *     a    = sum_{u in N-(v)} h_u / sqrt(d^_out(u) d^_in(v))
+ *            + h_v / sqrt(d^_out(v) d^_in(v)),
+ *     z    = W a + b,  cols = d_in.  deg_out is the full out-degree.
+ * Output: out[i][j] = ReLU(z_j) if relu else z_j, for v = dst_ids[i].
+ */
+int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
+             const uint8_t* keep_in, const int32_t* deg_out,
+             const void* H, int h_dtype, int64_t d_in,
+             const double* W, const double* bias, int64_t d_out, int relu,
+             int64_t n_dst, const int64_t* dst_ids, double* out) {
+    int64_t cols = agg == 0 ? 2 * d_in : d_in;
+    int64_t count = dst_ids ? n_dst : n;
+    int bad = 0;
+    if (agg == 1 && keep_in) return -1;   /* GCN is defined here for exact inference only */
+#pragma omp parallel
+    {
+        double* a = (double*)malloc((size_t)cols * sizeof(double));
+        if (!a) bad = 1;
+#pragma omp for schedule(dynamic, 256)
+        for (int64_t i = 0; i < count; i++) {
+            if (!a) continue;
+            int64_t v = dst_ids ? dst_ids[i] : i;
+            for (int64_t j = 0; j < cols; j++) a[j] = 0.0;
+            if (agg == 0) {
+                int64_t m = 0;
+                for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                    if (keep_in && !keep_in[k]) continue;
+                    int64_t u = in_src[k];
+                    for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, u * d_in + j);
+                    m++;
+                }
+                if (m > 0)
+                    for (int64_t j = 0; j < d_in; j++) a[j] = a[j] / (double)m;
+                for (int64_t j = 0; j < d_in; j++) a[d_in + j] = or_load(H, h_dtype, v * d_in + j);
+            } else {
+                double din_hat = (double)(in_off[v + 1] - in_off[v]) + 1.0;
+                for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                    int64_t u = in_src[k];
+                    double c = 1.0 / sqrt(((double)deg_out[u] + 1.0) * din_hat);
+                    for (int64_t j = 0; j < d_in; j++) a[j] += c * or_load(H, h_dtype, u * d_in + j);
+                }
+                double cs = 1.0 / sqrt(((double)deg_out[v] + 1.0) * din_hat);
+                for (int64_t j = 0; j < d_in; j++) a[j] += cs * or_load(H, h_dtype, v * d_in + j);
+            }
+            for (int64_t o = 0; o < d_out; o++) {
+                double z = bias ? bias[o] : 0.0;
+                for (int64_t j = 0; j < cols; j++) z += W[o * cols + j] * a[j];
+                if (relu && z < 0.0) z = 0.0;
+                out[i * d_out + o] = z;
+            }
+        }
+        free(a);
+    }
+    return bad ? -3 : 0;
+}
+
+/* ------------------------------------------------------------ reorder ---- */
+/*
+ * Degree/BFS vertex ordering (this build's reading of an "in-degree-sorted +
+ * BFS" topology-aware ordering; the paper's own ordering is an RCMK
+ * bootstrap refined by its Algorithm 1, Sec. 3.8).
+ *
+ *   - root order: all vertices by (in-degree descending, ID ascending);
+ *   - each root not yet visited starts a breadth-first search over IN-edges
+ *     (from a vertex to its in-neighbours, i.e. its message sources), so a
+ *     destination's sources receive consecutive ranks;
+ *   - a dequeued vertex appends its unvisited in-neighbours in
+ *     (in-degree descending, ID ascending) order;
+ *   - new_of_old[v] = position of v in the visit order.
+ * The order is unique, so results are compared bit for bit.
+ */
+static const int32_t* g_or_deg;
+static int or_rank_cmp(const void* x, const void* y) {
+    int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
+    if (g_or_deg[a] != g_or_deg[b]) return g_or_deg[a] > g_or_deg[b] ? -1 : 1;
+    return (a > b) - (a < b);
+}
+int or_reorder_bfs(int64_t n, const int64_t* in_off, const int32_t* in_src, int32_t* new_of_old) {
+    int32_t* deg = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    int32_t* order = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    int32_t* queue = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    uint8_t* seen = (uint8_t*)calloc((size_t)(n > 0 ? n : 1), 1);
+    int64_t maxd = 0;
+    for (int64_t v = 0; v < n; v++) {
+        deg[v] = (int32_t)(in_off[v + 1] - in_off[v]);
+        if (deg[v] > maxd) maxd = deg[v];
+        order[v] = (int32_t)v;
+    }
+    int32_t* kids = (int32_t*)malloc((size_t)(maxd > 0 ? maxd : 1) * sizeof(int32_t));
+    if (!deg || !order || !queue || !seen || !kids) return -3;
+    g_or_deg = deg;
+    qsort(order, (size_t)n, sizeof(int32_t), or_rank_cmp);
+    int64_t head = 0, tail = 0;
+    for (int64_t r = 0; r < n; r++) {
+        int32_t root = order[r];
+        if (seen[root]) continue;
+        seen[root] = 1;
+        queue[tail++] = root;
+        while (head < tail) {
+            int32_t x = queue[head++];
+            int64_t nk = 0;
+            for (int64_t k = in_off[x]; k < in_off[x + 1]; k++) {
+                int32_t w = in_src[k];
+                if (!seen[w]) { seen[w] = 1; kids[nk++] = w; }
+            }
+            qsort(kids, (size_t)nk, sizeof(int32_t), or_rank_cmp);
+            for (int64_t j = 0; j < nk; j++) queue[tail++] = kids[j];
+        }
+    }
+    for (int64_t i = 0; i < n; i++) new_of_old[queue[i]] = (int32_t)i;
+    free(deg); free(order); free(queue); free(seen); free(kids);
+    return 0;
+}
+
+/*
+ * Total span C(pi) = sum_v (max_{u in N-(v)} pi(u) - min_{u in N-(v)} pi(u))
+ * (Sec. 3.8), over vertices with at least one in-neighbour.
+ */
+int64_t or_total_span(int64_t n, const int64_t* in_off, const int32_t* in_src, const int32_t* pi) {
+    int64_t total = 0;
+    for (int64_t v = 0; v < n; v++) {
+        if (in_off[v + 1] == in_off[v]) continue;
+        int64_t lo = INT64_MAX, hi = INT64_MIN;
+        for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+            int64_t p = pi[in_src[k]];
+            if (p < lo) lo = p;
+            if (p > hi) hi = p;
+        }
+        total += hi - lo;
+    }
+    return total;
+}

@@ -1,0 +1,113 @@
+"""The oracle's pins must be strong enough to catch plausible mistakes.
+
+Each case plants one mistake in a copy of oracle.c (on the CPU, in a
+temporary directory), builds it, points the oracle front end at the mutant
+and runs the pins that should notice.  At least one must fail."""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle as O
+import tests.test_oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(O.__file__), "oracle.c")
+
+MUTANTS = {
+    # GCN: self message dropped
+    "gcn_no_self_term": (
+        "for (int64_t j = 0; j < d_in; j++) a[j] += cs * or_load(H, h_dtype, v * d_in + j);",
+        "(void)cs;",
+        [lambda: P.test_gcn_matches_dense(0, True)]),
+    # GCN: degree without the added self loop
+    "gcn_degree_without_self_loop": (
+        "double c = 1.0 / sqrt(((double)deg_out[u] + 1.0) * din_hat);",
+        "double c = 1.0 / sqrt(((double)deg_out[u] + (deg_out[u] ? 0.0 : 1.0)) * din_hat);",
+        [lambda: P.test_gcn_matches_dense(0, True), P.test_closed_form_gcn_degrees_only]),
+    # GCN: in- and out-degree swapped in the source factor
+    "gcn_degrees_swapped": (
+        "double din_hat = (double)(in_off[v + 1] - in_off[v]) + 1.0;",
+        "double din_hat = (double)deg_out[v] + 1.0;",
+        [lambda: P.test_gcn_matches_dense(1, False)]),
+    # SAGE: mean over all in-neighbours instead of the propagated ones
+    "sage_mean_over_full_degree": (
+        "for (int64_t j = 0; j < d_in; j++) a[j] = a[j] / (double)m;",
+        "for (int64_t j = 0; j < d_in; j++) a[j] = a[j] / (double)(in_off[v + 1] - in_off[v]);",
+        [P.test_sampled_sage_matches_dense_on_kept_edges]),
+    # SAGE: self and neighbour halves of W swapped
+    "sage_halves_swapped": (
+        "for (int64_t j = 0; j < d_in; j++) a[d_in + j] = or_load(H, h_dtype, v * d_in + j);",
+        "for (int64_t j = 0; j < d_in; j++) { double t = a[j]; a[j] = or_load(H, h_dtype, v * d_in + j); a[d_in + j] = t; }",
+        [lambda: P.test_sage_matches_dense(0, True)]),
+    # bias dropped
+    "no_bias": (
+        "double z = bias ? bias[o] : 0.0;",
+        "double z = 0.0;",
+        [lambda: P.test_sage_matches_dense(1, False)]),
+    # activation applied the wrong way round
+    "relu_flipped": (
+        "if (relu && z < 0.0) z = 0.0;",
+        "if (relu && z > 0.0) z = 0.0;",
+        [lambda: P.test_sage_matches_dense(0, True)]),
+    # sampler keeps the largest keys
+    "sampler_keeps_largest": (
+        "int kept = j < keep;",
+        "int kept = j >= d - keep;",
+        [P.test_sampler_brute_force_and_invariants]),
+    # sampler ignores the layer in the hash
+    "sampler_ignores_layer": (
+        "uint64_t args[3] = {(uint64_t)layer, (uint64_t)v, (uint64_t)u};",
+        "uint64_t args[3] = {(uint64_t)1, (uint64_t)v, (uint64_t)u};",
+        [P.test_sampler_brute_force_and_invariants, P.test_sampler_layers_differ]),
+    # hash with the increment left out
+    "hash_without_gamma": (
+        "uint64_t h = or_mix64(seed + 0x9e3779b97f4a7c15ULL + tag);",
+        "uint64_t h = or_mix64(seed + tag);",
+        [lambda: P.test_oracle_hash_matches_published_splitmix64(P_GOLDEN)]),
+    # CSR sorted by destination first
+    "csr_sorted_by_destination": (
+        "if (p->a != q->a) return p->a < q->a ? -1 : 1;\n    if (p->b != q->b) return p->b < q->b ? -1 : 1;",
+        "if (p->b != q->b) return p->b < q->b ? -1 : 1;\n    if (p->a != q->a) return p->a < q->a ? -1 : 1;",
+        [lambda: P.test_csr_brute_force(0)]),
+    # BFS children appended in discovery order instead of (d_in desc, id asc)
+    "bfs_children_unsorted": (
+        "qsort(kids, (size_t)nk, sizeof(int32_t), or_rank_cmp);",
+        "(void)0;",
+        [P.test_reorder_tree_levels, lambda: P.test_reorder_random_graphs_are_valid_bfs_orders(0)]),
+    # BFS over out-edges would need a different graph walk; a root-order slip instead:
+    "bfs_roots_by_id": (
+        "if (g_or_deg[a] != g_or_deg[b]) return g_or_deg[a] > g_or_deg[b] ? -1 : 1;",
+        "if (0) return 0;",
+        [P.test_reorder_star, P.test_reorder_path_and_two_components]),
+    # fp16 rounding truncates
+    "f16_truncates": (
+        "double r = nearbyint(q);\n    if (r >= 2048.0)",
+        "double r = floor(q);\n    if (r >= 2048.0)",
+        [P.test_round_store_matches_library_conversions]),
+}
+
+P_GOLDEN = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "tests", "golden")
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    old, new, pins = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/found"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(old, new))
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-o", str(so), str(path), "-lm"])
+    saved = O._lib
+    O._lib = O.load(str(so))
+    failures = 0
+    try:
+        for pin in pins:
+            try:
+                pin()
+            except (AssertionError, ValueError, RuntimeError):
+                failures += 1
+    finally:
+        O._lib = saved
+    assert failures > 0, f"no pin noticed mutant {name}"

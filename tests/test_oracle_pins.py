@@ -1,0 +1,446 @@
+"""Pins for the CPU oracle: each check below is something other than the
+oracle itself -- a published value, a dense matrix product (numpy), a closed
+form, brute force on a tiny input, or a hand-worked example -- chosen so that
+a plausible slip in the oracle (a dropped term, a swapped degree, a wrong
+index, a transposed weight) fails at least one of them."""
+import numpy as np
+import pytest
+
+import oracle as O
+import fixtures as F
+
+G = 0x9e3779b97f4a7c15
+
+
+def random_digraph(rng, n, p, isolated=0):
+    """Simple random digraph with ``isolated`` vertices that have no edges at all."""
+    A = rng.random((n, n)) < p
+    np.fill_diagonal(A, False)
+    if isolated:
+        iso = rng.choice(n, isolated, replace=False)
+        A[iso, :] = False
+        A[:, iso] = False
+    u, v = np.nonzero(A)
+    perm = rng.permutation(u.size)          # edge list order must not matter
+    return A, u[perm].astype(np.int32), v[perm].astype(np.int32)
+
+
+# --------------------------------------------------------------- hashing --
+
+def test_oracle_hash_matches_published_splitmix64(golden_dir):
+    refs = [int(l, 16) for l in open(f"{golden_dir}/splitmix64_state0.txt")
+            if l.strip() and not l.startswith("#")]
+    for k, ref in enumerate(refs):
+        assert O.hash_u64(0, (k * G) % 2**64) == ref
+
+
+def test_oracle_hash_multi_argument_chain(golden_dir):
+    """H(s, t, x) chains one mix per argument: H(0, 0, G) = mix64(mix64(G) + 2G);
+    with H(0, 0) pinned above, check H(0,0,x) against H(H(0,0) , x) form."""
+    h0 = O.hash_u64(0, 0)
+    for x in (0, 1, 12345):
+        assert O.hash_u64(0, 0, x) == O.hash_u64(h0, x)
+
+
+# ------------------------------------------------------------------- CSR --
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_csr_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    A, u, v = random_digraph(rng, 60, 0.08, isolated=5)
+    g = O.Graph(60, u, v)
+    pairs = sorted(zip(u.tolist(), v.tolist()))
+    assert g.col_dst.tolist() == [b for _, b in pairs]
+    for x in range(60):
+        assert g.row_off[x + 1] - g.row_off[x] == sum(1 for a, _ in pairs if a == x)
+    assert g.row_off[0] == 0 and g.row_off[-1] == u.size
+    assert (np.diff(g.row_off) >= 0).all()
+    assert np.array_equal(g.deg_out, A.sum(1)) and np.array_equal(g.deg_in, A.sum(0))
+    # in-lists: ascending sources, and in_pos points back to the same edge
+    for x in range(60):
+        srcs = g.in_src[g.in_off[x]:g.in_off[x + 1]]
+        assert srcs.tolist() == sorted(np.nonzero(A[:, x])[0].tolist())
+        for k in range(g.in_off[x], g.in_off[x + 1]):
+            p = g.in_pos[k]
+            assert g.col_dst[p] == x and g.row_off[g.in_src[k]] <= p < g.row_off[g.in_src[k] + 1]
+
+
+def test_csr_rejects_non_simple():
+    with pytest.raises(ValueError):
+        O.Graph(4, np.array([0, 1], np.int32), np.array([0, 2], np.int32))   # self loop
+    with pytest.raises(ValueError):
+        O.Graph(4, np.array([0, 0], np.int32), np.array([2, 2], np.int32))   # repeated pair
+    with pytest.raises(ValueError):
+        O.Graph(4, np.array([0], np.int32), np.array([4], np.int32))         # out of range
+
+
+def test_csr_empty_graph():
+    g = O.Graph(5, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert (g.row_off == 0).all() and g.e == 0
+
+
+# --------------------------------------------------------------- sampler --
+
+def test_sampler_brute_force_and_invariants():
+    rng = np.random.default_rng(3)
+    A, u, v = random_digraph(rng, 80, 0.15, isolated=4)
+    g = O.Graph(80, u, v)
+    seed, layer = 17, 2
+    prev = None
+    for k in (1, 2, 3, 5, 8):
+        words, keep_in, m = O.sample(g, seed, layer, k)
+        bits = O.mask_bits(words, g.e)
+        assert np.array_equal(m, np.minimum(g.deg_in, k))
+        assert bits.sum() == m.sum() and keep_in.sum() == m.sum()
+        # brute force: enumerate each v's in-edges, rank by (hash, u), keep k smallest
+        for x in range(80):
+            srcs = g.in_src[g.in_off[x]:g.in_off[x + 1]].tolist()
+            ranked = sorted(srcs, key=lambda s: (O.hash_u64(seed, 4, layer, x, s), s))
+            want = set(ranked[:k])
+            got = {s for j, s in enumerate(srcs) if keep_in[g.in_off[x] + j]}
+            assert got == want
+            # the CSR-order mask holds the same set
+            for s in srcs:
+                row = g.col_dst[g.row_off[s]:g.row_off[s + 1]]
+                p = g.row_off[s] + int(np.searchsorted(row, x))
+                assert bits[p] == (s in want)
+        # nesting: the set for k is inside the set for k+1 ...
+        if prev is not None:
+            assert not (prev & ~bits).any()
+        prev = bits
+
+
+def test_sampler_large_fanout_keeps_everything():
+    rng = np.random.default_rng(4)
+    _, u, v = random_digraph(rng, 50, 0.2)
+    g = O.Graph(50, u, v)
+    words, keep_in, m = O.sample(g, 5, 1, int(g.deg_in.max()))
+    assert O.mask_bits(words, g.e).all() and keep_in.all()
+    assert np.array_equal(m, g.deg_in)
+    words0, _, m0 = O.sample(g, 5, 1, 0)
+    assert O.mask_bits(words0, g.e).all() and np.array_equal(m0, g.deg_in)
+
+
+def test_sampler_layers_differ():
+    rng = np.random.default_rng(5)
+    _, u, v = random_digraph(rng, 120, 0.3)
+    g = O.Graph(120, u, v)
+    w1, _, _ = O.sample(g, 9, 1, 3)
+    w2, _, _ = O.sample(g, 9, 2, 3)
+    assert not np.array_equal(w1, w2)
+
+
+# -------------------------------------------------------- layer maths ------
+
+def dense_sage(A_keep, H, W_agg, W_self, b, relu):
+    """GraphSAGE-mean as dense matrix products: D_M^-1 A_M^T H W_agg^T + H W_self^T + b."""
+    m = A_keep.sum(0).astype(np.float64)
+    inv = np.where(m > 0, 1.0 / np.maximum(m, 1), 0.0)
+    agg = inv[:, None] * (A_keep.T.astype(np.float64) @ H)
+    z = agg @ W_agg.T + H @ W_self.T + b
+    return np.maximum(z, 0) if relu else z
+
+
+def dense_gcn(A, H, W, b, relu):
+    """Symmetric-normalised GCN with self loops as dense products:
+    D_in^-1/2 (A+I)^T D_out^-1/2 H W^T + b, D from the row/column sums of A+I."""
+    Ah = A.astype(np.float64) + np.eye(A.shape[0])
+    dout = Ah.sum(1)
+    din = Ah.sum(0)
+    P = np.diag(din ** -0.5) @ Ah.T @ np.diag(dout ** -0.5)
+    z = P @ H @ W.T + b
+    return np.maximum(z, 0) if relu else z
+
+
+@pytest.mark.parametrize("seed,relu", [(0, True), (1, False), (2, True)])
+def test_sage_matches_dense(seed, relu):
+    rng = np.random.default_rng(seed)
+    n, d_in, d_out = 96, 12, 7
+    A, u, v = random_digraph(rng, n, 0.06, isolated=6)
+    g = O.Graph(n, u, v)
+    H = rng.standard_normal((n, d_in))
+    W = rng.standard_normal((d_out, 2 * d_in))
+    b = rng.standard_normal(d_out)
+    H32 = H.astype(np.float32)
+    got = O.layer(O.SAGE_MEAN, g, H32, O.F32, W, b, relu)
+    ref = dense_sage(A, H32.astype(np.float64), W[:, :d_in], W[:, d_in:], b, relu)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed,relu", [(0, True), (1, False)])
+def test_gcn_matches_dense(seed, relu):
+    rng = np.random.default_rng(seed + 10)
+    n, d_in, d_out = 90, 9, 11
+    A, u, v = random_digraph(rng, n, 0.07, isolated=5)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in))
+    b = rng.standard_normal(d_out)
+    got = O.layer(O.GCN_SYM, g, H32, O.F32, W, b, relu)
+    ref = dense_gcn(A, H32.astype(np.float64), W, b, relu)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_sampled_sage_matches_dense_on_kept_edges():
+    rng = np.random.default_rng(7)
+    n, d_in, d_out = 100, 8, 5
+    A, u, v = random_digraph(rng, n, 0.12, isolated=3)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, 2 * d_in))
+    b = rng.standard_normal(d_out)
+    words, keep_in, _ = O.sample(g, 21, 1, 4)
+    bits = O.mask_bits(words, g.e)
+    A_keep = np.zeros_like(A)
+    src_csr = np.repeat(np.arange(n), np.diff(g.row_off))
+    A_keep[src_csr[bits], g.col_dst[bits]] = True
+    got = O.layer(O.SAGE_MEAN, g, H32, O.F32, W, b, True, keep_in=keep_in)
+    ref = dense_sage(A_keep, H32.astype(np.float64), W[:, :d_in], W[:, d_in:], b, True)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_subset_of_destinations_equals_rows_of_full():
+    rng = np.random.default_rng(8)
+    n = 70
+    A, u, v = random_digraph(rng, n, 0.1)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, 6)).astype(np.float32)
+    W = rng.standard_normal((4, 12))
+    full = O.layer(O.SAGE_MEAN, g, H32, O.F32, W, None, True)
+    ids = np.array([5, 0, 69, 5, 33], np.int64)
+    part = O.layer(O.SAGE_MEAN, g, H32, O.F32, W, None, True, dst_ids=ids)
+    assert np.array_equal(full[ids], part)
+
+
+def test_closed_form_sage_constant_features():
+    """Constant input c*1: every vertex with m >= 1 gets ReLU((W_agg + W_self) c1 + b),
+    vertices with no in-neighbour get ReLU(W_self c1 + b)."""
+    rng = np.random.default_rng(9)
+    n, d = 64, 5
+    A, u, v = random_digraph(rng, n, 0.05, isolated=4)
+    g = O.Graph(n, u, v)
+    c = 0.75
+    H = np.full((n, d), c, np.float32)
+    W = rng.standard_normal((3, 2 * d))
+    b = rng.standard_normal(3)
+    out = O.layer(O.SAGE_MEAN, g, H, O.F32, W, b, True)
+    with_nb = np.maximum((W[:, :d] + W[:, d:]) @ np.full(d, c) + b, 0)
+    without = np.maximum(W[:, d:] @ np.full(d, c) + b, 0)
+    for x in range(n):
+        np.testing.assert_allclose(out[x], with_nb if g.deg_in[x] > 0 else without, rtol=1e-13, atol=1e-13)
+
+
+def test_closed_form_sage_identity_is_neighbour_average():
+    """W_agg = I, W_self = 0, b = 0, no activation: the layer is plain averaging
+    of the in-neighbours' features."""
+    rng = np.random.default_rng(10)
+    n, d = 50, 4
+    A, u, v = random_digraph(rng, n, 0.1, isolated=2)
+    g = O.Graph(n, u, v)
+    H = rng.standard_normal((n, d)).astype(np.float32)
+    W = np.concatenate([np.eye(d), np.zeros((d, d))], axis=1)
+    out = O.layer(O.SAGE_MEAN, g, H, O.F32, W, None, False)
+    for x in range(n):
+        nb = [a for a, bb in zip(u.tolist(), v.tolist()) if bb == x]
+        want = np.mean(H[nb].astype(np.float64), axis=0) if nb else np.zeros(d)
+        np.testing.assert_allclose(out[x], want, rtol=1e-13, atol=1e-13)
+
+
+def test_closed_form_gcn_degrees_only():
+    """Constant c, W = I, b = 0, no activation:
+    out(v) = c * d^_in(v)^-1/2 * sum_{u in N-(v) + {v}} d^_out(u)^-1/2."""
+    rng = np.random.default_rng(11)
+    n, d = 40, 3
+    A, u, v = random_digraph(rng, n, 0.1, isolated=3)
+    g = O.Graph(n, u, v)
+    c = -1.25
+    H = np.full((n, d), c, np.float32)
+    out = O.layer(O.GCN_SYM, g, H, O.F32, np.eye(d), None, False)
+    dout = A.sum(1) + 1.0
+    din = A.sum(0) + 1.0
+    for x in range(n):
+        srcs = list(np.nonzero(A[:, x])[0]) + [x]
+        want = c * din[x] ** -0.5 * sum(dout[s] ** -0.5 for s in srcs)
+        np.testing.assert_allclose(out[x], np.full(d, want), rtol=1e-13)
+
+
+@pytest.mark.parametrize("kind", ["cycle", "complete"])
+def test_closed_form_gcn_regular_symmetric_graph_preserves_constants(kind):
+    n, d, c = 12, 4, 0.3
+    if kind == "cycle":
+        u = np.concatenate([np.arange(n), (np.arange(n) + 1) % n])
+        v = np.concatenate([(np.arange(n) + 1) % n, np.arange(n)])
+    else:
+        uu, vv = np.nonzero(~np.eye(n, dtype=bool))
+        u, v = uu, vv
+    g = O.Graph(n, u.astype(np.int32), v.astype(np.int32))
+    out = O.layer(O.GCN_SYM, g, np.full((n, d), c, np.float32), O.F32, np.eye(d), None, False)
+    np.testing.assert_allclose(out, float(np.float32(c)), rtol=1e-13)
+
+
+def test_gcn_symmetric_equals_kipf_form():
+    """On a symmetric graph the directed reading reduces to D^-1/2 (A+I) D^-1/2."""
+    rng = np.random.default_rng(12)
+    n = 30
+    A = rng.random((n, n)) < 0.15
+    A = A | A.T
+    np.fill_diagonal(A, False)
+    u, v = np.nonzero(A)
+    g = O.Graph(n, u.astype(np.int32), v.astype(np.int32))
+    H = rng.standard_normal((n, 5)).astype(np.float32)
+    W = rng.standard_normal((5, 5))
+    Ah = A + np.eye(n)
+    Dm = np.diag(Ah.sum(1) ** -0.5)
+    ref = Dm @ Ah @ Dm @ H.astype(np.float64) @ W.T
+    got = O.layer(O.GCN_SYM, g, H, O.F32, W, None, False)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_layer_16bit_inputs_widen_exactly():
+    rng = np.random.default_rng(13)
+    n, d = 30, 4
+    A, u, v = random_digraph(rng, n, 0.2)
+    g = O.Graph(n, u, v)
+    x32 = rng.standard_normal((n, d)).astype(np.float32)
+    W = rng.standard_normal((3, 2 * d))
+    for code in (F.BF16, F.F16):
+        bits = F.round16(x32, code)
+        wide = F.bits_to_float(bits, code).reshape(n, d)
+        assert np.array_equal(O.widen(bits, code), wide.astype(np.float64))
+        got = O.layer(O.SAGE_MEAN, g, bits, code, W, None, False)
+        ref = O.layer(O.SAGE_MEAN, g, wide, O.F32, W, None, False)
+        assert np.array_equal(got, ref)
+
+
+def test_round_store_matches_library_conversions():
+    import torch
+    rng = np.random.default_rng(14)
+    x = np.concatenate([rng.standard_normal(2000) * 10.0 ** rng.integers(-9, 5, 2000),
+                        [0.0, -0.0, 65519.99, 65520.0, 1e6, 2**-24, 2**-25, 1 + 2**-11]])
+    f32 = O.round_store(x, O.F32)
+    assert np.array_equal(f32, x.astype(np.float32))
+    assert np.array_equal(O.round_store(x, O.F16), x.astype(np.float32).astype(np.float16).view(np.uint16))
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(O.round_store(x, O.BF16), ref)
+
+
+# --------------------------------------------------------------- reorder --
+
+def _g(n, edges):
+    e = np.array(edges, np.int32).reshape(-1, 2)
+    return O.Graph(n, e[:, 0].copy(), e[:, 1].copy())
+
+
+def test_reorder_star():
+    # leaves 1..5 send to hub 0: hub first, then its sources by (d_in desc, id)
+    g = _g(6, [(i, 0) for i in range(1, 6)])
+    pi = O.reorder_bfs(g)
+    assert pi.tolist() == [0, 1, 2, 3, 4, 5]
+    # same star with the hub named 5
+    g = _g(6, [(i, 5) for i in range(0, 5)])
+    assert O.reorder_bfs(g).tolist() == [1, 2, 3, 4, 5, 0]
+
+
+def test_reorder_edgeless_is_identity():
+    g = O.Graph(7, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert O.reorder_bfs(g).tolist() == list(range(7))
+
+
+def test_reorder_path_and_two_components():
+    # path 0 -> 1 -> 2 -> 3: in-degrees 0,1,1,1; root order 1, 2, 3, 0.
+    # BFS over in-edges from 1 visits 0; root 2 adds only itself (its
+    # in-neighbour 1 is seen), and so does root 3.
+    g = _g(4, [(0, 1), (1, 2), (2, 3)])
+    order = [1, 0, 2, 3]                       # visit order worked by hand
+    pi = O.reorder_bfs(g)
+    assert [int(np.nonzero(pi == i)[0][0]) for i in range(4)] == order
+    # two components: {4 <- 5, 4 <- 6, 6 <- 7} and {0 <- 1, 0 <- 2, 0 <- 3}
+    g = _g(8, [(5, 4), (6, 4), (7, 6), (1, 0), (2, 0), (3, 0)])
+    # d_in: 0:3, 4:2, 6:1, others 0.  Roots: 0 (3), then 4 (2), then 6 (seen), ...
+    # BFS(0): 0, 1, 2, 3.  BFS(4): 4, then in-nbrs {5 (d 0), 6 (d 1)} -> 6, 5; then 7 from 6.
+    order = [0, 1, 2, 3, 4, 6, 5, 7]
+    pi = O.reorder_bfs(g)
+    assert [int(np.nonzero(pi == i)[0][0]) for i in range(8)] == order
+
+
+def test_reorder_tree_levels():
+    # a binary in-tree: 1,2 -> 0; 3,4 -> 1; 5,6 -> 2; extra 6 -> 4 gives 4 d_in 1
+    g = _g(7, [(1, 0), (2, 0), (3, 1), (4, 1), (5, 2), (6, 2), (6, 4)])
+    # d_in: 0:2, 1:2, 2:2, 4:1.  Root 0.  Children of 0: {1, 2} tie on d_in 2 -> 1, 2.
+    # children of 1: {3 (0), 4 (1)} -> 4, 3; children of 2: {5, 6} (6 not yet seen) -> 5, 6
+    # children of 4: {6} already seen.
+    order = [0, 1, 2, 4, 3, 5, 6]
+    pi = O.reorder_bfs(g)
+    assert [int(np.nonzero(pi == i)[0][0]) for i in range(7)] == order
+
+
+def bfs_order_is_valid(g, pi):
+    """Properties that characterise the ordering: a bijection; each vertex is
+    either a root (first unvisited in root order at its time) or appears after
+    the earliest-ranked vertex that has it as an in-neighbour (its discoverer);
+    children of one discoverer are contiguous in (d_in desc, id asc) order and
+    blocks of children follow their discoverers' order."""
+    n = g.n
+    order = np.empty(n, np.int64)
+    order[pi] = np.arange(n)
+    assert np.array_equal(np.sort(pi), np.arange(n))
+    key = lambda x: (-int(g.deg_in[x]), int(x))
+    pos = pi
+    disc = np.full(n, -1)
+    # discoverer of w: the earliest vertex (by position) before w that lists w as in-neighbour
+    for x in order:
+        for k in range(g.in_off[x], g.in_off[x + 1]):
+            w = g.in_src[k]
+            if pos[w] > pos[x] and disc[w] < 0:
+                disc[w] = x
+    roots = [x for x in order if disc[x] < 0]
+    # roots appear in root order among themselves
+    assert roots == sorted(roots, key=key)
+    # a root is the first unvisited vertex in global root order when it starts
+    rank = sorted(range(n), key=key)
+    for r in roots:
+        earlier = [x for x in rank[:rank.index(r)]]
+        assert all(pos[x] < pos[r] for x in earlier)
+    # non-roots in visit order: discoverer positions never decrease (blocks of
+    # children are contiguous and follow their parents' order), and each
+    # block is sorted by (d_in desc, id asc)
+    last = -1
+    for i, x in enumerate(order):
+        if disc[x] < 0:
+            continue
+        assert pos[disc[x]] < pos[x]
+        assert pos[disc[x]] >= last
+        if pos[disc[x]] == last:
+            assert key(order[i - 1]) < key(x)
+        last = pos[disc[x]]
+    return True
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_reorder_random_graphs_are_valid_bfs_orders(seed):
+    rng = np.random.default_rng(seed + 40)
+    _, u, v = random_digraph(rng, 70, 0.03, isolated=5)
+    g = O.Graph(70, u, v)
+    assert bfs_order_is_valid(g, O.reorder_bfs(g))
+
+
+def test_total_span_hand_example():
+    # v=3 has in-nbrs 0,1,2 at ranks 0,1,2 -> span 2; v=0 has in-nbr 2 -> span 0
+    g = _g(4, [(0, 3), (1, 3), (2, 3), (2, 0)])
+    assert O.total_span(g, np.arange(4, dtype=np.int32)) == 2
+    assert O.total_span(g, np.array([3, 0, 1, 2], np.int32)) == 3 - 0
+
+
+def test_span_equals_sum_of_active_counts():
+    """C(pi) = sum_t A(t) with A(t) = #{v : a(v) <= t < c(v)} (Sec. 3.8)."""
+    rng = np.random.default_rng(50)
+    _, u, v = random_digraph(rng, 40, 0.1)
+    g = O.Graph(40, u, v)
+    pi = rng.permutation(40).astype(np.int32)
+    total = 0
+    for t in range(40):
+        for x in range(40):
+            srcs = g.in_src[g.in_off[x]:g.in_off[x + 1]]
+            if srcs.size and pi[srcs].min() <= t < pi[srcs].max():
+                total += 1
+    assert O.total_span(g, pi) == total
