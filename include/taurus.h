@@ -1,0 +1,210 @@
+/*
+ * taurus.h -- C ABI of the MI355X layer-wise broadcast GNN inference library.
+ *
+ * Method: Taurus (arXiv 2607.17374).  Layer-wise inference (Sec. 2.3)
+ * recast as source-centric broadcast (Sec. 3.1): every layer streams each
+ * source vertex once, in chunks of contiguous vertex IDs (Sec. 3.3), pushes
+ * one message per propagated out-edge into its destination's partial
+ * aggregate, counts pending messages per destination (Sec. 3.4) and
+ * finalises a destination as soon as its count reaches zero (Sec. 3.6).
+ * Mean aggregation sends the normalised message h_u / |M(v)| (Sec. 3.4);
+ * GraphSAGE splits W = [W_agg W_self] so the self half is applied where the
+ * vertex is streamed (Sec. 3.9, "SAGEConv"); fanout-sampled inference keeps
+ * up to k in-edges per vertex and layer (Sec. 3.9, "Sampling-based
+ * Inference").
+ *
+ * All pointers named "device" are HIP device pointers on the current device;
+ * "host" pointers are ordinary host memory unless marked pinned (allocated
+ * with hipHostMalloc or an equivalent page-locked allocator).  Every call
+ * returns a taurus_status; on failure taurus_last_error() returns a
+ * human-readable message for the calling thread.  No C++ exception crosses
+ * this boundary.  A layer handle must be used by one thread at a time.
+ */
+#ifndef TAURUS_H
+#define TAURUS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TAURUS_OK = 0,
+    TAURUS_E_INVALID = -1,    /* bad argument; nothing was enqueued, handle unchanged        */
+    TAURUS_E_OOM = -2,        /* device or pinned allocation failed; handle poisoned          */
+    TAURUS_E_DEVICE = -3,     /* HIP runtime error; handle poisoned                           */
+    TAURUS_E_STATE = -4,      /* call out of order, chunk pushed twice, or poisoned handle    */
+    TAURUS_E_INCOMPLETE = -5, /* finalize found destinations with messages still pending      */
+    TAURUS_E_BUDGET = -6      /* library allocations would exceed desc.hbm_budget             */
+} taurus_status;
+
+typedef enum { TAURUS_F32 = 0, TAURUS_BF16 = 1, TAURUS_F16 = 2 } taurus_dtype;
+
+/* Aggregation/update families (Sec. 3.9 and the models of Sec. 4.1). */
+typedef enum {
+    TAURUS_SAGE_MEAN = 0, /* z_v = W_agg mean_{u in M(v)} h_u + W_self h_v + b (mean = 0 if M(v) empty)  */
+    TAURUS_GCN_SYM = 1    /* z_v = W sum_{u in N-(v) + {v}} h_u / sqrt(d^_out(u) d^_in(v)) + b,
+                             d^ = degree + 1 (one self loop per vertex); exact inference only         */
+} taurus_agg;
+
+/*
+ * Graph in CSR by source (Sec. 3.2: the topology is stored as CSR over
+ * out-edges so sources can be scanned sequentially).  Device pointers,
+ * caller-owned, read-only, valid until every layer built on it is destroyed:
+ *   row_off  int64[n+1], row_off[0] = 0, row_off[n] = e, non-decreasing;
+ *   col_dst  int32[e], destinations of row u in row_off[u]..row_off[u+1]-1,
+ *            strictly ascending within a row, no self loops.
+ * Edge (u, v) carries u's message to v; N-(v) = { u : (u, v) in E }.
+ */
+typedef struct {
+    int64_t n;
+    int64_t e;
+    const int64_t* row_off;
+    const int32_t* col_dst;
+} taurus_graph;
+
+/*
+ * One layer.  Host-side descriptor, copied at taurus_layer_init.
+ *   agg          taurus_agg.
+ *   d_in, d_out  input and output widths; multiples of 4, d_out <= 1024.
+ *   in_dtype     storage type of the layer input x (taurus_dtype).
+ *   out_dtype    storage type of the layer output (hidden layers usually keep
+ *                the input type; values are rounded to nearest even).
+ *   relu         1 applies ReLU to the output (all layers but the last).
+ *   weight       HOST fp32, row-major, copied at init.  GCN: [d_in][d_out],
+ *                y = x W.  SAGE: [d_in][2*d_out] = [W_agg^T | W_self^T], so
+ *                columns 0..d_out-1 act on the neighbour mean and columns
+ *                d_out..2*d_out-1 on the vertex's own input.  For 16-bit
+ *                in_dtype the weights are rounded to that type at init.
+ *   bias         HOST fp32 [d_out], or NULL for no bias; copied at init.
+ *   fanout       0 = exact inference (every in-edge propagates); k > 0 keeps
+ *                for each destination v its min(d_in(v), k) in-edges whose
+ *                rank key (H(seed, 4, layer, v, u), u) is smallest, where H
+ *                is the SplitMix64-based counter hash of taurus_hash().
+ *   layer        1-based layer number (only feeds the sampling hash).
+ *   seed         sampling seed.
+ *   chunk        source-chunk size C in vertices (> 0).  Chunk j covers
+ *                sources [j*C, min((j+1)*C, n)).
+ *   hbm_budget   bytes of device memory the library may allocate for this
+ *                layer (0 = unlimited); init fails with TAURUS_E_BUDGET if
+ *                the layer's structures do not fit.
+ *   hub_fraction fraction of vertices, by in-degree, whose accumulators stay
+ *                resident; only meaningful with an hbm_budget (reserved).
+ *   out          caller-owned [n][d_out] array of out_dtype receiving the
+ *                layer output; each row is written exactly once, when its
+ *                vertex completes.  Device memory unless out_on_host = 1.
+ *   out_on_host  0: out is device memory (only value supported now).
+ *   stream       hipStream_t on which all work of this layer is enqueued
+ *                (NULL = the default stream).
+ *   profile      1: time every kernel of the layer with HIP events; the
+ *                totals are returned in taurus_stats.
+ */
+typedef struct {
+    int32_t agg, d_in, d_out, in_dtype, out_dtype, relu;
+    const float* weight;
+    const float* bias;
+    int32_t fanout, layer;
+    uint64_t seed;
+    int64_t chunk;
+    int64_t hbm_budget;
+    double hub_fraction;
+    void* out;
+    int32_t out_on_host;
+    void* stream;
+    int32_t profile;
+} taurus_layer_desc;
+
+typedef struct taurus_layer taurus_layer;
+
+/* Per-layer statistics, filled by taurus_finalize. */
+typedef struct {
+    int64_t n, e;                  /* graph size                                        */
+    int64_t messages;              /* E_l: propagated in-edges (sum of |M(v)|)          */
+    int64_t self_terms;            /* self messages (= n)                               */
+    int64_t pairs;                 /* P_l: touched (destination, chunk) pairs incl. self */
+    int64_t completed;             /* vertices whose output row was written             */
+    int64_t pending_left;          /* vertices still waiting for messages               */
+    int64_t chunks, chunks_pushed;
+    int64_t tiles, split_segments; /* scatter work tiles, segments spanning tiles       */
+    int64_t evictions, reloads;    /* accumulator rows moved to/from host (0 in core)   */
+    int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
+    double hub_message_share;      /* share of messages landing on resident hubs        */
+    /* milliseconds, HIP-event timed when desc.profile = 1 (else 0) */
+    double ms_init, ms_gemm, ms_scatter, ms_fixup;
+    int64_t launches_gemm, launches_scatter, launches_fixup;
+} taurus_stats;
+
+/* Thread-local message describing the last failing call on this thread. */
+const char* taurus_last_error(void);
+
+/*
+ * H(seed, tag, args...) = mix64 chain of SplitMix64 (Steele, Lea and Flood,
+ * OOPSLA 2014): h = seed; for x in (tag, args...): h = mix64(h + G + x),
+ * G = 0x9e3779b97f4a7c15.  Host function, exported so callers can reproduce
+ * the sampling keys.  nargs <= 8.
+ */
+uint64_t taurus_hash(uint64_t seed, uint64_t tag, int32_t nargs, const uint64_t* args);
+
+/*
+ * Build CSR by source from an edge list (Sec. 3.2).  All arrays are device
+ * memory: src, dst int32[e] (read), row_off int64[n+1] and col_dst int32[e]
+ * (written, caller-owned).  The edge list must describe a simple graph
+ * (0 <= ids < n, no self loops, no repeated pair); otherwise
+ * TAURUS_E_INVALID and the outputs are unspecified.  The result is
+ * canonical: rows sorted by destination.  Enqueued on `stream`; returns after
+ * the work completed (it reads back a validity flag).  n < 2^31, e < 2^40.
+ */
+int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
+                     int64_t* row_off, int32_t* col_dst, void* stream);
+
+/*
+ * Create the state of one layer: copies the weights, computes degrees and
+ * normalisers, draws the fanout mask (fanout > 0), sets every vertex's
+ * pending-message count to |M(v)| + 1 (the self message counts as one
+ * arrival) and builds the per-chunk destination index.  *out receives the
+ * handle.  Blocks until the index is built.
+ */
+int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_layer** out);
+
+/*
+ * Stream one source chunk through the layer (Sec. 3.3-3.6): transform the
+ * chunk's rows, push their messages to the destinations and finalise every
+ * destination whose last message arrives.  [src_begin, src_end) must be a
+ * whole chunk: src_begin = j*chunk, src_end = min(src_begin + chunk, n).
+ * x points at the chunk's rows (row src_begin first), row-major
+ * [src_end - src_begin][d_in] of in_dtype; device memory if x_on_host = 0
+ * (the only value supported now).  x must stay valid and unchanged until
+ * the next call on this handle returns.  Chunks may be pushed in any order;
+ * each exactly once (a repeat returns TAURUS_E_STATE).  Asynchronous on the
+ * layer's stream.
+ */
+int taurus_push_chunk(taurus_layer* L, int64_t src_begin, int64_t src_end, const void* x,
+                      int32_t x_on_host);
+
+/*
+ * Wait for the layer's work, check that every destination completed and fill
+ * *stats (may be NULL).  Returns TAURUS_E_INCOMPLETE (with the count in
+ * stats->pending_left) if some destination still has pending messages, e.g.
+ * because a chunk was never pushed.  After TAURUS_OK every row of desc.out
+ * holds its final value.
+ */
+int taurus_finalize(taurus_layer* L, taurus_stats* stats);
+
+/*
+ * Copy the layer's propagated-edge mask to host memory: bit i of
+ * mask_bits_host[i / 64] (least significant bit first) is set if CSR edge i
+ * propagates in this layer (all ones for exact layers).  mask_bits_host has
+ * ceil(e/64) words; *n_kept receives the number of set bits (may be NULL).
+ * Synchronises the layer's stream.
+ */
+int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_kept);
+
+/* Release everything the layer allocated.  NULL is ignored. */
+void taurus_layer_destroy(taurus_layer* L);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TAURUS_H */

@@ -1,0 +1,139 @@
+"""Torch-facing wrapper of the C ABI.
+
+Torch provides device memory and streams; each function below only turns
+tensors into pointers and calls the library.  Names follow the C ABI:
+``build_csr`` = taurus_build_csr, ``Layer`` = taurus_layer_init / push_chunk /
+finalize / sampled_edges / destroy.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _native as N
+
+_TORCH_DTYPE = {N.F32: torch.float32, N.BF16: torch.bfloat16, N.F16: torch.float16}
+
+
+def torch_dtype(code: int):
+    return _TORCH_DTYPE[code]
+
+
+def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dev_ptr(t: torch.Tensor, dtype: torch.dtype, what: str) -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+def hash_u64(seed: int, tag: int, *args: int) -> int:
+    a = (ctypes.c_uint64 * max(1, len(args)))(*args)
+    return int(N.lib().taurus_hash(seed & (2**64 - 1), tag, len(args), ctypes.cast(a, ctypes.c_void_p)))
+
+
+def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
+    """taurus_build_csr: device edge list (int32) -> (row_off int64[n+1], col_dst int32[e])."""
+    e = src.numel()
+    row_off = torch.empty(n + 1, dtype=torch.int64, device=src.device)
+    col_dst = torch.empty(max(e, 1), dtype=torch.int32, device=src.device)[:e]
+    N.check(N.lib().taurus_build_csr(n, e, _dev_ptr(src, torch.int32, "src"), _dev_ptr(dst, torch.int32, "dst"),
+                                     row_off.data_ptr(), col_dst.data_ptr() if e else None,
+                                     _stream_ptr(stream)), "taurus_build_csr")
+    return row_off, col_dst
+
+
+class Layer:
+    """One layer handle (taurus_layer_init ... taurus_layer_destroy)."""
+
+    def __init__(self, n: int, row_off: torch.Tensor, col_dst: torch.Tensor, *, agg: int, d_in: int,
+                 d_out: int, weight_cat: np.ndarray, bias: Optional[np.ndarray], out: torch.Tensor,
+                 in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
+                 layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
+                 hub_fraction: float = 0.0, stream=None, profile: bool = False):
+        self._h = ctypes.c_void_p()
+        e = col_dst.numel()
+        self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
+                             col_dst.data_ptr() if e else None)
+        self._w = np.ascontiguousarray(weight_cat, dtype=np.float32)
+        self._b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        self.out = out
+        self.n, self.d_in, self.d_out, self.chunk, self.in_dtype = n, d_in, d_out, chunk, in_dtype
+        self.desc = N.LayerDesc(
+            agg=agg, d_in=d_in, d_out=d_out, in_dtype=in_dtype, out_dtype=out_dtype, relu=int(relu),
+            weight=self._w.ctypes.data, bias=None if self._b is None else self._b.ctypes.data,
+            fanout=fanout, layer=layer, seed=seed & (2**64 - 1), chunk=chunk, hbm_budget=hbm_budget,
+            hub_fraction=hub_fraction, out=_dev_ptr(out, _TORCH_DTYPE[out_dtype], "out"), out_on_host=0,
+            stream=_stream_ptr(stream), profile=int(profile))
+        self._keep = (row_off, col_dst)
+        N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
+                                          ctypes.byref(self._h)), "taurus_layer_init")
+
+    def push_chunk(self, begin: int, end: int, x: torch.Tensor) -> None:
+        """taurus_push_chunk with x = rows [begin, end) on the device."""
+        ptr = _dev_ptr(x, _TORCH_DTYPE[self.in_dtype], "x")
+        N.check(N.lib().taurus_push_chunk(self._h, begin, end, ptr, 0), "taurus_push_chunk")
+
+    def push_all(self, x: torch.Tensor, order: Optional[Sequence[int]] = None) -> None:
+        """Stream every chunk of the full input x [n][d_in] (vertex order by default)."""
+        nchunks = (self.n + self.chunk - 1) // self.chunk
+        for j in (range(nchunks) if order is None else order):
+            b, e = j * self.chunk, min((j + 1) * self.chunk, self.n)
+            self.push_chunk(b, e, x[b:e])
+
+    def finalize(self) -> dict:
+        st = N.Stats()
+        rc = N.lib().taurus_finalize(self._h, ctypes.byref(st))
+        d = st.as_dict()
+        if rc != N.OK:
+            raise N.TaurusError(rc, "taurus_finalize", N.last_error())
+        return d
+
+    def sampled_edges(self):
+        """(mask_words uint64[ceil(e/64)], n_kept)."""
+        words = np.zeros((self.graph.e + 63) // 64, dtype=np.uint64)
+        kept = ctypes.c_int64()
+        N.check(N.lib().taurus_sampled_edges(self._h, words.ctypes.data if words.size else None,
+                                             ctypes.byref(kept)), "taurus_sampled_edges")
+        return words, kept.value
+
+    def destroy(self) -> None:
+        if self._h:
+            N.lib().taurus_layer_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def run_layers(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, x: torch.Tensor, layers: list,
+               *, chunk: int, stream=None, profile: bool = False, outs: Optional[list] = None):
+    """Layer-wise inference: layer l's output is layer l+1's input.
+
+    ``layers`` holds dicts with keys agg, d_in, d_out, weight_cat, bias,
+    in_dtype, out_dtype, relu, fanout, layer, seed.  Returns (outputs, stats)."""
+    h = x
+    results, stats = [], []
+    for i, spec in enumerate(layers):
+        out = outs[i] if outs is not None else torch.empty(
+            (n, spec["d_out"]), dtype=_TORCH_DTYPE[spec.get("out_dtype", N.F32)], device=x.device)
+        L = Layer(n, row_off, col_dst, out=out, chunk=chunk, stream=stream, profile=profile, **spec)
+        L.push_all(h)
+        stats.append(L.finalize())
+        L.destroy()
+        results.append(out)
+        h = out
+    return results, stats

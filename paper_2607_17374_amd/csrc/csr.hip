@@ -1,0 +1,77 @@
+// CSR by source (Sec. 3.2: topology is stored as CSR over out-edges so that
+// sources are scanned in vertex order).  Built by a stable radix sort of the
+// (u, v) pairs packed into 64-bit keys; row offsets come from a binary search
+// of each row's first key in the sorted array.
+#include "internal.hpp"
+
+namespace taurus {
+
+// pack (u, v) into u << vbits | v and flag out-of-range ids and self loops
+__global__ void k_pack_edges(const int32_t* __restrict__ src, const int32_t* __restrict__ dst, int64_t e,
+                             int64_t n, int vbits, uint64_t* __restrict__ keys, int* __restrict__ bad) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= e) return;
+    const int64_t u = src[i], v = dst[i];
+    if (u < 0 || u >= n || v < 0 || v >= n || u == v) {
+        atomicOr(bad, 1);
+        keys[i] = 0;
+        return;
+    }
+    keys[i] = ((uint64_t)u << vbits) | (uint64_t)v;
+}
+
+// col_dst from the sorted keys; a key equal to its predecessor is a repeat
+__global__ void k_unpack_cols(const uint64_t* __restrict__ keys, int64_t e, int vbits,
+                              int32_t* __restrict__ col_dst, int* __restrict__ bad) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= e) return;
+    const uint64_t k = keys[i];
+    col_dst[i] = (int32_t)(k & (((uint64_t)1 << vbits) - 1));
+    if (i > 0 && keys[i - 1] == k) atomicOr(bad, 2);
+}
+
+// row_off[u] = first position whose source is >= u (binary search), u in [0, n]
+__global__ void k_row_offsets(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
+                              int64_t* __restrict__ row_off) {
+    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (u > n) return;
+    const uint64_t target = (uint64_t)u << vbits;
+    int64_t lo = 0, hi = e;
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if (keys[mid] < target) lo = mid + 1;
+        else hi = mid;
+    }
+    row_off[u] = lo;
+}
+
+int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                   int32_t* col_dst, hipStream_t s) {
+    if (n <= 0 || n >= ((int64_t)1 << 31) || e < 0 || e >= ((int64_t)1 << 40))
+        fail(TAURUS_E_INVALID, "taurus_build_csr: n=%lld e=%lld out of range", (long long)n, (long long)e);
+    if (!row_off || (e > 0 && (!src || !dst || !col_dst)))
+        fail(TAURUS_E_INVALID, "taurus_build_csr: null pointer");
+    Arena arena;
+    const int vbits = bits_for(n - 1) > 0 ? bits_for(n - 1) : 1;
+    int* bad = arena.alloc<int>(1, "flag");
+    TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));
+    uint64_t* keys = arena.alloc<uint64_t>(e > 0 ? e : 1, "edge keys");
+    const int T = 256;
+    if (e > 0) {
+        k_pack_edges<<<(unsigned)ceil_div(e, T), T, 0, s>>>(src, dst, e, n, vbits, keys, bad);
+        TAURUS_CHECK_LAUNCH();
+        radix_sort_u64(keys, nullptr, e, 2 * vbits, arena, s);
+        k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(keys, e, vbits, col_dst, bad);
+        TAURUS_CHECK_LAUNCH();
+    }
+    k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(keys, e, n, vbits, row_off);
+    TAURUS_CHECK_LAUNCH();
+    int hbad = 0;
+    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    if (hbad & 1) fail(TAURUS_E_INVALID, "taurus_build_csr: vertex id out of range or self loop");
+    if (hbad & 2) fail(TAURUS_E_INVALID, "taurus_build_csr: repeated edge");
+    return TAURUS_OK;
+}
+
+}  // namespace taurus

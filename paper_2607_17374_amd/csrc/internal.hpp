@@ -1,0 +1,89 @@
+// Internal helpers of the HIP library: status propagation, error text,
+// tracked device allocations and the primitive entry points shared by the
+// translation units (scan, radix sort).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/taurus.h"
+
+namespace taurus {
+
+void set_error(const char* fmt, ...);
+
+// Thrown inside the library only; every C entry point catches it.
+struct Failure {
+    int status;
+};
+
+[[noreturn]] void fail(int status, const char* fmt, ...);
+
+#define TAURUS_HIP(expr)                                                                   \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess) {                                                            \
+            ::taurus::fail(e_ == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE,     \
+                           "%s failed: %s (%s:%d)", #expr, hipGetErrorString(e_), __FILE__, \
+                           __LINE__);                                                      \
+        }                                                                                  \
+    } while (0)
+
+#define TAURUS_CHECK_LAUNCH() TAURUS_HIP(hipGetLastError())
+
+// Device allocations owned by one object, with a byte budget.
+class Arena {
+public:
+    explicit Arena(int64_t budget = 0) : budget_(budget) {}
+    ~Arena() { release(); }
+    Arena(const Arena&) = delete;
+    Arena& operator=(const Arena&) = delete;
+
+    template <typename T>
+    T* alloc(int64_t count, const char* what) {
+        return static_cast<T*>(alloc_bytes(count * (int64_t)sizeof(T), what));
+    }
+    void* alloc_bytes(int64_t bytes, const char* what);
+    void free_ptr(void* p);
+    void release();
+    void set_budget(int64_t budget) { budget_ = budget; }
+    int64_t bytes() const { return bytes_; }
+    int64_t peak() const { return peak_; }
+
+private:
+    struct Block {
+        void* p;
+        int64_t bytes;
+    };
+    std::vector<Block> blocks_;
+    int64_t budget_ = 0, bytes_ = 0, peak_ = 0;
+};
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int bits_for(int64_t maxval) {  // bits needed to represent 0..maxval
+    int b = 0;
+    while (b < 63 && ((int64_t)1 << b) <= maxval) b++;
+    return b;
+}
+
+// ---- primitives (prims.hip) ------------------------------------------------
+// Exclusive prefix sum of n uint32 counts into uint64 offsets; out[n] = total
+// when out has n+1 slots (write_total).  Temporary storage from `arena`.
+void scan_u32_to_u64(const uint32_t* in, uint64_t* out, int64_t n, bool write_total, Arena& arena,
+                     hipStream_t s);
+// Same for int32 inputs into int64 outputs.
+void scan_i32_to_i64(const int32_t* in, int64_t* out, int64_t n, bool write_total, Arena& arena,
+                     hipStream_t s);
+
+// Stable LSD radix sort of 64-bit keys over bits [0, key_bits), carrying
+// optional 32-bit values.  keys/vals are sorted in place (ping-pong buffers
+// come from `arena` and are released on return).
+void radix_sort_u64(uint64_t* keys, uint32_t* vals, int64_t n, int key_bits, Arena& arena,
+                    hipStream_t s);
+
+}  // namespace taurus

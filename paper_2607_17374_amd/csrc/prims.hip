@@ -1,0 +1,316 @@
+// Device-wide primitives used while building graph structures: an exclusive
+// prefix sum and a stable LSD radix sort of 64-bit keys with 32-bit values.
+// Both are written for wave64: wave-level scans use cross-lane shuffles and
+// the radix ranking matches digits within a wave with eight ballots.
+#include <cstdarg>
+
+#include "internal.hpp"
+
+namespace taurus {
+
+// ---------------------------------------------------------------- errors ----
+static thread_local std::string g_last_error;
+
+void set_error(const char* fmt, ...) {
+    char buf[1024];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+}
+
+void fail(int status, const char* fmt, ...) {
+    char buf[1024];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    throw Failure{status};
+}
+
+const char* last_error_cstr() { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------- arena -----
+void* Arena::alloc_bytes(int64_t bytes, const char* what) {
+    if (bytes <= 0) bytes = 16;
+    bytes = (bytes + 255) & ~(int64_t)255;
+    if (budget_ > 0 && bytes_ + bytes > budget_)
+        fail(TAURUS_E_BUDGET, "allocating %lld bytes for %s exceeds the budget (%lld of %lld in use)",
+             (long long)bytes, what, (long long)bytes_, (long long)budget_);
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, (size_t)bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        fail(e == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE,
+             "hipMalloc(%lld) for %s failed: %s", (long long)bytes, what, hipGetErrorString(e));
+    }
+    blocks_.push_back({p, bytes});
+    bytes_ += bytes;
+    if (bytes_ > peak_) peak_ = bytes_;
+    return p;
+}
+
+void Arena::free_ptr(void* p) {
+    for (size_t i = 0; i < blocks_.size(); i++) {
+        if (blocks_[i].p == p) {
+            (void)hipFree(p);
+            bytes_ -= blocks_[i].bytes;
+            blocks_.erase(blocks_.begin() + (long)i);
+            return;
+        }
+    }
+}
+
+void Arena::release() {
+    for (auto& b : blocks_) (void)hipFree(b.p);
+    blocks_.clear();
+    bytes_ = 0;
+}
+
+// ---------------------------------------------------------------- scan ------
+constexpr int SCAN_THREADS = 256;
+constexpr int SCAN_ITEMS = 16;
+constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+
+// inclusive scan across a wave64 with shuffles
+__device__ inline uint64_t wave_incl_scan(uint64_t x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        uint64_t y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    return x;
+}
+
+// exclusive scan of one value per thread across the block; returns the
+// block total in *total
+__device__ inline uint64_t block_excl_scan(uint64_t x, uint64_t* total) {
+    __shared__ uint64_t wsum[SCAN_THREADS / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t inc = wave_incl_scan(x);
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    uint64_t before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < SCAN_THREADS / 64; w++) {
+        if (w < wave) before += wsum[w];
+        all += wsum[w];
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - x;
+}
+
+template <typename Tin>
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile_sums(const Tin* __restrict__ in, int64_t n,
+                                                                 uint64_t* __restrict__ sums) {
+    const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+    uint64_t s = 0;
+    for (int i = threadIdx.x; i < SCAN_TILE; i += SCAN_THREADS) {
+        int64_t g = base + i;
+        if (g < n) s += (uint64_t)in[g];
+    }
+    uint64_t total;
+    (void)block_excl_scan(s, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+template <typename Tin, typename Tout>
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile_apply(const Tin* __restrict__ in, int64_t n,
+                                                                  const uint64_t* __restrict__ offsets,
+                                                                  Tout* __restrict__ out) {
+    __shared__ uint64_t stage[SCAN_TILE];
+    const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+    for (int i = threadIdx.x; i < SCAN_TILE; i += SCAN_THREADS) {
+        int64_t g = base + i;
+        stage[i] = g < n ? (uint64_t)in[g] : 0;
+    }
+    __syncthreads();
+    uint64_t v[SCAN_ITEMS];
+    uint64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; j++) {
+        v[j] = stage[threadIdx.x * SCAN_ITEMS + j];
+        s += v[j];
+    }
+    uint64_t total;
+    uint64_t run = block_excl_scan(s, &total) + (offsets ? offsets[blockIdx.x] : 0);
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; j++) {
+        stage[threadIdx.x * SCAN_ITEMS + j] = run;
+        run += v[j];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < SCAN_TILE; i += SCAN_THREADS) {
+        int64_t g = base + i;
+        if (g < n) out[g] = (Tout)stage[i];
+    }
+}
+
+template <typename Tout>
+__global__ void k_write_total(const uint64_t* __restrict__ sums_scanned, const uint64_t* __restrict__ sums,
+                              int64_t nb, Tout* __restrict__ out, int64_t n) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) out[n] = (Tout)(sums_scanned[nb - 1] + sums[nb - 1]);
+}
+template <typename Tout>
+__global__ void k_write_zero(Tout* __restrict__ out) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) out[0] = 0;
+}
+
+// exclusive scan of n values (any integer type) into out (uint64/int64)
+template <typename Tin, typename Tout>
+static void scan_impl(const Tin* in, Tout* out, int64_t n, bool write_total, Arena& arena, hipStream_t s) {
+    if (n == 0) {
+        if (write_total) {
+            k_write_zero<<<1, 64, 0, s>>>(out);
+            TAURUS_CHECK_LAUNCH();
+        }
+        return;
+    }
+    const int64_t nb = ceil_div(n, SCAN_TILE);
+    uint64_t* sums = arena.alloc<uint64_t>(nb, "scan block sums");
+    uint64_t* sums_scanned = arena.alloc<uint64_t>(nb, "scan block offsets");
+    k_scan_tile_sums<Tin><<<(unsigned)nb, SCAN_THREADS, 0, s>>>(in, n, sums);
+    TAURUS_CHECK_LAUNCH();
+    if (nb == 1) {
+        k_write_zero<<<1, 64, 0, s>>>(sums_scanned);
+        TAURUS_CHECK_LAUNCH();
+    } else {
+        scan_impl<uint64_t, uint64_t>(sums, sums_scanned, nb, false, arena, s);
+    }
+    k_scan_tile_apply<Tin, Tout><<<(unsigned)nb, SCAN_THREADS, 0, s>>>(in, n, sums_scanned, out);
+    TAURUS_CHECK_LAUNCH();
+    if (write_total) {
+        k_write_total<Tout><<<1, 64, 0, s>>>(sums_scanned, sums, nb, out, n);
+        TAURUS_CHECK_LAUNCH();
+    }
+    TAURUS_HIP(hipStreamSynchronize(s));
+    arena.free_ptr(sums_scanned);
+    arena.free_ptr(sums);
+}
+
+void scan_u32_to_u64(const uint32_t* in, uint64_t* out, int64_t n, bool write_total, Arena& arena,
+                     hipStream_t s) {
+    scan_impl<uint32_t, uint64_t>(in, out, n, write_total, arena, s);
+}
+void scan_i32_to_i64(const int32_t* in, int64_t* out, int64_t n, bool write_total, Arena& arena,
+                     hipStream_t s) {
+    scan_impl<int32_t, int64_t>(in, out, n, write_total, arena, s);
+}
+
+// ---------------------------------------------------------------- radix -----
+constexpr int RS_THREADS = 256;
+constexpr int RS_ITEMS = 16;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
+constexpr int RS_WAVES = RS_THREADS / 64;
+
+__global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __restrict__ keys, int64_t n,
+                                                           int shift, int64_t nblocks,
+                                                           uint32_t* __restrict__ hist) {
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+    for (int i = threadIdx.x; i < RS_TILE; i += RS_THREADS) {
+        int64_t g = base + i;
+        if (g < n) atomicAdd(&h[(keys[g] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// Scatter one tile stably: items are ranked in index order, 256 at a time.
+// Within a round a lane's rank among equal digits of its wave comes from the
+// eight-ballot digit match; earlier waves and earlier rounds add their counts.
+__global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
+    const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
+    int64_t nblocks, const uint64_t* __restrict__ offs, uint64_t* __restrict__ kout,
+    uint32_t* __restrict__ vout, int* __restrict__ bad) {
+    __shared__ uint64_t base[256];
+    __shared__ uint32_t run[256];
+    __shared__ uint32_t wcnt[RS_WAVES][256];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    base[tid] = offs[(int64_t)tid * nblocks + blockIdx.x];
+    run[tid] = 0;
+    const int64_t tile0 = (int64_t)blockIdx.x * RS_TILE;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int r = 0; r < RS_ITEMS; r++) {
+        const int64_t g = tile0 + (int64_t)r * RS_THREADS + tid;
+        const bool valid = g < n;
+        uint64_t key = valid ? kin[g] : 0;
+        uint32_t val = (valid && vin) ? vin[g] : 0;
+        const uint32_t d = (uint32_t)((key >> shift) & 255u);
+#pragma unroll
+        for (int w = 0; w < RS_WAVES; w++) wcnt[w][tid] = 0;
+        __syncthreads();
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; b++) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const uint32_t rank_w = (uint32_t)__popcll(peers & lt_mask);
+        if (valid && rank_w == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
+        __syncthreads();
+        if (valid) {
+            uint32_t before = run[d];
+            for (int w = 0; w < wave; w++) before += wcnt[w][d];
+            const uint64_t pos = base[d] + before + rank_w;
+            if (pos < (uint64_t)n) {
+                kout[pos] = key;
+                if (vin) vout[pos] = val;
+            } else {
+                atomicOr(bad, 1);
+            }
+        }
+        __syncthreads();
+        uint32_t add = 0;
+#pragma unroll
+        for (int w = 0; w < RS_WAVES; w++) add += wcnt[w][tid];
+        run[tid] += add;
+    }
+}
+
+void radix_sort_u64(uint64_t* keys, uint32_t* vals, int64_t n, int key_bits, Arena& arena,
+                    hipStream_t s) {
+    if (n <= 1 || key_bits <= 0) return;
+    const int64_t nblocks = ceil_div(n, RS_TILE);
+    if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
+    uint64_t* k2 = arena.alloc<uint64_t>(n, "radix keys");
+    uint32_t* v2 = vals ? arena.alloc<uint32_t>(n, "radix values") : nullptr;
+    uint32_t* hist = arena.alloc<uint32_t>(256 * nblocks, "radix histogram");
+    uint64_t* offs = arena.alloc<uint64_t>(256 * nblocks, "radix offsets");
+    int* bad = arena.alloc<int>(1, "radix flag");
+    TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));
+    uint64_t *ka = keys, *kb = k2;
+    uint32_t *va = vals, *vb = v2;
+    int passes = 0;
+    for (int shift = 0; shift < key_bits; shift += 8, passes++) {
+        k_radix_hist<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(ka, n, shift, nblocks, hist);
+        TAURUS_CHECK_LAUNCH();
+        scan_u32_to_u64(hist, offs, 256 * nblocks, false, arena, s);
+        k_radix_scatter<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(ka, va, n, shift, nblocks, offs, kb, vb, bad);
+        TAURUS_CHECK_LAUNCH();
+        std::swap(ka, kb);
+        std::swap(va, vb);
+    }
+    if (ka != keys) {
+        TAURUS_HIP(hipMemcpyAsync(keys, ka, (size_t)n * 8, hipMemcpyDeviceToDevice, s));
+        if (vals) TAURUS_HIP(hipMemcpyAsync(vals, va, (size_t)n * 4, hipMemcpyDeviceToDevice, s));
+    }
+    int hbad = 0;
+    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    arena.free_ptr(bad);
+    arena.free_ptr(offs);
+    arena.free_ptr(hist);
+    if (hbad) fail(TAURUS_E_DEVICE, "radix sort: internal offset out of range");
+    if (v2) arena.free_ptr(v2);
+    arena.free_ptr(k2);
+}
+
+}  // namespace taurus

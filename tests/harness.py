@@ -1,0 +1,109 @@
+"""Shared test/measurement helpers: run a workload on the GPU through the C
+ABI, run the oracle on the CPU, and compare the two.
+
+The GPU side and the oracle side only meet here, in the comparison; their
+inputs come from ``fixtures`` (the seeded generator both may use)."""
+from __future__ import annotations
+
+import numpy as np
+
+import fixtures as F
+from fixtures import workloads as WL
+
+# tolerance of the embedding comparison: fp32 paths 1e-4, 16-bit storage 1e-2
+RTOL = {F.F32: 1e-4, F.BF16: 1e-2, F.F16: 1e-2}
+
+
+def compare(y: np.ndarray, o: np.ndarray, rtol: float) -> dict:
+    """Element-wise |y - o| <= rtol * (|o| + RMS(o)); RMS over the whole
+    layer output of the oracle guards ReLU zeros and cancellation.  Also the
+    paper's summary statistics: mean per-vertex max abs error and mean
+    relative error."""
+    y = np.asarray(y, np.float64)
+    o = np.asarray(o, np.float64)
+    assert y.shape == o.shape, (y.shape, o.shape)
+    if o.size == 0:
+        return dict(n_bad=0, max_abs=0.0, mean_vertex_max_abs=0.0, mean_rel=0.0, rms=0.0, worst=None)
+    rms = float(np.sqrt(np.mean(o * o)))
+    err = np.abs(y - o)
+    bound = rtol * (np.abs(o) + rms)
+    bad = err > bound
+    rel = err / (np.abs(o) + rms + 1e-300)
+    worst = np.unravel_index(int(np.argmax(err - bound)), err.shape)
+    return dict(n_bad=int(bad.sum()), max_abs=float(err.max()), mean_vertex_max_abs=float(err.max(axis=1).mean()),
+                mean_rel=float(rel.mean()), max_rel=float(rel.max()), rms=rms,
+                worst=(tuple(int(i) for i in worst), float(y[worst]), float(o[worst])))
+
+
+def layer_specs(w: WL.Workload, fanouts=None):
+    """Per-layer keyword arguments of paper_2607_17374_amd.Layer for workload w."""
+    specs = []
+    for li in range(1, w.layers + 1):
+        p = WL.layer_params(w, li)
+        in_dt, out_dt = w.layer_dtypes(li)
+        specs.append(dict(agg=w.agg, d_in=p.d_in, d_out=p.d_out, weight_cat=p.weight_cat(), bias=p.b,
+                          in_dtype=in_dt, out_dtype=out_dt, relu=li < w.layers,
+                          fanout=(fanouts[li - 1] if fanouts else w.fanout(li)), layer=li, seed=w.seed))
+    return specs
+
+
+def oracle_model(w: WL.Workload, src=None, dst=None):
+    """Full oracle run of workload w -> (oracle graph, [fp64 outputs per layer])."""
+    import oracle as O
+    if src is None:
+        src, dst = WL.graph(w)
+    g = O.Graph(w.n, src, dst)
+    X = WL.input_features(w)
+    H, h_dtype = X, w.feat_dtype
+    zs = []
+    for li in range(1, w.layers + 1):
+        p = WL.layer_params(w, li)
+        keep = None
+        if w.fanout(li) > 0:
+            _, keep, _ = O.sample(g, w.seed, li, w.fanout(li))
+        z = O.layer(w.agg, g, H, h_dtype, p.W, p.b, li < w.layers, keep_in=keep)
+        zs.append(z)
+        _, out_dt = w.layer_dtypes(li)
+        H = O.round_store(z, out_dt)
+        h_dtype = out_dt
+    return g, zs
+
+
+def gpu_graph(w: WL.Workload, src=None, dst=None, device="cuda"):
+    import torch
+    import paper_2607_17374_amd as T
+    if src is None:
+        src, dst = WL.graph(w)
+    s = torch.from_numpy(np.ascontiguousarray(src)).to(device)
+    d = torch.from_numpy(np.ascontiguousarray(dst)).to(device)
+    row_off, col_dst = T.build_csr(w.n, s, d)
+    return row_off, col_dst
+
+
+def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, profile=False, stream=None):
+    """Run every layer of w through the C ABI; returns ([outputs], [stats])."""
+    import torch
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    if X is None:
+        xh = WL.input_features(w)
+        X = torch.from_numpy(xh.view(np.int16) if xh.dtype == np.uint16 else xh).cuda()
+        if w.feat_dtype != F.F32:
+            X = X.view(torch_dtype(w.feat_dtype))
+    chunk = chunk or w.chunk
+    h = X
+    outs, stats = [], []
+    for spec in layer_specs(w):
+        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=X.device)
+        L = T.Layer(w.n, row_off, col_dst, out=out, chunk=chunk, profile=profile, stream=stream, **spec)
+        L.push_all(h, order=order)
+        stats.append(L.finalize())
+        L.destroy()
+        outs.append(out)
+        h = out
+    return outs, stats
+
+
+def to_numpy_f64(t, dtype_code: int) -> np.ndarray:
+    import torch
+    return t.detach().to(torch.float64).cpu().numpy() if dtype_code != F.F32 else t.detach().cpu().numpy().astype(np.float64)

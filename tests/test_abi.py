@@ -1,0 +1,75 @@
+"""The C ABI library loads and exports what include/taurus.h declares; host
+functions and argument validation work without a GPU (no compute calls)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "taurus.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(taurus_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def native():
+    from paper_2607_17374_amd import _native as N
+    return N
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("taurus_layer_init", "taurus_push_chunk", "taurus_finalize", "taurus_sampled_edges",
+                     "taurus_build_csr", "taurus_layer_destroy", "taurus_last_error", "taurus_hash"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(native):
+    L = native.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert name in native.SIGNATURES, f"binding lacks {name}"
+
+
+def test_binding_structs_match_header_layout(native):
+    # field order and sizes as declared in taurus.h (x86-64 alignment)
+    assert ctypes.sizeof(native.Graph) == 32
+    assert native.LayerDesc.weight.offset == 24 and native.LayerDesc.seed.offset == 48
+    assert native.LayerDesc.out.offset == 80 and native.LayerDesc.stream.offset == 96
+    assert ctypes.sizeof(native.LayerDesc) == 112
+    assert ctypes.sizeof(native.Stats) == 14 * 8 + 5 * 8 + 3 * 8
+
+
+def test_hash_matches_published_splitmix64(golden_dir):
+    from paper_2607_17374_amd.api import hash_u64
+    G = 0x9e3779b97f4a7c15
+    refs = [int(l, 16) for l in open(f"{golden_dir}/splitmix64_state0.txt") if l.strip() and not l.startswith("#")]
+    for k, ref in enumerate(refs):
+        assert hash_u64(0, (k * G) % 2**64) == ref
+
+
+def test_invalid_arguments_rejected_before_device_work(native):
+    L = native.lib()
+    g = native.Graph(0, 0, None, None)
+    d = native.LayerDesc()
+    h = ctypes.c_void_p()
+    assert L.taurus_layer_init(ctypes.byref(g), ctypes.byref(d), ctypes.byref(h)) == native.E_INVALID
+    assert "graph size" in native.last_error()
+    assert L.taurus_layer_init(None, None, ctypes.byref(h)) == native.E_INVALID
+    assert L.taurus_push_chunk(None, 0, 1, None, 0) == native.E_INVALID
+    assert L.taurus_finalize(None, None) == native.E_INVALID
+    assert L.taurus_sampled_edges(None, None, None) == native.E_INVALID
+    assert L.taurus_build_csr(0, 0, None, None, None, None, None) == native.E_INVALID
+    L.taurus_layer_destroy(None)
+    # width not a multiple of 4
+    g = native.Graph(10, 0, 1, None)
+    w = np.zeros(16, np.float32)
+    d = native.LayerDesc(agg=0, d_in=6, d_out=4, weight=w.ctypes.data, chunk=4, out=1)
+    assert L.taurus_layer_init(ctypes.byref(g), ctypes.byref(d), ctypes.byref(h)) == native.E_INVALID
+    assert "multiples of 4" in native.last_error()
