@@ -41,6 +41,10 @@ typedef enum {
 
 typedef enum { TAURUS_F32 = 0, TAURUS_BF16 = 1, TAURUS_F16 = 2 } taurus_dtype;
 
+/* Per-graph structures shared by the exact layers over one graph (see
+ * taurus_plan_create). */
+typedef struct taurus_plan taurus_plan;
+
 /* Aggregation/update families (Sec. 3.9 and the models of Sec. 4.1). */
 typedef enum {
     TAURUS_SAGE_MEAN = 0, /* z_v = W_agg mean_{u in M(v)} h_u + W_self h_v + b (mean = 0 if M(v) empty)  */
@@ -99,6 +103,11 @@ typedef struct {
  *                (NULL = the default stream).
  *   profile      1: time every kernel of the layer with HIP events; the
  *                totals are returned in taurus_stats.
+ *   plan         NULL, or a plan built for this graph (same n, e, row_off,
+ *                col_dst pointers) and this chunk size: an exact layer
+ *                (fanout = 0) then reuses the plan's chunk index instead of
+ *                building its own.  A plan with another graph or chunk size
+ *                is TAURUS_E_INVALID.
  */
 typedef struct {
     int32_t agg, d_in, d_out, in_dtype, out_dtype, relu;
@@ -113,6 +122,7 @@ typedef struct {
     int32_t out_on_host;
     void* stream;
     int32_t profile;
+    const taurus_plan* plan;
 } taurus_layer_desc;
 
 typedef struct taurus_layer taurus_layer;
@@ -126,7 +136,9 @@ typedef struct {
     int64_t completed;             /* vertices whose output row was written             */
     int64_t pending_left;          /* vertices still waiting for messages               */
     int64_t chunks, chunks_pushed;
-    int64_t tiles, split_segments; /* scatter work tiles, segments spanning tiles       */
+    int64_t short_units;           /* segments of <= 8 messages (one row-group each)    */
+    int64_t wave_units;            /* pieces of longer segments (one wave each)         */
+    int64_t split_segments;        /* hub segments cut into several pieces              */
     int64_t evictions, reloads;    /* accumulator rows moved to/from host (0 in core)   */
     int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
     double hub_message_share;      /* share of messages landing on resident hubs        */
@@ -157,6 +169,24 @@ uint64_t taurus_hash(uint64_t seed, uint64_t tag, int32_t nargs, const uint64_t*
  */
 int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
                      int64_t* row_off, int32_t* col_dst, void* stream);
+
+/*
+ * Build the exact chunk index of a graph once, for every exact layer that
+ * streams it with source chunks of `chunk` vertices: the propagated in-edges
+ * and one self item per vertex, grouped by (source chunk, destination), each
+ * vertex's arrival count |N-(v)| + 1, and the list of destination segments
+ * that straddle scatter tiles (Sec. 3.3-3.4: the reader streams contiguous
+ * vertex ranges; the orchestrator keeps O(|V|) pending counts).  The graph
+ * is validated (row_off monotone from 0 to e, col_dst in [0, n), rows
+ * strictly ascending, no self loops); an invalid graph is
+ * TAURUS_E_INVALID.  The graph arrays must stay valid and unchanged while the
+ * plan or any layer using it lives.  Blocks until built.  The plan's device
+ * memory is held until the plan and every layer that uses it are destroyed.
+ */
+int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, taurus_plan** out);
+
+/* Release a plan (layers still using it keep its index alive).  NULL is ignored. */
+void taurus_plan_destroy(taurus_plan* plan);
 
 /*
  * Create the state of one layer: copies the weights, computes degrees and

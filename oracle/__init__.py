@@ -68,7 +68,13 @@ def load(path: str):
     L.or_reorder_bfs.argtypes = [i64, vp, vp, vp]
     L.or_total_span.restype = i64
     L.or_total_span.argtypes = [i64, vp, vp, vp]
+    L.or_threads.restype = i32
+    L.or_threads.argtypes = []
     return L
+
+
+def threads() -> int:
+    return int(lib().or_threads())
 
 
 def _p(a):

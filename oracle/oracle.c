@@ -32,9 +32,13 @@
  * brute force and the published SplitMix64 outputs); none is unpinned.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* number of OpenMP threads the oracle's parallel loops use */
+int or_threads(void) { return omp_get_max_threads(); }
 
 /* ------------------------------------------------------------ helpers ---- */
 

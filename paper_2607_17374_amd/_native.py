@@ -39,13 +39,14 @@ class LayerDesc(ctypes.Structure):
                 ("fanout", ctypes.c_int32), ("layer", ctypes.c_int32), ("seed", ctypes.c_uint64),
                 ("chunk", ctypes.c_int64), ("hbm_budget", ctypes.c_int64), ("hub_fraction", ctypes.c_double),
                 ("out", ctypes.c_void_p), ("out_on_host", ctypes.c_int32),
-                ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32)]
+                ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p)]
 
 
 class Stats(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int64) for name in (
         "n", "e", "messages", "self_terms", "pairs", "completed", "pending_left", "chunks",
-        "chunks_pushed", "tiles", "split_segments", "evictions", "reloads", "device_bytes")] + [
+        "chunks_pushed", "short_units", "wave_units", "split_segments", "evictions", "reloads",
+        "device_bytes")] + [
         ("hub_message_share", ctypes.c_double), ("ms_init", ctypes.c_double), ("ms_gemm", ctypes.c_double),
         ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),
         ("launches_gemm", ctypes.c_int64), ("launches_scatter", ctypes.c_int64),
@@ -68,6 +69,9 @@ SIGNATURES = {
     "taurus_finalize": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(Stats)]),
     "taurus_sampled_edges": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]),
     "taurus_layer_destroy": (None, [ctypes.c_void_p]),
+    "taurus_plan_create": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_int64, ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_void_p)]),
+    "taurus_plan_destroy": (None, [ctypes.c_void_p]),
 }
 
 _lib = None

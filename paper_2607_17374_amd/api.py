@@ -53,6 +53,35 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
     return row_off, col_dst
 
 
+class Plan:
+    """taurus_plan_create / taurus_plan_destroy: the exact chunk index of a
+    graph for one chunk size, shared by every exact layer over it."""
+
+    def __init__(self, n: int, row_off: torch.Tensor, col_dst: torch.Tensor, chunk: int, stream=None):
+        self._h = ctypes.c_void_p()
+        e = col_dst.numel()
+        self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"), col_dst.data_ptr() if e else None)
+        self.chunk = chunk
+        self._keep = (row_off, col_dst)
+        N.check(N.lib().taurus_plan_create(ctypes.byref(self.graph), chunk, _stream_ptr(stream),
+                                           ctypes.byref(self._h)), "taurus_plan_create")
+
+    @property
+    def handle(self):
+        return self._h.value
+
+    def destroy(self) -> None:
+        if self._h:
+            N.lib().taurus_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
 class Layer:
     """One layer handle (taurus_layer_init ... taurus_layer_destroy)."""
 
@@ -60,7 +89,7 @@ class Layer:
                  d_out: int, weight_cat: np.ndarray, bias: Optional[np.ndarray], out: torch.Tensor,
                  in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
-                 hub_fraction: float = 0.0, stream=None, profile: bool = False):
+                 hub_fraction: float = 0.0, stream=None, profile: bool = False, plan: "Plan" = None):
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
@@ -74,8 +103,8 @@ class Layer:
             weight=self._w.ctypes.data, bias=None if self._b is None else self._b.ctypes.data,
             fanout=fanout, layer=layer, seed=seed & (2**64 - 1), chunk=chunk, hbm_budget=hbm_budget,
             hub_fraction=hub_fraction, out=_dev_ptr(out, _TORCH_DTYPE[out_dtype], "out"), out_on_host=0,
-            stream=_stream_ptr(stream), profile=int(profile))
-        self._keep = (row_off, col_dst)
+            stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None)
+        self._keep = (row_off, col_dst, plan)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")
 
@@ -127,13 +156,17 @@ def run_layers(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, x: torch.Te
     in_dtype, out_dtype, relu, fanout, layer, seed.  Returns (outputs, stats)."""
     h = x
     results, stats = [], []
+    plan = Plan(n, row_off, col_dst, chunk, stream=stream) if any(s.get("fanout", 0) == 0 for s in layers) else None
     for i, spec in enumerate(layers):
         out = outs[i] if outs is not None else torch.empty(
             (n, spec["d_out"]), dtype=_TORCH_DTYPE[spec.get("out_dtype", N.F32)], device=x.device)
-        L = Layer(n, row_off, col_dst, out=out, chunk=chunk, stream=stream, profile=profile, **spec)
+        L = Layer(n, row_off, col_dst, out=out, chunk=chunk, stream=stream, profile=profile,
+                  plan=plan if spec.get("fanout", 0) == 0 else None, **spec)
         L.push_all(h)
         stats.append(L.finalize())
         L.destroy()
         results.append(out)
         h = out
+    if plan is not None:
+        plan.destroy()
     return results, stats

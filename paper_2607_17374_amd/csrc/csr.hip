@@ -51,7 +51,7 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
         fail(TAURUS_E_INVALID, "taurus_build_csr: n=%lld e=%lld out of range", (long long)n, (long long)e);
     if (!row_off || (e > 0 && (!src || !dst || !col_dst)))
         fail(TAURUS_E_INVALID, "taurus_build_csr: null pointer");
-    Arena arena;
+    Arena arena(s);
     const int vbits = bits_for(n - 1) > 0 ? bits_for(n - 1) : 1;
     int* bad = arena.alloc<int>(1, "flag");
     TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));

@@ -36,11 +36,15 @@ struct Failure {
 
 #define TAURUS_CHECK_LAUNCH() TAURUS_HIP(hipGetLastError())
 
-// Device allocations owned by one object, with a byte budget.
+// Device allocations owned by one object, with a byte budget.  Memory is
+// stream ordered (hipMallocAsync / hipFreeAsync on the owner's stream) from
+// the device's default pool, which keeps freed blocks for reuse, so layers
+// created one after another recycle each other's buffers.
 class Arena {
 public:
-    explicit Arena(int64_t budget = 0) : budget_(budget) {}
+    explicit Arena(hipStream_t s = nullptr, int64_t budget = 0) : stream_(s), budget_(budget) {}
     ~Arena() { release(); }
+    void set_stream(hipStream_t s) { stream_ = s; }
     Arena(const Arena&) = delete;
     Arena& operator=(const Arena&) = delete;
 
@@ -61,6 +65,7 @@ private:
         int64_t bytes;
     };
     std::vector<Block> blocks_;
+    hipStream_t stream_ = nullptr;
     int64_t budget_ = 0, bytes_ = 0, peak_ = 0;
 };
 

@@ -1,32 +1,35 @@
 // One GNN layer as source-centric broadcast (Taurus, Sec. 3.1-3.6).
 //
-// Per layer (taurus_layer_init):
-//   - pending[v] = |M(v)| + 1: every propagated in-edge and the vertex's own
-//     self message each count as one arrival (Sec. 3.4: O(|V|) pending
-//     counts; a vertex completes when its count reaches zero);
-//   - the chunk index: all propagated in-edges (u, v) plus one self item
-//     (v, v) per vertex, stably sorted by (chunk of the source, v).  In
-//     chunk j the messages to one destination are then one contiguous
-//     segment, with sources ascending and the self item last;
-//   - the segments that straddle scatter tiles, so their partial sums can be
-//     combined in a fixed order after the tile pass (no float atomics).
+// Per graph and chunk size (the chunk index, shared by exact layers):
+//   - all propagated in-edges (u, v) plus one self item (v, v) per vertex,
+//     stably sorted by (chunk of the source, v).  In chunk j the messages to
+//     one destination are then one contiguous segment, sources ascending and
+//     the self item last;
+//   - each vertex's arrival count |M(v)| + 1: every propagated in-edge and
+//     the self message count once (Sec. 3.4: O(|V|) pending counts; a vertex
+//     completes when its count reaches zero);
+//   - degree-bucketed work units: a segment of at most SHORT_LEN messages is
+//     one short unit (handled by a row-group of lanes); a longer one is cut
+//     into pieces of at most PIECE_LEN messages (each handled by a whole
+//     wave); a segment cut into several pieces (a hub) is completed by the
+//     fix-up pass, which sums the pieces' partial rows in a fixed order.
 // Per chunk (taurus_push_chunk):
-//   1. transform: Y = X_c W (GCN rows scaled by d^_out(u)^-1/2; GraphSAGE
-//      Y = [X_c W_agg^T | X_c W_self^T]);
-//   2. scatter: for every segment, the sum of its source rows scaled once by
+//   1. transform: Y = X_c W on the matrix cores (GCN rows scaled by
+//      d^_out(u)^-1/2; GraphSAGE Y = [X_c W_agg^T | X_c W_self^T]);
+//   2. scatter: per unit, the sum of its source rows scaled once by
 //      1/|M(v)| (the per-message normalisation of Sec. 3.4 applied to the
 //      segment sum) plus the self row, added to v's fp32 accumulator; the
 //      pending count drops by the segment length;
 //   3. finalise in place: the flush that brings pending[v] to zero writes
 //      out[v] = act(phi_v * acc[v] + b) directly (GCN phi_v = d^_in(v)^-1/2,
 //      GraphSAGE phi_v = 1), the graduation step of Sec. 3.6;
-//   4. fix-up: segments cut by tile boundaries are summed from per-tile
-//      carries and flushed the same way.
+//   4. fix-up: hub segments sum their pieces and flush the same way.
 // A flush is the only writer of its destination within a kernel (segments
 // of one chunk are disjoint, kernels of one layer are stream ordered), so
-// accumulators are updated with plain loads and stores.
+// accumulators are updated with plain loads and stores, no atomics.
 #include <algorithm>
 #include <chrono>
+#include <memory>
 
 #include "internal.hpp"
 
@@ -41,22 +44,16 @@ const char* last_error_cstr();
 
 constexpr uint32_t SELF_BIT = 0x80000000u;
 constexpr int SC_THREADS = 256;
-constexpr int SC_TILE = 1024;
+constexpr int SHORT_LEN = 8;    // segments up to this many messages: one row-group
+constexpr int PIECE_LEN = 512;  // longer segments: pieces of this many messages, one wave each
 
 // ------------------------------------------------------------ init kernels --
 
-__global__ void k_in_degree(const int32_t* __restrict__ col_dst, int64_t e, int32_t* __restrict__ deg_in) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < e) atomicAdd(&deg_in[col_dst[i]], 1);
-}
-
-// pending and expected arrival counts: |M(v)| propagated messages + 1 self
-__global__ void k_init_counts(const int32_t* __restrict__ m, int64_t n, int2* __restrict__ cnt) {
+// pending and expected arrival counts: the number of index items of v,
+// i.e. |M(v)| propagated messages + 1 self message
+__global__ void k_init_counts(const int32_t* __restrict__ items, int64_t n, int2* __restrict__ cnt) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (v < n) {
-        const int x = m[v] + 1;
-        cnt[v] = make_int2(x, x);
-    }
+    if (v < n) cnt[v] = make_int2(items[v], items[v]);
 }
 
 // GCN source factor d^_out(u)^-1/2 with d^_out = out-degree + 1
@@ -123,35 +120,93 @@ __global__ void k_chunk_bounds(const uint64_t* __restrict__ keys, int64_t total,
     offs[j] = lo;
 }
 
-// number of distinct (chunk, destination) pairs among the first `total` keys
-__global__ void k_count_pairs(const uint64_t* __restrict__ keys, int64_t total,
-                              unsigned long long* __restrict__ pairs) {
+// head[i] = 1 where a new (chunk, destination) segment starts
+__global__ void k_seg_heads(const uint64_t* __restrict__ keys, int64_t total, int32_t* __restrict__ head) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool head = i < total && (i == 0 || keys[i] != keys[i - 1]);
-    const uint64_t b = __ballot(head);
-    if ((threadIdx.x & 63) == 0 && b) atomicAdd(pairs, (unsigned long long)__popcll(b));
+    if (i < total) head[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1 : 0;
 }
 
-__global__ void k_split_items(const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals,
-                              int64_t total, int vbits, int32_t* __restrict__ dst, uint32_t* __restrict__ src) {
+// seg_start[s] = first item of segment s; seg_start[P] = total
+__global__ void k_seg_starts(const int32_t* __restrict__ head, const int64_t* __restrict__ seg_id, int64_t total,
+                             int64_t* __restrict__ seg_start) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < total) {
-        dst[i] = (int32_t)(keys[i] & (((uint64_t)1 << vbits) - 1));
-        src[i] = vals[i];
+    if (i < total && head[i]) seg_start[seg_id[i]] = i;
+    if (i == 0) seg_start[seg_id[total]] = total;
+}
+
+// Per segment: add its length to the destination's item count, and count the
+// work units it becomes (short unit, wave pieces, fix-up entry).
+__global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
+                               int vbits, int32_t* __restrict__ items_per_v, int32_t* __restrict__ n_short,
+                               int32_t* __restrict__ n_long, int32_t* __restrict__ n_fix) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= P) return;
+    const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
+    const uint64_t v = keys[b] & (((uint64_t)1 << vbits) - 1);
+    atomicAdd(&items_per_v[v], (int)len);
+    const int pieces = len <= SHORT_LEN ? 0 : (int)((len + PIECE_LEN - 1) / PIECE_LEN);
+    n_short[s] = len <= SHORT_LEN ? 1 : 0;
+    n_long[s] = pieces;
+    n_fix[s] = pieces > 1 ? 1 : 0;
+}
+
+// Write the work units.  unit = {first item relative to its chunk, length,
+// destination, slot}; slot = global wave-unit index for pieces of a hub
+// segment (their partial rows go to the carry buffer), else -1.  fix-up
+// entry = {destination, first wave-unit index, number of pieces, 0}.
+__global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
+                           int vbits, const int64_t* __restrict__ chunk_off, const int64_t* __restrict__ o_short,
+                           const int64_t* __restrict__ o_long, const int64_t* __restrict__ o_fix,
+                           int4* __restrict__ u_short, int4* __restrict__ u_long, int4* __restrict__ u_fix) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= P) return;
+    const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
+    const uint64_t key = keys[b];
+    const int v = (int)(key & (((uint64_t)1 << vbits) - 1));
+    const int64_t rel = b - chunk_off[key >> vbits];
+    if (len <= SHORT_LEN) {
+        u_short[o_short[s]] = make_int4((int)rel, (int)len, v, -1);
+        return;
     }
+    const int pieces = (int)((len + PIECE_LEN - 1) / PIECE_LEN);
+    const int64_t first = o_long[s];
+    for (int q = 0; q < pieces; q++) {
+        const int64_t off = (int64_t)q * PIECE_LEN;
+        const int plen = (int)min((int64_t)PIECE_LEN, len - off);
+        u_long[first + q] = make_int4((int)(rel + off), plen, v, pieces > 1 ? (int)(first + q) : -1);
+    }
+    if (pieces > 1) u_fix[o_fix[s]] = make_int4(v, (int)first, pieces, 0);
 }
 
-__global__ void k_gather_bounds(const int32_t* __restrict__ dst, const int64_t* __restrict__ pos, int64_t np,
-                                int2* __restrict__ out) {
-    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (j < np) out[j] = make_int2(dst[pos[j] - 1], dst[pos[j]]);
+__global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, uint32_t* __restrict__ src) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < total) src[i] = vals[i];
 }
 
-__global__ void k_count_pending(const int2* __restrict__ cnt, int64_t n, unsigned long long* __restrict__ left) {
+// per-chunk starts of the three unit lists: values of the scans at each
+// chunk's first segment (chunk_off[nchunks] = total maps to segment P)
+__global__ void k_chunk_unit_bases(const int64_t* __restrict__ chunk_off, int64_t nchunks,
+                                   const int64_t* __restrict__ seg_id, const int64_t* __restrict__ o_short,
+                                   const int64_t* __restrict__ o_long, const int64_t* __restrict__ o_fix,
+                                   int64_t* __restrict__ bases) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k > nchunks) return;
+    const int64_t s = seg_id[chunk_off[k]];
+    bases[k * 3 + 0] = o_short[s];
+    bases[k * 3 + 1] = o_long[s];
+    bases[k * 3 + 2] = o_fix[s];
+}
+
+__global__ __launch_bounds__(256) void k_count_pending(const int2* __restrict__ cnt, int64_t n,
+                                                       unsigned long long* __restrict__ left) {
+    __shared__ unsigned int blk;
+    if (threadIdx.x == 0) blk = 0;
+    __syncthreads();
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool open = v < n && cnt[v].x != 0;
-    const uint64_t b = __ballot(open);
-    if ((threadIdx.x & 63) == 0 && b) atomicAdd(left, (unsigned long long)__popcll(b));
+    const uint64_t b = __ballot(v < n && cnt[v].x != 0);
+    if ((threadIdx.x & 63) == 0 && b) atomicAdd(&blk, (unsigned int)__popcll(b));
+    __syncthreads();
+    if (threadIdx.x == 0 && blk) atomicAdd(left, (unsigned long long)blk);
 }
 
 // ---------------------------------------------------------- scatter kernels --
@@ -160,9 +215,7 @@ struct ScatterParams {
     const float* Y;        // chunk transform, row stride ystride floats
     int64_t ystride;
     int self_col;          // column offset of the self half (GraphSAGE) or 0 (GCN)
-    const int32_t* dst;    // chunk items: destination
     const uint32_t* src;   // chunk items: local source row | SELF_BIT
-    int64_t nitems;
     int2* cnt;             // {pending, expected}
     float* acc;            // [n][d_o] fp32 accumulators
     int d_o;
@@ -171,8 +224,9 @@ struct ScatterParams {
     int out_dtype;         // 0 fp32, 1 bf16, 2 fp16
     const float* bias;     // [d_o]
     void* out;             // [n][d_o]
-    float* carry;          // per tile: [2][d_o] partial contributions (left, right piece)
-    int32_t* carry_cnt;    // per tile: [2] message counts of the pieces
+    float* carry;          // per hub piece of the chunk: [d_o] partial contribution
+    int32_t* carry_cnt;    // per hub piece: message count
+    int64_t long_base;     // global index of the chunk's first wave unit (carry slot 0)
 };
 
 __device__ inline float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
@@ -249,133 +303,112 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
     if (lane == 0) p.cnt[v].x = left;
 }
 
-// One workgroup reduces SC_TILE consecutive items of a chunk.  Row-group rg
-// (G lanes, one float4 per lane and VEC) walks its own sub-range; runs whose
-// segment is entirely inside the sub-range are flushed at once, runs open to
-// the left or right are parked in LDS, merged across row-groups, and either
-// flushed (closed inside the tile) or left as the tile's carry.
-template <int G, int VEC>
-__global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p) {
-    constexpr int NRG = SC_THREADS / G;
-    constexpr int PER = SC_TILE / NRG;
-    __shared__ int32_t s_dst[SC_TILE];
-    __shared__ uint32_t s_src[SC_TILE];
-    __shared__ int s_pv[2 * NRG], s_pc[2 * NRG], s_pf[2 * NRG];
-    __shared__ float4 s_prow[2 * NRG][G * VEC];
-
-    const int tid = threadIdx.x, rg = tid / G, lane = tid % G;
-    const int64_t t0 = (int64_t)blockIdx.x * SC_TILE;
-    const int nt = (int)min((int64_t)SC_TILE, p.nitems - t0);
-    for (int i = tid; i < nt; i += SC_THREADS) {
-        s_dst[i] = p.dst[t0 + i];
-        s_src[i] = p.src[t0 + i];
-    }
-    if (tid < 2 * NRG) {
-        s_pv[tid] = -1;
-        s_pc[tid] = 0;
-        s_pf[tid] = 0;
-    }
-    const int prev_v = t0 > 0 ? p.dst[t0 - 1] : -1;
-    const int next_v = t0 + nt < p.nitems ? p.dst[t0 + nt] : -1;
-    __syncthreads();
-
-    const int a = rg * PER, b = min(a + PER, nt);
-    if (a < b) {
-        const bool lopen = (a > 0 ? s_dst[a - 1] : prev_v) == s_dst[a];
-        int cur = s_dst[a], count = 0;
-        bool first = true;
-        float4 sa[VEC], ss[VEC];
+// Add the source rows of items first, first + step, ... (fewer than len) of
+// the chunk into sa (neighbour messages) and ss (the self message), with B
+// row loads in flight at a time.
+template <int G, int VEC, int B>
+__device__ inline void gather_rows(const ScatterParams& p, int first, int len, int step, int lane,
+                                   float4 (&sa)[VEC], float4 (&ss)[VEC]) {
+    for (int i0 = 0; i0 < len; i0 += B * step) {
+        float4 rows[B][VEC];
+        bool self[B];
 #pragma unroll
-        for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
-        auto emit = [&](bool lo, bool ro) {
-            const int2 pe = p.cnt[cur];
-            const float sig = seg_scale(p.agg, pe.y);
-            float4 c[VEC];
+        for (int u = 0; u < B; u++) {
+            const int i = i0 + u * step;
+            self[u] = false;
 #pragma unroll
-            for (int j = 0; j < VEC; j++) c[j] = f4_axpy(sig, sa[j], ss[j]);
-            if (!lo && !ro) {
-                flush_owner<G, VEC>(p, cur, pe, c, count, lane);
-            } else {
-                const int slot = 2 * rg + (lo ? 0 : 1);
+            for (int j = 0; j < VEC; j++) rows[u][j] = f4_zero();
+            if (i < len) {
+                const uint32_t code = p.src[first + i];
+                self[u] = (code & SELF_BIT) != 0;
+                const float* row = p.Y + (int64_t)(code & ~SELF_BIT) * p.ystride + (self[u] ? p.self_col : 0);
 #pragma unroll
-                for (int j = 0; j < VEC; j++) s_prow[slot][j * G + lane] = c[j];
-                if (lane == 0) {
-                    s_pv[slot] = cur;
-                    s_pc[slot] = count;
-                    s_pf[slot] = (lo ? 1 : 0) | (ro ? 2 : 0);
+                for (int j = 0; j < VEC; j++) {
+                    const int col = (j * G + lane) * 4;
+                    if (col < p.d_o) rows[u][j] = *reinterpret_cast<const float4*>(row + col);
                 }
             }
-        };
-        for (int i = a; i < b; i++) {
-            const int v = s_dst[i];
-            if (v != cur) {
-                emit(first && lopen, false);
-                first = false;
-                cur = v;
-                count = 0;
+        }
 #pragma unroll
-                for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
-            }
-            const uint32_t code = s_src[i];
-            const bool self = (code & SELF_BIT) != 0;
-            const float* row = p.Y + (int64_t)(code & ~SELF_BIT) * p.ystride + (self ? p.self_col : 0);
+        for (int u = 0; u < B; u++)
 #pragma unroll
             for (int j = 0; j < VEC; j++) {
-                const int col = (j * G + lane) * 4;
-                if (col < p.d_o) {
-                    const float4 y = *reinterpret_cast<const float4*>(row + col);
-                    if (self) ss[j] = f4_add(ss[j], y);
-                    else sa[j] = f4_add(sa[j], y);
-                }
+                if (self[u]) ss[j] = f4_add(ss[j], rows[u][j]);
+                else sa[j] = f4_add(sa[j], rows[u][j]);
             }
-            count++;
-        }
-        const bool ropen = (b < nt ? s_dst[b] : next_v) == cur;
-        emit(first && lopen, ropen);
-    }
-    __syncthreads();
-
-    // merge parked pieces: the row-group owning the first slot of a run of
-    // equal destinations sums the run
-#pragma unroll
-    for (int q = 0; q < 2; q++) {
-        const int s = 2 * rg + q;
-        const int v = s_pv[s];
-        if (v < 0) continue;
-        int ps = s - 1;
-        while (ps >= 0 && s_pv[ps] < 0) ps--;
-        if (ps >= 0 && s_pv[ps] == v) continue;
-        float4 c[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = s_prow[s][j * G + lane];
-        int count = s_pc[s], last = s;
-        for (int ns = s + 1; ns < 2 * NRG; ns++) {
-            const int w = s_pv[ns];
-            if (w < 0) continue;
-            if (w != v) break;
-#pragma unroll
-            for (int j = 0; j < VEC; j++) c[j] = f4_add(c[j], s_prow[ns][j * G + lane]);
-            count += s_pc[ns];
-            last = ns;
-        }
-        const bool lo = (s_pf[s] & 1) != 0, ro = (s_pf[last] & 2) != 0;
-        if (!lo && !ro) {
-            flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane);
-        } else {
-            const int side = lo ? 0 : 1;
-            float* crow = p.carry + ((int64_t)blockIdx.x * 2 + side) * p.d_o;
-#pragma unroll
-            for (int j = 0; j < VEC; j++) {
-                const int col = (j * G + lane) * 4;
-                if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
-            }
-            if (lane == 0) p.carry_cnt[blockIdx.x * 2 + side] = count;
-        }
     }
 }
 
-// A segment cut by tile boundaries spans tiles t0..t1: its pieces are the
-// right carry of t0 and the left carries of t0+1..t1, summed in that order.
+// Degree-bucketed scatter of one chunk.  Blocks [0, short_blocks) take short
+// units, one per row-group of G lanes (SC_THREADS / G units per block); the
+// remaining blocks take wave units, one per wave (4 per block): the wave's
+// 64/G row-groups split the piece's items, reduce across row-groups with
+// cross-lane shuffles, and row-group 0 flushes (or parks the partial row of
+// a hub piece in its carry slot).
+template <int G, int VEC>
+__global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p, const int4* __restrict__ u_short,
+                                                        int64_t n_short, int64_t short_blocks,
+                                                        const int4* __restrict__ u_long, int64_t n_long) {
+    constexpr int NRG = SC_THREADS / G;
+    constexpr int R = 64 / G;
+    constexpr int B = 8 / VEC;
+    if ((int64_t)blockIdx.x < short_blocks) {
+        const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+        const int64_t ui = (int64_t)blockIdx.x * NRG + rg;
+        if (ui >= n_short) return;
+        const int4 w = u_short[ui];
+        const int2 pe = p.cnt[w.z];
+        float4 sa[VEC], ss[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
+        gather_rows<G, VEC, B>(p, w.x, w.y, 1, lane, sa, ss);
+        const float sig = seg_scale(p.agg, pe.y);
+        float4 c[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) c[j] = f4_axpy(sig, sa[j], ss[j]);
+        flush_owner<G, VEC>(p, w.z, pe, c, w.y, lane);
+        return;
+    }
+    const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
+    const int rg = l64 / G, lane = l64 % G;
+    const int64_t ui = ((int64_t)blockIdx.x - short_blocks) * (SC_THREADS / 64) + wave;
+    if (ui >= n_long) return;
+    const int4 w = u_long[ui];
+    const int2 pe = p.cnt[w.z];
+    float4 sa[VEC], ss[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
+    gather_rows<G, VEC, B>(p, w.x + rg, w.y - rg, R, lane, sa, ss);
+#pragma unroll
+    for (int d = G; d < 64; d <<= 1)
+#pragma unroll
+        for (int j = 0; j < VEC; j++) {
+            sa[j].x += __shfl_xor(sa[j].x, d, 64); sa[j].y += __shfl_xor(sa[j].y, d, 64);
+            sa[j].z += __shfl_xor(sa[j].z, d, 64); sa[j].w += __shfl_xor(sa[j].w, d, 64);
+            ss[j].x += __shfl_xor(ss[j].x, d, 64); ss[j].y += __shfl_xor(ss[j].y, d, 64);
+            ss[j].z += __shfl_xor(ss[j].z, d, 64); ss[j].w += __shfl_xor(ss[j].w, d, 64);
+        }
+    if (rg != 0) return;
+    const float sig = seg_scale(p.agg, pe.y);
+    float4 c[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; j++) c[j] = f4_axpy(sig, sa[j], ss[j]);
+    if (w.w < 0) {
+        flush_owner<G, VEC>(p, w.z, pe, c, w.y, lane);
+    } else {
+        const int64_t slot = (int64_t)w.w - p.long_base;
+        float* crow = p.carry + slot * p.d_o;
+#pragma unroll
+        for (int j = 0; j < VEC; j++) {
+            const int col = (j * G + lane) * 4;
+            if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+        }
+        if (lane == 0) p.carry_cnt[slot] = w.y;
+    }
+}
+
+// A hub segment's pieces occupy consecutive carry slots; their partial rows
+// are summed in slot order and flushed.
 template <int G, int VEC>
 __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix) {
     constexpr int NRG = SC_THREADS / G;
@@ -383,33 +416,30 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
     const int64_t idx = (int64_t)blockIdx.x * NRG + rg;
     if (idx >= nfix) return;
     const int4 f = fix[idx];
-    const int v = f.x, ta = f.y, tb = f.z;
+    const int v = f.x;
+    const int64_t first = (int64_t)f.y - p.long_base;
     float4 c[VEC];
-    const float* crow = p.carry + ((int64_t)ta * 2 + 1) * p.d_o;
 #pragma unroll
-    for (int j = 0; j < VEC; j++) {
-        const int col = (j * G + lane) * 4;
-        c[j] = col < p.d_o ? *reinterpret_cast<const float4*>(crow + col) : f4_zero();
-    }
-    int count = p.carry_cnt[ta * 2 + 1];
-    for (int t = ta + 1; t <= tb; t++) {
-        const float* lrow = p.carry + ((int64_t)t * 2) * p.d_o;
+    for (int j = 0; j < VEC; j++) c[j] = f4_zero();
+    int count = 0;
+    for (int q = 0; q < f.z; q++) {
+        const float* crow = p.carry + (first + q) * p.d_o;
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
             const int col = (j * G + lane) * 4;
-            if (col < p.d_o) c[j] = f4_add(c[j], *reinterpret_cast<const float4*>(lrow + col));
+            if (col < p.d_o) c[j] = f4_add(c[j], *reinterpret_cast<const float4*>(crow + col));
         }
-        count += p.carry_cnt[t * 2];
+        count += p.carry_cnt[first + q];
     }
     flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane);
 }
 
-typedef void (*scatter_fn)(ScatterParams);
-typedef void (*fixup_fn)(ScatterParams, const int4*, int64_t);
-
 template <int G, int VEC>
-static void launch_scatter(const ScatterParams& p, int64_t ntiles, hipStream_t s) {
-    k_scatter<G, VEC><<<(unsigned)ntiles, SC_THREADS, 0, s>>>(p);
+static void launch_scatter(const ScatterParams& p, const int4* us, int64_t ns, const int4* ul, int64_t nl,
+                           hipStream_t s) {
+    constexpr int NRG = SC_THREADS / G;
+    const int64_t sb = ceil_div(ns, NRG), lb = ceil_div(nl, SC_THREADS / 64);
+    k_scatter<G, VEC><<<(unsigned)(sb + lb), SC_THREADS, 0, s>>>(p, us, ns, sb, ul, nl);
 }
 template <int G, int VEC>
 static void launch_fixup(const ScatterParams& p, const int4* fix, int64_t nfix, hipStream_t s) {
@@ -428,105 +458,86 @@ static void row_group_shape(int d_o, int* G, int* VEC) {
     *VEC = vec;
 }
 
-static void dispatch_scatter(int G, int VEC, const ScatterParams& p, int64_t ntiles, hipStream_t s) {
-    switch (G * 10 + VEC) {
-        case 41: launch_scatter<4, 1>(p, ntiles, s); break;
-        case 81: launch_scatter<8, 1>(p, ntiles, s); break;
-        case 161: launch_scatter<16, 1>(p, ntiles, s); break;
-        case 321: launch_scatter<32, 1>(p, ntiles, s); break;
-        case 641: launch_scatter<64, 1>(p, ntiles, s); break;
-        case 642: launch_scatter<64, 2>(p, ntiles, s); break;
-        case 644: launch_scatter<64, 4>(p, ntiles, s); break;
-        default: fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
+#define TAURUS_ROW_SHAPES(X) X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(64, 2) X(64, 4)
+
+static void dispatch_scatter(int G, int VEC, const ScatterParams& p, const int4* us, int64_t ns, const int4* ul,
+                             int64_t nl, hipStream_t s) {
+#define TAURUS_CASE(g, v)                              \
+    if (G == g && VEC == v) {                          \
+        launch_scatter<g, v>(p, us, ns, ul, nl, s);    \
+        TAURUS_CHECK_LAUNCH();                         \
+        return;                                        \
     }
-    TAURUS_CHECK_LAUNCH();
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
 }
 static void dispatch_fixup(int G, int VEC, const ScatterParams& p, const int4* fix, int64_t nfix, hipStream_t s) {
-    switch (G * 10 + VEC) {
-        case 41: launch_fixup<4, 1>(p, fix, nfix, s); break;
-        case 81: launch_fixup<8, 1>(p, fix, nfix, s); break;
-        case 161: launch_fixup<16, 1>(p, fix, nfix, s); break;
-        case 321: launch_fixup<32, 1>(p, fix, nfix, s); break;
-        case 641: launch_fixup<64, 1>(p, fix, nfix, s); break;
-        case 642: launch_fixup<64, 2>(p, fix, nfix, s); break;
-        case 644: launch_fixup<64, 4>(p, fix, nfix, s); break;
-        default: fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
+#define TAURUS_CASE(g, v)                              \
+    if (G == g && VEC == v) {                          \
+        launch_fixup<g, v>(p, fix, nfix, s);           \
+        TAURUS_CHECK_LAUNCH();                         \
+        return;                                        \
     }
-    TAURUS_CHECK_LAUNCH();
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
 }
 
 }  // namespace taurus
 
-// ------------------------------------------------------------- layer state --
 
-struct taurus_layer {
-    taurus_graph g{};
-    taurus_layer_desc d{};
-    hipStream_t s = nullptr;
-    taurus::Arena arena;
-    bool poisoned = false;
-    int64_t n = 0, C = 0, nchunks = 0, messages = 0, pairs = 0, ntiles_total = 0;
-    int d_o = 0, ncols = 0, G = 0, VEC = 0, max_tiles = 0;
-    int2* cnt = nullptr;
-    float* n_out = nullptr;
-    float* acc = nullptr;
-    float* wpack = nullptr;
-    float* bias = nullptr;
-    float* Y = nullptr;
-    int32_t* item_dst = nullptr;
-    uint32_t* item_src = nullptr;
-    int4* fix = nullptr;
-    float* carry = nullptr;
-    int32_t* carry_cnt = nullptr;
-    uint64_t* mask = nullptr;
-    std::vector<int64_t> chunk_off, fix_off;
-    std::vector<uint8_t> pushed;
-    int64_t npushed = 0;
-    double ms_init = 0;
-    std::vector<hipEvent_t> events;  // 4 per pushed chunk when profiling
-    ~taurus_layer() {
-        for (auto ev : events) (void)hipEventDestroy(ev);
-    }
-};
+// ------------------------------------------------------------- chunk index --
 
 namespace taurus {
 
-static void validate(const taurus_graph* g, const taurus_layer_desc* d) {
-    if (!g || !d) fail(TAURUS_E_INVALID, "null graph or descriptor");
+// The structures a layer streams over, fixed by (graph, chunk size, edge
+// mask): the item sources grouped by (chunk, destination), per-vertex item
+// counts (|M(v)| + 1), and per chunk the short units, the wave units and the
+// fix-up entries of hub segments.  Exact layers over one graph and chunk
+// size share one index.
+struct ChunkIndex {
+    Arena arena;
+    taurus_graph g{};
+    int64_t C = 0, nchunks = 0, kept = 0, pairs = 0;
+    int64_t n_short = 0, n_long = 0, n_fix = 0, max_long_per_chunk = 0;
+    bool sampled = false;
+    int32_t* items_per_v = nullptr;
+    uint32_t* item_src = nullptr;
+    int4* u_short = nullptr;
+    int4* u_long = nullptr;
+    int4* u_fix = nullptr;
+    std::vector<int64_t> chunk_off, short_off, long_off, fix_off;
+    double ms_build = 0;
+    ChunkIndex(hipStream_t s, int64_t budget) : arena(s, budget) {}
+    // The index may outlive the stream it was built on: wait for the device,
+    // then return the memory on the null stream.
+    ~ChunkIndex() {
+        (void)hipDeviceSynchronize();
+        arena.set_stream(nullptr);
+        arena.release();
+    }
+};
+
+static void check_graph_args(const taurus_graph* g) {
+    if (!g) fail(TAURUS_E_INVALID, "null graph");
     if (g->n <= 0 || g->n >= ((int64_t)1 << 31) || g->e < 0)
         fail(TAURUS_E_INVALID, "graph size n=%lld e=%lld out of range", (long long)g->n, (long long)g->e);
     if (!g->row_off || (g->e > 0 && !g->col_dst)) fail(TAURUS_E_INVALID, "graph arrays are null");
-    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM) fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
-    if (d->d_in <= 0 || d->d_out <= 0 || d->d_in % 4 || d->d_out % 4 || d->d_out > 1024 || d->d_in > 8192)
-        fail(TAURUS_E_INVALID, "d_in=%d d_out=%d: widths must be positive multiples of 4, d_out <= 1024",
-             d->d_in, d->d_out);
-    if (d->in_dtype != TAURUS_F32)
-        fail(TAURUS_E_INVALID, "in_dtype %d: only fp32 layer inputs are supported by this build", d->in_dtype);
-    if (d->out_dtype < 0 || d->out_dtype > 2) fail(TAURUS_E_INVALID, "out_dtype %d", d->out_dtype);
-    if (!d->weight) fail(TAURUS_E_INVALID, "weight is null");
-    if (d->chunk <= 0 || d->chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)d->chunk);
-    if (d->fanout < 0) fail(TAURUS_E_INVALID, "fanout %d", d->fanout);
-    if (d->fanout > 0) fail(TAURUS_E_INVALID, "fanout sampling is not supported by this build");
-    if (d->agg == TAURUS_GCN_SYM && d->fanout > 0) fail(TAURUS_E_INVALID, "GCN is defined for exact inference only");
-    if (!d->out) fail(TAURUS_E_INVALID, "out is null");
-    if (d->out_on_host != 0) fail(TAURUS_E_INVALID, "out_on_host=%d is not supported by this build", d->out_on_host);
-    if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
 }
 
-static void layer_init(taurus_layer* L) {
+static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C, const uint64_t* mask,
+                                               hipStream_t s, int64_t budget) {
     const auto t_start = std::chrono::steady_clock::now();
-    hipStream_t s = L->s;
-    const taurus_graph& g = L->g;
-    const taurus_layer_desc& d = L->d;
-    const int64_t n = g.n, e = g.e, C = d.chunk;
-    L->n = n;
-    L->C = C;
-    L->nchunks = ceil_div(n, C);
-    L->d_o = d.d_out;
-    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.d_out;
-    row_group_shape(L->d_o, &L->G, &L->VEC);
+    auto idx = std::make_shared<ChunkIndex>(s, budget);
+    const int64_t n = g.n, e = g.e;
+    idx->g = g;
+    idx->C = C;
+    idx->nchunks = ceil_div(n, C);
+    idx->sampled = mask != nullptr;
     const int T = 256;
-    Arena tmp;  // init-only temporaries
+    const int64_t nch = idx->nchunks;
+    Arena tmp(s);
 
     // the caller's graph must be a valid simple CSR before anything indexes with it
     int* bad = tmp.alloc<int>(1, "graph flag");
@@ -538,16 +549,185 @@ static void layer_init(taurus_layer* L) {
     TAURUS_HIP(hipStreamSynchronize(s));
     if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
 
-    // degrees and arrival counts
-    int32_t* m = tmp.alloc<int32_t>(n, "in-degrees");
-    TAURUS_HIP(hipMemsetAsync(m, 0, (size_t)n * 4, s));
-    if (e > 0) {
-        k_in_degree<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.col_dst, e, m);
-        TAURUS_CHECK_LAUNCH();
+    // items sorted by (source chunk, destination), stably
+    const int vbits = std::max(1, bits_for(n - 1));
+    const int cbits = bits_for(nch);
+    if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
+    const int64_t total = e + n;
+    uint64_t* keys = tmp.alloc<uint64_t>(total, "index keys");
+    uint32_t* vals = tmp.alloc<uint32_t>(total, "index values");
+    k_make_items<<<(unsigned)ceil_div(total, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, nch, vbits, mask, keys,
+                                                            vals, bad);
+    TAURUS_CHECK_LAUNCH();
+    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    if (hbad) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
+    radix_sort_u64(keys, vals, total, vbits + cbits, tmp, s);
+
+    int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
+    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, total, nch, vbits, doffs);
+    TAURUS_CHECK_LAUNCH();
+    idx->chunk_off.resize((size_t)nch + 1);
+    TAURUS_HIP(hipMemcpyAsync(idx->chunk_off.data(), doffs, (size_t)(nch + 1) * 8, hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    const int64_t kept_total = idx->chunk_off[(size_t)nch];
+    idx->kept = kept_total - n;
+
+    // segments: heads, ids, starts
+    int32_t* head = tmp.alloc<int32_t>(kept_total, "segment heads");
+    int64_t* seg_id = tmp.alloc<int64_t>(kept_total + 1, "segment ids");
+    k_seg_heads<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(keys, kept_total, head);
+    TAURUS_CHECK_LAUNCH();
+    scan_i32_to_i64(head, seg_id, kept_total, true, tmp, s);
+    int64_t P = 0;
+    TAURUS_HIP(hipMemcpyAsync(&P, seg_id + kept_total, 8, hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    idx->pairs = P;
+    int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
+    k_seg_starts<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(head, seg_id, kept_total, seg_start);
+    TAURUS_CHECK_LAUNCH();
+
+    // classify segments into work units
+    idx->items_per_v = idx->arena.alloc<int32_t>(n, "items per vertex");
+    TAURUS_HIP(hipMemsetAsync(idx->items_per_v, 0, (size_t)n * 4, s));
+    int32_t* c_short = tmp.alloc<int32_t>(P, "short counts");
+    int32_t* c_long = tmp.alloc<int32_t>(P, "wave counts");
+    int32_t* c_fix = tmp.alloc<int32_t>(P, "fix counts");
+    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, idx->items_per_v, c_short,
+                                                          c_long, c_fix);
+    TAURUS_CHECK_LAUNCH();
+    int64_t* o_short = tmp.alloc<int64_t>(P + 1, "short offsets");
+    int64_t* o_long = tmp.alloc<int64_t>(P + 1, "wave offsets");
+    int64_t* o_fix = tmp.alloc<int64_t>(P + 1, "fix offsets");
+    scan_i32_to_i64(c_short, o_short, P, true, tmp, s);
+    scan_i32_to_i64(c_long, o_long, P, true, tmp, s);
+    scan_i32_to_i64(c_fix, o_fix, P, true, tmp, s);
+    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * 3, "chunk unit bases");
+    k_chunk_unit_bases<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, o_short, o_long, o_fix,
+                                                                    dbases);
+    TAURUS_CHECK_LAUNCH();
+    std::vector<int64_t> bases((size_t)(nch + 1) * 3);
+    TAURUS_HIP(hipMemcpyAsync(bases.data(), dbases, bases.size() * 8, hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    idx->short_off.resize((size_t)nch + 1);
+    idx->long_off.resize((size_t)nch + 1);
+    idx->fix_off.resize((size_t)nch + 1);
+    for (int64_t k = 0; k <= nch; k++) {
+        idx->short_off[k] = bases[k * 3 + 0];
+        idx->long_off[k] = bases[k * 3 + 1];
+        idx->fix_off[k] = bases[k * 3 + 2];
     }
-    L->messages = e;
+    idx->n_short = idx->short_off[nch];
+    idx->n_long = idx->long_off[nch];
+    idx->n_fix = idx->fix_off[nch];
+    for (int64_t k = 0; k < nch; k++)
+        idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->long_off[k + 1] - idx->long_off[k]);
+    if (idx->n_long >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many wave units");
+    idx->u_short = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_short), "short units");
+    idx->u_long = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_long), "wave units");
+    idx->u_fix = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_fix), "fix-up entries");
+    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, doffs, o_short, o_long, o_fix,
+                                                      idx->u_short, idx->u_long, idx->u_fix);
+    TAURUS_CHECK_LAUNCH();
+    idx->item_src = idx->arena.alloc<uint32_t>(std::max<int64_t>(1, kept_total), "item sources");
+    k_take_src<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(vals, kept_total, idx->item_src);
+    TAURUS_CHECK_LAUNCH();
+    tmp.release();
+    TAURUS_HIP(hipStreamSynchronize(s));
+    idx->ms_build = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    return idx;
+}
+
+}  // namespace taurus
+
+// ------------------------------------------------------------- handles -----
+
+struct taurus_plan {
+    taurus_graph g{};
+    int64_t chunk = 0;
+    std::shared_ptr<taurus::ChunkIndex> idx;
+};
+
+struct taurus_layer {
+    taurus_graph g{};
+    taurus_layer_desc d{};
+    hipStream_t s = nullptr;
+    taurus::Arena arena;
+    std::shared_ptr<taurus::ChunkIndex> idx;
+    bool poisoned = false;
+    int64_t n = 0, C = 0, nchunks = 0;
+    int d_o = 0, ncols = 0, G = 0, VEC = 0;
+    int2* cnt = nullptr;
+    float* n_out = nullptr;
+    float* acc = nullptr;
+    float* wpack = nullptr;
+    float* bias = nullptr;
+    float* Y = nullptr;
+    float* carry = nullptr;
+    int32_t* carry_cnt = nullptr;
+    uint64_t* mask = nullptr;
+    std::vector<uint8_t> pushed;
+    int64_t npushed = 0;
+    double ms_init = 0, ms_index = 0;
+    std::vector<hipEvent_t> events;  // 4 per chunk when profiling
+    ~taurus_layer() {
+        for (auto ev : events)
+            if (ev) (void)hipEventDestroy(ev);
+    }
+};
+
+namespace taurus {
+
+static void validate_desc(const taurus_layer_desc* d) {
+    if (!d) fail(TAURUS_E_INVALID, "null descriptor");
+    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM) fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
+    if (d->d_in <= 0 || d->d_out <= 0 || d->d_in % 4 || d->d_out % 4 || d->d_out > 1024 || d->d_in > 8192)
+        fail(TAURUS_E_INVALID, "d_in=%d d_out=%d: widths must be positive multiples of 4, d_out <= 1024",
+             d->d_in, d->d_out);
+    if (d->in_dtype != TAURUS_F32)
+        fail(TAURUS_E_INVALID, "in_dtype %d: only fp32 layer inputs are supported by this build", d->in_dtype);
+    if (d->out_dtype < 0 || d->out_dtype > 2) fail(TAURUS_E_INVALID, "out_dtype %d", d->out_dtype);
+    if (!d->weight) fail(TAURUS_E_INVALID, "weight is null");
+    if (d->chunk <= 0 || d->chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)d->chunk);
+    if (d->fanout < 0) fail(TAURUS_E_INVALID, "fanout %d", d->fanout);
+    if (d->fanout > 0) fail(TAURUS_E_INVALID, "fanout sampling is not supported by this build");
+    if (!d->out) fail(TAURUS_E_INVALID, "out is null");
+    if (d->out_on_host != 0) fail(TAURUS_E_INVALID, "out_on_host=%d is not supported by this build", d->out_on_host);
+    if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
+}
+
+static bool same_graph(const taurus_graph& a, const taurus_graph& b) {
+    return a.n == b.n && a.e == b.e && a.row_off == b.row_off && a.col_dst == b.col_dst;
+}
+
+static void layer_init(taurus_layer* L) {
+    const auto t_start = std::chrono::steady_clock::now();
+    hipStream_t s = L->s;
+    const taurus_graph& g = L->g;
+    const taurus_layer_desc& d = L->d;
+    const int64_t n = g.n, C = d.chunk;
+    L->n = n;
+    L->C = C;
+    L->nchunks = ceil_div(n, C);
+    L->d_o = d.d_out;
+    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.d_out;
+    row_group_shape(L->d_o, &L->G, &L->VEC);
+    const int T = 256;
+
+    // chunk index: shared from the plan for exact layers, else built here
+    const taurus_plan* plan = d.plan;
+    if (plan) {
+        if (!same_graph(plan->g, g) || plan->chunk != C)
+            fail(TAURUS_E_INVALID, "plan was built for another graph or chunk size");
+        L->idx = plan->idx;
+    } else {
+        L->idx = build_index(g, C, L->mask, s, 0);
+        L->ms_index = L->idx->ms_build;
+    }
+    const ChunkIndex& idx = *L->idx;
+
     L->cnt = L->arena.alloc<int2>(n, "pending counts");
-    k_init_counts<<<(unsigned)ceil_div(n, T), T, 0, s>>>(m, n, L->cnt);
+    k_init_counts<<<(unsigned)ceil_div(n, T), T, 0, s>>>(idx.items_per_v, n, L->cnt);
     TAURUS_CHECK_LAUNCH();
     if (d.agg == TAURUS_GCN_SYM) {
         L->n_out = L->arena.alloc<float>(n, "source norms");
@@ -565,96 +745,19 @@ static void layer_init(taurus_layer* L) {
     L->bias = L->arena.alloc<float>(L->d_o, "bias");
     TAURUS_HIP(hipMemcpyAsync(L->bias, hb.data(), hb.size() * 4, hipMemcpyHostToDevice, s));
 
-    // chunk index
-    const int vbits = std::max(1, bits_for(n - 1));
-    const int cbits = bits_for(L->nchunks);
-    if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "key does not fit 64 bits");
-    const int64_t total = e + n;
-    uint64_t* keys = tmp.alloc<uint64_t>(total, "index keys");
-    uint32_t* vals = tmp.alloc<uint32_t>(total, "index values");
-    k_make_items<<<(unsigned)ceil_div(total, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, L->nchunks, vbits,
-                                                            L->mask, keys, vals, bad);
-    TAURUS_CHECK_LAUNCH();
-    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    if (hbad) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
-    radix_sort_u64(keys, vals, total, vbits + cbits, tmp, s);
-    int64_t* doffs = tmp.alloc<int64_t>(L->nchunks + 1, "chunk offsets");
-    k_chunk_bounds<<<(unsigned)ceil_div(L->nchunks + 1, T), T, 0, s>>>(keys, total, L->nchunks, vbits, doffs);
-    TAURUS_CHECK_LAUNCH();
-    L->chunk_off.resize((size_t)L->nchunks + 1);
-    TAURUS_HIP(hipMemcpyAsync(L->chunk_off.data(), doffs, (size_t)(L->nchunks + 1) * 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    const int64_t kept_total = L->chunk_off[(size_t)L->nchunks];
-    unsigned long long* dpairs = tmp.alloc<unsigned long long>(1, "pair count");
-    TAURUS_HIP(hipMemsetAsync(dpairs, 0, 8, s));
-    k_count_pairs<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(keys, kept_total, dpairs);
-    TAURUS_CHECK_LAUNCH();
-    L->item_dst = L->arena.alloc<int32_t>(kept_total, "item destinations");
-    L->item_src = L->arena.alloc<uint32_t>(kept_total, "item sources");
-    k_split_items<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(keys, vals, kept_total, vbits, L->item_dst,
-                                                                 L->item_src);
-    TAURUS_CHECK_LAUNCH();
-    unsigned long long hpairs = 0;
-    TAURUS_HIP(hipMemcpyAsync(&hpairs, dpairs, 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    L->pairs = (int64_t)hpairs;
-    tmp.free_ptr(vals);
-    tmp.free_ptr(keys);
-
-    // tiles and the segments that straddle them
-    std::vector<int64_t> bpos;
-    for (int64_t k = 0; k < L->nchunks; k++) {
-        const int64_t cnt_k = L->chunk_off[k + 1] - L->chunk_off[k];
-        const int64_t nt = ceil_div(cnt_k, SC_TILE);
-        L->ntiles_total += nt;
-        L->max_tiles = (int)std::max<int64_t>(L->max_tiles, nt);
-        for (int64_t t = 1; t < nt; t++) bpos.push_back(L->chunk_off[k] + t * SC_TILE);
-    }
-    std::vector<int2> bval(bpos.size());
-    if (!bpos.empty()) {
-        int64_t* dpos = tmp.alloc<int64_t>((int64_t)bpos.size(), "tile bounds");
-        int2* dval = tmp.alloc<int2>((int64_t)bpos.size(), "tile bound values");
-        TAURUS_HIP(hipMemcpyAsync(dpos, bpos.data(), bpos.size() * 8, hipMemcpyHostToDevice, s));
-        k_gather_bounds<<<(unsigned)ceil_div((int64_t)bpos.size(), T), T, 0, s>>>(L->item_dst, dpos,
-                                                                                 (int64_t)bpos.size(), dval);
-        TAURUS_CHECK_LAUNCH();
-        TAURUS_HIP(hipMemcpyAsync(bval.data(), dval, bpos.size() * sizeof(int2), hipMemcpyDeviceToHost, s));
-        TAURUS_HIP(hipStreamSynchronize(s));
-    }
-    std::vector<int4> hfix;
-    L->fix_off.assign((size_t)L->nchunks + 1, 0);
-    size_t bi = 0;
-    for (int64_t k = 0; k < L->nchunks; k++) {
-        L->fix_off[k] = (int64_t)hfix.size();
-        const int64_t nt = ceil_div(L->chunk_off[k + 1] - L->chunk_off[k], SC_TILE);
-        bool prev_split = false;
-        int prev_v = -1;
-        for (int64_t t = 1; t < nt; t++, bi++) {
-            const int2 bv = bval[bi];  // (dst before, dst at) tile t's first item
-            const bool split = bv.x == bv.y;
-            if (split) {
-                if (prev_split && prev_v == bv.y) hfix.back().z = (int)t;  // tile t-1 lies inside the segment
-                else hfix.push_back(make_int4(bv.y, (int)(t - 1), (int)t, 0));
-            }
-            prev_split = split;
-            prev_v = bv.y;
-        }
-    }
-    L->fix_off[(size_t)L->nchunks] = (int64_t)hfix.size();
-    if (!hfix.empty()) {
-        L->fix = L->arena.alloc<int4>((int64_t)hfix.size(), "fix-up list");
-        TAURUS_HIP(hipMemcpyAsync(L->fix, hfix.data(), hfix.size() * sizeof(int4), hipMemcpyHostToDevice, s));
-    }
-
     // working buffers
     L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
     L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
-    L->carry = L->arena.alloc<float>((int64_t)std::max(1, L->max_tiles) * 2 * L->d_o, "tile carries");
-    L->carry_cnt = L->arena.alloc<int32_t>((int64_t)std::max(1, L->max_tiles) * 2, "tile carry counts");
+    const int64_t slots = std::max<int64_t>(1, idx.max_long_per_chunk);
+    L->carry = L->arena.alloc<float>(slots * L->d_o, "hub piece carries");
+    L->carry_cnt = L->arena.alloc<int32_t>(slots, "hub piece counts");
     L->pushed.assign((size_t)L->nchunks, 0);
+    if (d.profile) {  // four events per chunk: before/after transform, scatter, fix-up
+        L->events.assign((size_t)L->nchunks * 4, nullptr);
+        for (auto& ev : L->events) TAURUS_HIP(hipEventCreate(&ev));
+    }
+    // host-side copies above read pageable memory that must stay valid until they ran
     TAURUS_HIP(hipStreamSynchronize(s));
-    tmp.release();
     L->ms_init = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
 }
 
@@ -667,28 +770,23 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     if (x_on_host != 0) fail(TAURUS_E_INVALID, "host-resident chunks are not supported by this build");
     const int64_t k = b / L->C;
     if (L->pushed[(size_t)k]) fail(TAURUS_E_STATE, "chunk %lld pushed twice", (long long)k);
+    const ChunkIndex& idx = *L->idx;
     hipStream_t s = L->s;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     if (L->d.profile) {
-        for (int i = 0; i < 4; i++) {
-            TAURUS_HIP(hipEventCreate(&ev[i]));
-            L->events.push_back(ev[i]);
-        }
+        for (int i = 0; i < 4; i++) ev[i] = L->events[(size_t)k * 4 + i];
         TAURUS_HIP(hipEventRecord(ev[0], s));
     }
     L->pushed[(size_t)k] = 1;
     L->npushed++;
-    const int64_t rows = e - b;
-    gemm_f32(static_cast<const float*>(x), rows, L->d.d_in, L->wpack, L->ncols, L->n_out ? L->n_out + b : nullptr,
+    gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, L->n_out ? L->n_out + b : nullptr,
              L->Y, s);
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
     ScatterParams p;
     p.Y = L->Y;
     p.ystride = L->ncols;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
-    p.dst = L->item_dst + L->chunk_off[(size_t)k];
-    p.src = L->item_src + L->chunk_off[(size_t)k];
-    p.nitems = L->chunk_off[(size_t)k + 1] - L->chunk_off[(size_t)k];
+    p.src = idx.item_src + idx.chunk_off[(size_t)k];
     p.cnt = L->cnt;
     p.acc = L->acc;
     p.d_o = L->d_o;
@@ -699,18 +797,23 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.out = L->d.out;
     p.carry = L->carry;
     p.carry_cnt = L->carry_cnt;
-    const int64_t ntiles = ceil_div(p.nitems, SC_TILE);
-    if (ntiles > 0) dispatch_scatter(L->G, L->VEC, p, ntiles, s);
+    p.long_base = idx.long_off[(size_t)k];
+    const int64_t ns = idx.short_off[(size_t)k + 1] - idx.short_off[(size_t)k];
+    const int64_t nl = idx.long_off[(size_t)k + 1] - idx.long_off[(size_t)k];
+    if (ns + nl > 0)
+        dispatch_scatter(L->G, L->VEC, p, idx.u_short + idx.short_off[(size_t)k], ns,
+                         idx.u_long + idx.long_off[(size_t)k], nl, s);
     if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
-    const int64_t nfix = L->fix_off[(size_t)k + 1] - L->fix_off[(size_t)k];
-    if (nfix > 0) dispatch_fixup(L->G, L->VEC, p, L->fix + L->fix_off[(size_t)k], nfix, s);
+    const int64_t nfix = idx.fix_off[(size_t)k + 1] - idx.fix_off[(size_t)k];
+    if (nfix > 0) dispatch_fixup(L->G, L->VEC, p, idx.u_fix + idx.fix_off[(size_t)k], nfix, s);
     if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
 }
 
 static int finalize(taurus_layer* L, taurus_stats* st) {
     if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
     hipStream_t s = L->s;
-    Arena tmp;
+    const ChunkIndex& idx = *L->idx;
+    Arena tmp(s);
     unsigned long long* dleft = tmp.alloc<unsigned long long>(1, "pending count");
     TAURUS_HIP(hipMemsetAsync(dleft, 0, 8, s));
     k_count_pending<<<(unsigned)ceil_div(L->n, 256), 256, 0, s>>>(L->cnt, L->n, dleft);
@@ -722,18 +825,21 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         std::memset(st, 0, sizeof(*st));
         st->n = L->n;
         st->e = L->g.e;
-        st->messages = L->messages;
+        st->messages = idx.kept;
         st->self_terms = L->n;
-        st->pairs = L->pairs;
+        st->pairs = idx.pairs;
         st->pending_left = (int64_t)left;
         st->completed = L->n - (int64_t)left;
         st->chunks = L->nchunks;
         st->chunks_pushed = L->npushed;
-        st->tiles = L->ntiles_total;
-        st->split_segments = L->fix_off.empty() ? 0 : L->fix_off.back();
-        st->device_bytes = L->arena.peak();
+        st->short_units = idx.n_short;
+        st->wave_units = idx.n_long;
+        st->split_segments = idx.n_fix;
+        st->device_bytes = L->arena.peak() + (L->ms_index > 0 ? idx.arena.peak() : 0);
         st->ms_init = L->ms_init;
         for (size_t i = 0; i + 3 < L->events.size(); i += 4) {
+            const size_t k = i / 4;
+            if (!L->pushed[k]) continue;
             float a = 0, b = 0, c = 0;
             TAURUS_HIP(hipEventElapsedTime(&a, L->events[i], L->events[i + 1]));
             TAURUS_HIP(hipEventElapsedTime(&b, L->events[i + 1], L->events[i + 2]));
@@ -742,8 +848,8 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
             st->ms_scatter += b;
             st->ms_fixup += c;
             st->launches_gemm++;
-            st->launches_scatter++;
-            st->launches_fixup++;
+            st->launches_scatter += (idx.short_off[k + 1] > idx.short_off[k] || idx.long_off[k + 1] > idx.long_off[k]) ? 1 : 0;
+            st->launches_fixup += idx.fix_off[k + 1] > idx.fix_off[k] ? 1 : 0;
         }
     }
     return left ? TAURUS_E_INCOMPLETE : TAURUS_OK;
@@ -754,19 +860,6 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
 // ------------------------------------------------------------------ C ABI --
 
 using namespace taurus;
-
-#define TAURUS_GUARD(body)                                                 \
-    try {                                                                  \
-        body;                                                              \
-    } catch (const Failure& f_) {                                          \
-        return f_.status;                                                  \
-    } catch (const std::exception& x_) {                                   \
-        set_error("internal error: %s", x_.what());                        \
-        return TAURUS_E_DEVICE;                                            \
-    } catch (...) {                                                        \
-        set_error("internal error");                                       \
-        return TAURUS_E_DEVICE;                                            \
-    }
 
 extern "C" {
 
@@ -785,8 +878,40 @@ uint64_t taurus_hash(uint64_t seed, uint64_t tag, int32_t nargs, const uint64_t*
 
 int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
                      int32_t* col_dst, void* stream) {
-    TAURUS_GUARD(return build_csr_impl(n, e, src, dst, row_off, col_dst, static_cast<hipStream_t>(stream)));
+    try {
+        return build_csr_impl(n, e, src, dst, row_off, col_dst, static_cast<hipStream_t>(stream));
+    } catch (const Failure& f) {
+        return f.status;
+    } catch (const std::exception& x) {
+        set_error("internal error: %s", x.what());
+        return TAURUS_E_DEVICE;
+    }
 }
+
+int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, taurus_plan** out) {
+    if (!out) {
+        set_error("out handle pointer is null");
+        return TAURUS_E_INVALID;
+    }
+    *out = nullptr;
+    try {
+        check_graph_args(g);
+        if (chunk <= 0 || chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)chunk);
+        auto P = std::make_unique<taurus_plan>();
+        P->g = *g;
+        P->chunk = chunk;
+        P->idx = build_index(*g, chunk, nullptr, static_cast<hipStream_t>(stream), 0);
+        *out = P.release();
+        return TAURUS_OK;
+    } catch (const Failure& f) {
+        return f.status;
+    } catch (const std::exception& x) {
+        set_error("internal error: %s", x.what());
+        return TAURUS_E_DEVICE;
+    }
+}
+
+void taurus_plan_destroy(taurus_plan* P) { delete P; }
 
 int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_layer** out) {
     if (!out) {
@@ -796,19 +921,23 @@ int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_
     *out = nullptr;
     taurus_layer* L = nullptr;
     try {
-        validate(g, d);
+        check_graph_args(g);
+        validate_desc(d);
         L = new taurus_layer();
         L->g = *g;
         L->d = *d;
         L->s = static_cast<hipStream_t>(d->stream);
+        L->arena.set_stream(L->s);
         L->arena.set_budget(d->hbm_budget);
         layer_init(L);
         *out = L;
         return TAURUS_OK;
     } catch (const Failure& f) {
+        if (L) (void)hipStreamSynchronize(L->s);
         delete L;
         return f.status;
     } catch (const std::exception& x) {
+        if (L) (void)hipStreamSynchronize(L->s);
         delete L;
         set_error("internal error: %s", x.what());
         return TAURUS_E_DEVICE;
@@ -835,10 +964,11 @@ int taurus_finalize(taurus_layer* L, taurus_stats* stats) {
         return TAURUS_E_INVALID;
     }
     try {
-        int rc = finalize(L, stats);
+        taurus_stats local;
+        taurus_stats* st = stats ? stats : &local;
+        int rc = finalize(L, st);
         if (rc == TAURUS_E_INCOMPLETE)
-            set_error("%lld destinations still have pending messages",
-                      (long long)(stats ? stats->pending_left : -1));
+            set_error("%lld destinations still have pending messages", (long long)st->pending_left);
         return rc;
     } catch (const Failure& f) {
         if (f.status == TAURUS_E_OOM || f.status == TAURUS_E_DEVICE) L->poisoned = true;
@@ -851,7 +981,7 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
         set_error("null argument");
         return TAURUS_E_INVALID;
     }
-    TAURUS_GUARD({
+    try {
         const int64_t words = ceil_div(L->g.e, 64);
         if (L->mask) {
             TAURUS_HIP(hipMemcpyAsync(mask_bits_host, L->mask, (size_t)words * 8, hipMemcpyDeviceToHost, L->s));
@@ -860,9 +990,11 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
             for (int64_t w = 0; w < words; w++) mask_bits_host[w] = ~0ull;
             if (L->g.e % 64) mask_bits_host[words - 1] = (1ull << (L->g.e % 64)) - 1;
         }
-        if (n_kept) *n_kept = L->messages;
+        if (n_kept) *n_kept = L->idx->kept;
         return TAURUS_OK;
-    });
+    } catch (const Failure& f) {
+        return f.status;
+    }
 }
 
 void taurus_layer_destroy(taurus_layer* L) {

@@ -33,18 +33,32 @@ void fail(int status, const char* fmt, ...) {
 const char* last_error_cstr() { return g_last_error.c_str(); }
 
 // ---------------------------------------------------------------- arena -----
+static void keep_pool_memory() {
+    static bool done[64] = {false};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || done[dev]) return;
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+        uint64_t keep = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+    }
+    (void)hipGetLastError();
+    done[dev] = true;
+}
+
 void* Arena::alloc_bytes(int64_t bytes, const char* what) {
     if (bytes <= 0) bytes = 16;
     bytes = (bytes + 255) & ~(int64_t)255;
     if (budget_ > 0 && bytes_ + bytes > budget_)
         fail(TAURUS_E_BUDGET, "allocating %lld bytes for %s exceeds the budget (%lld of %lld in use)",
              (long long)bytes, what, (long long)bytes_, (long long)budget_);
+    keep_pool_memory();
     void* p = nullptr;
-    hipError_t e = hipMalloc(&p, (size_t)bytes);
+    hipError_t e = hipMallocAsync(&p, (size_t)bytes, stream_);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         fail(e == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE,
-             "hipMalloc(%lld) for %s failed: %s", (long long)bytes, what, hipGetErrorString(e));
+             "hipMallocAsync(%lld) for %s failed: %s", (long long)bytes, what, hipGetErrorString(e));
     }
     blocks_.push_back({p, bytes});
     bytes_ += bytes;
@@ -55,7 +69,7 @@ void* Arena::alloc_bytes(int64_t bytes, const char* what) {
 void Arena::free_ptr(void* p) {
     for (size_t i = 0; i < blocks_.size(); i++) {
         if (blocks_[i].p == p) {
-            (void)hipFree(p);
+            (void)hipFreeAsync(p, stream_);
             bytes_ -= blocks_[i].bytes;
             blocks_.erase(blocks_.begin() + (long)i);
             return;
@@ -64,7 +78,7 @@ void Arena::free_ptr(void* p) {
 }
 
 void Arena::release() {
-    for (auto& b : blocks_) (void)hipFree(b.p);
+    for (auto& b : blocks_) (void)hipFreeAsync(b.p, stream_);
     blocks_.clear();
     bytes_ = 0;
 }
@@ -187,7 +201,6 @@ static void scan_impl(const Tin* in, Tout* out, int64_t n, bool write_total, Are
         k_write_total<Tout><<<1, 64, 0, s>>>(sums_scanned, sums, nb, out, n);
         TAURUS_CHECK_LAUNCH();
     }
-    TAURUS_HIP(hipStreamSynchronize(s));
     arena.free_ptr(sums_scanned);
     arena.free_ptr(sums);
 }

@@ -26,7 +26,8 @@ def native():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for required in ("taurus_layer_init", "taurus_push_chunk", "taurus_finalize", "taurus_sampled_edges",
-                     "taurus_build_csr", "taurus_layer_destroy", "taurus_last_error", "taurus_hash"):
+                     "taurus_build_csr", "taurus_layer_destroy", "taurus_last_error", "taurus_hash",
+                     "taurus_plan_create", "taurus_plan_destroy"):
         assert required in names
 
 
@@ -42,8 +43,9 @@ def test_binding_structs_match_header_layout(native):
     assert ctypes.sizeof(native.Graph) == 32
     assert native.LayerDesc.weight.offset == 24 and native.LayerDesc.seed.offset == 48
     assert native.LayerDesc.out.offset == 80 and native.LayerDesc.stream.offset == 96
-    assert ctypes.sizeof(native.LayerDesc) == 112
-    assert ctypes.sizeof(native.Stats) == 14 * 8 + 5 * 8 + 3 * 8
+    assert native.LayerDesc.plan.offset == 112
+    assert ctypes.sizeof(native.LayerDesc) == 120
+    assert ctypes.sizeof(native.Stats) == 15 * 8 + 5 * 8 + 3 * 8
 
 
 def test_hash_matches_published_splitmix64(golden_dir):
@@ -67,6 +69,11 @@ def test_invalid_arguments_rejected_before_device_work(native):
     assert L.taurus_sampled_edges(None, None, None) == native.E_INVALID
     assert L.taurus_build_csr(0, 0, None, None, None, None, None) == native.E_INVALID
     L.taurus_layer_destroy(None)
+    L.taurus_plan_destroy(None)
+    hp = ctypes.c_void_p()
+    assert L.taurus_plan_create(None, 16, None, ctypes.byref(hp)) == native.E_INVALID
+    g1 = native.Graph(10, 0, 1, None)
+    assert L.taurus_plan_create(ctypes.byref(g1), 0, None, ctypes.byref(hp)) == native.E_INVALID
     # width not a multiple of 4
     g = native.Graph(10, 0, 1, None)
     w = np.zeros(16, np.float32)

@@ -103,14 +103,35 @@ def test_sage_small_workload_full(torch_cuda):
 
 
 @pytest.mark.parametrize("chunk", [1, 7, 1000, 4096, 10000])
-def test_chunk_size_invariance(torch_cuda, chunk):
+@pytest.mark.parametrize("use_plan", [True, False])
+def test_chunk_size_invariance(torch_cuda, chunk, use_plan):
     w = WL.SAGE_RMAT_4K
-    _note(f"chunk invariance chunk={chunk}")
+    _note(f"chunk invariance chunk={chunk} plan={use_plan}")
     src, dst = WL.graph(w)
     _, zs = H.oracle_model(w, src, dst)
     row_off, col_dst = H.gpu_graph(w, src, dst)
-    outs, _ = H.gpu_model(w, row_off, col_dst, chunk=chunk)
+    outs, _ = H.gpu_model(w, row_off, col_dst, chunk=chunk, use_plan=use_plan)
     _check_model(w, outs, zs, f"chunk {chunk}")
+
+
+def test_plan_mismatch_rejected(torch_cuda):
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    _note("plan mismatch")
+    w = WL.SAGE_RMAT_4K
+    row_off, col_dst = H.gpu_graph(w)
+    plan = T.Plan(w.n, row_off, col_dst, 512)
+    spec = H.layer_specs(w)[0]
+    out = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+    with pytest.raises(T.TaurusError) as ex:
+        T.Layer(w.n, row_off, col_dst, out=out, chunk=1024, plan=plan, **spec)
+    assert ex.value.status == -1
+    # a layer keeps the shared index alive after the plan is destroyed
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=512, plan=plan, **spec)
+    plan.destroy()
+    L.push_all(torch.from_numpy(WL.input_features(w)).cuda())
+    assert L.finalize()["pending_left"] == 0
+    L.destroy()
 
 
 def test_chunk_order_invariance(torch_cuda):
