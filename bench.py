@@ -34,20 +34,75 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
-def scatter_algorithmic_bytes(st: dict, d_o: int, ncols: int, out_bytes: int) -> float:
-    """Bytes the scatter step must move for one layer (all its launches).
+# a segment of more than this many messages is cut into pieces of this length
+# and completed by the fix-up kernel; the library's work-unit counts are
+# checked against the ones derived here
+PIECE_LEN = 512
+SHORT_LEN = 8
 
-    the work-unit table (16 bytes per unit) and each item's source code (4);
-    the chunk transform Y read once (4 * ncols per vertex); pending/expected
-    counts 8 read + 4 written per (destination, chunk) pair; accumulator
-    rows: every pair but a vertex's first reads its row and every pair but
-    its last writes it (4 * d_o each); one output row per vertex.  Hub
-    segments completed by the fix-up pass are taken out (their accumulator
-    traffic is the fix-up kernel's)."""
-    n, items, pairs = st["n"], st["messages"] + st["self_terms"], st["pairs"]
-    units, splits = st["short_units"] + st["wave_units"], st["split_segments"]
-    return (16.0 * units + 4.0 * items + 4.0 * n * ncols + 12.0 * pairs + 8.0 * d_o * (pairs - n)
-            + out_bytes * d_o * n - 8.0 * d_o * splits)
+
+def flush_model(src, dst, n: int, chunk: int) -> dict:
+    """Per-kernel flush structure of one exact layer, from the graph alone.
+
+    A segment is the run of messages from one source chunk to one
+    destination.  Chunks are pushed in ascending order and, within a chunk,
+    the self pass runs before the scatter, so for destination v (own chunk
+    c(v)) a segment from chunk j is its first flush (accumulator logically
+    zero, no read) iff j is v's smallest message chunk and j < c(v), and its
+    last (output row written instead of the accumulator) iff j is v's largest
+    message chunk and j >= c(v)."""
+    import numpy as np
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    key = (src // chunk) * n + dst
+    seg, lens = np.unique(key, return_counts=True)
+    ch, v = seg // n, seg % n
+    cv = v // chunk
+    big = np.iinfo(np.int64).max
+    minch = np.full(n, big, dtype=np.int64)
+    maxch = np.full(n, -1, dtype=np.int64)
+    np.minimum.at(minch, v, ch)
+    np.maximum.at(maxch, v, ch)
+    fresh = (ch == minch[v]) & (ch < cv)
+    final = (ch == maxch[v]) & (ch >= cv)
+    split = lens > PIECE_LEN
+    pieces = np.where(lens > SHORT_LEN, (lens + PIECE_LEN - 1) // PIECE_LEN, 1)
+    own = np.arange(n, dtype=np.int64) // chunk
+    has_msg = maxch >= 0
+    self_read = has_msg & (minch < own)          # an earlier chunk already flushed into v
+    self_final = ~has_msg | (maxch < own)        # no later segment: the self flush completes v
+    active_src = np.unique(src).size
+    return {
+        "messages": int(src.size), "segments": int(seg.size), "units": int(pieces.sum()),
+        "short_units": int((lens <= SHORT_LEN).sum()), "split_segments": int(split.sum()),
+        "active_src": int(active_src),
+        # scatter-owned flushes (segments completed in the scatter kernel)
+        "sc_flush": int((~split).sum()), "sc_fresh": int((~split & fresh).sum()),
+        "sc_final": int((~split & final).sum()), "split_pieces": int(pieces[split].sum()),
+        "fx_fresh": int((split & fresh).sum()), "fx_final": int((split & final).sum()),
+        "self_read": int(self_read.sum()), "self_final": int(self_final.sum()),
+    }
+
+
+def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int) -> dict:
+    """Algorithmic HBM bytes of each per-layer kernel (all its launches).
+
+    flush: counts read 8 + written 4; the accumulator row read (4 d_o) unless
+    the flush is v's first; the accumulator row written (4 d_o), or the output
+    row (out_bytes d_o) for v's last flush.
+    scatter: 16 per work unit, 4 per message (source code), each source's Y
+    row once (4 d_o), the flushes it owns, and a hub piece's partial row and
+    count (4 d_o + 4) to the carry buffer.
+    self: each vertex's self row of Y (4 d_o) and one flush.
+    fix-up: 16 per hub segment, its pieces' carries read back, one flush."""
+    def flushes(k, fresh, final):
+        return 12.0 * k + 4.0 * d_o * (k - fresh) + out_bytes * d_o * final + 4.0 * d_o * (k - final)
+    sc = (16.0 * fm["units"] + 4.0 * fm["messages"] + 4.0 * d_o * fm["active_src"]
+          + flushes(fm["sc_flush"], fm["sc_fresh"], fm["sc_final"]) + (4.0 * d_o + 4.0) * fm["split_pieces"])
+    se = 4.0 * d_o * n + flushes(n, n - fm["self_read"], fm["self_final"])
+    fx = (16.0 * fm["split_segments"] + (4.0 * d_o + 4.0) * fm["split_pieces"]
+          + flushes(fm["split_segments"], fm["fx_fresh"], fm["fx_final"]))
+    return {"scatter": sc, "self": se, "fixup": fx}
 
 
 def main():
@@ -89,6 +144,7 @@ def main():
             c.copy_(a)
         del a, c
     torch.cuda.synchronize()
+    fm = flush_model(src, dst, w.n, w.chunk)
 
     def step():
         t0 = time.perf_counter()
@@ -123,33 +179,39 @@ def main():
     # per-layer figures, averaged over the timed steps
     nl = len(specs)
     layers = []
-    tot_bytes = tot_ms = tot_launch = 0.0
+    tot = {"scatter": [0.0, 0.0, 0], "self": [0.0, 0.0, 0], "fixup": [0.0, 0.0, 0]}  # bytes, ms, launches
     gemm_flops = gemm_ms = 0.0
+    model_ok = True
     for li in range(nl):
         sts = [r[2][li] for r in runs]
         d_o, d_in = specs[li]["d_out"], specs[li]["d_in"]
         ncols = d_o  # GCN transform width
         wall = float(np.mean([s["wall_ms"] for s in sts]))
         st = sts[-1]
-        b = scatter_algorithmic_bytes(st, d_o, ncols, 4)
-        sc_ms = float(np.mean([s["ms_scatter"] for s in sts]))
-        launches = st["launches_scatter"]
+        kb = kernel_bytes(fm, w.n, d_o, 4)
+        checks = (st["short_units"] == fm["short_units"], st["wave_units"] == fm["units"] - fm["short_units"],
+                  st["split_segments"] == fm["split_segments"], st["pairs"] == fm["segments"] + w.n,
+                  st["messages"] == fm["messages"])
+        if not all(checks):
+            model_ok = False
+            print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
+        ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts])) for k in ("gemm", "self", "scatter", "fixup", "init")}
         if profile:
-            tot_bytes += b * len(sts)
-            tot_ms += sum(s["ms_scatter"] for s in sts)
-            tot_launch += launches * len(sts)
+            for k in tot:
+                tot[k][0] += kb[k] * len(sts)
+                tot[k][1] += sum(s[f"ms_{k}"] for s in sts)
+                tot[k][2] += sum(s[f"launches_{k}"] for s in sts)
             gemm_flops += 2.0 * w.n * d_in * ncols * len(sts)
             gemm_ms += sum(s["ms_gemm"] for s in sts)
         layers.append({
             "layer": li + 1, "d_in": d_in, "d_out": d_o, "edges": st["messages"], "pairs": st["pairs"],
             "wall_ms": round(wall, 3), "gteps": round(st["messages"] / (wall * 1e-3) / 1e9, 3),
-            "vertices_per_s": round(w.n / (wall * 1e-3), 1), "init_ms": round(float(np.mean([s["ms_init"] for s in sts])), 3),
-            "gemm_ms": round(float(np.mean([s["ms_gemm"] for s in sts])), 3), "scatter_ms": round(sc_ms, 3),
-            "fixup_ms": round(float(np.mean([s["ms_fixup"] for s in sts])), 3),
-            "scatter_launches": launches, "short_units": st["short_units"], "wave_units": st["wave_units"],
+            "vertices_per_s": round(w.n / (wall * 1e-3), 1),
+            **{f"{k}_ms": round(v, 3) for k, v in ms.items()},
+            "short_units": st["short_units"], "wave_units": st["wave_units"],
             "split_segments": st["split_segments"],
-            "scatter_algorithmic_gb": round(b / 1e9, 4),
-            "scatter_gbs": round(b / (sc_ms * 1e-3) / 1e9, 1) if sc_ms > 0 else None,
+            **{f"{k}_algorithmic_gb": round(kb[k] / 1e9, 4) for k in kb},
+            **{f"{k}_gbs": (round(kb[k] / (ms[k] * 1e-3) / 1e9, 1) if ms[k] > 0 else None) for k in kb},
         })
     csr_ms = float(np.mean([r[0] for r in runs]))
     plan_ms = float(np.mean([r[1] for r in runs]))
@@ -157,12 +219,13 @@ def main():
     value = total_edges / (ms_step * 1e-3) / 1e9
 
     roofline = None
-    if profile and tot_ms > 0:
-        achieved = tot_bytes / (tot_ms * 1e-3) / 1e9
+    if profile and tot["scatter"][1] > 0:
+        byt, ms_, nlaunch = tot["scatter"]
+        achieved = byt / (ms_ * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_scatter",
-                    "avg_launch_us": round(tot_ms * 1e3 / tot_launch, 2),
-                    "bytes_per_launch": round(tot_bytes / tot_launch, 0)}
+                    "avg_launch_us": round(ms_ * 1e3 / nlaunch, 2), "bytes_per_launch": round(byt / nlaunch, 0),
+                    "model_check": model_ok}
     gemm = None
     if profile and gemm_ms > 0:
         tf = gemm_flops / (gemm_ms * 1e-3) / 1e12

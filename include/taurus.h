@@ -132,7 +132,9 @@ typedef struct {
     int64_t n, e;                  /* graph size                                        */
     int64_t messages;              /* E_l: propagated in-edges (sum of |M(v)|)          */
     int64_t self_terms;            /* self messages (= n)                               */
-    int64_t pairs;                 /* P_l: touched (destination, chunk) pairs incl. self */
+    int64_t pairs;                 /* accumulator flushes: (destination, chunk) segments
+                                      of propagated messages, plus one self flush per
+                                      vertex                                            */
     int64_t completed;             /* vertices whose output row was written             */
     int64_t pending_left;          /* vertices still waiting for messages               */
     int64_t chunks, chunks_pushed;
@@ -143,8 +145,8 @@ typedef struct {
     int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
     double hub_message_share;      /* share of messages landing on resident hubs        */
     /* milliseconds, HIP-event timed when desc.profile = 1 (else 0) */
-    double ms_init, ms_gemm, ms_scatter, ms_fixup;
-    int64_t launches_gemm, launches_scatter, launches_fixup;
+    double ms_init, ms_gemm, ms_self, ms_scatter, ms_fixup;
+    int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
 } taurus_stats;
 
 /* Thread-local message describing the last failing call on this thread. */

@@ -48,9 +48,9 @@ class Stats(ctypes.Structure):
         "chunks_pushed", "short_units", "wave_units", "split_segments", "evictions", "reloads",
         "device_bytes")] + [
         ("hub_message_share", ctypes.c_double), ("ms_init", ctypes.c_double), ("ms_gemm", ctypes.c_double),
-        ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),
-        ("launches_gemm", ctypes.c_int64), ("launches_scatter", ctypes.c_int64),
-        ("launches_fixup", ctypes.c_int64)]
+        ("ms_self", ctypes.c_double), ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),
+        ("launches_gemm", ctypes.c_int64), ("launches_self", ctypes.c_int64),
+        ("launches_scatter", ctypes.c_int64), ("launches_fixup", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

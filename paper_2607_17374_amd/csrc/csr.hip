@@ -54,23 +54,26 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
     Arena arena(s);
     const int vbits = bits_for(n - 1) > 0 ? bits_for(n - 1) : 1;
     int* bad = arena.alloc<int>(1, "flag");
-    TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));
-    uint64_t* keys = arena.alloc<uint64_t>(e > 0 ? e : 1, "edge keys");
+    fill_i32(bad, 1, 0, s);
+    SortBuffers sb{{arena.alloc<uint64_t>(e > 0 ? e : 1, "edge keys"), nullptr}, {nullptr, nullptr}, 0};
     const int T = 256;
     if (e > 0) {
-        k_pack_edges<<<(unsigned)ceil_div(e, T), T, 0, s>>>(src, dst, e, n, vbits, keys, bad);
+        sb.keys[1] = arena.alloc<uint64_t>(e, "edge keys (ping-pong)");
+        k_pack_edges<<<(unsigned)ceil_div(e, T), T, 0, s>>>(src, dst, e, n, vbits, sb.keys[0], bad);
         TAURUS_CHECK_LAUNCH();
-        radix_sort_u64(keys, nullptr, e, 2 * vbits, arena, s);
-        k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(keys, e, vbits, col_dst, bad);
+        radix_sort_u64(sb, e, 2 * vbits, arena, s, bad, 4);
+        k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, vbits, col_dst, bad);
         TAURUS_CHECK_LAUNCH();
     }
-    k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(keys, e, n, vbits, row_off);
+    k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);
     TAURUS_CHECK_LAUNCH();
     int hbad = 0;
-    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
+    Readback rb;
+    rb.add(&hbad, bad, 1);
+    rb.run(s);
     if (hbad & 1) fail(TAURUS_E_INVALID, "taurus_build_csr: vertex id out of range or self loop");
     if (hbad & 2) fail(TAURUS_E_INVALID, "taurus_build_csr: repeated edge");
+    if (hbad & 4) fail(TAURUS_E_DEVICE, "taurus_build_csr: radix sort offset out of range");
     return TAURUS_OK;
 }
 

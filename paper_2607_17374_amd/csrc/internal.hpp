@@ -36,9 +36,39 @@ struct Failure {
 
 #define TAURUS_CHECK_LAUNCH() TAURUS_HIP(hipGetLastError())
 
-// Device allocations owned by one object, with a byte budget.  Memory is
-// stream ordered (hipMallocAsync / hipFreeAsync on the owner's stream) from
-// the device's default pool, which keeps freed blocks for reuse, so layers
+// Device memory cache (prims.hip): device_acquire returns a block of at
+// least `bytes` usable in stream order on `s` (*got = its size);
+// device_release hands it back after the work queued on `s` so far.
+void* device_acquire(size_t bytes, hipStream_t s, size_t* got);
+void device_release(void* p, hipStream_t s);
+
+// Pinned host buffer of at least `bytes` for the calling thread (reused by
+// its next call).
+void* pinned_staging(size_t bytes);
+
+// Small device-to-host reads gathered into one pinned transfer and one
+// stream synchronisation: add() any number, then run().
+class Readback {
+public:
+    void add(void* host, const void* dev, size_t bytes);
+    template <typename T>
+    void add(T* host, const T* dev, int64_t count) {
+        add(static_cast<void*>(host), static_cast<const void*>(dev), (size_t)count * sizeof(T));
+    }
+    void run(hipStream_t s);
+
+private:
+    struct Item {
+        void* host;
+        const void* dev;
+        size_t bytes, off;
+    };
+    std::vector<Item> items_;
+    size_t total_ = 0;
+};
+
+// Device allocations owned by one object, with a byte budget, taken from and
+// returned to the device memory cache on the owner's stream, so objects
 // created one after another recycle each other's buffers.
 class Arena {
 public:
@@ -85,10 +115,20 @@ void scan_u32_to_u64(const uint32_t* in, uint64_t* out, int64_t n, bool write_to
 void scan_i32_to_i64(const int32_t* in, int64_t* out, int64_t n, bool write_total, Arena& arena,
                      hipStream_t s);
 
+// p[0..n) = v
+void fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+
 // Stable LSD radix sort of 64-bit keys over bits [0, key_bits), carrying
-// optional 32-bit values.  keys/vals are sorted in place (ping-pong buffers
-// come from `arena` and are released on return).
-void radix_sort_u64(uint64_t* keys, uint32_t* vals, int64_t n, int key_bits, Arena& arena,
-                    hipStream_t s);
+// optional 32-bit values, ping-ponging between two caller buffers: the input
+// is keys[cur] (vals[cur]); on return cur names the buffer holding the
+// result.  An internal inconsistency sets bit `bad_bit` of *bad (device
+// memory); the caller reads it at its next synchronisation.
+struct SortBuffers {
+    uint64_t* keys[2];
+    uint32_t* vals[2];  // both null when no values are carried
+    int cur;
+};
+void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
+                    int bad_bit);
 
 }  // namespace taurus

@@ -1,35 +1,39 @@
 // One GNN layer as source-centric broadcast (Taurus, Sec. 3.1-3.6).
 //
 // Per graph and chunk size (the chunk index, shared by exact layers):
-//   - all propagated in-edges (u, v) plus one self item (v, v) per vertex,
-//     stably sorted by (chunk of the source, v).  In chunk j the messages to
-//     one destination are then one contiguous segment, sources ascending and
-//     the self item last;
+//   - the propagated in-edges (u, v), stably sorted by (chunk of the source,
+//     v): in chunk j the messages to one destination form one contiguous
+//     segment, sources ascending;
 //   - each vertex's arrival count |M(v)| + 1: every propagated in-edge and
 //     the self message count once (Sec. 3.4: O(|V|) pending counts; a vertex
 //     completes when its count reaches zero);
-//   - degree-bucketed work units: a segment of at most SHORT_LEN messages is
-//     one short unit (handled by a row-group of lanes); a longer one is cut
-//     into pieces of at most PIECE_LEN messages (each handled by a whole
-//     wave); a segment cut into several pieces (a hub) is completed by the
-//     fix-up pass, which sums the pieces' partial rows in a fixed order.
+//   - degree-bucketed work units: segments of 1, 2, 3-4 and 5-8 messages form
+//     four short classes, each reduced by a row-group of lanes with a loop of
+//     fixed length; longer segments are cut into pieces of at most PIECE_LEN
+//     messages, each reduced by a whole wave; a segment cut into several
+//     pieces (a hub) is completed by the fix-up pass, which sums the pieces'
+//     partial rows in a fixed order.
 // Per chunk (taurus_push_chunk):
 //   1. transform: Y = X_c W on the matrix cores (GCN rows scaled by
 //      d^_out(u)^-1/2; GraphSAGE Y = [X_c W_agg^T | X_c W_self^T]);
-//   2. scatter: per unit, the sum of its source rows scaled once by
+//   2. self pass: every vertex of the chunk adds its self row (the vertex's
+//      own message: the W_self half for GraphSAGE, its normalised row for
+//      GCN) to its accumulator -- a streaming pass over consecutive rows;
+//   3. scatter: per unit, the sum of its source rows scaled once by
 //      1/|M(v)| (the per-message normalisation of Sec. 3.4 applied to the
-//      segment sum) plus the self row, added to v's fp32 accumulator; the
-//      pending count drops by the segment length;
-//   3. finalise in place: the flush that brings pending[v] to zero writes
+//      segment sum) is added to v's fp32 accumulator; the pending count
+//      drops by the segment length;
+//   4. finalise in place: the flush that brings pending[v] to zero writes
 //      out[v] = act(phi_v * acc[v] + b) directly (GCN phi_v = d^_in(v)^-1/2,
 //      GraphSAGE phi_v = 1), the graduation step of Sec. 3.6;
-//   4. fix-up: hub segments sum their pieces and flush the same way.
+//   5. fix-up: hub segments sum their pieces and flush the same way.
 // A flush is the only writer of its destination within a kernel (segments
 // of one chunk are disjoint, kernels of one layer are stream ordered), so
 // accumulators are updated with plain loads and stores, no atomics.
 #include <algorithm>
 #include <chrono>
 #include <memory>
+#include <mutex>
 
 #include "internal.hpp"
 
@@ -42,18 +46,22 @@ void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const f
 void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& packed);
 const char* last_error_cstr();
 
-constexpr uint32_t SELF_BIT = 0x80000000u;
 constexpr int SC_THREADS = 256;
-constexpr int SHORT_LEN = 8;    // segments up to this many messages: one row-group
-constexpr int PIECE_LEN = 512;  // longer segments: pieces of this many messages, one wave each
+constexpr int NCLASS = 4;                           // short segment classes
+constexpr int PIECE_LEN = 512;                      // longer segments: pieces of this many messages
+constexpr int NOT_FIRST = 1 << 30;                  // unit.y flag (see k_seg_emit)
+constexpr int LEN_MASK = NOT_FIRST - 1;
+constexpr int NLIST = NCLASS + 2;                   // short classes, wave units, fix-up entries
+
+// longest segment of short class c: 1, 2, 4, 8
+__host__ __device__ constexpr int class_len(int c) { return 1 << c; }
 
 // ------------------------------------------------------------ init kernels --
 
-// pending and expected arrival counts: the number of index items of v,
-// i.e. |M(v)| propagated messages + 1 self message
-__global__ void k_init_counts(const int32_t* __restrict__ items, int64_t n, int2* __restrict__ cnt) {
+// pending and expected arrival counts: |M(v)| propagated messages + 1 self
+__global__ void k_init_counts(const int32_t* __restrict__ m, int64_t n, int2* __restrict__ cnt) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (v < n) cnt[v] = make_int2(items[v], items[v]);
+    if (v < n) cnt[v] = make_int2(m[v] + 1, m[v] + 1);
 }
 
 // GCN source factor d^_out(u)^-1/2 with d^_out = out-degree + 1
@@ -77,32 +85,26 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 
 // Chunk-index items.  CSR edge i (source u = the row containing i) becomes
 // key (chunk(u) << vbits | v), value u - chunk(u)*C; a dropped edge gets
-// chunk = nchunks so it sorts after every kept item.  Vertex v's self item
-// is (chunk(v) << vbits | v, (v - chunk(v)*C) | SELF_BIT).
+// chunk = nchunks so it sorts after every kept item.
 __global__ void k_make_items(const int64_t* __restrict__ row_off, const int32_t* __restrict__ col_dst,
                              int64_t e, int64_t n, int64_t C, int64_t nchunks, int vbits,
                              const uint64_t* __restrict__ mask, uint64_t* __restrict__ keys,
                              uint32_t* __restrict__ vals, int* __restrict__ bad) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < e) {
-        int64_t lo = 0, hi = n;  // largest u with row_off[u] <= i
-        while (hi - lo > 1) {
-            const int64_t mid = (lo + hi) >> 1;
-            if (row_off[mid] <= i) lo = mid;
-            else hi = mid;
-        }
-        const int64_t u = lo, v = col_dst[i];
-        // rows strictly ascending, no self loops (a simple graph)
-        if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
-        const bool kept = !mask || ((mask[i >> 6] >> (i & 63)) & 1ull);
-        const int64_t ch = kept ? u / C : nchunks;
-        keys[i] = ((uint64_t)ch << vbits) | (uint64_t)v;
-        vals[i] = (uint32_t)(u - (u / C) * C);
-    } else if (i < e + n) {
-        const int64_t v = i - e, ch = v / C;
-        keys[i] = ((uint64_t)ch << vbits) | (uint64_t)v;
-        vals[i] = (uint32_t)(v - ch * C) | SELF_BIT;
+    if (i >= e) return;
+    int64_t lo = 0, hi = n;  // largest u with row_off[u] <= i
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (row_off[mid] <= i) lo = mid;
+        else hi = mid;
     }
+    const int64_t u = lo, v = col_dst[i];
+    // rows strictly ascending, no self loops (a simple graph)
+    if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
+    const bool kept = !mask || ((mask[i >> 6] >> (i & 63)) & 1ull);
+    const int64_t ch = kept ? u / C : nchunks;
+    keys[i] = ((uint64_t)ch << vbits) | (uint64_t)v;
+    vals[i] = (uint32_t)(u - (u / C) * C);
 }
 
 // offs[j] = first sorted position whose chunk field is >= j, j in [0, nchunks]
@@ -121,9 +123,11 @@ __global__ void k_chunk_bounds(const uint64_t* __restrict__ keys, int64_t total,
 }
 
 // head[i] = 1 where a new (chunk, destination) segment starts
-__global__ void k_seg_heads(const uint64_t* __restrict__ keys, int64_t total, int32_t* __restrict__ head) {
+// (items past *kept, the dropped edges, get 0)
+__global__ void k_seg_heads(const uint64_t* __restrict__ keys, int64_t n_items, const int64_t* __restrict__ kept,
+                            int32_t* __restrict__ head) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < total) head[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1 : 0;
+    if (i < n_items) head[i] = (i < *kept && (i == 0 || keys[i] != keys[i - 1])) ? 1 : 0;
 }
 
 // seg_start[s] = first item of segment s; seg_start[P] = total
@@ -134,67 +138,86 @@ __global__ void k_seg_starts(const int32_t* __restrict__ head, const int64_t* __
     if (i == 0) seg_start[seg_id[total]] = total;
 }
 
-// Per segment: add its length to the destination's item count, and count the
-// work units it becomes (short unit, wave pieces, fix-up entry).
+// work list of a segment: short class 0..NCLASS-1 by length, or NCLASS (wave pieces)
+__device__ inline int seg_class(int64_t len) {
+#pragma unroll
+    for (int c = 0; c < NCLASS; c++)
+        if (len <= class_len(c)) return c;
+    return NCLASS;
+}
+
+// Per segment: add its length to the destination's message count, note the
+// destination's first chunk, and count the entries it adds to each list
+// (cnt[list * P + s]; lists = short classes, wave units, fix-up entries).
 __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                               int vbits, int32_t* __restrict__ items_per_v, int32_t* __restrict__ n_short,
-                               int32_t* __restrict__ n_long, int32_t* __restrict__ n_fix) {
+                               int vbits, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
+                               int32_t* __restrict__ cnt) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
     const uint64_t v = keys[b] & (((uint64_t)1 << vbits) - 1);
-    atomicAdd(&items_per_v[v], (int)len);
-    const int pieces = len <= SHORT_LEN ? 0 : (int)((len + PIECE_LEN - 1) / PIECE_LEN);
-    n_short[s] = len <= SHORT_LEN ? 1 : 0;
-    n_long[s] = pieces;
-    n_fix[s] = pieces > 1 ? 1 : 0;
+    atomicAdd(&m[v], (int)len);
+    atomicMin(&first_chunk[v], (int)(keys[b] >> vbits));
+    const int cls = seg_class(len);
+    const int pieces = cls == NCLASS ? (int)((len + PIECE_LEN - 1) / PIECE_LEN) : 0;
+#pragma unroll
+    for (int c = 0; c < NCLASS; c++) cnt[(int64_t)c * P + s] = cls == c ? 1 : 0;
+    cnt[(int64_t)NCLASS * P + s] = pieces;
+    cnt[(int64_t)(NCLASS + 1) * P + s] = pieces > 1 ? 1 : 0;
 }
 
-// Write the work units.  unit = {first item relative to its chunk, length,
-// destination, slot}; slot = global wave-unit index for pieces of a hub
-// segment (their partial rows go to the carry buffer), else -1.  fix-up
-// entry = {destination, first wave-unit index, number of pieces, 0}.
+// Write the work units into one buffer holding the lists one after another;
+// off[l * P + s] = position of segment s's first entry of list l (an
+// exclusive scan of the per-list counts laid out list by list).  unit =
+// {first item relative to its chunk, length | NOT_FIRST, destination, slot}.
+// NOT_FIRST marks a segment that is not its destination's first in ascending
+// chunk order: when chunks are pushed in that order its accumulator row
+// already holds a partial sum, so the scatter may fetch the row together with
+// the counts (the pending count still decides whether the row is used).
+// slot = buffer position of a hub segment's piece (its partial row goes to
+// the carry buffer), else -1.  fix-up entry = {destination, position of the
+// first piece, pieces, 0}.
 __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                           int vbits, const int64_t* __restrict__ chunk_off, const int64_t* __restrict__ o_short,
-                           const int64_t* __restrict__ o_long, const int64_t* __restrict__ o_fix,
-                           int4* __restrict__ u_short, int4* __restrict__ u_long, int4* __restrict__ u_fix) {
+                           int vbits, const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
+                           const int64_t* __restrict__ off, int4* __restrict__ units) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
     const uint64_t key = keys[b];
     const int v = (int)(key & (((uint64_t)1 << vbits) - 1));
-    const int64_t rel = b - chunk_off[key >> vbits];
-    if (len <= SHORT_LEN) {
-        u_short[o_short[s]] = make_int4((int)rel, (int)len, v, -1);
+    const int chunk = (int)(key >> vbits);
+    const int64_t rel = b - chunk_off[chunk];
+    const int nf = chunk != first_chunk[v] ? NOT_FIRST : 0;
+    const int cls = seg_class(len);
+    if (cls < NCLASS) {
+        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)len | nf, v, 0);
         return;
     }
     const int pieces = (int)((len + PIECE_LEN - 1) / PIECE_LEN);
-    const int64_t first = o_long[s];
+    const int64_t first = off[(int64_t)NCLASS * P + s];
     for (int q = 0; q < pieces; q++) {
-        const int64_t off = (int64_t)q * PIECE_LEN;
-        const int plen = (int)min((int64_t)PIECE_LEN, len - off);
-        u_long[first + q] = make_int4((int)(rel + off), plen, v, pieces > 1 ? (int)(first + q) : -1);
+        const int64_t o = (int64_t)q * PIECE_LEN;
+        const int plen = (int)min((int64_t)PIECE_LEN, len - o);
+        units[first + q] = make_int4((int)(rel + o), plen | nf, v, pieces > 1 ? (int)(first + q) : -1);
     }
-    if (pieces > 1) u_fix[o_fix[s]] = make_int4(v, (int)first, pieces, 0);
+    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, 0);
 }
 
-__global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, uint32_t* __restrict__ src) {
+__global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, int32_t* __restrict__ src) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < total) src[i] = vals[i];
+    if (i < total) src[i] = (int32_t)vals[i];
 }
 
-// per-chunk starts of the three unit lists: values of the scans at each
-// chunk's first segment (chunk_off[nchunks] = total maps to segment P)
+// per-chunk starts of every list: the scan at each chunk's first segment
+// (chunk_off[nchunks] = total maps to segment P, i.e. the end of each list)
 __global__ void k_chunk_unit_bases(const int64_t* __restrict__ chunk_off, int64_t nchunks,
-                                   const int64_t* __restrict__ seg_id, const int64_t* __restrict__ o_short,
-                                   const int64_t* __restrict__ o_long, const int64_t* __restrict__ o_fix,
+                                   const int64_t* __restrict__ seg_id, const int64_t* __restrict__ off, int64_t P,
                                    int64_t* __restrict__ bases) {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (k > nchunks) return;
     const int64_t s = seg_id[chunk_off[k]];
-    bases[k * 3 + 0] = o_short[s];
-    bases[k * 3 + 1] = o_long[s];
-    bases[k * 3 + 2] = o_fix[s];
+#pragma unroll
+    for (int l = 0; l < NLIST; l++) bases[k * NLIST + l] = off[(int64_t)l * P + s];
 }
 
 __global__ __launch_bounds__(256) void k_count_pending(const int2* __restrict__ cnt, int64_t n,
@@ -215,7 +238,7 @@ struct ScatterParams {
     const float* Y;        // chunk transform, row stride ystride floats
     int64_t ystride;
     int self_col;          // column offset of the self half (GraphSAGE) or 0 (GCN)
-    const uint32_t* src;   // chunk items: local source row | SELF_BIT
+    const int32_t* src;    // chunk items: local source row
     int2* cnt;             // {pending, expected}
     float* acc;            // [n][d_o] fp32 accumulators
     int d_o;
@@ -227,6 +250,13 @@ struct ScatterParams {
     float* carry;          // per hub piece of the chunk: [d_o] partial contribution
     int32_t* carry_cnt;    // per hub piece: message count
     int64_t long_base;     // global index of the chunk's first wave unit (carry slot 0)
+    int64_t first_row;     // first vertex of the chunk
+    int64_t rows;          // vertices in the chunk
+};
+
+struct ChunkUnits {        // this chunk's slice of the short classes and wave units
+    const int4* u[NCLASS + 1];
+    int64_t n[NCLASS + 1];
 };
 
 __device__ inline float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
@@ -234,6 +264,7 @@ __device__ inline float4 f4_add(float4 a, float4 b) { return make_float4(a.x + b
 __device__ inline float4 f4_axpy(float s, float4 a, float4 b) {
     return make_float4(fmaf(s, a.x, b.x), fmaf(s, a.y, b.y), fmaf(s, a.z, b.z), fmaf(s, a.w, b.w));
 }
+__device__ inline float4 f4_scale(float s, float4 a) { return make_float4(s * a.x, s * a.y, s * a.z, s * a.w); }
 
 __device__ inline uint32_t f32_to_bf16_bits(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -267,22 +298,30 @@ __device__ inline float seg_scale(int agg, int expect) {
 }
 
 // Sole-owner flush of contribution c (already scaled) carrying `count`
-// messages to v.  pe = {pending, expected} as read before the flush.
+// messages to v.  pe = {pending, expected} as read before the flush.  pre
+// holds v's accumulator row if it was fetched early (have_pre).
 template <int G, int VEC>
 __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const float4 (&c)[VEC], int count,
-                                   int lane) {
+                                   int lane, const float4 (&pre)[VEC], bool have_pre) {
     const int left = pe.x - count;
     const bool fresh = pe.x == pe.y;  // nothing accumulated yet: acc[v] is logically zero
     float* arow = p.acc + (int64_t)v * p.d_o;
+    float4 t[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; j++) {
+        const int col = (j * G + lane) * 4;
+        t[j] = c[j];
+        if (!fresh && col < p.d_o)
+            t[j] = f4_add(have_pre ? pre[j] : *reinterpret_cast<const float4*>(arow + col), c[j]);
+    }
     if (left == 0) {
         const float phi = p.agg == 1 ? 1.0f / sqrtf((float)pe.y) : 1.0f;
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
             const int col = (j * G + lane) * 4;
             if (col < p.d_o) {
-                float4 t = fresh ? c[j] : f4_add(*reinterpret_cast<const float4*>(arow + col), c[j]);
                 const float4 b = *reinterpret_cast<const float4*>(p.bias + col);
-                float4 z = f4_axpy(phi, t, b);
+                float4 z = f4_axpy(phi, t[j], b);
                 if (p.relu) {
                     z.x = fmaxf(z.x, 0.f); z.y = fmaxf(z.y, 0.f);
                     z.z = fmaxf(z.z, 0.f); z.w = fmaxf(z.w, 0.f);
@@ -294,117 +333,176 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
             const int col = (j * G + lane) * 4;
-            if (col < p.d_o) {
-                float4 t = fresh ? c[j] : f4_add(*reinterpret_cast<const float4*>(arow + col), c[j]);
-                *reinterpret_cast<float4*>(arow + col) = t;
-            }
+            if (col < p.d_o) *reinterpret_cast<float4*>(arow + col) = t[j];
         }
     }
     if (lane == 0) p.cnt[v].x = left;
 }
 
-// Add the source rows of items first, first + step, ... (fewer than len) of
-// the chunk into sa (neighbour messages) and ss (the self message), with B
-// row loads in flight at a time.
-template <int G, int VEC, int B>
-__device__ inline void gather_rows(const ScatterParams& p, int first, int len, int step, int lane,
-                                   float4 (&sa)[VEC], float4 (&ss)[VEC]) {
-    for (int i0 = 0; i0 < len; i0 += B * step) {
-        float4 rows[B][VEC];
-        bool self[B];
+template <int G, int VEC>
+__device__ inline void prefetch_acc(const ScatterParams& p, int v, int lane, float4 (&pre)[VEC]) {
 #pragma unroll
-        for (int u = 0; u < B; u++) {
-            const int i = i0 + u * step;
-            self[u] = false;
-#pragma unroll
-            for (int j = 0; j < VEC; j++) rows[u][j] = f4_zero();
-            if (i < len) {
-                const uint32_t code = p.src[first + i];
-                self[u] = (code & SELF_BIT) != 0;
-                const float* row = p.Y + (int64_t)(code & ~SELF_BIT) * p.ystride + (self[u] ? p.self_col : 0);
-#pragma unroll
-                for (int j = 0; j < VEC; j++) {
-                    const int col = (j * G + lane) * 4;
-                    if (col < p.d_o) rows[u][j] = *reinterpret_cast<const float4*>(row + col);
-                }
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < B; u++)
-#pragma unroll
-            for (int j = 0; j < VEC; j++) {
-                if (self[u]) ss[j] = f4_add(ss[j], rows[u][j]);
-                else sa[j] = f4_add(sa[j], rows[u][j]);
-            }
+    for (int j = 0; j < VEC; j++) {
+        const int col = (j * G + lane) * 4;
+        pre[j] = col < p.d_o ? *reinterpret_cast<const float4*>(p.acc + (int64_t)v * p.d_o + col) : f4_zero();
     }
 }
 
-// Degree-bucketed scatter of one chunk.  Blocks [0, short_blocks) take short
-// units, one per row-group of G lanes (SC_THREADS / G units per block); the
-// remaining blocks take wave units, one per wave (4 per block): the wave's
-// 64/G row-groups split the piece's items, reduce across row-groups with
-// cross-lane shuffles, and row-group 0 flushes (or parks the partial row of
-// a hub piece in its carry slot).
+// Self pass: every vertex of the chunk receives its own message, the self
+// row of Y (one arrival), in vertex order -- consecutive rows of Y and of
+// the accumulators.
 template <int G, int VEC>
-__global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p, const int4* __restrict__ u_short,
-                                                        int64_t n_short, int64_t short_blocks,
-                                                        const int4* __restrict__ u_long, int64_t n_long) {
+__global__ __launch_bounds__(SC_THREADS) void k_self(ScatterParams p) {
     constexpr int NRG = SC_THREADS / G;
-    constexpr int R = 64 / G;
-    constexpr int B = 8 / VEC;
-    if ((int64_t)blockIdx.x < short_blocks) {
-        const int rg = threadIdx.x / G, lane = threadIdx.x % G;
-        const int64_t ui = (int64_t)blockIdx.x * NRG + rg;
-        if (ui >= n_short) return;
-        const int4 w = u_short[ui];
-        const int2 pe = p.cnt[w.z];
-        float4 sa[VEC], ss[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
-        gather_rows<G, VEC, B>(p, w.x, w.y, 1, lane, sa, ss);
-        const float sig = seg_scale(p.agg, pe.y);
-        float4 c[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = f4_axpy(sig, sa[j], ss[j]);
-        flush_owner<G, VEC>(p, w.z, pe, c, w.y, lane);
-        return;
-    }
-    const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
-    const int rg = l64 / G, lane = l64 % G;
-    const int64_t ui = ((int64_t)blockIdx.x - short_blocks) * (SC_THREADS / 64) + wave;
-    if (ui >= n_long) return;
-    const int4 w = u_long[ui];
-    const int2 pe = p.cnt[w.z];
-    float4 sa[VEC], ss[VEC];
-#pragma unroll
-    for (int j = 0; j < VEC; j++) sa[j] = ss[j] = f4_zero();
-    gather_rows<G, VEC, B>(p, w.x + rg, w.y - rg, R, lane, sa, ss);
-#pragma unroll
-    for (int d = G; d < 64; d <<= 1)
-#pragma unroll
-        for (int j = 0; j < VEC; j++) {
-            sa[j].x += __shfl_xor(sa[j].x, d, 64); sa[j].y += __shfl_xor(sa[j].y, d, 64);
-            sa[j].z += __shfl_xor(sa[j].z, d, 64); sa[j].w += __shfl_xor(sa[j].w, d, 64);
-            ss[j].x += __shfl_xor(ss[j].x, d, 64); ss[j].y += __shfl_xor(ss[j].y, d, 64);
-            ss[j].z += __shfl_xor(ss[j].z, d, 64); ss[j].w += __shfl_xor(ss[j].w, d, 64);
-        }
-    if (rg != 0) return;
-    const float sig = seg_scale(p.agg, pe.y);
-    float4 c[VEC];
-#pragma unroll
-    for (int j = 0; j < VEC; j++) c[j] = f4_axpy(sig, sa[j], ss[j]);
-    if (w.w < 0) {
-        flush_owner<G, VEC>(p, w.z, pe, c, w.y, lane);
-    } else {
-        const int64_t slot = (int64_t)w.w - p.long_base;
-        float* crow = p.carry + slot * p.d_o;
+    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t stride = (int64_t)gridDim.x * NRG;
+    for (int64_t r = (int64_t)blockIdx.x * NRG + rg; r < p.rows; r += stride) {
+        const int v = (int)(p.first_row + r);
+        const int2 pe = p.cnt[v];
+        const float* row = p.Y + r * p.ystride + p.self_col;
+        float4 c[VEC], pre[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
             const int col = (j * G + lane) * 4;
-            if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+            c[j] = col < p.d_o ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+            pre[j] = f4_zero();
         }
-        if (lane == 0) p.carry_cnt[slot] = w.y;
+        flush_owner<G, VEC>(p, v, pe, c, 1, lane, pre, false);
     }
+}
+
+// Short class of segments of at most LEN messages: each row-group walks the
+// class's units (grid stride); a unit's source codes, counts and (SPEC)
+// accumulator row are requested together, then its rows; the next unit is
+// fetched while this one is processed.
+template <int G, int VEC, bool SPEC, int LEN>
+__device__ inline void short_class(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
+    constexpr int NRG = SC_THREADS / G;
+    constexpr int B = LEN * VEC <= 16 ? LEN : 16 / VEC;  // rows in flight per batch
+    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t stride = (int64_t)gridDim.x * NRG;
+    int64_t ui = (int64_t)blockIdx.x * NRG + rg;
+    int4 w = ui < n ? units[ui] : make_int4(0, 0, 0, 0);
+    while (ui < n) {
+        const int64_t un = ui + stride;
+        const int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
+        const int v = w.z, len = w.y & LEN_MASK;
+        const int2 pe = p.cnt[v];
+        int32_t code[LEN];
+#pragma unroll
+        for (int i = 0; i < LEN; i++) code[i] = (LEN == 1 || i < len) ? p.src[w.x + i] : 0;
+        float4 pre[VEC];
+        const bool have_pre = SPEC && (w.y & NOT_FIRST);
+        if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
+        float4 sa[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
+#pragma unroll
+        for (int i0 = 0; i0 < LEN; i0 += B) {
+            float4 rows[B][VEC];
+#pragma unroll
+            for (int u = 0; u < B; u++) {
+                const int i = i0 + u;
+                const float* row = p.Y + (int64_t)code[i] * p.ystride;
+#pragma unroll
+                for (int j = 0; j < VEC; j++) {
+                    const int col = (j * G + lane) * 4;
+                    rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < B; u++)
+#pragma unroll
+                for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
+        }
+        const float sig = seg_scale(p.agg, pe.y);
+        float4 c[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
+        flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
+        ui = un;
+        w = wn;
+    }
+}
+
+// Wave units (pieces of segments longer than the short classes): one per
+// wave; the wave's 64/G row-groups split the piece's rows, reduce across
+// row-groups with cross-lane shuffles, and row-group 0 flushes (or parks the
+// partial row of a hub piece in its carry slot).
+template <int G, int VEC, bool SPEC>
+__device__ inline void wave_units(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
+    constexpr int R = 64 / G;
+    constexpr int B = 16 / VEC;
+    const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
+    const int rg = l64 / G, lane = l64 % G;
+    const int64_t wstride = (int64_t)gridDim.x * (SC_THREADS / 64);
+    for (int64_t ui = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave; ui < n; ui += wstride) {
+        const int4 w = units[ui];
+        const int v = w.z, len = w.y & LEN_MASK;
+        const int2 pe = p.cnt[v];
+        float4 pre[VEC];
+        const bool have_pre = SPEC && (w.y & NOT_FIRST) && w.w < 0 && rg == 0;
+        if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
+        float4 sa[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
+        for (int i0 = rg; i0 < len; i0 += B * R) {
+            float4 rows[B][VEC];
+#pragma unroll
+            for (int u = 0; u < B; u++) {
+                const int i = i0 + u * R;
+                const int64_t code = i < len ? p.src[w.x + i] : 0;
+                const float* row = p.Y + code * p.ystride;
+#pragma unroll
+                for (int j = 0; j < VEC; j++) {
+                    const int col = (j * G + lane) * 4;
+                    rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < B; u++)
+#pragma unroll
+                for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
+        }
+#pragma unroll
+        for (int d = G; d < 64; d <<= 1)
+#pragma unroll
+            for (int j = 0; j < VEC; j++) {
+                sa[j].x += __shfl_xor(sa[j].x, d, 64);
+                sa[j].y += __shfl_xor(sa[j].y, d, 64);
+                sa[j].z += __shfl_xor(sa[j].z, d, 64);
+                sa[j].w += __shfl_xor(sa[j].w, d, 64);
+            }
+        if (rg != 0) continue;
+        const float sig = seg_scale(p.agg, pe.y);
+        float4 c[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
+        if (w.w < 0) {
+            flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
+        } else {
+            const int64_t slot = (int64_t)w.w - p.long_base;
+            float* crow = p.carry + slot * p.d_o;
+#pragma unroll
+            for (int j = 0; j < VEC; j++) {
+                const int col = (j * G + lane) * 4;
+                if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+            }
+            if (lane == 0) p.carry_cnt[slot] = len;
+        }
+    }
+}
+
+// Degree-bucketed scatter of one chunk, persistent: the grid is sized to
+// what the GPU holds at once and walks the short classes, then the wave
+// units.
+template <int G, int VEC, bool SPEC>
+__global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p, ChunkUnits cu) {
+    short_class<G, VEC, SPEC, 1>(p, cu.u[0], cu.n[0]);
+    short_class<G, VEC, SPEC, 2>(p, cu.u[1], cu.n[1]);
+    short_class<G, VEC, SPEC, 4>(p, cu.u[2], cu.n[2]);
+    short_class<G, VEC, SPEC, 8>(p, cu.u[3], cu.n[3]);
+    wave_units<G, VEC, SPEC>(p, cu.u[NCLASS], cu.n[NCLASS]);
 }
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
@@ -418,9 +516,9 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
     const int4 f = fix[idx];
     const int v = f.x;
     const int64_t first = (int64_t)f.y - p.long_base;
-    float4 c[VEC];
+    float4 c[VEC], pre[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; j++) c[j] = f4_zero();
+    for (int j = 0; j < VEC; j++) c[j] = pre[j] = f4_zero();
     int count = 0;
     for (int q = 0; q < f.z; q++) {
         const float* crow = p.carry + (first + q) * p.d_o;
@@ -431,91 +529,147 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
         }
         count += p.carry_cnt[first + q];
     }
-    flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane);
+    flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane, pre, false);
 }
 
-template <int G, int VEC>
-static void launch_scatter(const ScatterParams& p, const int4* us, int64_t ns, const int4* ul, int64_t nl,
-                           hipStream_t s) {
-    constexpr int NRG = SC_THREADS / G;
-    const int64_t sb = ceil_div(ns, NRG), lb = ceil_div(nl, SC_THREADS / 64);
-    k_scatter<G, VEC><<<(unsigned)(sb + lb), SC_THREADS, 0, s>>>(p, us, ns, sb, ul, nl);
-}
-template <int G, int VEC>
-static void launch_fixup(const ScatterParams& p, const int4* fix, int64_t nfix, hipStream_t s) {
-    constexpr int NRG = SC_THREADS / G;
-    k_fixup<G, VEC><<<(unsigned)ceil_div(nfix, NRG), SC_THREADS, 0, s>>>(p, fix, nfix);
+// ------------------------------------------------------------- dispatch ---
+
+// Scatter configuration: G lanes per row-group with VEC float4 per lane,
+// SPEC early accumulator fetch, and the persistent grid sizes.
+struct ScatterShape {
+    int G, VEC, SPEC;
+    int64_t max_blocks;
+};
+
+static int env_int(const char* name, int dflt) {
+    const char* v = getenv(name);
+    return v && *v ? atoi(v) : dflt;
 }
 
-// lanes per row-group: one float4 per lane up to 64 lanes, then VEC float4s
-static void row_group_shape(int d_o, int* G, int* VEC) {
+template <int G, int VEC, bool SPEC>
+static int64_t resident_blocks() {
+    int dev = 0, cus = 0, per_cu = 0;
+    TAURUS_HIP(hipGetDevice(&dev));
+    TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    TAURUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_scatter<G, VEC, SPEC>, SC_THREADS, 0));
+    return (int64_t)std::max(1, cus) * std::max(1, per_cu);
+}
+
+// Row-group shape for an output width: aim for `vec_target` float4 per lane
+// (fewer lanes per destination, more destinations per wave), at least 4 and
+// at most 64 lanes.
+static ScatterShape scatter_shape(int d_o) {
+    const int vec_target = env_int("TAURUS_SCATTER_VEC", 2);
     const int q = (d_o + 3) / 4;
     int g = 4;
-    while (g < q && g < 64) g <<= 1;
+    while (g < 64 && g * vec_target < q) g <<= 1;
     int vec = (q + g - 1) / g;
     if (vec == 3) vec = 4;
-    *G = g;
-    *VEC = vec;
+    if (vec > 4) {
+        g = 64;
+        vec = (q + 63) / 64;
+        if (vec == 3) vec = 4;
+    }
+    ScatterShape sh;
+    sh.G = g;
+    sh.VEC = vec;
+    sh.SPEC = env_int("TAURUS_SCATTER_SPEC", 0) ? 1 : 0;
+    sh.max_blocks = 0;
+    return sh;
 }
 
-#define TAURUS_ROW_SHAPES(X) X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(64, 2) X(64, 4)
+#define TAURUS_ROW_SHAPES(X) \
+    X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(4, 2) X(8, 2) X(16, 2) X(32, 2) X(64, 2) \
+    X(4, 4) X(8, 4) X(16, 4) X(32, 4) X(64, 4)
 
-static void dispatch_scatter(int G, int VEC, const ScatterParams& p, const int4* us, int64_t ns, const int4* ul,
-                             int64_t nl, hipStream_t s) {
-#define TAURUS_CASE(g, v)                              \
-    if (G == g && VEC == v) {                          \
-        launch_scatter<g, v>(p, us, ns, ul, nl, s);    \
-        TAURUS_CHECK_LAUNCH();                         \
-        return;                                        \
+static void dispatch_self(const ScatterShape& sh, const ScatterParams& p, hipStream_t s) {
+#define TAURUS_CASE(g, v)                                                                  \
+    if (sh.G == g && sh.VEC == v) {                                                        \
+        const int64_t want = ceil_div(p.rows, SC_THREADS / g);                             \
+        const int64_t blocks = std::max<int64_t>(1, std::min(want, sh.max_blocks));        \
+        k_self<g, v><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p);                           \
+        TAURUS_CHECK_LAUNCH();                                                             \
+        return;                                                                            \
     }
     TAURUS_ROW_SHAPES(TAURUS_CASE)
 #undef TAURUS_CASE
-    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
 }
-static void dispatch_fixup(int G, int VEC, const ScatterParams& p, const int4* fix, int64_t nfix, hipStream_t s) {
-#define TAURUS_CASE(g, v)                              \
-    if (G == g && VEC == v) {                          \
-        launch_fixup<g, v>(p, fix, nfix, s);           \
-        TAURUS_CHECK_LAUNCH();                         \
-        return;                                        \
+
+static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, const ChunkUnits& cu, hipStream_t s) {
+    int64_t want = ceil_div(cu.n[NCLASS], SC_THREADS / 64);
+    for (int c = 0; c < NCLASS; c++) want = std::max(want, ceil_div(cu.n[c], SC_THREADS / sh.G));
+    const int64_t blocks = std::max<int64_t>(1, std::min(want, sh.max_blocks));
+#define TAURUS_CASE(g, v)                                                                  \
+    if (sh.G == g && sh.VEC == v) {                                                        \
+        if (sh.SPEC) k_scatter<g, v, true><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu); \
+        else k_scatter<g, v, false><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu);        \
+        TAURUS_CHECK_LAUNCH();                                                             \
+        return;                                                                            \
     }
     TAURUS_ROW_SHAPES(TAURUS_CASE)
 #undef TAURUS_CASE
-    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", G, VEC);
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
 }
 
-}  // namespace taurus
+static int64_t scatter_resident_blocks(const ScatterShape& sh) {
+#define TAURUS_CASE(g, v)                                                                  \
+    if (sh.G == g && sh.VEC == v)                                                          \
+        return sh.SPEC ? resident_blocks<g, v, true>() : resident_blocks<g, v, false>();
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
+}
 
+static void dispatch_fixup(const ScatterShape& sh, const ScatterParams& p, const int4* fix, int64_t nfix,
+                           hipStream_t s) {
+#define TAURUS_CASE(g, v)                                                                         \
+    if (sh.G == g && sh.VEC == v) {                                                               \
+        k_fixup<g, v><<<(unsigned)ceil_div(nfix, SC_THREADS / g), SC_THREADS, 0, s>>>(p, fix, nfix); \
+        TAURUS_CHECK_LAUNCH();                                                                    \
+        return;                                                                                   \
+    }
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
+}
 
 // ------------------------------------------------------------- chunk index --
 
-namespace taurus {
-
 // The structures a layer streams over, fixed by (graph, chunk size, edge
-// mask): the item sources grouped by (chunk, destination), per-vertex item
-// counts (|M(v)| + 1), and per chunk the short units, the wave units and the
-// fix-up entries of hub segments.  Exact layers over one graph and chunk
-// size share one index.
+// mask): the item sources grouped by (chunk, destination), per-vertex
+// message counts |M(v)|, and per chunk the slices of the work lists.
+// Exact layers over one graph and chunk size share one index.
 struct ChunkIndex {
     Arena arena;
     taurus_graph g{};
-    int64_t C = 0, nchunks = 0, kept = 0, pairs = 0;
-    int64_t n_short = 0, n_long = 0, n_fix = 0, max_long_per_chunk = 0;
+    int64_t C = 0, nchunks = 0, kept = 0, segments = 0, max_long_per_chunk = 0;
+    int64_t n_list[NLIST] = {0, 0, 0, 0, 0, 0};
     bool sampled = false;
-    int32_t* items_per_v = nullptr;
-    uint32_t* item_src = nullptr;
-    int4* u_short = nullptr;
-    int4* u_long = nullptr;
-    int4* u_fix = nullptr;
-    std::vector<int64_t> chunk_off, short_off, long_off, fix_off;
+    hipStream_t built_on = nullptr;
+    hipEvent_t ready = nullptr;    // recorded after the last kernel that writes the index
+    int32_t* m = nullptr;          // |M(v)|
+    int32_t* item_src = nullptr;   // local source row per item
+    int4* units = nullptr;         // the work lists, one after another
+    std::vector<int64_t> chunk_off;              // items before each chunk
+    std::vector<int64_t> list_off[NLIST];        // buffer position of each chunk's first entry of list l
     double ms_build = 0;
-    ChunkIndex(hipStream_t s, int64_t budget) : arena(s, budget) {}
-    // The index may outlive the stream it was built on: wait for the device,
-    // then return the memory on the null stream.
+    ChunkIndex(hipStream_t s, int64_t budget) : arena(s, budget), built_on(s) {}
+    // The index may outlive the stream it was built on and be read from other
+    // streams: wait for the device, then return the memory on the null stream.
     ~ChunkIndex() {
         (void)hipDeviceSynchronize();
+        if (ready) (void)hipEventDestroy(ready);
         arena.set_stream(nullptr);
         arena.release();
+    }
+    const int4* list_at(int l, int64_t k) const { return units + list_off[l][(size_t)k]; }
+    int64_t list_count(int l, int64_t k) const {
+        return list_off[l][(size_t)k + 1] - list_off[l][(size_t)k];
+    }
+    // make stream s wait until the index is complete
+    void wait_ready(hipStream_t s) const {
+        if (ready && s != built_on) TAURUS_HIP(hipStreamWaitEvent(s, ready, 0));
     }
 };
 
@@ -524,6 +678,10 @@ static void check_graph_args(const taurus_graph* g) {
     if (g->n <= 0 || g->n >= ((int64_t)1 << 31) || g->e < 0)
         fail(TAURUS_E_INVALID, "graph size n=%lld e=%lld out of range", (long long)g->n, (long long)g->e);
     if (!g->row_off || (g->e > 0 && !g->col_dst)) fail(TAURUS_E_INVALID, "graph arrays are null");
+}
+
+static double ms_since(std::chrono::steady_clock::time_point t0) {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
 
 static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C, const uint64_t* mask,
@@ -538,103 +696,111 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     const int T = 256;
     const int64_t nch = idx->nchunks;
     Arena tmp(s);
+    auto finish = [&]() {
+        TAURUS_HIP(hipEventCreateWithFlags(&idx->ready, hipEventDisableTiming));
+        TAURUS_HIP(hipEventRecord(idx->ready, s));
+        idx->ms_build = ms_since(t_start);
+    };
 
-    // the caller's graph must be a valid simple CSR before anything indexes with it
+    idx->m = idx->arena.alloc<int32_t>(n, "message counts");
+    fill_i32(idx->m, n, 0, s);
+    idx->chunk_off.assign((size_t)nch + 1, 0);
+    for (int l = 0; l < NLIST; l++) idx->list_off[l].assign((size_t)nch + 1, 0);
+    // flags: 1, 2 invalid CSR; 4 unsorted row or self loop; 8 sort inconsistency
     int* bad = tmp.alloc<int>(1, "graph flag");
-    TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));
+    fill_i32(bad, 1, 0, s);
     k_validate_graph<<<(unsigned)ceil_div(std::max(n, e), T), T, 0, s>>>(g.row_off, g.col_dst, n, e, bad);
     TAURUS_CHECK_LAUNCH();
     int hbad = 0;
-    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
+    if (e == 0) {  // no messages: the self passes do all the work
+        Readback rb;
+        rb.add(&hbad, bad, 1);
+        rb.run(s);
+        if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
+        finish();
+        return idx;
+    }
 
-    // items sorted by (source chunk, destination), stably
+    // Items sorted by (source chunk, destination), stably.  Everything up to
+    // the readback below is memory safe on an invalid graph (indices come
+    // from binary searches and thread ids only); the flags are checked before
+    // any kernel indexes by destination.
     const int vbits = std::max(1, bits_for(n - 1));
     const int cbits = bits_for(nch);
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
-    const int64_t total = e + n;
-    uint64_t* keys = tmp.alloc<uint64_t>(total, "index keys");
-    uint32_t* vals = tmp.alloc<uint32_t>(total, "index values");
-    k_make_items<<<(unsigned)ceil_div(total, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, nch, vbits, mask, keys,
-                                                            vals, bad);
+    SortBuffers sb{{tmp.alloc<uint64_t>(e, "index keys"), tmp.alloc<uint64_t>(e, "index keys (ping-pong)")},
+                   {tmp.alloc<uint32_t>(e, "index values"), tmp.alloc<uint32_t>(e, "index values (ping-pong)")},
+                   0};
+    k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, nch, vbits, mask,
+                                                        sb.keys[0], sb.vals[0], bad);
     TAURUS_CHECK_LAUNCH();
-    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    if (hbad) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
-    radix_sort_u64(keys, vals, total, vbits + cbits, tmp, s);
-
+    radix_sort_u64(sb, e, vbits + cbits, tmp, s, bad, 8);
+    const uint64_t* keys = sb.keys[sb.cur];
+    const uint32_t* vals = sb.vals[sb.cur];
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
-    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, total, nch, vbits, doffs);
+    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, e, nch, vbits, doffs);
     TAURUS_CHECK_LAUNCH();
-    idx->chunk_off.resize((size_t)nch + 1);
-    TAURUS_HIP(hipMemcpyAsync(idx->chunk_off.data(), doffs, (size_t)(nch + 1) * 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    const int64_t kept_total = idx->chunk_off[(size_t)nch];
-    idx->kept = kept_total - n;
-
-    // segments: heads, ids, starts
-    int32_t* head = tmp.alloc<int32_t>(kept_total, "segment heads");
-    int64_t* seg_id = tmp.alloc<int64_t>(kept_total + 1, "segment ids");
-    k_seg_heads<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(keys, kept_total, head);
+    int32_t* head = tmp.alloc<int32_t>(e, "segment heads");
+    int64_t* seg_id = tmp.alloc<int64_t>(e + 1, "segment ids");
+    k_seg_heads<<<(unsigned)ceil_div(e, T), T, 0, s>>>(keys, e, doffs + nch, head);
     TAURUS_CHECK_LAUNCH();
-    scan_i32_to_i64(head, seg_id, kept_total, true, tmp, s);
+    scan_i32_to_i64(head, seg_id, e, true, tmp, s);
     int64_t P = 0;
-    TAURUS_HIP(hipMemcpyAsync(&P, seg_id + kept_total, 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    idx->pairs = P;
-    int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
-    k_seg_starts<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(head, seg_id, kept_total, seg_start);
-    TAURUS_CHECK_LAUNCH();
-
-    // classify segments into work units
-    idx->items_per_v = idx->arena.alloc<int32_t>(n, "items per vertex");
-    TAURUS_HIP(hipMemsetAsync(idx->items_per_v, 0, (size_t)n * 4, s));
-    int32_t* c_short = tmp.alloc<int32_t>(P, "short counts");
-    int32_t* c_long = tmp.alloc<int32_t>(P, "wave counts");
-    int32_t* c_fix = tmp.alloc<int32_t>(P, "fix counts");
-    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, idx->items_per_v, c_short,
-                                                          c_long, c_fix);
-    TAURUS_CHECK_LAUNCH();
-    int64_t* o_short = tmp.alloc<int64_t>(P + 1, "short offsets");
-    int64_t* o_long = tmp.alloc<int64_t>(P + 1, "wave offsets");
-    int64_t* o_fix = tmp.alloc<int64_t>(P + 1, "fix offsets");
-    scan_i32_to_i64(c_short, o_short, P, true, tmp, s);
-    scan_i32_to_i64(c_long, o_long, P, true, tmp, s);
-    scan_i32_to_i64(c_fix, o_fix, P, true, tmp, s);
-    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * 3, "chunk unit bases");
-    k_chunk_unit_bases<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, o_short, o_long, o_fix,
-                                                                    dbases);
-    TAURUS_CHECK_LAUNCH();
-    std::vector<int64_t> bases((size_t)(nch + 1) * 3);
-    TAURUS_HIP(hipMemcpyAsync(bases.data(), dbases, bases.size() * 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    idx->short_off.resize((size_t)nch + 1);
-    idx->long_off.resize((size_t)nch + 1);
-    idx->fix_off.resize((size_t)nch + 1);
-    for (int64_t k = 0; k <= nch; k++) {
-        idx->short_off[k] = bases[k * 3 + 0];
-        idx->long_off[k] = bases[k * 3 + 1];
-        idx->fix_off[k] = bases[k * 3 + 2];
+    {
+        Readback rb;
+        rb.add(&hbad, bad, 1);
+        rb.add(idx->chunk_off.data(), doffs, nch + 1);
+        rb.add(&P, seg_id + e, 1);
+        rb.run(s);
     }
-    idx->n_short = idx->short_off[nch];
-    idx->n_long = idx->long_off[nch];
-    idx->n_fix = idx->fix_off[nch];
+    if (hbad & 3) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
+    if (hbad & 4) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
+    if (hbad & 8) fail(TAURUS_E_DEVICE, "chunk index: radix sort offset out of range");
+    const int64_t kept = idx->chunk_off[(size_t)nch];
+    idx->kept = kept;
+    idx->segments = P;
+    if (kept == 0) {
+        finish();
+        return idx;
+    }
+
+    // segments into the work lists
+    int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
+    k_seg_starts<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(head, seg_id, kept, seg_start);
+    TAURUS_CHECK_LAUNCH();
+    int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
+    fill_i32(first_chunk, n, 0x7fffffff, s);
+    int32_t* lcnt = tmp.alloc<int32_t>(P * NLIST, "list counts");
+    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, idx->m, first_chunk, lcnt);
+    TAURUS_CHECK_LAUNCH();
+    int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
+    scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
+    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list bases");
+    k_chunk_unit_bases<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, loff, P, dbases);
+    TAURUS_CHECK_LAUNCH();
+    std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);
+    int64_t total_units = 0;
+    {
+        Readback rb;
+        rb.add(bases.data(), dbases, (nch + 1) * NLIST);
+        rb.add(&total_units, loff + P * NLIST, 1);
+        rb.run(s);
+    }
+    for (int l = 0; l < NLIST; l++) {
+        for (int64_t k = 0; k <= nch; k++) idx->list_off[l][(size_t)k] = bases[(size_t)k * NLIST + l];
+        idx->n_list[l] = idx->list_off[l][(size_t)nch] - idx->list_off[l][0];
+    }
     for (int64_t k = 0; k < nch; k++)
-        idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->long_off[k + 1] - idx->long_off[k]);
-    if (idx->n_long >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many wave units");
-    idx->u_short = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_short), "short units");
-    idx->u_long = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_long), "wave units");
-    idx->u_fix = idx->arena.alloc<int4>(std::max<int64_t>(1, idx->n_fix), "fix-up entries");
-    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, doffs, o_short, o_long, o_fix,
-                                                      idx->u_short, idx->u_long, idx->u_fix);
+        idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->list_count(NCLASS, k));
+    if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
+    idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
+    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, doffs, first_chunk, loff,
+                                                      idx->units);
     TAURUS_CHECK_LAUNCH();
-    idx->item_src = idx->arena.alloc<uint32_t>(std::max<int64_t>(1, kept_total), "item sources");
-    k_take_src<<<(unsigned)ceil_div(kept_total, T), T, 0, s>>>(vals, kept_total, idx->item_src);
+    idx->item_src = idx->arena.alloc<int32_t>(kept, "item sources");
+    k_take_src<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(vals, kept, idx->item_src);
     TAURUS_CHECK_LAUNCH();
-    tmp.release();
-    TAURUS_HIP(hipStreamSynchronize(s));
-    idx->ms_build = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    finish();
     return idx;
 }
 
@@ -656,7 +822,8 @@ struct taurus_layer {
     std::shared_ptr<taurus::ChunkIndex> idx;
     bool poisoned = false;
     int64_t n = 0, C = 0, nchunks = 0;
-    int d_o = 0, ncols = 0, G = 0, VEC = 0;
+    int d_o = 0, ncols = 0;
+    taurus::ScatterShape shape{};
     int2* cnt = nullptr;
     float* n_out = nullptr;
     float* acc = nullptr;
@@ -669,12 +836,46 @@ struct taurus_layer {
     std::vector<uint8_t> pushed;
     int64_t npushed = 0;
     double ms_init = 0, ms_index = 0;
-    std::vector<hipEvent_t> events;  // 4 per chunk when profiling
-    ~taurus_layer() {
-        for (auto ev : events)
-            if (ev) (void)hipEventDestroy(ev);
-    }
+    std::vector<hipEvent_t> events;  // EV_PER_CHUNK per chunk when profiling
+    ~taurus_layer();
 };
+
+namespace taurus {
+
+// events per pushed chunk: before the transform, the self pass, the scatter,
+// the fix-up, and after it
+constexpr int EV_PER_CHUNK = 5;
+
+// Timing events are recycled across layers (creating them costs more than
+// recording them).
+static std::mutex g_event_mu;
+static std::vector<hipEvent_t>* g_free_events = new std::vector<hipEvent_t>();
+
+static hipEvent_t timing_event_acquire() {
+    {
+        std::lock_guard<std::mutex> g(g_event_mu);
+        if (!g_free_events->empty()) {
+            hipEvent_t ev = g_free_events->back();
+            g_free_events->pop_back();
+            return ev;
+        }
+    }
+    hipEvent_t ev = nullptr;
+    TAURUS_HIP(hipEventCreate(&ev));
+    return ev;
+}
+
+static void timing_event_release(hipEvent_t ev) {
+    if (!ev) return;
+    std::lock_guard<std::mutex> g(g_event_mu);
+    g_free_events->push_back(ev);
+}
+
+}  // namespace taurus
+
+taurus_layer::~taurus_layer() {
+    for (auto ev : events) taurus::timing_event_release(ev);
+}
 
 namespace taurus {
 
@@ -711,7 +912,8 @@ static void layer_init(taurus_layer* L) {
     L->nchunks = ceil_div(n, C);
     L->d_o = d.d_out;
     L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.d_out;
-    row_group_shape(L->d_o, &L->G, &L->VEC);
+    L->shape = scatter_shape(L->d_o);
+    L->shape.max_blocks = scatter_resident_blocks(L->shape) * std::max(1, env_int("TAURUS_SCATTER_WAVES", 1));
     const int T = 256;
 
     // chunk index: shared from the plan for exact layers, else built here
@@ -720,6 +922,7 @@ static void layer_init(taurus_layer* L) {
         if (!same_graph(plan->g, g) || plan->chunk != C)
             fail(TAURUS_E_INVALID, "plan was built for another graph or chunk size");
         L->idx = plan->idx;
+        L->idx->wait_ready(s);
     } else {
         L->idx = build_index(g, C, L->mask, s, 0);
         L->ms_index = L->idx->ms_build;
@@ -727,7 +930,7 @@ static void layer_init(taurus_layer* L) {
     const ChunkIndex& idx = *L->idx;
 
     L->cnt = L->arena.alloc<int2>(n, "pending counts");
-    k_init_counts<<<(unsigned)ceil_div(n, T), T, 0, s>>>(idx.items_per_v, n, L->cnt);
+    k_init_counts<<<(unsigned)ceil_div(n, T), T, 0, s>>>(idx.m, n, L->cnt);
     TAURUS_CHECK_LAUNCH();
     if (d.agg == TAURUS_GCN_SYM) {
         L->n_out = L->arena.alloc<float>(n, "source norms");
@@ -735,15 +938,18 @@ static void layer_init(taurus_layer* L) {
         TAURUS_CHECK_LAUNCH();
     }
 
-    // weights and bias
+    // packed weights and bias, one transfer through pinned staging (the
+    // synchronisation at the end keeps the staging buffer until it is done)
     std::vector<float> packed;
     gemm_pack_weights_f32(d.weight, d.d_in, L->ncols, packed);
-    L->wpack = L->arena.alloc<float>((int64_t)packed.size(), "packed weights");
-    TAURUS_HIP(hipMemcpyAsync(L->wpack, packed.data(), packed.size() * 4, hipMemcpyHostToDevice, s));
-    std::vector<float> hb((size_t)L->d_o, 0.0f);
-    if (d.bias) std::copy(d.bias, d.bias + L->d_o, hb.begin());
-    L->bias = L->arena.alloc<float>(L->d_o, "bias");
-    TAURUS_HIP(hipMemcpyAsync(L->bias, hb.data(), hb.size() * 4, hipMemcpyHostToDevice, s));
+    const size_t wfloats = (packed.size() + 63) / 64 * 64;
+    const size_t pbytes = (wfloats + (size_t)L->d_o) * 4;
+    float* stage = static_cast<float*>(pinned_staging(pbytes));
+    std::copy(packed.begin(), packed.end(), stage);
+    for (int j = 0; j < L->d_o; j++) stage[wfloats + (size_t)j] = d.bias ? d.bias[j] : 0.0f;
+    L->wpack = L->arena.alloc<float>((int64_t)(pbytes / 4), "packed weights and bias");
+    L->bias = L->wpack + wfloats;
+    TAURUS_HIP(hipMemcpyAsync(L->wpack, stage, pbytes, hipMemcpyHostToDevice, s));
 
     // working buffers
     L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
@@ -752,13 +958,18 @@ static void layer_init(taurus_layer* L) {
     L->carry = L->arena.alloc<float>(slots * L->d_o, "hub piece carries");
     L->carry_cnt = L->arena.alloc<int32_t>(slots, "hub piece counts");
     L->pushed.assign((size_t)L->nchunks, 0);
-    if (d.profile) {  // four events per chunk: before/after transform, scatter, fix-up
-        L->events.assign((size_t)L->nchunks * 4, nullptr);
-        for (auto& ev : L->events) TAURUS_HIP(hipEventCreate(&ev));
+    if (d.profile) {
+        L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
+        for (auto& ev : L->events) ev = timing_event_acquire();
     }
-    // host-side copies above read pageable memory that must stay valid until they ran
     TAURUS_HIP(hipStreamSynchronize(s));
-    L->ms_init = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    L->ms_init = ms_since(t_start);
+}
+
+static bool chunk_has_units(const ChunkIndex& idx, int64_t k) {
+    for (int l = 0; l <= NCLASS; l++)
+        if (idx.list_count(l, k) > 0) return true;
+    return false;
 }
 
 static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int32_t x_on_host) {
@@ -772,9 +983,9 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     if (L->pushed[(size_t)k]) fail(TAURUS_E_STATE, "chunk %lld pushed twice", (long long)k);
     const ChunkIndex& idx = *L->idx;
     hipStream_t s = L->s;
-    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipEvent_t ev[EV_PER_CHUNK] = {};
     if (L->d.profile) {
-        for (int i = 0; i < 4; i++) ev[i] = L->events[(size_t)k * 4 + i];
+        for (int i = 0; i < EV_PER_CHUNK; i++) ev[i] = L->events[(size_t)k * EV_PER_CHUNK + i];
         TAURUS_HIP(hipEventRecord(ev[0], s));
     }
     L->pushed[(size_t)k] = 1;
@@ -786,7 +997,7 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.Y = L->Y;
     p.ystride = L->ncols;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
-    p.src = idx.item_src + idx.chunk_off[(size_t)k];
+    p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
     p.cnt = L->cnt;
     p.acc = L->acc;
     p.d_o = L->d_o;
@@ -797,16 +1008,23 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.out = L->d.out;
     p.carry = L->carry;
     p.carry_cnt = L->carry_cnt;
-    p.long_base = idx.long_off[(size_t)k];
-    const int64_t ns = idx.short_off[(size_t)k + 1] - idx.short_off[(size_t)k];
-    const int64_t nl = idx.long_off[(size_t)k + 1] - idx.long_off[(size_t)k];
-    if (ns + nl > 0)
-        dispatch_scatter(L->G, L->VEC, p, idx.u_short + idx.short_off[(size_t)k], ns,
-                         idx.u_long + idx.long_off[(size_t)k], nl, s);
+    p.long_base = idx.list_off[NCLASS][(size_t)k];
+    p.first_row = b;
+    p.rows = e - b;
+    dispatch_self(L->shape, p, s);
     if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
-    const int64_t nfix = idx.fix_off[(size_t)k + 1] - idx.fix_off[(size_t)k];
-    if (nfix > 0) dispatch_fixup(L->G, L->VEC, p, idx.u_fix + idx.fix_off[(size_t)k], nfix, s);
+    if (chunk_has_units(idx, k)) {
+        ChunkUnits cu;
+        for (int l = 0; l <= NCLASS; l++) {
+            cu.u[l] = idx.list_at(l, k);
+            cu.n[l] = idx.list_count(l, k);
+        }
+        dispatch_scatter(L->shape, p, cu, s);
+    }
     if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
+    const int64_t nfix = idx.list_count(NCLASS + 1, k);
+    if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
+    if (ev[4]) TAURUS_HIP(hipEventRecord(ev[4], s));
 }
 
 static int finalize(taurus_layer* L, taurus_stats* st) {
@@ -815,41 +1033,42 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
     const ChunkIndex& idx = *L->idx;
     Arena tmp(s);
     unsigned long long* dleft = tmp.alloc<unsigned long long>(1, "pending count");
-    TAURUS_HIP(hipMemsetAsync(dleft, 0, 8, s));
+    fill_i32(reinterpret_cast<int32_t*>(dleft), 2, 0, s);
     k_count_pending<<<(unsigned)ceil_div(L->n, 256), 256, 0, s>>>(L->cnt, L->n, dleft);
     TAURUS_CHECK_LAUNCH();
     unsigned long long left = 0;
-    TAURUS_HIP(hipMemcpyAsync(&left, dleft, 8, hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
+    Readback rb;
+    rb.add(&left, dleft, 1);
+    rb.run(s);
     if (st) {
         std::memset(st, 0, sizeof(*st));
         st->n = L->n;
         st->e = L->g.e;
         st->messages = idx.kept;
         st->self_terms = L->n;
-        st->pairs = idx.pairs;
+        st->pairs = idx.segments + L->n;
         st->pending_left = (int64_t)left;
         st->completed = L->n - (int64_t)left;
         st->chunks = L->nchunks;
         st->chunks_pushed = L->npushed;
-        st->short_units = idx.n_short;
-        st->wave_units = idx.n_long;
-        st->split_segments = idx.n_fix;
+        for (int c = 0; c < NCLASS; c++) st->short_units += idx.n_list[c];
+        st->wave_units = idx.n_list[NCLASS];
+        st->split_segments = idx.n_list[NCLASS + 1];
         st->device_bytes = L->arena.peak() + (L->ms_index > 0 ? idx.arena.peak() : 0);
         st->ms_init = L->ms_init;
-        for (size_t i = 0; i + 3 < L->events.size(); i += 4) {
-            const size_t k = i / 4;
-            if (!L->pushed[k]) continue;
-            float a = 0, b = 0, c = 0;
-            TAURUS_HIP(hipEventElapsedTime(&a, L->events[i], L->events[i + 1]));
-            TAURUS_HIP(hipEventElapsedTime(&b, L->events[i + 1], L->events[i + 2]));
-            TAURUS_HIP(hipEventElapsedTime(&c, L->events[i + 2], L->events[i + 3]));
-            st->ms_gemm += a;
-            st->ms_scatter += b;
-            st->ms_fixup += c;
+        for (int64_t k = 0; k < L->nchunks && !L->events.empty(); k++) {
+            if (!L->pushed[(size_t)k]) continue;
+            hipEvent_t* ev = &L->events[(size_t)k * EV_PER_CHUNK];
+            float t[EV_PER_CHUNK - 1] = {};
+            for (int i = 0; i + 1 < EV_PER_CHUNK; i++) TAURUS_HIP(hipEventElapsedTime(&t[i], ev[i], ev[i + 1]));
+            st->ms_gemm += t[0];
+            st->ms_self += t[1];
+            st->ms_scatter += t[2];
+            st->ms_fixup += t[3];
             st->launches_gemm++;
-            st->launches_scatter += (idx.short_off[k + 1] > idx.short_off[k] || idx.long_off[k + 1] > idx.long_off[k]) ? 1 : 0;
-            st->launches_fixup += idx.fix_off[k + 1] > idx.fix_off[k] ? 1 : 0;
+            st->launches_self++;
+            st->launches_scatter += chunk_has_units(idx, k) ? 1 : 0;
+            st->launches_fixup += idx.list_count(NCLASS + 1, k) > 0 ? 1 : 0;
         }
     }
     return left ? TAURUS_E_INCOMPLETE : TAURUS_OK;

@@ -2,7 +2,11 @@
 // prefix sum and a stable LSD radix sort of 64-bit keys with 32-bit values.
 // Both are written for wave64: wave-level scans use cross-lane shuffles and
 // the radix ranking matches digits within a wave with eight ballots.
+#include <algorithm>
 #include <cstdarg>
+#include <map>
+#include <mutex>
+#include <unordered_map>
 
 #include "internal.hpp"
 
@@ -32,44 +36,190 @@ void fail(int status, const char* fmt, ...) {
 
 const char* last_error_cstr() { return g_last_error.c_str(); }
 
-// ---------------------------------------------------------------- arena -----
-static void keep_pool_memory() {
-    static bool done[64] = {false};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || done[dev]) return;
-    hipMemPool_t pool;
-    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-        uint64_t keep = UINT64_MAX;
-        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-    }
-    (void)hipGetLastError();
-    done[dev] = true;
+// ------------------------------------------------------ device memory cache --
+// Device memory comes from hipMalloc once and is then recycled.  A released
+// block goes to a free list keyed by (device, size class) with the stream it
+// was released on and an event recorded there.  A later request of the same
+// class takes it at once on that stream (stream order covers the earlier
+// use), or on another stream after making that stream wait for the event.
+// Requests are rounded up to a class (at most 1/8 above the request), so
+// buffers of similar size share blocks.  On hipMalloc failure every cached
+// block of the device is returned to the driver and the request retried once.
+namespace {
+
+struct FreeBlock {
+    void* p;
+    hipStream_t s;
+};
+
+struct BlockInfo {
+    int dev;
+    size_t cls;
+    hipEvent_t ev;  // recorded on release; created on the first release
+};
+
+struct DeviceCache {
+    std::mutex mu;
+    std::map<std::pair<int, size_t>, std::vector<FreeBlock>> free_lists;
+    std::unordered_map<void*, BlockInfo> blocks;  // every block obtained from hipMalloc
+};
+
+// lives until the process ends: blocks may be released from static destructors
+DeviceCache& device_cache() {
+    static DeviceCache* c = new DeviceCache();
+    return *c;
 }
 
-void* Arena::alloc_bytes(int64_t bytes, const char* what) {
-    if (bytes <= 0) bytes = 16;
-    bytes = (bytes + 255) & ~(int64_t)255;
-    if (budget_ > 0 && bytes_ + bytes > budget_)
-        fail(TAURUS_E_BUDGET, "allocating %lld bytes for %s exceeds the budget (%lld of %lld in use)",
-             (long long)bytes, what, (long long)bytes_, (long long)budget_);
-    keep_pool_memory();
+size_t size_class(size_t bytes) {
+    if (bytes <= 4096) return 4096;
+    const int k = 63 - __builtin_clzll((unsigned long long)bytes);  // 2^k <= bytes
+    const size_t step = (size_t)1 << std::max(k - 3, 12);
+    return (bytes + step - 1) / step * step;
+}
+
+// hipFree every cached block of device dev (the caller holds no lock)
+void trim_device(int dev) {
+    DeviceCache& c = device_cache();
+    (void)hipDeviceSynchronize();
+    std::lock_guard<std::mutex> g(c.mu);
+    for (auto it = c.free_lists.begin(); it != c.free_lists.end();) {
+        if (it->first.first != dev) {
+            ++it;
+            continue;
+        }
+        for (const FreeBlock& b : it->second) {
+            auto bi = c.blocks.find(b.p);
+            if (bi != c.blocks.end()) {
+                if (bi->second.ev) (void)hipEventDestroy(bi->second.ev);
+                c.blocks.erase(bi);
+            }
+            (void)hipFree(b.p);
+        }
+        it = c.free_lists.erase(it);
+    }
+    (void)hipGetLastError();
+}
+
+}  // namespace
+
+void* device_acquire(size_t bytes, hipStream_t s, size_t* got) {
+    int dev = 0;
+    TAURUS_HIP(hipGetDevice(&dev));
+    const size_t cls = size_class(bytes);
+    *got = cls;
+    DeviceCache& c = device_cache();
+    {
+        std::lock_guard<std::mutex> g(c.mu);
+        auto it = c.free_lists.find({dev, cls});
+        if (it != c.free_lists.end() && !it->second.empty()) {
+            std::vector<FreeBlock>& v = it->second;
+            size_t pick = v.size() - 1;
+            for (size_t i = v.size(); i-- > 0;)
+                if (v[i].s == s) {
+                    pick = i;
+                    break;
+                }
+            const FreeBlock b = v[pick];
+            v.erase(v.begin() + (long)pick);
+            if (b.s != s) TAURUS_HIP(hipStreamWaitEvent(s, c.blocks.at(b.p).ev, 0));
+            return b.p;
+        }
+    }
     void* p = nullptr;
-    hipError_t e = hipMallocAsync(&p, (size_t)bytes, stream_);
+    hipError_t e = hipMalloc(&p, cls);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        trim_device(dev);
+        e = hipMalloc(&p, cls);
+    }
     if (e != hipSuccess) {
         (void)hipGetLastError();
-        fail(e == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE,
-             "hipMallocAsync(%lld) for %s failed: %s", (long long)bytes, what, hipGetErrorString(e));
+        fail(e == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE, "hipMalloc(%zu) failed: %s", cls,
+             hipGetErrorString(e));
     }
-    blocks_.push_back({p, bytes});
-    bytes_ += bytes;
+    std::lock_guard<std::mutex> g(c.mu);
+    c.blocks[p] = BlockInfo{dev, cls, nullptr};
+    return p;
+}
+
+void device_release(void* p, hipStream_t s) {
+    if (!p) return;
+    DeviceCache& c = device_cache();
+    std::lock_guard<std::mutex> g(c.mu);
+    auto bi = c.blocks.find(p);
+    if (bi == c.blocks.end()) return;
+    BlockInfo& info = bi->second;
+    if (!info.ev && hipEventCreateWithFlags(&info.ev, hipEventDisableTiming) != hipSuccess) {
+        // no event: wait here so that any stream may take the block
+        (void)hipGetLastError();
+        info.ev = nullptr;
+        (void)hipStreamSynchronize(s);
+        (void)hipFree(p);
+        c.blocks.erase(bi);
+        return;
+    }
+    (void)hipEventRecord(info.ev, s);
+    c.free_lists[{info.dev, info.cls}].push_back(FreeBlock{p, s});
+}
+
+// ------------------------------------------------------------ pinned staging --
+// One pinned host buffer per host thread for small transfers, grown on demand
+// and kept until the process ends.
+void* pinned_staging(size_t bytes) {
+    static thread_local void* buf = nullptr;
+    static thread_local size_t cap = 0;
+    if (bytes > cap) {
+        size_t want = std::max<size_t>(bytes, 64 << 10);
+        void* p = nullptr;
+        TAURUS_HIP(hipHostMalloc(&p, want, hipHostMallocDefault));
+        if (buf) (void)hipHostFree(buf);
+        buf = p;
+        cap = want;
+    }
+    return buf;
+}
+
+void Readback::add(void* host, const void* dev, size_t bytes) {
+    items_.push_back({host, dev, bytes, total_});
+    total_ += (bytes + 15) & ~(size_t)15;
+}
+
+void Readback::run(hipStream_t s) {
+    if (items_.empty()) return;
+    char* stage = static_cast<char*>(pinned_staging(total_));
+    for (const Item& it : items_)
+        TAURUS_HIP(hipMemcpyAsync(stage + it.off, it.dev, it.bytes, hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    for (const Item& it : items_) std::memcpy(it.host, stage + it.off, it.bytes);
+    items_.clear();
+    total_ = 0;
+}
+
+// ---------------------------------------------------------------- arena -----
+void* Arena::alloc_bytes(int64_t bytes, const char* what) {
+    if (bytes <= 0) bytes = 16;
+    const int64_t cls = (int64_t)size_class((size_t)bytes);
+    if (budget_ > 0 && bytes_ + cls > budget_)
+        fail(TAURUS_E_BUDGET, "allocating %lld bytes for %s exceeds the budget (%lld of %lld in use)",
+             (long long)cls, what, (long long)bytes_, (long long)budget_);
+    size_t got = 0;
+    void* p = nullptr;
+    try {
+        p = device_acquire((size_t)bytes, stream_, &got);
+    } catch (const Failure&) {
+        set_error("%s (for %s)", last_error_cstr(), what);
+        throw;
+    }
+    blocks_.push_back({p, (int64_t)got});
+    bytes_ += (int64_t)got;
     if (bytes_ > peak_) peak_ = bytes_;
     return p;
 }
 
 void Arena::free_ptr(void* p) {
-    for (size_t i = 0; i < blocks_.size(); i++) {
+    for (size_t i = blocks_.size(); i-- > 0;) {
         if (blocks_[i].p == p) {
-            (void)hipFreeAsync(p, stream_);
+            device_release(p, stream_);
             bytes_ -= blocks_[i].bytes;
             blocks_.erase(blocks_.begin() + (long)i);
             return;
@@ -78,9 +228,22 @@ void Arena::free_ptr(void* p) {
 }
 
 void Arena::release() {
-    for (auto& b : blocks_) (void)hipFreeAsync(b.p, stream_);
+    for (auto& b : blocks_) device_release(b.p, stream_);
     blocks_.clear();
     bytes_ = 0;
+}
+
+// ----------------------------------------------------------------- fills ----
+template <typename T>
+__global__ void k_fill(T* __restrict__ p, int64_t n, T v) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+void fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
+    if (n <= 0) return;
+    k_fill<int32_t><<<(unsigned)ceil_div(n, 256), 256, 0, s>>>(p, n, v);
+    TAURUS_CHECK_LAUNCH();
 }
 
 // ---------------------------------------------------------------- scan ------
@@ -241,7 +404,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __res
 __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
     int64_t nblocks, const uint64_t* __restrict__ offs, uint64_t* __restrict__ kout,
-    uint32_t* __restrict__ vout, int* __restrict__ bad) {
+    uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
     __shared__ uint64_t base[256];
     __shared__ uint32_t run[256];
     __shared__ uint32_t wcnt[RS_WAVES][256];
@@ -277,7 +440,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
                 kout[pos] = key;
                 if (vin) vout[pos] = val;
             } else {
-                atomicOr(bad, 1);
+                atomicOr(bad, bad_bit);
             }
         }
         __syncthreads();
@@ -288,42 +451,25 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     }
 }
 
-void radix_sort_u64(uint64_t* keys, uint32_t* vals, int64_t n, int key_bits, Arena& arena,
-                    hipStream_t s) {
+void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
+                    int bad_bit) {
     if (n <= 1 || key_bits <= 0) return;
     const int64_t nblocks = ceil_div(n, RS_TILE);
     if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
-    uint64_t* k2 = arena.alloc<uint64_t>(n, "radix keys");
-    uint32_t* v2 = vals ? arena.alloc<uint32_t>(n, "radix values") : nullptr;
     uint32_t* hist = arena.alloc<uint32_t>(256 * nblocks, "radix histogram");
     uint64_t* offs = arena.alloc<uint64_t>(256 * nblocks, "radix offsets");
-    int* bad = arena.alloc<int>(1, "radix flag");
-    TAURUS_HIP(hipMemsetAsync(bad, 0, sizeof(int), s));
-    uint64_t *ka = keys, *kb = k2;
-    uint32_t *va = vals, *vb = v2;
-    int passes = 0;
-    for (int shift = 0; shift < key_bits; shift += 8, passes++) {
-        k_radix_hist<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(ka, n, shift, nblocks, hist);
+    for (int shift = 0; shift < key_bits; shift += 8) {
+        const int c = b.cur;
+        k_radix_hist<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
         TAURUS_CHECK_LAUNCH();
         scan_u32_to_u64(hist, offs, 256 * nblocks, false, arena, s);
-        k_radix_scatter<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(ka, va, n, shift, nblocks, offs, kb, vb, bad);
+        k_radix_scatter<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks, offs,
+                                                                 b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
         TAURUS_CHECK_LAUNCH();
-        std::swap(ka, kb);
-        std::swap(va, vb);
+        b.cur = 1 - c;
     }
-    if (ka != keys) {
-        TAURUS_HIP(hipMemcpyAsync(keys, ka, (size_t)n * 8, hipMemcpyDeviceToDevice, s));
-        if (vals) TAURUS_HIP(hipMemcpyAsync(vals, va, (size_t)n * 4, hipMemcpyDeviceToDevice, s));
-    }
-    int hbad = 0;
-    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
-    TAURUS_HIP(hipStreamSynchronize(s));
-    arena.free_ptr(bad);
     arena.free_ptr(offs);
     arena.free_ptr(hist);
-    if (hbad) fail(TAURUS_E_DEVICE, "radix sort: internal offset out of range");
-    if (v2) arena.free_ptr(v2);
-    arena.free_ptr(k2);
 }
 
 }  // namespace taurus
