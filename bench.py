@@ -105,6 +105,111 @@ def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int) -> dict:
     return {"scatter": sc, "self": se, "fixup": fx}
 
 
+# ---------------------------------------------------------------- profiles --
+PROFILE = os.path.join(ROOT, "profiles", "k_scatter_gcn2-rmat-1m.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "layer.hip")
+GIB_KIB = float(1 << 20)
+
+
+def source_digest() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def profiled_traffic():
+    """HBM bytes per k_scatter launch from the committed counter summary, or
+    None when there is none or the kernel source changed since it was taken."""
+    try:
+        text = open(PROFILE).read()
+    except OSError:
+        return None
+    vals = dict(line.strip().split(": ", 1) for line in text.splitlines()
+                if line.startswith("    ") and ": " in line)
+    if vals.get("source_sha256") != source_digest():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _short_name(name: str) -> str:
+    import re
+    return re.sub(r"\(.*", "", name).replace("void ", "").strip()
+
+
+def _counter_means(d: str, counter: str) -> dict:
+    """kernel short name -> (dispatches, mean counter value per dispatch)."""
+    import csv
+    import glob
+    acc = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            k = _short_name(r["Kernel_Name"])
+            n, t = acc.get(k, (0, 0.0))
+            acc[k] = (n + 1, t + float(r["Counter_Value"]))
+    return {k: (n, t / n) for k, (n, t) in acc.items()}
+
+
+def summarize_profile(trace_dir: str, fetch_dir: str, write_dir: str) -> str:
+    import csv
+    import glob
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not stats:
+        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
+    rows = list(csv.DictReader(open(stats[0])))
+    out = ["# k_scatter on gcn2-rmat-1m (2-layer GCN 128->128->64, RMAT 1M vertices / 20M edges, "
+           "65,536-vertex chunks)", "",
+           "Commands, from the repository root on one MI355X:", "",
+           "    rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_gcn -o gcn -- "
+           "python3 bench.py --steps 10 --warmup 2 --no-cpu-baseline",
+           "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o p -- "
+           "python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --no-profile --copy-calibration",
+           "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o p -- "
+           "python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --no-profile --copy-calibration",
+           "    python3 bench.py --summarize-profile gpurun_out/prof_gcn gpurun_out/pmc_fetch gpurun_out/pmc_write",
+           "", "## Kernel time (--kernel-trace --stats, 12 steps)", "",
+           "| kernel | calls | total ms | average us | % |", "|---|---|---|---|---|"]
+    for r in rows[:16]:
+        out.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    sc = [r for r in rows if "k_scatter<" in r["Name"]]
+    calls = sum(int(r["Calls"]) for r in sc)
+    tot_ns = sum(float(r["TotalDurationNs"]) for r in sc)
+    fetch = _counter_means(fetch_dir, "FETCH_SIZE")
+    write = _counter_means(write_dir, "WRITE_SIZE")
+
+    def pick(d, pred):
+        ks = [k for k in d if pred(k)]
+        n = sum(d[k][0] for k in ks)
+        return n, (sum(d[k][0] * d[k][1] for k in ks) / n if n else float("nan"))
+
+    _, f_cal = pick(fetch, lambda k: "neg_kernel" in k)
+    _, w_cal = pick(write, lambda k: "neg_kernel" in k)
+    nf, f_sc = pick(fetch, lambda k: "k_scatter<" in k)
+    nw, w_sc = pick(write, lambda k: "k_scatter<" in k)
+    ff, fw = GIB_KIB / f_cal, GIB_KIB / w_cal
+    traffic = (f_sc * ff + w_sc * fw) * 1024.0
+    out += ["", "## HBM traffic of k_scatter (--pmc, one counter per run)", "",
+            f"Calibration: torch neg over 1 GiB (1,048,576 KiB read and written) reads FETCH_SIZE "
+            f"{f_cal:.0f} KiB and WRITE_SIZE {w_cal:.0f} KiB per dispatch, so the factors are "
+            f"{ff:.3f} (fetch) and {fw:.3f} (write).", "",
+            f"k_scatter, mean over {nf} / {nw} dispatches (both layers): FETCH_SIZE {f_sc:.0f} KiB, "
+            f"WRITE_SIZE {w_sc:.0f} KiB per dispatch; scaled: {traffic / 1e6:.1f} MB per launch.", "",
+            "Machine-readable (bench.py reports traffic only while the kernel source digest matches):", "",
+            "    kernel: k_scatter",
+            f"    launches: {calls}",
+            f"    avg_launch_us: {tot_ns / max(calls, 1) / 1e3:.2f}",
+            f"    fetch_factor: {ff:.4f}",
+            f"    write_factor: {fw:.4f}",
+            f"    traffic_bytes_per_launch: {traffic:.0f}",
+            f"    source_sha256: {source_digest()}"]
+    return "\n".join(out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,7 +219,12 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy, the reference kernel for HBM byte counters")
+    ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="print the profile summary of a kernel-trace run and FETCH_SIZE / WRITE_SIZE runs")
     args = ap.parse_args()
+    if args.summarize_profile:
+        print(summarize_profile(*args.summarize_profile))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the path has no multi-GPU mode; see DESIGN.md for how it would shard)", file=sys.stderr)
@@ -138,10 +248,12 @@ def main():
     outs = [torch.empty((w.n, s["d_out"]), dtype=torch.float32, device=dev) for s in specs]
     profile = not args.no_profile
     if args.copy_calibration:
-        a = torch.ones(1 << 28, dtype=torch.float32, device=dev)     # 1 GiB
+        # a plain streaming kernel of known size for the byte counters:
+        # neg reads 1 GiB and writes 1 GiB
+        a = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         c = torch.empty_like(a)
         for _ in range(3):
-            c.copy_(a)
+            torch.neg(a, out=c)
         del a, c
     torch.cuda.synchronize()
     fm = flush_model(src, dst, w.n, w.chunk)
@@ -223,7 +335,7 @@ def main():
         byt, ms_, nlaunch = tot["scatter"]
         achieved = byt / (ms_ * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_scatter",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(), "kernel": "k_scatter",
                     "avg_launch_us": round(ms_ * 1e3 / nlaunch, 2), "bytes_per_launch": round(byt / nlaunch, 0),
                     "model_check": model_ok}
     gemm = None
