@@ -10,7 +10,7 @@
  *   - graph storage: CSR by source (Sec. 3.2, "Data Layout"), built by
  *     sorting the (u, v) pairs, plus in-neighbour lists for the gather;
  *   - one layer = Aggregate over in-neighbours then Update and activation
- *     (Background, Eqs. gnn-1 and gnn-2), evaluated per destination in fp64
+ *     (Sec. 2.1, Eqs. (1)-(2)), evaluated per destination in fp64
  *     with in-neighbours visited in ascending source ID.  The paper states
  *     that source-centric broadcast is semantically equal to this gather for
  *     the same message set, Aggregate and Update (Sec. 3.1), so the gather is
