@@ -86,25 +86,67 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 // Chunk-index items.  CSR edge i (source u = the row containing i) becomes
 // key (chunk(u) << vbits | v), value u - chunk(u)*C; a dropped edge gets
 // chunk = nchunks so it sorts after every kept item.
-__global__ void k_make_items(const int64_t* __restrict__ row_off, const int32_t* __restrict__ col_dst,
-                             int64_t e, int64_t n, int64_t C, int64_t nchunks, int vbits,
-                             const uint64_t* __restrict__ mask, uint64_t* __restrict__ keys,
-                             uint32_t* __restrict__ vals, int* __restrict__ bad) {
+//
+// Rows are found without a per-lane binary search (a chain of ~log2 n
+// dependent loads): the wave finds the row u0 of its first edge with a
+// 64-ary search (all lanes probe at once, ~log64 n dependent loads), stages
+// row_off[u0+1 .. u0+64] in LDS, and each lane locates its own edge among
+// those; an edge more than 64 rows past u0 (only after many empty rows)
+// falls back to a binary search of the rest.
+__global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
+                                                    const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
+                                                    int64_t C, int64_t nchunks, int vbits,
+                                                    const uint64_t* __restrict__ mask, uint64_t* __restrict__ keys,
+                                                    uint32_t* __restrict__ vals, int* __restrict__ bad) {
+    __shared__ int64_t ro[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= e) return;
-    int64_t lo = 0, hi = n;  // largest u with row_off[u] <= i
-    while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (row_off[mid] <= i) lo = mid;
-        else hi = mid;
+    const int64_t i0 = i - lane;  // the wave's first edge
+    // largest u0 in [0, n) with row_off[u0] <= i0; probes stay in [0, n]
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 64) {
+        const int64_t step = (hi - lo + 63) >> 6;
+        const int64_t p = min(lo + (int64_t)(lane + 1) * step, hi);
+        const int k = __popcll(__ballot(row_off[p] <= i0));
+        const int64_t nlo = lo + (int64_t)k * step;
+        hi = min(nlo + step, hi);
+        lo = nlo;
     }
-    const int64_t u = lo, v = col_dst[i];
+    {
+        const int64_t p = lo + lane + 1;
+        const int k = __popcll(__ballot(p <= hi && row_off[p] <= i0));
+        lo += k;
+    }
+    const int64_t u0 = min(lo, n - 1);
+    const int64_t q = u0 + 1 + lane;
+    ro[wave][lane] = q <= n ? row_off[q] : INT64_MAX;
+    __syncthreads();
+    if (i >= e) return;
+    // u = u0 + #{j : row_off[u0 + 1 + j] <= i}
+    int64_t u;
+    if (ro[wave][63] <= i) {
+        int64_t a = u0 + 64, z = n;  // largest u in [a, n) with row_off[u] <= i
+        while (z - a > 1) {
+            const int64_t mid = (a + z) >> 1;
+            if (row_off[mid] <= i) a = mid;
+            else z = mid;
+        }
+        u = min(a, n - 1);
+    } else {
+        int c = 0;
+#pragma unroll
+        for (int half = 32; half >= 1; half >>= 1)
+            if (ro[wave][c + half - 1] <= i) c += half;
+        u = u0 + c;
+    }
+    const int64_t v = col_dst[i];
     // rows strictly ascending, no self loops (a simple graph)
     if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
     const bool kept = !mask || ((mask[i >> 6] >> (i & 63)) & 1ull);
-    const int64_t ch = kept ? u / C : nchunks;
+    const uint32_t cu = (uint32_t)u / (uint32_t)C;  // u < 2^31 and C < 2^31: 32-bit division
+    const int64_t ch = kept ? (int64_t)cu : nchunks;
     keys[i] = ((uint64_t)ch << vbits) | (uint64_t)v;
-    vals[i] = (uint32_t)(u - (u / C) * C);
+    vals[i] = (uint32_t)u - cu * (uint32_t)C;
 }
 
 // offs[j] = first sorted position whose chunk field is >= j, j in [0, nchunks]

@@ -383,71 +383,140 @@ constexpr int RS_ITEMS = 16;
 constexpr int RS_TILE = RS_THREADS * RS_ITEMS;
 constexpr int RS_WAVES = RS_THREADS / 64;
 
+// Lanes of a wave holding the same 8-bit digit d: eight ballots, one per bit.
+__device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int bt = 0; bt < 8; bt++) {
+        const bool bit = (d >> bt) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+// Per tile: count of each digit (LDS atomics; the tile's loads are issued
+// before any of them).
 __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __restrict__ keys, int64_t n,
                                                            int shift, int64_t nblocks,
                                                            uint32_t* __restrict__ hist) {
     __shared__ uint32_t h[256];
     h[threadIdx.x] = 0;
-    __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * RS_TILE;
-    for (int i = threadIdx.x; i < RS_TILE; i += RS_THREADS) {
-        int64_t g = base + i;
-        if (g < n) atomicAdd(&h[(keys[g] >> shift) & 255u], 1u);
+    uint32_t d[RS_ITEMS];
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; r++) {
+        const int64_t g = base + r * RS_THREADS + threadIdx.x;
+        d[r] = g < n ? (uint32_t)((keys[g] >> shift) & 255u) : 256u;
     }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; r++)
+        if (d[r] < 256u) atomicAdd(&h[d[r]], 1u);
     __syncthreads();
     hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-// Scatter one tile stably: items are ranked in index order, 256 at a time.
-// Within a round a lane's rank among equal digits of its wave comes from the
-// eight-ballot digit match; earlier waves and earlier rounds add their counts.
+// Scatter one tile stably, staged through LDS so that each digit's items
+// leave the block as one contiguous run.  Wave w ranks the tile's items
+// [w * RS_WITEMS, (w + 1) * RS_WITEMS) in index order, 64 per round: a lane's
+// rank is the wave's running count of its digit plus its rank among the
+// lanes holding that digit (digit match).  The waves' counts are then scanned
+// per digit, so wave w's items of digit d follow those of waves < w, and the
+// digit's start within the tile comes from the tile histogram.  The ranked
+// tile is written to LDS in digit order and copied out: LDS slot i of digit
+// d goes to offs[d] + (i - start of d in the tile).
+constexpr int RS_WITEMS = RS_TILE / RS_WAVES;   // items per wave
 __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
-    int64_t nblocks, const uint64_t* __restrict__ offs, uint64_t* __restrict__ kout,
-    uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
-    __shared__ uint64_t base[256];
-    __shared__ uint32_t run[256];
-    __shared__ uint32_t wcnt[RS_WAVES][256];
+    int64_t nblocks, const uint32_t* __restrict__ hist, const uint64_t* __restrict__ offs,
+    uint64_t* __restrict__ kout, uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
+    __shared__ uint64_t skey[RS_TILE];
+    __shared__ uint32_t sval[RS_TILE];
+    __shared__ uint64_t gbase[256];
+    __shared__ uint32_t dstart[256];
+    __shared__ uint32_t wcnt[RS_WAVES][256];   // per wave: running count, then its offset within the digit
+    __shared__ uint32_t wsum[RS_WAVES];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    base[tid] = offs[(int64_t)tid * nblocks + blockIdx.x];
-    run[tid] = 0;
     const int64_t tile0 = (int64_t)blockIdx.x * RS_TILE;
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int count = (int)min((int64_t)RS_TILE, n - tile0);
+    const int wbase = wave * RS_WITEMS;
+
+    // request the wave's items first
+    uint64_t keys[RS_ITEMS];
+    uint32_t vals[RS_ITEMS];
+#pragma unroll
     for (int r = 0; r < RS_ITEMS; r++) {
-        const int64_t g = tile0 + (int64_t)r * RS_THREADS + tid;
-        const bool valid = g < n;
-        uint64_t key = valid ? kin[g] : 0;
-        uint32_t val = (valid && vin) ? vin[g] : 0;
+        const int li = wbase + r * 64 + lane;
+        keys[r] = li < count ? kin[tile0 + li] : 0;
+        vals[r] = (li < count && vin) ? vin[tile0 + li] : 0;
+    }
+#pragma unroll
+    for (int w = 0; w < RS_WAVES; w++) wcnt[w][tid] = 0;
+    // digit starts within the tile: exclusive scan of the tile histogram
+    const uint32_t h = hist[(int64_t)tid * nblocks + blockIdx.x];
+    uint32_t incl = h;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    gbase[tid] = offs[(int64_t)tid * nblocks + blockIdx.x];
+    __syncthreads();
+    uint32_t before_w = 0;
+#pragma unroll
+    for (int w = 0; w < RS_WAVES; w++)
+        if (w < wave) before_w += wsum[w];
+    dstart[tid] = before_w + incl - h;
+
+    // rank within the wave (no block barrier: the counters are the wave's own)
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t rank[RS_ITEMS];
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; r++) {
+        const bool valid = wbase + r * 64 + lane < count;
+        const uint32_t d = (uint32_t)((keys[r] >> shift) & 255u);
+        const uint64_t peers = digit_peers(d, valid);
+        const uint32_t run = valid ? wcnt[wave][d] : 0u;
+        rank[r] = run + (uint32_t)__popcll(peers & lt_mask);
+        if (valid && (peers & lt_mask) == 0) wcnt[wave][d] = run + (uint32_t)__popcll(peers);
+    }
+    __syncthreads();
+    // per digit: offsets of the waves within the tile's run of that digit
+    {
+        uint32_t acc = dstart[tid];
+#pragma unroll
+        for (int w = 0; w < RS_WAVES; w++) {
+            const uint32_t c = wcnt[w][tid];
+            wcnt[w][tid] = acc;
+            acc += c;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; r++) {
+        if (wbase + r * 64 + lane >= count) continue;
+        const uint32_t d = (uint32_t)((keys[r] >> shift) & 255u);
+        const uint32_t lpos = wcnt[wave][d] + rank[r];
+        if (lpos < (uint32_t)count) {
+            skey[lpos] = keys[r];
+            if (vin) sval[lpos] = vals[r];
+        } else {
+            atomicOr(bad, bad_bit);
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < count; i += RS_THREADS) {
+        const uint64_t key = skey[i];
         const uint32_t d = (uint32_t)((key >> shift) & 255u);
-#pragma unroll
-        for (int w = 0; w < RS_WAVES; w++) wcnt[w][tid] = 0;
-        __syncthreads();
-        uint64_t peers = __ballot(valid);
-#pragma unroll
-        for (int b = 0; b < 8; b++) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t m = __ballot(bit);
-            peers &= bit ? m : ~m;
+        const uint64_t pos = gbase[d] + (uint64_t)(i - (int)dstart[d]);
+        if (pos < (uint64_t)n) {
+            kout[pos] = key;
+            if (vin) vout[pos] = sval[i];
+        } else {
+            atomicOr(bad, bad_bit);
         }
-        const uint32_t rank_w = (uint32_t)__popcll(peers & lt_mask);
-        if (valid && rank_w == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
-        __syncthreads();
-        if (valid) {
-            uint32_t before = run[d];
-            for (int w = 0; w < wave; w++) before += wcnt[w][d];
-            const uint64_t pos = base[d] + before + rank_w;
-            if (pos < (uint64_t)n) {
-                kout[pos] = key;
-                if (vin) vout[pos] = val;
-            } else {
-                atomicOr(bad, bad_bit);
-            }
-        }
-        __syncthreads();
-        uint32_t add = 0;
-#pragma unroll
-        for (int w = 0; w < RS_WAVES; w++) add += wcnt[w][tid];
-        run[tid] += add;
     }
 }
 
@@ -463,8 +532,8 @@ void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipSt
         k_radix_hist<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
         TAURUS_CHECK_LAUNCH();
         scan_u32_to_u64(hist, offs, 256 * nblocks, false, arena, s);
-        k_radix_scatter<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks, offs,
-                                                                 b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
+        k_radix_scatter<<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks, hist,
+                                                                 offs, b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
         TAURUS_CHECK_LAUNCH();
         b.cur = 1 - c;
     }
