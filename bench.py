@@ -6,10 +6,10 @@ N(0,1) fp32 features of width 128, layer widths 128 -> 128 -> 64, sources
 streamed in 65,536-vertex chunks.  Inputs (edge list, features) are seeded
 synthetic data resident in HBM before the timed region.
 
-One step = the whole hot path once: CSR build from the edge list, the
-chunk index (a plan shared by both exact layers), then for each layer init
-(pending counts, weights), all chunk pushes (MFMA transform, scatter with
-fused finalise, fix-up) and finalize.
+One step = the whole hot path once: CSR build from the edge list, then for
+each layer init (the chunk index, built by layer 1 and shared with layer 2
+through a plan; pending counts, weights), all chunk pushes (MFMA transform,
+self pass, scatter with fused finalise, fix-up) and finalize.
 
 Output: one JSON line.  value = aggregated edges per second per layer
 (sum over layers of the propagated edges / step time) in GTEPS.  roofline =
@@ -307,7 +307,8 @@ def main():
         if not all(checks):
             model_ok = False
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
-        ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts])) for k in ("gemm", "self", "scatter", "fixup", "init")}
+        ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
+              for k in ("gemm", "self", "scatter", "fixup", "init", "index")}
         if profile:
             for k in tot:
                 tot[k][0] += kb[k] * len(sts)

@@ -41,7 +41,7 @@ typedef enum {
 
 typedef enum { TAURUS_F32 = 0, TAURUS_BF16 = 1, TAURUS_F16 = 2 } taurus_dtype;
 
-/* Per-graph structures shared by the exact layers over one graph (see
+/* Per-graph structures shared by the layers over one graph (see
  * taurus_plan_create). */
 typedef struct taurus_plan taurus_plan;
 
@@ -71,8 +71,11 @@ typedef struct {
 /*
  * One layer.  Host-side descriptor, copied at taurus_layer_init.
  *   agg          taurus_agg.
- *   d_in, d_out  input and output widths; multiples of 4, d_out <= 1024.
- *   in_dtype     storage type of the layer input x (taurus_dtype).
+ *   d_in, d_out  input and output widths; multiples of 4 (d_in a multiple
+ *                of 8 for 16-bit inputs), d_out <= 1024.
+ *   in_dtype     storage type of the layer input x (taurus_dtype); the
+ *                transform multiplies in that type (16-bit: bf16 or fp16
+ *                matrix cores) and accumulates in fp32.
  *   out_dtype    storage type of the layer output (hidden layers usually keep
  *                the input type; values are rounded to nearest even).
  *   relu         1 applies ReLU to the output (all layers but the last).
@@ -82,10 +85,12 @@ typedef struct {
  *                d_out..2*d_out-1 on the vertex's own input.  For 16-bit
  *                in_dtype the weights are rounded to that type at init.
  *   bias         HOST fp32 [d_out], or NULL for no bias; copied at init.
- *   fanout       0 = exact inference (every in-edge propagates); k > 0 keeps
- *                for each destination v its min(d_in(v), k) in-edges whose
- *                rank key (H(seed, 4, layer, v, u), u) is smallest, where H
- *                is the SplitMix64-based counter hash of taurus_hash().
+ *   fanout       0 = exact inference (every in-edge propagates); k in
+ *                [1, 64] keeps for each destination v its min(d_in(v), k)
+ *                in-edges whose rank key (H(seed, 4, layer, v, u), u) is
+ *                smallest, where H is the SplitMix64-based counter hash of
+ *                taurus_hash() (GraphSAGE layers only: the sampled GCN
+ *                normalisation is not defined here).
  *   layer        1-based layer number (only feeds the sampling hash).
  *   seed         sampling seed.
  *   chunk        source-chunk size C in vertices (> 0).  Chunk j covers
@@ -103,11 +108,12 @@ typedef struct {
  *                (NULL = the default stream).
  *   profile      1: time every kernel of the layer with HIP events; the
  *                totals are returned in taurus_stats.
- *   plan         NULL, or a plan built for this graph (same n, e, row_off,
+ *   plan         NULL, or a plan made for this graph (same n, e, row_off,
  *                col_dst pointers) and this chunk size: an exact layer
- *                (fanout = 0) then reuses the plan's chunk index instead of
- *                building its own.  A plan with another graph or chunk size
- *                is TAURUS_E_INVALID.
+ *                (fanout = 0) then shares the plan's chunk index, and a
+ *                sampled layer its in-edge lists, instead of building its
+ *                own.  A plan with another graph or chunk size is
+ *                TAURUS_E_INVALID.
  */
 typedef struct {
     int32_t agg, d_in, d_out, in_dtype, out_dtype, relu;
@@ -145,7 +151,10 @@ typedef struct {
     int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
     double hub_message_share;      /* share of messages landing on resident hubs        */
     /* milliseconds, HIP-event timed when desc.profile = 1 (else 0) */
-    double ms_init, ms_gemm, ms_self, ms_scatter, ms_fixup;
+    double ms_init;                /* wall time of taurus_layer_init                    */
+    double ms_index;               /* of which: sampling and chunk-index build (0 when
+                                      the plan already held the index)                  */
+    double ms_gemm, ms_self, ms_scatter, ms_fixup;
     int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
 } taurus_stats;
 
@@ -173,28 +182,33 @@ int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* ds
                      int64_t* row_off, int32_t* col_dst, void* stream);
 
 /*
- * Build the exact chunk index of a graph once, for every exact layer that
- * streams it with source chunks of `chunk` vertices: the propagated in-edges
- * and one self item per vertex, grouped by (source chunk, destination), each
- * vertex's arrival count |N-(v)| + 1, and the list of destination segments
- * that straddle scatter tiles (Sec. 3.3-3.4: the reader streams contiguous
- * vertex ranges; the orchestrator keeps O(|V|) pending counts).  The graph
- * is validated (row_off monotone from 0 to e, col_dst in [0, n), rows
- * strictly ascending, no self loops); an invalid graph is
- * TAURUS_E_INVALID.  The graph arrays must stay valid and unchanged while the
- * plan or any layer using it lives.  Blocks until built.  The plan's device
- * memory is held until the plan and every layer that uses it are destroyed.
+ * A plan holds the per-graph structures that layers over one graph and chunk
+ * size share: the exact chunk index (every in-edge grouped by source chunk
+ * and destination, with each vertex's message count |N-(v)|; Sec. 3.3-3.4:
+ * the reader streams contiguous vertex ranges and the orchestrator keeps
+ * O(|V|) pending counts) for exact layers, and the in-edges grouped by
+ * destination for the fanout sampler of sampled layers.  Each structure is
+ * built by the first layer that needs it (on that layer's stream; the graph
+ * is validated then: row_off monotone from 0 to e, col_dst in [0, n), rows
+ * strictly ascending, no self loops, else TAURUS_E_INVALID) and reused by
+ * later layers.  Creating the plan only records the graph and chunk size
+ * (stream is unused).  The graph arrays must stay valid and unchanged while
+ * the plan or any layer using it lives.  The plan's device memory is held
+ * until the plan and every layer that uses it are destroyed.  Layers that
+ * share a plan may run on different streams; the first use of a structure
+ * must not race with another layer's first use of it from another thread
+ * (the plan serialises the build itself).
  */
 int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, taurus_plan** out);
 
-/* Release a plan (layers still using it keep its index alive).  NULL is ignored. */
+/* Release a plan (layers still using it keep its structures alive).  NULL is ignored. */
 void taurus_plan_destroy(taurus_plan* plan);
 
 /*
  * Create the state of one layer: copies the weights, computes degrees and
- * normalisers, draws the fanout mask (fanout > 0), sets every vertex's
- * pending-message count to |M(v)| + 1 (the self message counts as one
- * arrival) and builds the per-chunk destination index.  *out receives the
+ * normalisers, draws the fanout mask (fanout > 0), builds or takes the
+ * per-chunk destination index, and sets every vertex's pending-message count
+ * to |M(v)| + 1 (the self message counts as one arrival).  *out receives the
  * handle.  Blocks until the index is built.
  */
 int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_layer** out);

@@ -47,7 +47,8 @@ class Stats(ctypes.Structure):
         "n", "e", "messages", "self_terms", "pairs", "completed", "pending_left", "chunks",
         "chunks_pushed", "short_units", "wave_units", "split_segments", "evictions", "reloads",
         "device_bytes")] + [
-        ("hub_message_share", ctypes.c_double), ("ms_init", ctypes.c_double), ("ms_gemm", ctypes.c_double),
+        ("hub_message_share", ctypes.c_double), ("ms_init", ctypes.c_double), ("ms_index", ctypes.c_double),
+        ("ms_gemm", ctypes.c_double),
         ("ms_self", ctypes.c_double), ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),
         ("launches_gemm", ctypes.c_int64), ("launches_self", ctypes.c_int64),
         ("launches_scatter", ctypes.c_int64), ("launches_fixup", ctypes.c_int64)]

@@ -54,8 +54,10 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
 
 
 class Plan:
-    """taurus_plan_create / taurus_plan_destroy: the exact chunk index of a
-    graph for one chunk size, shared by every exact layer over it."""
+    """taurus_plan_create / taurus_plan_destroy: the per-graph structures
+    (exact chunk index, in-edge lists for sampling) for one chunk size,
+    shared by the layers over it and built by the first layer that needs
+    each."""
 
     def __init__(self, n: int, row_off: torch.Tensor, col_dst: torch.Tensor, chunk: int, stream=None):
         self._h = ctypes.c_void_p()
@@ -156,12 +158,11 @@ def run_layers(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, x: torch.Te
     in_dtype, out_dtype, relu, fanout, layer, seed.  Returns (outputs, stats)."""
     h = x
     results, stats = [], []
-    plan = Plan(n, row_off, col_dst, chunk, stream=stream) if any(s.get("fanout", 0) == 0 for s in layers) else None
+    plan = Plan(n, row_off, col_dst, chunk, stream=stream)
     for i, spec in enumerate(layers):
         out = outs[i] if outs is not None else torch.empty(
             (n, spec["d_out"]), dtype=_TORCH_DTYPE[spec.get("out_dtype", N.F32)], device=x.device)
-        L = Layer(n, row_off, col_dst, out=out, chunk=chunk, stream=stream, profile=profile,
-                  plan=plan if spec.get("fanout", 0) == 0 else None, **spec)
+        L = Layer(n, row_off, col_dst, out=out, chunk=chunk, stream=stream, profile=profile, plan=plan, **spec)
         L.push_all(h)
         stats.append(L.finalize())
         L.destroy()

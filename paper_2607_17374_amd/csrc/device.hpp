@@ -1,0 +1,77 @@
+// Device helpers shared by the chunk index and the fanout sampler.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace taurus {
+
+// SplitMix64 finaliser and increment (Steele, Lea and Flood, OOPSLA 2014).
+constexpr uint64_t SM64_GAMMA = 0x9e3779b97f4a7c15ULL;
+
+__host__ __device__ inline uint64_t mix64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+// Sampling rank hash H(seed, 4, layer, v, u): the counter hash chained over
+// the tag and arguments (h = mix64(h + gamma + x) for each), split so that
+// the per-destination prefix H(seed, 4, layer, v) is computed once.
+__host__ __device__ inline uint64_t sample_prefix(uint64_t seed, uint64_t layer, uint64_t v) {
+    uint64_t h = mix64(seed + SM64_GAMMA + 4u);
+    h = mix64(h + SM64_GAMMA + layer);
+    return mix64(h + SM64_GAMMA + v);
+}
+__host__ __device__ inline uint64_t sample_key(uint64_t prefix, uint64_t u) { return mix64(prefix + SM64_GAMMA + u); }
+
+// Row (source) of CSR edge i = lane's edge, for all 64 lanes of a wave whose
+// first edge is i0 = i - lane.  The wave finds the row u0 of i0 with a 64-ary
+// search (every lane probes at once, ~log64(n) dependent loads instead of
+// ~log2(n) per lane), stages row_off[u0+1 .. u0+64] in `ro` (64 entries of
+// LDS owned by the wave), and each lane locates its own edge among those; an
+// edge more than 64 rows past u0 (only after many empty rows) falls back to
+// a binary search of the rest.  All probes stay in [0, n], also for lanes
+// with i >= e and for invalid offsets; the result is in [0, n).  Every lane
+// of the wave must call it (it uses ballots and a wave-level barrier between
+// its LDS writes and reads).
+__device__ inline int64_t wave_edge_row(const int64_t* __restrict__ row_off, int64_t n, int64_t i,
+                                        int64_t* ro) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i0 = i - lane;
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 64) {
+        const int64_t step = (hi - lo + 63) >> 6;
+        const int64_t p = min(lo + (int64_t)(lane + 1) * step, hi);
+        const int k = __popcll(__ballot(row_off[p] <= i0));
+        const int64_t nlo = lo + (int64_t)k * step;
+        hi = min(nlo + step, hi);
+        lo = nlo;
+    }
+    {
+        const int64_t p = lo + lane + 1;
+        const int k = __popcll(__ballot(p <= hi && row_off[p] <= i0));
+        lo += k;
+    }
+    const int64_t u0 = min(lo, n - 1);
+    const int64_t q = u0 + 1 + lane;
+    ro[lane] = q <= n ? row_off[q] : INT64_MAX;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    if (ro[63] <= i) {
+        int64_t a = u0 + 64, z = n;  // largest u in [a, n) with row_off[u] <= i
+        while (z - a > 1) {
+            const int64_t mid = (a + z) >> 1;
+            if (row_off[mid] <= i) a = mid;
+            else z = mid;
+        }
+        return min(a, n - 1);
+    }
+    int c = 0;
+#pragma unroll
+    for (int half = 32; half >= 1; half >>= 1)
+        if (ro[c + half - 1] <= i) c += half;
+    return u0 + c;
+}
+
+}  // namespace taurus

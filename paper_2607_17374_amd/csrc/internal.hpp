@@ -7,7 +7,9 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <chrono>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -130,5 +132,25 @@ struct SortBuffers {
 };
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
                     int bad_bit);
+
+// In-edges grouped by destination, sources ascending (sample.hip): built once
+// per graph for the fanout sampler.  Complete when build_csc returns.
+struct Csc {
+    Arena arena;
+    int64_t* in_off = nullptr;  // [n+1]
+    int32_t* in_src = nullptr;  // [e]
+    double ms_build = 0;
+    explicit Csc(hipStream_t s) : arena(s) {}
+    // may be read from other streams than the one it was built on
+    ~Csc() {
+        (void)hipDeviceSynchronize();
+        arena.set_stream(nullptr);
+        arena.release();
+    }
+};
+std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s);
+// mask (device, ceil(e/64) words) = the fanout-k sample of layer `layer`
+void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer, int k, uint64_t* mask,
+                 hipStream_t s);
 
 }  // namespace taurus

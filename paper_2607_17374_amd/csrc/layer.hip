@@ -35,6 +35,7 @@
 #include <memory>
 #include <mutex>
 
+#include "device.hpp"
 #include "internal.hpp"
 
 namespace taurus {
@@ -44,6 +45,9 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
 void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const float* rscale, float* Y,
               hipStream_t s);
 void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& packed);
+void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
+             float* Y, hipStream_t s);
+void gemm_pack_weights_16(const float* W, int K, int Nc, int dtype, std::vector<uint16_t>& packed);
 const char* last_error_cstr();
 
 constexpr int SC_THREADS = 256;
@@ -86,59 +90,15 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 // Chunk-index items.  CSR edge i (source u = the row containing i) becomes
 // key (chunk(u) << vbits | v), value u - chunk(u)*C; a dropped edge gets
 // chunk = nchunks so it sorts after every kept item.
-//
-// Rows are found without a per-lane binary search (a chain of ~log2 n
-// dependent loads): the wave finds the row u0 of its first edge with a
-// 64-ary search (all lanes probe at once, ~log64 n dependent loads), stages
-// row_off[u0+1 .. u0+64] in LDS, and each lane locates its own edge among
-// those; an edge more than 64 rows past u0 (only after many empty rows)
-// falls back to a binary search of the rest.
 __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
                                                     const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
                                                     int64_t C, int64_t nchunks, int vbits,
                                                     const uint64_t* __restrict__ mask, uint64_t* __restrict__ keys,
                                                     uint32_t* __restrict__ vals, int* __restrict__ bad) {
     __shared__ int64_t ro[4][64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t i0 = i - lane;  // the wave's first edge
-    // largest u0 in [0, n) with row_off[u0] <= i0; probes stay in [0, n]
-    int64_t lo = 0, hi = n;
-    while (hi - lo > 64) {
-        const int64_t step = (hi - lo + 63) >> 6;
-        const int64_t p = min(lo + (int64_t)(lane + 1) * step, hi);
-        const int k = __popcll(__ballot(row_off[p] <= i0));
-        const int64_t nlo = lo + (int64_t)k * step;
-        hi = min(nlo + step, hi);
-        lo = nlo;
-    }
-    {
-        const int64_t p = lo + lane + 1;
-        const int k = __popcll(__ballot(p <= hi && row_off[p] <= i0));
-        lo += k;
-    }
-    const int64_t u0 = min(lo, n - 1);
-    const int64_t q = u0 + 1 + lane;
-    ro[wave][lane] = q <= n ? row_off[q] : INT64_MAX;
-    __syncthreads();
+    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
     if (i >= e) return;
-    // u = u0 + #{j : row_off[u0 + 1 + j] <= i}
-    int64_t u;
-    if (ro[wave][63] <= i) {
-        int64_t a = u0 + 64, z = n;  // largest u in [a, n) with row_off[u] <= i
-        while (z - a > 1) {
-            const int64_t mid = (a + z) >> 1;
-            if (row_off[mid] <= i) a = mid;
-            else z = mid;
-        }
-        u = min(a, n - 1);
-    } else {
-        int c = 0;
-#pragma unroll
-        for (int half = 32; half >= 1; half >>= 1)
-            if (ro[wave][c + half - 1] <= i) c += half;
-        u = u0 + c;
-    }
     const int64_t v = col_dst[i];
     // rows strictly ascending, no self loops (a simple graph)
     if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
@@ -853,7 +813,11 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
 struct taurus_plan {
     taurus_graph g{};
     int64_t chunk = 0;
-    std::shared_ptr<taurus::ChunkIndex> idx;
+    // built by the first layer that needs them, on that layer's stream
+    std::mutex mu;
+    std::shared_ptr<taurus::ChunkIndex> idx;  // exact layers
+    std::shared_ptr<taurus::Csc> csc;         // sampled layers
+    double ms_build = 0;                      // time the plan's structures took to build
 };
 
 struct taurus_layer {
@@ -875,6 +839,7 @@ struct taurus_layer {
     float* carry = nullptr;
     int32_t* carry_cnt = nullptr;
     uint64_t* mask = nullptr;
+    void* wpack_any = nullptr;  // packed weights (fp32 or 16-bit fragments)
     std::vector<uint8_t> pushed;
     int64_t npushed = 0;
     double ms_init = 0, ms_index = 0;
@@ -927,13 +892,16 @@ static void validate_desc(const taurus_layer_desc* d) {
     if (d->d_in <= 0 || d->d_out <= 0 || d->d_in % 4 || d->d_out % 4 || d->d_out > 1024 || d->d_in > 8192)
         fail(TAURUS_E_INVALID, "d_in=%d d_out=%d: widths must be positive multiples of 4, d_out <= 1024",
              d->d_in, d->d_out);
-    if (d->in_dtype != TAURUS_F32)
-        fail(TAURUS_E_INVALID, "in_dtype %d: only fp32 layer inputs are supported by this build", d->in_dtype);
+    if (d->in_dtype < TAURUS_F32 || d->in_dtype > TAURUS_F16) fail(TAURUS_E_INVALID, "in_dtype %d", d->in_dtype);
+    if (d->in_dtype != TAURUS_F32 && d->d_in % 8)
+        fail(TAURUS_E_INVALID, "d_in=%d: 16-bit inputs need a multiple of 8", d->d_in);
     if (d->out_dtype < 0 || d->out_dtype > 2) fail(TAURUS_E_INVALID, "out_dtype %d", d->out_dtype);
     if (!d->weight) fail(TAURUS_E_INVALID, "weight is null");
     if (d->chunk <= 0 || d->chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)d->chunk);
-    if (d->fanout < 0) fail(TAURUS_E_INVALID, "fanout %d", d->fanout);
-    if (d->fanout > 0) fail(TAURUS_E_INVALID, "fanout sampling is not supported by this build");
+    if (d->fanout < 0 || d->fanout > 64) fail(TAURUS_E_INVALID, "fanout %d outside [0, 64]", d->fanout);
+    if (d->fanout > 0 && d->agg != TAURUS_SAGE_MEAN)
+        fail(TAURUS_E_INVALID, "fanout sampling is defined for GraphSAGE-mean layers only");
+    if (d->fanout > 0 && d->layer < 1) fail(TAURUS_E_INVALID, "layer %d: sampled layers are numbered from 1", d->layer);
     if (!d->out) fail(TAURUS_E_INVALID, "out is null");
     if (d->out_on_host != 0) fail(TAURUS_E_INVALID, "out_on_host=%d is not supported by this build", d->out_on_host);
     if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
@@ -958,17 +926,40 @@ static void layer_init(taurus_layer* L) {
     L->shape.max_blocks = scatter_resident_blocks(L->shape) * std::max(1, env_int("TAURUS_SCATTER_WAVES", 1));
     const int T = 256;
 
-    // chunk index: shared from the plan for exact layers, else built here
-    const taurus_plan* plan = d.plan;
-    if (plan) {
-        if (!same_graph(plan->g, g) || plan->chunk != C)
-            fail(TAURUS_E_INVALID, "plan was built for another graph or chunk size");
+    // chunk index: exact layers share the plan's (built here if it is the
+    // first user); a sampled layer draws its mask (from the plan's CSC) and
+    // builds its own index of the kept edges
+    taurus_plan* plan = const_cast<taurus_plan*>(d.plan);
+    if (plan && (!same_graph(plan->g, g) || plan->chunk != C))
+        fail(TAURUS_E_INVALID, "plan was built for another graph or chunk size");
+    const auto t_index = std::chrono::steady_clock::now();
+    if (d.fanout > 0) {
+        std::shared_ptr<Csc> csc;
+        if (plan) {
+            std::lock_guard<std::mutex> lock(plan->mu);
+            if (!plan->csc) {
+                plan->csc = build_csc(g, s);
+                plan->ms_build += plan->csc->ms_build;
+            }
+            csc = plan->csc;
+        } else {
+            csc = build_csc(g, s);
+        }
+        L->mask = L->arena.alloc<uint64_t>(std::max<int64_t>(1, ceil_div(g.e, 64)), "fanout mask");
+        sample_mask(g, *csc, d.seed, d.layer, d.fanout, L->mask, s);
+        L->idx = build_index(g, C, L->mask, s, 0);
+    } else if (plan) {
+        std::lock_guard<std::mutex> lock(plan->mu);
+        if (!plan->idx) {
+            plan->idx = build_index(g, C, nullptr, s, 0);
+            plan->ms_build += plan->idx->ms_build;
+        }
         L->idx = plan->idx;
         L->idx->wait_ready(s);
     } else {
-        L->idx = build_index(g, C, L->mask, s, 0);
-        L->ms_index = L->idx->ms_build;
+        L->idx = build_index(g, C, nullptr, s, 0);
     }
+    L->ms_index = ms_since(t_index);
     const ChunkIndex& idx = *L->idx;
 
     L->cnt = L->arena.alloc<int2>(n, "pending counts");
@@ -982,16 +973,27 @@ static void layer_init(taurus_layer* L) {
 
     // packed weights and bias, one transfer through pinned staging (the
     // synchronisation at the end keeps the staging buffer until it is done)
-    std::vector<float> packed;
-    gemm_pack_weights_f32(d.weight, d.d_in, L->ncols, packed);
-    const size_t wfloats = (packed.size() + 63) / 64 * 64;
-    const size_t pbytes = (wfloats + (size_t)L->d_o) * 4;
-    float* stage = static_cast<float*>(pinned_staging(pbytes));
-    std::copy(packed.begin(), packed.end(), stage);
-    for (int j = 0; j < L->d_o; j++) stage[wfloats + (size_t)j] = d.bias ? d.bias[j] : 0.0f;
-    L->wpack = L->arena.alloc<float>((int64_t)(pbytes / 4), "packed weights and bias");
-    L->bias = L->wpack + wfloats;
-    TAURUS_HIP(hipMemcpyAsync(L->wpack, stage, pbytes, hipMemcpyHostToDevice, s));
+    std::vector<float> packed32;
+    std::vector<uint16_t> packed16;
+    size_t wbytes = 0;
+    if (d.in_dtype == TAURUS_F32) {
+        gemm_pack_weights_f32(d.weight, d.d_in, L->ncols, packed32);
+        wbytes = packed32.size() * 4;
+    } else {
+        gemm_pack_weights_16(d.weight, d.d_in, L->ncols, d.in_dtype, packed16);
+        wbytes = packed16.size() * 2;
+    }
+    wbytes = (wbytes + 255) / 256 * 256;
+    const size_t pbytes = wbytes + (size_t)L->d_o * 4;
+    char* stage = static_cast<char*>(pinned_staging(pbytes));
+    if (!packed32.empty()) std::memcpy(stage, packed32.data(), packed32.size() * 4);
+    if (!packed16.empty()) std::memcpy(stage, packed16.data(), packed16.size() * 2);
+    float* sbias = reinterpret_cast<float*>(stage + wbytes);
+    for (int j = 0; j < L->d_o; j++) sbias[j] = d.bias ? d.bias[j] : 0.0f;
+    L->wpack_any = L->arena.alloc_bytes((int64_t)pbytes, "packed weights and bias");
+    L->wpack = static_cast<float*>(L->wpack_any);
+    L->bias = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + wbytes);
+    TAURUS_HIP(hipMemcpyAsync(L->wpack_any, stage, pbytes, hipMemcpyHostToDevice, s));
 
     // working buffers
     L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
@@ -1032,8 +1034,12 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     }
     L->pushed[(size_t)k] = 1;
     L->npushed++;
-    gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, L->n_out ? L->n_out + b : nullptr,
-             L->Y, s);
+    const float* rscale = L->n_out ? L->n_out + b : nullptr;
+    if (L->d.in_dtype == TAURUS_F32)
+        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, L->Y, s);
+    else
+        gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
+                static_cast<const uint16_t*>(L->wpack_any), L->ncols, rscale, L->Y, s);
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
     ScatterParams p;
     p.Y = L->Y;
@@ -1098,6 +1104,7 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         st->split_segments = idx.n_list[NCLASS + 1];
         st->device_bytes = L->arena.peak() + (L->ms_index > 0 ? idx.arena.peak() : 0);
         st->ms_init = L->ms_init;
+        st->ms_index = L->ms_index;
         for (int64_t k = 0; k < L->nchunks && !L->events.empty(); k++) {
             if (!L->pushed[(size_t)k]) continue;
             hipEvent_t* ev = &L->events[(size_t)k * EV_PER_CHUNK];
@@ -1161,7 +1168,7 @@ int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, tauru
         auto P = std::make_unique<taurus_plan>();
         P->g = *g;
         P->chunk = chunk;
-        P->idx = build_index(*g, chunk, nullptr, static_cast<hipStream_t>(stream), 0);
+        (void)stream;  // structures are built by the first layer that uses them, on its stream
         *out = P.release();
         return TAURUS_OK;
     } catch (const Failure& f) {

@@ -83,7 +83,8 @@ def gpu_graph(w: WL.Workload, src=None, dst=None, device="cuda"):
 def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, profile=False, stream=None,
               use_plan=True):
     """Run every layer of w through the C ABI; returns ([outputs], [stats]).
-    Exact layers share one plan (chunk index) unless use_plan is False."""
+    The layers share one plan (exact chunk index, in-edge lists for sampling)
+    unless use_plan is False."""
     import torch
     import paper_2607_17374_amd as T
     from paper_2607_17374_amd.api import torch_dtype
@@ -96,12 +97,11 @@ def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, 
     h = X
     outs, stats = [], []
     specs = layer_specs(w)
-    plan = T.Plan(w.n, row_off, col_dst, chunk, stream=stream) if use_plan and any(
-        s["fanout"] == 0 for s in specs) else None
+    plan = T.Plan(w.n, row_off, col_dst, chunk, stream=stream) if use_plan else None
     for spec in specs:
         out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=X.device)
         L = T.Layer(w.n, row_off, col_dst, out=out, chunk=chunk, profile=profile, stream=stream,
-                    plan=plan if spec["fanout"] == 0 else None, **spec)
+                    plan=plan, **spec)
         L.push_all(h, order=order)
         stats.append(L.finalize())
         L.destroy()
