@@ -182,6 +182,39 @@ int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* ds
                      int64_t* row_off, int32_t* col_dst, void* stream);
 
 /*
+ * Degree/BFS vertex ordering (Sec. 3.8: a topology-aware order in which a
+ * destination's sources receive nearby ranks, shrinking the span between
+ * its first and last message).  new_of_old (device int32[n], written) is
+ * the visit order of a breadth-first search over in-edges: roots are taken
+ * in (in-degree descending, ID ascending) order, every root not yet visited
+ * starts a new search, and a dequeued vertex appends its unvisited
+ * in-neighbours in the same order.  The order is unique.  The graph is
+ * validated (TAURUS_E_INVALID).  Returns after the work completed.
+ */
+int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream);
+
+/*
+ * CSR of the relabelled graph: edge (u, v) becomes (new_of_old[u],
+ * new_of_old[v]).  row_off int64[n+1] and col_dst int32[e] are caller-owned
+ * device memory, written in canonical form (as taurus_build_csr).
+ * new_of_old must be a permutation of [0, n) (else TAURUS_E_INVALID).
+ * Returns after the work completed.
+ */
+int taurus_relabel_graph(const taurus_graph* g, const int32_t* new_of_old, int64_t* row_off, int32_t* col_dst,
+                         void* stream);
+
+/*
+ * Move rows of row_bytes bytes (a multiple of 4) between vertex numberings:
+ * inverse = 0: out[new_of_old[v]] = in[v] (features into the new order);
+ * inverse = 1: out[v] = in[new_of_old[v]] (outputs back to the old order).
+ * in, out: device [n][row_bytes], not overlapping.  new_of_old must be a
+ * permutation (checked; TAURUS_E_INVALID).  Returns after the check; the
+ * copy itself is asynchronous on `stream`.
+ */
+int taurus_permute_rows(const void* in, void* out, int64_t n, int64_t row_bytes, const int32_t* new_of_old,
+                        int32_t inverse, void* stream);
+
+/*
  * A plan holds the per-graph structures that layers over one graph and chunk
  * size share: the exact chunk index (every in-edge grouped by source chunk
  * and destination, with each vertex's message count |N-(v)|; Sec. 3.3-3.4:

@@ -53,6 +53,45 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
     return row_off, col_dst
 
 
+def _graph(n: int, row_off: torch.Tensor, col_dst: torch.Tensor) -> N.Graph:
+    e = col_dst.numel()
+    return N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"), _dev_ptr(col_dst, torch.int32, "col_dst") if e else None)
+
+
+def reorder(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, stream=None) -> torch.Tensor:
+    """taurus_reorder: degree/BFS order, new_of_old int32[n] on the device."""
+    g = _graph(n, row_off, col_dst)
+    out = torch.empty(n, dtype=torch.int32, device=row_off.device)
+    N.check(N.lib().taurus_reorder(ctypes.byref(g), out.data_ptr(), _stream_ptr(stream)), "taurus_reorder")
+    return out
+
+
+def relabel_graph(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, new_of_old: torch.Tensor, stream=None):
+    """taurus_relabel_graph: CSR of the graph with vertex v renamed new_of_old[v]."""
+    g = _graph(n, row_off, col_dst)
+    e = col_dst.numel()
+    r2 = torch.empty(n + 1, dtype=torch.int64, device=row_off.device)
+    c2 = torch.empty(max(e, 1), dtype=torch.int32, device=row_off.device)[:e]
+    N.check(N.lib().taurus_relabel_graph(ctypes.byref(g), _dev_ptr(new_of_old, torch.int32, "new_of_old"),
+                                         r2.data_ptr(), c2.data_ptr() if e else None, _stream_ptr(stream)),
+            "taurus_relabel_graph")
+    return r2, c2
+
+
+def permute_rows(x: torch.Tensor, new_of_old: torch.Tensor, inverse: bool = False, stream=None) -> torch.Tensor:
+    """taurus_permute_rows: rows of x [n][...] into the new numbering
+    (out[new_of_old[v]] = x[v]), or back (inverse: out[v] = x[new_of_old[v]])."""
+    if not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous device tensor")
+    n = x.shape[0]
+    out = torch.empty_like(x)
+    row_bytes = x[0].numel() * x.element_size() if n else 0
+    N.check(N.lib().taurus_permute_rows(x.data_ptr(), out.data_ptr(), n, row_bytes,
+                                        _dev_ptr(new_of_old, torch.int32, "new_of_old"), int(inverse),
+                                        _stream_ptr(stream)), "taurus_permute_rows")
+    return out
+
+
 class Plan:
     """taurus_plan_create / taurus_plan_destroy: the per-graph structures
     (exact chunk index, in-edge lists for sampling) for one chunk size,

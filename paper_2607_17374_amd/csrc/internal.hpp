@@ -149,6 +149,8 @@ struct Csc {
     }
 };
 std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s);
+// row_off monotone from 0 to e and col_dst in [0, n), else TAURUS_E_INVALID (synchronises)
+void validate_csr(const taurus_graph& g, hipStream_t s);
 // mask (device, ceil(e/64) words) = the fanout-k sample of layer `layer`
 void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer, int k, uint64_t* mask,
                  hipStream_t s);

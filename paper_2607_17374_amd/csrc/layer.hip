@@ -1123,6 +1123,26 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
     return left ? TAURUS_E_INCOMPLETE : TAURUS_OK;
 }
 
+int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s);
+int relabel_impl(const taurus_graph& g, const int32_t* new_of_old, int64_t* row_off, int32_t* col_dst,
+                 hipStream_t s);
+int permute_rows_impl(const void* in, void* out, int64_t n, int64_t row_bytes, const int32_t* new_of_old,
+                      int inverse, hipStream_t s);
+
+// Runs an entry point's body: library failures become their status, any
+// other exception TAURUS_E_DEVICE; nothing crosses the C boundary.
+template <typename F>
+static int guarded(F&& f) {
+    try {
+        return f();
+    } catch (const Failure& x) {
+        return x.status;
+    } catch (const std::exception& x) {
+        set_error("internal error: %s", x.what());
+        return TAURUS_E_DEVICE;
+    }
+}
+
 }  // namespace taurus
 
 // ------------------------------------------------------------------ C ABI --
@@ -1180,6 +1200,36 @@ int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, tauru
 }
 
 void taurus_plan_destroy(taurus_plan* P) { delete P; }
+
+int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream) {
+    return guarded([&] {
+        check_graph_args(g);
+        if (!new_of_old) fail(TAURUS_E_INVALID, "new_of_old is null");
+        return reorder_impl(*g, new_of_old, static_cast<hipStream_t>(stream));
+    });
+}
+
+int taurus_relabel_graph(const taurus_graph* g, const int32_t* new_of_old, int64_t* row_off, int32_t* col_dst,
+                         void* stream) {
+    return guarded([&] {
+        check_graph_args(g);
+        if (!new_of_old || !row_off || (g->e > 0 && !col_dst)) fail(TAURUS_E_INVALID, "null output or permutation");
+        return relabel_impl(*g, new_of_old, row_off, col_dst, static_cast<hipStream_t>(stream));
+    });
+}
+
+int taurus_permute_rows(const void* in, void* out, int64_t n, int64_t row_bytes, const int32_t* new_of_old,
+                        int32_t inverse, void* stream) {
+    return guarded([&] {
+        if (n <= 0 || n >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "n=%lld out of range", (long long)n);
+        if (row_bytes <= 0 || row_bytes % 4) fail(TAURUS_E_INVALID, "row_bytes=%lld: a positive multiple of 4",
+                                                  (long long)row_bytes);
+        if (!in || !out || !new_of_old) fail(TAURUS_E_INVALID, "null pointer");
+        if (in == out) fail(TAURUS_E_INVALID, "in and out must not overlap");
+        if (inverse != 0 && inverse != 1) fail(TAURUS_E_INVALID, "inverse=%d", inverse);
+        return permute_rows_impl(in, out, n, row_bytes, new_of_old, inverse, static_cast<hipStream_t>(stream));
+    });
+}
 
 int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_layer** out) {
     if (!out) {

@@ -35,6 +35,20 @@ __global__ void k_validate_csr(const int64_t* __restrict__ row_off, const int32_
     }
 }
 
+void validate_csr(const taurus_graph& g, hipStream_t s) {
+    Arena tmp(s);
+    int* bad = tmp.alloc<int>(1, "graph flag");
+    fill_i32(bad, 1, 0, s);
+    k_validate_csr<<<(unsigned)ceil_div(std::max(std::max(g.n, g.e), (int64_t)1), 256), 256, 0, s>>>(
+        g.row_off, g.col_dst, g.n, g.e, bad);
+    TAURUS_CHECK_LAUNCH();
+    int hbad = 0;
+    Readback rb;
+    rb.add(&hbad, bad, 1);
+    rb.run(s);
+    if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
+}
+
 // CSR edge i -> sort key v, value u; in-degree counts
 __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
@@ -55,18 +69,11 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
     auto c = std::make_shared<Csc>(s);
     const int64_t n = g.n, e = g.e;
     const int T = 256;
+    validate_csr(g, s);
     Arena tmp(s);
-    int* bad = tmp.alloc<int>(1, "graph flag");
+    int* bad = tmp.alloc<int>(1, "sort flag");
     fill_i32(bad, 1, 0, s);
-    k_validate_csr<<<(unsigned)ceil_div(std::max(n, e), T), T, 0, s>>>(g.row_off, g.col_dst, n, e, bad);
-    TAURUS_CHECK_LAUNCH();
     int hbad = 0;
-    {
-        Readback rb;
-        rb.add(&hbad, bad, 1);
-        rb.run(s);
-    }
-    if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
     int32_t* deg = tmp.alloc<int32_t>(n, "in-degrees");
     fill_i32(deg, n, 0, s);
     c->in_off = c->arena.alloc<int64_t>(n + 1, "in-edge offsets");
