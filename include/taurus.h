@@ -95,15 +95,27 @@ typedef struct {
  *   seed         sampling seed.
  *   chunk        source-chunk size C in vertices (> 0).  Chunk j covers
  *                sources [j*C, min((j+1)*C, n)).
- *   hbm_budget   bytes of device memory the library may allocate for this
- *                layer (0 = unlimited); init fails with TAURUS_E_BUDGET if
- *                the layer's structures do not fit.
- *   hub_fraction fraction of vertices, by in-degree, whose accumulators stay
- *                resident; only meaningful with an hbm_budget (reserved).
+ *   hbm_budget   bytes of device memory the library may hold for this layer
+ *                (its own buffers plus the chunk index it uses; 0 =
+ *                unlimited).  When the dense accumulators [n][d_out] fp32 do
+ *                not fit, they live in a pool of rows: hubs stay resident,
+ *                other destinations take rows while they are pending, and
+ *                when a chunk's destinations find too few free rows the
+ *                pending vertices with the fewest outstanding messages (then
+ *                lowest ID) that the chunk does not touch are evicted to a
+ *                pinned host store and reloaded before their next message
+ *                (Sec. 3.5).  Results are the same as in core.  Init fails
+ *                with TAURUS_E_BUDGET if the fixed structures, the hubs and
+ *                one chunk's destinations cannot fit.
+ *   hub_fraction fraction in [0, 1] of vertices, by message count (ties by
+ *                lower ID), whose accumulators stay resident for the whole
+ *                layer when the pool is in use (Sec. 3.5.1).
  *   out          caller-owned [n][d_out] array of out_dtype receiving the
  *                layer output; each row is written exactly once, when its
  *                vertex completes.  Device memory unless out_on_host = 1.
- *   out_on_host  0: out is device memory (only value supported now).
+ *   out_on_host  0: out is device memory; 1: out is pinned host memory
+ *                (allocated with hipHostMalloc) written by the kernels over
+ *                the host link as vertices complete.
  *   stream       hipStream_t on which all work of this layer is enqueued
  *                (NULL = the default stream).
  *   profile      1: time every kernel of the layer with HIP events; the
@@ -148,6 +160,8 @@ typedef struct {
     int64_t wave_units;            /* pieces of longer segments (one wave each)         */
     int64_t split_segments;        /* hub segments cut into several pieces              */
     int64_t evictions, reloads;    /* accumulator rows moved to/from host (0 in core)   */
+    int64_t h2d_bytes, d2h_bytes;  /* host-link bytes: host chunks and reloads in;
+                                      evictions and host-resident output rows out       */
     int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
     double hub_message_share;      /* share of messages landing on resident hubs        */
     /* milliseconds, HIP-event timed when desc.profile = 1 (else 0) */
@@ -252,9 +266,11 @@ int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_
  * destination whose last message arrives.  [src_begin, src_end) must be a
  * whole chunk: src_begin = j*chunk, src_end = min(src_begin + chunk, n).
  * x points at the chunk's rows (row src_begin first), row-major
- * [src_end - src_begin][d_in] of in_dtype; device memory if x_on_host = 0
- * (the only value supported now).  x must stay valid and unchanged until
- * the next call on this handle returns.  Chunks may be pushed in any order;
+ * [src_end - src_begin][d_in] of in_dtype: device memory if x_on_host = 0,
+ * pinned host memory if x_on_host = 1 (copied on the layer's own copy
+ * stream into a device staging buffer, overlapping the previous chunk's
+ * compute; Sec. 3.3).  x must stay valid and unchanged until the next call
+ * on this handle returns.  Chunks may be pushed in any order;
  * each exactly once (a repeat returns TAURUS_E_STATE).  Asynchronous on the
  * layer's stream.
  */

@@ -46,7 +46,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int64) for name in (
         "n", "e", "messages", "self_terms", "pairs", "completed", "pending_left", "chunks",
         "chunks_pushed", "short_units", "wave_units", "split_segments", "evictions", "reloads",
-        "device_bytes")] + [
+        "h2d_bytes", "d2h_bytes", "device_bytes")] + [
         ("hub_message_share", ctypes.c_double), ("ms_init", ctypes.c_double), ("ms_index", ctypes.c_double),
         ("ms_gemm", ctypes.c_double),
         ("ms_self", ctypes.c_double), ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),

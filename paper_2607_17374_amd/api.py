@@ -37,6 +37,19 @@ def _dev_ptr(t: torch.Tensor, dtype: torch.dtype, what: str) -> int:
     return t.data_ptr()
 
 
+def _buf_ptr(t: torch.Tensor, dtype: torch.dtype, what: str):
+    """(pointer, on_host) of a device tensor or of a pinned host tensor."""
+    if t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if t.is_cuda:
+        return t.data_ptr(), 0
+    if not t.is_pinned():
+        raise ValueError(f"{what} on the host must be pinned memory")
+    return t.data_ptr(), 1
+
+
 def hash_u64(seed: int, tag: int, *args: int) -> int:
     a = (ctypes.c_uint64 * max(1, len(args)))(*args)
     return int(N.lib().taurus_hash(seed & (2**64 - 1), tag, len(args), ctypes.cast(a, ctypes.c_void_p)))
@@ -138,21 +151,23 @@ class Layer:
         self._w = np.ascontiguousarray(weight_cat, dtype=np.float32)
         self._b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
         self.out = out
+        out_ptr, out_on_host = _buf_ptr(out, _TORCH_DTYPE[out_dtype], "out")
         self.n, self.d_in, self.d_out, self.chunk, self.in_dtype = n, d_in, d_out, chunk, in_dtype
         self.desc = N.LayerDesc(
             agg=agg, d_in=d_in, d_out=d_out, in_dtype=in_dtype, out_dtype=out_dtype, relu=int(relu),
             weight=self._w.ctypes.data, bias=None if self._b is None else self._b.ctypes.data,
             fanout=fanout, layer=layer, seed=seed & (2**64 - 1), chunk=chunk, hbm_budget=hbm_budget,
-            hub_fraction=hub_fraction, out=_dev_ptr(out, _TORCH_DTYPE[out_dtype], "out"), out_on_host=0,
+            hub_fraction=hub_fraction, out=out_ptr, out_on_host=out_on_host,
             stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None)
         self._keep = (row_off, col_dst, plan)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")
 
     def push_chunk(self, begin: int, end: int, x: torch.Tensor) -> None:
-        """taurus_push_chunk with x = rows [begin, end) on the device."""
-        ptr = _dev_ptr(x, _TORCH_DTYPE[self.in_dtype], "x")
-        N.check(N.lib().taurus_push_chunk(self._h, begin, end, ptr, 0), "taurus_push_chunk")
+        """taurus_push_chunk with x = rows [begin, end), on the device or in
+        pinned host memory (then it must stay unchanged until the next call)."""
+        ptr, on_host = _buf_ptr(x, _TORCH_DTYPE[self.in_dtype], "x")
+        N.check(N.lib().taurus_push_chunk(self._h, begin, end, ptr, on_host), "taurus_push_chunk")
 
     def push_all(self, x: torch.Tensor, order: Optional[Sequence[int]] = None) -> None:
         """Stream every chunk of the full input x [n][d_in] (vertex order by default)."""

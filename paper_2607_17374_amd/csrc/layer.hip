@@ -37,6 +37,7 @@
 
 #include "device.hpp"
 #include "internal.hpp"
+#include "resident.hpp"
 
 namespace taurus {
 
@@ -242,7 +243,8 @@ struct ScatterParams {
     int self_col;          // column offset of the self half (GraphSAGE) or 0 (GCN)
     const int32_t* src;    // chunk items: local source row
     int2* cnt;             // {pending, expected}
-    float* acc;            // [n][d_o] fp32 accumulators
+    float* acc;            // fp32 accumulator rows, d_o floats each
+    const int32_t* slot;   // accumulator row of each vertex (residency pool), or null: row v
     int d_o;
     int agg;               // 0 GraphSAGE-mean, 1 GCN
     int relu;
@@ -294,6 +296,10 @@ __device__ inline void store_out4(void* out, int dtype, int64_t idx, float4 z) {
     }
 }
 
+__device__ inline float* acc_row(const ScatterParams& p, int v) {
+    return p.acc + (int64_t)(p.slot ? p.slot[v] : v) * p.d_o;
+}
+
 __device__ inline float seg_scale(int agg, int expect) {
     // GraphSAGE-mean: 1/|M(v)| (|M(v)| = expect - 1); GCN: sources are pre-scaled
     return agg == 0 ? (expect > 1 ? 1.0f / (float)(expect - 1) : 0.0f) : 1.0f;
@@ -307,7 +313,7 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
                                    int lane, const float4 (&pre)[VEC], bool have_pre) {
     const int left = pe.x - count;
     const bool fresh = pe.x == pe.y;  // nothing accumulated yet: acc[v] is logically zero
-    float* arow = p.acc + (int64_t)v * p.d_o;
+    float* arow = acc_row(p, v);
     float4 t[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; j++) {
@@ -346,7 +352,7 @@ __device__ inline void prefetch_acc(const ScatterParams& p, int v, int lane, flo
 #pragma unroll
     for (int j = 0; j < VEC; j++) {
         const int col = (j * G + lane) * 4;
-        pre[j] = col < p.d_o ? *reinterpret_cast<const float4*>(p.acc + (int64_t)v * p.d_o + col) : f4_zero();
+        pre[j] = col < p.d_o ? *reinterpret_cast<const float4*>(acc_row(p, v) + col) : f4_zero();
     }
 }
 
@@ -840,6 +846,14 @@ struct taurus_layer {
     int32_t* carry_cnt = nullptr;
     uint64_t* mask = nullptr;
     void* wpack_any = nullptr;  // packed weights (fp32 or 16-bit fragments)
+    void* out_dev = nullptr;    // desc.out as kernels address it
+    std::unique_ptr<taurus::Residency> res;  // accumulator pool under a budget (null: dense rows)
+    // host-resident chunks: two device staging buffers filled on a copy stream
+    hipStream_t copy_stream = nullptr;
+    void* stage[2] = {nullptr, nullptr};
+    hipEvent_t h2d_done[2] = {nullptr, nullptr}, gemm_done[2] = {nullptr, nullptr};
+    bool stage_used[2] = {false, false};
+    int64_t host_pushes = 0, h2d_bytes = 0;
     std::vector<uint8_t> pushed;
     int64_t npushed = 0;
     double ms_init = 0, ms_index = 0;
@@ -882,6 +896,14 @@ static void timing_event_release(hipEvent_t ev) {
 
 taurus_layer::~taurus_layer() {
     for (auto ev : events) taurus::timing_event_release(ev);
+    if (copy_stream) {
+        (void)hipStreamSynchronize(copy_stream);
+        for (int i = 0; i < 2; i++) {
+            if (h2d_done[i]) (void)hipEventDestroy(h2d_done[i]);
+            if (gemm_done[i]) (void)hipEventDestroy(gemm_done[i]);
+        }
+        (void)hipStreamDestroy(copy_stream);
+    }
 }
 
 namespace taurus {
@@ -903,7 +925,8 @@ static void validate_desc(const taurus_layer_desc* d) {
         fail(TAURUS_E_INVALID, "fanout sampling is defined for GraphSAGE-mean layers only");
     if (d->fanout > 0 && d->layer < 1) fail(TAURUS_E_INVALID, "layer %d: sampled layers are numbered from 1", d->layer);
     if (!d->out) fail(TAURUS_E_INVALID, "out is null");
-    if (d->out_on_host != 0) fail(TAURUS_E_INVALID, "out_on_host=%d is not supported by this build", d->out_on_host);
+    if (d->out_on_host != 0 && d->out_on_host != 1) fail(TAURUS_E_INVALID, "out_on_host=%d", d->out_on_host);
+    if (d->hub_fraction < 0.0 || d->hub_fraction > 1.0) fail(TAURUS_E_INVALID, "hub_fraction %g", d->hub_fraction);
     if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
 }
 
@@ -995,13 +1018,53 @@ static void layer_init(taurus_layer* L) {
     L->bias = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + wbytes);
     TAURUS_HIP(hipMemcpyAsync(L->wpack_any, stage, pbytes, hipMemcpyHostToDevice, s));
 
+    // output as kernels address it: device memory, or pinned host memory
+    // mapped into the device's address space
+    if (d.out_on_host) {
+        if (hipHostGetDevicePointer(&L->out_dev, d.out, 0) != hipSuccess) {
+            (void)hipGetLastError();
+            fail(TAURUS_E_INVALID, "out_on_host = 1 but out is not pinned host memory");
+        }
+    } else {
+        L->out_dev = d.out;
+    }
+
     // working buffers
-    L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
     L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
-    const int64_t slots = std::max<int64_t>(1, idx.max_long_per_chunk);
-    L->carry = L->arena.alloc<float>(slots * L->d_o, "hub piece carries");
-    L->carry_cnt = L->arena.alloc<int32_t>(slots, "hub piece counts");
+    const int64_t carry_rows = std::max<int64_t>(1, idx.max_long_per_chunk);
+    L->carry = L->arena.alloc<float>(carry_rows * L->d_o, "hub piece carries");
+    L->carry_cnt = L->arena.alloc<int32_t>(carry_rows, "hub piece counts");
     L->pushed.assign((size_t)L->nchunks, 0);
+
+    // Accumulators: dense rows [n][d_out] when they fit the budget; else a
+    // pool of slots with resident hubs and eviction to pinned host memory.
+    const int64_t row_bytes = (int64_t)L->d_o * 4;
+    const int64_t index_bytes = L->idx->arena.bytes();
+    const int64_t dense = n * row_bytes;
+    if (d.hbm_budget == 0 || L->arena.bytes() + index_bytes + dense + (dense >> 3) <= d.hbm_budget) {
+        L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
+    } else {
+        const int64_t staging = 2 * std::min(C, n) * (int64_t)d.d_in * (d.in_dtype == TAURUS_F32 ? 4 : 2) * 9 / 8;
+        const int64_t avail =
+            d.hbm_budget - L->arena.bytes() - index_bytes - Residency::fixed_bytes(n) * 9 / 8 - staging;
+        const int64_t S = std::min<int64_t>(n, std::max<int64_t>(0, avail) * 8 / 9 / (row_bytes + 4));
+        const int64_t H = (int64_t)std::ceil(d.hub_fraction * (double)n);
+        int64_t max_dc = 0;
+        for (int64_t k = 0; k < L->nchunks; k++) {
+            int64_t t = std::min(C, n - k * C);
+            for (int l = 0; l <= NCLASS; l++) t += idx.list_count(l, k);
+            max_dc = std::max(max_dc, t);
+        }
+        if (S < H + std::min(max_dc, n - H))
+            fail(TAURUS_E_BUDGET,
+                 "budget %lld leaves %lld accumulator slots; %lld hubs plus one chunk's %lld destinations need more",
+                 (long long)d.hbm_budget, (long long)S, (long long)H, (long long)max_dc);
+        L->res = std::make_unique<Residency>(s, n, L->d_o, S, H, idx.m, idx.kept);
+        const int64_t total = L->arena.bytes() + index_bytes + L->res->arena.bytes();
+        if (total > d.hbm_budget)
+            fail(TAURUS_E_BUDGET, "residency structures take %lld bytes, above the budget %lld", (long long)total,
+                 (long long)d.hbm_budget);
+    }
     if (d.profile) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
@@ -1016,17 +1079,51 @@ static bool chunk_has_units(const ChunkIndex& idx, int64_t k) {
     return false;
 }
 
+// Host-resident chunk (pinned): copy it on the layer's copy stream into one
+// of two device staging buffers while the previous chunk computes.  A
+// buffer is refilled only after the transform that read it; the caller's x
+// must stay valid until the next call returns, so the previous chunk's copy
+// is waited for here.
+static const void* stage_host_chunk(taurus_layer* L, const void* x, int64_t rows) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, x) != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        fail(TAURUS_E_INVALID, "x_on_host = 1 but x is not pinned host memory");
+    }
+    const size_t elem = L->d.in_dtype == TAURUS_F32 ? 4 : 2;
+    const size_t bytes = (size_t)rows * (size_t)L->d.d_in * elem;
+    if (!L->copy_stream) {
+        TAURUS_HIP(hipStreamCreateWithFlags(&L->copy_stream, hipStreamNonBlocking));
+        for (int i = 0; i < 2; i++) {
+            L->stage[i] = L->arena.alloc_bytes((int64_t)(std::min(L->C, L->n) * L->d.d_in * elem), "chunk staging");
+            TAURUS_HIP(hipEventCreateWithFlags(&L->h2d_done[i], hipEventDisableTiming));
+            TAURUS_HIP(hipEventCreateWithFlags(&L->gemm_done[i], hipEventDisableTiming));
+        }
+    }
+    const int prev = (int)((L->host_pushes + 1) & 1), cur = (int)(L->host_pushes & 1);
+    if (L->stage_used[prev]) TAURUS_HIP(hipEventSynchronize(L->h2d_done[prev]));
+    if (L->stage_used[cur]) TAURUS_HIP(hipStreamWaitEvent(L->copy_stream, L->gemm_done[cur], 0));
+    TAURUS_HIP(hipMemcpyAsync(L->stage[cur], x, bytes, hipMemcpyHostToDevice, L->copy_stream));
+    TAURUS_HIP(hipEventRecord(L->h2d_done[cur], L->copy_stream));
+    TAURUS_HIP(hipStreamWaitEvent(L->s, L->h2d_done[cur], 0));
+    L->stage_used[cur] = true;
+    L->host_pushes++;
+    L->h2d_bytes += (int64_t)bytes;
+    return L->stage[cur];
+}
+
 static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int32_t x_on_host) {
     if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
     if (b < 0 || e > L->n || b >= e || b % L->C != 0 || e != std::min(b + L->C, L->n))
         fail(TAURUS_E_INVALID, "chunk [%lld, %lld) is not a whole chunk of size %lld",
              (long long)b, (long long)e, (long long)L->C);
     if (!x) fail(TAURUS_E_INVALID, "x is null");
-    if (x_on_host != 0) fail(TAURUS_E_INVALID, "host-resident chunks are not supported by this build");
+    if (x_on_host != 0 && x_on_host != 1) fail(TAURUS_E_INVALID, "x_on_host=%d", x_on_host);
     const int64_t k = b / L->C;
     if (L->pushed[(size_t)k]) fail(TAURUS_E_STATE, "chunk %lld pushed twice", (long long)k);
     const ChunkIndex& idx = *L->idx;
     hipStream_t s = L->s;
+    if (x_on_host) x = stage_host_chunk(L, x, e - b);
     hipEvent_t ev[EV_PER_CHUNK] = {};
     if (L->d.profile) {
         for (int i = 0; i < EV_PER_CHUNK; i++) ev[i] = L->events[(size_t)k * EV_PER_CHUNK + i];
@@ -1034,12 +1131,23 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     }
     L->pushed[(size_t)k] = 1;
     L->npushed++;
+    ResChunk rc{};
+    if (L->res) {
+        for (int l = 0; l < RES_LISTS; l++) {
+            rc.u[l] = idx.list_at(l, k);
+            rc.n[l] = idx.list_count(l, k);
+        }
+        rc.first_row = b;
+        rc.rows = e - b;
+        L->res->prepare(rc, (int32_t)k, L->cnt, s);
+    }
     const float* rscale = L->n_out ? L->n_out + b : nullptr;
     if (L->d.in_dtype == TAURUS_F32)
         gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, L->Y, s);
     else
         gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
                 static_cast<const uint16_t*>(L->wpack_any), L->ncols, rscale, L->Y, s);
+    if (x_on_host) TAURUS_HIP(hipEventRecord(L->gemm_done[(L->host_pushes - 1) & 1], s));
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
     ScatterParams p;
     p.Y = L->Y;
@@ -1047,13 +1155,14 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
     p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
     p.cnt = L->cnt;
-    p.acc = L->acc;
+    p.acc = L->res ? L->res->pool : L->acc;
+    p.slot = L->res ? L->res->slot_of : nullptr;
     p.d_o = L->d_o;
     p.agg = L->d.agg;
     p.relu = L->d.relu;
     p.out_dtype = L->d.out_dtype;
     p.bias = L->bias;
-    p.out = L->d.out;
+    p.out = L->out_dev;
     p.carry = L->carry;
     p.carry_cnt = L->carry_cnt;
     p.long_base = idx.list_off[NCLASS][(size_t)k];
@@ -1073,6 +1182,7 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     const int64_t nfix = idx.list_count(NCLASS + 1, k);
     if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
     if (ev[4]) TAURUS_HIP(hipEventRecord(ev[4], s));
+    if (L->res) L->res->release(rc, L->cnt, s);
 }
 
 static int finalize(taurus_layer* L, taurus_stats* st) {
@@ -1105,6 +1215,16 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         st->device_bytes = L->arena.peak() + (L->ms_index > 0 ? idx.arena.peak() : 0);
         st->ms_init = L->ms_init;
         st->ms_index = L->ms_index;
+        const int64_t row_bytes = (int64_t)L->d_o * 4;
+        const int64_t out_bytes = (int64_t)L->d_o * (L->d.out_dtype == TAURUS_F32 ? 4 : 2);
+        if (L->res) {
+            st->evictions = L->res->evictions;
+            st->reloads = L->res->reload_count(s);
+            st->hub_message_share = L->res->hub_share;
+            st->device_bytes += L->res->arena.peak();
+        }
+        st->h2d_bytes = L->h2d_bytes + st->reloads * row_bytes;
+        st->d2h_bytes = st->evictions * row_bytes + (L->d.out_on_host ? (L->n - (int64_t)left) * out_bytes : 0);
         for (int64_t k = 0; k < L->nchunks && !L->events.empty(); k++) {
             if (!L->pushed[(size_t)k]) continue;
             hipEvent_t* ev = &L->events[(size_t)k * EV_PER_CHUNK];
@@ -1271,7 +1391,10 @@ int taurus_push_chunk(taurus_layer* L, int64_t src_begin, int64_t src_end, const
         push_chunk(L, src_begin, src_end, x, x_on_host);
         return TAURUS_OK;
     } catch (const Failure& f) {
-        if (f.status == TAURUS_E_OOM || f.status == TAURUS_E_DEVICE) L->poisoned = true;
+        // argument errors leave the handle as it was; a failure once the
+        // chunk's work has started poisons it
+        if (f.status == TAURUS_E_OOM || f.status == TAURUS_E_DEVICE || f.status == TAURUS_E_BUDGET)
+            L->poisoned = true;
         return f.status;
     }
 }

@@ -1,0 +1,345 @@
+// Accumulator residency under a device-memory budget (Sec. 3.5: a GPU
+// store keeps the accumulators of high in-degree hub vertices resident; the
+// partial states of other destinations live in a bounded pool and, when the
+// pool runs short, those with the fewest pending messages are evicted to
+// host memory and reloaded before their next message; Sec. 3.5.3).
+//
+// Accumulator rows live in a pool of S slots; slot_of[v] names v's row (or
+// -1).  Hubs -- the top hub_fraction of vertices by (message count
+// descending, ID ascending) -- own slots 0..H-1 for the whole layer.  Before
+// chunk k runs:
+//   1. every destination the chunk touches (its work units and its own
+//      vertices, for the self message) is marked with k; those still pending
+//      and without a slot are listed;
+//   2. if the free slots do not cover the list, victims are chosen among
+//      resident, non-hub, still-pending vertices the chunk does not touch:
+//      fewest pending first, then lowest ID (a 16,384-bin histogram of the
+//      pending counts gives the threshold; ties at the threshold are ranked
+//      by an exclusive scan in vertex order; counts at or above the last bin
+//      are ranked by ID only, which changes which rows move, never results);
+//      their rows are written to the pinned host store and their slots freed;
+//   3. listed vertices take free slots; evicted ones copy their row back.
+// After the chunk, touched vertices that completed return their slots.
+// Rows are moved by exact copies, so results equal the in-core run's.
+#include "internal.hpp"
+#include "resident.hpp"
+
+namespace taurus {
+
+constexpr int RES_BINS = 16384;
+
+// chunk work: items are the units of the chunk's lists, then its own rows
+__device__ inline int dest_of(const ResChunk& c, int64_t t) {
+#pragma unroll
+    for (int l = 0; l < RES_LISTS; l++) {
+        if (t < c.n[l]) return c.u[l][t].z;
+        t -= c.n[l];
+    }
+    return (int)(c.first_row + t);
+}
+
+__global__ void k_res_collect(ResChunk c, int64_t total, int32_t k, const int32_t* __restrict__ slot_of,
+                              const int2* __restrict__ cnt, int32_t* __restrict__ dc_mark,
+                              int32_t* __restrict__ want, int32_t* __restrict__ need,
+                              unsigned long long* __restrict__ need_count) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= total) return;
+    const int v = dest_of(c, t);
+    dc_mark[v] = k;
+    if (slot_of[v] < 0 && cnt[v].x > 0 && atomicExch(&want[v], 1) == 0) need[atomicAdd(need_count, 1ull)] = v;
+}
+
+__device__ inline bool res_candidate(int v, int32_t k, const int32_t* slot_of, const uint8_t* hub,
+                                     const int32_t* dc_mark, const int2* cnt) {
+    return slot_of[v] >= 0 && !hub[v] && dc_mark[v] != k && cnt[v].x > 0;
+}
+
+__global__ __launch_bounds__(1024) void k_res_hist(int64_t n, int32_t k, const int32_t* __restrict__ slot_of,
+                                                   const uint8_t* __restrict__ hub,
+                                                   const int32_t* __restrict__ dc_mark,
+                                                   const int2* __restrict__ cnt, unsigned int* __restrict__ hist) {
+    __shared__ unsigned int h[RES_BINS];
+    for (int i = threadIdx.x; i < RES_BINS; i += blockDim.x) h[i] = 0;
+    __syncthreads();
+    for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < n; v += (int64_t)gridDim.x * blockDim.x)
+        if (res_candidate((int)v, k, slot_of, hub, dc_mark, cnt))
+            atomicAdd(&h[min(cnt[v].x, RES_BINS - 1)], 1u);
+    __syncthreads();
+    for (int i = threadIdx.x; i < RES_BINS; i += blockDim.x)
+        if (h[i]) atomicAdd(&hist[i], h[i]);
+}
+
+__global__ void k_res_tie_flags(int64_t n, int32_t k, int32_t tau, const int32_t* __restrict__ slot_of,
+                                const uint8_t* __restrict__ hub, const int32_t* __restrict__ dc_mark,
+                                const int2* __restrict__ cnt, int32_t* __restrict__ tie) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v >= n) return;
+    tie[v] = res_candidate((int)v, k, slot_of, hub, dc_mark, cnt) && min(cnt[v].x, RES_BINS - 1) == tau ? 1 : 0;
+}
+
+__global__ void k_res_victims(int64_t n, int32_t k, int32_t tau, int64_t tie_take,
+                              const int32_t* __restrict__ slot_of, const uint8_t* __restrict__ hub,
+                              const int32_t* __restrict__ dc_mark, const int2* __restrict__ cnt,
+                              const int64_t* __restrict__ tie_rank, int32_t* __restrict__ victims,
+                              unsigned long long* __restrict__ count) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v >= n || !res_candidate((int)v, k, slot_of, hub, dc_mark, cnt)) return;
+    const int b = min(cnt[v].x, RES_BINS - 1);
+    if (b < tau || (b == tau && tie_rank[v] < tie_take)) victims[atomicAdd(count, 1ull)] = (int32_t)v;
+}
+
+// one wave per victim: row to the host store, slot back to the free list
+__global__ __launch_bounds__(256) void k_res_evict(const int32_t* __restrict__ victims, int64_t nv, int d_o,
+                                                   float* __restrict__ pool, float* __restrict__ store,
+                                                   int32_t* __restrict__ slot_of, uint8_t* __restrict__ evicted,
+                                                   int32_t* __restrict__ free_list, int32_t base) {
+    const int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (j >= nv) return;
+    const int v = victims[j];
+    const int32_t s = slot_of[v];
+    const float4* src = reinterpret_cast<const float4*>(pool + (int64_t)s * d_o);
+    float4* dst = reinterpret_cast<float4*>(store + (int64_t)v * d_o);
+    for (int q = lane; q < d_o / 4; q += 64) dst[q] = src[q];
+    if (lane == 0) {
+        slot_of[v] = -1;
+        evicted[v] = 1;
+        free_list[base + j] = s;
+    }
+}
+
+// one wave per listed vertex: take slot free_list[top - 1 - j]; reload if evicted
+__global__ __launch_bounds__(256) void k_res_assign(const int32_t* __restrict__ need, int64_t nn, int d_o,
+                                                    const int32_t* __restrict__ free_list, int64_t top,
+                                                    float* __restrict__ pool, const float* __restrict__ store,
+                                                    int32_t* __restrict__ slot_of, uint8_t* __restrict__ evicted,
+                                                    int32_t* __restrict__ want,
+                                                    unsigned long long* __restrict__ reloads) {
+    const int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (j >= nn) return;
+    const int v = need[j];
+    const int32_t s = free_list[top - 1 - j];
+    if (evicted[v]) {
+        const float4* src = reinterpret_cast<const float4*>(store + (int64_t)v * d_o);
+        float4* dst = reinterpret_cast<float4*>(pool + (int64_t)s * d_o);
+        for (int q = lane; q < d_o / 4; q += 64) dst[q] = src[q];
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (lane == 0) {
+        if (evicted[v]) {
+            evicted[v] = 0;
+            atomicAdd(reloads, 1ull);
+        }
+        slot_of[v] = s;
+        want[v] = 0;
+    }
+}
+
+// touched vertices that completed give their slot back (hub slots stay)
+__global__ void k_res_release(ResChunk c, int64_t total, const int2* __restrict__ cnt,
+                              const uint8_t* __restrict__ hub, int32_t* __restrict__ slot_of,
+                              int32_t* __restrict__ free_list, int32_t* __restrict__ free_top) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= total) return;
+    const int v = dest_of(c, t);
+    if (cnt[v].x != 0 || hub[v]) return;
+    const int32_t s = atomicExch(&slot_of[v], -1);
+    if (s >= 0) free_list[atomicAdd(free_top, 1)] = s;
+}
+
+__global__ void k_res_set(int32_t* __restrict__ p, int32_t v) { *p = v; }
+
+// hubs: vertices order[0..H) take slots 0..H-1; free list = H..S-1
+__global__ void k_res_init(const uint32_t* __restrict__ order, int64_t H, int64_t S, int32_t* __restrict__ slot_of,
+                           uint8_t* __restrict__ hub, int32_t* __restrict__ free_list) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < H) {
+        const uint32_t v = order[t];
+        slot_of[v] = (int32_t)t;
+        hub[v] = 1;
+    }
+    if (t < S - H) free_list[t] = (int32_t)(H + t);
+}
+
+__global__ void k_hub_keys(const int32_t* __restrict__ m, int64_t n, int idbits, int64_t maxm,
+                           uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v >= n) return;
+    keys[v] = ((uint64_t)(maxm - m[v]) << idbits) | (uint64_t)v;
+    vals[v] = (uint32_t)v;
+}
+
+__global__ void k_fill_u8(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__global__ void k_sum_hub_messages(const int32_t* __restrict__ m, const uint8_t* __restrict__ hub, int64_t n,
+                                   unsigned long long* __restrict__ sum) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n && hub[v]) atomicAdd(sum, (unsigned long long)m[v]);
+}
+
+int64_t Residency::fixed_bytes(int64_t n) {
+    // slot_of, dc_mark, want, tie flags (int32); tie ranks (int64); victims,
+    // need list (int32); hub, evicted (u8); histogram
+    return n * (4 + 4 + 4 + 4 + 8 + 4 + 4 + 1 + 1) + RES_BINS * 4 + 4096;
+}
+
+Residency::Residency(hipStream_t s, int64_t n_, int d_o_, int64_t slots, int64_t hubs, const int32_t* m,
+                     int64_t messages)
+    : arena(s), n(n_), d_o(d_o_), S(slots), H(hubs) {
+    const int T = 256;
+    const unsigned nb = (unsigned)ceil_div(n, T);
+    slot_of = arena.alloc<int32_t>(n, "accumulator slots");
+    dc_mark = arena.alloc<int32_t>(n, "chunk marks");
+    want = arena.alloc<int32_t>(n, "slot requests");
+    tie = arena.alloc<int32_t>(n, "eviction ties");
+    tie_rank = arena.alloc<int64_t>(n + 1, "eviction tie ranks");
+    victims = arena.alloc<int32_t>(n, "eviction victims");
+    need = arena.alloc<int32_t>(n, "slot list");
+    hub = arena.alloc<uint8_t>(n, "hub flags");
+    evicted = arena.alloc<uint8_t>(n, "evicted flags");
+    hist = arena.alloc<unsigned int>(RES_BINS, "pending histogram");
+    counters = arena.alloc<unsigned long long>(4, "residency counters");
+    free_list = arena.alloc<int32_t>(S, "free slots");
+    free_top = arena.alloc<int32_t>(1, "free slot count");
+    pool = arena.alloc<float>(S * (int64_t)d_o, "accumulator pool");
+    fill_i32(slot_of, n, -1, s);
+    fill_i32(dc_mark, n, -1, s);
+    fill_i32(want, n, 0, s);
+    k_fill_u8<<<nb, T, 0, s>>>(hub, n, 0);
+    TAURUS_CHECK_LAUNCH();
+    k_fill_u8<<<nb, T, 0, s>>>(evicted, n, 0);
+    TAURUS_CHECK_LAUNCH();
+    fill_i32(reinterpret_cast<int32_t*>(counters), 8, 0, s);
+    // hubs: the first H vertices by (message count descending, ID ascending)
+    Arena tmp(s);
+    uint32_t* order = nullptr;
+    if (H > 0) {
+        const int idbits = std::max(1, bits_for(n - 1));
+        const int mbits = std::max(1, bits_for(std::max<int64_t>(messages, 1)));
+        if (idbits + mbits > 64) fail(TAURUS_E_INVALID, "hub key does not fit 64 bits");
+        SortBuffers sb{{tmp.alloc<uint64_t>(n, "hub keys"), tmp.alloc<uint64_t>(n, "hub keys (ping-pong)")},
+                       {tmp.alloc<uint32_t>(n, "hub order"), tmp.alloc<uint32_t>(n, "hub order (ping-pong)")},
+                       0};
+        int* bad = tmp.alloc<int>(1, "sort flag");
+        fill_i32(bad, 1, 0, s);
+        k_hub_keys<<<nb, T, 0, s>>>(m, n, idbits, messages, sb.keys[0], sb.vals[0]);
+        TAURUS_CHECK_LAUNCH();
+        radix_sort_u64(sb, n, idbits + mbits, tmp, s, bad, 1);
+        order = sb.vals[sb.cur];
+    }
+    k_res_init<<<(unsigned)ceil_div(std::max<int64_t>(S, 1), T), T, 0, s>>>(order, H, S, slot_of, hub, free_list);
+    TAURUS_CHECK_LAUNCH();
+    k_res_set<<<1, 1, 0, s>>>(free_top, (int32_t)(S - H));
+    TAURUS_CHECK_LAUNCH();
+    unsigned long long hub_msgs = 0;
+    if (H > 0) {
+        k_sum_hub_messages<<<nb, T, 0, s>>>(m, hub, n, counters + 3);
+        TAURUS_CHECK_LAUNCH();
+    }
+    Readback rb;
+    rb.add(&hub_msgs, counters + 3, 1);
+    rb.run(s);
+    hub_share = messages > 0 ? (double)hub_msgs / (double)messages : 0.0;
+    // host store for evicted rows: pinned, written and read by kernels only
+    TAURUS_HIP(hipHostMalloc(&store_host, (size_t)n * d_o * sizeof(float), hipHostMallocDefault));
+    TAURUS_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&store_dev), store_host, 0));
+}
+
+Residency::~Residency() {
+    (void)hipDeviceSynchronize();
+    if (store_host) (void)hipHostFree(store_host);
+}
+
+void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream_t s) {
+    const int T = 256;
+    const int64_t total = c.total();
+    unsigned long long* need_count = counters;
+    fill_i32(reinterpret_cast<int32_t*>(need_count), 2, 0, s);
+    k_res_collect<<<(unsigned)ceil_div(std::max<int64_t>(total, 1), T), T, 0, s>>>(c, total, k, slot_of, cnt, dc_mark,
+                                                                                  want, need, need_count);
+    TAURUS_CHECK_LAUNCH();
+    unsigned long long nn = 0;
+    int32_t top = 0;
+    {
+        Readback rb;
+        rb.add(&nn, need_count, 1);
+        rb.add(&top, free_top, 1);
+        rb.run(s);
+    }
+    if (nn > (unsigned long long)top) {
+        const int64_t M = (int64_t)nn - top;
+        // threshold of the pending counts among candidates
+        fill_i32(reinterpret_cast<int32_t*>(hist), RES_BINS, 0, s);
+        k_res_hist<<<1024, 1024, 0, s>>>(n, k, slot_of, hub, dc_mark, cnt, hist);
+        TAURUS_CHECK_LAUNCH();
+        std::vector<unsigned int> hh(RES_BINS);
+        {
+            Readback rb;
+            rb.add(hh.data(), hist, RES_BINS);
+            rb.run(s);
+        }
+        int64_t below = 0;
+        int tau = -1;
+        for (int b = 0; b < RES_BINS; b++) {
+            if (below + hh[(size_t)b] >= M) {
+                tau = b;
+                break;
+            }
+            below += hh[(size_t)b];
+        }
+        if (tau < 0)
+            fail(TAURUS_E_BUDGET, "accumulator pool: chunk %d needs %lld slots, only %lld can be freed", k,
+                 (long long)nn, (long long)(top + below));
+        k_res_tie_flags<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, slot_of, hub, dc_mark, cnt, tie);
+        TAURUS_CHECK_LAUNCH();
+        Arena tmp(s);
+        scan_i32_to_i64(tie, tie_rank, n, false, tmp, s);
+        unsigned long long* vcount = counters + 1;
+        fill_i32(reinterpret_cast<int32_t*>(vcount), 2, 0, s);
+        k_res_victims<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, M - below, slot_of, hub, dc_mark, cnt,
+                                                             tie_rank, victims, vcount);
+        TAURUS_CHECK_LAUNCH();
+        unsigned long long got = 0;
+        {
+            Readback rb;
+            rb.add(&got, vcount, 1);
+            rb.run(s);
+        }
+        if ((int64_t)got != M)
+            fail(TAURUS_E_DEVICE, "eviction chose %llu victims instead of %lld", got, (long long)M);
+        k_res_evict<<<(unsigned)ceil_div(M * 64, T), T, 0, s>>>(victims, M, d_o, pool, store_dev, slot_of, evicted,
+                                                              free_list, top);
+        TAURUS_CHECK_LAUNCH();
+        evictions += M;
+        top += (int32_t)M;
+    }
+    if (nn > 0) {
+        k_res_assign<<<(unsigned)ceil_div((int64_t)nn * 64, T), T, 0, s>>>(need, (int64_t)nn, d_o, free_list, top,
+                                                                         pool, store_dev, slot_of, evicted, want,
+                                                                         counters + 2);
+        TAURUS_CHECK_LAUNCH();
+        k_res_set<<<1, 1, 0, s>>>(free_top, top - (int32_t)nn);
+        TAURUS_CHECK_LAUNCH();
+    }
+}
+
+void Residency::release(const ResChunk& c, const int2* cnt, hipStream_t s) {
+    const int64_t total = c.total();
+    if (total == 0) return;
+    k_res_release<<<(unsigned)ceil_div(total, 256), 256, 0, s>>>(c, total, cnt, hub, slot_of, free_list, free_top);
+    TAURUS_CHECK_LAUNCH();
+}
+
+int64_t Residency::reload_count(hipStream_t s) {
+    unsigned long long r = 0;
+    Readback rb;
+    rb.add(&r, counters + 2, 1);
+    rb.run(s);
+    return (int64_t)r;
+}
+
+}  // namespace taurus

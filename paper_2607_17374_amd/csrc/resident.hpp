@@ -1,0 +1,59 @@
+// Accumulator residency under a device-memory budget (resident.hip).
+#pragma once
+
+#include "internal.hpp"
+
+namespace taurus {
+
+constexpr int RES_LISTS = 5;  // the four short classes and the wave units of a chunk
+
+// The destinations one chunk touches: its work units (v = unit.z) and its
+// own vertices [first_row, first_row + rows) (the self message).
+struct ResChunk {
+    const int4* u[RES_LISTS];
+    int64_t n[RES_LISTS];
+    int64_t first_row, rows;
+    int64_t total() const {
+        int64_t t = rows;
+        for (int l = 0; l < RES_LISTS; l++) t += n[l];
+        return t;
+    }
+};
+
+class Residency {
+public:
+    // slots: pool rows (hubs included); hubs: resident hub rows; m: message
+    // counts per vertex (hub order); messages: their sum
+    Residency(hipStream_t s, int64_t n, int d_o, int64_t slots, int64_t hubs, const int32_t* m, int64_t messages);
+    ~Residency();
+    Residency(const Residency&) = delete;
+    Residency& operator=(const Residency&) = delete;
+
+    // device bytes the residency structures take besides the pool
+    static int64_t fixed_bytes(int64_t n);
+
+    // give every pending destination of chunk k a slot, evicting if needed
+    void prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream_t s);
+    // free the slots of the chunk's destinations that completed
+    void release(const ResChunk& c, const int2* cnt, hipStream_t s);
+    int64_t reload_count(hipStream_t s);
+
+    Arena arena;
+    int64_t n, d_o, S, H;
+    float* pool = nullptr;       // [S][d_o]
+    int32_t* slot_of = nullptr;  // [n], -1 = no row
+    int64_t evictions = 0;
+    double hub_share = 0;        // share of the layer's messages addressed to hubs
+
+private:
+    int32_t *dc_mark = nullptr, *want = nullptr, *tie = nullptr, *victims = nullptr, *need = nullptr;
+    int64_t* tie_rank = nullptr;
+    uint8_t *hub = nullptr, *evicted = nullptr;
+    unsigned int* hist = nullptr;
+    unsigned long long* counters = nullptr;  // [0] listed, [1] victims, [2] reloads, [3] hub messages
+    int32_t *free_list = nullptr, *free_top = nullptr;
+    float* store_host = nullptr;  // pinned [n][d_o]
+    float* store_dev = nullptr;   // the same memory as seen by kernels
+};
+
+}  // namespace taurus

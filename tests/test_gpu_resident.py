@@ -1,0 +1,167 @@
+"""Accumulator residency under a device-memory budget (hubs, eviction to
+pinned host memory, reload) and host-resident chunks and outputs, on the GPU
+(needs an MI355X)."""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+import fixtures as F
+from fixtures import workloads as WL
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+PIECE = 512          # the library's hub-piece length (work units per long segment)
+FIXED_PER_VERTEX = 34
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _note(msg):
+    print(f"[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _max_chunk_destinations(src, dst, n, chunk):
+    """Upper bound of the destinations one chunk touches: its work units
+    (segments, long ones counted per piece) plus its own vertices."""
+    key = (src.astype(np.int64) // chunk) * n + dst
+    seg, lens = np.unique(key, return_counts=True)
+    units = np.where(lens > 8, (lens + PIECE - 1) // PIECE, 1)
+    per_chunk = np.bincount(seg // n, weights=units, minlength=(n + chunk - 1) // chunk)
+    rows = np.minimum(chunk, n - np.arange(per_chunk.size) * chunk)
+    return int((per_chunk + rows).max())
+
+
+def _budget(stats_incore, n, d_out, d_in, chunk, slots):
+    """A budget that leaves about `slots` accumulator rows (mirrors the
+    library's planning: everything but the dense rows, the residency arrays,
+    two staging buffers, then the pool, each with 1/8 rounding room)."""
+    row = d_out * 4
+    dense = n * row
+    other = stats_incore["device_bytes"] - dense
+    staging = 2 * min(chunk, n) * d_in * 4 * 9 // 8
+    return int(other + FIXED_PER_VERTEX * n * 9 // 8 + 4096 + staging + slots * (row + 4) * 9 // 8 + (1 << 20))
+
+
+def _run(torch, w, row_off, col_dst, X, budget=0, hub_fraction=0.0):
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    outs, stats = [], []
+    h = X
+    for li, spec in enumerate(H.layer_specs(w), start=1):
+        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device="cuda")
+        b = budget[li - 1] if isinstance(budget, list) else budget
+        L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, hbm_budget=b, hub_fraction=hub_fraction, **spec)
+        L.push_all(h)
+        stats.append(L.finalize())
+        L.destroy()
+        outs.append(out)
+        h = out
+    return outs, stats
+
+
+def test_budget_eviction_matches_incore_c4_shape(torch_cuda):
+    """C4's model (GraphSAGE-mean 512 -> 256 -> 128, fp32, U[-1,1) features,
+    RMAT(.57,.19,.19), vertex IDs shuffled) at 1/2000 of the vertices, with 1% hub vertices and a
+    budget that holds well under half of the accumulator rows: outputs equal
+    the in-core run bit for bit, rows were evicted and reloaded, and sampled
+    destinations match the oracle."""
+    import oracle as O
+    torch = torch_cuda
+    # random vertex IDs: with natural RMAT IDs the first chunks alone touch
+    # most vertices at this scale, leaving nothing to evict
+    w = dataclasses.replace(WL.SAGE_OOC_RMAT_269M, random_ids=True).scaled(n=1 << 17, e=1 << 21, chunk=1024)
+    _note(f"{w.name}: in core")
+    src, dst = WL.graph(w)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    X = torch.from_numpy(WL.input_features(w)).cuda()
+    ref, ref_stats = _run(torch, w, row_off, col_dst, X)
+    need = _max_chunk_destinations(src, dst, w.n, w.chunk)
+    hubs = int(np.ceil(0.01 * w.n))
+    slots = hubs + need + (w.n - hubs - need) // 4
+    assert slots < w.n * 0.6, (need, slots)
+    budgets = [_budget(s, w.n, spec["d_out"], spec["d_in"], w.chunk, slots)
+               for s, spec in zip(ref_stats, H.layer_specs(w))]
+    _note(f"  budgets {budgets} (slots {slots}, chunk destinations {need})")
+    outs, stats = _run(torch, w, row_off, col_dst, X, budget=budgets, hub_fraction=0.01)
+    for li, (a, b, st) in enumerate(zip(outs, ref, stats), start=1):
+        assert torch.equal(a, b), li
+        assert st["evictions"] > 0 and st["reloads"] > 0, st
+        assert 0.0 < st["hub_message_share"] < 1.0
+        assert st["d2h_bytes"] == st["evictions"] * w.dims[li] * 4
+        assert st["device_bytes"] <= budgets[li - 1] + (1 << 20)
+    # sampled destinations against the oracle, each layer fed the GPU's previous output
+    g = O.Graph(w.n, src, dst)
+    rng = np.random.default_rng(9)
+    d_in = np.diff(g.in_off)
+    ids = np.unique(np.concatenate([rng.choice(w.n, 1024, replace=False), np.argsort(-d_in, kind="stable")[:32],
+                                    np.flatnonzero(d_in == 0)[:32]]))
+    h = WL.input_features(w)
+    for li in range(1, w.layers + 1):
+        p = WL.layer_params(w, li)
+        z = O.layer(w.agg, g, h, F.F32, p.W, p.b, li < w.layers, dst_ids=ids)
+        r = H.compare(outs[li - 1].cpu().numpy()[ids], z, H.RTOL[F.F32])
+        assert r["n_bad"] == 0, (li, r)
+        h = outs[li - 1].cpu().numpy()
+
+
+def test_host_chunks_and_host_outputs(torch_cuda):
+    """Chunks in pinned host memory (staged on the layer's copy stream) and
+    outputs written straight into pinned host memory give the device run's
+    values bit for bit."""
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    w = WL.SAGE_RMAT_4K
+    _note("host chunks / host outputs")
+    row_off, col_dst = H.gpu_graph(w)
+    xh = torch.from_numpy(WL.input_features(w))
+    X = xh.cuda()
+    Xp = xh.pin_memory()
+    spec = H.layer_specs(w)[0]
+    ref = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+    L = T.Layer(w.n, row_off, col_dst, out=ref, chunk=w.chunk, **spec)
+    L.push_all(X)
+    L.finalize()
+    L.destroy()
+    out_h = torch.empty((w.n, spec["d_out"]), dtype=torch.float32).pin_memory()
+    L = T.Layer(w.n, row_off, col_dst, out=out_h, chunk=w.chunk, **spec)
+    L.push_all(Xp)
+    st = L.finalize()
+    L.destroy()
+    assert torch.equal(out_h, ref.cpu())
+    assert st["h2d_bytes"] == w.n * spec["d_in"] * 4
+    assert st["d2h_bytes"] == w.n * spec["d_out"] * 4
+    # pageable host memory is refused
+    with pytest.raises(ValueError):
+        T.Layer(w.n, row_off, col_dst, out=torch.empty((w.n, spec["d_out"])), chunk=w.chunk, **spec)
+
+
+def test_budget_errors(torch_cuda):
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    w = WL.SAGE_RMAT_4K
+    _note("budget errors")
+    row_off, col_dst = H.gpu_graph(w)
+    spec = H.layer_specs(w)[0]
+    out = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **spec)
+    L.push_all(torch.from_numpy(WL.input_features(w)).cuda())
+    incore = L.finalize()["device_bytes"]
+    L.destroy()
+    half = incore - w.n * spec["d_out"] * 4 // 2      # the pool, not the dense rows: half the rows at most
+    for bad in (dict(hbm_budget=1 << 20), dict(hbm_budget=half, hub_fraction=0.9)):
+        with pytest.raises(T.TaurusError) as ex:
+            T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **dict(spec, **bad))
+        assert ex.value.status == -6, bad
+    with pytest.raises(T.TaurusError) as ex:
+        T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **dict(spec, hub_fraction=1.5))
+    assert ex.value.status == -1
