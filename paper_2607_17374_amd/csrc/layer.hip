@@ -379,64 +379,123 @@ __global__ __launch_bounds__(SC_THREADS) void k_self(ScatterParams p) {
     }
 }
 
+// What a unit's flush needs besides its rows: the counts and, when the unit
+// is probably not its vertex's first flush, the accumulator row (hint:
+// NOT_FIRST, or v belongs to this chunk or an earlier one, so its self
+// message came first in ascending order; the pending count decides whether
+// the row is used).  Within one scatter launch each destination has at most
+// one flushing unit and no other kernel touches it, so both may be read at
+// any time before that flush -- which lets a row-group fetch them for its
+// next unit while the current unit's rows are in flight.
+template <int G, int VEC, bool SPEC>
+__device__ inline void fetch_flush_state(const ScatterParams& p, int4 w, int lane, bool flushes, int2& pe,
+                                         float4 (&pre)[VEC], bool& have_pre) {
+    const int v = w.z;
+    pe = p.cnt[v];
+    have_pre = SPEC && flushes && ((w.y & NOT_FIRST) || (int64_t)v < p.first_row + p.rows);
+    if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
+}
+
+template <int LEN>
+__device__ inline void load_codes(const ScatterParams& p, int4 w, int32_t (&code)[LEN]) {
+    const int len = w.y & LEN_MASK;
+#pragma unroll
+    for (int i = 0; i < LEN; i++) code[i] = (LEN == 1 || i < len) ? p.src[w.x + i] : 0;
+}
+
+template <int G, int VEC, int B>
+__device__ inline void load_rows(const ScatterParams& p, const int32_t* code, int i0, int len, int step, int lane,
+                                 float4 (&rows)[B][VEC]) {
+#pragma unroll
+    for (int u = 0; u < B; u++) {
+        const int i = i0 + u * step;
+        const float* row = p.Y + (int64_t)code[u] * p.ystride;
+#pragma unroll
+        for (int j = 0; j < VEC; j++) {
+            const int col = (j * G + lane) * 4;
+            rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+        }
+    }
+}
+
+template <int VEC, int B>
+__device__ inline void add_rows(float4 (&sa)[VEC], const float4 (&rows)[B][VEC]) {
+#pragma unroll
+    for (int u = 0; u < B; u++)
+#pragma unroll
+        for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
+}
+
 // Short class of segments of at most LEN messages: each row-group walks the
-// class's units (grid stride); a unit's source codes, counts and (SPEC)
-// accumulator row are requested together, then its rows; the next unit is
-// fetched while this one is processed.
+// class's units (grid stride), software-pipelined: the first batch of this
+// unit's rows is requested, then the next unit's source codes and flush
+// state and the descriptor after it, and only then are the rows summed and
+// the unit flushed.
 template <int G, int VEC, bool SPEC, int LEN>
 __device__ inline void short_class(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
     constexpr int NRG = SC_THREADS / G;
     constexpr int B = LEN * VEC <= 16 ? LEN : 16 / VEC;  // rows in flight per batch
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t stride = (int64_t)gridDim.x * NRG;
-    int64_t ui = (int64_t)blockIdx.x * NRG + rg;
-    int4 w = ui < n ? units[ui] : make_int4(0, 0, 0, 0);
-    while (ui < n) {
-        const int64_t un = ui + stride;
-        const int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
-        const int v = w.z, len = w.y & LEN_MASK;
-        const int2 pe = p.cnt[v];
-        int32_t code[LEN];
-#pragma unroll
-        for (int i = 0; i < LEN; i++) code[i] = (LEN == 1 || i < len) ? p.src[w.x + i] : 0;
-        float4 pre[VEC];
-        const bool have_pre = SPEC && (w.y & NOT_FIRST);
-        if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
+    int64_t un = (int64_t)blockIdx.x * NRG + rg;
+    if (un >= n) return;  // the whole row-group
+    int4 w = units[un];
+    int32_t code[LEN];
+    load_codes<LEN>(p, w, code);
+    int2 pe;
+    float4 pre[VEC];
+    bool have_pre;
+    fetch_flush_state<G, VEC, SPEC>(p, w, lane, true, pe, pre, have_pre);
+    un += stride;
+    int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
+    for (;;) {
+        const int len = w.y & LEN_MASK;
+        float4 rows[B][VEC];
+        load_rows<G, VEC, B>(p, code, 0, len, 1, lane, rows);
+        const bool more = un < n;
+        int32_t ncode[LEN];
+        int2 npe = make_int2(0, 0);
+        float4 npre[VEC];
+        bool nhave = false;
+        if (more) {
+            load_codes<LEN>(p, wn, ncode);
+            fetch_flush_state<G, VEC, SPEC>(p, wn, lane, true, npe, npre, nhave);
+        }
+        const int64_t un2 = un + stride;
+        const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
         float4 sa[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
+        add_rows<VEC, B>(sa, rows);
 #pragma unroll
-        for (int i0 = 0; i0 < LEN; i0 += B) {
-            float4 rows[B][VEC];
-#pragma unroll
-            for (int u = 0; u < B; u++) {
-                const int i = i0 + u;
-                const float* row = p.Y + (int64_t)code[i] * p.ystride;
-#pragma unroll
-                for (int j = 0; j < VEC; j++) {
-                    const int col = (j * G + lane) * 4;
-                    rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < B; u++)
-#pragma unroll
-                for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
+        for (int i0 = B; i0 < LEN; i0 += B) {
+            load_rows<G, VEC, B>(p, code + i0, i0, len, 1, lane, rows);
+            add_rows<VEC, B>(sa, rows);
         }
         const float sig = seg_scale(p.agg, pe.y);
         float4 c[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
-        flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
-        ui = un;
+        flush_owner<G, VEC>(p, w.z, pe, c, len, lane, pre, have_pre);
+        if (!more) break;
         w = wn;
+        pe = npe;
+        have_pre = nhave;
+#pragma unroll
+        for (int j = 0; j < VEC; j++) pre[j] = npre[j];
+#pragma unroll
+        for (int i = 0; i < LEN; i++) code[i] = ncode[i];
+        un = un2;
+        wn = wn2;
     }
 }
 
 // Wave units (pieces of segments longer than the short classes): one per
 // wave; the wave's 64/G row-groups split the piece's rows, reduce across
 // row-groups with cross-lane shuffles, and row-group 0 flushes (or parks the
-// partial row of a hub piece in its carry slot).
+// partial row of a hub piece in its carry slot).  Pipelined like the short
+// classes: the next unit's first-round source codes and flush state are
+// requested while this unit's first rows are in flight.
 template <int G, int VEC, bool SPEC>
 __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
     constexpr int R = 64 / G;
@@ -444,33 +503,49 @@ __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict
     const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
     const int rg = l64 / G, lane = l64 % G;
     const int64_t wstride = (int64_t)gridDim.x * (SC_THREADS / 64);
-    for (int64_t ui = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave; ui < n; ui += wstride) {
-        const int4 w = units[ui];
+    int64_t un = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave;
+    if (un >= n) return;  // the whole wave
+    auto round_codes = [&](int4 u, int i0, int32_t (&code)[B]) {
+        const int len = u.y & LEN_MASK;
+#pragma unroll
+        for (int k = 0; k < B; k++) {
+            const int i = i0 + k * R;
+            code[k] = i < len ? p.src[u.x + i] : 0;
+        }
+    };
+    int4 w = units[un];
+    int32_t code[B];
+    round_codes(w, rg, code);
+    int2 pe;
+    float4 pre[VEC];
+    bool have_pre;
+    fetch_flush_state<G, VEC, SPEC>(p, w, lane, w.w < 0 && rg == 0, pe, pre, have_pre);
+    un += wstride;
+    int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
+    for (;;) {
         const int v = w.z, len = w.y & LEN_MASK;
-        const int2 pe = p.cnt[v];
-        float4 pre[VEC];
-        const bool have_pre = SPEC && (w.y & NOT_FIRST) && w.w < 0 && rg == 0;
-        if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
+        float4 rows[B][VEC];
+        load_rows<G, VEC, B>(p, code, rg, len, R, lane, rows);
+        const bool more = un < n;
+        int32_t ncode[B];
+        int2 npe = make_int2(0, 0);
+        float4 npre[VEC];
+        bool nhave = false;
+        if (more) {
+            round_codes(wn, rg, ncode);
+            fetch_flush_state<G, VEC, SPEC>(p, wn, lane, wn.w < 0 && rg == 0, npe, npre, nhave);
+        }
+        const int64_t un2 = un + wstride;
+        const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
         float4 sa[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
-        for (int i0 = rg; i0 < len; i0 += B * R) {
-            float4 rows[B][VEC];
-#pragma unroll
-            for (int u = 0; u < B; u++) {
-                const int i = i0 + u * R;
-                const int64_t code = i < len ? p.src[w.x + i] : 0;
-                const float* row = p.Y + code * p.ystride;
-#pragma unroll
-                for (int j = 0; j < VEC; j++) {
-                    const int col = (j * G + lane) * 4;
-                    rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < B; u++)
-#pragma unroll
-                for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
+        add_rows<VEC, B>(sa, rows);
+        for (int i0 = rg + B * R; i0 < len; i0 += B * R) {
+            int32_t c2[B];
+            round_codes(w, i0, c2);
+            load_rows<G, VEC, B>(p, c2, i0, len, R, lane, rows);
+            add_rows<VEC, B>(sa, rows);
         }
 #pragma unroll
         for (int d = G; d < 64; d <<= 1)
@@ -481,23 +556,34 @@ __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict
                 sa[j].z += __shfl_xor(sa[j].z, d, 64);
                 sa[j].w += __shfl_xor(sa[j].w, d, 64);
             }
-        if (rg != 0) continue;
-        const float sig = seg_scale(p.agg, pe.y);
-        float4 c[VEC];
+        if (rg == 0) {
+            const float sig = seg_scale(p.agg, pe.y);
+            float4 c[VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
-        if (w.w < 0) {
-            flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
-        } else {
-            const int64_t slot = (int64_t)w.w - p.long_base;
-            float* crow = p.carry + slot * p.d_o;
+            for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
+            if (w.w < 0) {
+                flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
+            } else {
+                const int64_t slot = (int64_t)w.w - p.long_base;
+                float* crow = p.carry + slot * p.d_o;
 #pragma unroll
-            for (int j = 0; j < VEC; j++) {
-                const int col = (j * G + lane) * 4;
-                if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+                for (int j = 0; j < VEC; j++) {
+                    const int col = (j * G + lane) * 4;
+                    if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+                }
+                if (lane == 0) p.carry_cnt[slot] = len;
             }
-            if (lane == 0) p.carry_cnt[slot] = len;
         }
+        if (!more) break;
+        w = wn;
+        pe = npe;
+        have_pre = nhave;
+#pragma unroll
+        for (int j = 0; j < VEC; j++) pre[j] = npre[j];
+#pragma unroll
+        for (int k = 0; k < B; k++) code[k] = ncode[k];
+        un = un2;
+        wn = wn2;
     }
 }
 
