@@ -9,7 +9,7 @@ synthetic data resident in HBM before the timed region.
 One step = the whole hot path once: CSR build from the edge list, then for
 each layer init (the chunk index, built by layer 1 and shared with layer 2
 through a plan; pending counts, weights), all chunk pushes (MFMA transform,
-self pass, scatter with fused finalise, fix-up) and finalize.
+scatter with the self messages and fused finalise, fix-up) and finalize.
 
 Output: one JSON line.  value = aggregated edges per second per layer
 (sum over layers of the propagated edges / step time) in GTEPS.  roofline =
@@ -42,15 +42,15 @@ SHORT_LEN = 8
 
 
 def flush_model(src, dst, n: int, chunk: int) -> dict:
-    """Per-kernel flush structure of one exact layer, from the graph alone.
+    """Flush structure of one exact layer, from the graph alone.
 
     A segment is the run of messages from one source chunk to one
-    destination.  Chunks are pushed in ascending order and, within a chunk,
-    the self pass runs before the scatter, so for destination v (own chunk
-    c(v)) a segment from chunk j is its first flush (accumulator logically
-    zero, no read) iff j is v's smallest message chunk and j < c(v), and its
-    last (output row written instead of the accumulator) iff j is v's largest
-    message chunk and j >= c(v)."""
+    destination; a destination's segment from its own chunk also carries its
+    self message, and a destination without one flushes its self message
+    alone when its own chunk is pushed.  With chunks pushed in ascending
+    order, v's first flush is in chunk min(first message chunk, own chunk)
+    (no accumulator read) and its last in max(last message chunk, own
+    chunk) (output row written instead of the accumulator)."""
     import numpy as np
     src = np.asarray(src, dtype=np.int64)
     dst = np.asarray(dst, dtype=np.int64)
@@ -58,51 +58,55 @@ def flush_model(src, dst, n: int, chunk: int) -> dict:
     seg, lens = np.unique(key, return_counts=True)
     ch, v = seg // n, seg % n
     cv = v // chunk
-    big = np.iinfo(np.int64).max
-    minch = np.full(n, big, dtype=np.int64)
+    minch = np.full(n, np.iinfo(np.int64).max, dtype=np.int64)
     maxch = np.full(n, -1, dtype=np.int64)
     np.minimum.at(minch, v, ch)
     np.maximum.at(maxch, v, ch)
-    fresh = (ch == minch[v]) & (ch < cv)
-    final = (ch == maxch[v]) & (ch >= cv)
+    own_v = np.arange(n, dtype=np.int64) // chunk
+    first = np.minimum(minch, own_v)
+    last = np.maximum(maxch, own_v)
+    fresh = ch == first[v]
+    final = ch == last[v]
     split = lens > PIECE_LEN
     pieces = np.where(lens > SHORT_LEN, (lens + PIECE_LEN - 1) // PIECE_LEN, 1)
-    own = np.arange(n, dtype=np.int64) // chunk
-    has_msg = maxch >= 0
-    self_read = has_msg & (minch < own)          # an earlier chunk already flushed into v
-    self_final = ~has_msg | (maxch < own)        # no later segment: the self flush completes v
-    active_src = np.unique(src).size
+    has_own = np.zeros(n, dtype=bool)
+    has_own[v[ch == cv]] = True
+    alone = ~has_own                      # vertices flushing their self message alone
     return {
         "messages": int(src.size), "segments": int(seg.size), "units": int(pieces.sum()),
         "short_units": int((lens <= SHORT_LEN).sum()), "split_segments": int(split.sum()),
-        "active_src": int(active_src),
-        # scatter-owned flushes (segments completed in the scatter kernel)
+        "active_src": int(np.unique(src).size), "own_segments": int(has_own.sum()),
         "sc_flush": int((~split).sum()), "sc_fresh": int((~split & fresh).sum()),
         "sc_final": int((~split & final).sum()), "split_pieces": int(pieces[split].sum()),
         "fx_fresh": int((split & fresh).sum()), "fx_final": int((split & final).sum()),
-        "self_read": int(self_read.sum()), "self_final": int(self_final.sum()),
+        "alone": int(alone.sum()), "alone_fresh": int((alone & (own_v == first)).sum()),
+        "alone_final": int((alone & (own_v == last)).sum()),
     }
 
 
-def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int) -> dict:
+def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int, sage: bool) -> dict:
     """Algorithmic HBM bytes of each per-layer kernel (all its launches).
 
     flush: counts read 8 + written 4; the accumulator row read (4 d_o) unless
     the flush is v's first; the accumulator row written (4 d_o), or the output
     row (out_bytes d_o) for v's last flush.
-    scatter: 16 per work unit, 4 per message (source code), each source's Y
-    row once (4 d_o), the flushes it owns, and a hub piece's partial row and
-    count (4 d_o + 4) to the carry buffer.
-    self: each vertex's self row of Y (4 d_o) and one flush.
+    scatter: 16 per work unit, 4 per message (source code), the chunk
+    transform's rows once -- every vertex's self row, and for GraphSAGE also
+    the aggregation half of each source's row (4 d_o each) -- one flag byte
+    per vertex for the self pass, the flushes it owns (segments that are not
+    split, and vertices flushing their self message alone), and a hub piece's
+    partial row and count (4 d_o + 4) to the carry buffer.
     fix-up: 16 per hub segment, its pieces' carries read back, one flush."""
     def flushes(k, fresh, final):
         return 12.0 * k + 4.0 * d_o * (k - fresh) + out_bytes * d_o * final + 4.0 * d_o * (k - final)
-    sc = (16.0 * fm["units"] + 4.0 * fm["messages"] + 4.0 * d_o * fm["active_src"]
-          + flushes(fm["sc_flush"], fm["sc_fresh"], fm["sc_final"]) + (4.0 * d_o + 4.0) * fm["split_pieces"])
-    se = 4.0 * d_o * n + flushes(n, n - fm["self_read"], fm["self_final"])
+    y_rows = n + (fm["active_src"] if sage else 0)
+    sc = (16.0 * fm["units"] + 4.0 * fm["messages"] + 4.0 * d_o * y_rows + 1.0 * n
+          + flushes(fm["sc_flush"], fm["sc_fresh"], fm["sc_final"])
+          + flushes(fm["alone"], fm["alone_fresh"], fm["alone_final"])
+          + (4.0 * d_o + 4.0) * fm["split_pieces"])
     fx = (16.0 * fm["split_segments"] + (4.0 * d_o + 4.0) * fm["split_pieces"]
           + flushes(fm["split_segments"], fm["fx_fresh"], fm["fx_final"]))
-    return {"scatter": sc, "self": se, "fixup": fx}
+    return {"scatter": sc, "fixup": fx}
 
 
 # ---------------------------------------------------------------- profiles --
@@ -291,7 +295,7 @@ def main():
     # per-layer figures, averaged over the timed steps
     nl = len(specs)
     layers = []
-    tot = {"scatter": [0.0, 0.0, 0], "self": [0.0, 0.0, 0], "fixup": [0.0, 0.0, 0]}  # bytes, ms, launches
+    tot = {"scatter": [0.0, 0.0, 0], "fixup": [0.0, 0.0, 0]}  # bytes, ms, launches
     gemm_flops = gemm_ms = 0.0
     model_ok = True
     for li in range(nl):
@@ -300,15 +304,15 @@ def main():
         ncols = d_o  # GCN transform width
         wall = float(np.mean([s["wall_ms"] for s in sts]))
         st = sts[-1]
-        kb = kernel_bytes(fm, w.n, d_o, 4)
+        kb = kernel_bytes(fm, w.n, d_o, 4, sage=False)
         checks = (st["short_units"] == fm["short_units"], st["wave_units"] == fm["units"] - fm["short_units"],
-                  st["split_segments"] == fm["split_segments"], st["pairs"] == fm["segments"] + w.n,
+                  st["split_segments"] == fm["split_segments"], st["pairs"] == fm["segments"] + fm["alone"],
                   st["messages"] == fm["messages"])
         if not all(checks):
             model_ok = False
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
         ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
-              for k in ("gemm", "self", "scatter", "fixup", "init", "index")}
+              for k in ("gemm", "scatter", "fixup", "init", "index")}
         if profile:
             for k in tot:
                 tot[k][0] += kb[k] * len(sts)

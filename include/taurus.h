@@ -168,7 +168,8 @@ typedef struct {
     double ms_init;                /* wall time of taurus_layer_init                    */
     double ms_index;               /* of which: sampling and chunk-index build (0 when
                                       the plan already held the index)                  */
-    double ms_gemm, ms_self, ms_scatter, ms_fixup;
+    double ms_gemm, ms_self, ms_scatter, ms_fixup;  /* ms_self stays 0: the self messages
+                                      run inside the scatter launch, timed in ms_scatter */
     int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
 } taurus_stats;
 

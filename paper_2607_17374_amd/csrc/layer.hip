@@ -54,8 +54,9 @@ const char* last_error_cstr();
 constexpr int SC_THREADS = 256;
 constexpr int NCLASS = 4;                           // short segment classes
 constexpr int PIECE_LEN = 512;                      // longer segments: pieces of this many messages
-constexpr int NOT_FIRST = 1 << 30;                  // unit.y flag (see k_seg_emit)
-constexpr int LEN_MASK = NOT_FIRST - 1;
+constexpr int NOT_FIRST = 1 << 30;                  // unit.y flags (see k_seg_emit)
+constexpr int SELF_HERE = 1 << 29;
+constexpr int LEN_MASK = SELF_HERE - 1;
 constexpr int NLIST = NCLASS + 2;                   // short classes, wave units, fix-up entries
 
 // longest segment of short class c: 1, 2, 4, 8
@@ -177,12 +178,17 @@ __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t*
 // chunk order: when chunks are pushed in that order its accumulator row
 // already holds a partial sum, so the scatter may fetch the row together with
 // the counts (the pending count still decides whether the row is used).
-// slot = buffer position of a hub segment's piece (its partial row goes to
-// the carry buffer), else -1.  fix-up entry = {destination, position of the
-// first piece, pieces, 0}.
+// SELF_HERE marks the segment from v's own chunk: v's self message (its own
+// row of the chunk transform, one arrival) joins that segment's flush
+// instead of being flushed on its own, and has_own[v] is set so the
+// chunk's self pass skips v.  slot = buffer position of a hub segment's
+// piece (its partial row goes to the carry buffer), else -1.  fix-up entry
+// = {destination, position of the first piece, pieces, SELF_HERE or 0}.
 __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                           int vbits, const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
-                           const int64_t* __restrict__ off, int4* __restrict__ units) {
+                           int vbits, int64_t C, const int64_t* __restrict__ chunk_off,
+                           const int32_t* __restrict__ first_chunk, const int64_t* __restrict__ off,
+                           int4* __restrict__ units, uint8_t* __restrict__ has_own,
+                           unsigned long long* __restrict__ own_count) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
@@ -191,9 +197,15 @@ __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __r
     const int chunk = (int)(key >> vbits);
     const int64_t rel = b - chunk_off[chunk];
     const int nf = chunk != first_chunk[v] ? NOT_FIRST : 0;
+    const bool own = (uint32_t)v / (uint32_t)C == (uint32_t)chunk;
+    const int self = own ? SELF_HERE : 0;
+    if (own) {
+        has_own[v] = 1;
+        atomicAdd(own_count, 1ull);
+    }
     const int cls = seg_class(len);
     if (cls < NCLASS) {
-        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)len | nf, v, 0);
+        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)len | nf | self, v, 0);
         return;
     }
     const int pieces = (int)((len + PIECE_LEN - 1) / PIECE_LEN);
@@ -201,9 +213,10 @@ __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __r
     for (int q = 0; q < pieces; q++) {
         const int64_t o = (int64_t)q * PIECE_LEN;
         const int plen = (int)min((int64_t)PIECE_LEN, len - o);
-        units[first + q] = make_int4((int)(rel + o), plen | nf, v, pieces > 1 ? (int)(first + q) : -1);
+        units[first + q] = pieces > 1 ? make_int4((int)(rel + o), plen | nf, v, (int)(first + q))
+                                      : make_int4((int)(rel + o), plen | nf | self, v, -1);
     }
-    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, 0);
+    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, self);
 }
 
 __global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, int32_t* __restrict__ src) {
@@ -242,6 +255,7 @@ struct ScatterParams {
     int64_t ystride;
     int self_col;          // column offset of the self half (GraphSAGE) or 0 (GCN)
     const int32_t* src;    // chunk items: local source row
+    const uint8_t* has_own;  // v has a segment from its own chunk (its self message rides on it)
     int2* cnt;             // {pending, expected}
     float* acc;            // fp32 accumulator rows, d_o floats each
     const int32_t* slot;   // accumulator row of each vertex (residency pool), or null: row v
@@ -356,16 +370,30 @@ __device__ inline void prefetch_acc(const ScatterParams& p, int v, int lane, flo
     }
 }
 
-// Self pass: every vertex of the chunk receives its own message, the self
-// row of Y (one arrival), in vertex order -- consecutive rows of Y and of
-// the accumulators.
+// v's own row of the chunk transform (its self message): the W_self half for
+// GraphSAGE, the normalised row for GCN
 template <int G, int VEC>
-__global__ __launch_bounds__(SC_THREADS) void k_self(ScatterParams p) {
+__device__ inline void load_self_row(const ScatterParams& p, int v, int lane, float4 (&srow)[VEC]) {
+    const float* row = p.Y + ((int64_t)v - p.first_row) * p.ystride + p.self_col;
+#pragma unroll
+    for (int j = 0; j < VEC; j++) {
+        const int col = (j * G + lane) * 4;
+        srow[j] = col < p.d_o ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+    }
+}
+
+// Self pass over the chunk's own vertices that have no segment from this
+// chunk (the others take their self message with that segment): one
+// arrival each, in vertex order -- consecutive rows of Y and of the
+// accumulators.  These vertices have no other flush in the launch.
+template <int G, int VEC>
+__device__ inline void self_rows(const ScatterParams& p) {
     constexpr int NRG = SC_THREADS / G;
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t stride = (int64_t)gridDim.x * NRG;
     for (int64_t r = (int64_t)blockIdx.x * NRG + rg; r < p.rows; r += stride) {
         const int v = (int)(p.first_row + r);
+        if (p.has_own[v]) continue;
         const int2 pe = p.cnt[v];
         const float* row = p.Y + r * p.ystride + p.self_col;
         float4 c[VEC], pre[VEC];
@@ -450,8 +478,10 @@ __device__ inline void short_class(const ScatterParams& p, const int4* __restric
     int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
     for (;;) {
         const int len = w.y & LEN_MASK;
-        float4 rows[B][VEC];
+        const bool self = (w.y & SELF_HERE) != 0;
+        float4 rows[B][VEC], srow[VEC];
         load_rows<G, VEC, B>(p, code, 0, len, 1, lane, rows);
+        if (self) load_self_row<G, VEC>(p, w.z, lane, srow);
         const bool more = un < n;
         int32_t ncode[LEN];
         int2 npe = make_int2(0, 0);
@@ -475,8 +505,8 @@ __device__ inline void short_class(const ScatterParams& p, const int4* __restric
         const float sig = seg_scale(p.agg, pe.y);
         float4 c[VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
-        flush_owner<G, VEC>(p, w.z, pe, c, len, lane, pre, have_pre);
+        for (int j = 0; j < VEC; j++) c[j] = self ? f4_axpy(sig, sa[j], srow[j]) : f4_scale(sig, sa[j]);
+        flush_owner<G, VEC>(p, w.z, pe, c, len + (self ? 1 : 0), lane, pre, have_pre);
         if (!more) break;
         w = wn;
         pe = npe;
@@ -524,8 +554,10 @@ __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict
     int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
     for (;;) {
         const int v = w.z, len = w.y & LEN_MASK;
-        float4 rows[B][VEC];
+        const bool self = rg == 0 && (w.y & SELF_HERE) != 0;  // single-piece units only
+        float4 rows[B][VEC], srow[VEC];
         load_rows<G, VEC, B>(p, code, rg, len, R, lane, rows);
+        if (self) load_self_row<G, VEC>(p, v, lane, srow);
         const bool more = un < n;
         int32_t ncode[B];
         int2 npe = make_int2(0, 0);
@@ -560,9 +592,9 @@ __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict
             const float sig = seg_scale(p.agg, pe.y);
             float4 c[VEC];
 #pragma unroll
-            for (int j = 0; j < VEC; j++) c[j] = f4_scale(sig, sa[j]);
+            for (int j = 0; j < VEC; j++) c[j] = self ? f4_axpy(sig, sa[j], srow[j]) : f4_scale(sig, sa[j]);
             if (w.w < 0) {
-                flush_owner<G, VEC>(p, v, pe, c, len, lane, pre, have_pre);
+                flush_owner<G, VEC>(p, v, pe, c, len + (self ? 1 : 0), lane, pre, have_pre);
             } else {
                 const int64_t slot = (int64_t)w.w - p.long_base;
                 float* crow = p.carry + slot * p.d_o;
@@ -588,10 +620,14 @@ __device__ inline void wave_units(const ScatterParams& p, const int4* __restrict
 }
 
 // Degree-bucketed scatter of one chunk, persistent: the grid is sized to
-// what the GPU holds at once and walks the short classes, then the wave
-// units.
+// what the GPU holds at once and walks the self pass, the short classes,
+// then the wave units.
+// (VEC = 2 without the early accumulator fetch fits 4 waves per SIMD
+// without spilling; the other shapes keep the compiler's own choice)
 template <int G, int VEC, bool SPEC>
-__global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p, ChunkUnits cu) {
+__global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(VEC == 2 && !SPEC ? 4 : 1)))
+void k_scatter(ScatterParams p, ChunkUnits cu) {
+    self_rows<G, VEC>(p);
     short_class<G, VEC, SPEC, 1>(p, cu.u[0], cu.n[0]);
     short_class<G, VEC, SPEC, 2>(p, cu.u[1], cu.n[1]);
     short_class<G, VEC, SPEC, 4>(p, cu.u[2], cu.n[2]);
@@ -600,7 +636,8 @@ __global__ __launch_bounds__(SC_THREADS) void k_scatter(ScatterParams p, ChunkUn
 }
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
-// are summed in slot order and flushed.
+// are summed in slot order (plus v's self row if the segment is from v's own
+// chunk) and flushed.
 template <int G, int VEC>
 __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix) {
     constexpr int NRG = SC_THREADS / G;
@@ -622,6 +659,13 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
             if (col < p.d_o) c[j] = f4_add(c[j], *reinterpret_cast<const float4*>(crow + col));
         }
         count += p.carry_cnt[first + q];
+    }
+    if (f.w & SELF_HERE) {
+        float4 srow[VEC];
+        load_self_row<G, VEC>(p, v, lane, srow);
+#pragma unroll
+        for (int j = 0; j < VEC; j++) c[j] = f4_add(c[j], srow[j]);
+        count += 1;
     }
     flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane, pre, false);
 }
@@ -676,22 +720,8 @@ static ScatterShape scatter_shape(int d_o) {
     X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(4, 2) X(8, 2) X(16, 2) X(32, 2) X(64, 2) \
     X(4, 4) X(8, 4) X(16, 4) X(32, 4) X(64, 4)
 
-static void dispatch_self(const ScatterShape& sh, const ScatterParams& p, hipStream_t s) {
-#define TAURUS_CASE(g, v)                                                                  \
-    if (sh.G == g && sh.VEC == v) {                                                        \
-        const int64_t want = ceil_div(p.rows, SC_THREADS / g);                             \
-        const int64_t blocks = std::max<int64_t>(1, std::min(want, sh.max_blocks));        \
-        k_self<g, v><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p);                           \
-        TAURUS_CHECK_LAUNCH();                                                             \
-        return;                                                                            \
-    }
-    TAURUS_ROW_SHAPES(TAURUS_CASE)
-#undef TAURUS_CASE
-    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
-}
-
 static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, const ChunkUnits& cu, hipStream_t s) {
-    int64_t want = ceil_div(cu.n[NCLASS], SC_THREADS / 64);
+    int64_t want = std::max(ceil_div(cu.n[NCLASS], SC_THREADS / 64), ceil_div(p.rows, SC_THREADS / sh.G));
     for (int c = 0; c < NCLASS; c++) want = std::max(want, ceil_div(cu.n[c], SC_THREADS / sh.G));
     const int64_t blocks = std::max<int64_t>(1, std::min(want, sh.max_blocks));
 #define TAURUS_CASE(g, v)                                                                  \
@@ -743,6 +773,8 @@ struct ChunkIndex {
     hipStream_t built_on = nullptr;
     hipEvent_t ready = nullptr;    // recorded after the last kernel that writes the index
     int32_t* m = nullptr;          // |M(v)|
+    uint8_t* has_own = nullptr;    // v has a segment from its own chunk
+    unsigned long long* own_count = nullptr;  // number of such vertices
     int32_t* item_src = nullptr;   // local source row per item
     int4* units = nullptr;         // the work lists, one after another
     std::vector<int64_t> chunk_off;              // items before each chunk
@@ -798,6 +830,10 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
 
     idx->m = idx->arena.alloc<int32_t>(n, "message counts");
     fill_i32(idx->m, n, 0, s);
+    idx->has_own = idx->arena.alloc<uint8_t>(ceil_div(n, 4) * 4, "own-chunk segment flags");
+    fill_i32(reinterpret_cast<int32_t*>(idx->has_own), ceil_div(n, 4), 0, s);
+    idx->own_count = idx->arena.alloc<unsigned long long>(1, "own-chunk segment count");
+    fill_i32(reinterpret_cast<int32_t*>(idx->own_count), 2, 0, s);
     idx->chunk_off.assign((size_t)nch + 1, 0);
     for (int l = 0; l < NLIST; l++) idx->list_off[l].assign((size_t)nch + 1, 0);
     // flags: 1, 2 invalid CSR; 4 unsorted row or self loop; 8 sort inconsistency
@@ -888,8 +924,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->list_count(NCLASS, k));
     if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
     idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
-    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, doffs, first_chunk, loff,
-                                                      idx->units);
+    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, doffs, first_chunk, loff,
+                                                      idx->units, idx->has_own, idx->own_count);
     TAURUS_CHECK_LAUNCH();
     idx->item_src = idx->arena.alloc<int32_t>(kept, "item sources");
     k_take_src<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(vals, kept, idx->item_src);
@@ -949,9 +985,9 @@ struct taurus_layer {
 
 namespace taurus {
 
-// events per pushed chunk: before the transform, the self pass, the scatter,
-// the fix-up, and after it
-constexpr int EV_PER_CHUNK = 5;
+// events per pushed chunk: before the transform, the scatter (self pass
+// included), the fix-up, and after it
+constexpr int EV_PER_CHUNK = 4;
 
 // Timing events are recycled across layers (creating them costs more than
 // recording them).
@@ -1159,12 +1195,6 @@ static void layer_init(taurus_layer* L) {
     L->ms_init = ms_since(t_start);
 }
 
-static bool chunk_has_units(const ChunkIndex& idx, int64_t k) {
-    for (int l = 0; l <= NCLASS; l++)
-        if (idx.list_count(l, k) > 0) return true;
-    return false;
-}
-
 // Host-resident chunk (pinned): copy it on the layer's copy stream into one
 // of two device staging buffers while the previous chunk computes.  A
 // buffer is refilled only after the transform that read it; the caller's x
@@ -1240,6 +1270,7 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.ystride = L->ncols;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
     p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
+    p.has_own = idx.has_own;
     p.cnt = L->cnt;
     p.acc = L->res ? L->res->pool : L->acc;
     p.slot = L->res ? L->res->slot_of : nullptr;
@@ -1254,20 +1285,16 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.long_base = idx.list_off[NCLASS][(size_t)k];
     p.first_row = b;
     p.rows = e - b;
-    dispatch_self(L->shape, p, s);
-    if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
-    if (chunk_has_units(idx, k)) {
-        ChunkUnits cu;
-        for (int l = 0; l <= NCLASS; l++) {
-            cu.u[l] = idx.list_at(l, k);
-            cu.n[l] = idx.list_count(l, k);
-        }
-        dispatch_scatter(L->shape, p, cu, s);
+    ChunkUnits cu;
+    for (int l = 0; l <= NCLASS; l++) {
+        cu.u[l] = idx.list_at(l, k);
+        cu.n[l] = idx.list_count(l, k);
     }
-    if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
+    dispatch_scatter(L->shape, p, cu, s);
+    if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
     const int64_t nfix = idx.list_count(NCLASS + 1, k);
     if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
-    if (ev[4]) TAURUS_HIP(hipEventRecord(ev[4], s));
+    if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
     if (L->res) L->res->release(rc, L->cnt, s);
 }
 
@@ -1280,9 +1307,10 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
     fill_i32(reinterpret_cast<int32_t*>(dleft), 2, 0, s);
     k_count_pending<<<(unsigned)ceil_div(L->n, 256), 256, 0, s>>>(L->cnt, L->n, dleft);
     TAURUS_CHECK_LAUNCH();
-    unsigned long long left = 0;
+    unsigned long long left = 0, own = 0;
     Readback rb;
     rb.add(&left, dleft, 1);
+    rb.add(&own, idx.own_count, 1);
     rb.run(s);
     if (st) {
         std::memset(st, 0, sizeof(*st));
@@ -1290,7 +1318,7 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         st->e = L->g.e;
         st->messages = idx.kept;
         st->self_terms = L->n;
-        st->pairs = idx.segments + L->n;
+        st->pairs = idx.segments + L->n - (int64_t)own;  // own-chunk segments carry their vertex's self message
         st->pending_left = (int64_t)left;
         st->completed = L->n - (int64_t)left;
         st->chunks = L->nchunks;
@@ -1317,12 +1345,10 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
             float t[EV_PER_CHUNK - 1] = {};
             for (int i = 0; i + 1 < EV_PER_CHUNK; i++) TAURUS_HIP(hipEventElapsedTime(&t[i], ev[i], ev[i + 1]));
             st->ms_gemm += t[0];
-            st->ms_self += t[1];
-            st->ms_scatter += t[2];
-            st->ms_fixup += t[3];
+            st->ms_scatter += t[1];
+            st->ms_fixup += t[2];
             st->launches_gemm++;
-            st->launches_self++;
-            st->launches_scatter += chunk_has_units(idx, k) ? 1 : 0;
+            st->launches_scatter++;
             st->launches_fixup += idx.list_count(NCLASS + 1, k) > 0 ? 1 : 0;
         }
     }
