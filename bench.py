@@ -347,7 +347,7 @@ def main():
     if profile and gemm_ms > 0:
         tf = gemm_flops / (gemm_ms * 1e-3) / 1e12
         gemm = {"bound": "mfma", "achieved": round(tf, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4), "kernel": "k_gemm_f32"}
+                "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4), "kernel": "k_gemm_panel"}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -28,12 +28,8 @@ namespace taurus {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int GEMM_WM = 2;  // 16-row blocks per wave
-constexpr int GEMM_WN = 2;  // 16-col blocks per wave
-constexpr int GEMM_TM = 2 * GEMM_WM * 16;  // workgroup tile rows (2 waves along M)
-constexpr int GEMM_TN = 2 * GEMM_WN * 16;  // workgroup tile cols (2 waves along N)
-
-int gemm_packed_blocks_n(int nc) { return (int)ceil_div(nc, GEMM_TN) * (GEMM_TN / 16); }
+// packed weights cover whole 64-column groups (zero padded)
+int gemm_packed_blocks_n(int nc) { return (int)ceil_div(nc, 64) * 4; }
 int gemm_packed_blocks_k(int k) { return (int)ceil_div(k, 16); }
 
 // Host-side repack of a row-major [K][Nc] fp32 matrix into MFMA B fragments.
@@ -48,57 +44,6 @@ void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& pa
                     float w = (k < K && col < Nc) ? W[(size_t)k * Nc + col] : 0.0f;
                     packed[(((size_t)kb * NBP + nb) * 64 + l) * 4 + c] = w;
                 }
-}
-
-__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X, int64_t M, int K,
-                                                  const float4* __restrict__ Wp, int NBP, int Nc,
-                                                  const float* __restrict__ rscale, float* __restrict__ Y) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int wm = wave & 1, wn = wave >> 1;
-    const int64_t m0 = (int64_t)blockIdx.x * GEMM_TM + wm * (GEMM_WM * 16);
-    const int nb0 = blockIdx.y * (GEMM_TN / 16) + wn * GEMM_WN;
-    const int li = lane & 15, lk = lane >> 4;
-    floatx4 acc[GEMM_WM][GEMM_WN];
-#pragma unroll
-    for (int i = 0; i < GEMM_WM; i++)
-#pragma unroll
-        for (int j = 0; j < GEMM_WN; j++) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int KB = (K + 15) >> 4;
-    for (int kb = 0; kb < KB; kb++) {
-        const int k = kb * 16 + 4 * lk;
-        float4 a[GEMM_WM], b[GEMM_WN];
-#pragma unroll
-        for (int i = 0; i < GEMM_WM; i++) {
-            const int64_t row = m0 + i * 16 + li;
-            a[i] = (row < M && k < K) ? *reinterpret_cast<const float4*>(X + row * K + k)
-                                      : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int j = 0; j < GEMM_WN; j++) b[j] = Wp[((int64_t)kb * NBP + nb0 + j) * 64 + lane];
-#pragma unroll
-        for (int i = 0; i < GEMM_WM; i++)
-#pragma unroll
-            for (int j = 0; j < GEMM_WN; j++) {
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].z, b[j].z, acc[i][j], 0, 0, 0);
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i].w, b[j].w, acc[i][j], 0, 0, 0);
-            }
-    }
-    // D fragment: lane l holds rows 4*(l/16) + r, column l%16
-#pragma unroll
-    for (int i = 0; i < GEMM_WM; i++)
-#pragma unroll
-        for (int r = 0; r < 4; r++) {
-            const int64_t row = m0 + i * 16 + 4 * lk + r;
-            if (row >= M) continue;
-            const float sc = rscale ? rscale[row] : 1.0f;
-#pragma unroll
-            for (int j = 0; j < GEMM_WN; j++) {
-                const int col = (nb0 + j) * 16 + li;
-                if (col < Nc) Y[row * Nc + col] = acc[i][j][r] * sc;
-            }
-        }
 }
 
 // ---------------------------------------------------------- 16-bit inputs --
@@ -146,70 +91,152 @@ __device__ inline floatx4 mfma16(uint4 a, uint4 b, floatx4 c) {
                                                       c, 0, 0, 0);
 }
 
-// X is [M][K] 16-bit, K a multiple of 8 (each lane's eight k are one 16-byte load).
+// ---------------------------------------------------- row-panel kernel -----
+// A workgroup owns 64 rows and a group of up to NB 16-column blocks (128
+// columns for NB = 8); each of its four waves computes 16 rows x all of the
+// group's columns, so every X row is read once per column group (once in
+// all for widths up to 128).  The group's packed weight fragments are staged
+// in LDS one K stage at a time (KS k-blocks), and a wave requests all of its
+// A fragments of the stage before the matrix-core work.
+//   fp32:   k-block = 16 k, fragment = one float4 per lane (4 MFMAs 16x16x4);
+//   16-bit: k-block = 32 k, fragment = eight 16-bit values (one 16x16x32 MFMA).
 template <int DT>
-__global__ __launch_bounds__(256) void k_gemm_16(const uint16_t* __restrict__ X, int64_t M, int K,
-                                                 const uint4* __restrict__ Wp, int NBP, int Nc,
-                                                 const float* __restrict__ rscale, float* __restrict__ Y) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int wm = wave & 1, wn = wave >> 1;
-    const int64_t m0 = (int64_t)blockIdx.x * GEMM_TM + wm * (GEMM_WM * 16);
-    const int nb0 = blockIdx.y * (GEMM_TN / 16) + wn * GEMM_WN;
-    const int li = lane & 15, lk = lane >> 4;
-    floatx4 acc[GEMM_WM][GEMM_WN];
-#pragma unroll
-    for (int i = 0; i < GEMM_WM; i++)
-#pragma unroll
-        for (int j = 0; j < GEMM_WN; j++) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int KB = (K + 31) >> 5;
-    for (int kb = 0; kb < KB; kb++) {
-        const int k = kb * 32 + 8 * lk;
-        uint4 a[GEMM_WM], b[GEMM_WN];
-#pragma unroll
-        for (int i = 0; i < GEMM_WM; i++) {
-            const int64_t row = m0 + i * 16 + li;
-            a[i] = (row < M && k < K) ? *reinterpret_cast<const uint4*>(X + row * K + k) : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int j = 0; j < GEMM_WN; j++) b[j] = Wp[((int64_t)kb * NBP + nb0 + j) * 64 + lane];
-#pragma unroll
-        for (int i = 0; i < GEMM_WM; i++)
-#pragma unroll
-            for (int j = 0; j < GEMM_WN; j++) acc[i][j] = mfma16<DT>(a[i], b[j], acc[i][j]);
+struct GemmOp;
+template <>
+struct GemmOp<TAURUS_F32> {
+    typedef float4 frag;
+    static constexpr int KBLK = 16;
+    static __device__ inline floatx4 mma(frag a, frag b, floatx4 c) {
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
     }
+    static __device__ inline frag load_a(const void* X, int64_t row, int K, int k) {
+        return *reinterpret_cast<const float4*>(static_cast<const float*>(X) + row * K + k);
+    }
+    static __device__ inline frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    // all NB column blocks of one k-block, component-major: consecutive
+    // products go to different accumulators instead of one dependent chain
+    template <int NB>
+    static __device__ inline void mma_all(frag a, const frag (&b)[NB], floatx4 (&acc)[NB]) {
 #pragma unroll
-    for (int i = 0; i < GEMM_WM; i++)
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[j].x, acc[j], 0, 0, 0);
 #pragma unroll
-        for (int r = 0; r < 4; r++) {
-            const int64_t row = m0 + i * 16 + 4 * lk + r;
-            if (row >= M) continue;
-            const float sc = rscale ? rscale[row] : 1.0f;
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[j].y, acc[j], 0, 0, 0);
 #pragma unroll
-            for (int j = 0; j < GEMM_WN; j++) {
-                const int col = (nb0 + j) * 16 + li;
-                if (col < Nc) Y[row * Nc + col] = acc[i][j][r] * sc;
-            }
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[j].z, acc[j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[j].w, acc[j], 0, 0, 0);
+    }
+};
+template <int DT>
+struct GemmOp16 {
+    typedef uint4 frag;
+    static constexpr int KBLK = 32;
+    static __device__ inline floatx4 mma(frag a, frag b, floatx4 c) { return mfma16<DT>(a, b, c); }
+    static __device__ inline frag load_a(const void* X, int64_t row, int K, int k) {
+        return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(X) + row * K + k);
+    }
+    static __device__ inline frag zero() { return make_uint4(0, 0, 0, 0); }
+    template <int NB>
+    static __device__ inline void mma_all(frag a, const frag (&b)[NB], floatx4 (&acc)[NB]) {
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = mfma16<DT>(a, b[j], acc[j]);
+    }
+};
+template <>
+struct GemmOp<TAURUS_BF16> : GemmOp16<TAURUS_BF16> {};
+template <>
+struct GemmOp<TAURUS_F16> : GemmOp16<TAURUS_F16> {};
+
+constexpr int PANEL_ROWS = 64;
+constexpr int PANEL_KS = 4;   // k-blocks per LDS stage
+
+// PANEL_NB: 16-column blocks per workgroup (8 = 128 columns; 4 for narrow outputs)
+template <int DT, int PANEL_NB>
+__global__ __launch_bounds__(256) void k_gemm_panel(const void* __restrict__ X, int64_t M, int K,
+                                                    const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP,
+                                                    int Nc, const float* __restrict__ rscale,
+                                                    float* __restrict__ Y) {
+    typedef GemmOp<DT> Op;
+    typedef typename Op::frag frag;
+    __shared__ frag sB[PANEL_KS * PANEL_NB * 64];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int li = lane & 15, lk = lane >> 4;
+    const int nb0 = blockIdx.y * PANEL_NB;
+    const int nbs = min(PANEL_NB, NBP - nb0);  // column blocks of this group
+    const int64_t row = (int64_t)blockIdx.x * PANEL_ROWS + wave * 16 + li;
+    const int KB = (K + Op::KBLK - 1) / Op::KBLK;
+    floatx4 acc[PANEL_NB];
+#pragma unroll
+    for (int j = 0; j < PANEL_NB; j++) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int kb0 = 0; kb0 < KB; kb0 += PANEL_KS) {
+        const int ks = min(PANEL_KS, KB - kb0);
+        __syncthreads();  // the previous stage's fragments are no longer read
+        // the whole stage is written (zero fragments past the K or column
+        // range), so every product below is unconditional
+#pragma unroll 2
+        for (int i = threadIdx.x; i < PANEL_KS * PANEL_NB * 64; i += 256) {
+            const int kk = i / (PANEL_NB * 64), r = i - kk * (PANEL_NB * 64), j = r >> 6, l = r & 63;
+            sB[i] = (kk < ks && j < nbs) ? Wp[((int64_t)(kb0 + kk) * NBP + nb0 + j) * 64 + l] : Op::zero();
         }
+        frag a[PANEL_KS];
+#pragma unroll
+        for (int kk = 0; kk < PANEL_KS; kk++) {
+            const int k = (kb0 + kk) * Op::KBLK + (Op::KBLK / 4) * lk;
+            a[kk] = (kk < ks && row < M && k < K) ? Op::load_a(X, row, K, k) : Op::zero();
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < PANEL_KS; kk++) {
+            frag b[PANEL_NB];
+#pragma unroll
+            for (int j = 0; j < PANEL_NB; j++) b[j] = sB[(kk * PANEL_NB + j) * 64 + lane];
+            Op::template mma_all<PANEL_NB>(a[kk], b, acc);
+        }
+    }
+    // D fragment: lane l holds rows 4*(l/16) + r, column l%16
+    const int64_t rbase = (int64_t)blockIdx.x * PANEL_ROWS + wave * 16 + 4 * lk;
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+        const int64_t orow = rbase + r;
+        if (orow >= M) continue;
+        const float sc = rscale ? rscale[orow] : 1.0f;
+#pragma unroll
+        for (int j = 0; j < PANEL_NB; j++) {
+            const int col = (nb0 + j) * 16 + li;
+            if (j < nbs && col < Nc) Y[orow * Nc + col] = acc[j][r] * sc;
+        }
+    }
 }
 
-void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
-             float* Y, hipStream_t s) {
-    if (M <= 0) return;
+template <int DT>
+static void launch_panel(const void* X, int64_t M, int K, const void* Wp, int Nc, const float* rscale, float* Y,
+                         hipStream_t s) {
     const int NBP = gemm_packed_blocks_n(Nc);
-    dim3 grid((unsigned)ceil_div(M, GEMM_TM), (unsigned)(NBP / (GEMM_TN / 16)));
-    const uint4* wp = reinterpret_cast<const uint4*>(Wp);
-    if (dtype == TAURUS_BF16) k_gemm_16<TAURUS_BF16><<<grid, 256, 0, s>>>(X, M, K, wp, NBP, Nc, rscale, Y);
-    else k_gemm_16<TAURUS_F16><<<grid, 256, 0, s>>>(X, M, K, wp, NBP, Nc, rscale, Y);
+    const auto* w = static_cast<const typename GemmOp<DT>::frag*>(Wp);
+    if (NBP <= 4) {
+        dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), 1);
+        k_gemm_panel<DT, 4><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y);
+    } else {
+        dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), (unsigned)ceil_div(NBP, 8));
+        k_gemm_panel<DT, 8><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y);
+    }
     TAURUS_CHECK_LAUNCH();
 }
 
 void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const float* rscale, float* Y,
               hipStream_t s) {
     if (M <= 0) return;
-    const int NBP = gemm_packed_blocks_n(Nc);
-    dim3 grid((unsigned)ceil_div(M, GEMM_TM), (unsigned)(NBP / (GEMM_TN / 16)));
-    k_gemm_f32<<<grid, 256, 0, s>>>(X, M, K, reinterpret_cast<const float4*>(Wp), NBP, Nc, rscale, Y);
-    TAURUS_CHECK_LAUNCH();
+    launch_panel<TAURUS_F32>(X, M, K, Wp, Nc, rscale, Y, s);
+}
+
+void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
+             float* Y, hipStream_t s) {
+    if (M <= 0) return;
+    if (dtype == TAURUS_BF16) launch_panel<TAURUS_BF16>(X, M, K, Wp, Nc, rscale, Y, s);
+    else launch_panel<TAURUS_F16>(X, M, K, Wp, Nc, rscale, Y, s);
 }
 
 }  // namespace taurus
