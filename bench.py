@@ -221,6 +221,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--full-profile", action="store_true",
+                    help="events around every kernel (adds the transform's MFMA roofline; more events in the stream)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy, the reference kernel for HBM byte counters")
     ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
@@ -250,7 +252,8 @@ def main():
     dst_d = torch.from_numpy(dst).to(dev)
     specs = H.layer_specs(w)
     outs = [torch.empty((w.n, s["d_out"]), dtype=torch.float32, device=dev) for s in specs]
-    profile = not args.no_profile
+    # HIP events around the scatter launches only (2), or every kernel (1)
+    profile = 0 if args.no_profile else (1 if args.full_profile else 2)
     if args.copy_calibration:
         # a plain streaming kernel of known size for the byte counters:
         # neg reads 1 GiB and writes 1 GiB

@@ -118,7 +118,8 @@ typedef struct {
  *                the host link as vertices complete.
  *   stream       hipStream_t on which all work of this layer is enqueued
  *                (NULL = the default stream).
- *   profile      1: time every kernel of the layer with HIP events; the
+ *   profile      1: time every kernel of the layer with HIP events; 2: time
+ *                only the scatter launches (fewer events in the stream); the
  *                totals are returned in taurus_stats.
  *   plan         NULL, or a plan made for this graph (same n, e, row_off,
  *                col_dst pointers) and this chunk size: an exact layer
@@ -164,7 +165,7 @@ typedef struct {
                                       evictions and host-resident output rows out       */
     int64_t device_bytes;          /* peak bytes allocated by the library for the layer */
     double hub_message_share;      /* share of messages landing on resident hubs        */
-    /* milliseconds, HIP-event timed when desc.profile = 1 (else 0) */
+    /* milliseconds, HIP-event timed when desc.profile = 1 (only ms_scatter when 2; else 0) */
     double ms_init;                /* wall time of taurus_layer_init                    */
     double ms_index;               /* of which: sampling and chunk-index build (0 when
                                       the plan already held the index)                  */

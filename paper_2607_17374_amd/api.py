@@ -143,7 +143,7 @@ class Layer:
                  d_out: int, weight_cat: np.ndarray, bias: Optional[np.ndarray], out: torch.Tensor,
                  in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
-                 hub_fraction: float = 0.0, stream=None, profile: bool = False, plan: "Plan" = None):
+                 hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None):
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),

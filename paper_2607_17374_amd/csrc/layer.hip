@@ -1050,6 +1050,7 @@ static void validate_desc(const taurus_layer_desc* d) {
     if (d->out_on_host != 0 && d->out_on_host != 1) fail(TAURUS_E_INVALID, "out_on_host=%d", d->out_on_host);
     if (d->hub_fraction < 0.0 || d->hub_fraction > 1.0) fail(TAURUS_E_INVALID, "hub_fraction %g", d->hub_fraction);
     if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
+    if (d->profile < 0 || d->profile > 2) fail(TAURUS_E_INVALID, "profile %d", d->profile);
 }
 
 static bool same_graph(const taurus_graph& a, const taurus_graph& b) {
@@ -1240,10 +1241,13 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     const ChunkIndex& idx = *L->idx;
     hipStream_t s = L->s;
     if (x_on_host) x = stage_host_chunk(L, x, e - b);
+    // profile 1: events around every kernel; profile 2: around the scatter
+    // launch only (ev[1] and ev[2])
     hipEvent_t ev[EV_PER_CHUNK] = {};
     if (L->d.profile) {
-        for (int i = 0; i < EV_PER_CHUNK; i++) ev[i] = L->events[(size_t)k * EV_PER_CHUNK + i];
-        TAURUS_HIP(hipEventRecord(ev[0], s));
+        for (int i = 0; i < EV_PER_CHUNK; i++)
+            if (L->d.profile == 1 || i == 1 || i == 2) ev[i] = L->events[(size_t)k * EV_PER_CHUNK + i];
+        if (ev[0]) TAURUS_HIP(hipEventRecord(ev[0], s));
     }
     L->pushed[(size_t)k] = 1;
     L->npushed++;
@@ -1343,7 +1347,8 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
             if (!L->pushed[(size_t)k]) continue;
             hipEvent_t* ev = &L->events[(size_t)k * EV_PER_CHUNK];
             float t[EV_PER_CHUNK - 1] = {};
-            for (int i = 0; i + 1 < EV_PER_CHUNK; i++) TAURUS_HIP(hipEventElapsedTime(&t[i], ev[i], ev[i + 1]));
+            for (int i = 0; i + 1 < EV_PER_CHUNK; i++)
+                if (L->d.profile == 1 || i == 1) TAURUS_HIP(hipEventElapsedTime(&t[i], ev[i], ev[i + 1]));
             st->ms_gemm += t[0];
             st->ms_scatter += t[1];
             st->ms_fixup += t[2];
