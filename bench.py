@@ -34,11 +34,13 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
-# a segment of more than this many messages is cut into pieces of this length
-# and completed by the fix-up kernel; the library's work-unit counts are
-# checked against the ones derived here
+# A segment's slots are its messages plus, for the segment from the
+# destination's own chunk, the self message.  Segments of at most SHORT_LEN
+# slots are short units; longer ones are cut into pieces of at most PIECE_LEN
+# slots, and a segment cut into several is completed by the fix-up kernel.
+# The library's work-unit counts are checked against the ones derived here.
 PIECE_LEN = 512
-SHORT_LEN = 8
+SHORT_LEN = 16
 
 
 def flush_model(src, dst, n: int, chunk: int) -> dict:
@@ -67,14 +69,15 @@ def flush_model(src, dst, n: int, chunk: int) -> dict:
     last = np.maximum(maxch, own_v)
     fresh = ch == first[v]
     final = ch == last[v]
-    split = lens > PIECE_LEN
-    pieces = np.where(lens > SHORT_LEN, (lens + PIECE_LEN - 1) // PIECE_LEN, 1)
+    slots = lens + (ch == cv)
+    split = slots > PIECE_LEN
+    pieces = np.where(slots > SHORT_LEN, (slots + PIECE_LEN - 1) // PIECE_LEN, 1)
     has_own = np.zeros(n, dtype=bool)
     has_own[v[ch == cv]] = True
     alone = ~has_own                      # vertices flushing their self message alone
     return {
         "messages": int(src.size), "segments": int(seg.size), "units": int(pieces.sum()),
-        "short_units": int((lens <= SHORT_LEN).sum()), "split_segments": int(split.sum()),
+        "short_units": int((slots <= SHORT_LEN).sum()), "split_segments": int(split.sum()),
         "active_src": int(np.unique(src).size), "own_segments": int(has_own.sum()),
         "sc_flush": int((~split).sum()), "sc_fresh": int((~split & fresh).sum()),
         "sc_final": int((~split & final).sum()), "split_pieces": int(pieces[split].sum()),

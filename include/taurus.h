@@ -94,7 +94,9 @@ typedef struct {
  *   layer        1-based layer number (only feeds the sampling hash).
  *   seed         sampling seed.
  *   chunk        source-chunk size C in vertices (> 0).  Chunk j covers
- *                sources [j*C, min((j+1)*C, n)).
+ *                sources [j*C, min((j+1)*C, n)).  The chunk's transform,
+ *                min(C, n) rows of d_out (GCN) or 2*d_out (GraphSAGE) fp32,
+ *                must fit 2^31 - 2^24 bytes, else TAURUS_E_INVALID.
  *   hbm_budget   bytes of device memory the library may hold for this layer
  *                (its own buffers plus the chunk index it uses; 0 =
  *                unlimited).  When the dense accumulators [n][d_out] fp32 do
@@ -157,8 +159,11 @@ typedef struct {
     int64_t completed;             /* vertices whose output row was written             */
     int64_t pending_left;          /* vertices still waiting for messages               */
     int64_t chunks, chunks_pushed;
-    int64_t short_units;           /* segments of <= 8 messages (one row-group each)    */
-    int64_t wave_units;            /* pieces of longer segments (one wave each)         */
+    int64_t short_units;           /* segments of <= 16 slots, batched per row-group; a
+                                      segment's slots are its messages plus the self
+                                      message when it comes from v's own chunk         */
+    int64_t wave_units;            /* pieces of <= 512 slots of longer segments (one
+                                      wave each)                                        */
     int64_t split_segments;        /* hub segments cut into several pieces              */
     int64_t evictions, reloads;    /* accumulator rows moved to/from host (0 in core)   */
     int64_t h2d_bytes, d2h_bytes;  /* host-link bytes: host chunks and reloads in;

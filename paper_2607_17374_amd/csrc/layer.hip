@@ -52,14 +52,17 @@ void gemm_pack_weights_16(const float* W, int K, int Nc, int dtype, std::vector<
 const char* last_error_cstr();
 
 constexpr int SC_THREADS = 256;
-constexpr int NCLASS = 4;                           // short segment classes
-constexpr int PIECE_LEN = 512;                      // longer segments: pieces of this many messages
+constexpr int NCLASS = 5;                           // short segment classes
+constexpr int PIECE_LEN = 512;                      // longer segments: pieces of this many slots
 constexpr int NOT_FIRST = 1 << 30;                  // unit.y flags (see k_seg_emit)
 constexpr int SELF_HERE = 1 << 29;
 constexpr int LEN_MASK = SELF_HERE - 1;
 constexpr int NLIST = NCLASS + 2;                   // short classes, wave units, fix-up entries
+static_assert(RES_LISTS == NCLASS + 1, "residency walks the short classes and the wave units");
+constexpr uint8_t OWN_SEGMENT = 1;                  // per-vertex flags: v has a segment from its own chunk
+constexpr uint8_t SELF_FIRST = 2;                   //   no message to v comes from an earlier chunk
 
-// longest segment of short class c: 1, 2, 4, 8
+// most slots of a segment in short class c: 1, 2, 4, 8, 16
 __host__ __device__ constexpr int class_len(int c) { return 1 << c; }
 
 // ------------------------------------------------------------ init kernels --
@@ -142,28 +145,37 @@ __global__ void k_seg_starts(const int32_t* __restrict__ head, const int64_t* __
     if (i == 0) seg_start[seg_id[total]] = total;
 }
 
-// work list of a segment: short class 0..NCLASS-1 by length, or NCLASS (wave pieces)
-__device__ inline int seg_class(int64_t len) {
+// work list of a segment: short class 0..NCLASS-1 by slot count, or NCLASS (wave pieces)
+__device__ inline int seg_class(int64_t slots) {
 #pragma unroll
     for (int c = 0; c < NCLASS; c++)
-        if (len <= class_len(c)) return c;
+        if (slots <= class_len(c)) return c;
     return NCLASS;
+}
+
+// A segment's slots: its messages, plus the destination's self message when
+// the segment comes from the destination's own chunk (it rides on that
+// segment's flush as the last slot, one arrival).
+__device__ inline int64_t seg_slots(int64_t len, uint32_t v, uint32_t chunk, int64_t C) {
+    return len + (v / (uint32_t)C == chunk ? 1 : 0);
 }
 
 // Per segment: add its length to the destination's message count, note the
 // destination's first chunk, and count the entries it adds to each list
 // (cnt[list * P + s]; lists = short classes, wave units, fix-up entries).
 __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                               int vbits, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
+                               int vbits, int64_t C, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
                                int32_t* __restrict__ cnt) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
     const uint64_t v = keys[b] & (((uint64_t)1 << vbits) - 1);
+    const uint32_t chunk = (uint32_t)(keys[b] >> vbits);
     atomicAdd(&m[v], (int)len);
-    atomicMin(&first_chunk[v], (int)(keys[b] >> vbits));
-    const int cls = seg_class(len);
-    const int pieces = cls == NCLASS ? (int)((len + PIECE_LEN - 1) / PIECE_LEN) : 0;
+    atomicMin(&first_chunk[v], (int)chunk);
+    const int64_t slots = seg_slots(len, (uint32_t)v, chunk, C);
+    const int cls = seg_class(slots);
+    const int pieces = cls == NCLASS ? (int)((slots + PIECE_LEN - 1) / PIECE_LEN) : 0;
 #pragma unroll
     for (int c = 0; c < NCLASS; c++) cnt[(int64_t)c * P + s] = cls == c ? 1 : 0;
     cnt[(int64_t)NCLASS * P + s] = pieces;
@@ -173,17 +185,19 @@ __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t*
 // Write the work units into one buffer holding the lists one after another;
 // off[l * P + s] = position of segment s's first entry of list l (an
 // exclusive scan of the per-list counts laid out list by list).  unit =
-// {first item relative to its chunk, length | NOT_FIRST, destination, slot}.
-// NOT_FIRST marks a segment that is not its destination's first in ascending
-// chunk order: when chunks are pushed in that order its accumulator row
-// already holds a partial sum, so the scatter may fetch the row together with
-// the counts (the pending count still decides whether the row is used).
-// SELF_HERE marks the segment from v's own chunk: v's self message (its own
-// row of the chunk transform, one arrival) joins that segment's flush
-// instead of being flushed on its own, and has_own[v] is set so the
-// chunk's self pass skips v.  slot = buffer position of a hub segment's
-// piece (its partial row goes to the carry buffer), else -1.  fix-up entry
-// = {destination, position of the first piece, pieces, SELF_HERE or 0}.
+// {first item relative to its chunk, slots | NOT_FIRST | SELF_HERE,
+// destination, slot}.  NOT_FIRST marks a segment that is not its
+// destination's first flush when chunks are pushed in ascending order (the
+// first flush is in the earlier of the first message chunk and the own
+// chunk): its accumulator row then already holds a partial sum, so the
+// scatter fetches the row together with the rows of its messages (the
+// pending count still decides whether the row is used).  SELF_HERE marks a
+// unit whose last slot is the destination's self message (the segment from
+// its own chunk; of a cut segment, the last piece); OWN_SEGMENT is set for
+// that vertex so the chunk's self pass skips it.  A piece covers slots
+// [q * PIECE_LEN, ...) of its segment.  slot = buffer position of a hub
+// segment's piece (its partial row goes to the carry buffer), else -1.
+// fix-up entry = {destination, position of the first piece, pieces, 0}.
 __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
                            int vbits, int64_t C, const int64_t* __restrict__ chunk_off,
                            const int32_t* __restrict__ first_chunk, const int64_t* __restrict__ off,
@@ -196,27 +210,36 @@ __global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __r
     const int v = (int)(key & (((uint64_t)1 << vbits) - 1));
     const int chunk = (int)(key >> vbits);
     const int64_t rel = b - chunk_off[chunk];
-    const int nf = chunk != first_chunk[v] ? NOT_FIRST : 0;
-    const bool own = (uint32_t)v / (uint32_t)C == (uint32_t)chunk;
-    const int self = own ? SELF_HERE : 0;
+    const int own_chunk = (int)((uint32_t)v / (uint32_t)C);
+    const int nf = chunk != min(first_chunk[v], own_chunk) ? NOT_FIRST : 0;
+    const bool own = own_chunk == chunk;
     if (own) {
-        has_own[v] = 1;
+        has_own[v] = OWN_SEGMENT;
         atomicAdd(own_count, 1ull);
     }
-    const int cls = seg_class(len);
+    const int64_t slots = len + (own ? 1 : 0);
+    const int cls = seg_class(slots);
     if (cls < NCLASS) {
-        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)len | nf | self, v, 0);
+        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)slots | nf | (own ? SELF_HERE : 0), v, 0);
         return;
     }
-    const int pieces = (int)((len + PIECE_LEN - 1) / PIECE_LEN);
+    const int pieces = (int)((slots + PIECE_LEN - 1) / PIECE_LEN);
     const int64_t first = off[(int64_t)NCLASS * P + s];
     for (int q = 0; q < pieces; q++) {
         const int64_t o = (int64_t)q * PIECE_LEN;
-        const int plen = (int)min((int64_t)PIECE_LEN, len - o);
-        units[first + q] = pieces > 1 ? make_int4((int)(rel + o), plen | nf, v, (int)(first + q))
-                                      : make_int4((int)(rel + o), plen | nf | self, v, -1);
+        const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
+        const int self = (own && q == pieces - 1) ? SELF_HERE : 0;
+        units[first + q] = make_int4((int)(rel + o), plen | nf | self, v, pieces > 1 ? (int)(first + q) : -1);
     }
-    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, self);
+    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, 0);
+}
+
+// SELF_FIRST: v's own chunk is no later than its first message chunk, so
+// with chunks pushed in ascending order its self message is its first flush
+__global__ void k_self_first(const int32_t* __restrict__ first_chunk, int64_t n, int64_t C,
+                             uint8_t* __restrict__ has_own) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) has_own[v] = (has_own[v] & OWN_SEGMENT) | ((int64_t)first_chunk[v] >= v / C ? SELF_FIRST : 0);
 }
 
 __global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, int32_t* __restrict__ src) {
@@ -254,8 +277,9 @@ struct ScatterParams {
     const float* Y;        // chunk transform, row stride ystride floats
     int64_t ystride;
     int self_col;          // column offset of the self half (GraphSAGE) or 0 (GCN)
+    int y_bytes;           // bytes of Y addressable by the gathers (< 2^31)
     const int32_t* src;    // chunk items: local source row
-    const uint8_t* has_own;  // v has a segment from its own chunk (its self message rides on it)
+    const uint8_t* has_own;  // per vertex: OWN_SEGMENT | SELF_FIRST
     int2* cnt;             // {pending, expected}
     float* acc;            // fp32 accumulator rows, d_o floats each
     const int32_t* slot;   // accumulator row of each vertex (residency pool), or null: row v
@@ -266,7 +290,7 @@ struct ScatterParams {
     const float* bias;     // [d_o]
     void* out;             // [n][d_o]
     float* carry;          // per hub piece of the chunk: [d_o] partial contribution
-    int32_t* carry_cnt;    // per hub piece: message count
+    int32_t* carry_cnt;    // per hub piece: arrival count
     int64_t long_base;     // global index of the chunk's first wave unit (carry slot 0)
     int64_t first_row;     // first vertex of the chunk
     int64_t rows;          // vertices in the chunk
@@ -275,7 +299,20 @@ struct ScatterParams {
 struct ChunkUnits {        // this chunk's slice of the short classes and wave units
     const int4* u[NCLASS + 1];
     int64_t n[NCLASS + 1];
+    // Row-group work of the short classes (longest first) and the self pass
+    // is one sequence of batches laid after the row-groups the wave pieces
+    // occupy; phase c starts at rot[c] of it (rot[NCLASS]: the self pass), so
+    // on a small chunk the phases run side by side on different row-groups
+    // instead of one after another on every row-group.
+    int64_t rot[NCLASS + 1];
 };
+
+// First batch of a phase starting at `rot` of the row-group sequence for
+// row-group gid of `stride` (the batches of gid are those congruent to gid).
+__device__ inline int64_t phase_first(int64_t gid, int64_t rot, int64_t stride) {
+    const int64_t d = (gid - rot) % stride;
+    return d < 0 ? d + stride : d;
+}
 
 __device__ inline float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ inline float4 f4_add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
@@ -314,27 +351,87 @@ __device__ inline float* acc_row(const ScatterParams& p, int v) {
     return p.acc + (int64_t)(p.slot ? p.slot[v] : v) * p.d_o;
 }
 
+// weight of a message slot: GraphSAGE-mean 1/|M(v)| (|M(v)| = expected - 1),
+// GCN 1 (sources are pre-scaled); the self slot always weighs 1
 __device__ inline float seg_scale(int agg, int expect) {
-    // GraphSAGE-mean: 1/|M(v)| (|M(v)| = expect - 1); GCN: sources are pre-scaled
     return agg == 0 ? (expect > 1 ? 1.0f / (float)(expect - 1) : 0.0f) : 1.0f;
 }
 
-// Sole-owner flush of contribution c (already scaled) carrying `count`
-// messages to v.  pe = {pending, expected} as read before the flush.  pre
+// Rows in flight per row-group: 16 slots of up to two float4 per lane, 8 of
+// four.
+__host__ __device__ constexpr int slots_per_round(int vec) { return vec <= 2 ? 16 : 8; }
+
+// Units of short class `len` a row-group takes at once: their rows plus
+// one early accumulator row each stay within 20 rows of up to two float4
+// per lane (10 of four), and at most 8 units.
+__host__ __device__ constexpr int batch_units(int vec, int len) {
+    const int k = (vec <= 2 ? 20 : 10) / (len + 1);
+    return k < 1 ? 1 : (k > 8 ? 8 : k);
+}
+
+// vertices per row-group batch of the self pass
+__host__ __device__ constexpr int self_batch_rows(int vec) { return vec <= 2 ? 8 : 4; }
+
+// Gathers of rows of the chunk transform go through a buffer resource: a
+// slot is the 32-bit byte offset of its row in Y, and an offset past the end
+// of Y (NO_ROW, an empty slot) reads as zeros, so no load is predicated.  A
+// lane reads columns (j*G + lane)*4 .. +3 of the row for j < VEC; columns at
+// or past d_o (widths that do not fill G*VEC float4) hold neighbouring data
+// and are never stored.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+constexpr uint32_t NO_ROW = 0x7fffff00u;   // > any y_bytes; NO_ROW + a row's bytes stays below 2^32
+
+__device__ inline __amdgpu_buffer_rsrc_t y_rsrc(const ScatterParams& p) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)p.Y, (short)0, p.y_bytes, 0x00020000);
+}
+
+// byte offset of local row r's message half, and of its self half
+__device__ inline uint32_t msg_off(const ScatterParams& p, int r) { return (uint32_t)r * (uint32_t)(p.ystride * 4); }
+__device__ inline uint32_t self_off(const ScatterParams& p, int r) {
+    return (uint32_t)r * (uint32_t)(p.ystride * 4) + (uint32_t)p.self_col * 4u;
+}
+
+template <int G, int VEC>
+__device__ inline void gather_row(__amdgpu_buffer_rsrc_t rs, uint32_t off, int lane, float4 (&r)[VEC]) {
+    const uint32_t o = off + (uint32_t)lane * 16u;
+#pragma unroll
+    for (int j = 0; j < VEC; j++) {
+        const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(rs, o, j * G * 16, 0);
+        r[j] = make_float4(__uint_as_float(q.x), __uint_as_float(q.y), __uint_as_float(q.z), __uint_as_float(q.w));
+    }
+}
+
+template <int G, int VEC>
+__device__ inline void load_acc_row(const ScatterParams& p, int v, int lane, float4 (&r)[VEC]) {
+    const float* arow = acc_row(p, v);
+#pragma unroll
+    for (int j = 0; j < VEC; j++) {
+        const int col = (j * G + lane) * 4;
+        r[j] = col < p.d_o ? *reinterpret_cast<const float4*>(arow + col) : f4_zero();
+    }
+}
+
+// Sole-owner flush of contribution c (already weighted) carrying `count`
+// arrivals to v.  pe = {pending, expected} as read before the flush.  pre
 // holds v's accumulator row if it was fetched early (have_pre).
 template <int G, int VEC>
 __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const float4 (&c)[VEC], int count,
                                    int lane, const float4 (&pre)[VEC], bool have_pre) {
     const int left = pe.x - count;
     const bool fresh = pe.x == pe.y;  // nothing accumulated yet: acc[v] is logically zero
-    float* arow = acc_row(p, v);
     float4 t[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; j++) {
-        const int col = (j * G + lane) * 4;
-        t[j] = c[j];
-        if (!fresh && col < p.d_o)
-            t[j] = f4_add(have_pre ? pre[j] : *reinterpret_cast<const float4*>(arow + col), c[j]);
+    for (int j = 0; j < VEC; j++) t[j] = c[j];
+    if (!fresh) {
+        float4 a[VEC];
+        if (have_pre) {
+#pragma unroll
+            for (int j = 0; j < VEC; j++) a[j] = pre[j];
+        } else {
+            load_acc_row<G, VEC>(p, v, lane, a);
+        }
+#pragma unroll
+        for (int j = 0; j < VEC; j++) t[j] = f4_add(a[j], t[j]);
     }
     if (left == 0) {
         const float phi = p.agg == 1 ? 1.0f / sqrtf((float)pe.y) : 1.0f;
@@ -352,6 +449,7 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
             }
         }
     } else {
+        float* arow = acc_row(p, v);
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
             const int col = (j * G + lane) * 4;
@@ -361,283 +459,355 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
     if (lane == 0) p.cnt[v].x = left;
 }
 
-template <int G, int VEC>
-__device__ inline void prefetch_acc(const ScatterParams& p, int v, int lane, float4 (&pre)[VEC]) {
+// Value of `reg[k / G]` held by lane k % G of this row-group (k < NREG * G).
+template <int G, int NREG>
+__device__ inline int rg_pick(const int (&reg)[NREG], int k) {
+    int r = 0;
 #pragma unroll
-    for (int j = 0; j < VEC; j++) {
-        const int col = (j * G + lane) * 4;
-        pre[j] = col < p.d_o ? *reinterpret_cast<const float4*>(acc_row(p, v) + col) : f4_zero();
+    for (int q = 0; q < NREG; q++) {
+        const int t = __shfl(reg[q], k % G, G);
+        if (k / G == q) r = t;
     }
+    return r;
 }
 
-// v's own row of the chunk transform (its self message): the W_self half for
-// GraphSAGE, the normalised row for GCN
-template <int G, int VEC>
-__device__ inline void load_self_row(const ScatterParams& p, int v, int lane, float4 (&srow)[VEC]) {
-    const float* row = p.Y + ((int64_t)v - p.first_row) * p.ystride + p.self_col;
-#pragma unroll
-    for (int j = 0; j < VEC; j++) {
-        const int col = (j * G + lane) * 4;
-        srow[j] = col < p.d_o ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
-    }
-}
-
-// Self pass over the chunk's own vertices that have no segment from this
-// chunk (the others take their self message with that segment): one
-// arrival each, in vertex order -- consecutive rows of Y and of the
-// accumulators.  These vertices have no other flush in the launch.
-template <int G, int VEC>
-__device__ inline void self_rows(const ScatterParams& p) {
+// Short class of segments of at most LEN slots (messages plus the self
+// slot of an own-chunk segment).  A row-group takes K consecutive units of
+// the class at a time, K*LEN slots in all, so that up to 16 rows plus the
+// accumulator rows of the K destinations are in flight at once.  Loads are
+// spread over the row-group's lanes (descriptor k in lane k % G, slot j's
+// row offset in lane j % G) and shared by shuffles.  Slot 0 of a unit with
+// SELF_HERE is the destination's own row (weight 1), its other slots are
+// messages (weight sigma_v).  Software-pipelined: the next batch's row
+// offsets and the descriptors after it are requested while this batch's
+// rows are in flight.
+template <int G, int VEC, int LEN>
+__device__ inline void short_batches(const ScatterParams& p, const int4* __restrict__ units, int64_t n, int64_t rot) {
+    constexpr int SLOTS = slots_per_round(VEC);
+    constexpr int K = batch_units(VEC, LEN);                                  // units per batch
+    constexpr int TS = K * LEN;                                               // slots per batch
+    constexpr int RB = TS < SLOTS ? TS : SLOTS;                               // rows per round
+    static_assert(TS <= SLOTS || K == 1, "a batch of several units fits one round");
+    constexpr int KD = (K + G - 1) / G;                                       // descriptor registers
+    constexpr int CR = (TS + G - 1) / G;                                      // offset registers
     constexpr int NRG = SC_THREADS / G;
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t nb = (n + K - 1) / K;
     const int64_t stride = (int64_t)gridDim.x * NRG;
-    for (int64_t r = (int64_t)blockIdx.x * NRG + rg; r < p.rows; r += stride) {
-        const int v = (int)(p.first_row + r);
-        if (p.has_own[v]) continue;
-        const int2 pe = p.cnt[v];
-        const float* row = p.Y + r * p.ystride + p.self_col;
-        float4 c[VEC], pre[VEC];
+    int64_t b = phase_first((int64_t)blockIdx.x * NRG + rg, rot, stride);
+    if (b >= nb) return;  // the whole row-group
+    const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+
+    // descriptor k of batch bb in lane k % G, register k / G; an empty unit
+    // has no slots and v = -1
+    auto load_desc = [&](int64_t bb, int (&dx)[KD], int (&dy)[KD], int (&dv)[KD]) {
 #pragma unroll
-        for (int j = 0; j < VEC; j++) {
-            const int col = (j * G + lane) * 4;
-            c[j] = col < p.d_o ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
-            pre[j] = f4_zero();
+        for (int q = 0; q < KD; q++) {
+            const int k = q * G + lane;
+            const int64_t u = bb * K + k;
+            int4 w = make_int4(0, 0, -1, 0);
+            if (k < K && bb < nb && u < n) w = units[u];
+            dx[q] = w.x;
+            dy[q] = w.y;
+            dv[q] = w.z;
         }
-        flush_owner<G, VEC>(p, v, pe, c, 1, lane, pre, false);
-    }
-}
-
-// What a unit's flush needs besides its rows: the counts and, when the unit
-// is probably not its vertex's first flush, the accumulator row (hint:
-// NOT_FIRST, or v belongs to this chunk or an earlier one, so its self
-// message came first in ascending order; the pending count decides whether
-// the row is used).  Within one scatter launch each destination has at most
-// one flushing unit and no other kernel touches it, so both may be read at
-// any time before that flush -- which lets a row-group fetch them for its
-// next unit while the current unit's rows are in flight.
-template <int G, int VEC, bool SPEC>
-__device__ inline void fetch_flush_state(const ScatterParams& p, int4 w, int lane, bool flushes, int2& pe,
-                                         float4 (&pre)[VEC], bool& have_pre) {
-    const int v = w.z;
-    pe = p.cnt[v];
-    have_pre = SPEC && flushes && ((w.y & NOT_FIRST) || (int64_t)v < p.first_row + p.rows);
-    if (have_pre) prefetch_acc<G, VEC>(p, v, lane, pre);
-}
-
-template <int LEN>
-__device__ inline void load_codes(const ScatterParams& p, int4 w, int32_t (&code)[LEN]) {
-    const int len = w.y & LEN_MASK;
+    };
+    // slot j = (unit j / LEN, position j % LEN) of the batch in lane j % G
+    auto load_offsets = [&](const int (&dx)[KD], const int (&dy)[KD], const int (&dv)[KD], uint32_t (&off)[CR]) {
 #pragma unroll
-    for (int i = 0; i < LEN; i++) code[i] = (LEN == 1 || i < len) ? p.src[w.x + i] : 0;
-}
-
-template <int G, int VEC, int B>
-__device__ inline void load_rows(const ScatterParams& p, const int32_t* code, int i0, int len, int step, int lane,
-                                 float4 (&rows)[B][VEC]) {
-#pragma unroll
-    for (int u = 0; u < B; u++) {
-        const int i = i0 + u * step;
-        const float* row = p.Y + (int64_t)code[u] * p.ystride;
-#pragma unroll
-        for (int j = 0; j < VEC; j++) {
-            const int col = (j * G + lane) * 4;
-            rows[u][j] = (i < len && col < p.d_o) ? *reinterpret_cast<const float4*>(row + col) : f4_zero();
+        for (int q = 0; q < CR; q++) {
+            const int j = q * G + lane;
+            const int k = j / LEN, i = j % LEN;
+            const int x = rg_pick<G, KD>(dx, k), y = rg_pick<G, KD>(dy, k), v = rg_pick<G, KD>(dv, k);
+            const int self = (y & SELF_HERE) ? 1 : 0;
+            const int slots = y & LEN_MASK;
+            uint32_t o = NO_ROW;
+            if (j < TS && i < slots) {
+                if (self && i == 0) o = self_off(p, (int)((int64_t)v - p.first_row));
+                else o = msg_off(p, p.src[x + i - self]);
+            }
+            off[q] = o;
         }
-    }
-}
+    };
 
-template <int VEC, int B>
-__device__ inline void add_rows(float4 (&sa)[VEC], const float4 (&rows)[B][VEC]) {
-#pragma unroll
-    for (int u = 0; u < B; u++)
-#pragma unroll
-        for (int j = 0; j < VEC; j++) sa[j] = f4_add(sa[j], rows[u][j]);
-}
-
-// Short class of segments of at most LEN messages: each row-group walks the
-// class's units (grid stride), software-pipelined: the first batch of this
-// unit's rows is requested, then the next unit's source codes and flush
-// state and the descriptor after it, and only then are the rows summed and
-// the unit flushed.
-template <int G, int VEC, bool SPEC, int LEN>
-__device__ inline void short_class(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
-    constexpr int NRG = SC_THREADS / G;
-    constexpr int B = LEN * VEC <= 16 ? LEN : 16 / VEC;  // rows in flight per batch
-    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
-    const int64_t stride = (int64_t)gridDim.x * NRG;
-    int64_t un = (int64_t)blockIdx.x * NRG + rg;
-    if (un >= n) return;  // the whole row-group
-    int4 w = units[un];
-    int32_t code[LEN];
-    load_codes<LEN>(p, w, code);
-    int2 pe;
-    float4 pre[VEC];
-    bool have_pre;
-    fetch_flush_state<G, VEC, SPEC>(p, w, lane, true, pe, pre, have_pre);
-    un += stride;
-    int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
+    int dx[KD], dy[KD], dv[KD];
+    uint32_t off[CR];
+    load_desc(b, dx, dy, dv);
+    load_offsets(dx, dy, dv, off);
+    int64_t b1 = b + stride;
+    int nx[KD], ny[KD], nv[KD];
+    load_desc(b1, nx, ny, nv);
     for (;;) {
-        const int len = w.y & LEN_MASK;
-        const bool self = (w.y & SELF_HERE) != 0;
-        float4 rows[B][VEC], srow[VEC];
-        load_rows<G, VEC, B>(p, code, 0, len, 1, lane, rows);
-        if (self) load_self_row<G, VEC>(p, w.z, lane, srow);
-        const bool more = un < n;
-        int32_t ncode[LEN];
-        int2 npe = make_int2(0, 0);
-        float4 npre[VEC];
-        bool nhave = false;
-        if (more) {
-            load_codes<LEN>(p, wn, ncode);
-            fetch_flush_state<G, VEC, SPEC>(p, wn, lane, true, npe, npre, nhave);
+        // this batch's rows (the first round of them), counts and early
+        // accumulator rows
+        float4 rows[RB][VEC];
+        uint32_t so[TS];
+#pragma unroll
+        for (int j = 0; j < TS; j++) so[j] = (uint32_t)__shfl((int)off[j / G], j % G, G);
+#pragma unroll
+        for (int j = 0; j < RB; j++) gather_row<G, VEC>(rs, so[j], lane, rows[j]);
+        int2 pe_l[KD];
+#pragma unroll
+        for (int q = 0; q < KD; q++) pe_l[q] = dv[q] >= 0 ? p.cnt[dv[q]] : make_int2(0, 0);
+        int uy[K], uv[K];
+        float4 pre[K][VEC];
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            uy[k] = __shfl(dy[k / G], k % G, G);
+            uv[k] = __shfl(dv[k / G], k % G, G);
+            if (uv[k] >= 0 && (uy[k] & NOT_FIRST)) load_acc_row<G, VEC>(p, uv[k], lane, pre[k]);
         }
-        const int64_t un2 = un + stride;
-        const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
-        float4 sa[VEC];
+        // next batch's row offsets, and the descriptors of the one after
+        const bool more = b1 < nb;
+        uint32_t noff[CR];
 #pragma unroll
-        for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
-        add_rows<VEC, B>(sa, rows);
+        for (int q = 0; q < CR; q++) noff[q] = NO_ROW;
+        if (more) load_offsets(nx, ny, nv, noff);
+        const int64_t b2 = b1 + stride;
+        int mx[KD], my[KD], mv[KD];
+        load_desc(b2, mx, my, mv);
+        // sum and flush each unit of this batch
 #pragma unroll
-        for (int i0 = B; i0 < LEN; i0 += B) {
-            load_rows<G, VEC, B>(p, code + i0, i0, len, 1, lane, rows);
-            add_rows<VEC, B>(sa, rows);
+        for (int k = 0; k < K; k++) {
+            int2 pe;
+            pe.x = __shfl(pe_l[k / G].x, k % G, G);
+            pe.y = __shfl(pe_l[k / G].y, k % G, G);
+            const float sig = seg_scale(p.agg, pe.y);
+            const float w0 = (uy[k] & SELF_HERE) ? 1.0f : sig;  // slot 0: own row or a message
+            float4 sa[VEC], c[VEC];
+#pragma unroll
+            for (int jv = 0; jv < VEC; jv++) {
+                sa[jv] = f4_zero();
+                c[jv] = f4_scale(w0, rows[(k * LEN) % RB][jv]);
+            }
+#pragma unroll
+            for (int i = 1; i < LEN; i++) {
+                const int j = k * LEN + i;
+                if (j >= RB && j % RB == 0) {  // next round (a single-unit batch)
+#pragma unroll
+                    for (int jj = 0; jj < RB; jj++) gather_row<G, VEC>(rs, so[j + jj], lane, rows[jj]);
+                }
+#pragma unroll
+                for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_add(sa[jv], rows[j % RB][jv]);
+            }
+            if (uv[k] < 0) continue;
+#pragma unroll
+            for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], c[jv]);
+            flush_owner<G, VEC>(p, uv[k], pe, c, uy[k] & LEN_MASK, lane, pre[k], (uy[k] & NOT_FIRST) != 0);
         }
-        const float sig = seg_scale(p.agg, pe.y);
-        float4 c[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = self ? f4_axpy(sig, sa[j], srow[j]) : f4_scale(sig, sa[j]);
-        flush_owner<G, VEC>(p, w.z, pe, c, len + (self ? 1 : 0), lane, pre, have_pre);
         if (!more) break;
-        w = wn;
-        pe = npe;
-        have_pre = nhave;
+        b = b1;
+        b1 = b2;
 #pragma unroll
-        for (int j = 0; j < VEC; j++) pre[j] = npre[j];
+        for (int q = 0; q < KD; q++) {
+            dx[q] = nx[q]; dy[q] = ny[q]; dv[q] = nv[q];
+            nx[q] = mx[q]; ny[q] = my[q]; nv[q] = mv[q];
+        }
 #pragma unroll
-        for (int i = 0; i < LEN; i++) code[i] = ncode[i];
-        un = un2;
-        wn = wn2;
+        for (int q = 0; q < CR; q++) off[q] = noff[q];
     }
 }
 
-// Wave units (pieces of segments longer than the short classes): one per
-// wave; the wave's 64/G row-groups split the piece's rows, reduce across
-// row-groups with cross-lane shuffles, and row-group 0 flushes (or parks the
-// partial row of a hub piece in its carry slot).  Pipelined like the short
-// classes: the next unit's first-round source codes and flush state are
-// requested while this unit's first rows are in flight.
-template <int G, int VEC, bool SPEC>
-__device__ inline void wave_units(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
-    constexpr int R = 64 / G;
-    constexpr int B = 16 / VEC;
+// Wave units (pieces of at most PIECE_LEN slots of the longer segments): one
+// per wave.  The piece's message row offsets are loaded at once, one per
+// lane and register (message i in lane i % 64, register i / 64), and handed
+// out by shuffles; each round every row-group gathers SLOTS rows.  A piece
+// with SELF_HERE (the last piece of an own-chunk segment) holds the
+// destination's own row as its last slot, fetched by row-group 0 beside the
+// rounds.  The row-groups' partial sums are combined with cross-lane
+// shuffles and row-group 0 flushes (or parks the partial row of a hub piece
+// in its carry slot).  The next piece's descriptor is fetched ahead and its
+// offsets are requested while the first round's rows are in flight.
+template <int G, int VEC>
+__device__ inline void wave_pieces(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
+    constexpr int SLOTS = slots_per_round(VEC);
+    constexpr int NREG = PIECE_LEN / 64;
     const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
     const int rg = l64 / G, lane = l64 % G;
     const int64_t wstride = (int64_t)gridDim.x * (SC_THREADS / 64);
     int64_t un = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave;
     if (un >= n) return;  // the whole wave
-    auto round_codes = [&](int4 u, int i0, int32_t (&code)[B]) {
-        const int len = u.y & LEN_MASK;
+    const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    auto load_offsets = [&](int4 w, uint32_t (&cr)[NREG]) {
+        const int items = (w.y & LEN_MASK) - ((w.y & SELF_HERE) ? 1 : 0);
 #pragma unroll
-        for (int k = 0; k < B; k++) {
-            const int i = i0 + k * R;
-            code[k] = i < len ? p.src[u.x + i] : 0;
+        for (int t = 0; t < NREG; t++) {
+            const int i = t * 64 + l64;
+            cr[t] = i < items ? msg_off(p, p.src[w.x + i]) : NO_ROW;
         }
     };
     int4 w = units[un];
-    int32_t code[B];
-    round_codes(w, rg, code);
-    int2 pe;
-    float4 pre[VEC];
-    bool have_pre;
-    fetch_flush_state<G, VEC, SPEC>(p, w, lane, w.w < 0 && rg == 0, pe, pre, have_pre);
-    un += wstride;
-    int4 wn = un < n ? units[un] : make_int4(0, 0, 0, 0);
+    uint32_t cr[NREG];
+    load_offsets(w, cr);
+    int64_t un1 = un + wstride;
+    int4 wn = un1 < n ? units[un1] : make_int4(0, 0, 0, 0);
     for (;;) {
-        const int v = w.z, len = w.y & LEN_MASK;
-        const bool self = rg == 0 && (w.y & SELF_HERE) != 0;  // single-piece units only
-        float4 rows[B][VEC], srow[VEC];
-        load_rows<G, VEC, B>(p, code, rg, len, R, lane, rows);
-        if (self) load_self_row<G, VEC>(p, v, lane, srow);
-        const bool more = un < n;
-        int32_t ncode[B];
-        int2 npe = make_int2(0, 0);
-        float4 npre[VEC];
-        bool nhave = false;
-        if (more) {
-            round_codes(wn, rg, ncode);
-            fetch_flush_state<G, VEC, SPEC>(p, wn, lane, wn.w < 0 && rg == 0, npe, npre, nhave);
-        }
-        const int64_t un2 = un + wstride;
-        const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
+        const int v = w.z, L = w.y & LEN_MASK;
+        const bool self = (w.y & SELF_HERE) != 0;
+        const int items = L - (self ? 1 : 0);
+        const bool flush = w.w < 0;
+        const int2 pe = p.cnt[v];
+        float4 pre[VEC], srow[VEC];
+        const bool have_pre = flush && rg == 0 && (w.y & NOT_FIRST);
+        if (have_pre) load_acc_row<G, VEC>(p, v, lane, pre);
+        gather_row<G, VEC>(rs, self && rg == 0 ? self_off(p, (int)((int64_t)v - p.first_row)) : NO_ROW, lane, srow);
+        const bool more = un1 < n;
+        uint32_t ncr[NREG];
+#pragma unroll
+        for (int t = 0; t < NREG; t++) ncr[t] = NO_ROW;
         float4 sa[VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; j++) sa[j] = f4_zero();
-        add_rows<VEC, B>(sa, rows);
-        for (int i0 = rg + B * R; i0 < len; i0 += B * R) {
-            int32_t c2[B];
-            round_codes(w, i0, c2);
-            load_rows<G, VEC, B>(p, c2, i0, len, R, lane, rows);
-            add_rows<VEC, B>(sa, rows);
+        for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_zero();
+        // one round: SLOTS row offsets of this row-group -> rows -> sum
+        auto round = [&](const uint32_t (&o)[SLOTS]) {
+            float4 rows[SLOTS][VEC];
+#pragma unroll
+            for (int k = 0; k < SLOTS; k++) gather_row<G, VEC>(rs, o[k], lane, rows[k]);
+#pragma unroll
+            for (int k = 0; k < SLOTS; k++)
+#pragma unroll
+                for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_add(sa[jv], rows[k][jv]);
+        };
+        const int nreg = (items + 63) / 64;
+        bool first = true;
+        if constexpr (G <= SLOTS) {
+            // a round takes M registers: slot k of row-group rg is lane
+            // G*rg + k % G of register k / G
+            constexpr int M = SLOTS / G;
+            for (int r = 0; r < nreg; r += M) {
+                uint32_t o[SLOTS];
+#pragma unroll
+                for (int k = 0; k < SLOTS; k++) o[k] = (uint32_t)__shfl((int)cr[k / G], G * rg + k % G, 64);
+                if (first && more) load_offsets(wn, ncr);
+                first = false;
+                round(o);
+#pragma unroll
+                for (int t = 0; t < NREG; t++) cr[t] = t + M < NREG ? cr[t + M] : NO_ROW;
+            }
+        } else {
+            // a register takes G / SLOTS rounds: slot k of row-group rg in
+            // round h is lane G*rg + SLOTS*h + k
+            constexpr int H = G / SLOTS;
+            for (int r = 0; r < nreg; r++) {
+#pragma unroll 1
+                for (int h = 0; h < H; h++) {
+                    uint32_t o[SLOTS];
+#pragma unroll
+                    for (int k = 0; k < SLOTS; k++) o[k] = (uint32_t)__shfl((int)cr[0], G * rg + SLOTS * h + k, 64);
+                    if (first && more) load_offsets(wn, ncr);
+                    first = false;
+                    round(o);
+                }
+#pragma unroll
+                for (int t = 0; t < NREG; t++) cr[t] = t + 1 < NREG ? cr[t + 1] : NO_ROW;
+            }
         }
+        if (first && more) load_offsets(wn, ncr);
+        const int64_t un2 = un1 + wstride;
+        const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
+        const float sig = seg_scale(p.agg, pe.y);
+        float4 c[VEC];
+#pragma unroll
+        for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], srow[jv]);
 #pragma unroll
         for (int d = G; d < 64; d <<= 1)
 #pragma unroll
-            for (int j = 0; j < VEC; j++) {
-                sa[j].x += __shfl_xor(sa[j].x, d, 64);
-                sa[j].y += __shfl_xor(sa[j].y, d, 64);
-                sa[j].z += __shfl_xor(sa[j].z, d, 64);
-                sa[j].w += __shfl_xor(sa[j].w, d, 64);
+            for (int jv = 0; jv < VEC; jv++) {
+                c[jv].x += __shfl_xor(c[jv].x, d, 64);
+                c[jv].y += __shfl_xor(c[jv].y, d, 64);
+                c[jv].z += __shfl_xor(c[jv].z, d, 64);
+                c[jv].w += __shfl_xor(c[jv].w, d, 64);
             }
         if (rg == 0) {
-            const float sig = seg_scale(p.agg, pe.y);
-            float4 c[VEC];
-#pragma unroll
-            for (int j = 0; j < VEC; j++) c[j] = self ? f4_axpy(sig, sa[j], srow[j]) : f4_scale(sig, sa[j]);
-            if (w.w < 0) {
-                flush_owner<G, VEC>(p, v, pe, c, len + (self ? 1 : 0), lane, pre, have_pre);
+            if (flush) {
+                flush_owner<G, VEC>(p, v, pe, c, L, lane, pre, have_pre);
             } else {
                 const int64_t slot = (int64_t)w.w - p.long_base;
                 float* crow = p.carry + slot * p.d_o;
 #pragma unroll
-                for (int j = 0; j < VEC; j++) {
-                    const int col = (j * G + lane) * 4;
-                    if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+                for (int jv = 0; jv < VEC; jv++) {
+                    const int col = (jv * G + lane) * 4;
+                    if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[jv];
                 }
-                if (lane == 0) p.carry_cnt[slot] = len;
+                if (lane == 0) p.carry_cnt[slot] = L;
             }
         }
         if (!more) break;
         w = wn;
-        pe = npe;
-        have_pre = nhave;
-#pragma unroll
-        for (int j = 0; j < VEC; j++) pre[j] = npre[j];
-#pragma unroll
-        for (int k = 0; k < B; k++) code[k] = ncode[k];
-        un = un2;
         wn = wn2;
+        un1 = un2;
+#pragma unroll
+        for (int t = 0; t < NREG; t++) cr[t] = ncr[t];
+    }
+}
+
+// Self pass over the chunk's own vertices without a segment from this
+// chunk (the others take their self message in their segment's flush): one
+// arrival each.  A row-group takes K consecutive vertices at a time --
+// consecutive rows of Y and of the accumulators.  These vertices have no
+// other flush in the launch.
+template <int G, int VEC>
+__device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
+    constexpr int K = self_batch_rows(VEC);
+    constexpr int KD = (K + G - 1) / G;
+    constexpr int NRG = SC_THREADS / G;
+    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t nrg = (int64_t)gridDim.x * NRG;
+    const int64_t stride = nrg * K;
+    const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    for (int64_t r0 = phase_first((int64_t)blockIdx.x * NRG + rg, rot, nrg) * K; r0 < p.rows; r0 += stride) {
+        int fl[KD];
+        int2 pe_l[KD];
+#pragma unroll
+        for (int q = 0; q < KD; q++) {
+            const int k = q * G + lane;
+            const int64_t r = r0 + k;
+            fl[q] = OWN_SEGMENT;  // nothing to do
+            pe_l[q] = make_int2(0, 0);
+            if (k < K && r < p.rows) {
+                fl[q] = p.has_own[p.first_row + r];
+                if (!(fl[q] & OWN_SEGMENT)) pe_l[q] = p.cnt[p.first_row + r];
+            }
+        }
+        float4 rows[K][VEC], pre[K][VEC];
+        int f[K];
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            f[k] = rg_pick<G, KD>(fl, k);
+            const bool todo = !(f[k] & OWN_SEGMENT);
+            gather_row<G, VEC>(rs, todo ? self_off(p, (int)(r0 + k)) : NO_ROW, lane, rows[k]);
+            if (todo && !(f[k] & SELF_FIRST)) load_acc_row<G, VEC>(p, (int)(p.first_row + r0 + k), lane, pre[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < K; k++) {
+            if (f[k] & OWN_SEGMENT) continue;
+            int2 pe;
+            pe.x = __shfl(pe_l[k / G].x, k % G, G);
+            pe.y = __shfl(pe_l[k / G].y, k % G, G);
+            flush_owner<G, VEC>(p, (int)(p.first_row + r0 + k), pe, rows[k], 1, lane, pre[k],
+                                !(f[k] & SELF_FIRST));
+        }
     }
 }
 
 // Degree-bucketed scatter of one chunk, persistent: the grid is sized to
-// what the GPU holds at once and walks the self pass, the short classes,
-// then the wave units.
-// (VEC = 2 without the early accumulator fetch fits 4 waves per SIMD
-// without spilling; the other shapes keep the compiler's own choice)
-template <int G, int VEC, bool SPEC>
-__global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(VEC == 2 && !SPEC ? 4 : 1)))
+// what the GPU holds at once and walks the wave pieces (longest work
+// first), the short classes from long to short, then the self pass.
+template <int G, int VEC>
+__global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
 void k_scatter(ScatterParams p, ChunkUnits cu) {
-    self_rows<G, VEC>(p);
-    short_class<G, VEC, SPEC, 1>(p, cu.u[0], cu.n[0]);
-    short_class<G, VEC, SPEC, 2>(p, cu.u[1], cu.n[1]);
-    short_class<G, VEC, SPEC, 4>(p, cu.u[2], cu.n[2]);
-    short_class<G, VEC, SPEC, 8>(p, cu.u[3], cu.n[3]);
-    wave_units<G, VEC, SPEC>(p, cu.u[NCLASS], cu.n[NCLASS]);
+    wave_pieces<G, VEC>(p, cu.u[NCLASS], cu.n[NCLASS]);
+    short_batches<G, VEC, 16>(p, cu.u[4], cu.n[4], cu.rot[4]);
+    short_batches<G, VEC, 8>(p, cu.u[3], cu.n[3], cu.rot[3]);
+    short_batches<G, VEC, 4>(p, cu.u[2], cu.n[2], cu.rot[2]);
+    short_batches<G, VEC, 2>(p, cu.u[1], cu.n[1], cu.rot[1]);
+    short_batches<G, VEC, 1>(p, cu.u[0], cu.n[0], cu.rot[0]);
+    self_batches<G, VEC>(p, cu.rot[NCLASS]);
 }
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
-// are summed in slot order (plus v's self row if the segment is from v's own
-// chunk) and flushed.
+// (the last one holding the self row of an own-chunk segment) are summed in
+// slot order and flushed.
 template <int G, int VEC>
 __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix) {
     constexpr int NRG = SC_THREADS / G;
@@ -660,22 +830,15 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
         }
         count += p.carry_cnt[first + q];
     }
-    if (f.w & SELF_HERE) {
-        float4 srow[VEC];
-        load_self_row<G, VEC>(p, v, lane, srow);
-#pragma unroll
-        for (int j = 0; j < VEC; j++) c[j] = f4_add(c[j], srow[j]);
-        count += 1;
-    }
     flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane, pre, false);
 }
 
 // ------------------------------------------------------------- dispatch ---
 
 // Scatter configuration: G lanes per row-group with VEC float4 per lane,
-// SPEC early accumulator fetch, and the persistent grid sizes.
+// and the persistent grid size.
 struct ScatterShape {
-    int G, VEC, SPEC;
+    int G, VEC;
     int64_t max_blocks;
 };
 
@@ -684,23 +847,22 @@ static int env_int(const char* name, int dflt) {
     return v && *v ? atoi(v) : dflt;
 }
 
-template <int G, int VEC, bool SPEC>
+template <int G, int VEC>
 static int64_t resident_blocks() {
     int dev = 0, cus = 0, per_cu = 0;
     TAURUS_HIP(hipGetDevice(&dev));
     TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    TAURUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_scatter<G, VEC, SPEC>, SC_THREADS, 0));
+    TAURUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_scatter<G, VEC>, SC_THREADS, 0));
     return (int64_t)std::max(1, cus) * std::max(1, per_cu);
 }
 
-// Row-group shape for an output width: aim for `vec_target` float4 per lane
-// (fewer lanes per destination, more destinations per wave), at least 4 and
-// at most 64 lanes.
+// Row-group shape for an output width: two float4 per lane where the width
+// allows (fewer lanes per destination, more destinations per wave), at least
+// 4 and at most 64 lanes.
 static ScatterShape scatter_shape(int d_o) {
-    const int vec_target = env_int("TAURUS_SCATTER_VEC", 2);
     const int q = (d_o + 3) / 4;
     int g = 4;
-    while (g < 64 && g * vec_target < q) g <<= 1;
+    while (g < 64 && g * 2 < q) g <<= 1;
     int vec = (q + g - 1) / g;
     if (vec == 3) vec = 4;
     if (vec > 4) {
@@ -711,25 +873,30 @@ static ScatterShape scatter_shape(int d_o) {
     ScatterShape sh;
     sh.G = g;
     sh.VEC = vec;
-    sh.SPEC = env_int("TAURUS_SCATTER_SPEC", 0) ? 1 : 0;
     sh.max_blocks = 0;
     return sh;
 }
 
-#define TAURUS_ROW_SHAPES(X) \
-    X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(4, 2) X(8, 2) X(16, 2) X(32, 2) X(64, 2) \
-    X(4, 4) X(8, 4) X(16, 4) X(32, 4) X(64, 4)
+// the shapes scatter_shape() yields for widths 4..1024
+#define TAURUS_ROW_SHAPES(X) X(4, 1) X(4, 2) X(8, 2) X(16, 2) X(32, 2) X(64, 2) X(64, 4)
 
-static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, const ChunkUnits& cu, hipStream_t s) {
-    int64_t want = std::max(ceil_div(cu.n[NCLASS], SC_THREADS / 64), ceil_div(p.rows, SC_THREADS / sh.G));
-    for (int c = 0; c < NCLASS; c++) want = std::max(want, ceil_div(cu.n[c], SC_THREADS / sh.G));
-    const int64_t blocks = std::max<int64_t>(1, std::min(want, sh.max_blocks));
-#define TAURUS_CASE(g, v)                                                                  \
-    if (sh.G == g && sh.VEC == v) {                                                        \
-        if (sh.SPEC) k_scatter<g, v, true><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu); \
-        else k_scatter<g, v, false><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu);        \
-        TAURUS_CHECK_LAUNCH();                                                             \
-        return;                                                                            \
+static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, ChunkUnits cu, hipStream_t s) {
+    const int nrg = SC_THREADS / sh.G;
+    // the row-group sequence: wave pieces' row-groups, then the short
+    // classes from the longest, then the self pass
+    int64_t t = cu.n[NCLASS] * (64 / sh.G);
+    for (int c = NCLASS - 1; c >= 0; c--) {
+        cu.rot[c] = t;
+        t += ceil_div(cu.n[c], batch_units(sh.VEC, class_len(c)));
+    }
+    cu.rot[NCLASS] = t;
+    t += ceil_div(p.rows, self_batch_rows(sh.VEC));
+    const int64_t blocks = std::max<int64_t>(1, std::min(ceil_div(t, nrg), sh.max_blocks));
+#define TAURUS_CASE(g, v)                                                         \
+    if (sh.G == g && sh.VEC == v) {                                               \
+        k_scatter<g, v><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu);           \
+        TAURUS_CHECK_LAUNCH();                                                    \
+        return;                                                                   \
     }
     TAURUS_ROW_SHAPES(TAURUS_CASE)
 #undef TAURUS_CASE
@@ -737,9 +904,8 @@ static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, con
 }
 
 static int64_t scatter_resident_blocks(const ScatterShape& sh) {
-#define TAURUS_CASE(g, v)                                                                  \
-    if (sh.G == g && sh.VEC == v)                                                          \
-        return sh.SPEC ? resident_blocks<g, v, true>() : resident_blocks<g, v, false>();
+#define TAURUS_CASE(g, v) \
+    if (sh.G == g && sh.VEC == v) return resident_blocks<g, v>();
     TAURUS_ROW_SHAPES(TAURUS_CASE)
 #undef TAURUS_CASE
     fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
@@ -768,12 +934,12 @@ struct ChunkIndex {
     Arena arena;
     taurus_graph g{};
     int64_t C = 0, nchunks = 0, kept = 0, segments = 0, max_long_per_chunk = 0;
-    int64_t n_list[NLIST] = {0, 0, 0, 0, 0, 0};
+    int64_t n_list[NLIST] = {};
     bool sampled = false;
     hipStream_t built_on = nullptr;
     hipEvent_t ready = nullptr;    // recorded after the last kernel that writes the index
     int32_t* m = nullptr;          // |M(v)|
-    uint8_t* has_own = nullptr;    // v has a segment from its own chunk
+    uint8_t* has_own = nullptr;    // per vertex: OWN_SEGMENT, SELF_FIRST
     unsigned long long* own_count = nullptr;  // number of such vertices
     int32_t* item_src = nullptr;   // local source row per item
     int4* units = nullptr;         // the work lists, one after another
@@ -830,8 +996,11 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
 
     idx->m = idx->arena.alloc<int32_t>(n, "message counts");
     fill_i32(idx->m, n, 0, s);
-    idx->has_own = idx->arena.alloc<uint8_t>(ceil_div(n, 4) * 4, "own-chunk segment flags");
-    fill_i32(reinterpret_cast<int32_t*>(idx->has_own), ceil_div(n, 4), 0, s);
+    // a vertex without messages is SELF_FIRST; the flags of the others are
+    // set once the segments are known
+    idx->has_own = idx->arena.alloc<uint8_t>(ceil_div(n, 4) * 4, "per-vertex self-message flags");
+    static_assert(SELF_FIRST == 2, "flag bytes are filled as 0x02");
+    fill_i32(reinterpret_cast<int32_t*>(idx->has_own), ceil_div(n, 4), 0x02020202, s);
     idx->own_count = idx->arena.alloc<unsigned long long>(1, "own-chunk segment count");
     fill_i32(reinterpret_cast<int32_t*>(idx->own_count), 2, 0, s);
     idx->chunk_off.assign((size_t)nch + 1, 0);
@@ -901,7 +1070,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
     fill_i32(first_chunk, n, 0x7fffffff, s);
     int32_t* lcnt = tmp.alloc<int32_t>(P * NLIST, "list counts");
-    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, idx->m, first_chunk, lcnt);
+    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m, first_chunk,
+                                                          lcnt);
     TAURUS_CHECK_LAUNCH();
     int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
     scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
@@ -926,6 +1096,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
     k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, doffs, first_chunk, loff,
                                                       idx->units, idx->has_own, idx->own_count);
+    TAURUS_CHECK_LAUNCH();
+    k_self_first<<<(unsigned)ceil_div(n, T), T, 0, s>>>(first_chunk, n, C, idx->has_own);
     TAURUS_CHECK_LAUNCH();
     idx->item_src = idx->arena.alloc<int32_t>(kept, "item sources");
     k_take_src<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(vals, kept, idx->item_src);
@@ -1153,6 +1325,9 @@ static void layer_init(taurus_layer* L) {
     }
 
     // working buffers
+    // the scatter addresses Y with 32-bit byte offsets
+    if (std::min<int64_t>(C, n) * (int64_t)L->ncols * 4 > (int64_t)0x7f000000)
+        fail(TAURUS_E_INVALID, "chunk %lld x %d transform columns exceeds 2 GiB of fp32", (long long)C, L->ncols);
     L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
     const int64_t carry_rows = std::max<int64_t>(1, idx.max_long_per_chunk);
     L->carry = L->arena.alloc<float>(carry_rows * L->d_o, "hub piece carries");
@@ -1273,6 +1448,7 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.Y = L->Y;
     p.ystride = L->ncols;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
+    p.y_bytes = (int)(std::min(L->C, L->n) * (int64_t)L->ncols * 4);
     p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
     p.has_own = idx.has_own;
     p.cnt = L->cnt;

@@ -5,7 +5,7 @@
 
 namespace taurus {
 
-constexpr int RES_LISTS = 5;  // the four short classes and the wave units of a chunk
+constexpr int RES_LISTS = 6;  // the five short classes and the wave units of a chunk
 
 // The destinations one chunk touches: its work units (v = unit.z) and its
 // own vertices [first_row, first_row + rows) (the self message).
