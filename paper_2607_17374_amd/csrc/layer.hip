@@ -54,7 +54,7 @@ const char* last_error_cstr();
 constexpr int SC_THREADS = 256;
 constexpr int NCLASS = 5;                           // short segment classes
 constexpr int PIECE_LEN = 512;                      // longer segments: pieces of this many slots
-constexpr int NOT_FIRST = 1 << 30;                  // unit.y flags (see k_seg_emit)
+constexpr int NOT_FIRST = 1 << 30;                  // unit.y flags (see seg_unit)
 constexpr int SELF_HERE = 1 << 29;
 constexpr int LEN_MASK = SELF_HERE - 1;
 constexpr int NLIST = NCLASS + 2;                   // short classes, wave units, fix-up entries
@@ -161,11 +161,13 @@ __device__ inline int64_t seg_slots(int64_t len, uint32_t v, uint32_t chunk, int
 }
 
 // Per segment: add its length to the destination's message count, note the
-// destination's first chunk, and count the entries it adds to each list
-// (cnt[list * P + s]; lists = short classes, wave units, fix-up entries).
+// destination's first chunk, mark a segment from the destination's own chunk
+// (OWN_SEGMENT; it carries the self message) and record the segment's slot
+// count.
 __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
                                int vbits, int64_t C, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
-                               int32_t* __restrict__ cnt) {
+                               int32_t* __restrict__ slots_of, uint8_t* __restrict__ has_own,
+                               unsigned long long* __restrict__ own_count) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
@@ -174,64 +176,138 @@ __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t*
     atomicAdd(&m[v], (int)len);
     atomicMin(&first_chunk[v], (int)chunk);
     const int64_t slots = seg_slots(len, (uint32_t)v, chunk, C);
-    const int cls = seg_class(slots);
-    const int pieces = cls == NCLASS ? (int)((slots + PIECE_LEN - 1) / PIECE_LEN) : 0;
-#pragma unroll
-    for (int c = 0; c < NCLASS; c++) cnt[(int64_t)c * P + s] = cls == c ? 1 : 0;
-    cnt[(int64_t)NCLASS * P + s] = pieces;
-    cnt[(int64_t)(NCLASS + 1) * P + s] = pieces > 1 ? 1 : 0;
-}
-
-// Write the work units into one buffer holding the lists one after another;
-// off[l * P + s] = position of segment s's first entry of list l (an
-// exclusive scan of the per-list counts laid out list by list).  unit =
-// {first item relative to its chunk, slots | NOT_FIRST | SELF_HERE,
-// destination, slot}.  NOT_FIRST marks a segment that is not its
-// destination's first flush when chunks are pushed in ascending order (the
-// first flush is in the earlier of the first message chunk and the own
-// chunk): its accumulator row then already holds a partial sum, so the
-// scatter fetches the row together with the rows of its messages (the
-// pending count still decides whether the row is used).  SELF_HERE marks a
-// unit whose last slot is the destination's self message (the segment from
-// its own chunk; of a cut segment, the last piece); OWN_SEGMENT is set for
-// that vertex so the chunk's self pass skips it.  A piece covers slots
-// [q * PIECE_LEN, ...) of its segment.  slot = buffer position of a hub
-// segment's piece (its partial row goes to the carry buffer), else -1.
-// fix-up entry = {destination, position of the first piece, pieces, 0}.
-__global__ void k_seg_emit(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                           int vbits, int64_t C, const int64_t* __restrict__ chunk_off,
-                           const int32_t* __restrict__ first_chunk, const int64_t* __restrict__ off,
-                           int4* __restrict__ units, uint8_t* __restrict__ has_own,
-                           unsigned long long* __restrict__ own_count) {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= P) return;
-    const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
-    const uint64_t key = keys[b];
-    const int v = (int)(key & (((uint64_t)1 << vbits) - 1));
-    const int chunk = (int)(key >> vbits);
-    const int64_t rel = b - chunk_off[chunk];
-    const int own_chunk = (int)((uint32_t)v / (uint32_t)C);
-    const int nf = chunk != min(first_chunk[v], own_chunk) ? NOT_FIRST : 0;
-    const bool own = own_chunk == chunk;
-    if (own) {
+    if (slots > len) {
         has_own[v] = OWN_SEGMENT;
         atomicAdd(own_count, 1ull);
     }
-    const int64_t slots = len + (own ? 1 : 0);
+    slots_of[s] = (int32_t)slots;
+}
+
+// entries segment s adds to work list l: 1 in its short class, its pieces in
+// the wave list, 1 in the fix-up list when cut into several pieces
+__device__ inline int list_entries(int l, int64_t slots) {
     const int cls = seg_class(slots);
-    if (cls < NCLASS) {
-        units[off[(int64_t)cls * P + s]] = make_int4((int)rel, (int)slots | nf | (own ? SELF_HERE : 0), v, 0);
-        return;
+    if (l < NCLASS) return cls == l ? 1 : 0;
+    const int pieces = cls == NCLASS ? (int)((slots + PIECE_LEN - 1) / PIECE_LEN) : 0;
+    return l == NCLASS ? pieces : (pieces > 1 ? 1 : 0);
+}
+
+__global__ void k_list_counts(const int32_t* __restrict__ slots_of, int64_t P, int l, int32_t* __restrict__ cnt) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s < P) cnt[s] = list_entries(l, slots_of[s]);
+}
+
+// all lists at once: cnt[l * P + s] = entries of segment s in list l
+__global__ void k_list_counts_all(const int32_t* __restrict__ slots_of, int64_t P, int32_t* __restrict__ cnt) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= P) return;
+    const int64_t slots = slots_of[s];
+#pragma unroll
+    for (int l = 0; l < NLIST; l++) cnt[(int64_t)l * P + s] = list_entries(l, slots);
+}
+
+// totals[l] += entries of every segment in list l (one block-level sum per
+// list, then one atomic per block and list)
+__global__ __launch_bounds__(256) void k_list_totals(const int32_t* __restrict__ slots_of, int64_t P,
+                                                     unsigned long long* __restrict__ totals) {
+    __shared__ unsigned long long part[NLIST];
+    if (threadIdx.x < NLIST) part[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s < P) {
+        const int64_t slots = slots_of[s];
+#pragma unroll
+        for (int l = 0; l < NLIST; l++) {
+            const int c = list_entries(l, slots);
+            if (c) atomicAdd(&part[l], (unsigned long long)c);
+        }
     }
+    __syncthreads();
+    if (threadIdx.x < NLIST && part[threadIdx.x]) atomicAdd(&totals[threadIdx.x], part[threadIdx.x]);
+}
+
+// bases[k] = position in list l (offsets `off`, an exclusive scan of the
+// list's entries per segment) of chunk k's first entry; chunk_seg[k] = the
+// chunk's first segment, chunk_seg[nchunks] = P
+__global__ void k_list_chunk_bases(const int64_t* __restrict__ chunk_seg, int64_t nchunks,
+                                   const int64_t* __restrict__ off, int64_t* __restrict__ bases) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k <= nchunks) bases[k] = off[chunk_seg[k]];
+}
+
+__global__ void k_chunk_segments(const int64_t* __restrict__ chunk_off, int64_t nchunks,
+                                 const int64_t* __restrict__ seg_id, int64_t* __restrict__ chunk_seg) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k <= nchunks) chunk_seg[k] = seg_id[chunk_off[k]];
+}
+
+// What a unit of segment s says besides its slots: {first item relative to
+// its chunk, NOT_FIRST, destination, SELF_HERE when the segment carries the
+// self message}.  NOT_FIRST marks a segment that is not its destination's
+// first flush when chunks are pushed in ascending order (the first flush is
+// in the earlier of the first message chunk and the own chunk): its
+// accumulator row then already holds a partial sum, so the scatter fetches
+// the row together with the rows of its messages (the pending count still
+// decides whether the row is used).
+struct SegUnit {
+    int64_t rel;
+    int nf, v, self;
+};
+__device__ inline SegUnit seg_unit(const uint64_t* keys, const int64_t* seg_start, int64_t s, int vbits, int64_t C,
+                                   const int64_t* chunk_off, const int32_t* first_chunk) {
+    const int64_t b = seg_start[s];
+    const uint64_t key = keys[b];
+    SegUnit u;
+    u.v = (int)(key & (((uint64_t)1 << vbits) - 1));
+    const int chunk = (int)(key >> vbits);
+    u.rel = b - chunk_off[chunk];
+    const int own_chunk = (int)((uint32_t)u.v / (uint32_t)C);
+    u.nf = chunk != min(first_chunk[u.v], own_chunk) ? NOT_FIRST : 0;
+    u.self = own_chunk == chunk ? SELF_HERE : 0;
+    return u;
+}
+
+// Short class l: unit = {first item, slots | NOT_FIRST | SELF_HERE, v, 0} at
+// off[s] (the list's exclusive scan).
+__global__ void k_emit_short(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start,
+                             const int32_t* __restrict__ slots_of, int64_t P, int l, int vbits, int64_t C,
+                             const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
+                             const int64_t* __restrict__ off, int4* __restrict__ units) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= P) return;
+    const int slots = slots_of[s];
+    if (seg_class(slots) != l) return;
+    const SegUnit u = seg_unit(keys, seg_start, s, vbits, C, chunk_off, first_chunk);
+    units[off[s]] = make_int4((int)u.rel, slots | u.nf | u.self, u.v, 0);
+}
+
+// Longer segments: piece q covers slots [q * PIECE_LEN, ...) of the segment;
+// the self slot is the segment's last slot, so SELF_HERE goes on its last
+// piece.  A piece = {first item, slots | flags, v, slot}, slot = its position
+// in the work-list buffer (base + its position in the wave list) when the
+// segment has several pieces (a hub: its partial row goes to the carry
+// buffer), else -1.  A hub also gets a fix-up entry {v, buffer position of
+// its first piece, pieces, 0} at fix_off[s].
+__global__ void k_emit_long(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start,
+                            const int32_t* __restrict__ slots_of, int64_t P, int vbits, int64_t C,
+                            const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
+                            const int64_t* __restrict__ off, const int64_t* __restrict__ fix_off,
+                            int4* __restrict__ units, int4* __restrict__ fix, int base) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= P) return;
+    const int64_t slots = slots_of[s];
+    if (seg_class(slots) != NCLASS) return;
+    const SegUnit u = seg_unit(keys, seg_start, s, vbits, C, chunk_off, first_chunk);
     const int pieces = (int)((slots + PIECE_LEN - 1) / PIECE_LEN);
-    const int64_t first = off[(int64_t)NCLASS * P + s];
+    const int64_t first = off[s];
     for (int q = 0; q < pieces; q++) {
         const int64_t o = (int64_t)q * PIECE_LEN;
         const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
-        const int self = (own && q == pieces - 1) ? SELF_HERE : 0;
-        units[first + q] = make_int4((int)(rel + o), plen | nf | self, v, pieces > 1 ? (int)(first + q) : -1);
+        const int self = q == pieces - 1 ? u.self : 0;
+        units[first + q] =
+            make_int4((int)(u.rel + o), plen | u.nf | self, u.v, pieces > 1 ? base + (int)(first + q) : -1);
     }
-    if (pieces > 1) units[off[(int64_t)(NCLASS + 1) * P + s]] = make_int4(v, (int)first, pieces, 0);
+    if (pieces > 1) fix[fix_off[s]] = make_int4(u.v, base + (int)first, pieces, 0);
 }
 
 // SELF_FIRST: v's own chunk is no later than its first message chunk, so
@@ -245,18 +321,6 @@ __global__ void k_self_first(const int32_t* __restrict__ first_chunk, int64_t n,
 __global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, int32_t* __restrict__ src) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < total) src[i] = (int32_t)vals[i];
-}
-
-// per-chunk starts of every list: the scan at each chunk's first segment
-// (chunk_off[nchunks] = total maps to segment P, i.e. the end of each list)
-__global__ void k_chunk_unit_bases(const int64_t* __restrict__ chunk_off, int64_t nchunks,
-                                   const int64_t* __restrict__ seg_id, const int64_t* __restrict__ off, int64_t P,
-                                   int64_t* __restrict__ bases) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k > nchunks) return;
-    const int64_t s = seg_id[chunk_off[k]];
-#pragma unroll
-    for (int l = 0; l < NLIST; l++) bases[k * NLIST + l] = off[(int64_t)l * P + s];
 }
 
 __global__ __launch_bounds__(256) void k_count_pending(const int2* __restrict__ cnt, int64_t n,
@@ -1036,6 +1100,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     radix_sort_u64(sb, e, vbits + cbits, tmp, s, bad, 8);
     const uint64_t* keys = sb.keys[sb.cur];
     const uint32_t* vals = sb.vals[sb.cur];
+    tmp.free_ptr(sb.keys[1 - sb.cur]);
+    tmp.free_ptr(sb.vals[1 - sb.cur]);
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
     k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, e, nch, vbits, doffs);
     TAURUS_CHECK_LAUNCH();
@@ -1063,42 +1129,122 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         return idx;
     }
 
-    // segments into the work lists
+    // segments into the work lists, list by list with one count buffer and
+    // one offset buffer (two for the wave pieces and their fix-up entries)
     int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
     k_seg_starts<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(head, seg_id, kept, seg_start);
     TAURUS_CHECK_LAUNCH();
+    int64_t* chunk_seg = tmp.alloc<int64_t>(nch + 1, "first segment per chunk");
+    k_chunk_segments<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, chunk_seg);
+    TAURUS_CHECK_LAUNCH();
+    tmp.free_ptr(head);
+    tmp.free_ptr(seg_id);
     int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
     fill_i32(first_chunk, n, 0x7fffffff, s);
-    int32_t* lcnt = tmp.alloc<int32_t>(P * NLIST, "list counts");
+    int32_t* slots_of = tmp.alloc<int32_t>(P, "segment slots");
     k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m, first_chunk,
-                                                          lcnt);
-    TAURUS_CHECK_LAUNCH();
-    int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
-    scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
-    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list bases");
-    k_chunk_unit_bases<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, loff, P, dbases);
-    TAURUS_CHECK_LAUNCH();
-    std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);
-    int64_t total_units = 0;
-    {
-        Readback rb;
-        rb.add(bases.data(), dbases, (nch + 1) * NLIST);
-        rb.add(&total_units, loff + P * NLIST, 1);
-        rb.run(s);
-    }
-    for (int l = 0; l < NLIST; l++) {
-        for (int64_t k = 0; k <= nch; k++) idx->list_off[l][(size_t)k] = bases[(size_t)k * NLIST + l];
-        idx->n_list[l] = idx->list_off[l][(size_t)nch] - idx->list_off[l][0];
-    }
-    for (int64_t k = 0; k < nch; k++)
-        idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->list_count(NCLASS, k));
-    if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
-    idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
-    k_seg_emit<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, doffs, first_chunk, loff,
-                                                      idx->units, idx->has_own, idx->own_count);
+                                                          slots_of, idx->has_own, idx->own_count);
     TAURUS_CHECK_LAUNCH();
     k_self_first<<<(unsigned)ceil_div(n, T), T, 0, s>>>(first_chunk, n, C, idx->has_own);
     TAURUS_CHECK_LAUNCH();
+    // Unit positions: one exclusive scan over all lists (P * NLIST counts,
+    // positions absolute in the work-list buffer), or, when those arrays
+    // would be large, list by list with one count buffer and one offset
+    // buffer (two for the wave pieces and their fix-up entries).  Both give
+    // the same lists.
+    const int lean_env = env_int("TAURUS_INDEX_LEAN", -1);
+    const bool lean = lean_env >= 0 ? lean_env != 0 : P * NLIST * 12 > ((int64_t)1 << 30);
+    const unsigned gP = (unsigned)ceil_div(P, T), gC = (unsigned)ceil_div(nch + 1, T);
+    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list bases");
+    std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);
+    int64_t list_base[NLIST + 1] = {0};
+    if (!lean) {
+        int32_t* lcnt = tmp.alloc<int32_t>(P * NLIST, "list counts");
+        k_list_counts_all<<<gP, T, 0, s>>>(slots_of, P, lcnt);
+        TAURUS_CHECK_LAUNCH();
+        int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
+        scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
+        for (int l = 0; l < NLIST; l++) {
+            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff + (int64_t)l * P, dbases + (int64_t)l * (nch + 1));
+            TAURUS_CHECK_LAUNCH();
+        }
+        int64_t total_units = 0;
+        {
+            Readback rb;
+            rb.add(bases.data(), dbases, (nch + 1) * NLIST);
+            rb.add(&total_units, loff + P * NLIST, 1);
+            rb.run(s);
+        }
+        if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
+        idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
+        for (int l = 0; l < NCLASS; l++) {
+            k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, l, vbits, C, doffs, first_chunk,
+                                          loff + (int64_t)l * P, idx->units);
+            TAURUS_CHECK_LAUNCH();
+        }
+        k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk,
+                                     loff + (int64_t)NCLASS * P, loff + (int64_t)(NCLASS + 1) * P, idx->units,
+                                     idx->units, 0);
+        TAURUS_CHECK_LAUNCH();
+        for (int l = 0; l < NLIST; l++) {
+            for (int64_t k = 0; k <= nch; k++) idx->list_off[l][(size_t)k] = bases[(size_t)l * (nch + 1) + (size_t)k];
+            idx->n_list[l] = idx->list_off[l][(size_t)nch] - idx->list_off[l][0];
+        }
+    } else {
+        unsigned long long* dtot = tmp.alloc<unsigned long long>(NLIST, "list totals");
+        fill_i32(reinterpret_cast<int32_t*>(dtot), 2 * NLIST, 0, s);
+        k_list_totals<<<gP, T, 0, s>>>(slots_of, P, dtot);
+        TAURUS_CHECK_LAUNCH();
+        unsigned long long tot[NLIST] = {};
+        {
+            Readback rb;
+            rb.add(tot, dtot, NLIST);
+            rb.run(s);
+        }
+        for (int l = 0; l < NLIST; l++) list_base[l + 1] = list_base[l] + (int64_t)tot[l];
+        const int64_t total_units = list_base[NLIST];
+        if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
+        idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
+        int32_t* lcnt = tmp.alloc<int32_t>(P, "list counts");
+        int64_t* loff = tmp.alloc<int64_t>(P + 1, "list offsets");
+        for (int l = 0; l < NCLASS; l++) {
+            k_list_counts<<<gP, T, 0, s>>>(slots_of, P, l, lcnt);
+            TAURUS_CHECK_LAUNCH();
+            scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
+            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, dbases + (int64_t)l * (nch + 1));
+            TAURUS_CHECK_LAUNCH();
+            k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, l, vbits, C, doffs, first_chunk, loff,
+                                          idx->units + list_base[l]);
+            TAURUS_CHECK_LAUNCH();
+        }
+        int64_t* loff_fix = tmp.alloc<int64_t>(P + 1, "fix-up list offsets");
+        k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS + 1, lcnt);
+        TAURUS_CHECK_LAUNCH();
+        scan_i32_to_i64(lcnt, loff_fix, P, true, tmp, s);
+        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff_fix, dbases + (int64_t)(NCLASS + 1) * (nch + 1));
+        TAURUS_CHECK_LAUNCH();
+        k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS, lcnt);
+        TAURUS_CHECK_LAUNCH();
+        scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
+        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, dbases + (int64_t)NCLASS * (nch + 1));
+        TAURUS_CHECK_LAUNCH();
+        k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk, loff, loff_fix,
+                                     idx->units + list_base[NCLASS], idx->units + list_base[NCLASS + 1],
+                                     (int)list_base[NCLASS]);
+        TAURUS_CHECK_LAUNCH();
+        {
+            Readback rb;
+            rb.add(bases.data(), dbases, (nch + 1) * NLIST);
+            rb.run(s);
+        }
+        for (int l = 0; l < NLIST; l++) {
+            for (int64_t k = 0; k <= nch; k++)
+                idx->list_off[l][(size_t)k] = list_base[l] + bases[(size_t)l * (nch + 1) + (size_t)k];
+            idx->n_list[l] = (int64_t)tot[l];
+        }
+    }
+    for (int64_t k = 0; k < nch; k++)
+        idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->list_count(NCLASS, k));
     idx->item_src = idx->arena.alloc<int32_t>(kept, "item sources");
     k_take_src<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(vals, kept, idx->item_src);
     TAURUS_CHECK_LAUNCH();

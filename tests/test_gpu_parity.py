@@ -157,6 +157,33 @@ def test_gcn_scaled_workload(torch_cuda):
     assert all(st["split_segments"] > 0 for st in stats)   # hubs straddle tiles
 
 
+@pytest.mark.parametrize("which", ["gcn-scaled", "sage-4k"])
+def test_lean_index_build_same_lists(torch_cuda, which):
+    """The memory-lean chunk-index build (work lists one at a time, used for
+    large graphs) gives the same work lists as the single-scan build: the
+    outputs are bit-identical and match the oracle."""
+    import os
+    w = WL.GCN_RMAT_1M.scaled(30000, 400000, chunk=4096) if which == "gcn-scaled" else WL.SAGE_RMAT_4K
+    _note(f"lean index {w.name}")
+    src, dst = WL.graph(w)
+    _, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    got = {}
+    try:
+        for lean in ("0", "1"):
+            os.environ["TAURUS_INDEX_LEAN"] = lean
+            outs, stats = H.gpu_model(w, row_off, col_dst)
+            got[lean] = ([o.cpu() for o in outs], stats)
+    finally:
+        os.environ.pop("TAURUS_INDEX_LEAN", None)
+    for a, b in zip(got["0"][0], got["1"][0]):
+        assert torch_cuda.equal(a, b)
+    for sa, sb in zip(got["0"][1], got["1"][1]):
+        for k in ("short_units", "wave_units", "split_segments", "pairs", "messages"):
+            assert sa[k] == sb[k], k
+    _check_model(w, got["1"][0], zs, f"{w.name} lean")
+
+
 def test_gcn_full_size_bench_configuration(torch_cuda):
     """The benchmark workload (1M vertices, 20M edges, 64K chunks), every output row."""
     w = WL.GCN_RMAT_1M
