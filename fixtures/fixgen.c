@@ -25,6 +25,7 @@
 #include <stdlib.h>
 #include <string.h>
 #include <omp.h>
+#include <stdio.h>
 
 #define FX_GAMMA 0x9e3779b97f4a7c15ULL
 
@@ -142,6 +143,9 @@ int64_t fx_rmat(uint64_t seed, int64_t n, int64_t e, double a, double b, double 
         }
         attempt += batch;
         if (attempt > e * 64 + (int64_t)max_batch * 4) { err = 2; break; }
+        /* large graphs take minutes: a progress line every 2^28 edges */
+        if (e >= ((int64_t)1 << 28) && (accepted >> 28) != ((accepted - batch) >> 28) && accepted < e)
+            fprintf(stderr, "rmat: %lld of %lld edges\n", (long long)accepted, (long long)e);
     }
     for (int t = 0; t < nthr; t++) free(sets[t].slots);
     free(sets); free(cand); free(ok);

@@ -70,6 +70,16 @@ def load(path: str):
     L.or_total_span.argtypes = [i64, vp, vp, vp]
     L.or_threads.restype = i32
     L.or_threads.argtypes = []
+    L.or_in_lists_from_edges.restype = i32
+    L.or_in_lists_from_edges.argtypes = [i64, i64, vp, vp, vp, vp, vp]
+    L.or_digest_edges.restype = None
+    L.or_digest_edges.argtypes = [i64, vp, vp, vp]
+    L.or_digest_csr.restype = None
+    L.or_digest_csr.argtypes = [i64, vp, vp, vp, vp]
+    L.or_digest_in_lists.restype = None
+    L.or_digest_in_lists.argtypes = [i64, vp, vp, vp, vp]
+    L.or_csr_check.restype = i32
+    L.or_csr_check.argtypes = [i64, i64, vp, vp]
     return L
 
 
@@ -106,14 +116,70 @@ class Graph:
         self.deg_in = np.diff(self.in_off).astype(np.int32)
 
 
+class EdgeGraph:
+    """In-neighbour lists and out-degrees built straight from the edge list
+    (no CSR and no sort of the pairs), for graphs too large for ``Graph``.
+    Usable by ``layer``, ``sample`` (keep_in and m only) and
+    ``reorder_bfs``."""
+
+    def __init__(self, n: int, src: np.ndarray, dst: np.ndarray):
+        src = np.ascontiguousarray(src, np.int32)
+        dst = np.ascontiguousarray(dst, np.int32)
+        self.n, self.e = n, src.size
+        self.in_off = np.empty(n + 1, np.int64)
+        self.in_src = np.empty(self.e, np.int32)
+        self.deg_out = np.empty(n, np.int32)
+        if lib().or_in_lists_from_edges(n, self.e, _p(src), _p(dst), _p(self.in_off), _p(self.in_src),
+                                        _p(self.deg_out)):
+            raise MemoryError("or_in_lists_from_edges")
+        self.deg_in = np.diff(self.in_off).astype(np.int32)
+        self.row_off = None
+        self.in_pos = None
+
+
+def digest_edges(src: np.ndarray, dst: np.ndarray) -> tuple:
+    """(count, sum, xor) set digest of the pairs (src[i], dst[i])."""
+    src = np.ascontiguousarray(src, np.int32)
+    dst = np.ascontiguousarray(dst, np.int32)
+    out = np.zeros(3, np.uint64)
+    lib().or_digest_edges(src.size, _p(src), _p(dst), _p(out))
+    return tuple(int(x) for x in out)
+
+
+def digest_csr(n: int, row_off: np.ndarray, col_dst: np.ndarray, mask_words: np.ndarray | None = None) -> tuple:
+    """Set digest of a CSR's edges (only those whose mask bit is set, if given)."""
+    row_off = np.ascontiguousarray(row_off, np.int64)
+    col_dst = np.ascontiguousarray(col_dst, np.int32)
+    mw = None if mask_words is None else np.ascontiguousarray(mask_words, np.uint64)
+    out = np.zeros(3, np.uint64)
+    lib().or_digest_csr(n, _p(row_off), _p(col_dst), _p(mw), _p(out))
+    return tuple(int(x) for x in out)
+
+
+def digest_in_lists(g, keep_in: np.ndarray | None = None) -> tuple:
+    """Set digest of the (u, v) pairs of g's in-lists (kept entries only, if given)."""
+    kin = None if keep_in is None else np.ascontiguousarray(keep_in, np.uint8)
+    out = np.zeros(3, np.uint64)
+    lib().or_digest_in_lists(g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(out))
+    return tuple(int(x) for x in out)
+
+
+def csr_check(n: int, row_off: np.ndarray, col_dst: np.ndarray) -> int:
+    """0 if the CSR has the canonical shape (see or_csr_check), else the rule it breaks."""
+    row_off = np.ascontiguousarray(row_off, np.int64)
+    col_dst = np.ascontiguousarray(col_dst, np.int32)
+    return int(lib().or_csr_check(n, col_dst.size, _p(row_off), _p(col_dst)))
+
+
 def hash_u64(seed: int, tag: int, *args: int) -> int:
     a = np.array(args, dtype=np.uint64) if args else np.zeros(1, np.uint64)
     return int(lib().or_hash(seed & (2**64 - 1), tag, len(args), _p(a)))
 
 
-def sample(g: Graph, seed: int, layer: int, k: int):
-    """Fanout mask of one layer -> (mask_words uint64[ceil(e/64)], keep_in uint8[e], m int32[n])."""
-    words = np.zeros((g.e + 63) // 64, np.uint64)
+def sample(g, seed: int, layer: int, k: int):
+    """Fanout mask of one layer -> (mask_words uint64[ceil(e/64)], keep_in uint8[e], m int32[n]).
+    For an EdgeGraph (no CSR positions) mask_words is None."""
+    words = np.zeros((g.e + 63) // 64, np.uint64) if g.in_pos is not None else None
     keep_in = np.zeros(g.e, np.uint8)
     m = np.zeros(g.n, np.int32)
     lib().or_sample(g.n, _p(g.row_off), _p(g.in_off), _p(g.in_src), _p(g.in_pos),

@@ -104,6 +104,122 @@ int or_build_in_lists(int64_t n, const int64_t* row_off, const int32_t* col_dst,
     return 0;
 }
 
+/*
+ * In-neighbour lists straight from the edge list, for graphs too large for
+ * the sort above: N^-(v) = {u : (u, v) in E}, sources ascending, by counting
+ * in-degrees, placing each source, then sorting each list.  Also the
+ * out-degree of every vertex.  The pairs are assumed valid and distinct (the
+ * generator's promise; the CSR checks below test the GPU's CSR against the
+ * same list).  Returns 0, or -3 when out of memory.
+ */
+static int or_i32_cmp(const void* x, const void* y) {
+    int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
+    return (a > b) - (a < b);
+}
+int or_in_lists_from_edges(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* in_off,
+                           int32_t* in_src, int32_t* deg_out) {
+    int64_t* fill = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    if (!fill) return -3;
+#pragma omp parallel for schedule(static)
+    for (int64_t v = 0; v <= n; v++) in_off[v] = 0;
+#pragma omp parallel for schedule(static)
+    for (int64_t v = 0; v < n; v++) deg_out[v] = 0;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < e; i++) {
+        __atomic_fetch_add(&in_off[dst[i] + 1], 1, __ATOMIC_RELAXED);
+        __atomic_fetch_add(&deg_out[src[i]], 1, __ATOMIC_RELAXED);
+    }
+    for (int64_t v = 0; v < n; v++) in_off[v + 1] += in_off[v];
+#pragma omp parallel for schedule(static)
+    for (int64_t v = 0; v < n; v++) fill[v] = in_off[v];
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < e; i++) {
+        int64_t k = __atomic_fetch_add(&fill[dst[i]], 1, __ATOMIC_RELAXED);
+        in_src[k] = src[i];
+    }
+    free(fill);
+#pragma omp parallel for schedule(dynamic, 4096)
+    for (int64_t v = 0; v < n; v++) {
+        int64_t d = in_off[v + 1] - in_off[v];
+        if (d > 1) qsort(in_src + in_off[v], (size_t)d, sizeof(int32_t), or_i32_cmp);
+    }
+    return 0;
+}
+
+/*
+ * Order-independent digests of an edge set, for comparing graphs whose
+ * arrays are too large to compare or sort on the host: with
+ * f(u, v) = mix64(u * 2^32 + v + G) (a bijection of the pair), out[0] = the
+ * number of edges, out[1] = the sum and out[2] = the xor of f over the set.
+ * Equal sets give equal digests; unequal ones collide with probability about
+ * 2^-64.  Over the raw edge list; over a CSR (the edges whose mask bit is set
+ * when mask_words is given); over in-neighbour lists (the entries with
+ * keep_in set when given).
+ */
+static uint64_t or_mix64(uint64_t z);
+static uint64_t or_pair_digest(uint64_t u, uint64_t v) { return or_mix64((u << 32) + v + 0x9e3779b97f4a7c15ULL); }
+
+void or_digest_edges(int64_t e, const int32_t* src, const int32_t* dst, uint64_t* out) {
+    uint64_t sum = 0, x = 0;
+#pragma omp parallel for reduction(+ : sum) reduction(^ : x) schedule(static)
+    for (int64_t i = 0; i < e; i++) {
+        uint64_t h = or_pair_digest((uint64_t)src[i], (uint64_t)dst[i]);
+        sum += h;
+        x ^= h;
+    }
+    out[0] = (uint64_t)e; out[1] = sum; out[2] = x;
+}
+
+void or_digest_csr(int64_t n, const int64_t* row_off, const int32_t* col_dst, const uint64_t* mask_words,
+                   uint64_t* out) {
+    uint64_t sum = 0, x = 0, cnt = 0;
+#pragma omp parallel for reduction(+ : sum, cnt) reduction(^ : x) schedule(dynamic, 4096)
+    for (int64_t u = 0; u < n; u++)
+        for (int64_t i = row_off[u]; i < row_off[u + 1]; i++) {
+            if (mask_words && !((mask_words[i >> 6] >> (i & 63)) & 1ULL)) continue;
+            uint64_t h = or_pair_digest((uint64_t)u, (uint64_t)col_dst[i]);
+            sum += h; x ^= h; cnt++;
+        }
+    out[0] = cnt; out[1] = sum; out[2] = x;
+}
+
+void or_digest_in_lists(int64_t n, const int64_t* in_off, const int32_t* in_src, const uint8_t* keep_in,
+                        uint64_t* out) {
+    uint64_t sum = 0, x = 0, cnt = 0;
+#pragma omp parallel for reduction(+ : sum, cnt) reduction(^ : x) schedule(dynamic, 4096)
+    for (int64_t v = 0; v < n; v++)
+        for (int64_t j = in_off[v]; j < in_off[v + 1]; j++) {
+            if (keep_in && !keep_in[j]) continue;
+            uint64_t h = or_pair_digest((uint64_t)in_src[j], (uint64_t)v);
+            sum += h; x ^= h; cnt++;
+        }
+    out[0] = cnt; out[1] = sum; out[2] = x;
+}
+
+/*
+ * Canonical CSR shape: row_off[0] = 0, non-decreasing, row_off[n] = e;
+ * every row strictly ascending, in [0, n), no self loop.  Returns 0 or the
+ * first violated rule (1 offsets, 2 range, 3 order or repeat, 4 self loop).
+ * With the digest equal to the edge list's, such a CSR is the canonical one.
+ */
+int or_csr_check(int64_t n, int64_t e, const int64_t* row_off, const int32_t* col_dst) {
+    if (row_off[0] != 0 || row_off[n] != e) return 1;
+    int bad = 0;
+#pragma omp parallel for reduction(max : bad) schedule(dynamic, 4096)
+    for (int64_t u = 0; u < n; u++) {
+        if (row_off[u + 1] < row_off[u]) { bad = bad > 1 ? bad : 1; continue; }
+        for (int64_t i = row_off[u]; i < row_off[u + 1]; i++) {
+            int32_t v = col_dst[i];
+            int r = 0;
+            if (v < 0 || v >= n) r = 2;
+            else if (i > row_off[u] && col_dst[i - 1] >= v) r = 3;
+            else if (v == u) r = 4;
+            if (r > bad) bad = r;
+        }
+    }
+    return bad;
+}
+
 /* --------------------------------------------------- counter-based hash -- */
 /*
  * H(s, t, x1..xk): h = s; for x in (t, x1..xk): h = mix64(h + G + x), with
@@ -143,8 +259,8 @@ static int or_cand_cmp(const void* x, const void* y) {
 void or_sample(int64_t n, const int64_t* row_off, const int64_t* in_off, const int32_t* in_src,
                const int64_t* in_pos, uint64_t seed, int64_t layer, int64_t k,
                uint64_t* mask_words, uint8_t* keep_in, int32_t* m_out) {
-    int64_t e = row_off[n];
-    memset(mask_words, 0, (size_t)((e + 63) / 64) * sizeof(uint64_t));
+    /* mask_words NULL: only keep_in and m_out (row_off and in_pos unused) */
+    if (mask_words) memset(mask_words, 0, (size_t)((row_off[n] + 63) / 64) * sizeof(uint64_t));
 #pragma omp parallel
     {
         or_cand* buf = NULL;
@@ -167,7 +283,7 @@ void or_sample(int64_t n, const int64_t* row_off, const int64_t* in_off, const i
                 int kept = j < keep;
                 int64_t idx = buf[j].pos;            /* in-list index */
                 if (keep_in) keep_in[idx] = (uint8_t)kept;
-                if (kept) {
+                if (kept && mask_words) {
                     int64_t p = in_pos[idx];         /* CSR position */
                     __atomic_fetch_or(&mask_words[p >> 6], 1ULL << (p & 63), __ATOMIC_RELAXED);
                 }

@@ -115,3 +115,50 @@ def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, 
 def to_numpy_f64(t, dtype_code: int) -> np.ndarray:
     import torch
     return t.detach().to(torch.float64).cpu().numpy() if dtype_code != F.F32 else t.detach().cpu().numpy().astype(np.float64)
+
+
+def in_neighbours(g, vs: np.ndarray, keep_in: np.ndarray | None = None) -> np.ndarray:
+    """Sources of the in-edges of the vertices vs (kept ones only when a
+    sampled layer's keep_in mask over the in-lists is given), as a sorted
+    unique array."""
+    vs = np.asarray(vs, np.int64)
+    lo, hi = g.in_off[vs], g.in_off[vs + 1]
+    cnt = hi - lo
+    if cnt.sum() == 0:
+        return np.zeros(0, np.int64)
+    pos = np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt) + np.arange(cnt.sum())
+    if keep_in is not None:
+        pos = pos[keep_in[pos] != 0]
+    return np.unique(g.in_src[pos].astype(np.int64))
+
+
+def oracle_sampled_layers(w: WL.Workload, g, X: np.ndarray, ids: list, keeps: list | None = None) -> list:
+    """Oracle outputs (fp64) of every layer of w at the destination sample
+    ids[l - 1], each layer fed the oracle's own previous layer, which is
+    evaluated only on the vertices the later layers read (the samples, the
+    destinations' own rows and their propagated in-neighbours).  X: the
+    layer-1 input in storage dtype; keeps[l - 1]: the oracle sampler's keep_in
+    for sampled layers, else None."""
+    import oracle as O
+    L = w.layers
+    keeps = keeps or [None] * L
+    need = [None] * L
+    need[L - 1] = np.unique(np.asarray(ids[L - 1], np.int64))
+    for li in range(L - 1, 0, -1):          # layer li's outputs read by layer li + 1
+        nxt = need[li]
+        need[li - 1] = np.unique(np.concatenate([np.asarray(ids[li - 1], np.int64), nxt,
+                                                 in_neighbours(g, nxt, keeps[li])]))
+    H, h_dtype = X, w.feat_dtype
+    out = []
+    for li in range(1, L + 1):
+        p = WL.layer_params(w, li)
+        z = O.layer(w.agg, g, H, h_dtype, p.W, p.b, li < L, keep_in=keeps[li - 1], dst_ids=need[li - 1])
+        pos = np.searchsorted(need[li - 1], np.asarray(ids[li - 1], np.int64))
+        out.append(z[pos])
+        if li < L:
+            _, out_dt = w.layer_dtypes(li)
+            rows = O.round_store(z, out_dt)
+            H = np.zeros((w.n, rows.shape[1]), rows.dtype)
+            H[need[li - 1]] = rows
+            h_dtype = out_dt
+    return out

@@ -99,19 +99,16 @@ def test_budget_eviction_matches_incore_c4_shape(torch_cuda):
         assert 0.0 < st["hub_message_share"] < 1.0
         assert st["d2h_bytes"] == st["evictions"] * w.dims[li] * 4
         assert st["device_bytes"] <= budgets[li - 1] + (1 << 20)
-    # sampled destinations against the oracle, each layer fed the GPU's previous output
+    # sampled destinations against the oracle, each layer fed the oracle's own previous layer
     g = O.Graph(w.n, src, dst)
     rng = np.random.default_rng(9)
     d_in = np.diff(g.in_off)
     ids = np.unique(np.concatenate([rng.choice(w.n, 1024, replace=False), np.argsort(-d_in, kind="stable")[:32],
                                     np.flatnonzero(d_in == 0)[:32]]))
-    h = WL.input_features(w)
-    for li in range(1, w.layers + 1):
-        p = WL.layer_params(w, li)
-        z = O.layer(w.agg, g, h, F.F32, p.W, p.b, li < w.layers, dst_ids=ids)
+    zs = H.oracle_sampled_layers(w, g, WL.input_features(w), [ids] * w.layers)
+    for li, z in enumerate(zs, start=1):
         r = H.compare(outs[li - 1].cpu().numpy()[ids], z, H.RTOL[F.F32])
         assert r["n_bad"] == 0, (li, r)
-        h = outs[li - 1].cpu().numpy()
 
 
 def test_host_chunks_and_host_outputs(torch_cuda):

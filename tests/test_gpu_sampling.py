@@ -120,14 +120,6 @@ def test_fanout_above_max_degree_equals_exact(torch_cuda):
     assert np.array_equal(outs[0], outs[1])
 
 
-def _bits(t, dtype):
-    """Device tensor of a 16-bit storage dtype -> uint16 bit patterns (fp32 stays fp32)."""
-    import torch
-    if dtype == F.F32:
-        return t.detach().cpu().numpy()
-    return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
-
-
 def _destination_sample(rng, g, count):
     d_in = np.diff(g.in_off)
     ids = set(rng.choice(g.n, size=min(count, g.n), replace=False).tolist())
@@ -141,8 +133,8 @@ def test_sampled_bf16_model_c3_shape(torch_cuda):
     128 -> 256 -> 256 -> 172 on an RMAT graph of the same recipe at 1/800 of
     the vertices.  Per layer: the mask bit-exact against the oracle's
     sampler, and a seeded destination sample (plus the top in-degrees and
-    zero in-degree vertices) against the oracle layer fed with the GPU's
-    previous output."""
+    zero in-degree vertices) against the oracle, each layer fed the oracle's
+    own previous layer."""
     import oracle as O
     import paper_2607_17374_amd as T
     from paper_2607_17374_amd.api import torch_dtype
@@ -156,7 +148,8 @@ def test_sampled_bf16_model_c3_shape(torch_cuda):
     X = torch.from_numpy(xh.view(np.int16)).cuda().view(torch_dtype(w.feat_dtype))
     plan = T.Plan(w.n, row_off, col_dst, w.chunk)
     rng = np.random.default_rng(31)
-    h, h_bits, h_dtype = X, xh, w.feat_dtype
+    h = X
+    outs, all_ids, keeps = [], [], []
     for li, spec in enumerate(H.layer_specs(w), start=1):
         _note(f"  layer {li} fanout {spec['fanout']}")
         out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device="cuda")
@@ -168,14 +161,16 @@ def test_sampled_bf16_model_c3_shape(torch_cuda):
         st = L.finalize()
         L.destroy()
         assert st["messages"] == kept == int(m.sum())
-        ids = _destination_sample(rng, g, 2048)
-        p = WL.layer_params(w, li)
-        z = O.layer(w.agg, g, h_bits, h_dtype, p.W, p.b, li < w.layers, keep_in=keep_in, dst_ids=ids)
+        all_ids.append(_destination_sample(rng, g, 2048))
+        keeps.append(keep_in)
+        outs.append(out)
+        h = out
+    plan.destroy()
+    zs = H.oracle_sampled_layers(w, g, xh, all_ids, keeps)
+    for li, (out, ids, z, spec) in enumerate(zip(outs, all_ids, zs, H.layer_specs(w)), start=1):
         y = H.to_numpy_f64(out, spec["out_dtype"])[ids]
         r = H.compare(y, z, H.RTOL[w.feat_dtype])
         assert r["n_bad"] == 0, (li, r)
-        h, h_bits, h_dtype = out, _bits(out, spec["out_dtype"]), spec["out_dtype"]
-    plan.destroy()
 
 
 @pytest.mark.parametrize("base,dtype", [(WL.SAGE_RMAT_4K, F.BF16), (WL.SAGE_RMAT_4K, F.F16),

@@ -444,3 +444,81 @@ def test_span_equals_sum_of_active_counts():
             if srcs.size and pi[srcs].min() <= t < pi[srcs].max():
                 total += 1
     assert O.total_span(g, pi) == total
+
+
+# ---- large-graph helpers: in-lists from the edge list, set digests, CSR shape
+
+def _edge_list(rng, n, p):
+    _, u, v = random_digraph(rng, n, p, isolated=3)
+    perm = rng.permutation(u.size)           # any edge order
+    return u[perm].astype(np.int32), v[perm].astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_edge_graph_in_lists_equal_graph(seed):
+    rng = np.random.default_rng(seed + 70)
+    u, v = _edge_list(rng, 60, 0.08)
+    g = O.Graph(60, u, v)
+    eg = O.EdgeGraph(60, u, v)
+    assert np.array_equal(eg.in_off, g.in_off) and np.array_equal(eg.in_src, g.in_src)
+    assert np.array_equal(eg.deg_out, g.deg_out) and np.array_equal(eg.deg_in, g.deg_in)
+    # the fanout sampler sees the same lists: same kept entries and counts
+    for k in (1, 3):
+        _, keep_g, m_g = O.sample(g, 11, 2, k)
+        words, keep_e, m_e = O.sample(eg, 11, 2, k)
+        assert words is None and np.array_equal(keep_g, keep_e) and np.array_equal(m_g, m_e)
+
+
+def test_set_digests_agree_and_separate():
+    rng = np.random.default_rng(80)
+    u, v = _edge_list(rng, 50, 0.1)
+    g = O.Graph(50, u, v)
+    d = O.digest_edges(u, v)
+    assert d[0] == u.size
+    assert O.digest_csr(50, g.row_off, g.col_dst) == d == O.digest_in_lists(g)
+    # one destination moved: a different set, a different digest
+    col = g.col_dst.copy()
+    i = int(np.flatnonzero(np.diff(g.row_off) > 0)[0])
+    col[g.row_off[i]] = (col[g.row_off[i]] + 1) % 50
+    assert O.digest_csr(50, g.row_off, col) != d
+    # the kept edges of a sampled layer: mask over the CSR == keep_in over the in-lists
+    words, keep_in, m = O.sample(g, 5, 1, 2)
+    dm = O.digest_csr(50, g.row_off, g.col_dst, words)
+    assert dm == O.digest_in_lists(g, keep_in) and dm[0] == int(m.sum())
+
+
+def test_csr_check_rules():
+    rng = np.random.default_rng(90)
+    u, v = _edge_list(rng, 40, 0.1)
+    g = O.Graph(40, u, v)
+    assert O.csr_check(40, g.row_off, g.col_dst) == 0
+    row = int(np.flatnonzero(np.diff(g.row_off) >= 2)[0])
+    a = g.row_off[row]
+    col = g.col_dst.copy(); col[a], col[a + 1] = col[a + 1], col[a]
+    assert O.csr_check(40, g.row_off, col) == 3                # out of order
+    col = g.col_dst.copy(); col[a] = row
+    assert O.csr_check(40, g.row_off, col) in (3, 4)           # self loop (may also break the order)
+    col = g.col_dst.copy(); col[a] = 40
+    assert O.csr_check(40, g.row_off, col) in (2, 3)           # out of range
+    ro = g.row_off.copy(); ro[-1] += 1
+    assert O.csr_check(40, ro, g.col_dst) == 1                 # offsets
+
+
+@pytest.mark.parametrize("which", ["sage-sampled", "gcn"])
+def test_oracle_chain_on_samples_equals_full_oracle(which):
+    """The sampled-destination chain (each layer on the vertices the next one
+    reads, fed the oracle's own previous layer) equals the full oracle."""
+    from fixtures import workloads as WL
+    from tests import harness as H
+    if which == "gcn":
+        w = WL.GCN_RMAT_1M.scaled(n=3000, e=40000, chunk=1024)
+    else:
+        w = WL.SAGE_FANOUT_RMAT_100M.scaled(n=3000, e=40000, chunk=1024)
+    src, dst = WL.graph(w)
+    g, zs = H.oracle_model(w, src, dst)
+    rng = np.random.default_rng(3)
+    ids = [np.sort(rng.choice(w.n, 200, replace=False)) for _ in range(w.layers)]
+    keeps = [O.sample(g, w.seed, li, w.fanout(li))[1] if w.fanout(li) else None for li in range(1, w.layers + 1)]
+    out = H.oracle_sampled_layers(w, g, WL.input_features(w), ids, keeps)
+    for li in range(w.layers):
+        assert np.array_equal(out[li], zs[li][ids[li]]), li
