@@ -1539,11 +1539,13 @@ static const void* stage_host_chunk(taurus_layer* L, const void* x, int64_t rows
         }
     }
     const int prev = (int)((L->host_pushes + 1) & 1), cur = (int)(L->host_pushes & 1);
-    if (L->stage_used[prev]) TAURUS_HIP(hipEventSynchronize(L->h2d_done[prev]));
     if (L->stage_used[cur]) TAURUS_HIP(hipStreamWaitEvent(L->copy_stream, L->gemm_done[cur], 0));
     TAURUS_HIP(hipMemcpyAsync(L->stage[cur], x, bytes, hipMemcpyHostToDevice, L->copy_stream));
     TAURUS_HIP(hipEventRecord(L->h2d_done[cur], L->copy_stream));
     TAURUS_HIP(hipStreamWaitEvent(L->s, L->h2d_done[cur], 0));
+    // the previous chunk's x is released to the caller once its copy is done;
+    // waiting after this chunk's copy is queued keeps the copy engine busy
+    if (L->stage_used[prev]) TAURUS_HIP(hipEventSynchronize(L->h2d_done[prev]));
     L->stage_used[cur] = true;
     L->host_pushes++;
     L->h2d_bytes += (int64_t)bytes;

@@ -2,6 +2,7 @@
 
     python tests/fullsize.py gcn2-skew-rmat-50m          # 50M vertices, 1B edges
     python tests/fullsize.py sage3-fanout-rmat-100m      # 100M vertices, 1.6B edges
+    python tests/fullsize.py sage2-ooc-rmat-269m --scale 8   # out of core, at 1/8
     python tests/fullsize.py <workload> --scale 64       # the same recipe at 1/64
 
 Not collected by pytest (a run takes minutes and most of the GPU's memory);
@@ -21,6 +22,12 @@ Checks, all against the oracle (which never reads anything the GPU made):
     oracle's own previous layer), with the tolerance of the test suite;
   - reordered workloads: the reordered run, un-permuted, against the run in
     the original IDs, every element.
+
+The out-of-core workload streams every chunk from pinned host memory
+(generated before the timed layers, so the host link and not the generator
+is measured), writes its outputs to pinned host memory and keeps its
+accumulators under the HBM budget (scaled with the graph) with 1% resident
+hubs; it reports the host-link bytes and rates beside a plain pinned copy.
 """
 from __future__ import annotations
 
@@ -251,21 +258,136 @@ def run_c3(w) -> dict:
     return res
 
 
+def link_peak_gbs(gib: int = 4) -> float:
+    """Host-to-device rate of one large copy from pinned memory (the link as
+    the copy engines see it)."""
+    import torch
+    src = torch.empty(gib << 28, dtype=torch.float32).pin_memory()
+    dst = torch.empty_like(src, device="cuda")
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t = time.time()
+    for _ in range(3):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    gbs = 3 * src.numel() * 4 / (time.time() - t) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
+
+
+def run_c4(w) -> dict:
+    import torch
+    import oracle as O
+    import paper_2607_17374_amd as T
+    import fixtures as F
+    from fixtures import workloads as WL
+    from tests import harness as H
+    res = {"workload": w.name, "n": w.n, "e": w.e, "hbm_budget": w.hbm_budget, "hub_fraction": w.hub_fraction}
+    res["link_peak_h2d_gbs"] = round(link_peak_gbs(), 2)
+    say(f"pinned host-to-device copy: {res['link_peak_h2d_gbs']} GB/s")
+    src, dst = WL.graph(w)
+    say(f"edge list: {src.size} edges")
+    g = O.EdgeGraph(w.n, src, dst)
+    dig = O.digest_edges(src, dst)
+    say("oracle in-lists and edge digest")
+    s = torch.from_numpy(src).cuda()
+    d = torch.from_numpy(dst).cuda()
+    row_off, col_dst = T.build_csr(w.n, s, d)
+    torch.cuda.synchronize()
+    del s, d, src, dst
+    torch.cuda.empty_cache()
+    c = check_csr(w.n, row_off, col_dst, dig)
+    del c["_host"]
+    res["csr"] = c
+    # layer-1 input in pinned host memory, in pieces of whole chunks of at
+    # most 8 GiB each (pinned allocations are capped on this host)
+    row_bytes = w.dims[0] * 4
+    step = max(w.chunk, ((8 << 30) // row_bytes) // w.chunk * w.chunk)
+    pieces = []
+    for v0 in range(0, w.n, step):
+        v1 = min(w.n, v0 + step)
+        piece = torch.from_numpy(F.features(w.seed, w.feat_dist, v0, v1, w.dims[0], F.F32)).pin_memory()
+        pieces.append((v0, v1, piece))
+        say(f"features rows {v1}/{w.n} (pinned)")
+
+    def push_layer1(L):
+        for v0, v1, piece in pieces:
+            for b in range(v0, v1, w.chunk):
+                L.push_chunk(b, min(b + w.chunk, v1), piece[b - v0:min(b + w.chunk, v1) - v0])
+
+
+    ids = [destination_sample(w.seed * 1000 + li, g.deg_in) for li in range(1, w.layers + 1)]
+    h = None
+    host, stats = [], []
+    plan = T.Plan(w.n, row_off, col_dst, w.chunk)
+    for li, spec in enumerate(H.layer_specs(w), start=1):
+        out = torch.empty((w.n, spec["d_out"]), dtype=torch.float32).pin_memory()
+        torch.cuda.synchronize()
+        t0 = time.time()
+        L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, plan=plan, hbm_budget=w.hbm_budget,
+                    hub_fraction=w.hub_fraction, **spec)
+        t_init = time.time() - t0
+        t1 = time.time()
+        if h is None:
+            push_layer1(L)
+        else:
+            L.push_all(h)
+        st = L.finalize()
+        t_run = time.time() - t1
+        L.destroy()
+        link = st["h2d_bytes"] + st["d2h_bytes"]
+        st.update(layer=li, init_s=round(t_init, 3), push_finalize_s=round(t_run, 3),
+                  h2d_gbs=round(st["h2d_bytes"] / t_run / 1e9, 2), link_gbs=round(link / t_run / 1e9, 2),
+                  gteps=round(st["messages"] / (t_init + t_run) / 1e9, 3))
+        say(f"layer {li}: {st['messages']} messages, init {t_init:.2f} s, chunks {t_run:.2f} s; "
+            f"h2d {st['h2d_bytes'] / 1e9:.1f} GB ({st['h2d_gbs']} GB/s), d2h {st['d2h_bytes'] / 1e9:.1f} GB, "
+            f"evictions {st['evictions']}, reloads {st['reloads']}, hub messages {st['hub_message_share']:.3f}, "
+            f"device bytes {st['device_bytes'] / 1e9:.1f} GB, completed {st['completed']}/{w.n}")
+        assert st["pending_left"] == 0
+        stats.append(st)
+        host.append(out.numpy()[ids[li - 1]].astype(np.float64))
+        del h
+        h = out
+        torch.cuda.empty_cache()
+    plan.destroy()
+    del h, out
+    res["stats"] = stats
+    # the oracle gets the layer-1 input as one host array (built from the pieces)
+    X = np.concatenate([piece.numpy() for _, _, piece in pieces])
+    pieces.clear()
+    res["embeddings"] = embeddings(w, g, X, {"GPU": host}, ids, [None] * w.layers)
+    return res
+
+
 def main():
     from fixtures import workloads as WL
     import argparse
     ap = argparse.ArgumentParser()
     ap.add_argument("workload", nargs="?", default="gcn2-skew-rmat-50m")
     ap.add_argument("--scale", type=int, default=1, help="run the recipe at 1/scale of the vertices and edges")
+    ap.add_argument("--chunk", type=int, default=0, help="override the chunk size (out of core: after scaling)")
+    ap.add_argument("--budget-frac", type=float, default=1.0, help="out of core: multiply the HBM budget")
+    ap.add_argument("--tag", default="", help="suffix of the summary file name")
     args = ap.parse_args()
     w = {x.name: x for x in WL.ALL}[args.workload]
     if args.scale > 1:
+        import dataclasses
         w = w.scaled(w.n // args.scale, w.e // args.scale, name=f"{w.name}-div{args.scale}")
+        if w.out_of_core:
+            # budget and chunk scale with the graph: the same number of chunks,
+            # so each chunk holds the full-size share of the edges
+            w = dataclasses.replace(w, hbm_budget=w.hbm_budget // args.scale,
+                                    chunk=max(1024, w.chunk // args.scale))
+    if args.chunk or args.budget_frac != 1.0 or args.tag:
+        import dataclasses
+        w = dataclasses.replace(w, chunk=args.chunk or w.chunk, hbm_budget=int(w.hbm_budget * args.budget_frac),
+                                name=w.name + (f"-{args.tag}" if args.tag else ""))
     import torch
     assert torch.cuda.is_available(), "needs a GPU"
     import oracle as O
     say(f"{w.name}: n={w.n} e={w.e}; oracle threads {O.threads()}")
-    res = run_c5(w) if w.reorder else run_c3(w)
+    res = run_c5(w) if w.reorder else (run_c4(w) if w.out_of_core else run_c3(w))
     res["seconds"] = round(time.time() - T0, 1)
     os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
     path = os.path.join(ROOT, "gpurun_out", f"fullsize_{w.name}.json")
