@@ -80,6 +80,10 @@ def load(path: str):
     L.or_digest_in_lists.argtypes = [i64, vp, vp, vp, vp]
     L.or_csr_check.restype = i32
     L.or_csr_check.argtypes = [i64, i64, vp, vp]
+    L.or_ta_step.restype = None
+    L.or_ta_step.argtypes = [i64, vp, vp, vp, vp, vp, vp, vp]
+    L.or_reorder_ta.restype = i32
+    L.or_reorder_ta.argtypes = [i64, vp, vp, vp, vp, vp, i32, vp, vp, vp]
     return L
 
 
@@ -233,6 +237,29 @@ def reorder_bfs(g: Graph) -> np.ndarray:
     if lib().or_reorder_bfs(g.n, _p(g.in_off), _p(g.in_src), _p(out)):
         raise MemoryError("or_reorder_bfs")
     return out
+
+
+def ta_step(g: Graph, r: np.ndarray):
+    """One update of Alg. 1 (Sec. 3.8): positions r -> (centres mu, new positions r)."""
+    r = np.ascontiguousarray(r, np.float64)
+    mu = np.empty(g.n, np.float64)
+    r2 = np.empty(g.n, np.float64)
+    lib().or_ta_step(g.n, _p(g.row_off), _p(g.col_dst), _p(g.in_off), _p(g.in_src), _p(r), _p(mu), _p(r2))
+    return mu, r2
+
+
+def reorder_ta(g: Graph, pi0: np.ndarray | None = None, iterations: int = 5):
+    """Alg. 1 from bootstrap pi0 (identity if None) -> (new_of_old int32[n],
+    spans int64[iterations + 1] (C(pi0), then after each update; 0 past the
+    last update made), updates made)."""
+    pi = np.empty(g.n, np.int32)
+    spans = np.zeros(iterations + 1, np.int64)
+    done = ctypes.c_int(0)
+    p0 = None if pi0 is None else np.ascontiguousarray(pi0, np.int32)
+    if lib().or_reorder_ta(g.n, _p(g.row_off), _p(g.col_dst), _p(g.in_off), _p(g.in_src), _p(p0), iterations,
+                           _p(pi), _p(spans), ctypes.byref(done)):
+        raise MemoryError("or_reorder_ta")
+    return pi, spans, done.value
 
 
 def total_span(g: Graph, pi: np.ndarray) -> int:

@@ -499,3 +499,88 @@ int64_t or_total_span(int64_t n, const int64_t* in_off, const int32_t* in_src, c
     }
     return total;
 }
+
+/* ------------------------------------- topology-aware reordering (Alg. 1) -- */
+/*
+ * Sec. 3.8 minimises the in-neighbourhood dispersion
+ *     J(r, mu) = sum_v 1/d(v) sum_{u in N(v)} (r(u) - mu(v))^2
+ * over real positions r by alternating its two closed-form minimisers
+ *     mu*(v) = (1/d(v)) sum_{u in N(v)} r(u)                      (Eq. for mu*)
+ *     r*(w)  = sum_{v : w in N(v)} mu(v)/d(v) / sum_{v : w in N(v)} 1/d(v)
+ * and ranks the vertices by r (Alg. 1).  N(v) holds v's propagated
+ * in-neighbours and v itself -- every vertex aggregates a self message, so
+ * d(v) = d_in(v) + 1 >= 1 -- hence {v : w in N(v)} = {w} and w's
+ * out-neighbours.  Reading of this build: every sum is taken in fp64 in a
+ * fixed order, the self term first and then the neighbours in ascending ID,
+ * and ArgSort breaks ties by the lower vertex ID.
+ *
+ * One update: r_in -> mu -> r_out (CSR for the out-neighbours, in-lists for
+ * the in-neighbours).
+ */
+void or_ta_step(int64_t n, const int64_t* row_off, const int32_t* col_dst, const int64_t* in_off,
+                const int32_t* in_src, const double* r_in, double* mu, double* r_out) {
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int64_t v = 0; v < n; v++) {
+        double s = r_in[v];
+        for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) s += r_in[in_src[k]];
+        mu[v] = s / (double)(in_off[v + 1] - in_off[v] + 1);
+    }
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int64_t w = 0; w < n; w++) {
+        double d = (double)(in_off[w + 1] - in_off[w] + 1);
+        double num = mu[w] / d, den = 1.0 / d;
+        for (int64_t i = row_off[w]; i < row_off[w + 1]; i++) {
+            int32_t v = col_dst[i];
+            double dv = (double)(in_off[v + 1] - in_off[v] + 1);
+            num += mu[v] / dv;
+            den += 1.0 / dv;
+        }
+        r_out[w] = num / den;
+    }
+}
+
+typedef struct { double r; int32_t v; } or_pos;
+static int or_pos_cmp(const void* x, const void* y) {
+    const or_pos* a = (const or_pos*)x; const or_pos* b = (const or_pos*)y;
+    if (a->r != b->r) return a->r < b->r ? -1 : 1;
+    return (a->v > b->v) - (a->v < b->v);
+}
+
+/*
+ * Alg. 1 from the bootstrap pi0 (new ID of each vertex; NULL = identity):
+ * r = pi0, then up to `iters` updates, each followed by pi = ArgSort(r);
+ * stops after an update that leaves pi unchanged.  spans[0] = C(pi0) and
+ * spans[t] = C(pi) after update t (or_total_span); *done = updates made.
+ * Returns 0, or -3 when out of memory.
+ */
+int or_reorder_ta(int64_t n, const int64_t* row_off, const int32_t* col_dst, const int64_t* in_off,
+                  const int32_t* in_src, const int32_t* pi0, int iters, int32_t* pi_out, int64_t* spans,
+                  int* done) {
+    double* r = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    double* r2 = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    double* mu = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    or_pos* pos = (or_pos*)malloc((size_t)(n > 0 ? n : 1) * sizeof(or_pos));
+    if (!r || !r2 || !mu || !pos) return -3;
+    for (int64_t v = 0; v < n; v++) {
+        pi_out[v] = pi0 ? pi0[v] : (int32_t)v;
+        r[v] = (double)pi_out[v];
+    }
+    if (spans) spans[0] = or_total_span(n, in_off, in_src, pi_out);
+    *done = 0;
+    for (int t = 1; t <= iters; t++) {
+        or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);
+        double* tmp = r; r = r2; r2 = tmp;
+        for (int64_t v = 0; v < n; v++) { pos[v].r = r[v]; pos[v].v = (int32_t)v; }
+        qsort(pos, (size_t)n, sizeof(or_pos), or_pos_cmp);
+        int changed = 0;
+        for (int64_t k = 0; k < n; k++) {
+            if (pi_out[pos[k].v] != (int32_t)k) changed = 1;
+            pi_out[pos[k].v] = (int32_t)k;
+        }
+        *done = t;
+        if (spans) spans[t] = or_total_span(n, in_off, in_src, pi_out);
+        if (!changed) break;
+    }
+    free(r); free(r2); free(mu); free(pos);
+    return 0;
+}

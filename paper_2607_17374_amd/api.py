@@ -79,6 +79,21 @@ def reorder(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, stream=None) -
     return out
 
 
+def reorder_ta(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, pi0: Optional[torch.Tensor] = None,
+               iterations: int = 5, stream=None):
+    """taurus_reorder_ta: topology-aware order (Alg. 1) from bootstrap pi0
+    (identity if None) -> (new_of_old int32[n] on the device, spans
+    int64[iterations + 1] (C(pi0), then after each update), updates made)."""
+    g = _graph(n, row_off, col_dst)
+    out = torch.empty(n, dtype=torch.int32, device=row_off.device)
+    spans = np.zeros(iterations + 1, dtype=np.int64)
+    done = ctypes.c_int32(0)
+    p0 = None if pi0 is None else _dev_ptr(pi0, torch.int32, "pi0")
+    N.check(N.lib().taurus_reorder_ta(ctypes.byref(g), p0, iterations, out.data_ptr(), spans.ctypes.data,
+                                      ctypes.byref(done), _stream_ptr(stream)), "taurus_reorder_ta")
+    return out, spans, done.value
+
+
 def relabel_graph(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, new_of_old: torch.Tensor, stream=None):
     """taurus_relabel_graph: CSR of the graph with vertex v renamed new_of_old[v]."""
     g = _graph(n, row_off, col_dst)

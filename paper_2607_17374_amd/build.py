@@ -10,7 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 SO = os.path.join(HERE, "libtaurus.so")
-SOURCES = ["prims.hip", "csr.hip", "gemm.hip", "sample.hip", "reorder.hip", "resident.hip", "layer.hip"]
+SOURCES = ["prims.hip", "csr.hip", "gemm.hip", "sample.hip", "reorder.hip", "reorder_ta.hip", "resident.hip",
+           "layer.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -152,3 +152,70 @@ def test_reorder_error_paths(torch_cuda):
     with pytest.raises(T.TaurusError) as ex:
         T.reorder(n, row_off, broken)
     assert ex.value.status == -1
+
+
+@pytest.mark.parametrize("case", range(5))
+@pytest.mark.parametrize("boot", ["identity", "bfs"])
+def test_reorder_ta_bit_exact(torch_cuda, case, boot):
+    """Alg. 1 (topology-aware order) against the oracle: the order, the total
+    span after each update and the number of updates are equal."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    name, n, src, dst = _cases()[case]
+    _note(f"reorder_ta {name} from {boot}: n={n} e={src.size}")
+    g = O.Graph(n, src, dst)
+    row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(src).cuda(), torch_cuda.from_numpy(dst).cuda())
+    p0 = None if boot == "identity" else O.reorder_bfs(g)
+    pi, spans, done = T.reorder_ta(n, row_off, col_dst, None if p0 is None else torch_cuda.from_numpy(p0).cuda(), 6)
+    want, wspans, wdone = O.reorder_ta(g, p0, 6)
+    assert done == wdone
+    assert np.array_equal(pi.cpu().numpy(), want)
+    assert np.array_equal(spans, wspans)
+
+
+def test_reorder_ta_skewed_rmat_model(torch_cuda):
+    """C5's recipe (skewed RMAT, random IDs, fp16 GCN) at 1/400 of the
+    vertices: Alg. 1 from the degree/BFS order, bit-exact with the oracle; the
+    model on the relabelled graph, un-permuted, matches the oracle in the
+    original IDs."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    torch = torch_cuda
+    w = WL.GCN_SKEW_RMAT_50M.scaled(n=1 << 17, e=1 << 21, chunk=8192)
+    src, dst = WL.graph(w)
+    _note(f"reorder_ta {w.name}")
+    g, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    boot = T.reorder(w.n, row_off, col_dst)
+    pi, spans, done = T.reorder_ta(w.n, row_off, col_dst, boot, 5)
+    want, wspans, wdone = O.reorder_ta(g, boot.cpu().numpy(), 5)
+    assert done == wdone and np.array_equal(pi.cpu().numpy(), want) and np.array_equal(spans, wspans)
+    _note(f"  spans {spans[:done + 1].tolist()}")
+    r2, c2 = T.relabel_graph(w.n, row_off, col_dst, pi)
+    xh = WL.input_features(w)
+    X2 = T.permute_rows(torch.from_numpy(xh.view(np.int16)).cuda().view(torch_dtype(w.feat_dtype)), pi)
+    outs, _ = H.gpu_model(w, r2, c2, X=X2)
+    for li, (o, z) in enumerate(zip(outs, zs), start=1):
+        back = T.permute_rows(o, pi, inverse=True)
+        _, out_dt = w.layer_dtypes(li)
+        r = H.compare(H.to_numpy_f64(back, out_dt), z, H.RTOL[w.feat_dtype])
+        assert r["n_bad"] == 0, (li, r)
+
+
+def test_reorder_ta_error_paths(torch_cuda):
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    _note("reorder_ta errors")
+    n = 100
+    src = np.arange(1, n, dtype=np.int32)
+    dst = np.zeros(n - 1, dtype=np.int32)
+    row_off, col_dst = T.build_csr(n, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+    for bad in (torch.zeros(n, dtype=torch.int32, device="cuda"),            # repeated ranks
+                torch.arange(1, n + 1, dtype=torch.int32, device="cuda")):   # a rank out of range
+        with pytest.raises(T.TaurusError) as ex:
+            T.reorder_ta(n, row_off, col_dst, bad, 3)
+        assert ex.value.status == -1
+    with pytest.raises(T.TaurusError) as ex:
+        T.reorder_ta(n, row_off, col_dst, None, 0)
+    assert ex.value.status == -1

@@ -522,3 +522,83 @@ def test_oracle_chain_on_samples_equals_full_oracle(which):
     out = H.oracle_sampled_layers(w, g, WL.input_features(w), ids, keeps)
     for li in range(w.layers):
         assert np.array_equal(out[li], zs[li][ids[li]]), li
+
+
+# ---- topology-aware reordering (Sec. 3.8, Alg. 1)
+
+def _dispersion(g, r, mu):
+    """The objective of Sec. 3.8: J = sum_v 1/d(v) sum_{u in N(v)} (r(u) - mu(v))^2,
+    N(v) = v's in-neighbours and v itself (the self message), d(v) = |N(v)|."""
+    J = 0.0
+    for v in range(g.n):
+        nb = np.concatenate([[v], g.in_src[g.in_off[v]:g.in_off[v + 1]]])
+        J += np.sum((r[nb] - mu[v]) ** 2) / nb.size
+    return J
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_ta_updates_are_the_minimisers(seed):
+    """mu* minimises J for fixed r, and r* minimises J for fixed mu: no
+    perturbation of either lowers J (J is convex in each block)."""
+    rng = np.random.default_rng(seed + 100)
+    _, u, v = random_digraph(rng, 30, 0.12, isolated=2)
+    g = O.Graph(30, u, v)
+    r = rng.permutation(30).astype(np.float64) + rng.random(30)
+    mu, r2 = O.ta_step(g, r)
+    j_mu = _dispersion(g, r, mu)
+    j_r = _dispersion(g, r2, mu)
+    for _ in range(20):
+        d = rng.normal(scale=0.3, size=30)
+        assert _dispersion(g, r, mu + d) >= j_mu - 1e-9
+        assert _dispersion(g, r2 + d, mu) >= j_r - 1e-9
+    # one coordinate at a time (the minimiser is unique per coordinate)
+    for k in range(30):
+        e = np.zeros(30); e[k] = 1e-3
+        assert _dispersion(g, r, mu + e) > j_mu and _dispersion(g, r, mu - e) > j_mu
+        assert _dispersion(g, r2 + e, mu) > j_r and _dispersion(g, r2 - e, mu) > j_r
+
+
+def test_ta_dispersion_never_increases():
+    rng = np.random.default_rng(110)
+    _, u, v = random_digraph(rng, 40, 0.08)
+    g = O.Graph(40, u, v)
+    r = rng.permutation(40).astype(np.float64)
+    mu, _ = O.ta_step(g, r)
+    prev = _dispersion(g, r, mu)
+    for _ in range(6):
+        _, r = O.ta_step(g, r)
+        j_after_r = _dispersion(g, r, mu)
+        mu, _ = O.ta_step(g, r)
+        j_after_mu = _dispersion(g, r, mu)
+        assert j_after_r <= prev + 1e-9 and j_after_mu <= j_after_r + 1e-9
+        prev = j_after_mu
+
+
+def test_ta_special_cases():
+    # a directed path keeps its order: r = (1/6, 1, 2, 5/2) after one update
+    g = _g(4, [(0, 1), (1, 2), (2, 3)])
+    mu, r = O.ta_step(g, np.arange(4, dtype=np.float64))
+    assert np.allclose(mu, [0, 0.5, 1.5, 2.5]) and np.allclose(r, [1 / 6, 1, 2, 2.5])
+    pi, spans, done = O.reorder_ta(g, None, 5)
+    assert np.array_equal(pi, np.arange(4)) and done == 1 and spans[0] == spans[1] == 0
+    # no edges: every vertex is its own neighbourhood, so nothing moves
+    g = _g(5, [])
+    boot = np.array([3, 0, 4, 1, 2], np.int32)
+    pi, spans, done = O.reorder_ta(g, boot, 5)
+    assert np.array_equal(pi, boot) and done == 1 and spans[0] == 0
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_ta_order_is_a_permutation_with_consistent_spans(seed):
+    rng = np.random.default_rng(seed + 120)
+    _, u, v = random_digraph(rng, 60, 0.05, isolated=4)
+    g = O.Graph(60, u, v)
+    boot = rng.permutation(60).astype(np.int32)
+    pi, spans, done = O.reorder_ta(g, boot, 4)
+    assert np.array_equal(np.sort(pi), np.arange(60))
+    assert spans[0] == O.total_span(g, boot) and spans[done] == O.total_span(g, pi)
+    # the order is ArgSort(r) with ties by ID: recompute r by repeated steps
+    r = boot.astype(np.float64)
+    for _ in range(done):
+        _, r = O.ta_step(g, r)
+    assert np.array_equal(np.argsort(pi, kind="stable"), np.lexsort((np.arange(60), r)))
