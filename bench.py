@@ -236,7 +236,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the path has no multi-GPU mode; see DESIGN.md for how it would shard)", file=sys.stderr)
+              "(the path has no multi-GPU mode)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -217,18 +217,20 @@ int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream);
 /*
  * Topology-aware reordering (Sec. 3.8, Alg. 1): starting from the bootstrap
  * order pi0 (device int32[n], the new ID of each vertex, a permutation of
- * [0, n); NULL = the identity), positions r = pi0 are refined by up to
- * `iterations` (>= 1) updates of the dispersion minimisers
+ * [0, n); NULL = the identity), up to `iterations` (>= 1) updates each take
+ * the current order as positions r = pi and apply the dispersion minimisers
  *     mu(v) = (1/d(v)) sum_{u in N(v)} r(u)
  *     r(w)  = sum_{v : w in N(v)} mu(v)/d(v) / sum_{v : w in N(v)} 1/d(v)
  * with N(v) = v's in-neighbours plus v itself (the self message) and
- * d(v) = |N(v)|; after each update new_of_old = the ranks of r, ties by the
- * lower ID.  Stops early after an update that leaves the order unchanged.
+ * d(v) = |N(v)|; then new_of_old = the ranks of r, ties by the lower ID.
+ * An update that leaves the order unchanged is a fixed point: the loop stops
+ * there, with the result of running every update.
  * Sums are fp64 in a fixed order (own term, then neighbours by ascending ID),
  * so the order is the same on every run.  Outputs: new_of_old (device
  * int32[n], written); spans (host int64[iterations + 1] or NULL): the total
- * span C(pi) = sum_v (max - min rank of v's in-neighbours) of the bootstrap,
- * then after each update made; *updates (host, may be NULL): updates made.
+ * span C(pi) = sum_v (max - min rank over v and its in-neighbours) of the
+ * bootstrap, then after each update made; *updates (host, may be NULL):
+ * updates made.
  * Errors: TAURUS_E_INVALID for a graph that is not a valid CSR, a pi0 that is
  * not a permutation, or iterations < 1.  Returns after the work completed.
  */

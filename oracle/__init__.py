@@ -124,9 +124,10 @@ class EdgeGraph:
     """In-neighbour lists and out-degrees built straight from the edge list
     (no CSR and no sort of the pairs), for graphs too large for ``Graph``.
     Usable by ``layer``, ``sample`` (keep_in and m only) and
-    ``reorder_bfs``."""
+    ``reorder_bfs``; with out_lists also the CSR (the out-lists, built the
+    same way from the reversed pairs), which ``reorder_ta`` needs."""
 
-    def __init__(self, n: int, src: np.ndarray, dst: np.ndarray):
+    def __init__(self, n: int, src: np.ndarray, dst: np.ndarray, out_lists: bool = False):
         src = np.ascontiguousarray(src, np.int32)
         dst = np.ascontiguousarray(dst, np.int32)
         self.n, self.e = n, src.size
@@ -138,7 +139,15 @@ class EdgeGraph:
             raise MemoryError("or_in_lists_from_edges")
         self.deg_in = np.diff(self.in_off).astype(np.int32)
         self.row_off = None
+        self.col_dst = None
         self.in_pos = None
+        if out_lists:
+            self.row_off = np.empty(n + 1, np.int64)
+            self.col_dst = np.empty(self.e, np.int32)
+            scratch = np.empty(n, np.int32)
+            if lib().or_in_lists_from_edges(n, self.e, _p(dst), _p(src), _p(self.row_off), _p(self.col_dst),
+                                            _p(scratch)):
+                raise MemoryError("or_in_lists_from_edges")
 
 
 def digest_edges(src: np.ndarray, dst: np.ndarray) -> tuple:
@@ -251,7 +260,8 @@ def ta_step(g: Graph, r: np.ndarray):
 def reorder_ta(g: Graph, pi0: np.ndarray | None = None, iterations: int = 5):
     """Alg. 1 from bootstrap pi0 (identity if None) -> (new_of_old int32[n],
     spans int64[iterations + 1] (C(pi0), then after each update; 0 past the
-    last update made), updates made)."""
+    last update made), updates made).  Each update starts from the current
+    order as positions (r = pi) and ranks the new positions."""
     pi = np.empty(g.n, np.int32)
     spans = np.zeros(iterations + 1, np.int64)
     done = ctypes.c_int(0)
@@ -263,6 +273,7 @@ def reorder_ta(g: Graph, pi0: np.ndarray | None = None, iterations: int = 5):
 
 
 def total_span(g: Graph, pi: np.ndarray) -> int:
+    """C(pi) of Sec. 3.8 with the self message in every neighbourhood."""
     pi = np.ascontiguousarray(pi, np.int32)
     return int(lib().or_total_span(g.n, _p(g.in_off), _p(g.in_src), _p(pi)))
 

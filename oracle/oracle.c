@@ -25,7 +25,7 @@
  *     hash;
  *   - the degree/BFS vertex ordering used as a topology-aware bootstrap
  *     (Sec. 3.8 discusses bandwidth-style bootstraps; the exact ordering
- *     rule is this build's reading and is stated at or_reorder_bfs).
+ *     rule is a reading of the text and is stated at or_reorder_bfs).
  *
  * Parity status: every function here is pinned by CPU tests (dense
  * adjacency-matrix products, closed forms, hand-worked small graphs,
@@ -34,6 +34,7 @@
 #include <math.h>
 #include <omp.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -425,9 +426,9 @@ int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
 
 /* ------------------------------------------------------------ reorder ---- */
 /*
- * Degree/BFS vertex ordering (this build's reading of an "in-degree-sorted +
- * BFS" topology-aware ordering; the paper's own ordering is an RCMK
- * bootstrap refined by its Algorithm 1, Sec. 3.8).
+ * Degree/BFS vertex ordering: a reading of a degree-sorted breadth-first
+ * ordering as the cheap topology-aware bootstrap (the paper bootstraps with
+ * RCMK and refines with its Algorithm 1, Sec. 3.8; see or_reorder_ta).
  *
  *   - root order: all vertices by (in-degree descending, ID ascending);
  *   - each root not yet visited starts a breadth-first search over IN-edges
@@ -483,13 +484,16 @@ int or_reorder_bfs(int64_t n, const int64_t* in_off, const int32_t* in_src, int3
 
 /*
  * Total span C(pi) = sum_v (max_{u in N-(v)} pi(u) - min_{u in N-(v)} pi(u))
- * (Sec. 3.8), over vertices with at least one in-neighbour.
+ * (Sec. 3.8).  N-(v) holds v's in-neighbours and v itself: every vertex
+ * aggregates a self message, and a vertex with only that message has span 0,
+ * so a vertex's residency runs from its first to its last message, the self
+ * message included.
  */
 int64_t or_total_span(int64_t n, const int64_t* in_off, const int32_t* in_src, const int32_t* pi) {
     int64_t total = 0;
+#pragma omp parallel for reduction(+ : total) schedule(dynamic, 4096)
     for (int64_t v = 0; v < n; v++) {
-        if (in_off[v + 1] == in_off[v]) continue;
-        int64_t lo = INT64_MAX, hi = INT64_MIN;
+        int64_t lo = pi[v], hi = pi[v];
         for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
             int64_t p = pi[in_src[k]];
             if (p < lo) lo = p;
@@ -510,7 +514,7 @@ int64_t or_total_span(int64_t n, const int64_t* in_off, const int32_t* in_src, c
  * and ranks the vertices by r (Alg. 1).  N(v) holds v's propagated
  * in-neighbours and v itself -- every vertex aggregates a self message, so
  * d(v) = d_in(v) + 1 >= 1 -- hence {v : w in N(v)} = {w} and w's
- * out-neighbours.  Reading of this build: every sum is taken in fp64 in a
+ * out-neighbours.  Reading taken here: every sum is taken in fp64 in a
  * fixed order, the self term first and then the neighbours in ascending ID,
  * and ArgSort breaks ties by the lower vertex ID.
  *
@@ -547,9 +551,12 @@ static int or_pos_cmp(const void* x, const void* y) {
 }
 
 /*
- * Alg. 1 from the bootstrap pi0 (new ID of each vertex; NULL = identity):
- * r = pi0, then up to `iters` updates, each followed by pi = ArgSort(r);
- * stops after an update that leaves pi unchanged.  spans[0] = C(pi0) and
+ * Alg. 1 from the bootstrap pi0 (new ID of each vertex; NULL = identity).
+ * Each update takes the current order as the positions, r = pi, computes mu*
+ * and then r*, and ranks r*: pi = ArgSort(r*).  (Reading taken here: the
+ * ordering the sort yields is the position vector of the next update.)  An
+ * update that leaves pi unchanged is a fixed point, so the loop stops there
+ * and the result equals running every update.  spans[0] = C(pi0) and
  * spans[t] = C(pi) after update t (or_total_span); *done = updates made.
  * Returns 0, or -3 when out of memory.
  */
@@ -561,16 +568,13 @@ int or_reorder_ta(int64_t n, const int64_t* row_off, const int32_t* col_dst, con
     double* mu = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
     or_pos* pos = (or_pos*)malloc((size_t)(n > 0 ? n : 1) * sizeof(or_pos));
     if (!r || !r2 || !mu || !pos) return -3;
-    for (int64_t v = 0; v < n; v++) {
-        pi_out[v] = pi0 ? pi0[v] : (int32_t)v;
-        r[v] = (double)pi_out[v];
-    }
+    for (int64_t v = 0; v < n; v++) pi_out[v] = pi0 ? pi0[v] : (int32_t)v;
     if (spans) spans[0] = or_total_span(n, in_off, in_src, pi_out);
     *done = 0;
     for (int t = 1; t <= iters; t++) {
+        for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];
         or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);
-        double* tmp = r; r = r2; r2 = tmp;
-        for (int64_t v = 0; v < n; v++) { pos[v].r = r[v]; pos[v].v = (int32_t)v; }
+        for (int64_t v = 0; v < n; v++) { pos[v].r = r2[v]; pos[v].v = (int32_t)v; }
         qsort(pos, (size_t)n, sizeof(or_pos), or_pos_cmp);
         int changed = 0;
         for (int64_t k = 0; k < n; k++) {
@@ -579,6 +583,7 @@ int or_reorder_ta(int64_t n, const int64_t* row_off, const int32_t* col_dst, con
         }
         *done = t;
         if (spans) spans[t] = or_total_span(n, in_off, in_src, pi_out);
+        if (n >= (1 << 24)) fprintf(stderr, "reorder_ta: update %d of %d done\n", t, iters);
         if (!changed) break;
     }
     free(r); free(r2); free(mu); free(pos);

@@ -15,7 +15,8 @@ SOURCES = ["prims.hip", "csr.hip", "gemm.hip", "sample.hip", "reorder.hip", "reo
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
-    # packed fp32 ops are disabled for all device code
+    # packed fp32 ops are disabled for all device code: some of their forms
+    # have given silently wrong results on this architecture
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 

@@ -2,12 +2,14 @@
 //
 // Positions r minimise the in-neighbourhood dispersion
 //     J(r, mu) = sum_v 1/d(v) sum_{u in N(v)} (r(u) - mu(v))^2
-// by alternating its closed-form minimisers
+// with its closed-form minimisers
 //     mu(v) = (1/d(v)) sum_{u in N(v)} r(u),
 //     r(w)  = sum_{v : w in N(v)} mu(v)/d(v) / sum_{v : w in N(v)} 1/d(v),
-// and ranking the vertices by r.  N(v) is v's propagated in-neighbours plus v
+// and ranks the vertices by r.  N(v) is v's propagated in-neighbours plus v
 // itself (every vertex aggregates a self message), d(v) = d_in(v) + 1, so the
-// sources of r(w) are w and its out-neighbours.
+// sources of r(w) are w and its out-neighbours.  Each update starts from the
+// current order as the positions (r = pi), so an order that an update leaves
+// unchanged is a fixed point and stopping there is exact.
 //
 // Every sum runs in fp64 in one fixed order, the vertex's own term first and
 // then its neighbours in ascending ID (a thread per vertex walking its
@@ -67,20 +69,22 @@ __global__ void k_ta_positions(const int64_t* __restrict__ row_off, const int32_
     ids[w] = (uint32_t)w;
 }
 
-// new_of_old from the sorted order; flags a vertex whose rank changed
+// new_of_old from the sorted order, and the next update's positions r = pi;
+// flags a vertex whose rank changed
 __global__ void k_ta_ranks(const uint32_t* __restrict__ order, int64_t n, int32_t* __restrict__ pi,
-                           int* __restrict__ changed) {
+                           double* __restrict__ r, int* __restrict__ changed) {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= n) return;
     const uint32_t v = order[k];
+    r[v] = (double)k;
     if (pi[v] != (int32_t)k) {
         pi[v] = (int32_t)k;
         atomicOr(changed, 1);
     }
 }
 
-// C(pi) = sum over vertices with in-edges of (max - min) rank of their
-// propagated in-neighbours (the total span of Sec. 3.8)
+// C(pi) = sum over vertices of (max - min) rank over the vertex and its
+// propagated in-neighbours (the total span of Sec. 3.8, self message included)
 __global__ __launch_bounds__(256) void k_total_span(const int64_t* __restrict__ in_off,
                                                     const int32_t* __restrict__ in_src, int64_t n,
                                                     const int32_t* __restrict__ pi,
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(256) void k_total_span(const int64_t* __restrict__ 
     __syncthreads();
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v < n && in_off[v + 1] > in_off[v]) {
-        int32_t lo = INT32_MAX, hi = INT32_MIN;
+        int32_t lo = pi[v], hi = pi[v];
         for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
             const int32_t p = pi[in_src[k]];
             lo = min(lo, p);
@@ -149,7 +153,7 @@ int reorder_ta_impl(const taurus_graph& g, const int32_t* pi0, int iters, int32_
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, n, 64, tmp, s, flags + 1, 1);
         fill_i32(flags, 1, 0, s);
-        k_ta_ranks<<<gn, T, 0, s>>>(sb.vals[sb.cur], n, pi, flags);
+        k_ta_ranks<<<gn, T, 0, s>>>(sb.vals[sb.cur], n, pi, r, flags);
         TAURUS_CHECK_LAUNCH();
         int changed = 0;
         const int64_t c = read_span(&changed);

@@ -149,7 +149,7 @@ def run_c5(w) -> dict:
     res = {"workload": w.name, "n": w.n, "e": w.e}
     src, dst = WL.graph(w)
     say(f"edge list: {src.size} edges (random IDs)")
-    g = O.EdgeGraph(w.n, src, dst)
+    g = O.EdgeGraph(w.n, src, dst, out_lists=True)
     dig = O.digest_edges(src, dst)
     say("oracle in-lists and edge digest")
     s = torch.from_numpy(src).cuda()
@@ -174,7 +174,16 @@ def run_c5(w) -> dict:
     res["span_reordered"] = O.total_span(g, want)
     say(f"order bit-exact vs oracle: {res['reorder_bit_exact']}; total span {res['span_random_ids']} -> "
         f"{res['span_reordered']}")
-    del want
+    # topology-aware order (Alg. 1) from the degree/BFS order
+    pi_ta, spans, done = T.reorder_ta(w.n, row_off, col_dst, pi, 5)
+    torch.cuda.synchronize()
+    say(f"GPU topology-aware order: spans {spans[:done + 1].tolist()}")
+    want_ta, wspans, wdone = O.reorder_ta(g, want, 5)
+    res["reorder_ta_bit_exact"] = bool(np.array_equal(pi_ta.cpu().numpy(), want_ta) and done == wdone
+                                       and np.array_equal(spans, wspans))
+    res["span_ta"] = spans[:done + 1].tolist()
+    say(f"topology-aware order bit-exact vs oracle: {res['reorder_ta_bit_exact']}")
+    del want, want_ta
     ids = [destination_sample(w.seed * 1000 + li, g.deg_in) for li in range(1, w.layers + 1)]
     xh = WL.input_features(w)
     say("features")
@@ -184,27 +193,31 @@ def run_c5(w) -> dict:
     last_a_host = last_a.cpu()
     del last_a
     torch.cuda.empty_cache()
-    # reordered run: relabel the graph, permute the features, run, un-permute
-    r2, c2 = T.relabel_graph(w.n, row_off, col_dst, pi)
-    del row_off, col_dst
-    X2 = T.permute_rows(X, pi)
-    del X
-    torch.cuda.empty_cache()
-    say("relabelled graph and features")
-    ids_new = [pi_h[i].astype(np.int64) for i in ids]   # the same vertices under their new IDs
-    host_b, stats_b, last_b = run_model(w, r2, c2, X2, w.chunk, ids_new)
-    res["reordered"] = {"stats": stats_b}
-    del r2, c2, X2
-    back = T.permute_rows(last_b, pi, inverse=True).cpu()
-    del last_b
-    a64, b64 = last_a_host.double(), back.double()
-    rms = float(a64.pow(2).mean().sqrt())
-    bound = 1e-2 * (a64.abs() + rms)
-    res["orderings_last_layer"] = {"max_abs": float((a64 - b64).abs().max()),
-                                   "n_bad": int(((a64 - b64).abs() > bound).sum())}
-    say(f"reordered vs random IDs, last layer, every element: {res['orderings_last_layer']}")
-    del a64, b64, back, last_a_host
-    res["embeddings"] = embeddings(w, g, xh, {"random IDs": host_a, "reordered": host_b}, ids, [None] * w.layers)
+    # reordered runs: relabel the graph, permute the features, run, un-permute
+    runs = {"random IDs": host_a}
+    for label, perm in (("degree/BFS order", pi), ("topology-aware order", pi_ta)):
+        r2, c2 = T.relabel_graph(w.n, row_off, col_dst, perm)
+        X2 = T.permute_rows(X, perm)
+        torch.cuda.empty_cache()
+        say(f"{label}: relabelled graph and features")
+        ph = perm.cpu().numpy()
+        ids_new = [ph[i].astype(np.int64) for i in ids]   # the same vertices under their new IDs
+        host_b, stats_b, last_b = run_model(w, r2, c2, X2, w.chunk, ids_new)
+        res[label] = {"stats": stats_b}
+        del r2, c2, X2
+        back = T.permute_rows(last_b, perm, inverse=True).cpu()
+        del last_b
+        a64, b64 = last_a_host.double(), back.double()
+        rms = float(a64.pow(2).mean().sqrt())
+        bound = 1e-2 * (a64.abs() + rms)
+        res[label]["vs_random_ids_last_layer"] = {"max_abs": float((a64 - b64).abs().max()),
+                                                  "n_bad": int(((a64 - b64).abs() > bound).sum())}
+        say(f"{label} vs random IDs, last layer, every element: {res[label]['vs_random_ids_last_layer']}")
+        del a64, b64, back
+        runs[label] = host_b
+        torch.cuda.empty_cache()
+    del row_off, col_dst, X, last_a_host
+    res["embeddings"] = embeddings(w, g, xh, runs, ids, [None] * w.layers)
     return res
 
 

@@ -425,10 +425,16 @@ def test_reorder_random_graphs_are_valid_bfs_orders(seed):
 
 
 def test_total_span_hand_example():
-    # v=3 has in-nbrs 0,1,2 at ranks 0,1,2 -> span 2; v=0 has in-nbr 2 -> span 0
+    # every neighbourhood holds the self message: N(3) = {0,1,2,3} at ranks
+    # 0..3 -> span 3; N(0) = {0,2} -> 2; N(1) = {1}, N(2) = {2} -> 0
     g = _g(4, [(0, 3), (1, 3), (2, 3), (2, 0)])
-    assert O.total_span(g, np.arange(4, dtype=np.int32)) == 2
-    assert O.total_span(g, np.array([3, 0, 1, 2], np.int32)) == 3 - 0
+    assert O.total_span(g, np.arange(4, dtype=np.int32)) == 3 + 2
+    # ranks 3,0,1,2: N(3) spans 0..3 -> 3; N(0) at ranks {3, 1} -> 2
+    assert O.total_span(g, np.array([3, 0, 1, 2], np.int32)) == 3 + 2
+    # ranks 1,2,0,3 put vertex 2 next to vertex 0: N(3) -> 3; N(0) at ranks {1, 0} -> 1
+    assert O.total_span(g, np.array([1, 2, 0, 3], np.int32)) == 3 + 1
+    # no edges: every span is 0
+    assert O.total_span(_g(3, []), np.array([2, 0, 1], np.int32)) == 0
 
 
 def test_span_equals_sum_of_active_counts():
@@ -440,10 +446,13 @@ def test_span_equals_sum_of_active_counts():
     total = 0
     for t in range(40):
         for x in range(40):
-            srcs = g.in_src[g.in_off[x]:g.in_off[x + 1]]
-            if srcs.size and pi[srcs].min() <= t < pi[srcs].max():
+            nb = np.concatenate([[x], g.in_src[g.in_off[x]:g.in_off[x + 1]]])
+            if pi[nb].min() <= t < pi[nb].max():
                 total += 1
     assert O.total_span(g, pi) == total
+    # and the bandwidth bound C(pi) <= 2 |V| B, B = max edge length under pi
+    B = int(np.abs(pi[u].astype(np.int64) - pi[v]).max())
+    assert total <= 2 * 40 * B
 
 
 # ---- large-graph helpers: in-lists from the edge list, set digests, CSR shape
@@ -462,6 +471,9 @@ def test_edge_graph_in_lists_equal_graph(seed):
     eg = O.EdgeGraph(60, u, v)
     assert np.array_equal(eg.in_off, g.in_off) and np.array_equal(eg.in_src, g.in_src)
     assert np.array_equal(eg.deg_out, g.deg_out) and np.array_equal(eg.deg_in, g.deg_in)
+    eo = O.EdgeGraph(60, u, v, out_lists=True)
+    assert np.array_equal(eo.row_off, g.row_off) and np.array_equal(eo.col_dst, g.col_dst)
+    assert np.array_equal(O.reorder_ta(eo, None, 3)[0], O.reorder_ta(g, None, 3)[0])
     # the fanout sampler sees the same lists: same kept entries and counts
     for k in (1, 3):
         _, keep_g, m_g = O.sample(g, 11, 2, k)
@@ -580,7 +592,8 @@ def test_ta_special_cases():
     mu, r = O.ta_step(g, np.arange(4, dtype=np.float64))
     assert np.allclose(mu, [0, 0.5, 1.5, 2.5]) and np.allclose(r, [1 / 6, 1, 2, 2.5])
     pi, spans, done = O.reorder_ta(g, None, 5)
-    assert np.array_equal(pi, np.arange(4)) and done == 1 and spans[0] == spans[1] == 0
+    # each of 1, 2, 3 spans itself and its predecessor
+    assert np.array_equal(pi, np.arange(4)) and done == 1 and spans[0] == spans[1] == 3
     # no edges: every vertex is its own neighbourhood, so nothing moves
     g = _g(5, [])
     boot = np.array([3, 0, 4, 1, 2], np.int32)
@@ -597,8 +610,47 @@ def test_ta_order_is_a_permutation_with_consistent_spans(seed):
     pi, spans, done = O.reorder_ta(g, boot, 4)
     assert np.array_equal(np.sort(pi), np.arange(60))
     assert spans[0] == O.total_span(g, boot) and spans[done] == O.total_span(g, pi)
-    # the order is ArgSort(r) with ties by ID: recompute r by repeated steps
-    r = boot.astype(np.float64)
+    # each update ranks the positions computed from the previous order, ties by ID
+    prev = boot
     for _ in range(done):
-        _, r = O.ta_step(g, r)
-    assert np.array_equal(np.argsort(pi, kind="stable"), np.lexsort((np.arange(60), r)))
+        _, r = O.ta_step(g, prev.astype(np.float64))
+        order = np.lexsort((np.arange(60), r))
+        prev = np.empty(60, np.int32)
+        prev[order] = np.arange(60)
+    assert np.array_equal(pi, prev)
+
+
+def test_ta_updates_compose():
+    """An update depends on the current order only, so t updates equal t
+    single updates each started from the last order, and an unchanged order
+    is a fixed point (stopping there loses nothing)."""
+    rng = np.random.default_rng(130)
+    _, u, v = random_digraph(rng, 80, 0.04, isolated=3)
+    g = O.Graph(80, u, v)
+    boot = rng.permutation(80).astype(np.int32)
+    pi, spans, done = O.reorder_ta(g, boot, 8)
+    step, seen = boot, [O.total_span(g, boot)]
+    for _ in range(done):
+        step, sp, d1 = O.reorder_ta(g, step, 1)
+        assert d1 == 1
+        seen.append(int(sp[1]))
+    assert np.array_equal(step, pi) and seen == list(spans[:done + 1])
+    if done < 8:
+        again, _, d = O.reorder_ta(g, pi, 3)
+        assert np.array_equal(again, pi) and d == 1
+
+
+def test_ta_lowers_span_on_skewed_rmat():
+    """The trend the paper reports for Alg. 1 (Sec. 3.8, convergence study):
+    C(pi) falls from both an uninformed (original / random-ID) bootstrap and
+    a locality bootstrap.  Here on the skewed RMAT recipe with random IDs at
+    1/400 of its size, from the identity and from the degree/BFS order."""
+    from fixtures import workloads as WL
+    w = WL.GCN_SKEW_RMAT_50M.scaled(n=125_000, e=2_500_000, chunk=512)
+    src, dst = WL.graph(w)
+    g = O.Graph(w.n, src, dst)
+    for boot in (None, O.reorder_bfs(g)):
+        pi, spans, done = O.reorder_ta(g, boot, 5)
+        assert done == 5
+        assert spans[1] < spans[0] and spans[5] < 0.75 * spans[0], spans
+        assert spans[5] == O.total_span(g, pi)
