@@ -66,6 +66,8 @@ def load(path: str):
     L.or_layer.argtypes = [i32, i64, vp, vp, vp, vp, vp, i32, i64, vp, vp, i64, i32, i64, vp, vp]
     L.or_reorder_bfs.restype = i32
     L.or_reorder_bfs.argtypes = [i64, vp, vp, vp]
+    L.or_reorder_rcm.restype = i32
+    L.or_reorder_rcm.argtypes = [i64, vp, vp, vp, vp, vp]
     L.or_total_span.restype = i64
     L.or_total_span.argtypes = [i64, vp, vp, vp]
     L.or_threads.restype = i32
@@ -245,6 +247,14 @@ def reorder_bfs(g: Graph) -> np.ndarray:
     out = np.empty(g.n, np.int32)
     if lib().or_reorder_bfs(g.n, _p(g.in_off), _p(g.in_src), _p(out)):
         raise MemoryError("or_reorder_bfs")
+    return out
+
+
+def reorder_rcm(g: Graph) -> np.ndarray:
+    """RCMK order of the symmetrised graph (Sec. 3.8's bootstrap) -> new_of_old int32[n]."""
+    out = np.empty(g.n, np.int32)
+    if lib().or_reorder_rcm(g.n, _p(g.row_off), _p(g.col_dst), _p(g.in_off), _p(g.in_src), _p(out)):
+        raise MemoryError("or_reorder_rcm")
     return out
 
 

@@ -483,6 +483,76 @@ int or_reorder_bfs(int64_t n, const int64_t* in_off, const int32_t* in_src, int3
 }
 
 /*
+ * RCMK: reverse Cuthill-McKee, the bandwidth-reducing bootstrap the paper
+ * applies before Alg. 1 (Sec. 3.8 cites Chan and George's linear-time
+ * formulation).  It works on the symmetrised graph: S(v) = the distinct
+ * vertices u != v with (u, v) or (v, u) an edge, and delta(v) = |S(v)|.
+ *   - roots: every vertex in (delta ascending, ID ascending) order; each one
+ *     not yet visited starts a breadth-first search;
+ *   - a dequeued vertex appends its unvisited neighbours in S in the same
+ *     (delta ascending, ID ascending) order (Cuthill-McKee);
+ *   - the visit order is reversed: new_of_old[v] = n - 1 - position of v.
+ * Readings taken here: no pseudo-peripheral root search (the minimum degree
+ * vertex of each component starts it) and ties by the lower ID, so the order
+ * is unique and compared bit for bit.  Returns 0, or -3 when out of memory.
+ */
+static const int32_t* g_or_sdeg;
+static int or_cm_cmp(const void* x, const void* y) {
+    int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
+    if (g_or_sdeg[a] != g_or_sdeg[b]) return g_or_sdeg[a] < g_or_sdeg[b] ? -1 : 1;
+    return (a > b) - (a < b);
+}
+int or_reorder_rcm(int64_t n, const int64_t* row_off, const int32_t* col_dst, const int64_t* in_off,
+                   const int32_t* in_src, int32_t* new_of_old) {
+    size_t nn = (size_t)(n > 0 ? n : 1);
+    int64_t cap = row_off[n] + in_off[n];
+    int32_t* adj = (int32_t*)malloc((size_t)(cap > 0 ? cap : 1) * sizeof(int32_t));
+    int32_t* deg = (int32_t*)malloc(nn * sizeof(int32_t));
+    int32_t* order = (int32_t*)malloc(nn * sizeof(int32_t));
+    int32_t* queue = (int32_t*)malloc(nn * sizeof(int32_t));
+    int64_t* count = (int64_t*)calloc(nn + 1, sizeof(int64_t));
+    uint8_t* seen = (uint8_t*)calloc(nn, 1);
+    if (!adj || !deg || !order || !queue || !count || !seen) return -3;
+    /* S(v): out- and in-neighbours together, sorted, repeats dropped; v's
+     * list starts at row_off[v] + in_off[v] */
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int64_t v = 0; v < n; v++) {
+        int32_t* a = adj + row_off[v] + in_off[v];
+        int64_t k = 0;
+        for (int64_t i = row_off[v]; i < row_off[v + 1]; i++) a[k++] = col_dst[i];
+        for (int64_t i = in_off[v]; i < in_off[v + 1]; i++) a[k++] = in_src[i];
+        qsort(a, (size_t)k, sizeof(int32_t), or_i32_cmp);
+        int64_t m = 0;
+        for (int64_t i = 0; i < k; i++)
+            if (a[i] != v && (m == 0 || a[i] != a[m - 1])) a[m++] = a[i];
+        deg[v] = (int32_t)m;
+    }
+    /* root order: a counting sort by delta keeps IDs ascending within a degree */
+    for (int64_t v = 0; v < n; v++) count[deg[v] + 1]++;
+    for (int64_t d = 0; d < n; d++) count[d + 1] += count[d];
+    for (int64_t v = 0; v < n; v++) order[count[deg[v]]++] = (int32_t)v;
+    g_or_sdeg = deg;
+    int64_t head = 0, tail = 0;
+    for (int64_t r = 0; r < n; r++) {
+        int32_t root = order[r];
+        if (seen[root]) continue;
+        seen[root] = 1;
+        queue[tail++] = root;
+        while (head < tail) {
+            int32_t x = queue[head++];
+            const int32_t* a = adj + row_off[x] + in_off[x];
+            int64_t first = tail;
+            for (int64_t i = 0; i < deg[x]; i++)
+                if (!seen[a[i]]) { seen[a[i]] = 1; queue[tail++] = a[i]; }
+            qsort(queue + first, (size_t)(tail - first), sizeof(int32_t), or_cm_cmp);
+        }
+    }
+    for (int64_t i = 0; i < n; i++) new_of_old[queue[i]] = (int32_t)(n - 1 - i);
+    free(adj); free(deg); free(order); free(queue); free(count); free(seen);
+    return 0;
+}
+
+/*
  * Total span C(pi) = sum_v (max_{u in N-(v)} pi(u) - min_{u in N-(v)} pi(u))
  * (Sec. 3.8).  N-(v) holds v's in-neighbours and v itself: every vertex
  * aggregates a self message, and a vertex with only that message has span 0,

@@ -80,6 +80,41 @@ MUTANTS = {
         "if (g_or_deg[a] != g_or_deg[b]) return g_or_deg[a] > g_or_deg[b] ? -1 : 1;",
         "if (0) return 0;",
         [P.test_reorder_star, P.test_reorder_path_and_two_components]),
+    # total span without the self message
+    "span_without_self": (
+        "int64_t lo = pi[v], hi = pi[v];",
+        "if (in_off[v + 1] == in_off[v]) continue;\n        int64_t lo = INT64_MAX, hi = INT64_MIN;",
+        [P.test_total_span_hand_example, P.test_span_equals_sum_of_active_counts]),
+    # Alg. 1: centre without the vertex's own position
+    "ta_mu_without_self": (
+        "double s = r_in[v];",
+        "double s = 0.0;",
+        [lambda: P.test_ta_updates_are_the_minimisers(0), P.test_ta_special_cases]),
+    # Alg. 1: out-neighbour centres not weighted by 1/d
+    "ta_r_unweighted": (
+        "num += mu[v] / dv;",
+        "num += mu[v] / d;",
+        [lambda: P.test_ta_updates_are_the_minimisers(0)]),
+    # Alg. 1: real positions carried over instead of the new order
+    "ta_keeps_real_positions": (
+        "for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];\n        or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);",
+        "if (t == 1) for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];\n        or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);\n        memcpy(r, r2, (size_t)n * sizeof(double));",
+        [lambda: P.test_ta_order_is_a_permutation_with_consistent_spans(0), P.test_ta_updates_compose]),
+    # RCMK: Cuthill-McKee order not reversed
+    "rcm_not_reversed": (
+        "new_of_old[queue[i]] = (int32_t)(n - 1 - i);",
+        "new_of_old[queue[i]] = (int32_t)i;",
+        [P.test_rcm_matches_scipy, P.test_rcm_special_cases]),
+    # RCMK: children by descending degree
+    "rcm_children_by_degree_desc": (
+        "if (g_or_sdeg[a] != g_or_sdeg[b]) return g_or_sdeg[a] < g_or_sdeg[b] ? -1 : 1;",
+        "if (g_or_sdeg[a] != g_or_sdeg[b]) return g_or_sdeg[a] > g_or_sdeg[b] ? -1 : 1;",
+        [P.test_rcm_matches_scipy, lambda: P.test_rcm_random_graphs_are_valid(0)]),
+    # RCMK: a reciprocal pair counted twice in the symmetric degree
+    "rcm_repeats_kept": (
+        "if (a[i] != v && (m == 0 || a[i] != a[m - 1])) a[m++] = a[i];",
+        "if (a[i] != v) a[m++] = a[i];",
+        [P.test_rcm_special_cases, P.test_rcm_matches_scipy]),
     # fp16 rounding truncates
     "f16_truncates": (
         "double r = nearbyint(q);\n    if (r >= 2048.0)",

@@ -374,23 +374,21 @@ def test_reorder_tree_levels():
     assert [int(np.nonzero(pi == i)[0][0]) for i in range(7)] == order
 
 
-def bfs_order_is_valid(g, pi):
-    """Properties that characterise the ordering: a bijection; each vertex is
-    either a root (first unvisited in root order at its time) or appears after
-    the earliest-ranked vertex that has it as an in-neighbour (its discoverer);
-    children of one discoverer are contiguous in (d_in desc, id asc) order and
+def search_order_is_valid(n, order, nbrs, key):
+    """Properties that characterise a breadth-first visit order whose roots
+    and children are ranked by ``key``: a bijection; each vertex is either a
+    root (the first unvisited vertex in key order at its time) or appears
+    after the earliest-placed vertex that lists it in ``nbrs`` (its
+    discoverer); children of one discoverer are contiguous in key order and
     blocks of children follow their discoverers' order."""
-    n = g.n
-    order = np.empty(n, np.int64)
-    order[pi] = np.arange(n)
-    assert np.array_equal(np.sort(pi), np.arange(n))
-    key = lambda x: (-int(g.deg_in[x]), int(x))
-    pos = pi
+    order = [int(x) for x in order]
+    assert sorted(order) == list(range(n))
+    pos = np.empty(n, np.int64)
+    pos[order] = np.arange(n)
     disc = np.full(n, -1)
-    # discoverer of w: the earliest vertex (by position) before w that lists w as in-neighbour
+    # discoverer of w: the earliest vertex (by position) before w that lists w
     for x in order:
-        for k in range(g.in_off[x], g.in_off[x + 1]):
-            w = g.in_src[k]
+        for w in nbrs(x):
             if pos[w] > pos[x] and disc[w] < 0:
                 disc[w] = x
     roots = [x for x in order if disc[x] < 0]
@@ -399,11 +397,10 @@ def bfs_order_is_valid(g, pi):
     # a root is the first unvisited vertex in global root order when it starts
     rank = sorted(range(n), key=key)
     for r in roots:
-        earlier = [x for x in rank[:rank.index(r)]]
-        assert all(pos[x] < pos[r] for x in earlier)
+        assert all(pos[x] < pos[r] for x in rank[:rank.index(r)])
     # non-roots in visit order: discoverer positions never decrease (blocks of
     # children are contiguous and follow their parents' order), and each
-    # block is sorted by (d_in desc, id asc)
+    # block is sorted by key
     last = -1
     for i, x in enumerate(order):
         if disc[x] < 0:
@@ -414,6 +411,32 @@ def bfs_order_is_valid(g, pi):
             assert key(order[i - 1]) < key(x)
         last = pos[disc[x]]
     return True
+
+
+def bfs_order_is_valid(g, pi):
+    """The degree/BFS order: search over in-neighbours, key (d_in desc, id asc)."""
+    order = np.empty(g.n, np.int64)
+    order[np.asarray(pi, np.int64)] = np.arange(g.n)
+    return search_order_is_valid(g.n, order, lambda x: g.in_src[g.in_off[x]:g.in_off[x + 1]],
+                                 lambda x: (-int(g.deg_in[x]), int(x)))
+
+
+def symmetric_neighbours(g):
+    S = [set() for _ in range(g.n)]
+    for u in range(g.n):
+        for v in g.col_dst[g.row_off[u]:g.row_off[u + 1]]:
+            S[u].add(int(v))
+            S[int(v)].add(u)
+    return S
+
+
+def rcm_order_is_valid(g, pi):
+    """RCMK: the reversed order is a Cuthill-McKee search of the symmetrised
+    graph, key (symmetric degree asc, id asc)."""
+    S = symmetric_neighbours(g)
+    order = np.empty(g.n, np.int64)
+    order[g.n - 1 - np.asarray(pi, np.int64)] = np.arange(g.n)
+    return search_order_is_valid(g.n, order, lambda x: sorted(S[x]), lambda x: (len(S[x]), int(x)))
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2, 3])
@@ -654,3 +677,77 @@ def test_ta_lowers_span_on_skewed_rmat():
         assert done == 5
         assert spans[1] < spans[0] and spans[5] < 0.75 * spans[0], spans
         assert spans[5] == O.total_span(g, pi)
+
+
+# ---- RCMK bootstrap (Sec. 3.8 bootstraps Alg. 1 with it)
+
+def test_rcm_matches_scipy():
+    """scipy's reverse_cuthill_mckee follows the same textbook rules (minimum
+    degree root, children by ascending degree with ties in ID order,
+    reversed); on connected graphs with a single minimum-degree vertex its
+    order is fully determined, so the two must agree exactly."""
+    import scipy.sparse as sp
+    from scipy.sparse.csgraph import connected_components, reverse_cuthill_mckee
+    rng = np.random.default_rng(140)
+    checked = 0
+    while checked < 40:
+        n = int(rng.integers(5, 120))
+        A, u, v = random_digraph(rng, n, float(rng.uniform(0.02, 0.2)))
+        S = sp.csr_matrix((A | A.T).astype(np.int32))
+        deg = np.diff(S.indptr)
+        if u.size == 0 or connected_components(S)[0] != 1 or (deg == deg.min()).sum() != 1:
+            continue
+        perm = reverse_cuthill_mckee(S, symmetric_mode=True)
+        want = np.empty(n, np.int32)
+        want[perm] = np.arange(n)
+        assert np.array_equal(O.reorder_rcm(O.Graph(n, u, v)), want)
+        checked += 1
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_rcm_random_graphs_are_valid(seed):
+    rng = np.random.default_rng(seed + 150)
+    _, u, v = random_digraph(rng, 60, 0.03, isolated=6)       # several components
+    g = O.Graph(60, u, v)
+    assert rcm_order_is_valid(g, O.reorder_rcm(g))
+
+
+def test_rcm_bandwidth_on_shuffled_path_and_grid():
+    rng = np.random.default_rng(160)
+    # a path with shuffled labels and random edge directions: bandwidth 1
+    n = 50
+    lab = rng.permutation(n)
+    e = [(lab[i], lab[i + 1]) if rng.random() < 0.5 else (lab[i + 1], lab[i]) for i in range(n - 1)]
+    g = _g(n, e)
+    pi = O.reorder_rcm(g)
+    assert np.abs(pi[g.col_dst] - np.repeat(pi[:n], np.diff(g.row_off))).max() == 1
+    # a k x k grid with shuffled labels: Cuthill-McKee levels are anti-diagonals,
+    # so no edge is longer than 2k - 1 (random labels give about k^2)
+    k = 12
+    lab = rng.permutation(k * k)
+    e = []
+    for i in range(k):
+        for j in range(k):
+            if j + 1 < k:
+                e.append((lab[i * k + j], lab[i * k + j + 1]))
+            if i + 1 < k:
+                e.append((lab[(i + 1) * k + j], lab[i * k + j]))
+    g = _g(k * k, e)
+    pi = O.reorder_rcm(g)
+    src = np.repeat(np.arange(k * k), np.diff(g.row_off))
+    assert np.abs(pi[g.col_dst] - pi[src]).max() <= 2 * k - 1
+    assert rcm_order_is_valid(g, pi)
+
+
+def test_rcm_special_cases():
+    # no edges: every vertex is a root, in ID order, then reversed
+    assert O.reorder_rcm(_g(4, [])).tolist() == [3, 2, 1, 0]
+    # a star (hub 0 sends to 1..4): the leaves have degree 1; root 1, then
+    # the hub, then leaves 2, 3, 4; reversed
+    g = _g(5, [(0, i) for i in range(1, 5)])
+    assert O.reorder_rcm(g).tolist() == [3, 4, 2, 1, 0]
+    # a reciprocal pair counts once in the symmetric degree: all four degrees
+    # are 1, so the search starts at 0 (counted twice, 0 and 1 would have
+    # degree 2 and the search would start at 2, giving [1, 0, 3, 2])
+    g = _g(4, [(0, 1), (1, 0), (2, 3)])
+    assert O.reorder_rcm(g).tolist() == [3, 2, 1, 0]
