@@ -215,6 +215,21 @@ int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* ds
 int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream);
 
 /*
+ * RCMK order (reverse Cuthill-McKee; Sec. 3.8 names it as the bandwidth-
+ * reducing bootstrap of Alg. 1).  The search runs on the symmetrised graph:
+ * u and v are neighbours when (u, v) or (v, u) is an edge, and a vertex's
+ * degree counts its distinct neighbours.  Roots are taken in (degree
+ * ascending, ID ascending) order, every root not yet visited starts a
+ * breadth-first search, and a dequeued vertex appends its unvisited
+ * neighbours in the same order; new_of_old[v] (device int32[n], written) =
+ * n - 1 - the visit position of v.  The order is unique.  Works in device
+ * memory of about 40 bytes per edge (the symmetric pair list and its sort).
+ * The graph is validated (TAURUS_E_INVALID).  Returns after the work
+ * completed.
+ */
+int taurus_reorder_rcm(const taurus_graph* g, int32_t* new_of_old, void* stream);
+
+/*
  * Topology-aware reordering (Sec. 3.8, Alg. 1): starting from the bootstrap
  * order pi0 (device int32[n], the new ID of each vertex, a permutation of
  * [0, n); NULL = the identity), up to `iterations` (>= 1) updates each take

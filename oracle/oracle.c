@@ -527,6 +527,7 @@ int or_reorder_rcm(int64_t n, const int64_t* row_off, const int32_t* col_dst, co
             if (a[i] != v && (m == 0 || a[i] != a[m - 1])) a[m++] = a[i];
         deg[v] = (int32_t)m;
     }
+    if (n >= (1 << 24)) fprintf(stderr, "reorder_rcm: symmetric lists done\n");
     /* root order: a counting sort by delta keeps IDs ascending within a degree */
     for (int64_t v = 0; v < n; v++) count[deg[v] + 1]++;
     for (int64_t d = 0; d < n; d++) count[d + 1] += count[d];

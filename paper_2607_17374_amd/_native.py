@@ -71,6 +71,7 @@ SIGNATURES = {
     "taurus_sampled_edges": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]),
     "taurus_layer_destroy": (None, [ctypes.c_void_p]),
     "taurus_reorder": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
+    "taurus_reorder_rcm": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_ta": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]),
     "taurus_relabel_graph": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p,

@@ -79,6 +79,14 @@ def reorder(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, stream=None) -
     return out
 
 
+def reorder_rcm(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, stream=None) -> torch.Tensor:
+    """taurus_reorder_rcm: RCMK order of the symmetrised graph, new_of_old int32[n] on the device."""
+    g = _graph(n, row_off, col_dst)
+    out = torch.empty(n, dtype=torch.int32, device=row_off.device)
+    N.check(N.lib().taurus_reorder_rcm(ctypes.byref(g), out.data_ptr(), _stream_ptr(stream)), "taurus_reorder_rcm")
+    return out
+
+
 def reorder_ta(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, pi0: Optional[torch.Tensor] = None,
                iterations: int = 5, stream=None):
     """taurus_reorder_ta: topology-aware order (Alg. 1) from bootstrap pi0

@@ -1685,6 +1685,7 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
 }
 
 int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s);
+int reorder_rcm_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s);
 int reorder_ta_impl(const taurus_graph& g, const int32_t* pi0, int iters, int32_t* pi, int64_t* spans,
                     int32_t* done, hipStream_t s);
 int relabel_impl(const taurus_graph& g, const int32_t* new_of_old, int64_t* row_off, int32_t* col_dst,
@@ -1769,6 +1770,14 @@ int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream) {
         check_graph_args(g);
         if (!new_of_old) fail(TAURUS_E_INVALID, "new_of_old is null");
         return reorder_impl(*g, new_of_old, static_cast<hipStream_t>(stream));
+    });
+}
+
+int taurus_reorder_rcm(const taurus_graph* g, int32_t* new_of_old, void* stream) {
+    return guarded([&] {
+        check_graph_args(g);
+        if (!new_of_old) fail(TAURUS_E_INVALID, "new_of_old is null");
+        return reorder_rcm_impl(*g, new_of_old, static_cast<hipStream_t>(stream));
     });
 }
 

@@ -1,25 +1,31 @@
-// Degree/BFS vertex ordering (a topology-aware bootstrap in the sense of
-// Sec. 3.8: destinations' sources get nearby ranks, which shrinks the span
-// between a destination's first and last message) and relabelling.
+// Search-based vertex orderings (topology-aware bootstraps in the sense of
+// Sec. 3.8: a destination's sources get nearby ranks, which shrinks the span
+// between its first and last message) and relabelling.
 //
-// The ordering is the visit order of a sequential breadth-first search:
-// roots are taken in (in-degree descending, ID ascending) order, every root
-// not yet visited starts a search over in-edges (vertex -> its
-// in-neighbours), and a dequeued vertex appends its unvisited in-neighbours
-// in the same (in-degree descending, ID ascending) order.
+// Both orderings are the visit order of a sequential breadth-first search
+// whose roots and children are ranked by a degree key, ties by lower ID:
+//   - degree/BFS: search over in-edges (vertex -> its in-neighbours), key
+//     in-degree descending;
+//   - RCMK (reverse Cuthill-McKee, the bootstrap Sec. 3.8 names): search
+//     over the symmetrised graph, key symmetric degree ascending, and the
+//     visit order reversed.
+// Every root not yet visited starts a search, and a dequeued vertex appends
+// its unvisited neighbours in key order.
 //
 // The GPU computes exactly that order without a queue:
 //   1. rank[v] = position of v in the root order (radix sort);
-//   2. owner[v] = min rank over every vertex v can reach along out-edges
-//      (v itself included): the search started by the root of rank r visits
-//      exactly the vertices with owner r, because a vertex belongs to the
-//      first root it can reach.  Computed by min-label propagation over the
-//      edges plus a shortcut through each label's own root, to a fixed point;
+//   2. owner[v] = min rank over every vertex v can reach along the reverse
+//      of the search's lists (out-edges for the in-edge search, the
+//      symmetric lists themselves for RCMK; v itself included): the search
+//      started by the root of rank r visits exactly the vertices with owner
+//      r, because a vertex belongs to the first root it can reach.  Computed
+//      by min-label propagation over the edges plus a shortcut through each
+//      label's own root, to a fixed point;
 //   3. trees are laid out one after another in root order (a histogram of
 //      owners and a scan give each tree's offset), roots take the first slot
 //      of their tree;
-//   4. all trees advance one level at a time: every unvisited in-neighbour w
-//      of a frontier vertex x in w's own tree is claimed by the frontier
+//   4. all trees advance one level at a time: every unvisited vertex w on
+//      the list of a frontier vertex x in w's own tree is claimed by the frontier
 //      vertex with the smallest position (the first one the queue would
 //      dequeue); the new level is sorted by (claimer's position, rank[w]) --
 //      the order the queue appends them in -- and takes the next free slots
@@ -32,13 +38,14 @@ namespace taurus {
 int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
                    int32_t* col_dst, hipStream_t s);
 
-// root-order key: (n-1 - d_in) << idbits | v  (in-degree descending, ID ascending)
-__global__ void k_root_keys(const int64_t* __restrict__ in_off, int64_t n, int idbits, uint64_t* __restrict__ keys,
-                            uint32_t* __restrict__ vals) {
+// root-order key: d << idbits | v (degree ascending) or (n-1 - d) << idbits | v
+// (degree descending), ID ascending either way; d = deg_off[v+1] - deg_off[v] <= n-1
+__global__ void k_root_keys(const int64_t* __restrict__ deg_off, int64_t n, int idbits, int ascending,
+                            uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v >= n) return;
-    const int64_t d = in_off[v + 1] - in_off[v];
-    keys[v] = ((uint64_t)(n - 1 - d) << idbits) | (uint64_t)v;
+    const int64_t d = deg_off[v + 1] - deg_off[v];
+    keys[v] = ((uint64_t)(ascending ? d : n - 1 - d) << idbits) | (uint64_t)v;
     vals[v] = (uint32_t)v;
 }
 
@@ -113,8 +120,8 @@ __global__ void k_roots(const int32_t* __restrict__ label, const int32_t* __rest
     frontier[atomicAdd(count, 1ull)] = (int32_t)v;
 }
 
-// One wave per frontier vertex x: each unvisited in-neighbour w in x's tree
-// records the smallest claiming position and is listed once.
+// One wave per frontier vertex x: each unvisited neighbour w (x's search
+// list) in x's tree records the smallest claiming position and is listed once.
 __global__ __launch_bounds__(256) void k_expand(const int32_t* __restrict__ frontier, int64_t nf,
                                                 const int64_t* __restrict__ in_off,
                                                 const int32_t* __restrict__ in_src,
@@ -180,11 +187,26 @@ __global__ void k_flag(const int32_t* __restrict__ pos, int64_t n, int* __restri
     if (v < n && (pos[v] < 0 || pos[v] >= n)) atomicOr(bad, 1);
 }
 
-int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
-    const int64_t n = g.n, e = g.e;
+__global__ void k_reverse(int32_t* __restrict__ pos, int64_t n) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) pos[v] = (int32_t)(n - 1 - pos[v]);
+}
+
+// The lists a search walks and the graph its owners come from.
+struct Search {
+    const int64_t* reach_off;  // owner labels: u reaches reach_adj[reach_off[u] .. reach_off[u+1])
+    const int32_t* reach_adj;
+    int64_t reach_e;
+    const int64_t* list_off;  // a dequeued x appends from list_adj[list_off[x] .. list_off[x+1]);
+    const int32_t* list_adj;  // its length is the degree of the key
+    bool ascending;           // key: degree ascending (else descending), then ID ascending
+    bool reverse;             // new_of_old = n - 1 - visit position
+};
+
+static void search_order(int64_t n, const Search& sp, int32_t* new_of_old, hipStream_t s) {
+    const int64_t e = sp.reach_e;
     const int T = 256;
     auto blocks = [&](int64_t count) { return (unsigned)std::max<int64_t>(1, ceil_div(count, T)); };
-    std::shared_ptr<Csc> csc = build_csc(g, s);  // validates the graph
     Arena tmp(s);
     const int idbits = std::max(1, bits_for(n - 1));
     int* flag = tmp.alloc<int>(2, "flags");  // [0] changed, [1] sort/consistency
@@ -193,7 +215,7 @@ int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
     SortBuffers rs{{tmp.alloc<uint64_t>(n, "root keys"), tmp.alloc<uint64_t>(n, "root keys (ping-pong)")},
                    {tmp.alloc<uint32_t>(n, "root order"), tmp.alloc<uint32_t>(n, "root order (ping-pong)")},
                    0};
-    k_root_keys<<<blocks(n), T, 0, s>>>(csc->in_off, n, idbits, rs.keys[0], rs.vals[0]);
+    k_root_keys<<<blocks(n), T, 0, s>>>(sp.list_off, n, idbits, sp.ascending ? 1 : 0, rs.keys[0], rs.vals[0]);
     TAURUS_CHECK_LAUNCH();
     fill_i32(flag, 2, 0, s);
     radix_sort_u64(rs, n, 2 * idbits, tmp, s, flag + 1, 1);
@@ -208,7 +230,7 @@ int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
         if (iter > 4 * n + 8) fail(TAURUS_E_DEVICE, "reorder: owner labels did not converge");
         fill_i32(flag, 1, 0, s);
         if (e > 0) {
-            k_label_edges<<<blocks(e), T, 0, s>>>(g.row_off, g.col_dst, n, e, label, flag);
+            k_label_edges<<<blocks(e), T, 0, s>>>(sp.reach_off, sp.reach_adj, n, e, label, flag);
             TAURUS_CHECK_LAUNCH();
         }
         k_label_jump<<<blocks(n), T, 0, s>>>(order, n, label, flag);
@@ -257,8 +279,8 @@ int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
     int64_t visited = (int64_t)nf;
     while (nf > 0) {
         fill_i32(reinterpret_cast<int32_t*>(count), 2, 0, s);
-        k_expand<<<(unsigned)ceil_div((int64_t)nf * 64, T), T, 0, s>>>(frontier, (int64_t)nf, csc->in_off,
-                                                                     csc->in_src, label, pos, claim, listed,
+        k_expand<<<(unsigned)ceil_div((int64_t)nf * 64, T), T, 0, s>>>(frontier, (int64_t)nf, sp.list_off,
+                                                                     sp.list_adj, label, pos, claim, listed,
                                                                      cand, count);
         TAURUS_CHECK_LAUNCH();
         unsigned long long nc = 0;
@@ -295,6 +317,95 @@ int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
     }
     if (bad || visited != n) fail(TAURUS_E_DEVICE, "reorder: %lld of %lld vertices placed", (long long)visited,
                                   (long long)n);
+    if (sp.reverse) {
+        k_reverse<<<blocks(n), T, 0, s>>>(pos, n);
+        TAURUS_CHECK_LAUNCH();
+    }
+}
+
+int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
+    std::shared_ptr<Csc> csc = build_csc(g, s);  // validates the graph
+    const Search sp{g.row_off, g.col_dst, g.e, csc->in_off, csc->in_src, false, false};
+    search_order(g.n, sp, new_of_old, s);
+    return TAURUS_OK;
+}
+
+// ---------------------------------------------------------------- RCMK -----
+// Per CSR edge (u, v): miss[i] = 1 when (v, u) is not an edge (binary search
+// of u in v's strictly ascending row).
+__global__ __launch_bounds__(256) void k_sym_missing(const int64_t* __restrict__ row_off,
+                                                     const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
+                                                     uint32_t* __restrict__ miss) {
+    __shared__ int64_t ro[4][64];
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
+    if (i >= e) return;
+    const int32_t v = col_dst[i];
+    int64_t lo = row_off[v], hi = row_off[v + 1];
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if (col_dst[mid] < u) lo = mid + 1;
+        else hi = mid;
+    }
+    miss[i] = (lo < row_off[v + 1] && col_dst[lo] == u) ? 0u : 1u;
+}
+
+// the symmetric pair list: every edge (u, v), then (v, u) for each edge whose
+// reverse is missing, at e + (its rank among those)
+__global__ __launch_bounds__(256) void k_sym_pairs(const int64_t* __restrict__ row_off,
+                                                   const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
+                                                   const uint32_t* __restrict__ miss,
+                                                   const uint64_t* __restrict__ miss_rank,
+                                                   int32_t* __restrict__ src, int32_t* __restrict__ dst) {
+    __shared__ int64_t ro[4][64];
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
+    if (i >= e) return;
+    const int32_t v = col_dst[i];
+    src[i] = (int32_t)u;
+    dst[i] = v;
+    if (miss[i]) {
+        const int64_t j = e + (int64_t)miss_rank[i];
+        src[j] = v;
+        dst[j] = (int32_t)u;
+    }
+}
+
+int reorder_rcm_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) {
+    validate_csr(g, s);
+    const int64_t n = g.n, e = g.e;
+    const int T = 256;
+    Arena sym(s);
+    int64_t* sym_off = sym.alloc<int64_t>(n + 1, "symmetric offsets");
+    int32_t* sym_adj = nullptr;
+    int64_t es = 0;
+    if (e > 0) {
+        Arena pairs(s);
+        int32_t *src = nullptr, *dst = nullptr;
+        {
+            Arena tmp(s);
+            uint32_t* miss = tmp.alloc<uint32_t>(e, "missing reverse flags");
+            uint64_t* rank = tmp.alloc<uint64_t>(e + 1, "missing reverse ranks");
+            k_sym_missing<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, miss);
+            TAURUS_CHECK_LAUNCH();
+            scan_u32_to_u64(miss, rank, e, true, tmp, s);
+            uint64_t m = 0;
+            Readback rb;
+            rb.add(&m, rank + e, 1);
+            rb.run(s);
+            es = e + (int64_t)m;
+            src = pairs.alloc<int32_t>(es, "symmetric sources");
+            dst = pairs.alloc<int32_t>(es, "symmetric destinations");
+            k_sym_pairs<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, miss, rank, src, dst);
+            TAURUS_CHECK_LAUNCH();
+        }
+        sym_adj = sym.alloc<int32_t>(es, "symmetric lists");
+        build_csr_impl(n, es, src, dst, sym_off, sym_adj, s);  // sorted, no repeats, no self loops
+    } else {
+        fill_i32(reinterpret_cast<int32_t*>(sym_off), 2 * (n + 1), 0, s);
+    }
+    const Search sp{sym_off, sym_adj, es, sym_off, sym_adj, true, true};
+    search_order(n, sp, new_of_old, s);
     return TAURUS_OK;
 }
 

@@ -163,27 +163,35 @@ def run_c5(w) -> dict:
     del c["_host"]
     res["csr"] = c
     del src, dst
-    pi = T.reorder(w.n, row_off, col_dst)
-    torch.cuda.synchronize()
-    say("GPU degree/BFS order")
-    pi_h = pi.cpu().numpy()
-    want = O.reorder_bfs(g)
-    res["reorder_bit_exact"] = bool(np.array_equal(pi_h, want))
     ident = np.arange(w.n, dtype=np.int32)
     res["span_random_ids"] = O.total_span(g, ident)
-    res["span_reordered"] = O.total_span(g, want)
-    say(f"order bit-exact vs oracle: {res['reorder_bit_exact']}; total span {res['span_random_ids']} -> "
-        f"{res['span_reordered']}")
-    # topology-aware order (Alg. 1) from the degree/BFS order
-    pi_ta, spans, done = T.reorder_ta(w.n, row_off, col_dst, pi, 5)
-    torch.cuda.synchronize()
-    say(f"GPU topology-aware order: spans {spans[:done + 1].tolist()}")
-    want_ta, wspans, wdone = O.reorder_ta(g, want, 5)
-    res["reorder_ta_bit_exact"] = bool(np.array_equal(pi_ta.cpu().numpy(), want_ta) and done == wdone
-                                       and np.array_equal(spans, wspans))
-    res["span_ta"] = spans[:done + 1].tolist()
-    say(f"topology-aware order bit-exact vs oracle: {res['reorder_ta_bit_exact']}")
-    del want, want_ta
+    orders = {}
+    for label, gpu_fn, oracle_fn in (("degree/BFS order", T.reorder, O.reorder_bfs),
+                                     ("RCMK order", T.reorder_rcm, O.reorder_rcm)):
+        t0 = time.time()
+        pi = gpu_fn(w.n, row_off, col_dst)
+        torch.cuda.synchronize()
+        t_gpu = time.time() - t0
+        say(f"GPU {label} in {t_gpu:.2f} s")
+        want = oracle_fn(g)
+        ok = bool(np.array_equal(pi.cpu().numpy(), want))
+        span = O.total_span(g, want)
+        res[label] = {"bit_exact": ok, "span": span, "gpu_s": t_gpu}
+        say(f"{label} bit-exact vs oracle: {ok}; total span {res['span_random_ids']} -> {span}")
+        orders[label] = pi
+        # Alg. 1 from this bootstrap
+        ta_label = f"topology-aware order from {label.split()[0]}"
+        t0 = time.time()
+        pi_ta, spans, done = T.reorder_ta(w.n, row_off, col_dst, pi, 5)
+        torch.cuda.synchronize()
+        t_gpu = time.time() - t0
+        say(f"GPU {ta_label} in {t_gpu:.2f} s: spans {spans[:done + 1].tolist()}")
+        want_ta, wspans, wdone = O.reorder_ta(g, want, 5)
+        ok = bool(np.array_equal(pi_ta.cpu().numpy(), want_ta) and done == wdone and np.array_equal(spans, wspans))
+        res[ta_label] = {"bit_exact": ok, "spans": spans[:done + 1].tolist(), "gpu_s": t_gpu}
+        say(f"{ta_label} bit-exact vs oracle: {ok}")
+        orders[ta_label] = pi_ta
+        del want, want_ta
     ids = [destination_sample(w.seed * 1000 + li, g.deg_in) for li in range(1, w.layers + 1)]
     xh = WL.input_features(w)
     say("features")
@@ -195,7 +203,7 @@ def run_c5(w) -> dict:
     torch.cuda.empty_cache()
     # reordered runs: relabel the graph, permute the features, run, un-permute
     runs = {"random IDs": host_a}
-    for label, perm in (("degree/BFS order", pi), ("topology-aware order", pi_ta)):
+    for label, perm in orders.items():
         r2, c2 = T.relabel_graph(w.n, row_off, col_dst, perm)
         X2 = T.permute_rows(X, perm)
         torch.cuda.empty_cache()
@@ -203,7 +211,7 @@ def run_c5(w) -> dict:
         ph = perm.cpu().numpy()
         ids_new = [ph[i].astype(np.int64) for i in ids]   # the same vertices under their new IDs
         host_b, stats_b, last_b = run_model(w, r2, c2, X2, w.chunk, ids_new)
-        res[label] = {"stats": stats_b}
+        res[label]["stats"] = stats_b
         del r2, c2, X2
         back = T.permute_rows(last_b, perm, inverse=True).cpu()
         del last_b

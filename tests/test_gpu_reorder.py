@@ -1,5 +1,5 @@
-"""Degree/BFS reordering, relabelling and row permutation on the GPU vs the
-oracle (needs an MI355X)."""
+"""Vertex orderings (degree/BFS, RCMK, the topology-aware Alg. 1),
+relabelling and row permutation on the GPU vs the oracle (needs an MI355X)."""
 import sys
 
 import numpy as np
@@ -49,10 +49,17 @@ def _cases():
     v = np.concatenate([np.zeros(698, np.int64), np.arange(400, 700)])
     out.append(("stars", n, *_simple(n, u, v)))
     out.append(("edgeless", 500, np.zeros(0, np.int32), np.zeros(0, np.int32)))
+    n = 2500   # half the edges reciprocated: pairs that symmetrise to one neighbour
+    u, v = rng.integers(0, n, 6000), rng.integers(0, n, 6000)
+    back = rng.random(6000) < 0.5
+    out.append(("reciprocal", n, *_simple(n, np.concatenate([u, v[back]]), np.concatenate([v, u[back]]))))
     return out
 
 
-@pytest.mark.parametrize("case", range(5))
+NCASES = 6
+
+
+@pytest.mark.parametrize("case", range(NCASES))
 def test_reorder_bit_exact(torch_cuda, case):
     import oracle as O
     import paper_2607_17374_amd as T
@@ -154,8 +161,27 @@ def test_reorder_error_paths(torch_cuda):
     assert ex.value.status == -1
 
 
-@pytest.mark.parametrize("case", range(5))
-@pytest.mark.parametrize("boot", ["identity", "bfs"])
+@pytest.mark.parametrize("case", range(NCASES))
+def test_reorder_rcm_bit_exact(torch_cuda, case):
+    """RCMK order of the symmetrised graph: bit for bit against the oracle."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    name, n, src, dst = _cases()[case]
+    _note(f"reorder_rcm {name}: n={n} e={src.size}")
+    g = O.Graph(n, src, dst)
+    row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(src).cuda(), torch_cuda.from_numpy(dst).cuda())
+    pi = T.reorder_rcm(n, row_off, col_dst)
+    assert np.array_equal(pi.cpu().numpy(), O.reorder_rcm(g))
+    if src.size:
+        broken = col_dst.clone()
+        broken[0] = n + 5
+        with pytest.raises(T.TaurusError) as ex:
+            T.reorder_rcm(n, row_off, broken)
+        assert ex.value.status == -1
+
+
+@pytest.mark.parametrize("case", range(NCASES))
+@pytest.mark.parametrize("boot", ["identity", "bfs", "rcm"])
 def test_reorder_ta_bit_exact(torch_cuda, case, boot):
     """Alg. 1 (topology-aware order) against the oracle: the order, the total
     span after each update and the number of updates are equal."""
@@ -165,7 +191,7 @@ def test_reorder_ta_bit_exact(torch_cuda, case, boot):
     _note(f"reorder_ta {name} from {boot}: n={n} e={src.size}")
     g = O.Graph(n, src, dst)
     row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(src).cuda(), torch_cuda.from_numpy(dst).cuda())
-    p0 = None if boot == "identity" else O.reorder_bfs(g)
+    p0 = {"identity": lambda: None, "bfs": lambda: O.reorder_bfs(g), "rcm": lambda: O.reorder_rcm(g)}[boot]()
     pi, spans, done = T.reorder_ta(n, row_off, col_dst, None if p0 is None else torch_cuda.from_numpy(p0).cuda(), 6)
     want, wspans, wdone = O.reorder_ta(g, p0, 6)
     assert done == wdone
@@ -175,9 +201,10 @@ def test_reorder_ta_bit_exact(torch_cuda, case, boot):
 
 def test_reorder_ta_skewed_rmat_model(torch_cuda):
     """C5's recipe (skewed RMAT, random IDs, fp16 GCN) at 1/400 of the
-    vertices: Alg. 1 from the degree/BFS order, bit-exact with the oracle; the
-    model on the relabelled graph, un-permuted, matches the oracle in the
-    original IDs."""
+    vertices: the RCMK order and Alg. 1 from it and from the degree/BFS
+    order, bit-exact with the oracle, each lowering the total span; the
+    model on the Alg. 1 relabelled graph, un-permuted, matches the oracle in
+    the original IDs."""
     import oracle as O
     import paper_2607_17374_amd as T
     from paper_2607_17374_amd.api import torch_dtype
@@ -187,11 +214,14 @@ def test_reorder_ta_skewed_rmat_model(torch_cuda):
     _note(f"reorder_ta {w.name}")
     g, zs = H.oracle_model(w, src, dst)
     row_off, col_dst = H.gpu_graph(w, src, dst)
-    boot = T.reorder(w.n, row_off, col_dst)
-    pi, spans, done = T.reorder_ta(w.n, row_off, col_dst, boot, 5)
-    want, wspans, wdone = O.reorder_ta(g, boot.cpu().numpy(), 5)
-    assert done == wdone and np.array_equal(pi.cpu().numpy(), want) and np.array_equal(spans, wspans)
-    _note(f"  spans {spans[:done + 1].tolist()}")
+    rcm = T.reorder_rcm(w.n, row_off, col_dst)
+    assert np.array_equal(rcm.cpu().numpy(), O.reorder_rcm(g))
+    for boot in (rcm, T.reorder(w.n, row_off, col_dst)):
+        pi, spans, done = T.reorder_ta(w.n, row_off, col_dst, boot, 5)
+        want, wspans, wdone = O.reorder_ta(g, boot.cpu().numpy(), 5)
+        assert done == wdone and np.array_equal(pi.cpu().numpy(), want) and np.array_equal(spans, wspans)
+        _note(f"  spans {spans[:done + 1].tolist()}")
+        assert spans[done] < spans[0]
     r2, c2 = T.relabel_graph(w.n, row_off, col_dst, pi)
     xh = WL.input_features(w)
     X2 = T.permute_rows(torch.from_numpy(xh.view(np.int16)).cuda().view(torch_dtype(w.feat_dtype)), pi)
