@@ -177,6 +177,9 @@ typedef struct {
     double ms_gemm, ms_self, ms_scatter, ms_fixup;  /* ms_self stays 0: the self messages
                                       run inside the scatter launch, timed in ms_scatter */
     int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
+    int64_t pool_rows;             /* budgeted layers: accumulator rows of the pool,
+                                      hub rows included (0 in core)                     */
+    int64_t hub_rows;              /* of which resident hub rows                        */
 } taurus_stats;
 
 /* Thread-local message describing the last failing call on this thread. */

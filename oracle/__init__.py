@@ -69,6 +69,8 @@ def load(path: str):
     L.or_reorder_rcm.restype = i32
     L.or_reorder_rcm.argtypes = [i64, vp, vp, vp, vp, vp]
     L.or_total_span.restype = i64
+    L.or_active_profile.restype = None
+    L.or_active_profile.argtypes = [i64, vp, vp, vp, i64, vp]
     L.or_total_span.argtypes = [i64, vp, vp, vp]
     L.or_threads.restype = i32
     L.or_threads.argtypes = []
@@ -286,6 +288,15 @@ def total_span(g: Graph, pi: np.ndarray) -> int:
     """C(pi) of Sec. 3.8 with the self message in every neighbourhood."""
     pi = np.ascontiguousarray(pi, np.int32)
     return int(lib().or_total_span(g.n, _p(g.in_off), _p(g.in_src), _p(pi)))
+
+
+def active_profile(g: Graph, pi: np.ndarray, chunk: int) -> np.ndarray:
+    """A[k] of Sec. 3.8 at chunk granularity: destinations holding a partial
+    state after chunk k of the order pi (self message included)."""
+    pi = np.ascontiguousarray(pi, np.int32)
+    A = np.empty((g.n + chunk - 1) // chunk, np.int64)
+    lib().or_active_profile(g.n, _p(g.in_off), _p(g.in_src), _p(pi), chunk, _p(A))
+    return A
 
 
 def mask_bits(words: np.ndarray, e: int) -> np.ndarray:

@@ -575,6 +575,38 @@ int64_t or_total_span(int64_t n, const int64_t* in_off, const int32_t* in_src, c
     return total;
 }
 
+/*
+ * Residency profile at chunk granularity (Sec. 3.8's A(t), with t counted in
+ * chunks of `chunk` consecutive ranks): with N-(v) including v,
+ *     a(v) = min_{u in N-(v)} floor(pi(u) / chunk),  c(v) = max likewise,
+ *     A[k] = #{v : a(v) <= k < c(v)},  k = 0 .. ceil(n / chunk) - 1,
+ * the destinations holding a partial state after chunk k.  With chunk = 1,
+ * sum_k A[k] = C(pi) (the paper's identity M = C(pi)).
+ */
+void or_active_profile(int64_t n, const int64_t* in_off, const int32_t* in_src, const int32_t* pi, int64_t chunk,
+                       int64_t* A) {
+    int64_t nch = (n + chunk - 1) / chunk;
+    int64_t* diff = (int64_t*)calloc((size_t)nch + 1, sizeof(int64_t));
+#pragma omp parallel for schedule(dynamic, 4096)
+    for (int64_t v = 0; v < n; v++) {
+        int64_t lo = pi[v] / chunk, hi = lo;
+        for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+            int64_t c = pi[in_src[k]] / chunk;
+            if (c < lo) lo = c;
+            if (c > hi) hi = c;
+        }
+        if (hi > lo) {
+#pragma omp atomic
+            diff[lo] += 1;
+#pragma omp atomic
+            diff[hi] -= 1;
+        }
+    }
+    int64_t run = 0;
+    for (int64_t k = 0; k < nch; k++) { run += diff[k]; A[k] = run; }
+    free(diff);
+}
+
 /* ------------------------------------- topology-aware reordering (Alg. 1) -- */
 /*
  * Sec. 3.8 minimises the in-neighbourhood dispersion

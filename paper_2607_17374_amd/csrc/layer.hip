@@ -1664,6 +1664,8 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
             st->reloads = L->res->reload_count(s);
             st->hub_message_share = L->res->hub_share;
             st->device_bytes += L->res->arena.peak();
+            st->pool_rows = L->res->S;
+            st->hub_rows = L->res->H;
         }
         st->h2d_bytes = L->h2d_bytes + st->reloads * row_bytes;
         st->d2h_bytes = st->evictions * row_bytes + (L->d.out_on_host ? (L->n - (int64_t)left) * out_bytes : 0);

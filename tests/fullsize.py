@@ -140,6 +140,59 @@ def run_model(w, row_off, col_dst, X, plan_chunk, ids, mask_check=None, keep_inp
     return host, stats, h
 
 
+def residency_run(w, g, pi_host, row_off, col_dst, X, slot_list) -> dict:
+    """Residency of one ordering: the oracle's chunk-level profile A[k] of
+    the order, then the second layer of w (on input X) in core and under
+    budgets that leave about each of `slot_list` pool rows with 1% hubs.
+    Outputs must equal the in-core run bit for bit; reports evictions,
+    reloads and host-link bytes."""
+    import torch
+    import oracle as O
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    from tests import harness as H
+    A = O.active_profile(g, pi_host, w.chunk)
+    res = {"peak_active": int(A.max()), "mean_active": float(A.mean()), "budgeted": []}
+    say(f"  residency: peak A {res['peak_active']}, mean A {res['mean_active']:.0f}")
+    spec = H.layer_specs(w)[1]
+
+    def run(budget):
+        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=X.device)
+        torch.cuda.synchronize()
+        t0 = time.time()
+        L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, hbm_budget=budget,
+                    hub_fraction=0.01 if budget else 0.0, **spec)
+        L.push_all(X)
+        st = L.finalize()
+        L.destroy()
+        torch.cuda.synchronize()
+        return out, st, time.time() - t0
+
+    ref, st0, t_ref = run(0)
+    res["t_in_core"] = t_ref
+    for slots in slot_list:
+        budget = H.pool_budget(st0, w.n, spec["d_out"], spec["d_in"], w.chunk, slots)
+        try:
+            out, st, t = run(budget)
+        except T.TaurusError as ex:
+            if ex.status != -6:
+                raise
+            res["budgeted"].append({"slots_asked": slots, "refused": str(ex)})
+            say(f"  residency: about {slots} pool rows refused: {ex}")
+            continue
+        r = dict(slots_asked=slots, pool_rows=st["pool_rows"], equal_to_in_core=bool(torch.equal(ref, out)),
+                 evictions=st["evictions"], reloads=st["reloads"], d2h_bytes=st["d2h_bytes"],
+                 h2d_bytes=st["h2d_bytes"], device_bytes=st["device_bytes"], seconds=t)
+        res["budgeted"].append(r)
+        say(f"  residency: {r['pool_rows']} pool rows: {r['evictions']} evictions, {r['reloads']} reloads, "
+            f"{r['d2h_bytes'] / 1e9:.2f} GB out, {t:.2f} s (in core {t_ref:.2f} s), "
+            f"equal to in core: {r['equal_to_in_core']}")
+        del out
+    del ref
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_c5(w) -> dict:
     import torch
     import oracle as O
@@ -198,6 +251,8 @@ def run_c5(w) -> dict:
     X = torch.from_numpy(xh.view(np.int16)).cuda().view(torch_dtype(w.feat_dtype))
     host_a, stats_a, last_a = run_model(w, row_off, col_dst, X, w.chunk, ids)
     res["random_ids"] = {"stats": stats_a}
+    slots = [w.n * 7 // 25, w.n * 6 // 25, w.n // 5]      # 28%, 24% and 20% of the rows
+    res["random_ids"]["residency"] = residency_run(w, g, ident, row_off, col_dst, X, slots)
     last_a_host = last_a.cpu()
     del last_a
     torch.cuda.empty_cache()
@@ -212,6 +267,7 @@ def run_c5(w) -> dict:
         ids_new = [ph[i].astype(np.int64) for i in ids]   # the same vertices under their new IDs
         host_b, stats_b, last_b = run_model(w, r2, c2, X2, w.chunk, ids_new)
         res[label]["stats"] = stats_b
+        res[label]["residency"] = residency_run(w, g, ph, r2, c2, X2, slots)
         del r2, c2, X2
         back = T.permute_rows(last_b, perm, inverse=True).cpu()
         del last_b

@@ -45,7 +45,7 @@ def test_binding_structs_match_header_layout(native):
     assert native.LayerDesc.out.offset == 80 and native.LayerDesc.stream.offset == 96
     assert native.LayerDesc.plan.offset == 112
     assert ctypes.sizeof(native.LayerDesc) == 120
-    assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8
+    assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 2 * 8
 
 
 def test_hash_matches_published_splitmix64(golden_dir):

@@ -14,7 +14,6 @@ from tests import harness as H
 pytestmark = pytest.mark.gpu
 
 PIECE = 512          # the library's hub-piece length (work units per long segment)
-FIXED_PER_VERTEX = 34
 
 
 @pytest.fixture(scope="module")
@@ -39,17 +38,6 @@ def _max_chunk_destinations(src, dst, n, chunk):
     per_chunk = np.bincount(seg // n, weights=units, minlength=(n + chunk - 1) // chunk)
     rows = np.minimum(chunk, n - np.arange(per_chunk.size) * chunk)
     return int((per_chunk + rows).max())
-
-
-def _budget(stats_incore, n, d_out, d_in, chunk, slots):
-    """A budget that leaves about `slots` accumulator rows (mirrors the
-    library's planning: everything but the dense rows, the residency arrays,
-    two staging buffers, then the pool, each with 1/8 rounding room)."""
-    row = d_out * 4
-    dense = n * row
-    other = stats_incore["device_bytes"] - dense
-    staging = 2 * min(chunk, n) * d_in * 4 * 9 // 8
-    return int(other + FIXED_PER_VERTEX * n * 9 // 8 + 4096 + staging + slots * (row + 4) * 9 // 8 + (1 << 20))
 
 
 def _run(torch, w, row_off, col_dst, X, budget=0, hub_fraction=0.0):
@@ -89,7 +77,7 @@ def test_budget_eviction_matches_incore_c4_shape(torch_cuda):
     hubs = int(np.ceil(0.01 * w.n))
     slots = hubs + need + (w.n - hubs - need) // 4
     assert slots < w.n * 0.6, (need, slots)
-    budgets = [_budget(s, w.n, spec["d_out"], spec["d_in"], w.chunk, slots)
+    budgets = [H.pool_budget(s, w.n, spec["d_out"], spec["d_in"], w.chunk, slots)
                for s, spec in zip(ref_stats, H.layer_specs(w))]
     _note(f"  budgets {budgets} (slots {slots}, chunk destinations {need})")
     outs, stats = _run(torch, w, row_off, col_dst, X, budget=budgets, hub_fraction=0.01)

@@ -473,6 +473,17 @@ def test_span_equals_sum_of_active_counts():
             if pi[nb].min() <= t < pi[nb].max():
                 total += 1
     assert O.total_span(g, pi) == total
+    # the residency profile at chunk size 1 sums to the same total (M = C(pi)),
+    # and at other chunk sizes counts the partial states held after each chunk
+    assert O.active_profile(g, pi, 1).sum() == total
+    for chunk in (3, 7, 40):
+        A = O.active_profile(g, pi, chunk)
+        for k in range(A.size):
+            held = 0
+            for x in range(40):
+                nb = np.concatenate([[x], g.in_src[g.in_off[x]:g.in_off[x + 1]]])
+                held += int(pi[nb].min() // chunk <= k < pi[nb].max() // chunk)
+            assert A[k] == held
     # and the bandwidth bound C(pi) <= 2 |V| B, B = max edge length under pi
     B = int(np.abs(pi[u].astype(np.int64) - pi[v]).max())
     assert total <= 2 * 40 * B
