@@ -70,6 +70,8 @@ def load(path: str):
     L.or_reorder_rcm.argtypes = [i64, vp, vp, vp, vp, vp]
     L.or_total_span.restype = i64
     L.or_active_profile.restype = None
+    L.or_residency_sim.restype = i32
+    L.or_residency_sim.argtypes = [i64, vp, vp, vp, i64, i64, i64, i32, u64, vp, vp, vp]
     L.or_active_profile.argtypes = [i64, vp, vp, vp, i64, vp]
     L.or_total_span.argtypes = [i64, vp, vp, vp]
     L.or_threads.restype = i32
@@ -297,6 +299,27 @@ def active_profile(g: Graph, pi: np.ndarray, chunk: int) -> np.ndarray:
     A = np.empty((g.n + chunk - 1) // chunk, np.int64)
     lib().or_active_profile(g.n, _p(g.in_off), _p(g.in_src), _p(pi), chunk, _p(A))
     return A
+
+
+EVICTION = {"pending": 0, "random": 1, "fifo": 2, "lru": 3}
+
+
+def residency_sim(g: Graph, chunk: int, slots: int, hubs: int, policy: str = "pending", seed: int = 0,
+                  keep: np.ndarray | None = None):
+    """Slot-level simulation of a budgeted layer's residency (Sec. 3.5) ->
+    (evictions, reloads, reloads per vertex int32[n]).  keep: bool per CSR
+    edge (propagated edges of a sampled layer), None = every edge.  Raises
+    RuntimeError when the pool cannot free enough rows."""
+    ev, rl = ctypes.c_int64(0), ctypes.c_int64(0)
+    per = np.zeros(g.n, np.int32)
+    kp = None if keep is None else np.ascontiguousarray(keep, np.uint8)
+    rc = lib().or_residency_sim(g.n, _p(g.row_off), _p(g.col_dst), _p(kp), chunk, slots, hubs, EVICTION[policy],
+                                seed & (2**64 - 1), ctypes.byref(ev), ctypes.byref(rl), _p(per))
+    if rc == -3:
+        raise MemoryError("or_residency_sim")
+    if rc:
+        raise RuntimeError("residency: the pool cannot free enough rows")
+    return ev.value, rl.value, per
 
 
 def mask_bits(words: np.ndarray, e: int) -> np.ndarray:

@@ -607,6 +607,143 @@ void or_active_profile(int64_t n, const int64_t* in_off, const int32_t* in_src, 
     free(diff);
 }
 
+/*
+ * The residency protocol of a budgeted layer (Sec. 3.5), simulated at the
+ * level of slots: which partial states are evicted and reloaded, chunk by
+ * chunk, for a pool of S rows of which H hold hubs.  Chunks of `chunk`
+ * consecutive sources run in ascending order.  keep (per CSR edge, NULL =
+ * every edge) marks the propagated edges; M(v) = v's propagated in-edges.
+ *   - hubs: the H vertices first by (|M(v)| descending, ID ascending); their
+ *     rows never move;
+ *   - pending(v) starts at |M(v)| + 1 (the self message arrives in v's own
+ *     chunk);
+ *   - before chunk k: its touched vertices (destinations of its propagated
+ *     edges, and its own vertices) that hold no row ask for one; if the free
+ *     rows fall short by M, the M candidates (holding a row, not hubs, not
+ *     touched by chunk k, still pending) with the smallest (key, ID) are
+ *     evicted.  Keys (Sec. 3.5.3 and the policies of the eviction study):
+ *       0 fewest pending: min(pending, 16383);
+ *       1 random: H(seed, 7, k, v) >> 50;
+ *       2 FIFO: the chunk at which v last took a row;
+ *       3 LRU: the last chunk that touched v;
+ *     chunk numbers >> s, s the smallest shift that fits the chunk count
+ *     in 14 bits, then capped at 16383;
+ *   - the asking vertices take rows (an evicted one is reloaded), the chunk's
+ *     messages arrive, and touched vertices that completed free their rows.
+ * Outputs the eviction and reload totals and reloads per vertex.  Returns 0,
+ * -6 when the candidates cannot free enough rows, -3 when out of memory.
+ */
+static const int32_t* g_or_m;
+static int or_hub_cmp(const void* x, const void* y) {
+    int32_t a = *(const int32_t*)x, b = *(const int32_t*)y;
+    if (g_or_m[a] != g_or_m[b]) return g_or_m[a] > g_or_m[b] ? -1 : 1;
+    return (a > b) - (a < b);
+}
+typedef struct { int64_t key; int32_t v; } or_victim;
+static int or_victim_cmp(const void* x, const void* y) {
+    const or_victim* a = (const or_victim*)x; const or_victim* b = (const or_victim*)y;
+    if (a->key != b->key) return a->key < b->key ? -1 : 1;
+    return (a->v > b->v) - (a->v < b->v);
+}
+int or_residency_sim(int64_t n, const int64_t* row_off, const int32_t* col_dst, const uint8_t* keep, int64_t chunk,
+                     int64_t S, int64_t H, int policy, uint64_t seed, int64_t* evictions, int64_t* reloads,
+                     int32_t* reloads_of) {
+    size_t nn = (size_t)(n > 0 ? n : 1);
+    int32_t* m = (int32_t*)calloc(nn, sizeof(int32_t));
+    int32_t* order = (int32_t*)malloc(nn * sizeof(int32_t));
+    int64_t* pend = (int64_t*)malloc(nn * sizeof(int64_t));
+    int32_t* mark = (int32_t*)malloc(nn * sizeof(int32_t));
+    int32_t* adm = (int32_t*)calloc(nn, sizeof(int32_t));
+    uint8_t* hub = (uint8_t*)calloc(nn, 1);
+    uint8_t* resident = (uint8_t*)calloc(nn, 1);
+    uint8_t* evicted = (uint8_t*)calloc(nn, 1);
+    int32_t* touched = (int32_t*)malloc(nn * sizeof(int32_t));
+    int32_t* need = (int32_t*)malloc(nn * sizeof(int32_t));
+    or_victim* cand = (or_victim*)malloc(nn * sizeof(or_victim));
+    if (!m || !order || !pend || !mark || !adm || !hub || !resident || !evicted || !touched || !need || !cand)
+        return -3;
+    for (int64_t u = 0; u < n; u++)
+        for (int64_t i = row_off[u]; i < row_off[u + 1]; i++)
+            if (!keep || keep[i]) m[col_dst[i]]++;
+    for (int64_t v = 0; v < n; v++) {
+        order[v] = (int32_t)v;
+        pend[v] = (int64_t)m[v] + 1;
+        mark[v] = -1;
+        reloads_of[v] = 0;
+    }
+    g_or_m = m;
+    qsort(order, nn, sizeof(int32_t), or_hub_cmp);
+    for (int64_t j = 0; j < H && j < n; j++) { hub[order[j]] = 1; resident[order[j]] = 1; }
+    int64_t free_rows = S - H;
+    *evictions = 0;
+    *reloads = 0;
+    int rc = free_rows < 0 ? -6 : 0;
+    int64_t nch = (n + chunk - 1) / chunk;
+    int cbits = 0;
+    while (cbits < 63 && ((int64_t)1 << cbits) <= nch - 1) cbits++;
+    int shift = cbits > 14 ? cbits - 14 : 0;
+    for (int64_t k = 0; k < nch && rc == 0; k++) {
+        int64_t b = k * chunk, e = b + chunk < n ? b + chunk : n;
+        int64_t nt = 0, nq = 0;
+        for (int64_t u = b; u < e; u++)
+            for (int64_t i = row_off[u]; i < row_off[u + 1]; i++) {
+                int32_t v = col_dst[i];
+                if ((!keep || keep[i]) && mark[v] != (int32_t)k) { mark[v] = (int32_t)k; touched[nt++] = v; }
+            }
+        for (int64_t v = b; v < e; v++)
+            if (mark[v] != (int32_t)k) { mark[v] = (int32_t)k; touched[nt++] = (int32_t)v; }
+        /* the LRU key needs each candidate's last touch before chunk k: the
+         * candidates are exactly the vertices chunk k does not touch, so
+         * their marks still hold it */
+        for (int64_t t = 0; t < nt; t++)
+            if (pend[touched[t]] > 0 && !resident[touched[t]]) need[nq++] = touched[t];
+        if (nq > free_rows) {
+            int64_t M = nq - free_rows, nc = 0;
+            for (int64_t v = 0; v < n; v++) {
+                if (!resident[v] || hub[v] || mark[v] == (int32_t)k || pend[v] <= 0) continue;
+                int64_t key;
+                if (policy == 1) {
+                    uint64_t args[2] = {(uint64_t)k, (uint64_t)v};
+                    key = (int64_t)(or_hash(seed, 7, 2, args) >> 50);
+                } else if (policy == 2) {
+                    key = adm[v] >> shift;
+                } else if (policy == 3) {
+                    key = mark[v] >> shift;
+                } else {
+                    key = pend[v];
+                }
+                if (key > 16383) key = 16383;
+                cand[nc].key = key;
+                cand[nc].v = (int32_t)v;
+                nc++;
+            }
+            if (nc < M) { rc = -6; break; }
+            qsort(cand, (size_t)nc, sizeof(or_victim), or_victim_cmp);
+            for (int64_t j = 0; j < M; j++) { resident[cand[j].v] = 0; evicted[cand[j].v] = 1; }
+            free_rows += M;
+            *evictions += M;
+        }
+        for (int64_t j = 0; j < nq; j++) {
+            int32_t v = need[j];
+            resident[v] = 1;
+            adm[v] = (int32_t)k;
+            if (evicted[v]) { evicted[v] = 0; reloads_of[v]++; (*reloads)++; }
+        }
+        free_rows -= nq;
+        for (int64_t u = b; u < e; u++)
+            for (int64_t i = row_off[u]; i < row_off[u + 1]; i++)
+                if (!keep || keep[i]) pend[col_dst[i]]--;
+        for (int64_t v = b; v < e; v++) pend[v]--;
+        for (int64_t t = 0; t < nt; t++) {
+            int32_t v = touched[t];
+            if (pend[v] == 0 && !hub[v] && resident[v]) { resident[v] = 0; free_rows++; }
+        }
+    }
+    free(m); free(order); free(pend); free(mark); free(adm); free(hub); free(resident); free(evicted);
+    free(touched); free(need); free(cand);
+    return rc;
+}
+
 /* ------------------------------------- topology-aware reordering (Alg. 1) -- */
 /*
  * Sec. 3.8 minimises the in-neighbourhood dispersion

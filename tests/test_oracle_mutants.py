@@ -115,6 +115,26 @@ MUTANTS = {
         "if (a[i] != v && (m == 0 || a[i] != a[m - 1])) a[m++] = a[i];",
         "if (a[i] != v) a[m++] = a[i];",
         [P.test_rcm_special_cases, P.test_rcm_matches_scipy]),
+    # residency: LRU ranked by admission instead of last use
+    "residency_lru_by_admission": (
+        "key = mark[v] >> shift;",
+        "key = adm[v] >> shift;",
+        [lambda: P.test_residency_hand_cases("case1")]),
+    # residency: the self message not counted in pending
+    "residency_no_self_message": (
+        "pend[v] = (int64_t)m[v] + 1;",
+        "pend[v] = (int64_t)m[v];",
+        [lambda: P.test_residency_hand_cases("case1"), lambda: P.test_residency_invariants(0)]),
+    # residency: FIFO keeps the first admission across reloads
+    "residency_fifo_first_admission_only": (
+        "adm[v] = (int32_t)k;\n            if (evicted[v])",
+        "if (!evicted[v]) adm[v] = (int32_t)k;\n            if (evicted[v])",
+        [P.test_residency_fifo_readmission]),
+    # residency: most pending evicted first
+    "residency_most_pending_first": (
+        "key = pend[v];",
+        "key = 16383 - (pend[v] < 16383 ? pend[v] : 16383);",
+        [lambda: P.test_residency_hand_cases("case1"), P.test_fewest_pending_reloads_least]),
     # fp16 rounding truncates
     "f16_truncates": (
         "double r = nearbyint(q);\n    if (r >= 2048.0)",
