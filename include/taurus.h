@@ -41,6 +41,17 @@ typedef enum {
 
 typedef enum { TAURUS_F32 = 0, TAURUS_BF16 = 1, TAURUS_F16 = 2 } taurus_dtype;
 
+/* Eviction policies of a budgeted layer (desc.eviction).  The paper's
+ * policy evicts the partial states with the fewest pending messages
+ * (Sec. 3.5.3); random, FIFO and LRU are the policies it is compared with
+ * (Sec. 4, eviction study).  Ties go to the lower vertex ID. */
+typedef enum {
+    TAURUS_EVICT_PENDING = 0, /* fewest pending messages first                               */
+    TAURUS_EVICT_RANDOM = 1,  /* smallest H(seed, 7, chunk, v) >> 50 first, a fresh order per chunk */
+    TAURUS_EVICT_FIFO = 2,    /* earliest admission (the chunk at which the row was taken)    */
+    TAURUS_EVICT_LRU = 3      /* least recently used (the last chunk that sent a message)     */
+} taurus_eviction;
+
 /* Per-graph structures shared by the layers over one graph (see
  * taurus_plan_create). */
 typedef struct taurus_plan taurus_plan;
@@ -123,6 +134,10 @@ typedef struct {
  *   profile      1: time every kernel of the layer with HIP events; 2: time
  *                only the scatter launches (fewer events in the stream); the
  *                totals are returned in taurus_stats.
+ *   eviction     TAURUS_EVICT_* policy of a budgeted layer (ignored in core).
+ *                Victims are ranked by a 14-bit key: pending counts past
+ *                16383 share the last bin, and chunk numbers are shifted
+ *                right until the layer's chunk count fits 14 bits.
  *   plan         NULL, or a plan made for this graph (same n, e, row_off,
  *                col_dst pointers) and this chunk size: an exact layer
  *                (fanout = 0) then shares the plan's chunk index, and a
@@ -144,6 +159,7 @@ typedef struct {
     void* stream;
     int32_t profile;
     const taurus_plan* plan;
+    int32_t eviction;
 } taurus_layer_desc;
 
 typedef struct taurus_layer taurus_layer;
@@ -342,6 +358,16 @@ int taurus_finalize(taurus_layer* L, taurus_stats* stats);
  * Synchronises the layer's stream.
  */
 int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_kept);
+
+/*
+ * Reloads per vertex of a budgeted layer (the distribution the paper's
+ * eviction study plots, Sec. 4): counts (host int64[bins], bins >= 2)
+ * receives, for i < bins - 1, the number of vertices reloaded exactly i
+ * times, and in counts[bins - 1] those reloaded bins - 1 times or more.  An
+ * in-core layer reports counts[0] = n.  Any time after init; synchronises
+ * the layer's stream.
+ */
+int taurus_layer_reload_histogram(taurus_layer* L, int64_t* counts, int32_t bins);
 
 /* Release everything the layer allocated.  NULL is ignored. */
 void taurus_layer_destroy(taurus_layer* L);

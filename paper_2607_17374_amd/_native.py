@@ -39,7 +39,8 @@ class LayerDesc(ctypes.Structure):
                 ("fanout", ctypes.c_int32), ("layer", ctypes.c_int32), ("seed", ctypes.c_uint64),
                 ("chunk", ctypes.c_int64), ("hbm_budget", ctypes.c_int64), ("hub_fraction", ctypes.c_double),
                 ("out", ctypes.c_void_p), ("out_on_host", ctypes.c_int32),
-                ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p)]
+                ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p),
+                ("eviction", ctypes.c_int32)]
 
 
 class Stats(ctypes.Structure):
@@ -71,6 +72,7 @@ SIGNATURES = {
     "taurus_finalize": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(Stats)]),
     "taurus_sampled_edges": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]),
     "taurus_layer_destroy": (None, [ctypes.c_void_p]),
+    "taurus_layer_reload_histogram": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),
     "taurus_reorder": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_rcm": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_ta": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,

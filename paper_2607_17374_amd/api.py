@@ -128,6 +128,10 @@ def permute_rows(x: torch.Tensor, new_of_old: torch.Tensor, inverse: bool = Fals
     return out
 
 
+# eviction policies of a budgeted layer (taurus_eviction)
+EVICTION = {"pending": 0, "random": 1, "fifo": 2, "lru": 3}
+
+
 class Plan:
     """taurus_plan_create / taurus_plan_destroy: the per-graph structures
     (exact chunk index, in-edge lists for sampling) for one chunk size,
@@ -166,7 +170,8 @@ class Layer:
                  d_out: int, weight_cat: np.ndarray, bias: Optional[np.ndarray], out: torch.Tensor,
                  in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
-                 hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None):
+                 hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None,
+                 eviction: str = "pending"):
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
@@ -181,7 +186,8 @@ class Layer:
             weight=self._w.ctypes.data, bias=None if self._b is None else self._b.ctypes.data,
             fanout=fanout, layer=layer, seed=seed & (2**64 - 1), chunk=chunk, hbm_budget=hbm_budget,
             hub_fraction=hub_fraction, out=out_ptr, out_on_host=out_on_host,
-            stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None)
+            stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None,
+            eviction=EVICTION[eviction] if isinstance(eviction, str) else int(eviction))
         self._keep = (row_off, col_dst, plan)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")
@@ -206,6 +212,14 @@ class Layer:
         if rc != N.OK:
             raise N.TaurusError(rc, "taurus_finalize", N.last_error())
         return d
+
+    def reload_histogram(self, bins: int = 64) -> np.ndarray:
+        """taurus_layer_reload_histogram: vertices reloaded exactly i times
+        (i < bins - 1), then those reloaded bins - 1 times or more."""
+        counts = np.zeros(bins, dtype=np.int64)
+        N.check(N.lib().taurus_layer_reload_histogram(self._h, counts.ctypes.data, bins),
+                "taurus_layer_reload_histogram")
+        return counts
 
     def sampled_edges(self):
         """(mask_words uint64[ceil(e/64)], n_kept)."""

@@ -1367,6 +1367,8 @@ static void validate_desc(const taurus_layer_desc* d) {
     if (!d->out) fail(TAURUS_E_INVALID, "out is null");
     if (d->out_on_host != 0 && d->out_on_host != 1) fail(TAURUS_E_INVALID, "out_on_host=%d", d->out_on_host);
     if (d->hub_fraction < 0.0 || d->hub_fraction > 1.0) fail(TAURUS_E_INVALID, "hub_fraction %g", d->hub_fraction);
+    if (d->eviction < TAURUS_EVICT_PENDING || d->eviction > TAURUS_EVICT_LRU)
+        fail(TAURUS_E_INVALID, "eviction policy %d", (int)d->eviction);
     if (d->hbm_budget < 0) fail(TAURUS_E_INVALID, "hbm_budget < 0");
     if (d->profile < 0 || d->profile > 2) fail(TAURUS_E_INVALID, "profile %d", d->profile);
 }
@@ -1503,7 +1505,7 @@ static void layer_init(taurus_layer* L) {
             fail(TAURUS_E_BUDGET,
                  "budget %lld leaves %lld accumulator slots; %lld hubs plus one chunk's %lld destinations need more",
                  (long long)d.hbm_budget, (long long)S, (long long)H, (long long)max_dc);
-        L->res = std::make_unique<Residency>(s, n, L->d_o, S, H, idx.m, idx.kept);
+        L->res = std::make_unique<Residency>(s, n, L->d_o, S, H, idx.m, idx.kept, d.eviction, d.seed, L->nchunks);
         const int64_t total = L->arena.bytes() + index_bytes + L->res->arena.bytes();
         if (total > d.hbm_budget)
             fail(TAURUS_E_BUDGET, "residency structures take %lld bytes, above the budget %lld", (long long)total,
@@ -1899,6 +1901,24 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
             if (L->g.e % 64) mask_bits_host[words - 1] = (1ull << (L->g.e % 64)) - 1;
         }
         if (n_kept) *n_kept = L->idx->kept;
+        return TAURUS_OK;
+    } catch (const Failure& f) {
+        return f.status;
+    }
+}
+
+int taurus_layer_reload_histogram(taurus_layer* L, int64_t* counts, int32_t bins) {
+    if (!L || !counts || bins < 2) {
+        set_error("null argument or bins < 2");
+        return TAURUS_E_INVALID;
+    }
+    try {
+        if (L->res) {
+            L->res->reload_histogram(counts, bins, L->s);
+        } else {
+            for (int b = 0; b < bins; b++) counts[b] = 0;
+            counts[0] = L->n;
+        }
         return TAURUS_OK;
     } catch (const Failure& f) {
         return f.status;

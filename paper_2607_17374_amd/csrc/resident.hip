@@ -1,8 +1,10 @@
 // Accumulator residency under a device-memory budget (Sec. 3.5: a GPU
 // store keeps the accumulators of high in-degree hub vertices resident; the
 // partial states of other destinations live in a bounded pool and, when the
-// pool runs short, those with the fewest pending messages are evicted to
-// host memory and reloaded before their next message; Sec. 3.5.3).
+// pool runs short, victims are evicted to host memory and reloaded before
+// their next message).  The paper's policy evicts those with the fewest
+// pending messages (Sec. 3.5.3); random, first-in-first-out and
+// least-recently-used choices are its comparison policies (Sec. 4).
 //
 // Accumulator rows live in a pool of S slots; slot_of[v] names v's row (or
 // -1).  Hubs -- the top hub_fraction of vertices by (message count
@@ -12,15 +14,22 @@
 //      vertices, for the self message) is marked with k; those still pending
 //      and without a slot are listed;
 //   2. if the free slots do not cover the list, victims are chosen among
-//      resident, non-hub, still-pending vertices the chunk does not touch:
-//      fewest pending first, then lowest ID (a 16,384-bin histogram of the
-//      pending counts gives the threshold; ties at the threshold are ranked
-//      by an exclusive scan in vertex order; counts at or above the last bin
-//      are ranked by ID only, which changes which rows move, never results);
+//      resident, non-hub, still-pending vertices the chunk does not touch,
+//      smallest policy key first, then lowest ID.  Keys (14 bits):
+//        fewest pending: min(pending messages, 16383);
+//        random:         the top 14 bits of H(seed, 7, k, v);
+//        FIFO:           the chunk at which v last took a row;
+//        LRU:            the last chunk that sent v a message;
+//      chunk numbers are shifted right until the layer's chunk count fits
+//      14 bits, and values past the last bin share it.  A 16,384-bin
+//      histogram of the keys gives the threshold; ties at the threshold are
+//      ranked by an exclusive scan in vertex order.  The key only decides
+//      which rows move, never the results;
 //      their rows are written to the pinned host store and their slots freed;
 //   3. listed vertices take free slots; evicted ones copy their row back.
 // After the chunk, touched vertices that completed return their slots.
 // Rows are moved by exact copies, so results equal the in-core run's.
+#include "device.hpp"
 #include "internal.hpp"
 #include "resident.hpp"
 
@@ -54,37 +63,57 @@ __device__ inline bool res_candidate(int v, int32_t k, const int32_t* slot_of, c
     return slot_of[v] >= 0 && !hub[v] && dc_mark[v] != k && cnt[v].x > 0;
 }
 
+// What the eviction key of a candidate reads.
+struct EvictKeys {
+    int policy;     // TAURUS_EVICT_*
+    int shift;      // chunk numbers >> shift fit the bins
+    uint64_t seed;  // random policy
+    const int2* cnt;
+    const int32_t* dc_mark;  // last chunk that touched v
+    const int32_t* adm;      // chunk at which v last took a row
+};
+
+__device__ inline int res_key(int v, int32_t k, const EvictKeys& e) {
+    switch (e.policy) {
+        case TAURUS_EVICT_RANDOM: {
+            uint64_t h = mix64(e.seed + SM64_GAMMA + 7u);
+            h = mix64(h + SM64_GAMMA + (uint64_t)k);
+            h = mix64(h + SM64_GAMMA + (uint64_t)v);
+            return (int)(h >> 50);
+        }
+        case TAURUS_EVICT_FIFO: return min(max(e.adm[v], 0) >> e.shift, RES_BINS - 1);
+        case TAURUS_EVICT_LRU: return min(max(e.dc_mark[v], 0) >> e.shift, RES_BINS - 1);
+        default: return min(max(e.cnt[v].x, 0), RES_BINS - 1);
+    }
+}
+
 __global__ __launch_bounds__(1024) void k_res_hist(int64_t n, int32_t k, const int32_t* __restrict__ slot_of,
-                                                   const uint8_t* __restrict__ hub,
-                                                   const int32_t* __restrict__ dc_mark,
-                                                   const int2* __restrict__ cnt, unsigned int* __restrict__ hist) {
+                                                   const uint8_t* __restrict__ hub, EvictKeys e,
+                                                   unsigned int* __restrict__ hist) {
     __shared__ unsigned int h[RES_BINS];
     for (int i = threadIdx.x; i < RES_BINS; i += blockDim.x) h[i] = 0;
     __syncthreads();
     for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < n; v += (int64_t)gridDim.x * blockDim.x)
-        if (res_candidate((int)v, k, slot_of, hub, dc_mark, cnt))
-            atomicAdd(&h[min(cnt[v].x, RES_BINS - 1)], 1u);
+        if (res_candidate((int)v, k, slot_of, hub, e.dc_mark, e.cnt)) atomicAdd(&h[res_key((int)v, k, e)], 1u);
     __syncthreads();
     for (int i = threadIdx.x; i < RES_BINS; i += blockDim.x)
         if (h[i]) atomicAdd(&hist[i], h[i]);
 }
 
 __global__ void k_res_tie_flags(int64_t n, int32_t k, int32_t tau, const int32_t* __restrict__ slot_of,
-                                const uint8_t* __restrict__ hub, const int32_t* __restrict__ dc_mark,
-                                const int2* __restrict__ cnt, int32_t* __restrict__ tie) {
+                                const uint8_t* __restrict__ hub, EvictKeys e, int32_t* __restrict__ tie) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v >= n) return;
-    tie[v] = res_candidate((int)v, k, slot_of, hub, dc_mark, cnt) && min(cnt[v].x, RES_BINS - 1) == tau ? 1 : 0;
+    tie[v] = res_candidate((int)v, k, slot_of, hub, e.dc_mark, e.cnt) && res_key((int)v, k, e) == tau ? 1 : 0;
 }
 
 __global__ void k_res_victims(int64_t n, int32_t k, int32_t tau, int64_t tie_take,
-                              const int32_t* __restrict__ slot_of, const uint8_t* __restrict__ hub,
-                              const int32_t* __restrict__ dc_mark, const int2* __restrict__ cnt,
+                              const int32_t* __restrict__ slot_of, const uint8_t* __restrict__ hub, EvictKeys e,
                               const int64_t* __restrict__ tie_rank, int32_t* __restrict__ victims,
                               unsigned long long* __restrict__ count) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (v >= n || !res_candidate((int)v, k, slot_of, hub, dc_mark, cnt)) return;
-    const int b = min(cnt[v].x, RES_BINS - 1);
+    if (v >= n || !res_candidate((int)v, k, slot_of, hub, e.dc_mark, e.cnt)) return;
+    const int b = res_key((int)v, k, e);
     if (b < tau || (b == tau && tie_rank[v] < tie_take)) victims[atomicAdd(count, 1ull)] = (int32_t)v;
 }
 
@@ -108,12 +137,14 @@ __global__ __launch_bounds__(256) void k_res_evict(const int32_t* __restrict__ v
     }
 }
 
-// one wave per listed vertex: take slot free_list[top - 1 - j]; reload if evicted
+// one wave per listed vertex: take slot free_list[top - 1 - j] at chunk k;
+// reload if evicted
 __global__ __launch_bounds__(256) void k_res_assign(const int32_t* __restrict__ need, int64_t nn, int d_o,
-                                                    const int32_t* __restrict__ free_list, int64_t top,
+                                                    const int32_t* __restrict__ free_list, int64_t top, int32_t k,
                                                     float* __restrict__ pool, const float* __restrict__ store,
                                                     int32_t* __restrict__ slot_of, uint8_t* __restrict__ evicted,
-                                                    int32_t* __restrict__ want,
+                                                    int32_t* __restrict__ want, int32_t* __restrict__ adm,
+                                                    int32_t* __restrict__ reloads_of,
                                                     unsigned long long* __restrict__ reloads) {
     const int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
@@ -129,9 +160,11 @@ __global__ __launch_bounds__(256) void k_res_assign(const int32_t* __restrict__ 
     if (lane == 0) {
         if (evicted[v]) {
             evicted[v] = 0;
+            reloads_of[v] += 1;
             atomicAdd(reloads, 1ull);
         }
         slot_of[v] = s;
+        adm[v] = k;
         want[v] = 0;
     }
 }
@@ -181,21 +214,33 @@ __global__ void k_sum_hub_messages(const int32_t* __restrict__ m, const uint8_t*
     if (v < n && hub[v]) atomicAdd(sum, (unsigned long long)m[v]);
 }
 
+// histogram of per-vertex reload counts; the last bin takes the rest
+__global__ void k_reload_hist(const int32_t* __restrict__ reloads_of, int64_t n, int bins,
+                              unsigned long long* __restrict__ hist) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) atomicAdd(&hist[min(reloads_of[v], bins - 1)], 1ull);
+}
+
 int64_t Residency::fixed_bytes(int64_t n) {
-    // slot_of, dc_mark, want, tie flags (int32); tie ranks (int64); victims,
-    // need list (int32); hub, evicted (u8); histogram
-    return n * (4 + 4 + 4 + 4 + 8 + 4 + 4 + 1 + 1) + RES_BINS * 4 + 4096;
+    // slot_of, dc_mark, want, tie flags, admission chunks, reload counts
+    // (int32); tie ranks (int64); victims, need list (int32); hub, evicted
+    // (u8); histogram
+    return n * (4 + 4 + 4 + 4 + 4 + 4 + 8 + 4 + 4 + 1 + 1) + RES_BINS * 4 + 4096;
 }
 
 Residency::Residency(hipStream_t s, int64_t n_, int d_o_, int64_t slots, int64_t hubs, const int32_t* m,
-                     int64_t messages)
-    : arena(s), n(n_), d_o(d_o_), S(slots), H(hubs) {
+                     int64_t messages, int policy_, uint64_t seed_, int64_t nchunks)
+    : arena(s), n(n_), d_o(d_o_), S(slots), H(hubs), policy(policy_), seed(seed_) {
+    const int cbits = bits_for(std::max<int64_t>(nchunks - 1, 0));
+    chunk_shift = cbits > 14 ? cbits - 14 : 0;
     const int T = 256;
     const unsigned nb = (unsigned)ceil_div(n, T);
     slot_of = arena.alloc<int32_t>(n, "accumulator slots");
     dc_mark = arena.alloc<int32_t>(n, "chunk marks");
     want = arena.alloc<int32_t>(n, "slot requests");
     tie = arena.alloc<int32_t>(n, "eviction ties");
+    adm = arena.alloc<int32_t>(n, "admission chunks");
+    reloads_of = arena.alloc<int32_t>(n, "reloads per vertex");
     tie_rank = arena.alloc<int64_t>(n + 1, "eviction tie ranks");
     victims = arena.alloc<int32_t>(n, "eviction victims");
     need = arena.alloc<int32_t>(n, "slot list");
@@ -209,6 +254,8 @@ Residency::Residency(hipStream_t s, int64_t n_, int d_o_, int64_t slots, int64_t
     fill_i32(slot_of, n, -1, s);
     fill_i32(dc_mark, n, -1, s);
     fill_i32(want, n, 0, s);
+    fill_i32(adm, n, 0, s);
+    fill_i32(reloads_of, n, 0, s);
     k_fill_u8<<<nb, T, 0, s>>>(hub, n, 0);
     TAURUS_CHECK_LAUNCH();
     k_fill_u8<<<nb, T, 0, s>>>(evicted, n, 0);
@@ -273,8 +320,9 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
     if (nn > (unsigned long long)top) {
         const int64_t M = (int64_t)nn - top;
         // threshold of the pending counts among candidates
+        const EvictKeys ek{policy, chunk_shift, seed, cnt, dc_mark, adm};
         fill_i32(reinterpret_cast<int32_t*>(hist), RES_BINS, 0, s);
-        k_res_hist<<<1024, 1024, 0, s>>>(n, k, slot_of, hub, dc_mark, cnt, hist);
+        k_res_hist<<<1024, 1024, 0, s>>>(n, k, slot_of, hub, ek, hist);
         TAURUS_CHECK_LAUNCH();
         std::vector<unsigned int> hh(RES_BINS);
         {
@@ -294,14 +342,14 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
         if (tau < 0)
             fail(TAURUS_E_BUDGET, "accumulator pool: chunk %d needs %lld slots, only %lld can be freed", k,
                  (long long)nn, (long long)(top + below));
-        k_res_tie_flags<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, slot_of, hub, dc_mark, cnt, tie);
+        k_res_tie_flags<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, slot_of, hub, ek, tie);
         TAURUS_CHECK_LAUNCH();
         Arena tmp(s);
         scan_i32_to_i64(tie, tie_rank, n, false, tmp, s);
         unsigned long long* vcount = counters + 1;
         fill_i32(reinterpret_cast<int32_t*>(vcount), 2, 0, s);
-        k_res_victims<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, M - below, slot_of, hub, dc_mark, cnt,
-                                                             tie_rank, victims, vcount);
+        k_res_victims<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, M - below, slot_of, hub, ek, tie_rank,
+                                                             victims, vcount);
         TAURUS_CHECK_LAUNCH();
         unsigned long long got = 0;
         {
@@ -318,9 +366,9 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
         top += (int32_t)M;
     }
     if (nn > 0) {
-        k_res_assign<<<(unsigned)ceil_div((int64_t)nn * 64, T), T, 0, s>>>(need, (int64_t)nn, d_o, free_list, top,
+        k_res_assign<<<(unsigned)ceil_div((int64_t)nn * 64, T), T, 0, s>>>(need, (int64_t)nn, d_o, free_list, top, k,
                                                                          pool, store_dev, slot_of, evicted, want,
-                                                                         counters + 2);
+                                                                         adm, reloads_of, counters + 2);
         TAURUS_CHECK_LAUNCH();
         k_res_set<<<1, 1, 0, s>>>(free_top, top - (int32_t)nn);
         TAURUS_CHECK_LAUNCH();
@@ -332,6 +380,19 @@ void Residency::release(const ResChunk& c, const int2* cnt, hipStream_t s) {
     if (total == 0) return;
     k_res_release<<<(unsigned)ceil_div(total, 256), 256, 0, s>>>(c, total, cnt, hub, slot_of, free_list, free_top);
     TAURUS_CHECK_LAUNCH();
+}
+
+void Residency::reload_histogram(int64_t* counts, int bins, hipStream_t s) {
+    Arena tmp(s);
+    unsigned long long* h = tmp.alloc<unsigned long long>(bins, "reload histogram");
+    fill_i32(reinterpret_cast<int32_t*>(h), 2 * (int64_t)bins, 0, s);
+    k_reload_hist<<<(unsigned)ceil_div(std::max<int64_t>(n, 1), 256), 256, 0, s>>>(reloads_of, n, bins, h);
+    TAURUS_CHECK_LAUNCH();
+    std::vector<unsigned long long> hh((size_t)bins);
+    Readback rb;
+    rb.add(hh.data(), h, bins);
+    rb.run(s);
+    for (int b = 0; b < bins; b++) counts[b] = (int64_t)hh[(size_t)b];
 }
 
 int64_t Residency::reload_count(hipStream_t s) {

@@ -24,7 +24,9 @@ class Residency {
 public:
     // slots: pool rows (hubs included); hubs: resident hub rows; m: message
     // counts per vertex (hub order); messages: their sum
-    Residency(hipStream_t s, int64_t n, int d_o, int64_t slots, int64_t hubs, const int32_t* m, int64_t messages);
+    // policy: TAURUS_EVICT_*; seed: the random policy's; nchunks: the layer's chunk count
+    Residency(hipStream_t s, int64_t n, int d_o, int64_t slots, int64_t hubs, const int32_t* m, int64_t messages,
+              int policy, uint64_t seed, int64_t nchunks);
     ~Residency();
     Residency(const Residency&) = delete;
     Residency& operator=(const Residency&) = delete;
@@ -37,9 +39,14 @@ public:
     // free the slots of the chunk's destinations that completed
     void release(const ResChunk& c, const int2* cnt, hipStream_t s);
     int64_t reload_count(hipStream_t s);
+    // counts[i] = vertices reloaded i times (i < bins - 1), counts[bins - 1] = the rest
+    void reload_histogram(int64_t* counts, int bins, hipStream_t s);
 
     Arena arena;
     int64_t n, d_o, S, H;
+    int policy;
+    uint64_t seed;
+    int chunk_shift = 0;
     float* pool = nullptr;       // [S][d_o]
     int32_t* slot_of = nullptr;  // [n], -1 = no row
     int64_t evictions = 0;
@@ -47,6 +54,7 @@ public:
 
 private:
     int32_t *dc_mark = nullptr, *want = nullptr, *tie = nullptr, *victims = nullptr, *need = nullptr;
+    int32_t *adm = nullptr, *reloads_of = nullptr;
     int64_t* tie_rank = nullptr;
     uint8_t *hub = nullptr, *evicted = nullptr;
     unsigned int* hist = nullptr;

@@ -115,14 +115,14 @@ def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, 
 def pool_budget(stats_incore: dict, n: int, d_out: int, d_in: int, chunk: int, slots: int) -> int:
     """An hbm_budget that leaves about `slots` accumulator rows, from the
     statistics of the same layer run in core (mirrors the library's planning:
-    everything but the dense rows, about 34 bytes of residency arrays per
+    everything but the dense rows, about 42 bytes of residency arrays per
     vertex, two staging buffers, then the pool, each with 1/8 rounding
     room)."""
     row = d_out * 4
     dense = n * row
     other = stats_incore["device_bytes"] - dense
     staging = 2 * min(chunk, n) * d_in * 4 * 9 // 8
-    return int(other + 34 * n * 9 // 8 + 4096 + staging + slots * (row + 4) * 9 // 8 + (1 << 20))
+    return int(other + 42 * n * 9 // 8 + 4096 + staging + slots * (row + 4) * 9 // 8 + (1 << 20))
 
 
 def to_numpy_f64(t, dtype_code: int) -> np.ndarray:

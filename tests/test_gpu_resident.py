@@ -99,6 +99,43 @@ def test_budget_eviction_matches_incore_c4_shape(torch_cuda):
         assert r["n_bad"] == 0, (li, r)
 
 
+@pytest.mark.parametrize("policy", ["pending", "random", "fifo", "lru"])
+def test_eviction_policies_match_oracle_simulation(torch_cuda, policy):
+    """Every eviction policy on the C4-shaped graph at 1/2000 with 1% hubs and
+    a pool of about 35% of the rows: the output equals the in-core run bit for
+    bit, and the evictions, reloads and per-vertex reload histogram equal the
+    oracle's slot-level simulation of the same pool (integers, exactly)."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    w = dataclasses.replace(WL.SAGE_OOC_RMAT_269M, random_ids=True).scaled(n=1 << 17, e=1 << 21, chunk=1024)
+    src, dst = WL.graph(w)
+    _note(f"eviction {policy}: {w.name}")
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    X = torch.from_numpy(WL.input_features(w)).cuda()
+    spec = H.layer_specs(w)[0]
+    ref = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+    L = T.Layer(w.n, row_off, col_dst, out=ref, chunk=w.chunk, **spec)
+    L.push_all(X)
+    st0 = L.finalize()
+    L.destroy()
+    budget = H.pool_budget(st0, w.n, spec["d_out"], spec["d_in"], w.chunk, int(0.35 * w.n))
+    out = torch.empty_like(ref)
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, hbm_budget=budget, hub_fraction=0.01,
+                eviction=policy, **spec)
+    L.push_all(X)
+    st = L.finalize()
+    hist = L.reload_histogram(64)
+    L.destroy()
+    assert torch.equal(out, ref)
+    _note(f"  pool {st['pool_rows']} rows ({st['hub_rows']} hubs): {st['evictions']} evictions, "
+          f"{st['reloads']} reloads")
+    g = O.Graph(w.n, src, dst)
+    ev, rl, per = O.residency_sim(g, w.chunk, st["pool_rows"], st["hub_rows"], policy, seed=w.seed)
+    assert (st["evictions"], st["reloads"]) == (ev, rl) and ev > 0
+    assert np.array_equal(hist, np.bincount(np.minimum(per, 63), minlength=64))
+
+
 def test_host_chunks_and_host_outputs(torch_cuda):
     """Chunks in pinned host memory (staged on the layer's copy stream) and
     outputs written straight into pinned host memory give the device run's
@@ -147,6 +184,11 @@ def test_budget_errors(torch_cuda):
         with pytest.raises(T.TaurusError) as ex:
             T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **dict(spec, **bad))
         assert ex.value.status == -6, bad
-    with pytest.raises(T.TaurusError) as ex:
-        T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **dict(spec, hub_fraction=1.5))
-    assert ex.value.status == -1
+    for bad in (dict(hub_fraction=1.5), dict(eviction=7), dict(eviction=-1)):
+        with pytest.raises(T.TaurusError) as ex:
+            T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **dict(spec, **bad))
+        assert ex.value.status == -1, bad
+    # an in-core layer reports no reloads
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **spec)
+    assert L.reload_histogram(4).tolist() == [w.n, 0, 0, 0]
+    L.destroy()
