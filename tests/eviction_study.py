@@ -1,0 +1,163 @@
+"""Eviction policies under shrinking pools (the eviction and hot-store studies
+of Sec. 4) on the C4 recipe, on one GPU.
+
+    python tests/eviction_study.py                 # measure at 1/64, check at 1/512
+    python tests/eviction_study.py --scale 32 --check-scale 256
+
+For each vertex order (the generator's IDs, and Alg. 1 from the RCMK order),
+each pool size (a fraction of the rows, 1% of them hubs) and each policy
+(fewest pending, random, FIFO, LRU) the first layer (SAGE-mean 512 -> 256,
+fp32, features in HBM) runs under the budget that leaves that pool.  Every
+output must equal the in-core run bit for bit.  At the check scale the
+evictions, reloads and reloads per vertex must also equal the oracle's
+slot-level simulation of the same pool exactly.  Reports evictions, reloads,
+host-link bytes, wall time and the spread of reloads per vertex.
+
+Not collected by pytest; every run prints a line, and a JSON summary goes to
+gpurun_out/eviction_study.json.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+T0 = time.time()
+POLICIES = ("pending", "random", "fifo", "lru")
+FRACTIONS = (0.5, 0.35, 0.25, 0.15)
+
+
+def say(msg: str) -> None:
+    print(f"[{time.time() - T0:7.1f}s] {msg}", flush=True)
+
+
+def reload_spread(hist: np.ndarray) -> dict:
+    """Among vertices reloaded at least once: count, median and 90th
+    percentile of their reload counts, and the largest (the last bin holds
+    63 or more)."""
+    h = hist[1:].astype(np.int64)
+    tot = int(h.sum())
+    if tot == 0:
+        return {"reloaded": 0, "p50": 0, "p90": 0, "max": 0}
+    c = np.cumsum(h)
+    return {"reloaded": tot, "p50": int(np.searchsorted(c, 0.5 * tot) + 1),
+            "p90": int(np.searchsorted(c, 0.9 * tot) + 1), "max": int(np.flatnonzero(h)[-1] + 1)}
+
+
+def study(w, check: bool) -> list:
+    import torch
+    import oracle as O
+    import paper_2607_17374_amd as T
+    from fixtures import workloads as WL
+    from tests import harness as H
+    src, dst = WL.graph(w)
+    say(f"{w.name}: n={w.n} e={src.size} chunk={w.chunk}")
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    X = torch.from_numpy(WL.input_features(w)).cuda()
+    spec = H.layer_specs(w)[0]
+    rcm = T.reorder_rcm(w.n, row_off, col_dst)
+    ta, spans, done = T.reorder_ta(w.n, row_off, col_dst, rcm, 5)
+    say(f"Alg. 1 from RCMK: spans {spans[:done + 1].tolist()}")
+    out_rows = []
+    for order_name, perm in (("generator IDs", None), ("Alg. 1 order", ta)):
+        if perm is None:
+            ro, cd, Xo = row_off, col_dst, X
+            s_h, d_h = src, dst
+        else:
+            ro, cd = T.relabel_graph(w.n, row_off, col_dst, perm)
+            Xo = T.permute_rows(X, perm)
+            p = perm.cpu().numpy()
+            s_h, d_h = p[src], p[dst]
+        g = O.Graph(w.n, s_h.astype(np.int32), d_h.astype(np.int32)) if check else None
+        ref = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+        L = T.Layer(w.n, ro, cd, out=ref, chunk=w.chunk, **spec)
+        torch.cuda.synchronize()
+        t0 = time.time()
+        L.push_all(Xo)
+        st0 = L.finalize()
+        t_ref = time.time() - t0
+        L.destroy()
+        say(f"{order_name}: in core {t_ref:.2f} s, P = {st0['pairs']}")
+        for frac in FRACTIONS:
+            budget = H.pool_budget(st0, w.n, spec["d_out"], spec["d_in"], w.chunk, int(frac * w.n))
+            for policy in POLICIES:
+                row = {"order": order_name, "pool_fraction": frac, "policy": policy}
+                out = torch.empty_like(ref)
+                try:
+                    L = T.Layer(w.n, ro, cd, out=out, chunk=w.chunk, hbm_budget=budget, hub_fraction=0.01,
+                                eviction=policy, **spec)
+                except T.TaurusError as ex:
+                    if ex.status != -6:
+                        raise
+                    row["refused"] = True
+                    out_rows.append(row)
+                    say(f"  {order_name}, pool {frac:.2f}, {policy}: refused ({ex})")
+                    break
+                torch.cuda.synchronize()
+                t0 = time.time()
+                try:
+                    L.push_all(Xo)
+                    st = L.finalize()
+                except T.TaurusError as ex:
+                    if ex.status != -6:
+                        raise
+                    L.destroy()
+                    row["refused"] = True
+                    out_rows.append(row)
+                    say(f"  {order_name}, pool {frac:.2f}, {policy}: ran out of victims ({ex})")
+                    continue
+                t = time.time() - t0
+                hist = L.reload_histogram(64)
+                L.destroy()
+                row.update(pool_rows=st["pool_rows"], hub_rows=st["hub_rows"], evictions=st["evictions"],
+                           reloads=st["reloads"], d2h_bytes=st["d2h_bytes"], h2d_bytes=st["h2d_bytes"],
+                           seconds=round(t, 3), in_core_seconds=round(t_ref, 3),
+                           equal_to_in_core=bool(torch.equal(out, ref)), **reload_spread(hist))
+                if check:
+                    ev, rl, per = O.residency_sim(g, w.chunk, st["pool_rows"], st["hub_rows"], policy, seed=w.seed)
+                    row["oracle_equal"] = bool((ev, rl) == (st["evictions"], st["reloads"]) and np.array_equal(
+                        hist, np.bincount(np.minimum(per, 63), minlength=64)))
+                out_rows.append(row)
+                say(f"  {order_name}, pool {frac:.2f} ({row['pool_rows']} rows), {policy}: {row['evictions']} "
+                    f"evictions, {row['reloads']} reloads (reloaded vertices {row['reloaded']}, median "
+                    f"{row['p50']}, p90 {row['p90']}, max {row['max']}), {t:.2f} s vs {t_ref:.2f} s in core, "
+                    f"equal {row['equal_to_in_core']}" + (f", oracle {row['oracle_equal']}" if check else ""))
+                del out
+        if perm is not None:
+            del ro, cd, Xo
+        torch.cuda.empty_cache()
+    return out_rows
+
+
+def main():
+    from fixtures import workloads as WL
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--scale", type=int, default=64)
+    ap.add_argument("--check-scale", type=int, default=512)
+    args = ap.parse_args()
+    base = WL.SAGE_OOC_RMAT_269M
+    res = {}
+    for scale, check in ((args.check_scale, True), (args.scale, False)):
+        w = base.scaled(base.n // scale, base.e // scale, chunk=max(1024, base.chunk // scale),
+                        name=f"{base.name}-div{scale}")
+        res[w.name] = {"check": check, "runs": study(w, check)}
+    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+    path = os.path.join(ROOT, "gpurun_out", "eviction_study.json")
+    with open(path, "w") as f:
+        json.dump(res, f, indent=1)
+    bad = [r for v in res.values() for r in v["runs"]
+           if not r.get("refused") and (not r["equal_to_in_core"] or r.get("oracle_equal") is False)]
+    say(f"summary in {path}; {len(bad)} runs differ")
+    sys.exit(1 if bad else 0)
+
+
+if __name__ == "__main__":
+    main()
