@@ -15,7 +15,7 @@ import numpy as np
 from . import F32, BF16, F16, UNIFORM, NORMAL
 from . import rmat_edges, features, weights, bias, round16
 
-SAGE_MEAN, GCN_SYM = 0, 1
+SAGE_MEAN, GCN_SYM, GIN_SUM = 0, 1, 2
 
 
 @dataclass(frozen=True)

@@ -22,7 +22,7 @@ _SO = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "oracle.c")
 
 F32, BF16, F16 = 0, 1, 2
-SAGE_MEAN, GCN_SYM = 0, 1
+SAGE_MEAN, GCN_SYM, GIN_SUM = 0, 1, 2
 
 
 def build(force: bool = True) -> str:
@@ -224,7 +224,11 @@ def layer(agg: int, g: Graph, H: np.ndarray, h_dtype: int, W: np.ndarray, b: np.
     count = g.n if ids is None else ids.size
     out = np.empty((count, d_out), np.float64)
     kin = None if keep_in is None else np.ascontiguousarray(keep_in, np.uint8)
-    rc = lib().or_layer(agg, g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(g.deg_out),
+    deg_out = g.deg_out
+    if kin is not None:
+        # a sampled layer propagates over the kept edges: their out-degrees
+        deg_out = np.bincount(g.in_src[kin != 0], minlength=g.n).astype(np.int32)
+    rc = lib().or_layer(agg, g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(deg_out),
                         _p(H), h_dtype, d_in, _p(W), _p(bb), d_out, int(relu),
                         count, _p(ids), _p(out))
     if rc:

@@ -370,7 +370,14 @@ void or_widen(int64_t count, const void* in, int dtype, double* out) {
  *     directed graph: d^_out(u) = d_out(u) + 1, d^_in(v) = d_in(v) + 1,
  *     a    = sum_{u in N-(v)} h_u / sqrt(d^_out(u) d^_in(v))
  *            + h_v / sqrt(d^_out(v) d^_in(v)),
- *     z    = W a + b,  cols = d_in.  deg_out is the full out-degree.
+ *     z    = W a + b,  cols = d_in.  deg_out is the out-degree of the graph
+ *     the layer propagates over: the full one for exact inference; for a
+ *     sampled layer (keep_in) the kept out-degree, and d_in(v) = |M(v)|, so
+ *     the normalisation is that of the sampled graph with its self loops.
+ * agg 2, GIN (GINConv with a linear apply function and eps = 0, sum
+ *     aggregation):
+ *     a    = h_v + sum_{u in M(v)} h_u,
+ *     z    = W a + b,  cols = d_in.
  * Output: out[i][j] = ReLU(z_j) if relu else z_j, for v = dst_ids[i].
  */
 int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
@@ -381,7 +388,6 @@ int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
     int64_t cols = agg == 0 ? 2 * d_in : d_in;
     int64_t count = dst_ids ? n_dst : n;
     int bad = 0;
-    if (agg == 1 && keep_in) return -1;   /* GCN is defined here for exact inference only */
 #pragma omp parallel
     {
         double* a = (double*)malloc((size_t)cols * sizeof(double));
@@ -402,15 +408,26 @@ int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
                 if (m > 0)
                     for (int64_t j = 0; j < d_in; j++) a[j] = a[j] / (double)m;
                 for (int64_t j = 0; j < d_in; j++) a[d_in + j] = or_load(H, h_dtype, v * d_in + j);
-            } else {
-                double din_hat = (double)(in_off[v + 1] - in_off[v]) + 1.0;
+            } else if (agg == 1) {
+                int64_t m = 0;
+                for (int64_t k = in_off[v]; k < in_off[v + 1]; k++)
+                    if (!keep_in || keep_in[k]) m++;
+                double din_hat = (double)m + 1.0;
                 for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                    if (keep_in && !keep_in[k]) continue;
                     int64_t u = in_src[k];
                     double c = 1.0 / sqrt(((double)deg_out[u] + 1.0) * din_hat);
                     for (int64_t j = 0; j < d_in; j++) a[j] += c * or_load(H, h_dtype, u * d_in + j);
                 }
                 double cs = 1.0 / sqrt(((double)deg_out[v] + 1.0) * din_hat);
                 for (int64_t j = 0; j < d_in; j++) a[j] += cs * or_load(H, h_dtype, v * d_in + j);
+            } else {
+                for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                    if (keep_in && !keep_in[k]) continue;
+                    int64_t u = in_src[k];
+                    for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, u * d_in + j);
+                }
+                for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, v * d_in + j);
             }
             for (int64_t o = 0; o < d_out; o++) {
                 double z = bias ? bias[o] : 0.0;

@@ -27,7 +27,7 @@ MUTANTS = {
         [lambda: P.test_gcn_matches_dense(0, True), P.test_closed_form_gcn_degrees_only]),
     # GCN: in- and out-degree swapped in the source factor
     "gcn_degrees_swapped": (
-        "double din_hat = (double)(in_off[v + 1] - in_off[v]) + 1.0;",
+        "double din_hat = (double)m + 1.0;",
         "double din_hat = (double)deg_out[v] + 1.0;",
         [lambda: P.test_gcn_matches_dense(1, False)]),
     # SAGE: mean over all in-neighbours instead of the propagated ones
@@ -135,6 +135,16 @@ MUTANTS = {
         "key = pend[v];",
         "key = 16383 - (pend[v] < 16383 ? pend[v] : 16383);",
         [lambda: P.test_residency_hand_cases("case1"), P.test_fewest_pending_reloads_least]),
+    # sampled GCN normalised by the full in-degree
+    "gcn_sampled_full_in_degree": (
+        "double din_hat = (double)m + 1.0;",
+        "double din_hat = (double)(in_off[v + 1] - in_off[v]) + 1.0;",
+        [P.test_sampled_gcn_matches_dense_on_kept_edges]),
+    # GIN without its self term
+    "gin_no_self_term": (
+        "for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, v * d_in + j);\n            }",
+        "(void)0;\n            }",
+        [lambda: P.test_gin_matches_dense(False)]),
     # fp16 rounding truncates
     "f16_truncates": (
         "double r = nearbyint(q);\n    if (r >= 2048.0)",

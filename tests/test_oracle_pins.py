@@ -199,6 +199,56 @@ def test_sampled_sage_matches_dense_on_kept_edges():
     np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
 
 
+def test_sampled_gcn_matches_dense_on_kept_edges():
+    """A sampled GCN layer is the GCN of the sampled graph: the kept edges
+    plus one self loop per vertex, normalised by that graph's degrees."""
+    rng = np.random.default_rng(17)
+    n, d_in, d_out = 100, 8, 5
+    A, u, v = random_digraph(rng, n, 0.12, isolated=3)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in))
+    b = rng.standard_normal(d_out)
+    for k in (1, 4):
+        words, keep_in, _ = O.sample(g, 23, 2, k)
+        bits = O.mask_bits(words, g.e)
+        A_keep = np.zeros_like(A)
+        src_csr = np.repeat(np.arange(n), np.diff(g.row_off))
+        A_keep[src_csr[bits], g.col_dst[bits]] = True
+        got = O.layer(O.GCN_SYM, g, H32, O.F32, W, b, True, keep_in=keep_in)
+        ref = dense_gcn(A_keep, H32.astype(np.float64), W, b, True)
+        np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def dense_gin(A, H, W, b, relu):
+    """GIN with eps = 0 and a linear apply function: (A + I)^T H W^T + b."""
+    z = (A.astype(np.float64) + np.eye(A.shape[0])).T @ H @ W.T + b
+    return np.maximum(z, 0) if relu else z
+
+
+@pytest.mark.parametrize("sampled", [False, True])
+def test_gin_matches_dense(sampled):
+    rng = np.random.default_rng(27)
+    n, d_in, d_out = 90, 7, 6
+    A, u, v = random_digraph(rng, n, 0.08, isolated=4)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in))
+    b = rng.standard_normal(d_out)
+    keep_in, A_used = None, A
+    if sampled:
+        words, keep_in, _ = O.sample(g, 5, 1, 3)
+        bits = O.mask_bits(words, g.e)
+        A_used = np.zeros_like(A)
+        A_used[np.repeat(np.arange(n), np.diff(g.row_off))[bits], g.col_dst[bits]] = True
+    got = O.layer(O.GIN_SUM, g, H32, O.F32, W, b, False, keep_in=keep_in)
+    np.testing.assert_allclose(got, dense_gin(A_used, H32.astype(np.float64), W, b, False), rtol=1e-12, atol=1e-12)
+    # closed form: constant features c and identity weights give c (d_in(v) + 1)
+    ones = np.full((n, d_in), 0.5, np.float32)
+    z = O.layer(O.GIN_SUM, g, ones, O.F32, np.eye(d_in), None, False)
+    np.testing.assert_allclose(z, 0.5 * (np.diff(g.in_off)[:, None] + 1) * np.ones((1, d_in)), rtol=0, atol=0)
+
+
 def test_subset_of_destinations_equals_rows_of_full():
     rng = np.random.default_rng(8)
     n = 70
