@@ -34,6 +34,16 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
+# Model variants on the same graph and features: (family, fanouts per layer,
+# description).  Sampled layers keep min(d_in(v), k) in-edges per destination.
+VARIANTS = {
+    "gcn": (1, (), "2-layer GCN 128->128->64 (symmetric norm, self loops), exact"),
+    "gcn-sampled": (1, (10, 5), "2-layer GCN 128->128->64, fanouts (10, 5), norms of the sampled graph"),
+    "gin": (2, (), "2-layer GIN 128->128->64 (linear apply, eps = 0), exact"),
+    "gin-sampled": (2, (10, 5), "2-layer GIN 128->128->64, fanouts (10, 5)"),
+}
+
+
 # A segment's slots are its messages plus, for the segment from the
 # destination's own chunk, the self message.  Segments of at most SHORT_LEN
 # slots are short units; longer ones are cut into pieces of at most PIECE_LEN
@@ -228,6 +238,8 @@ def main():
                     help="events around every kernel (adds the transform's MFMA roofline; more events in the stream)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy, the reference kernel for HBM byte counters")
+    ap.add_argument("--variant", choices=sorted(VARIANTS), default="gcn",
+                    help="model family on the same graph (default: the exact GCN workload)")
     ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="print the profile summary of a kernel-trace run and FETCH_SIZE / WRITE_SIZE runs")
     args = ap.parse_args()
@@ -248,7 +260,10 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    w = WL.GCN_RMAT_1M
+    import dataclasses
+    agg, fanouts, desc = VARIANTS[args.variant]
+    w = dataclasses.replace(WL.GCN_RMAT_1M, agg=agg, fanouts=fanouts)
+    sampled = bool(fanouts)
     src, dst = WL.graph(w)
     X = torch.from_numpy(WL.input_features(w)).to(dev)
     src_d = torch.from_numpy(src).to(dev)
@@ -307,23 +322,26 @@ def main():
     for li in range(nl):
         sts = [r[2][li] for r in runs]
         d_o, d_in = specs[li]["d_out"], specs[li]["d_in"]
-        ncols = d_o  # GCN transform width
+        ncols = d_o  # GCN and GIN transform width
         wall = float(np.mean([s["wall_ms"] for s in sts]))
         st = sts[-1]
         kb = kernel_bytes(fm, w.n, d_o, 4, sage=False)
         checks = (st["short_units"] == fm["short_units"], st["wave_units"] == fm["units"] - fm["short_units"],
                   st["split_segments"] == fm["split_segments"], st["pairs"] == fm["segments"] + fm["alone"],
                   st["messages"] == fm["messages"])
+        if sampled:
+            checks = ()      # the flush model describes exact layers only
         if not all(checks):
             model_ok = False
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
         ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
               for k in ("gemm", "scatter", "fixup", "init", "index")}
-        if profile:
+        if profile and not sampled:
             for k in tot:
                 tot[k][0] += kb[k] * len(sts)
                 tot[k][1] += sum(s[f"ms_{k}"] for s in sts)
                 tot[k][2] += sum(s[f"launches_{k}"] for s in sts)
+        if profile:
             gemm_flops += 2.0 * w.n * d_in * ncols * len(sts)
             gemm_ms += sum(s["ms_gemm"] for s in sts)
         layers.append({
@@ -333,8 +351,9 @@ def main():
             **{f"{k}_ms": round(v, 3) for k, v in ms.items()},
             "short_units": st["short_units"], "wave_units": st["wave_units"],
             "split_segments": st["split_segments"],
-            **{f"{k}_algorithmic_gb": round(kb[k] / 1e9, 4) for k in kb},
-            **{f"{k}_gbs": (round(kb[k] / (ms[k] * 1e-3) / 1e9, 1) if ms[k] > 0 else None) for k in kb},
+            **({} if sampled else {f"{k}_algorithmic_gb": round(kb[k] / 1e9, 4) for k in kb}),
+            **({} if sampled else {f"{k}_gbs": (round(kb[k] / (ms[k] * 1e-3) / 1e9, 1) if ms[k] > 0 else None)
+                                   for k in kb}),
         })
     csr_ms = float(np.mean([r[0] for r in runs]))
     plan_ms = float(np.mean([r[1] for r in runs]))
@@ -364,15 +383,18 @@ def main():
         cpu = {"value": round(total_edges / t_or / 1e9, 5), "unit": "GTEPS", "cores": O.threads(),
                "kind": "oracle", "seconds": round(t_or, 2),
                "sample": "the full workload once: oracle CSR and in-lists, then both layers for all "
-                         "1,000,000 destinations in fp64 (value = both layers' 40M propagated edges / wall time)"}
+                         f"1,000,000 destinations in fp64 (value = both layers' {total_edges / 1e6:.1f}M "
+                         "propagated edges / wall time)"}
 
     line = {
         "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "gcn2-rmat-1m: 2-layer GCN 128->128->64 (symmetric norm, self loops), exact; "
+        "config": {"workload": f"{'gcn2-rmat-1m' if args.variant == 'gcn' else 'rmat-1m-' + args.variant}: "
+                               f"{desc}; "
                                "RMAT(0.57,0.19,0.19) 1,000,000 vertices / 20,000,000 edges; N(0,1) fp32 features; "
-                               "65,536-vertex source chunks; step = CSR build + chunk index + both layers",
+                               "65,536-vertex source chunks; step = CSR build + chunk index"
+                               f"{' (sampled: per-layer in-edge lists and masks)' if sampled else ''} + both layers",
                    "n": w.n, "e": w.e, "chunk": w.chunk, "csr_ms": round(csr_ms, 3),
                    "plan_ms": round(plan_ms, 3)},
         "per_layer": layers,

@@ -59,8 +59,10 @@ typedef struct taurus_plan taurus_plan;
 /* Aggregation/update families (Sec. 3.9 and the models of Sec. 4.1). */
 typedef enum {
     TAURUS_SAGE_MEAN = 0, /* z_v = W_agg mean_{u in M(v)} h_u + W_self h_v + b (mean = 0 if M(v) empty)  */
-    TAURUS_GCN_SYM = 1    /* z_v = W sum_{u in N-(v) + {v}} h_u / sqrt(d^_out(u) d^_in(v)) + b,
-                             d^ = degree + 1 (one self loop per vertex); exact inference only         */
+    TAURUS_GCN_SYM = 1,   /* z_v = W sum_{u in M(v) + {v}} h_u / sqrt(d^_out(u) d^_in(v)) + b,
+                             d^ = degree + 1 (one self loop per vertex); a sampled layer uses the
+                             degrees of its sampled graph: kept out-edges, d^_in(v) = |M(v)| + 1 */
+    TAURUS_GIN_SUM = 2    /* GINConv, linear apply, eps = 0: z_v = W (h_v + sum_{u in M(v)} h_u) + b */
 } taurus_agg;
 
 /*

@@ -79,6 +79,26 @@ __global__ void k_out_norm(const int64_t* __restrict__ row_off, int64_t n, float
     if (u < n) n_out[u] = 1.0f / sqrtf((float)(row_off[u + 1] - row_off[u] + 1));
 }
 
+// the same for a sampled layer: the out-degree counts u's kept edges (set
+// bits of the layer's mask over its CSR row)
+__global__ void k_out_norm_kept(const int64_t* __restrict__ row_off, const uint64_t* __restrict__ mask, int64_t n,
+                                float* __restrict__ n_out) {
+    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (u >= n) return;
+    const int64_t b = row_off[u + 1];
+    int64_t kept = 0;
+    for (int64_t i = row_off[u]; i < b;) {
+        const int64_t w = i >> 6;
+        const int64_t end = min(b, (w + 1) << 6);
+        const int lo = (int)(i & 63), len = (int)(end - i);
+        uint64_t bits = mask[w] >> lo;
+        if (len < 64) bits &= (1ull << len) - 1;
+        kept += __popcll(bits);
+        i = end;
+    }
+    n_out[u] = 1.0f / sqrtf((float)(kept + 1));
+}
+
 // Caller-supplied CSR: row_off[0] = 0, row_off[n] = e, non-decreasing, and
 // every col_dst in [0, n).  Checked before any kernel indexes with them.
 __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int32_t* __restrict__ col_dst,
@@ -95,11 +115,15 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 // Chunk-index items.  CSR edge i (source u = the row containing i) becomes
 // key (chunk(u) << vbits | v), value u - chunk(u)*C; a dropped edge gets
 // chunk = nchunks so it sorts after every kept item.
+// Every CSR edge is checked; a propagated one (all of them when mask is
+// null) writes its item at its position among the propagated edges
+// (word_off[w] = propagated edges before mask word w).
 __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
                                                     const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
-                                                    int64_t C, int64_t nchunks, int vbits,
-                                                    const uint64_t* __restrict__ mask, uint64_t* __restrict__ keys,
-                                                    uint32_t* __restrict__ vals, int* __restrict__ bad) {
+                                                    int64_t C, int vbits, const uint64_t* __restrict__ mask,
+                                                    const uint64_t* __restrict__ word_off,
+                                                    uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                    int* __restrict__ bad) {
     __shared__ int64_t ro[4][64];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
@@ -107,11 +131,26 @@ __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ 
     const int64_t v = col_dst[i];
     // rows strictly ascending, no self loops (a simple graph)
     if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
-    const bool kept = !mask || ((mask[i >> 6] >> (i & 63)) & 1ull);
+    int64_t pos = i;
+    if (mask) {
+        const uint64_t word = mask[i >> 6];
+        if (!((word >> (i & 63)) & 1ull)) return;
+        pos = (int64_t)word_off[i >> 6] + __popcll(word & ((1ull << (i & 63)) - 1ull));
+    }
     const uint32_t cu = (uint32_t)u / (uint32_t)C;  // u < 2^31 and C < 2^31: 32-bit division
-    const int64_t ch = kept ? (int64_t)cu : nchunks;
-    keys[i] = ((uint64_t)ch << vbits) | (uint64_t)v;
-    vals[i] = (uint32_t)u - cu * (uint32_t)C;
+    keys[pos] = ((uint64_t)cu << vbits) | (uint64_t)v;
+    vals[pos] = (uint32_t)u - cu * (uint32_t)C;
+}
+
+// propagated edges per mask word (bits at or past e are not edges)
+__global__ void k_mask_word_counts(const uint64_t* __restrict__ mask, int64_t words, int64_t e,
+                                   uint32_t* __restrict__ cnt) {
+    const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= words) return;
+    uint64_t m = mask[w];
+    const int64_t left = e - w * 64;
+    if (left < 64) m &= (1ull << left) - 1ull;
+    cnt[w] = (uint32_t)__popcll(m);
 }
 
 // offs[j] = first sorted position whose chunk field is >= j, j in [0, nchunks]
@@ -348,7 +387,7 @@ struct ScatterParams {
     float* acc;            // fp32 accumulator rows, d_o floats each
     const int32_t* slot;   // accumulator row of each vertex (residency pool), or null: row v
     int d_o;
-    int agg;               // 0 GraphSAGE-mean, 1 GCN
+    int agg;               // 0 GraphSAGE-mean, 1 GCN, 2 GIN
     int relu;
     int out_dtype;         // 0 fp32, 1 bf16, 2 fp16
     const float* bias;     // [d_o]
@@ -1084,6 +1123,26 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         return idx;
     }
 
+    // A sampled layer indexes its propagated edges only: their positions
+    // among the CSR edges come from a scan of the mask's per-word counts.
+    int64_t items = e;
+    uint64_t* word_off = nullptr;
+    if (mask) {
+        const int64_t words = ceil_div(e, 64);
+        uint32_t* wcnt = tmp.alloc<uint32_t>(words, "propagated edges per mask word");
+        word_off = tmp.alloc<uint64_t>(words + 1, "propagated edges before each mask word");
+        k_mask_word_counts<<<(unsigned)ceil_div(words, T), T, 0, s>>>(mask, words, e, wcnt);
+        TAURUS_CHECK_LAUNCH();
+        scan_u32_to_u64(wcnt, word_off, words, true, tmp, s);
+        uint64_t total = 0;
+        Readback rb;
+        rb.add(&total, word_off + words, 1);
+        rb.run(s);
+        items = (int64_t)total;
+        tmp.free_ptr(wcnt);
+    }
+    const int64_t items1 = std::max<int64_t>(items, 1);
+
     // Items sorted by (source chunk, destination), stably.  Everything up to
     // the readback below is memory safe on an invalid graph (indices come
     // from binary searches and thread ids only); the flags are checked before
@@ -1091,31 +1150,33 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     const int vbits = std::max(1, bits_for(n - 1));
     const int cbits = bits_for(nch);
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
-    SortBuffers sb{{tmp.alloc<uint64_t>(e, "index keys"), tmp.alloc<uint64_t>(e, "index keys (ping-pong)")},
-                   {tmp.alloc<uint32_t>(e, "index values"), tmp.alloc<uint32_t>(e, "index values (ping-pong)")},
+    SortBuffers sb{{tmp.alloc<uint64_t>(items1, "index keys"), tmp.alloc<uint64_t>(items1, "index keys (ping-pong)")},
+                   {tmp.alloc<uint32_t>(items1, "index values"),
+                    tmp.alloc<uint32_t>(items1, "index values (ping-pong)")},
                    0};
-    k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, nch, vbits, mask,
+    k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits, mask, word_off,
                                                         sb.keys[0], sb.vals[0], bad);
     TAURUS_CHECK_LAUNCH();
-    radix_sort_u64(sb, e, vbits + cbits, tmp, s, bad, 8);
+    if (word_off) tmp.free_ptr(word_off);
+    radix_sort_u64(sb, items, vbits + cbits, tmp, s, bad, 8);
     const uint64_t* keys = sb.keys[sb.cur];
     const uint32_t* vals = sb.vals[sb.cur];
     tmp.free_ptr(sb.keys[1 - sb.cur]);
     tmp.free_ptr(sb.vals[1 - sb.cur]);
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
-    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, e, nch, vbits, doffs);
+    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, items, nch, vbits, doffs);
     TAURUS_CHECK_LAUNCH();
-    int32_t* head = tmp.alloc<int32_t>(e, "segment heads");
-    int64_t* seg_id = tmp.alloc<int64_t>(e + 1, "segment ids");
-    k_seg_heads<<<(unsigned)ceil_div(e, T), T, 0, s>>>(keys, e, doffs + nch, head);
+    int32_t* head = tmp.alloc<int32_t>(items1, "segment heads");
+    int64_t* seg_id = tmp.alloc<int64_t>(items + 1, "segment ids");
+    k_seg_heads<<<(unsigned)ceil_div(items1, T), T, 0, s>>>(keys, items, doffs + nch, head);
     TAURUS_CHECK_LAUNCH();
-    scan_i32_to_i64(head, seg_id, e, true, tmp, s);
+    scan_i32_to_i64(head, seg_id, items, true, tmp, s);
     int64_t P = 0;
     {
         Readback rb;
         rb.add(&hbad, bad, 1);
         rb.add(idx->chunk_off.data(), doffs, nch + 1);
-        rb.add(&P, seg_id + e, 1);
+        rb.add(&P, seg_id + items, 1);
         rb.run(s);
     }
     if (hbad & 3) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
@@ -1350,7 +1411,8 @@ namespace taurus {
 
 static void validate_desc(const taurus_layer_desc* d) {
     if (!d) fail(TAURUS_E_INVALID, "null descriptor");
-    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM) fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
+    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM && d->agg != TAURUS_GIN_SUM)
+        fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
     if (d->d_in <= 0 || d->d_out <= 0 || d->d_in % 4 || d->d_out % 4 || d->d_out > 1024 || d->d_in > 8192)
         fail(TAURUS_E_INVALID, "d_in=%d d_out=%d: widths must be positive multiples of 4, d_out <= 1024",
              d->d_in, d->d_out);
@@ -1361,8 +1423,6 @@ static void validate_desc(const taurus_layer_desc* d) {
     if (!d->weight) fail(TAURUS_E_INVALID, "weight is null");
     if (d->chunk <= 0 || d->chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)d->chunk);
     if (d->fanout < 0 || d->fanout > 64) fail(TAURUS_E_INVALID, "fanout %d outside [0, 64]", d->fanout);
-    if (d->fanout > 0 && d->agg != TAURUS_SAGE_MEAN)
-        fail(TAURUS_E_INVALID, "fanout sampling is defined for GraphSAGE-mean layers only");
     if (d->fanout > 0 && d->layer < 1) fail(TAURUS_E_INVALID, "layer %d: sampled layers are numbered from 1", d->layer);
     if (!d->out) fail(TAURUS_E_INVALID, "out is null");
     if (d->out_on_host != 0 && d->out_on_host != 1) fail(TAURUS_E_INVALID, "out_on_host=%d", d->out_on_host);
@@ -1433,7 +1493,10 @@ static void layer_init(taurus_layer* L) {
     TAURUS_CHECK_LAUNCH();
     if (d.agg == TAURUS_GCN_SYM) {
         L->n_out = L->arena.alloc<float>(n, "source norms");
-        k_out_norm<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, n, L->n_out);
+        if (L->mask)
+            k_out_norm_kept<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, L->mask, n, L->n_out);
+        else
+            k_out_norm<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, n, L->n_out);
         TAURUS_CHECK_LAUNCH();
     }
 

@@ -6,13 +6,15 @@
 // The in-edges of each destination are read from a CSC, built once per
 // graph by a stable radix sort of the CSR edges by destination (sources stay
 // ascending within a destination).  Then, per layer:
-//   1. threshold: for every v with d_in(v) > k one wave finds tau_v, the k-th
+//   1. threshold: for every v with d_in(v) > k a wave finds tau_v, the k-th
 //      smallest rank pair of its in-edges.  The wave takes the in-edges 64
 //      at a time, sorts each batch across its lanes (bitonic network on
 //      (key, u) pairs) and merges it into a running sorted list of the 64
 //      smallest pairs so far; a batch with no pair below the running k-th
-//      smallest is skipped without sorting, so hubs cost little more than a
-//      pass over their keys;
+//      smallest is skipped without sorting.  Destinations with more than
+//      512 in-edges are cut into pieces taken by separate waves, whose
+//      k smallest pairs are merged when the last piece is done, so a hub
+//      costs no more wall time than a piece;
 //   2. mask: one pass over the CSR in edge order keeps (u, v) iff its pair is
 //      <= tau_v (tau_v = +inf when d_in(v) <= k); each wave's 64 decisions
 //      form one mask word by ballot, so no atomics are needed.
@@ -49,19 +51,30 @@ void validate_csr(const taurus_graph& g, hipStream_t s) {
     if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
 }
 
-// CSR edge i -> sort key v, value u; in-degree counts
+// CSR edge i -> sort key v, value u
 __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
-                                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                                   int32_t* __restrict__ deg) {
+                                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
     __shared__ int64_t ro[4][64];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
     if (i >= e) return;
-    const int32_t v = col_dst[i];
-    keys[i] = (uint64_t)v;
+    keys[i] = (uint64_t)col_dst[i];
     vals[i] = (uint32_t)u;
-    atomicAdd(&deg[v], 1);
+}
+
+// in_off[v] = first position of the sorted destinations that is >= v
+// (binary search; no atomics, so hubs cost nothing extra), v in [0, n]
+__global__ void k_csc_offsets(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int64_t* __restrict__ in_off) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v > n) return;
+    int64_t lo = 0, hi = e;
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if (keys[mid] < (uint64_t)v) lo = mid + 1;
+        else hi = mid;
+    }
+    in_off[v] = lo;
 }
 
 std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
@@ -74,21 +87,22 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
     int* bad = tmp.alloc<int>(1, "sort flag");
     fill_i32(bad, 1, 0, s);
     int hbad = 0;
-    int32_t* deg = tmp.alloc<int32_t>(n, "in-degrees");
-    fill_i32(deg, n, 0, s);
     c->in_off = c->arena.alloc<int64_t>(n + 1, "in-edge offsets");
     if (e > 0) {
         SortBuffers sb{{tmp.alloc<uint64_t>(e, "csc keys"), tmp.alloc<uint64_t>(e, "csc keys (ping-pong)")},
                        {c->arena.alloc<uint32_t>(e, "in-edge sources"),
                         c->arena.alloc<uint32_t>(e, "in-edge sources (ping-pong)")},
                        0};
-        k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0], deg);
+        k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0]);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
         c->in_src = reinterpret_cast<int32_t*>(sb.vals[sb.cur]);
         c->arena.free_ptr(sb.vals[1 - sb.cur]);
+        k_csc_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, c->in_off);
+        TAURUS_CHECK_LAUNCH();
+    } else {
+        fill_i32(reinterpret_cast<int32_t*>(c->in_off), 2 * (n + 1), 0, s);
     }
-    scan_i32_to_i64(deg, c->in_off, n, true, tmp, s);
     {
         Readback rb;
         rb.add(&hbad, bad, 1);
@@ -149,19 +163,61 @@ __device__ inline void merge_smallest(uint64_t& ck, uint32_t& cu, uint64_t bk, u
     for (int stride = 32; stride > 0; stride >>= 1) exchange(ck, cu, stride, (lane & stride) == 0);
 }
 
-// One wave per 64 consecutive destinations; destinations with more than k
-// in-edges are processed one after another by the whole wave.
+constexpr int SAMPLE_BATCHES = 8;
+// destinations with more in-edges than this are split into pieces of as many
+// in-edges (k_sample_pieces); the others are scanned whole (k_sample_threshold)
+constexpr int64_t SAMPLE_PIECE = 64 * SAMPLE_BATCHES;
+
+// The 64 smallest rank pairs among v's in-edges [a, b) merged into the
+// wave's running list (ck, cu), ascending by lane; pre = v's hash prefix.
+// SAMPLE_BATCHES batches of 64 in-edges are loaded at a time, so a long scan
+// keeps that many loads in flight; a batch with no pair below the running
+// k-th smallest is skipped without sorting.
+__device__ inline void scan_smallest(const int32_t* __restrict__ in_src, int64_t a, int64_t b, uint64_t pre, int k,
+                                     uint64_t& ck, uint32_t& cu) {
+    const int lane = threadIdx.x & 63;
+    for (int64_t base = a; base < b; base += 64 * SAMPLE_BATCHES) {
+        // past the end a lane holds (~0, ~0), which is never below a running
+        // pair and sorts last
+        uint32_t uu[SAMPLE_BATCHES];
+#pragma unroll
+        for (int t = 0; t < SAMPLE_BATCHES; t++) {
+            const int64_t idx = base + t * 64 + lane;
+            uu[t] = idx < b ? (uint32_t)in_src[idx] : ~0u;
+        }
+#pragma unroll
+        for (int t = 0; t < SAMPLE_BATCHES; t++) {
+            if (base + t * 64 >= b) break;  // uniform over the wave
+            const bool valid = base + t * 64 + lane < b;
+            uint32_t u = uu[t];
+            uint64_t key = valid ? sample_key(pre, u) : ~0ull;
+            const uint64_t tk = shfl64(ck, k - 1);
+            const uint32_t tu = __shfl(cu, k - 1, 64);
+            if (__ballot(valid && pair_less(key, u, tk, tu)) == 0) continue;
+            bitonic_sort64(key, u);
+            merge_smallest(ck, cu, key, u);
+        }
+    }
+}
+
+// destinations per wave of k_sample_threshold: few, so that a run of
+// mid-degree destinations (natural RMAT IDs cluster them) is spread over
+// many waves
+constexpr int SAMPLE_DPW = 8;
+
+// One wave per SAMPLE_DPW consecutive destinations; those with k < d_in <=
+// SAMPLE_PIECE are scanned one after another by the whole wave.
 __global__ __launch_bounds__(256) void k_sample_threshold(const int64_t* __restrict__ in_off,
                                                           const int32_t* __restrict__ in_src, int64_t n,
                                                           uint64_t seed, int layer, int k,
                                                           uint64_t* __restrict__ thr_key,
                                                           uint32_t* __restrict__ thr_u) {
     const int lane = threadIdx.x & 63;
-    const int64_t v0 = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6) << 6;
+    const int64_t v0 = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6) * SAMPLE_DPW;
     if (v0 >= n) return;  // uniform over the wave
     const int64_t myv = v0 + lane;
     int64_t b = 0, d = 0;
-    if (myv < n) {
+    if (lane < SAMPLE_DPW && myv < n) {
         b = in_off[myv];
         d = in_off[myv + 1] - b;
         if (d <= k) {  // every in-edge is kept
@@ -169,24 +225,90 @@ __global__ __launch_bounds__(256) void k_sample_threshold(const int64_t* __restr
             thr_u[myv] = ~0u;
         }
     }
-    uint64_t todo = __ballot(myv < n && d > k);
+    uint64_t todo = __ballot(lane < SAMPLE_DPW && myv < n && d > k && d <= SAMPLE_PIECE);
     while (todo) {
         const int j = __ffsll((unsigned long long)todo) - 1;
         todo &= todo - 1;
         const int64_t v = v0 + j;
         const int64_t vb = (int64_t)shfl64((uint64_t)b, j), vd = (int64_t)shfl64((uint64_t)d, j);
+        uint64_t ck = ~0ull;
+        uint32_t cu = ~0u;
+        scan_smallest(in_src, vb, vb + vd, sample_prefix(seed, (uint64_t)layer, (uint64_t)v), k, ck, cu);
+        if (lane == k - 1) {
+            thr_key[v] = ck;
+            thr_u[v] = cu;
+        }
+    }
+}
+
+// The destination whose in-edges hold CSC position pos (0 <= pos < e): the
+// largest v with in_off[v] <= pos, found by the whole wave (every lane with
+// the same pos) with a 64-ary search: each round the lanes probe 64 evenly
+// spaced offsets, and since in_off is non-decreasing the probes that pass
+// form a prefix of the lanes.
+__device__ inline int64_t covering(const int64_t* __restrict__ in_off, int64_t n, int64_t pos) {
+    const int lane = threadIdx.x & 63;
+    int64_t lo = 0, hi = n - 1;  // the answer lies in [lo, hi]
+    while (hi - lo >= 64) {
+        const int64_t step = (hi - lo + 63) / 64;
+        const int64_t q = min(lo + (int64_t)(lane + 1) * step, hi);
+        const int c = __popcll(__ballot(in_off[q] <= pos));
+        const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
+        lo = min(lo + (int64_t)c * step, hi);
+        hi = nhi;
+    }
+    const bool ok = lo + lane <= hi && in_off[lo + lane] <= pos;
+    return lo + __popcll(__ballot(ok)) - 1;
+}
+
+// Destinations with more than SAMPLE_PIECE in-edges.  One wave per piece of
+// SAMPLE_PIECE consecutive CSC positions.  A piece meets at most two such
+// destinations: the one holding its first position (slot 0) and one starting
+// inside it, which then holds its last position (slot 1).  For each, the
+// wave writes the k smallest pairs of its part of the piece to
+// piece_key/piece_u[(p * 2 + slot) * k + i]; the last piece of a destination
+// to finish (a counter per destination, behind a device-scope fence) merges
+// the destination's pieces in order and writes its threshold.
+__global__ __launch_bounds__(256) void k_sample_pieces(const int64_t* __restrict__ in_off,
+                                                       const int32_t* __restrict__ in_src, int64_t n, int64_t e,
+                                                       uint64_t seed, int layer, int k,
+                                                       uint64_t* __restrict__ piece_key,
+                                                       uint32_t* __restrict__ piece_u, int32_t* __restrict__ done,
+                                                       uint64_t* __restrict__ thr_key,
+                                                       uint32_t* __restrict__ thr_u) {
+    const int lane = threadIdx.x & 63;
+    const int64_t p = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    if (p >= (e + SAMPLE_PIECE - 1) / SAMPLE_PIECE) return;  // uniform over the wave
+    const int64_t start = p * SAMPLE_PIECE, end = min(e, start + SAMPLE_PIECE);
+    const int64_t va = covering(in_off, n, start), vz = covering(in_off, n, end - 1);
+    for (int slot = 0; slot < 2; slot++) {
+        if (slot == 1 && vz == va) break;
+        const int64_t v = slot == 0 ? va : vz;
+        const int64_t vb = in_off[v], ve = in_off[v + 1];
+        if (ve - vb <= SAMPLE_PIECE) continue;
         const uint64_t pre = sample_prefix(seed, (uint64_t)layer, (uint64_t)v);
         uint64_t ck = ~0ull;
         uint32_t cu = ~0u;
-        for (int64_t base = 0; base < vd; base += 64) {
-            const bool valid = base + lane < vd;
-            uint32_t u = valid ? (uint32_t)in_src[vb + base + lane] : ~0u;
-            uint64_t key = valid ? sample_key(pre, u) : ~0ull;
-            const uint64_t tk = shfl64(ck, k - 1);
-            const uint32_t tu = __shfl(cu, k - 1, 64);
-            if (__ballot(valid && pair_less(key, u, tk, tu)) == 0) continue;
-            bitonic_sort64(key, u);
-            merge_smallest(ck, cu, key, u);
+        scan_smallest(in_src, max(vb, start), min(ve, end), pre, k, ck, cu);
+        const int64_t r = (p * 2 + slot) * k;
+        if (lane < k) {
+            piece_key[r + lane] = ck;
+            piece_u[r + lane] = cu;
+        }
+        __threadfence();
+        const int64_t p0 = vb / SAMPLE_PIECE, p1 = (ve - 1) / SAMPLE_PIECE;
+        int last = 0;
+        if (lane == 0) last = atomicAdd(&done[v], 1) == (int)(p1 - p0) ? 1 : 0;
+        if (__shfl(last, 0, 64) == 0) continue;
+        __threadfence();
+        ck = ~0ull;
+        cu = ~0u;
+        for (int64_t q = p0; q <= p1; q++) {
+            // v holds the first position of every piece but possibly p0
+            const int64_t rq = (q * 2 + ((q == p0 && vb != q * SAMPLE_PIECE) ? 1 : 0)) * k;
+            const uint64_t bk = lane < k ? piece_key[rq + lane] : ~0ull;
+            const uint32_t bu = lane < k ? piece_u[rq + lane] : ~0u;
+            merge_smallest(ck, cu, bk, bu);
         }
         if (lane == k - 1) {
             thr_key[v] = ck;
@@ -225,7 +347,15 @@ void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer
     Arena tmp(s);
     uint64_t* thr_key = tmp.alloc<uint64_t>(n, "sampling thresholds");
     uint32_t* thr_u = tmp.alloc<uint32_t>(n, "sampling thresholds (sources)");
-    const int64_t waves = ceil_div(n, 64);
+    const int64_t pieces = ceil_div(e, SAMPLE_PIECE);
+    uint64_t* piece_key = tmp.alloc<uint64_t>(pieces * 2 * k, "piece pairs");
+    uint32_t* piece_u = tmp.alloc<uint32_t>(pieces * 2 * k, "piece pairs (sources)");
+    int32_t* done = tmp.alloc<int32_t>(n, "pieces done");
+    fill_i32(done, n, 0, s);
+    k_sample_pieces<<<(unsigned)ceil_div(pieces, 4), 256, 0, s>>>(csc.in_off, csc.in_src, n, e, seed, layer, k,
+                                                                 piece_key, piece_u, done, thr_key, thr_u);
+    TAURUS_CHECK_LAUNCH();
+    const int64_t waves = ceil_div(n, SAMPLE_DPW);
     k_sample_threshold<<<(unsigned)ceil_div(waves, 4), 256, 0, s>>>(csc.in_off, csc.in_src, n, seed, layer, k, thr_key,
                                                                    thr_u);
     TAURUS_CHECK_LAUNCH();

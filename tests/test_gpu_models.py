@@ -1,0 +1,127 @@
+"""GIN layers (exact and sampled) and sampled GCN layers on the GPU vs the
+oracle (needs an MI355X)."""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+import fixtures as F
+from fixtures import workloads as WL
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _note(msg):
+    print(f"[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _graph(rng, n):
+    """Simple digraph with in-degrees 0, small, medium and one vertex fed by
+    nearly every other vertex."""
+    pairs = set()
+    for v in range(n):
+        r = rng.random()
+        d = 0 if r < 0.2 else int(rng.integers(1, 16)) if r < 0.7 else int(rng.integers(16, 200))
+        for u in rng.choice(n, size=min(d, n - 1), replace=False):
+            if u != v:
+                pairs.add((int(u), v))
+    hub = int(rng.integers(0, n))
+    for u in range(n):
+        if u != hub and rng.random() < 0.9:
+            pairs.add((u, hub))
+    a = np.array(sorted(pairs), dtype=np.int32)
+    return a[:, 0].copy(), a[:, 1].copy()
+
+
+@pytest.mark.parametrize("agg,k", [(WL.GIN_SUM, 0), (WL.GIN_SUM, 5), (WL.GIN_SUM, 15),
+                                   (WL.GCN_SYM, 1), (WL.GCN_SYM, 5), (WL.GCN_SYM, 15)])
+def test_layer_matches_oracle(torch_cuda, agg, k):
+    """One fp32 layer (d 48 -> 40, bias, ReLU) over 3,000 vertices in three
+    chunks, every row against the oracle (the sampled GCN normalised by the
+    sampled graph's degrees)."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    rng = np.random.default_rng(300 + 10 * agg + k)
+    n, d_in, d_out, seed, layer = 3000, 48, 40, 77, 2
+    src, dst = _graph(rng, n)
+    _note(f"agg {agg} fanout {k}: n={n} e={src.size}")
+    g = O.Graph(n, src, dst)
+    X = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = (rng.standard_normal((d_out, d_in)) * 0.2).astype(np.float32)
+    b = rng.standard_normal(d_out).astype(np.float32)
+    row_off, col_dst = T.build_csr(n, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+    out = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    L = T.Layer(n, row_off, col_dst, agg=agg, d_in=d_in, d_out=d_out, weight_cat=np.ascontiguousarray(W.T), bias=b,
+                out=out, relu=True, fanout=k, layer=layer, seed=seed, chunk=1024)
+    L.push_all(torch.from_numpy(X).cuda())
+    st = L.finalize()
+    if k:
+        words, kept = L.sampled_edges()
+    L.destroy()
+    keep = None
+    if k:
+        want, keep, m = O.sample(g, seed, layer, k)
+        assert np.array_equal(words, want) and kept == int(m.sum()) == st["messages"]
+    z = O.layer(agg, g, X, O.F32, W.astype(np.float64), b.astype(np.float64), True, keep_in=keep)
+    r = H.compare(out.cpu().numpy(), z, H.RTOL[F.F32])
+    assert r["n_bad"] == 0, r
+
+
+@pytest.mark.parametrize("agg,dtype", [(WL.GIN_SUM, F.F32), (WL.GIN_SUM, F.BF16), (WL.GCN_SYM, F.BF16)])
+def test_sampled_model_on_rmat(torch_cuda, agg, dtype):
+    """A 2-layer model with fanouts (10, 5) on the RMAT recipe of the
+    in-memory workload at 1/16 of its vertices and edges, in 8,192-vertex
+    chunks, every row of each layer against the oracle fed its own previous
+    layer."""
+    import oracle as O
+    torch = torch_cuda
+    w = dataclasses.replace(WL.GCN_RMAT_1M, agg=agg, feat_dtype=dtype, fanouts=(10, 5)).scaled(
+        n=1_000_000 // 16, e=20_000_000 // 16, chunk=8192, name=f"rmat-1m-div16-agg{agg}-{dtype}")
+    _note(f"{w.name}")
+    src, dst = WL.graph(w)
+    g, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    outs, stats = H.gpu_model(w, row_off, col_dst)
+    for li, (o, z, st) in enumerate(zip(outs, zs, stats), start=1):
+        _, keep, m = O.sample(g, w.seed, li, w.fanout(li))
+        assert st["messages"] == int(m.sum())
+        _, out_dt = w.layer_dtypes(li)
+        r = H.compare(H.to_numpy_f64(o, out_dt), z, H.RTOL[dtype])
+        _note(f"  layer {li}: {r['n_bad']} bad, max abs {r['max_abs']:.2e}")
+        assert r["n_bad"] == 0, (li, r)
+
+
+def test_gin_closed_form_and_unknown_family(torch_cuda):
+    """GIN with unit features and weights counts each vertex's in-degree
+    plus one; an unknown family is refused."""
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    n = 100
+    src = np.arange(1, n, dtype=np.int32)
+    dst = np.zeros(n - 1, dtype=np.int32)
+    row_off, col_dst = T.build_csr(n, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+    out = torch.empty((n, 4), dtype=torch.float32, device="cuda")
+    with pytest.raises(T.TaurusError) as ex:
+        T.Layer(n, row_off, col_dst, agg=3, d_in=8, d_out=4, weight_cat=np.zeros((8, 4), np.float32), bias=None,
+                out=out, chunk=64)
+    assert ex.value.status == -1
+    L = T.Layer(n, row_off, col_dst, agg=WL.GIN_SUM, d_in=8, d_out=4, weight_cat=np.ones((8, 4), np.float32),
+                bias=None, out=out, chunk=64)
+    L.push_all(torch.ones((n, 8), dtype=torch.float32, device="cuda"))
+    L.finalize()
+    L.destroy()
+    # vertex 0 sums 99 sources and itself: 100 * 8 per output; the others 8
+    got = out.cpu().numpy()
+    assert np.all(got[0] == 800.0) and np.all(got[1:] == 8.0)
