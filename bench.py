@@ -128,10 +128,24 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "layer.hip")
 GIB_KIB = float(1 << 20)
 
 
+# the scatter kernels and their launch dispatch: the part of KERNEL_SOURCE
+# between these two section lines, plus the device helpers they include
+SCATTER_BEGIN = "// ---------------------------------------------------------- scatter kernels --"
+SCATTER_END = "// ------------------------------------------------------------- chunk index --"
+DEVICE_HELPERS = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "device.hpp")
+
+
 def source_digest() -> str:
+    """sha256 of the code that decides what k_scatter does: its kernels and
+    launch dispatch (the whole source file if the section lines are gone)
+    and the device helpers header."""
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    text = open(KERNEL_SOURCE).read()
+    a, b = text.find(SCATTER_BEGIN), text.find(SCATTER_END)
+    region = text[a:b] if 0 <= a < b else text
+    h = hashlib.sha256(region.encode())
+    h.update(open(DEVICE_HELPERS, "rb").read())
+    return h.hexdigest()
 
 
 def profiled_traffic():
