@@ -200,6 +200,17 @@ typedef struct {
     int64_t hub_rows;              /* of which resident hub rows                        */
 } taurus_stats;
 
+/*
+ * The library keeps device memory it no longer uses in a cache, so that the
+ * next layer reuses it (re-allocating tens of GB costs seconds).  This call
+ * hands cached blocks of the current device back to the runtime, smallest
+ * first, until at least `bytes` bytes are freed (bytes <= 0: all of them),
+ * for a caller whose own allocation ran out of memory.  Blocks in use are
+ * not touched.  Synchronises the device.  Returns the bytes freed, or a
+ * negative status.
+ */
+int64_t taurus_release_cached_memory(int64_t bytes);
+
 /* Thread-local message describing the last failing call on this thread. */
 const char* taurus_last_error(void);
 

@@ -73,6 +73,7 @@ SIGNATURES = {
     "taurus_sampled_edges": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]),
     "taurus_layer_destroy": (None, [ctypes.c_void_p]),
     "taurus_layer_reload_histogram": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),
+    "taurus_release_cached_memory": (ctypes.c_int64, [ctypes.c_int64]),
     "taurus_reorder": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_rcm": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_ta": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,

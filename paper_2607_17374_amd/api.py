@@ -128,6 +128,29 @@ def permute_rows(x: torch.Tensor, new_of_old: torch.Tensor, inverse: bool = Fals
     return out
 
 
+def release_cached_memory(nbytes: int = 0) -> int:
+    """taurus_release_cached_memory: hand the library's cached device blocks
+    back to the runtime, smallest first, until at least nbytes are freed (0:
+    all).  Returns the bytes freed."""
+    r = N.lib().taurus_release_cached_memory(int(nbytes))
+    if r < 0:
+        raise N.TaurusError(int(r), "taurus_release_cached_memory", N.last_error())
+    return int(r)
+
+
+def alloc_device(shape, dtype, device) -> torch.Tensor:
+    """torch.empty, handing back as much of the library's cached memory as
+    the allocation lacks (and retrying) when the device is out of memory."""
+    try:
+        return torch.empty(shape, dtype=dtype, device=device)
+    except torch.OutOfMemoryError:
+        need = int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size()
+        free, _ = torch.cuda.mem_get_info(device)
+        release_cached_memory(max(need - free, 0) + (1 << 30))
+        torch.cuda.empty_cache()
+        return torch.empty(shape, dtype=dtype, device=device)
+
+
 # eviction policies of a budgeted layer (taurus_eviction)
 EVICTION = {"pending": 0, "random": 1, "fifo": 2, "lru": 3}
 

@@ -41,8 +41,13 @@ struct Failure {
 // Device memory cache (prims.hip): device_acquire returns a block of at
 // least `bytes` usable in stream order on `s` (*got = its size);
 // device_release hands it back after the work queued on `s` so far.
-void* device_acquire(size_t bytes, hipStream_t s, size_t* got);
+// may_oversize: a request of 64 MB or more may take a cached block of up to
+// 1.5 times its size class (*got then names the block's class).
+void* device_acquire(size_t bytes, hipStream_t s, size_t* got, bool may_oversize = false);
 void device_release(void* p, hipStream_t s);
+// hipFree cached (unused) blocks of the current device, smallest first,
+// until at least `bytes` are freed (0: all); returns the bytes freed
+size_t release_cached(size_t bytes);
 
 // Pinned host buffer of at least `bytes` for the calling thread (reused by
 // its next call).

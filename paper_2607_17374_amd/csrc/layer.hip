@@ -1970,6 +1970,14 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
     }
 }
 
+int64_t taurus_release_cached_memory(int64_t bytes) {
+    try {
+        return (int64_t)release_cached(bytes <= 0 ? 0 : (size_t)bytes);
+    } catch (const Failure& f) {
+        return f.status;
+    }
+}
+
 int taurus_layer_reload_histogram(taurus_layer* L, int64_t* counts, int32_t bins) {
     if (!L || !counts || bins < 2) {
         set_error("null argument or bins < 2");

@@ -3,7 +3,10 @@
 // Both are written for wave64: wave-level scans use cross-lane shuffles and
 // the radix ranking matches digits within a wave with eight ballots.
 #include <algorithm>
+#include <chrono>
 #include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
 #include <map>
 #include <mutex>
 #include <unordered_map>
@@ -77,32 +80,59 @@ size_t size_class(size_t bytes) {
     return (bytes + step - 1) / step * step;
 }
 
-// hipFree every cached block of device dev (the caller holds no lock)
-void trim_device(int dev) {
+// TAURUS_ALLOC_LOG=1: one line on stderr per hipMalloc, hipFree and trim
+// of the device memory cache, with its size and wall time
+bool alloc_log() {
+    static const bool on = [] {
+        const char* v = std::getenv("TAURUS_ALLOC_LOG");
+        return v && v[0] == '1';
+    }();
+    return on;
+}
+
+double ms_now() {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now().time_since_epoch()).count();
+}
+
+// hipFree cached blocks of device dev, smallest first, until at least
+// `need` bytes are freed or none is left; returns the bytes freed.  Large
+// blocks are kept when small ones suffice: re-allocating a freed block of
+// tens of GB costs seconds.  The caller holds no lock.
+size_t trim_device(int dev, size_t need) {
     DeviceCache& c = device_cache();
+    const double t0 = alloc_log() ? ms_now() : 0.0;
+    size_t freed = 0;
     (void)hipDeviceSynchronize();
     std::lock_guard<std::mutex> g(c.mu);
-    for (auto it = c.free_lists.begin(); it != c.free_lists.end();) {
-        if (it->first.first != dev) {
-            ++it;
-            continue;
-        }
-        for (const FreeBlock& b : it->second) {
+    // free_lists is ordered by (device, size class)
+    for (auto it = c.free_lists.lower_bound({dev, 0});
+         it != c.free_lists.end() && it->first.first == dev && freed < need;) {
+        std::vector<FreeBlock>& v = it->second;
+        while (!v.empty() && freed < need) {
+            const FreeBlock b = v.back();
+            v.pop_back();
             auto bi = c.blocks.find(b.p);
             if (bi != c.blocks.end()) {
                 if (bi->second.ev) (void)hipEventDestroy(bi->second.ev);
                 c.blocks.erase(bi);
             }
             (void)hipFree(b.p);
+            freed += it->first.second;
         }
-        it = c.free_lists.erase(it);
+        if (v.empty()) it = c.free_lists.erase(it);
+        else ++it;
     }
     (void)hipGetLastError();
+    if (alloc_log()) std::fprintf(stderr, "[taurus alloc] trim: %.3f GB freed in %.1f ms\n", freed / 1e9, ms_now() - t0);
+    return freed;
 }
 
 }  // namespace
 
-void* device_acquire(size_t bytes, hipStream_t s, size_t* got) {
+// requests of at least this size may reuse a larger cached block
+constexpr size_t OVERSIZE_MIN = (size_t)64 << 20;
+
+void* device_acquire(size_t bytes, hipStream_t s, size_t* got, bool may_oversize) {
     int dev = 0;
     TAURUS_HIP(hipGetDevice(&dev));
     const size_t cls = size_class(bytes);
@@ -111,6 +141,17 @@ void* device_acquire(size_t bytes, hipStream_t s, size_t* got) {
     {
         std::lock_guard<std::mutex> g(c.mu);
         auto it = c.free_lists.find({dev, cls});
+        if ((it == c.free_lists.end() || it->second.empty()) && may_oversize && cls >= OVERSIZE_MIN) {
+            // a large request may take the smallest cached block up to 1.5x
+            // its class instead of a fresh hipMalloc
+            for (auto j = c.free_lists.upper_bound({dev, cls});
+                 j != c.free_lists.end() && j->first.first == dev && j->first.second <= cls + cls / 2; ++j)
+                if (!j->second.empty()) {
+                    it = j;
+                    *got = j->first.second;
+                    break;
+                }
+        }
         if (it != c.free_lists.end() && !it->second.empty()) {
             std::vector<FreeBlock>& v = it->second;
             size_t pick = v.size() - 1;
@@ -126,12 +167,17 @@ void* device_acquire(size_t bytes, hipStream_t s, size_t* got) {
         }
     }
     void* p = nullptr;
+    const double t0 = alloc_log() ? ms_now() : 0.0;
     hipError_t e = hipMalloc(&p, cls);
-    if (e == hipErrorOutOfMemory) {
+    while (e == hipErrorOutOfMemory) {
         (void)hipGetLastError();
-        trim_device(dev);
+        if (alloc_log()) std::fprintf(stderr, "[taurus alloc] hipMalloc(%.3f GB) out of memory\n", cls / 1e9);
+        if (trim_device(dev, cls) == 0) break;
         e = hipMalloc(&p, cls);
     }
+    if (alloc_log())
+        std::fprintf(stderr, "[taurus alloc] hipMalloc(%.3f GB): %s in %.1f ms\n", cls / 1e9,
+                     e == hipSuccess ? "ok" : "failed", ms_now() - t0);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         fail(e == hipErrorOutOfMemory ? TAURUS_E_OOM : TAURUS_E_DEVICE, "hipMalloc(%zu) failed: %s", cls,
@@ -140,6 +186,12 @@ void* device_acquire(size_t bytes, hipStream_t s, size_t* got) {
     std::lock_guard<std::mutex> g(c.mu);
     c.blocks[p] = BlockInfo{dev, cls, nullptr};
     return p;
+}
+
+size_t release_cached(size_t bytes) {
+    int dev = 0;
+    TAURUS_HIP(hipGetDevice(&dev));
+    return trim_device(dev, bytes == 0 ? SIZE_MAX : bytes);
 }
 
 void device_release(void* p, hipStream_t s) {
@@ -205,11 +257,13 @@ void* Arena::alloc_bytes(int64_t bytes, const char* what) {
     size_t got = 0;
     void* p = nullptr;
     try {
-        p = device_acquire((size_t)bytes, stream_, &got);
+        p = device_acquire((size_t)bytes, stream_, &got, budget_ <= 0);
     } catch (const Failure&) {
         set_error("%s (for %s)", last_error_cstr(), what);
         throw;
     }
+    // a block taken oversize is counted at the requested class
+    got = std::min(got, (size_t)cls);
     blocks_.push_back({p, (int64_t)got});
     bytes_ += (int64_t)got;
     if (bytes_ > peak_) peak_ = bytes_;

@@ -111,7 +111,7 @@ def run_model(w, row_off, col_dst, X, plan_chunk, ids, mask_check=None, keep_inp
     h = X
     host, stats = [], []
     for li, spec in enumerate(H.layer_specs(w), start=1):
-        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=dev)
+        out = T.alloc_device((w.n, spec["d_out"]), torch_dtype(spec["out_dtype"]), dev)
         torch.cuda.synchronize()
         t0 = time.time()
         L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, plan=plan, **spec)
@@ -157,7 +157,7 @@ def residency_run(w, g, pi_host, row_off, col_dst, X, slot_list) -> dict:
     spec = H.layer_specs(w)[1]
 
     def run(budget):
-        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=X.device)
+        out = T.alloc_device((w.n, spec["d_out"]), torch_dtype(spec["out_dtype"]), X.device)
         torch.cuda.synchronize()
         t0 = time.time()
         L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, hbm_budget=budget,

@@ -99,7 +99,7 @@ def gpu_model(w: WL.Workload, row_off, col_dst, X=None, chunk=None, order=None, 
     specs = layer_specs(w)
     plan = T.Plan(w.n, row_off, col_dst, chunk, stream=stream) if use_plan else None
     for spec in specs:
-        out = torch.empty((w.n, spec["d_out"]), dtype=torch_dtype(spec["out_dtype"]), device=X.device)
+        out = T.alloc_device((w.n, spec["d_out"]), torch_dtype(spec["out_dtype"]), X.device)
         L = T.Layer(w.n, row_off, col_dst, out=out, chunk=chunk, profile=profile, stream=stream,
                     plan=plan, **spec)
         L.push_all(h, order=order)

@@ -192,3 +192,29 @@ def test_budget_errors(torch_cuda):
     L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **spec)
     assert L.reload_histogram(4).tolist() == [w.n, 0, 0, 0]
     L.destroy()
+
+
+def test_release_cached_memory(torch_cuda):
+    """A destroyed layer's buffers stay cached for the next layer; releasing
+    hands them back to the runtime (partly: at least the bytes asked for,
+    smallest blocks first), and a second full release finds nothing."""
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    w = WL.SAGE_RMAT_4K
+    _note("release cached memory")
+    row_off, col_dst = H.gpu_graph(w)
+    spec = H.layer_specs(w)[0]
+    out = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **spec)
+    L.push_all(torch.from_numpy(WL.input_features(w)).cuda())
+    L.finalize()
+    L.destroy()
+    part = T.release_cached_memory(4096)
+    assert part >= 4096
+    rest = T.release_cached_memory(0)
+    assert rest > 0 and T.release_cached_memory(0) == 0
+    # the next layer allocates afresh and still works
+    L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, **spec)
+    L.push_all(torch.from_numpy(WL.input_features(w)).cuda())
+    L.finalize()
+    L.destroy()
