@@ -55,6 +55,8 @@ def lib():
         L.fx_weights.argtypes = [u64, i64, i64, i64, i64, i64, vp]
         L.fx_bias.restype = None
         L.fx_bias.argtypes = [u64, i64, i64, i64, vp]
+        L.fx_attention.restype = None
+        L.fx_attention.argtypes = [u64, i64, i64, vp]
         L.fx_round16.restype = None
         L.fx_round16.argtypes = [i64, vp, i32, vp]
         L.fx_random_ids.restype = i32
@@ -112,6 +114,13 @@ def weights(seed: int, layer: int, rows: int, cols: int, fan_in: int, fan_out: i
 def bias(seed: int, layer: int, d: int, fan_in: int) -> np.ndarray:
     out = np.empty(d, np.float32)
     lib().fx_bias(seed, layer, d, fan_in, _p(out))
+    return out
+
+
+def attention(seed: int, layer: int, d: int) -> np.ndarray:
+    """GAT attention vectors [2][d] fp32: row 0 for the source, row 1 for the destination."""
+    out = np.empty((2, d), np.float32)
+    lib().fx_attention(seed, layer, d, _p(out))
     return out
 
 

@@ -251,6 +251,19 @@ void fx_bias(uint64_t seed, int64_t layer, int64_t d, int64_t fan_in, float* out
     }
 }
 
+/* Attention vectors of a GAT layer, a (2 x d) matrix: row 0 multiplies the
+ * transformed source row, row 1 the transformed destination row;
+ * a_kj = sqrt(6 / (d + 1)) * (2 * ((H(seed,8,layer,k,j) >> 40) * 2^-24) - 1), fp32 */
+void fx_attention(uint64_t seed, int64_t layer, int64_t d, float* out) {
+    double a = sqrt(6.0 / (double)(d + 1));
+    for (int64_t k = 0; k < 2; k++)
+        for (int64_t j = 0; j < d; j++) {
+            uint64_t h = fx_step(fx_step(fx_step(fx_step(seed, 8), (uint64_t)layer), (uint64_t)k), (uint64_t)j);
+            double u = (double)(h >> 40) * 0x1.0p-24;
+            out[k * d + j] = (float)(a * (2.0 * u - 1.0));
+        }
+}
+
 /* Round an fp32 array to bf16 (dtype 1) or fp16 (dtype 2), RNE. */
 void fx_round16(int64_t n, const float* in, int dtype, uint16_t* out) {
 #pragma omp parallel for schedule(static)

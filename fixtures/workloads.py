@@ -15,7 +15,7 @@ import numpy as np
 from . import F32, BF16, F16, UNIFORM, NORMAL
 from . import rmat_edges, features, weights, bias, round16
 
-SAGE_MEAN, GCN_SYM, GIN_SUM = 0, 1, 2
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
 
 
 @dataclass(frozen=True)
@@ -115,6 +115,7 @@ class LayerParams:
     d_out: int
     W: np.ndarray             # fp32 (rows d_out), values already rounded to the storage dtype
     b: np.ndarray             # fp32 [d_out]
+    attn: np.ndarray | None = None   # GAT: [2][d_out] fp32, row 0 source, row 1 destination
 
     @property
     def W_agg(self):
@@ -139,4 +140,8 @@ def layer_params(w: Workload, layer: int) -> LayerParams:
         from . import bits_to_float
         W = bits_to_float(round16(W, w.feat_dtype), w.feat_dtype).reshape(W.shape)
     b = bias(w.seed, layer, d_out, fan_in=cols)
-    return LayerParams(layer, w.agg, d_in, d_out, W, b)
+    attn = None
+    if w.agg == GAT_ATT:
+        from . import attention
+        attn = attention(w.seed, layer, d_out)
+    return LayerParams(layer, w.agg, d_in, d_out, W, b, attn)

@@ -22,7 +22,7 @@ _SO = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "oracle.c")
 
 F32, BF16, F16 = 0, 1, 2
-SAGE_MEAN, GCN_SYM, GIN_SUM = 0, 1, 2
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
 
 
 def build(force: bool = True) -> str:
@@ -64,6 +64,8 @@ def load(path: str):
     L.or_widen.argtypes = [i64, vp, i32, vp]
     L.or_layer.restype = i32
     L.or_layer.argtypes = [i32, i64, vp, vp, vp, vp, vp, i32, i64, vp, vp, i64, i32, i64, vp, vp]
+    L.or_gat_layer.restype = i32
+    L.or_gat_layer.argtypes = [i64, vp, vp, vp, vp, i32, i64, vp, vp, vp, i64, i32, ctypes.c_double, i64, vp, vp]
     L.or_reorder_bfs.restype = i32
     L.or_reorder_bfs.argtypes = [i64, vp, vp, vp]
     L.or_reorder_rcm.restype = i32
@@ -236,6 +238,32 @@ def layer(agg: int, g: Graph, H: np.ndarray, h_dtype: int, W: np.ndarray, b: np.
     return out
 
 
+GAT_SLOPE = 0.2   # LeakyReLU negative slope of the attention scores
+
+
+def gat_layer(g: Graph, H: np.ndarray, h_dtype: int, W: np.ndarray, attn: np.ndarray, b: np.ndarray | None,
+              relu: bool, keep_in: np.ndarray | None = None, dst_ids: np.ndarray | None = None,
+              slope: float = GAT_SLOPE) -> np.ndarray:
+    """Single-head GAT layer in fp64 for ``dst_ids`` (all if None).  W [d_out][d_in];
+    attn [2][d_out] (row 0 source, row 1 destination)."""
+    H = np.ascontiguousarray(H)
+    d_in = H.shape[1]
+    W = np.ascontiguousarray(W, np.float64)
+    d_out = W.shape[0]
+    assert W.shape[1] == d_in and np.shape(attn) == (2, d_out)
+    a = np.ascontiguousarray(attn, np.float64)
+    bb = None if b is None else np.ascontiguousarray(b, np.float64)
+    ids = None if dst_ids is None else np.ascontiguousarray(dst_ids, np.int64)
+    count = g.n if ids is None else ids.size
+    out = np.empty((count, d_out), np.float64)
+    kin = None if keep_in is None else np.ascontiguousarray(keep_in, np.uint8)
+    rc = lib().or_gat_layer(g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(H), h_dtype, d_in, _p(W), _p(a), _p(bb),
+                            d_out, int(relu), float(slope), count, _p(ids), _p(out))
+    if rc:
+        raise MemoryError("or_gat_layer")
+    return out
+
+
 def round_store(x: np.ndarray, dtype: int) -> np.ndarray:
     """fp64 -> fp32 -> (bf16 | fp16), round to nearest even; 16-bit as uint16 bits."""
     x = np.ascontiguousarray(x, np.float64)
@@ -348,7 +376,10 @@ def run_model(w, g: Graph, X: np.ndarray, params):
         if w.fanout(li) > 0:
             _, keep, _ = sample(g, w.seed, li, w.fanout(li))
         relu = li < w.layers
-        z = layer(w.agg, g, H, h_dtype, p.W, p.b, relu, keep_in=keep)
+        if w.agg == GAT_ATT:
+            z = gat_layer(g, H, h_dtype, p.W, p.attn, p.b, relu, keep_in=keep)
+        else:
+            z = layer(w.agg, g, H, h_dtype, p.W, p.b, relu, keep_in=keep)
         _, out_dtype = w.layer_dtypes(li)
         H = round_store(z, out_dtype)
         h_dtype = out_dtype

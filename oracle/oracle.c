@@ -441,6 +441,89 @@ int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
     return bad ? -3 : 0;
 }
 
+/*
+ * GATConv, single head (Sec. 3.9, GATConv; Sec. 4.1 evaluates it):
+ *     h'_u    = W h_u                                   (W: d_out x d_in)
+ *     e_uv    = LeakyReLU(a^T [h'_u || h'_v])           (a = [a_src ; a_dst])
+ *     alpha_uv = softmax over u in N-(v) of e_uv
+ *     z_v     = sum_u alpha_uv h'_u + b,  out = ReLU(z) if relu.
+ * N-(v) holds v's propagated in-neighbours and v itself (every vertex
+ * aggregates a self message); keep_in selects the propagated in-edges (NULL
+ * = all).  attn = [a_src (d_out) | a_dst (d_out)]; slope = LeakyReLU's
+ * negative slope.  The softmax subtracts the neighbourhood's largest score
+ * (the same value in exact arithmetic).  h' is computed for every vertex.
+ * Returns 0, or -3 when out of memory.
+ */
+int or_gat_layer(int64_t n, const int64_t* in_off, const int32_t* in_src, const uint8_t* keep_in,
+                 const void* H, int h_dtype, int64_t d_in, const double* W, const double* attn,
+                 const double* bias, int64_t d_out, int relu, double slope, int64_t n_dst,
+                 const int64_t* dst_ids, double* out) {
+    double* hp = (double*)malloc((size_t)(n > 0 ? n : 1) * (size_t)d_out * sizeof(double));
+    double* sc = (double*)malloc((size_t)(n > 0 ? n : 1) * 2 * sizeof(double));
+    if (!hp || !sc) return -3;
+#pragma omp parallel for schedule(dynamic, 256)
+    for (int64_t u = 0; u < n; u++) {
+        double s_src = 0.0, s_dst = 0.0;
+        for (int64_t o = 0; o < d_out; o++) {
+            double z = 0.0;
+            for (int64_t j = 0; j < d_in; j++) z += W[o * d_in + j] * or_load(H, h_dtype, u * d_in + j);
+            hp[u * d_out + o] = z;
+            s_src += attn[o] * z;
+            s_dst += attn[d_out + o] * z;
+        }
+        sc[2 * u] = s_src;
+        sc[2 * u + 1] = s_dst;
+    }
+    int64_t count = dst_ids ? n_dst : n;
+    int bad = 0;
+#pragma omp parallel
+    {
+        double* a = (double*)malloc((size_t)d_out * sizeof(double));
+        if (!a) bad = 1;
+#pragma omp for schedule(dynamic, 256)
+        for (int64_t i = 0; i < count; i++) {
+            if (!a) continue;
+            int64_t v = dst_ids ? dst_ids[i] : i;
+            double tv = sc[2 * v + 1];
+            /* the largest score: the self message first, then the kept in-edges */
+            double e = sc[2 * v] + tv;
+            double m = e > 0.0 ? e : slope * e;
+            for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                if (keep_in && !keep_in[k]) continue;
+                e = sc[2 * (int64_t)in_src[k]] + tv;
+                e = e > 0.0 ? e : slope * e;
+                if (e > m) m = e;
+            }
+            /* unnormalised weights exp(e - m), their sum, and the weighted rows */
+            for (int64_t o = 0; o < d_out; o++) a[o] = 0.0;
+            double ssum = 0.0;
+            for (int64_t k = in_off[v] - 1; k < in_off[v + 1]; k++) {
+                int64_t u;
+                if (k < in_off[v]) {
+                    u = v;
+                } else {
+                    if (keep_in && !keep_in[k]) continue;
+                    u = in_src[k];
+                }
+                e = sc[2 * u] + tv;
+                e = e > 0.0 ? e : slope * e;
+                double w = exp(e - m);
+                ssum += w;
+                for (int64_t o = 0; o < d_out; o++) a[o] += w * hp[u * d_out + o];
+            }
+            for (int64_t o = 0; o < d_out; o++) {
+                double z = a[o] / ssum + (bias ? bias[o] : 0.0);
+                if (relu) z = z < 0.0 ? 0.0 : z;
+                out[i * d_out + o] = z;
+            }
+        }
+        free(a);
+    }
+    free(hp);
+    free(sc);
+    return bad ? -3 : 0;
+}
+
 /* ------------------------------------------------------------ reorder ---- */
 /*
  * Degree/BFS vertex ordering: a reading of a degree-sorted breadth-first

@@ -47,6 +47,14 @@ def layer_specs(w: WL.Workload, fanouts=None):
     return specs
 
 
+def oracle_layer(w: WL.Workload, p, g, H, h_dtype, relu, keep_in=None, dst_ids=None):
+    """The oracle layer of w's family with layer parameters p."""
+    import oracle as O
+    if w.agg == WL.GAT_ATT:
+        return O.gat_layer(g, H, h_dtype, p.W, p.attn, p.b, relu, keep_in=keep_in, dst_ids=dst_ids)
+    return O.layer(w.agg, g, H, h_dtype, p.W, p.b, relu, keep_in=keep_in, dst_ids=dst_ids)
+
+
 def oracle_model(w: WL.Workload, src=None, dst=None):
     """Full oracle run of workload w -> (oracle graph, [fp64 outputs per layer])."""
     import oracle as O
@@ -61,7 +69,7 @@ def oracle_model(w: WL.Workload, src=None, dst=None):
         keep = None
         if w.fanout(li) > 0:
             _, keep, _ = O.sample(g, w.seed, li, w.fanout(li))
-        z = O.layer(w.agg, g, H, h_dtype, p.W, p.b, li < w.layers, keep_in=keep)
+        z = oracle_layer(w, p, g, H, h_dtype, li < w.layers, keep_in=keep)
         zs.append(z)
         _, out_dt = w.layer_dtypes(li)
         H = O.round_store(z, out_dt)
@@ -165,7 +173,7 @@ def oracle_sampled_layers(w: WL.Workload, g, X: np.ndarray, ids: list, keeps: li
     out = []
     for li in range(1, L + 1):
         p = WL.layer_params(w, li)
-        z = O.layer(w.agg, g, H, h_dtype, p.W, p.b, li < L, keep_in=keeps[li - 1], dst_ids=need[li - 1])
+        z = oracle_layer(w, p, g, H, h_dtype, li < L, keep_in=keeps[li - 1], dst_ids=need[li - 1])
         pos = np.searchsorted(need[li - 1], np.asarray(ids[li - 1], np.int64))
         out.append(z[pos])
         if li < L:

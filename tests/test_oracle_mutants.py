@@ -145,6 +145,21 @@ MUTANTS = {
         "for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, v * d_in + j);\n            }",
         "(void)0;\n            }",
         [lambda: P.test_gin_matches_dense(False)]),
+    # GAT without the self message in the softmax
+    "gat_no_self_message": (
+        "for (int64_t k = in_off[v] - 1; k < in_off[v + 1]; k++) {",
+        "for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {",
+        [lambda: P.test_gat_matches_dense(False, True), P.test_gat_special_cases]),
+    # GAT: source and destination halves of a swapped
+    "gat_attention_halves_swapped": (
+        "s_src += attn[o] * z;\n            s_dst += attn[d_out + o] * z;",
+        "s_src += attn[d_out + o] * z;\n            s_dst += attn[o] * z;",
+        [lambda: P.test_gat_matches_dense(False, False)]),
+    # GAT: LeakyReLU slope on the positive side
+    "gat_leaky_relu_flipped": (
+        "e = e > 0.0 ? e : slope * e;\n                double w = exp(e - m);",
+        "e = e < 0.0 ? e : slope * e;\n                double w = exp(e - m);",
+        [lambda: P.test_gat_matches_dense(False, True)]),
     # fp16 rounding truncates
     "f16_truncates": (
         "double r = nearbyint(q);\n    if (r >= 2048.0)",

@@ -893,3 +893,60 @@ def test_fewest_pending_reloads_least():
     reloads = {p: O.residency_sim(g, w.chunk, S, H, p, seed=4)[1] for p in O.EVICTION}
     assert reloads["pending"] > 0
     assert all(reloads["pending"] < reloads[p] for p in ("random", "fifo", "lru")), reloads
+
+
+# ---- GATConv (Sec. 3.9): single head, self message in every neighbourhood
+
+def dense_gat(A, H, W, attn, b, relu, slope=0.2):
+    """Dense GAT: scores on (A + I), column softmax, attention-weighted rows."""
+    Hp = H @ W.T
+    s, t = Hp @ attn[0], Hp @ attn[1]
+    M = A.astype(bool) | np.eye(A.shape[0], dtype=bool)      # M[u, v]: u sends to v
+    E = s[:, None] + t[None, :]
+    E = np.where(E > 0, E, slope * E)
+    E = np.where(M, E, -np.inf)
+    P = np.exp(E - E.max(axis=0, keepdims=True))
+    P /= P.sum(axis=0, keepdims=True)                       # P[u, v] = alpha_uv
+    z = P.T @ Hp + b
+    return np.maximum(z, 0) if relu else z
+
+
+@pytest.mark.parametrize("sampled,relu", [(False, True), (False, False), (True, True)])
+def test_gat_matches_dense(sampled, relu):
+    rng = np.random.default_rng(210 + 2 * sampled + relu)
+    n, d_in, d_out = 80, 7, 6
+    A, u, v = random_digraph(rng, n, 0.09, isolated=4)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in))
+    attn = rng.standard_normal((2, d_out))
+    b = rng.standard_normal(d_out)
+    keep_in, A_used = None, A
+    if sampled:
+        words, keep_in, _ = O.sample(g, 9, 1, 3)
+        bits = O.mask_bits(words, g.e)
+        A_used = np.zeros_like(A)
+        A_used[np.repeat(np.arange(n), np.diff(g.row_off))[bits], g.col_dst[bits]] = True
+    got = O.gat_layer(g, H32, O.F32, W, attn, b, relu, keep_in=keep_in)
+    np.testing.assert_allclose(got, dense_gat(A_used, H32.astype(np.float64), W, attn, b, relu),
+                               rtol=1e-11, atol=1e-11)
+
+
+def test_gat_special_cases():
+    rng = np.random.default_rng(220)
+    n, d_in, d_out = 50, 5, 4
+    A, u, v = random_digraph(rng, n, 0.1, isolated=3)
+    g = O.Graph(n, u, v)
+    H = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in))
+    Hp = H.astype(np.float64) @ W.T
+    M = (A | np.eye(n, dtype=bool)).astype(np.float64)
+    mean = (M.T @ Hp) / M.sum(axis=0)[:, None]
+    # zero attention, or attention on the destination only: every score of a
+    # neighbourhood is equal, so GAT is the mean over N(v) and v
+    for attn in (np.zeros((2, d_out)), np.stack([np.zeros(d_out), rng.standard_normal(d_out)])):
+        np.testing.assert_allclose(O.gat_layer(g, H, O.F32, W, attn, None, False), mean, rtol=1e-12, atol=1e-12)
+    # a vertex without in-edges attends only to itself
+    iso = np.flatnonzero(np.diff(g.in_off) == 0)
+    z = O.gat_layer(g, H, O.F32, W, rng.standard_normal((2, d_out)), None, False, dst_ids=iso)
+    np.testing.assert_allclose(z, Hp[iso], rtol=1e-12, atol=1e-12)
