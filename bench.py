@@ -41,6 +41,9 @@ VARIANTS = {
     "gcn-sampled": (1, (10, 5), "2-layer GCN 128->128->64, fanouts (10, 5), norms of the sampled graph"),
     "gin": (2, (), "2-layer GIN 128->128->64 (linear apply, eps = 0), exact"),
     "gin-sampled": (2, (10, 5), "2-layer GIN 128->128->64, fanouts (10, 5)"),
+    "gat": (3, (), "2-layer single-head GAT 128->128->64 (LeakyReLU 0.2), exact: transform, softmax statistics "
+                   "and aggregation passes"),
+    "gat-sampled": (3, (10, 5), "2-layer single-head GAT 128->128->64, fanouts (10, 5)"),
 }
 
 

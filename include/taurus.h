@@ -62,7 +62,12 @@ typedef enum {
     TAURUS_GCN_SYM = 1,   /* z_v = W sum_{u in M(v) + {v}} h_u / sqrt(d^_out(u) d^_in(v)) + b,
                              d^ = degree + 1 (one self loop per vertex); a sampled layer uses the
                              degrees of its sampled graph: kept out-edges, d^_in(v) = |M(v)| + 1 */
-    TAURUS_GIN_SUM = 2    /* GINConv, linear apply, eps = 0: z_v = W (h_v + sum_{u in M(v)} h_u) + b */
+    TAURUS_GIN_SUM = 2,   /* GINConv, linear apply, eps = 0: z_v = W (h_v + sum_{u in M(v)} h_u) + b */
+    TAURUS_GAT_ATT = 3    /* GATConv, one head (Sec. 3.9): h' = W h, e_uv = LeakyReLU(a^T [h'_u || h'_v]),
+                             slope 0.2, alpha = softmax of e over M(v) + {v},
+                             z_v = sum alpha_uv h'_u + b; needs desc.attn; in core (hbm_budget 0).
+                             The pushes transform (pass 1); finalize runs the softmax statistics
+                             (pass 2) and the aggregation (pass 3) over every chunk            */
 } taurus_agg;
 
 /*
@@ -136,6 +141,9 @@ typedef struct {
  *   profile      1: time every kernel of the layer with HIP events; 2: time
  *                only the scatter launches (fewer events in the stream); the
  *                totals are returned in taurus_stats.
+ *   attn         GAT layers: host float[2][d_out], row 0 (a_src) scores the
+ *                transformed source row, row 1 (a_dst) the destination's;
+ *                read at init.  NULL for the other families.
  *   eviction     TAURUS_EVICT_* policy of a budgeted layer (ignored in core).
  *                Victims are ranked by a 14-bit key: pending counts past
  *                16383 share the last bin, and chunk numbers are shifted
@@ -162,6 +170,7 @@ typedef struct {
     int32_t profile;
     const taurus_plan* plan;
     int32_t eviction;
+    const float* attn;
 } taurus_layer_desc;
 
 typedef struct taurus_layer taurus_layer;

@@ -40,7 +40,7 @@ class LayerDesc(ctypes.Structure):
                 ("chunk", ctypes.c_int64), ("hbm_budget", ctypes.c_int64), ("hub_fraction", ctypes.c_double),
                 ("out", ctypes.c_void_p), ("out_on_host", ctypes.c_int32),
                 ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p),
-                ("eviction", ctypes.c_int32)]
+                ("eviction", ctypes.c_int32), ("attn", ctypes.c_void_p)]
 
 
 class Stats(ctypes.Structure):

@@ -194,13 +194,14 @@ class Layer:
                  in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
                  hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None,
-                 eviction: str = "pending"):
+                 eviction: str = "pending", attn: Optional[np.ndarray] = None):
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
                              col_dst.data_ptr() if e else None)
         self._w = np.ascontiguousarray(weight_cat, dtype=np.float32)
         self._b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        self._a = None if attn is None else np.ascontiguousarray(attn, dtype=np.float32).reshape(2, d_out)
         self.out = out
         out_ptr, out_on_host = _buf_ptr(out, _TORCH_DTYPE[out_dtype], "out")
         self.n, self.d_in, self.d_out, self.chunk, self.in_dtype = n, d_in, d_out, chunk, in_dtype
@@ -210,7 +211,8 @@ class Layer:
             fanout=fanout, layer=layer, seed=seed & (2**64 - 1), chunk=chunk, hbm_budget=hbm_budget,
             hub_fraction=hub_fraction, out=out_ptr, out_on_host=out_on_host,
             stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None,
-            eviction=EVICTION[eviction] if isinstance(eviction, str) else int(eviction))
+            eviction=EVICTION[eviction] if isinstance(eviction, str) else int(eviction),
+            attn=None if self._a is None else self._a.ctypes.data)
         self._keep = (row_off, col_dst, plan)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")

@@ -1315,6 +1315,234 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
 
 }  // namespace taurus
 
+namespace taurus {
+
+// ------------------------------------------------------------------- GAT --
+// Single-head GATConv (Sec. 3.9, GATConv) in three passes over the chunks:
+//   1. transform (taurus_push_chunk): h'_c = X_c W for the chunk, written to
+//      a table h' of every vertex, and two more columns s_u = a_src . h'_u
+//      and t_u = a_dst . h'_u, taken in fp32 from the transformed row;
+//   2. softmax statistics, topology only: per destination the largest score
+//      m_v and the sum S_v = sum_u exp(e_uv - m_v) over its neighbourhood
+//      (propagated messages and the self message), e_uv = LeakyReLU(s_u +
+//      t_v).  Walks the chunk index in chunk order; each segment merges its
+//      own (max, sum) into the destination's as the sole owner, hub pieces
+//      through per-piece scalar carries merged in piece order, so the
+//      result is deterministic;
+//   3. aggregation: the chunks of h' are streamed again and every message
+//      adds alpha_uv h'_u with alpha_uv = exp(e_uv - m_v) / S_v, through the
+//      sole-owner flush and fix-up of the other families.
+constexpr float GAT_SLOPE = 0.2f;
+
+struct GatParams {
+    const float* hp;  // [n][ystride]: h' then s, t
+    int64_t ystride;
+    int d_o;
+    float* m;         // [n] running largest score
+    float* S;         // [n] running sum of exp(score - m); 0 = none yet
+    float* scarry;    // per hub piece of the chunk: {max, sum}
+};
+
+// pass 1 after the chunk's transform: one wave per row of h' (row stride
+// ncols) writes s and t into columns d_o and d_o + 1
+__global__ __launch_bounds__(256) void k_gat_scores(float* __restrict__ hp, int64_t rows, int64_t ncols, int d_o,
+                                                    const float* __restrict__ attn) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    if (r >= rows) return;
+    float* row = hp + r * ncols;
+    float s = 0.f, t = 0.f;
+    for (int o = lane; o < d_o; o += 64) {
+        s = fmaf(attn[o], row[o], s);
+        t = fmaf(attn[d_o + o], row[o], t);
+    }
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) {
+        s += __shfl_xor(s, d, 64);
+        t += __shfl_xor(t, d, 64);
+    }
+    if (lane == 0) {
+        row[d_o] = s;
+        row[d_o + 1] = t;
+    }
+}
+
+__device__ inline float gat_score(const GatParams& q, int64_t u, int64_t v) {
+    const float e = q.hp[u * q.ystride + q.d_o] + q.hp[v * q.ystride + q.d_o + 1];
+    return e > 0.f ? e : GAT_SLOPE * e;
+}
+
+// (m, S) <- the statistics of both parts
+__device__ inline void gat_merge(float& m, float& S, float m2, float S2) {
+    if (S2 == 0.f) return;
+    if (S == 0.f) {
+        m = m2;
+        S = S2;
+        return;
+    }
+    const float M = fmaxf(m, m2);
+    S = S * expf(m - M) + S2 * expf(m2 - M);
+    m = M;
+}
+
+// Source vertex of slot i of a short unit (slot 0 of a SELF_HERE unit is
+// the destination itself) or of a wave piece (its last slot, with
+// SELF_HERE).
+__device__ inline int64_t short_slot_src(const ScatterParams& p, int4 w, int i) {
+    const int self = (w.y & SELF_HERE) ? 1 : 0;
+    return (self && i == 0) ? (int64_t)w.z : p.first_row + p.src[w.x + i - self];
+}
+__device__ inline int64_t piece_slot_src(const ScatterParams& p, int4 w, int i) {
+    const int items = (w.y & LEN_MASK) - ((w.y & SELF_HERE) ? 1 : 0);
+    return i < items ? p.first_row + p.src[w.x + i] : (int64_t)w.z;
+}
+
+// unit t of the chunk's short classes taken as one sequence
+__device__ inline int4 short_unit(const ChunkUnits& cu, int64_t t) {
+#pragma unroll
+    for (int c = 0; c < NCLASS; c++) {
+        if (t < cu.n[c]) return cu.u[c][t];
+        t -= cu.n[c];
+    }
+    return make_int4(0, 0, -1, 0);
+}
+
+// pass 2, short units: one thread each
+__global__ void k_gat_stats_short(ScatterParams p, ChunkUnits cu, GatParams q, int64_t total) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= total) return;
+    const int4 w = short_unit(cu, t);
+    const int v = w.z, L = w.y & LEN_MASK;
+    float mx = -INFINITY;
+    for (int i = 0; i < L; i++) mx = fmaxf(mx, gat_score(q, short_slot_src(p, w, i), v));
+    float sum = 0.f;
+    for (int i = 0; i < L; i++) sum += expf(gat_score(q, short_slot_src(p, w, i), v) - mx);
+    float m = q.m[v], S = q.S[v];
+    gat_merge(m, S, mx, sum);
+    q.m[v] = m;
+    q.S[v] = S;
+}
+
+// pass 2, wave pieces: one wave each; a hub piece parks its statistics
+__global__ __launch_bounds__(256) void k_gat_stats_pieces(ScatterParams p, const int4* __restrict__ units,
+                                                          int64_t n, GatParams q) {
+    const int lane = threadIdx.x & 63;
+    const int64_t un = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    if (un >= n) return;  // the whole wave
+    const int4 w = units[un];
+    const int v = w.z, L = w.y & LEN_MASK;
+    float mx = -INFINITY;
+    for (int i = lane; i < L; i += 64) mx = fmaxf(mx, gat_score(q, piece_slot_src(p, w, i), v));
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d, 64));
+    float sum = 0.f;
+    for (int i = lane; i < L; i += 64) sum += expf(gat_score(q, piece_slot_src(p, w, i), v) - mx);
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) sum += __shfl_xor(sum, d, 64);
+    if (lane != 0) return;
+    if (w.w < 0) {
+        float m = q.m[v], S = q.S[v];
+        gat_merge(m, S, mx, sum);
+        q.m[v] = m;
+        q.S[v] = S;
+    } else {
+        const int64_t slot = (int64_t)w.w - p.long_base;
+        q.scarry[2 * slot] = mx;
+        q.scarry[2 * slot + 1] = sum;
+    }
+}
+
+// pass 2, the chunk's own vertices without a segment from it, and the hub
+// segments' pieces in order
+__global__ void k_gat_stats_self(ScatterParams p, GatParams q) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= p.rows) return;
+    const int64_t v = p.first_row + r;
+    if (p.has_own[v] & OWN_SEGMENT) return;
+    float m = q.m[v], S = q.S[v];
+    gat_merge(m, S, gat_score(q, v, v), 1.f);
+    q.m[v] = m;
+    q.S[v] = S;
+}
+__global__ void k_gat_stats_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix, GatParams q) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= nfix) return;
+    const int4 f = fix[t];
+    const int v = f.x;
+    const int64_t first = (int64_t)f.y - p.long_base;
+    float m = q.m[v], S = q.S[v];
+    for (int j = 0; j < f.z; j++) gat_merge(m, S, q.scarry[2 * (first + j)], q.scarry[2 * (first + j) + 1]);
+    q.m[v] = m;
+    q.S[v] = S;
+}
+
+// pass 3: one row-group per unit (the short classes, then the wave pieces,
+// then the self pass); every slot's row of h' weighted by its attention
+template <int G, int VEC>
+__global__ __launch_bounds__(SC_THREADS) void k_gat_aggregate(ScatterParams p, ChunkUnits cu, GatParams q,
+                                                              int64_t nshort) {
+    constexpr int NRG = SC_THREADS / G;
+    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
+    const int64_t t = (int64_t)blockIdx.x * NRG + rg;
+    const int64_t npiece = cu.n[NCLASS];
+    const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    float4 c[VEC], pre[VEC], row[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; j++) c[j] = pre[j] = f4_zero();
+    if (t < nshort + npiece) {
+        const bool piece = t >= nshort;
+        const int4 w = piece ? cu.u[NCLASS][t - nshort] : short_unit(cu, t);
+        const int v = w.z, L = w.y & LEN_MASK;
+        const float tv_m = q.m[v], inv_s = 1.f / q.S[v];
+        for (int i = 0; i < L; i++) {
+            const int64_t u = piece ? piece_slot_src(p, w, i) : short_slot_src(p, w, i);
+            const float a = expf(gat_score(q, u, v) - tv_m) * inv_s;
+            gather_row<G, VEC>(rs, msg_off(p, (int)(u - p.first_row)), lane, row);
+#pragma unroll
+            for (int j = 0; j < VEC; j++) c[j] = f4_axpy(a, row[j], c[j]);
+        }
+        if (!piece || w.w < 0) {
+            flush_owner<G, VEC>(p, v, p.cnt[v], c, L, lane, pre, false);
+        } else {
+            const int64_t slot = (int64_t)w.w - p.long_base;
+            float* crow = p.carry + slot * p.d_o;
+#pragma unroll
+            for (int j = 0; j < VEC; j++) {
+                const int col = (j * G + lane) * 4;
+                if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
+            }
+            if (lane == 0) p.carry_cnt[slot] = L;
+        }
+        return;
+    }
+    const int64_t r = t - nshort - npiece;
+    if (r >= p.rows) return;
+    const int64_t v = p.first_row + r;
+    if (p.has_own[v] & OWN_SEGMENT) return;
+    const float a = expf(gat_score(q, v, v) - q.m[v]) / q.S[v];
+    gather_row<G, VEC>(rs, msg_off(p, (int)r), lane, row);
+#pragma unroll
+    for (int j = 0; j < VEC; j++) c[j] = f4_scale(a, row[j]);
+    flush_owner<G, VEC>(p, (int)v, p.cnt[v], c, 1, lane, pre, false);
+}
+
+static void dispatch_gat_aggregate(const ScatterShape& sh, const ScatterParams& p, const ChunkUnits& cu,
+                                   const GatParams& q, int64_t nshort, hipStream_t s) {
+    const int64_t work = nshort + cu.n[NCLASS] + p.rows;
+#define TAURUS_CASE(g, v)                                                                              \
+    if (sh.G == g && sh.VEC == v) {                                                                    \
+        k_gat_aggregate<g, v><<<(unsigned)ceil_div(work, SC_THREADS / g), SC_THREADS, 0, s>>>(p, cu, q, \
+                                                                                              nshort); \
+        TAURUS_CHECK_LAUNCH();                                                                         \
+        return;                                                                                        \
+    }
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
+}
+
+}  // namespace taurus
+
 // ------------------------------------------------------------- handles -----
 
 struct taurus_plan {
@@ -1346,6 +1574,12 @@ struct taurus_layer {
     float* carry = nullptr;
     int32_t* carry_cnt = nullptr;
     uint64_t* mask = nullptr;
+    float* gat_hp = nullptr;     // GAT: h' of every vertex, then s, t ([n][ncols])
+    float* gat_m = nullptr;      // GAT: per-destination largest score
+    float* gat_s = nullptr;      // GAT: per-destination sum of exp(score - max)
+    float* gat_carry = nullptr;  // GAT: per hub piece {max, sum}
+    const float* gat_attn = nullptr;  // GAT: a_src then a_dst on the device
+    bool gat_done = false;       // GAT: passes 2 and 3 have run
     void* wpack_any = nullptr;  // packed weights (fp32 or 16-bit fragments)
     void* out_dev = nullptr;    // desc.out as kernels address it
     std::unique_ptr<taurus::Residency> res;  // accumulator pool under a budget (null: dense rows)
@@ -1411,8 +1645,12 @@ namespace taurus {
 
 static void validate_desc(const taurus_layer_desc* d) {
     if (!d) fail(TAURUS_E_INVALID, "null descriptor");
-    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM && d->agg != TAURUS_GIN_SUM)
+    if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM && d->agg != TAURUS_GIN_SUM &&
+        d->agg != TAURUS_GAT_ATT)
         fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
+    if (d->agg == TAURUS_GAT_ATT && !d->attn) fail(TAURUS_E_INVALID, "a GAT layer needs its attention vectors");
+    if (d->agg == TAURUS_GAT_ATT && d->hbm_budget != 0)
+        fail(TAURUS_E_INVALID, "GAT layers run in core (hbm_budget must be 0)");
     if (d->d_in <= 0 || d->d_out <= 0 || d->d_in % 4 || d->d_out % 4 || d->d_out > 1024 || d->d_in > 8192)
         fail(TAURUS_E_INVALID, "d_in=%d d_out=%d: widths must be positive multiples of 4, d_out <= 1024",
              d->d_in, d->d_out);
@@ -1447,7 +1685,9 @@ static void layer_init(taurus_layer* L) {
     L->C = C;
     L->nchunks = ceil_div(n, C);
     L->d_o = d.d_out;
-    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.d_out;
+    // GraphSAGE: [W_agg | W_self]; GAT: W and the two attention columns,
+    // padded to a multiple of 4
+    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.agg == TAURUS_GAT_ATT ? d.d_out + 4 : d.d_out;
     L->shape = scatter_shape(L->d_o);
     L->shape.max_blocks = scatter_resident_blocks(L->shape) * std::max(1, env_int("TAURUS_SCATTER_WAVES", 1));
     const int T = 256;
@@ -1505,23 +1745,37 @@ static void layer_init(taurus_layer* L) {
     std::vector<float> packed32;
     std::vector<uint16_t> packed16;
     size_t wbytes = 0;
+    const float* wsrc = d.weight;
+    std::vector<float> wext;
+    if (d.agg == TAURUS_GAT_ATT) {
+        // [W^T | 0 0 0 0]: the four extra columns of h' (the two attention
+        // terms and padding) are filled after the transform
+        wext.assign((size_t)d.d_in * L->ncols, 0.0f);
+        for (int i = 0; i < d.d_in; i++)
+            for (int o = 0; o < d.d_out; o++) wext[(size_t)i * L->ncols + o] = d.weight[(size_t)i * d.d_out + o];
+        wsrc = wext.data();
+    }
     if (d.in_dtype == TAURUS_F32) {
-        gemm_pack_weights_f32(d.weight, d.d_in, L->ncols, packed32);
+        gemm_pack_weights_f32(wsrc, d.d_in, L->ncols, packed32);
         wbytes = packed32.size() * 4;
     } else {
-        gemm_pack_weights_16(d.weight, d.d_in, L->ncols, d.in_dtype, packed16);
+        gemm_pack_weights_16(wsrc, d.d_in, L->ncols, d.in_dtype, packed16);
         wbytes = packed16.size() * 2;
     }
     wbytes = (wbytes + 255) / 256 * 256;
-    const size_t pbytes = wbytes + (size_t)L->d_o * 4;
+    // bias, then (GAT) the attention vectors a_src, a_dst
+    const int nattn = d.agg == TAURUS_GAT_ATT ? 2 * L->d_o : 0;
+    const size_t pbytes = wbytes + (size_t)(L->d_o + nattn) * 4;
     char* stage = static_cast<char*>(pinned_staging(pbytes));
     if (!packed32.empty()) std::memcpy(stage, packed32.data(), packed32.size() * 4);
     if (!packed16.empty()) std::memcpy(stage, packed16.data(), packed16.size() * 2);
     float* sbias = reinterpret_cast<float*>(stage + wbytes);
     for (int j = 0; j < L->d_o; j++) sbias[j] = d.bias ? d.bias[j] : 0.0f;
+    for (int j = 0; j < nattn; j++) sbias[L->d_o + j] = d.attn[j];
     L->wpack_any = L->arena.alloc_bytes((int64_t)pbytes, "packed weights and bias");
     L->wpack = static_cast<float*>(L->wpack_any);
     L->bias = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + wbytes);
+    if (nattn) L->gat_attn = L->bias + L->d_o;
     TAURUS_HIP(hipMemcpyAsync(L->wpack_any, stage, pbytes, hipMemcpyHostToDevice, s));
 
     // output as kernels address it: device memory, or pinned host memory
@@ -1539,7 +1793,15 @@ static void layer_init(taurus_layer* L) {
     // the scatter addresses Y with 32-bit byte offsets
     if (std::min<int64_t>(C, n) * (int64_t)L->ncols * 4 > (int64_t)0x7f000000)
         fail(TAURUS_E_INVALID, "chunk %lld x %d transform columns exceeds 2 GiB of fp32", (long long)C, L->ncols);
-    L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
+    if (d.agg == TAURUS_GAT_ATT) {
+        L->gat_hp = L->arena.alloc<float>(n * (int64_t)L->ncols, "GAT transformed rows and scores");
+        L->gat_m = L->arena.alloc<float>(n, "GAT largest scores");
+        L->gat_s = L->arena.alloc<float>(n, "GAT score sums");
+        fill_i32(reinterpret_cast<int32_t*>(L->gat_s), n, 0, s);
+        L->gat_carry = L->arena.alloc<float>(2 * std::max<int64_t>(1, idx.max_long_per_chunk), "GAT piece statistics");
+    } else {
+        L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
+    }
     const int64_t carry_rows = std::max<int64_t>(1, idx.max_long_per_chunk);
     L->carry = L->arena.alloc<float>(carry_rows * L->d_o, "hub piece carries");
     L->carry_cnt = L->arena.alloc<int32_t>(carry_rows, "hub piece counts");
@@ -1650,13 +1912,22 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
         L->res->prepare(rc, (int32_t)k, L->cnt, s);
     }
     const float* rscale = L->n_out ? L->n_out + b : nullptr;
+    // GAT: the first pass only, into the layer's table of transformed rows
+    float* ydst = L->gat_hp ? L->gat_hp + b * (int64_t)L->ncols : L->Y;
     if (L->d.in_dtype == TAURUS_F32)
-        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, L->Y, s);
+        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, ydst, s);
     else
         gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
-                static_cast<const uint16_t*>(L->wpack_any), L->ncols, rscale, L->Y, s);
+                static_cast<const uint16_t*>(L->wpack_any), L->ncols, rscale, ydst, s);
     if (x_on_host) TAURUS_HIP(hipEventRecord(L->gemm_done[(L->host_pushes - 1) & 1], s));
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
+    if (L->gat_hp) {  // the attention terms of the chunk's rows; passes 2 and 3 run at finalize
+        k_gat_scores<<<(unsigned)ceil_div(e - b, 4), 256, 0, s>>>(ydst, e - b, L->ncols, L->d_o, L->gat_attn);
+        TAURUS_CHECK_LAUNCH();
+        if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
+        if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
+        return;
+    }
     ScatterParams p;
     p.Y = L->Y;
     p.ystride = L->ncols;
@@ -1691,10 +1962,90 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     if (L->res) L->res->release(rc, L->cnt, s);
 }
 
+// GAT passes 2 (softmax statistics) and 3 (aggregation) over every chunk,
+// in chunk order, once all chunks are transformed
+static void run_gat_passes(taurus_layer* L) {
+    hipStream_t s = L->s;
+    const ChunkIndex& idx = *L->idx;
+    GatParams q;
+    q.hp = L->gat_hp;
+    q.ystride = L->ncols;
+    q.d_o = L->d_o;
+    q.m = L->gat_m;
+    q.S = L->gat_s;
+    q.scarry = L->gat_carry;
+    auto params = [&](int64_t k) {
+        const int64_t b = k * L->C, e = std::min(b + L->C, L->n);
+        ScatterParams p{};
+        p.Y = L->gat_hp + b * (int64_t)L->ncols;
+        p.ystride = L->ncols;
+        p.self_col = 0;
+        p.y_bytes = (int)((e - b) * (int64_t)L->ncols * 4);
+        p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
+        p.has_own = idx.has_own;
+        p.cnt = L->cnt;
+        p.acc = L->acc;
+        p.slot = nullptr;
+        p.d_o = L->d_o;
+        p.agg = L->d.agg;
+        p.relu = L->d.relu;
+        p.out_dtype = L->d.out_dtype;
+        p.bias = L->bias;
+        p.out = L->out_dev;
+        p.carry = L->carry;
+        p.carry_cnt = L->carry_cnt;
+        p.long_base = idx.list_off[NCLASS][(size_t)k];
+        p.first_row = b;
+        p.rows = e - b;
+        return p;
+    };
+    auto units = [&](int64_t k, int64_t& nshort) {
+        ChunkUnits cu{};
+        nshort = 0;
+        for (int l = 0; l <= NCLASS; l++) {
+            cu.u[l] = idx.list_at(l, k);
+            cu.n[l] = idx.list_count(l, k);
+            if (l < NCLASS) nshort += cu.n[l];
+        }
+        return cu;
+    };
+    const int T = 256;
+    for (int64_t k = 0; k < L->nchunks; k++) {
+        const ScatterParams p = params(k);
+        int64_t nshort = 0;
+        const ChunkUnits cu = units(k, nshort);
+        if (nshort > 0) {
+            k_gat_stats_short<<<(unsigned)ceil_div(nshort, T), T, 0, s>>>(p, cu, q, nshort);
+            TAURUS_CHECK_LAUNCH();
+        }
+        if (cu.n[NCLASS] > 0) {
+            k_gat_stats_pieces<<<(unsigned)ceil_div(cu.n[NCLASS], T / 64), T, 0, s>>>(p, cu.u[NCLASS], cu.n[NCLASS], q);
+            TAURUS_CHECK_LAUNCH();
+        }
+        k_gat_stats_self<<<(unsigned)ceil_div(p.rows, T), T, 0, s>>>(p, q);
+        TAURUS_CHECK_LAUNCH();
+        const int64_t nfix = idx.list_count(NCLASS + 1, k);
+        if (nfix > 0) {
+            k_gat_stats_fixup<<<(unsigned)ceil_div(nfix, T), T, 0, s>>>(p, idx.list_at(NCLASS + 1, k), nfix, q);
+            TAURUS_CHECK_LAUNCH();
+        }
+    }
+    for (int64_t k = 0; k < L->nchunks; k++) {
+        const ScatterParams p = params(k);
+        int64_t nshort = 0;
+        const ChunkUnits cu = units(k, nshort);
+        dispatch_gat_aggregate(L->shape, p, cu, q, nshort, s);
+        const int64_t nfix = idx.list_count(NCLASS + 1, k);
+        if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
+    }
+    L->gat_done = true;
+}
+
 static int finalize(taurus_layer* L, taurus_stats* st) {
     if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
     hipStream_t s = L->s;
     const ChunkIndex& idx = *L->idx;
+    if (L->gat_hp && !L->gat_done && L->npushed == L->nchunks) run_gat_passes(L);
     Arena tmp(s);
     unsigned long long* dleft = tmp.alloc<unsigned long long>(1, "pending count");
     fill_i32(reinterpret_cast<int32_t*>(dleft), 2, 0, s);

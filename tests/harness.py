@@ -43,7 +43,8 @@ def layer_specs(w: WL.Workload, fanouts=None):
         in_dt, out_dt = w.layer_dtypes(li)
         specs.append(dict(agg=w.agg, d_in=p.d_in, d_out=p.d_out, weight_cat=p.weight_cat(), bias=p.b,
                           in_dtype=in_dt, out_dtype=out_dt, relu=li < w.layers,
-                          fanout=(fanouts[li - 1] if fanouts else w.fanout(li)), layer=li, seed=w.seed))
+                          fanout=(fanouts[li - 1] if fanouts else w.fanout(li)), layer=li, seed=w.seed,
+                          attn=p.attn))
     return specs
 
 

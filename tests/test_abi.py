@@ -44,7 +44,8 @@ def test_binding_structs_match_header_layout(native):
     assert native.LayerDesc.weight.offset == 24 and native.LayerDesc.seed.offset == 48
     assert native.LayerDesc.out.offset == 80 and native.LayerDesc.stream.offset == 96
     assert native.LayerDesc.plan.offset == 112 and native.LayerDesc.eviction.offset == 120
-    assert ctypes.sizeof(native.LayerDesc) == 128
+    assert native.LayerDesc.attn.offset == 128
+    assert ctypes.sizeof(native.LayerDesc) == 136
     assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 2 * 8
 
 

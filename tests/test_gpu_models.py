@@ -125,3 +125,72 @@ def test_gin_closed_form_and_unknown_family(torch_cuda):
     # vertex 0 sums 99 sources and itself: 100 * 8 per output; the others 8
     got = out.cpu().numpy()
     assert np.all(got[0] == 800.0) and np.all(got[1:] == 8.0)
+
+
+@pytest.mark.parametrize("k", [0, 5])
+def test_gat_layer_matches_oracle(torch_cuda, k):
+    """One single-head GAT layer (d 48 -> 40, bias, ReLU), exact and with
+    fanout 5, over 3,000 vertices in three chunks; the hub's segments are cut
+    into pieces, so the piece statistics and the fix-up run.  Every row
+    against the oracle."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    rng = np.random.default_rng(400 + k)
+    n, d_in, d_out, seed, layer = 3000, 48, 40, 31, 1
+    src, dst = _graph(rng, n)
+    _note(f"gat fanout {k}: n={n} e={src.size}")
+    g = O.Graph(n, src, dst)
+    X = rng.standard_normal((n, d_in)).astype(np.float32)
+    W = (rng.standard_normal((d_out, d_in)) * 0.2).astype(np.float32)
+    attn = rng.standard_normal((2, d_out)).astype(np.float32)
+    b = rng.standard_normal(d_out).astype(np.float32)
+    row_off, col_dst = T.build_csr(n, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+    out = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    L = T.Layer(n, row_off, col_dst, agg=WL.GAT_ATT, d_in=d_in, d_out=d_out, weight_cat=np.ascontiguousarray(W.T),
+                bias=b, out=out, relu=True, fanout=k, layer=layer, seed=seed, chunk=1024, attn=attn)
+    L.push_all(torch.from_numpy(X).cuda())
+    st = L.finalize()
+    L.destroy()
+    assert st["completed"] == n and (k or st["split_segments"] > 0)   # exact: the hub's segments are split
+    keep = O.sample(g, seed, layer, k)[1] if k else None
+    z = O.gat_layer(g, X, O.F32, W.astype(np.float64), attn.astype(np.float64), b.astype(np.float64), True,
+                    keep_in=keep)
+    r = H.compare(out.cpu().numpy(), z, H.RTOL[F.F32])
+    assert r["n_bad"] == 0, r
+
+
+@pytest.mark.parametrize("dtype,fanouts", [(F.F32, ()), (F.BF16, ()), (F.F32, (10, 5))])
+def test_gat_model_on_rmat(torch_cuda, dtype, fanouts):
+    """A 2-layer GAT on the RMAT recipe of the in-memory workload at 1/16,
+    8,192-vertex chunks, every row of each layer against the oracle fed its
+    own previous layer."""
+    torch = torch_cuda
+    w = dataclasses.replace(WL.GCN_RMAT_1M, agg=WL.GAT_ATT, feat_dtype=dtype, fanouts=fanouts).scaled(
+        n=1_000_000 // 16, e=20_000_000 // 16, chunk=8192, name=f"gat-rmat-1m-div16-{dtype}-{len(fanouts)}")
+    _note(w.name)
+    src, dst = WL.graph(w)
+    g, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    outs, stats = H.gpu_model(w, row_off, col_dst)
+    for li, (o, z) in enumerate(zip(outs, zs), start=1):
+        _, out_dt = w.layer_dtypes(li)
+        r = H.compare(H.to_numpy_f64(o, out_dt), z, H.RTOL[dtype])
+        _note(f"  layer {li}: {r['n_bad']} bad, max abs {r['max_abs']:.2e}")
+        assert r["n_bad"] == 0, (li, r)
+
+
+def test_gat_argument_errors(torch_cuda):
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    n = 100
+    src = np.arange(1, n, dtype=np.int32)
+    dst = np.zeros(n - 1, dtype=np.int32)
+    row_off, col_dst = T.build_csr(n, torch.from_numpy(src).cuda(), torch.from_numpy(dst).cuda())
+    out = torch.empty((n, 4), dtype=torch.float32, device="cuda")
+    base = dict(agg=WL.GAT_ATT, d_in=8, d_out=4, weight_cat=np.zeros((8, 4), np.float32), bias=None, out=out,
+                chunk=64)
+    for bad in (dict(), dict(attn=np.zeros((2, 4), np.float32), hbm_budget=1 << 30)):
+        with pytest.raises(T.TaurusError) as ex:
+            T.Layer(n, row_off, col_dst, **dict(base, **bad))
+        assert ex.value.status == -1, bad
