@@ -353,7 +353,7 @@ def main():
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
         ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
               for k in ("gemm", "scatter", "fixup", "init", "index")}
-        if profile and not sampled:
+        if profile and not sampled and agg != WL.GAT_ATT:   # GAT aggregates in its own passes
             for k in tot:
                 tot[k][0] += kb[k] * len(sts)
                 tot[k][1] += sum(s[f"ms_{k}"] for s in sts)
