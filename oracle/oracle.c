@@ -23,9 +23,17 @@
  *   - fanout sampling: up to k incoming edges kept per vertex, per layer
  *     (Sec. 3.9, "Sampling-based Inference"), ranked by a counter-based
  *     hash;
+ *   - GIN (GINConv with a linear apply function, sum aggregation) and
+ *     single-head GATConv (Sec. 3.9, "GATConv"; Sec. 4.1 evaluates both);
+ *     sampled GCN layers take the sampled graph's degrees;
  *   - the degree/BFS vertex ordering used as a topology-aware bootstrap
  *     (Sec. 3.8 discusses bandwidth-style bootstraps; the exact ordering
- *     rule is a reading of the text and is stated at or_reorder_bfs).
+ *     rule is a reading of the text and is stated at or_reorder_bfs), the
+ *     RCMK bootstrap and the topology-aware reordering of Alg. 1, with the
+ *     total span C(pi) and the chunk-level residency profile A(t) (Sec. 3.8);
+ *   - a slot-level simulation of a budgeted layer's residency with the
+ *     fewest-pending eviction policy (Sec. 3.5.3) and the random, FIFO and
+ *     LRU policies it is compared with (Sec. 4).
  *
  * Parity status: every function here is pinned by CPU tests (dense
  * adjacency-matrix products, closed forms, hand-worked small graphs,
