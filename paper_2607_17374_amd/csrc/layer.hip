@@ -397,6 +397,13 @@ struct ScatterParams {
     int64_t long_base;     // global index of the chunk's first wave unit (carry slot 0)
     int64_t first_row;     // first vertex of the chunk
     int64_t rows;          // vertices in the chunk
+    // GAT aggregation only (k_scatter<G, VEC, true>): the weight of message
+    // u -> v is exp(LeakyReLU(s_u + t_v) - m_v) / S_v, with s_u in column
+    // d_o of u's row of Y, t_v = att_t[v * ystride], m_v = att_m[v] and
+    // S_v = att_s[v]
+    const float* att_t;
+    const float* att_m;
+    const float* att_s;
 };
 
 struct ChunkUnits {        // this chunk's slice of the short classes and wave units
@@ -452,6 +459,15 @@ __device__ inline void store_out4(void* out, int dtype, int64_t idx, float4 z) {
 
 __device__ inline float* acc_row(const ScatterParams& p, int v) {
     return p.acc + (int64_t)(p.slot ? p.slot[v] : v) * p.d_o;
+}
+
+// GAT: LeakyReLU slope of the attention scores, and the attention weight of
+// the message from local row r of the chunk to v
+constexpr float ATT_SLOPE = 0.2f;
+__device__ inline float att_weight(const ScatterParams& p, int r, int v) {
+    const float e0 = p.Y[(int64_t)r * p.ystride + p.d_o] + p.att_t[(int64_t)v * p.ystride];
+    const float e = e0 > 0.f ? e0 : ATT_SLOPE * e0;
+    return expf(e - p.att_m[v]) / p.att_s[v];
 }
 
 // weight of a message slot: GraphSAGE-mean 1/|M(v)| (|M(v)| = expected - 1),
@@ -584,7 +600,7 @@ __device__ inline int rg_pick(const int (&reg)[NREG], int k) {
 // messages (weight sigma_v).  Software-pipelined: the next batch's row
 // offsets and the descriptors after it are requested while this batch's
 // rows are in flight.
-template <int G, int VEC, int LEN>
+template <int G, int VEC, int LEN, bool ATT>
 __device__ inline void short_batches(const ScatterParams& p, const int4* __restrict__ units, int64_t n, int64_t rot) {
     constexpr int SLOTS = slots_per_round(VEC);
     constexpr int K = batch_units(VEC, LEN);                                  // units per batch
@@ -616,7 +632,9 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
         }
     };
     // slot j = (unit j / LEN, position j % LEN) of the batch in lane j % G
-    auto load_offsets = [&](const int (&dx)[KD], const int (&dy)[KD], const int (&dv)[KD], uint32_t (&off)[CR]) {
+    // (with ATT, its attention weight beside it)
+    auto load_offsets = [&](const int (&dx)[KD], const int (&dy)[KD], const int (&dv)[KD], uint32_t (&off)[CR],
+                            float (&wt)[CR]) {
 #pragma unroll
         for (int q = 0; q < CR; q++) {
             const int j = q * G + lane;
@@ -630,13 +648,20 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
                 else o = msg_off(p, p.src[x + i - self]);
             }
             off[q] = o;
+            if constexpr (ATT) {
+                float a = 0.f;
+                if (j < TS && i < slots)
+                    a = att_weight(p, (self && i == 0) ? (int)((int64_t)v - p.first_row) : p.src[x + i - self], v);
+                wt[q] = a;
+            }
         }
     };
 
     int dx[KD], dy[KD], dv[KD];
     uint32_t off[CR];
+    float wt[CR];
     load_desc(b, dx, dy, dv);
-    load_offsets(dx, dy, dv, off);
+    load_offsets(dx, dy, dv, off, wt);
     int64_t b1 = b + stride;
     int nx[KD], ny[KD], nv[KD];
     load_desc(b1, nx, ny, nv);
@@ -647,6 +672,11 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
         uint32_t so[TS];
 #pragma unroll
         for (int j = 0; j < TS; j++) so[j] = (uint32_t)__shfl((int)off[j / G], j % G, G);
+        float sw[TS];
+        if constexpr (ATT) {
+#pragma unroll
+            for (int j = 0; j < TS; j++) sw[j] = __shfl(wt[j / G], j % G, G);
+        }
 #pragma unroll
         for (int j = 0; j < RB; j++) gather_row<G, VEC>(rs, so[j], lane, rows[j]);
         int2 pe_l[KD];
@@ -663,9 +693,13 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
         // next batch's row offsets, and the descriptors of the one after
         const bool more = b1 < nb;
         uint32_t noff[CR];
+        float nwt[CR];
 #pragma unroll
-        for (int q = 0; q < CR; q++) noff[q] = NO_ROW;
-        if (more) load_offsets(nx, ny, nv, noff);
+        for (int q = 0; q < CR; q++) {
+            noff[q] = NO_ROW;
+            nwt[q] = 0.f;
+        }
+        if (more) load_offsets(nx, ny, nv, noff, nwt);
         const int64_t b2 = b1 + stride;
         int mx[KD], my[KD], mv[KD];
         load_desc(b2, mx, my, mv);
@@ -676,7 +710,8 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
             pe.x = __shfl(pe_l[k / G].x, k % G, G);
             pe.y = __shfl(pe_l[k / G].y, k % G, G);
             const float sig = seg_scale(p.agg, pe.y);
-            const float w0 = (uy[k] & SELF_HERE) ? 1.0f : sig;  // slot 0: own row or a message
+            float w0 = (uy[k] & SELF_HERE) ? 1.0f : sig;  // slot 0: own row or a message
+            if constexpr (ATT) w0 = sw[k * LEN];
             float4 sa[VEC], c[VEC];
 #pragma unroll
             for (int jv = 0; jv < VEC; jv++) {
@@ -690,12 +725,19 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
 #pragma unroll
                     for (int jj = 0; jj < RB; jj++) gather_row<G, VEC>(rs, so[j + jj], lane, rows[jj]);
                 }
+                if constexpr (ATT) {
 #pragma unroll
-                for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_add(sa[jv], rows[j % RB][jv]);
+                    for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sw[j], rows[j % RB][jv], c[jv]);
+                } else {
+#pragma unroll
+                    for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_add(sa[jv], rows[j % RB][jv]);
+                }
             }
             if (uv[k] < 0) continue;
+            if constexpr (!ATT) {
 #pragma unroll
-            for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], c[jv]);
+                for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], c[jv]);
+            }
             flush_owner<G, VEC>(p, uv[k], pe, c, uy[k] & LEN_MASK, lane, pre[k], (uy[k] & NOT_FIRST) != 0);
         }
         if (!more) break;
@@ -707,7 +749,10 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
             nx[q] = mx[q]; ny[q] = my[q]; nv[q] = mv[q];
         }
 #pragma unroll
-        for (int q = 0; q < CR; q++) off[q] = noff[q];
+        for (int q = 0; q < CR; q++) {
+            off[q] = noff[q];
+            wt[q] = nwt[q];
+        }
     }
 }
 
@@ -721,7 +766,7 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
 // shuffles and row-group 0 flushes (or parks the partial row of a hub piece
 // in its carry slot).  The next piece's descriptor is fetched ahead and its
 // offsets are requested while the first round's rows are in flight.
-template <int G, int VEC>
+template <int G, int VEC, bool ATT>
 __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
     constexpr int SLOTS = slots_per_round(VEC);
     constexpr int NREG = PIECE_LEN / 64;
@@ -731,17 +776,19 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
     int64_t un = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave;
     if (un >= n) return;  // the whole wave
     const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
-    auto load_offsets = [&](int4 w, uint32_t (&cr)[NREG]) {
+    auto load_offsets = [&](int4 w, uint32_t (&cr)[NREG], float (&wt)[NREG]) {
         const int items = (w.y & LEN_MASK) - ((w.y & SELF_HERE) ? 1 : 0);
 #pragma unroll
         for (int t = 0; t < NREG; t++) {
             const int i = t * 64 + l64;
             cr[t] = i < items ? msg_off(p, p.src[w.x + i]) : NO_ROW;
+            if constexpr (ATT) wt[t] = i < items ? att_weight(p, p.src[w.x + i], w.z) : 0.f;
         }
     };
     int4 w = units[un];
     uint32_t cr[NREG];
-    load_offsets(w, cr);
+    float wt[NREG];
+    load_offsets(w, cr, wt);
     int64_t un1 = un + wstride;
     int4 wn = un1 < n ? units[un1] : make_int4(0, 0, 0, 0);
     for (;;) {
@@ -756,20 +803,28 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
         gather_row<G, VEC>(rs, self && rg == 0 ? self_off(p, (int)((int64_t)v - p.first_row)) : NO_ROW, lane, srow);
         const bool more = un1 < n;
         uint32_t ncr[NREG];
+        float nwt[NREG];
 #pragma unroll
-        for (int t = 0; t < NREG; t++) ncr[t] = NO_ROW;
+        for (int t = 0; t < NREG; t++) {
+            ncr[t] = NO_ROW;
+            nwt[t] = 0.f;
+        }
         float4 sa[VEC];
 #pragma unroll
         for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_zero();
         // one round: SLOTS row offsets of this row-group -> rows -> sum
-        auto round = [&](const uint32_t (&o)[SLOTS]) {
+        // (with ATT, each row times its weight ow[k])
+        auto round = [&](const uint32_t (&o)[SLOTS], const float (&ow)[SLOTS]) {
             float4 rows[SLOTS][VEC];
 #pragma unroll
             for (int k = 0; k < SLOTS; k++) gather_row<G, VEC>(rs, o[k], lane, rows[k]);
 #pragma unroll
             for (int k = 0; k < SLOTS; k++)
 #pragma unroll
-                for (int jv = 0; jv < VEC; jv++) sa[jv] = f4_add(sa[jv], rows[k][jv]);
+                for (int jv = 0; jv < VEC; jv++) {
+                    if constexpr (ATT) sa[jv] = f4_axpy(ow[k], rows[k][jv], sa[jv]);
+                    else sa[jv] = f4_add(sa[jv], rows[k][jv]);
+                }
         };
         const int nreg = (items + 63) / 64;
         bool first = true;
@@ -779,13 +834,20 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
             constexpr int M = SLOTS / G;
             for (int r = 0; r < nreg; r += M) {
                 uint32_t o[SLOTS];
+                float ow[SLOTS];
 #pragma unroll
-                for (int k = 0; k < SLOTS; k++) o[k] = (uint32_t)__shfl((int)cr[k / G], G * rg + k % G, 64);
-                if (first && more) load_offsets(wn, ncr);
+                for (int k = 0; k < SLOTS; k++) {
+                    o[k] = (uint32_t)__shfl((int)cr[k / G], G * rg + k % G, 64);
+                    if constexpr (ATT) ow[k] = __shfl(wt[k / G], G * rg + k % G, 64);
+                }
+                if (first && more) load_offsets(wn, ncr, nwt);
                 first = false;
-                round(o);
+                round(o, ow);
 #pragma unroll
-                for (int t = 0; t < NREG; t++) cr[t] = t + M < NREG ? cr[t + M] : NO_ROW;
+                for (int t = 0; t < NREG; t++) {
+                    cr[t] = t + M < NREG ? cr[t + M] : NO_ROW;
+                    if constexpr (ATT) wt[t] = t + M < NREG ? wt[t + M] : 0.f;
+                }
             }
         } else {
             // a register takes G / SLOTS rounds: slot k of row-group rg in
@@ -795,23 +857,37 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
 #pragma unroll 1
                 for (int h = 0; h < H; h++) {
                     uint32_t o[SLOTS];
+                    float ow[SLOTS];
 #pragma unroll
-                    for (int k = 0; k < SLOTS; k++) o[k] = (uint32_t)__shfl((int)cr[0], G * rg + SLOTS * h + k, 64);
-                    if (first && more) load_offsets(wn, ncr);
+                    for (int k = 0; k < SLOTS; k++) {
+                        o[k] = (uint32_t)__shfl((int)cr[0], G * rg + SLOTS * h + k, 64);
+                        if constexpr (ATT) ow[k] = __shfl(wt[0], G * rg + SLOTS * h + k, 64);
+                    }
+                    if (first && more) load_offsets(wn, ncr, nwt);
                     first = false;
-                    round(o);
+                    round(o, ow);
                 }
 #pragma unroll
-                for (int t = 0; t < NREG; t++) cr[t] = t + 1 < NREG ? cr[t + 1] : NO_ROW;
+                for (int t = 0; t < NREG; t++) {
+                    cr[t] = t + 1 < NREG ? cr[t + 1] : NO_ROW;
+                    if constexpr (ATT) wt[t] = t + 1 < NREG ? wt[t + 1] : 0.f;
+                }
             }
         }
-        if (first && more) load_offsets(wn, ncr);
+        if (first && more) load_offsets(wn, ncr, nwt);
         const int64_t un2 = un1 + wstride;
         const int4 wn2 = un2 < n ? units[un2] : make_int4(0, 0, 0, 0);
-        const float sig = seg_scale(p.agg, pe.y);
         float4 c[VEC];
+        if constexpr (ATT) {
+            // the self row (zeros unless SELF_HERE) times its attention
+            const float as = self ? att_weight(p, (int)((int64_t)v - p.first_row), v) : 0.f;
 #pragma unroll
-        for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], srow[jv]);
+            for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(as, srow[jv], sa[jv]);
+        } else {
+            const float sig = seg_scale(p.agg, pe.y);
+#pragma unroll
+            for (int jv = 0; jv < VEC; jv++) c[jv] = f4_axpy(sig, sa[jv], srow[jv]);
+        }
 #pragma unroll
         for (int d = G; d < 64; d <<= 1)
 #pragma unroll
@@ -840,7 +916,10 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
         wn = wn2;
         un1 = un2;
 #pragma unroll
-        for (int t = 0; t < NREG; t++) cr[t] = ncr[t];
+        for (int t = 0; t < NREG; t++) {
+            cr[t] = ncr[t];
+            wt[t] = nwt[t];
+        }
     }
 }
 
@@ -849,7 +928,7 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
 // arrival each.  A row-group takes K consecutive vertices at a time --
 // consecutive rows of Y and of the accumulators.  These vertices have no
 // other flush in the launch.
-template <int G, int VEC>
+template <int G, int VEC, bool ATT>
 __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
     constexpr int K = self_batch_rows(VEC);
     constexpr int KD = (K + G - 1) / G;
@@ -887,6 +966,11 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
             int2 pe;
             pe.x = __shfl(pe_l[k / G].x, k % G, G);
             pe.y = __shfl(pe_l[k / G].y, k % G, G);
+            if constexpr (ATT) {
+                const float as = att_weight(p, (int)(r0 + k), (int)(p.first_row + r0 + k));
+#pragma unroll
+                for (int jv = 0; jv < VEC; jv++) rows[k][jv] = f4_scale(as, rows[k][jv]);
+            }
             flush_owner<G, VEC>(p, (int)(p.first_row + r0 + k), pe, rows[k], 1, lane, pre[k],
                                 !(f[k] & SELF_FIRST));
         }
@@ -896,16 +980,17 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
 // Degree-bucketed scatter of one chunk, persistent: the grid is sized to
 // what the GPU holds at once and walks the wave pieces (longest work
 // first), the short classes from long to short, then the self pass.
-template <int G, int VEC>
+// ATT: GAT's aggregation pass, every slot weighted by its attention.
+template <int G, int VEC, bool ATT = false>
 __global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
 void k_scatter(ScatterParams p, ChunkUnits cu) {
-    wave_pieces<G, VEC>(p, cu.u[NCLASS], cu.n[NCLASS]);
-    short_batches<G, VEC, 16>(p, cu.u[4], cu.n[4], cu.rot[4]);
-    short_batches<G, VEC, 8>(p, cu.u[3], cu.n[3], cu.rot[3]);
-    short_batches<G, VEC, 4>(p, cu.u[2], cu.n[2], cu.rot[2]);
-    short_batches<G, VEC, 2>(p, cu.u[1], cu.n[1], cu.rot[1]);
-    short_batches<G, VEC, 1>(p, cu.u[0], cu.n[0], cu.rot[0]);
-    self_batches<G, VEC>(p, cu.rot[NCLASS]);
+    wave_pieces<G, VEC, ATT>(p, cu.u[NCLASS], cu.n[NCLASS]);
+    short_batches<G, VEC, 16, ATT>(p, cu.u[4], cu.n[4], cu.rot[4]);
+    short_batches<G, VEC, 8, ATT>(p, cu.u[3], cu.n[3], cu.rot[3]);
+    short_batches<G, VEC, 4, ATT>(p, cu.u[2], cu.n[2], cu.rot[2]);
+    short_batches<G, VEC, 2, ATT>(p, cu.u[1], cu.n[1], cu.rot[1]);
+    short_batches<G, VEC, 1, ATT>(p, cu.u[0], cu.n[0], cu.rot[0]);
+    self_batches<G, VEC, ATT>(p, cu.rot[NCLASS]);
 }
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
@@ -983,7 +1068,8 @@ static ScatterShape scatter_shape(int d_o) {
 // the shapes scatter_shape() yields for widths 4..1024
 #define TAURUS_ROW_SHAPES(X) X(4, 1) X(4, 2) X(8, 2) X(16, 2) X(32, 2) X(64, 2) X(64, 4)
 
-static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, ChunkUnits cu, hipStream_t s) {
+static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, ChunkUnits cu, hipStream_t s,
+                             bool att = false) {
     const int nrg = SC_THREADS / sh.G;
     // the row-group sequence: wave pieces' row-groups, then the short
     // classes from the longest, then the self pass
@@ -997,7 +1083,8 @@ static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, Chu
     const int64_t blocks = std::max<int64_t>(1, std::min(ceil_div(t, nrg), sh.max_blocks));
 #define TAURUS_CASE(g, v)                                                         \
     if (sh.G == g && sh.VEC == v) {                                               \
-        k_scatter<g, v><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu);           \
+        if (att) k_scatter<g, v, true><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu); \
+        else k_scatter<g, v><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu);      \
         TAURUS_CHECK_LAUNCH();                                                    \
         return;                                                                   \
     }
@@ -1329,10 +1416,11 @@ namespace taurus {
 //      own (max, sum) into the destination's as the sole owner, hub pieces
 //      through per-piece scalar carries merged in piece order, so the
 //      result is deterministic;
-//   3. aggregation: the chunks of h' are streamed again and every message
-//      adds alpha_uv h'_u with alpha_uv = exp(e_uv - m_v) / S_v, through the
-//      sole-owner flush and fix-up of the other families.
-constexpr float GAT_SLOPE = 0.2f;
+//   3. aggregation: the chunks of h' are streamed again through the
+//      scatter kernel of the other families (k_scatter<G, VEC, true>): every
+//      message adds alpha_uv h'_u with alpha_uv = exp(e_uv - m_v) / S_v,
+//      then the sole-owner flush and fix-up.
+constexpr float GAT_SLOPE = ATT_SLOPE;
 
 struct GatParams {
     const float* hp;  // [n][ystride]: h' then s, t
@@ -1474,71 +1562,6 @@ __global__ void k_gat_stats_fixup(ScatterParams p, const int4* __restrict__ fix,
     for (int j = 0; j < f.z; j++) gat_merge(m, S, q.scarry[2 * (first + j)], q.scarry[2 * (first + j) + 1]);
     q.m[v] = m;
     q.S[v] = S;
-}
-
-// pass 3: one row-group per unit (the short classes, then the wave pieces,
-// then the self pass); every slot's row of h' weighted by its attention
-template <int G, int VEC>
-__global__ __launch_bounds__(SC_THREADS) void k_gat_aggregate(ScatterParams p, ChunkUnits cu, GatParams q,
-                                                              int64_t nshort) {
-    constexpr int NRG = SC_THREADS / G;
-    const int rg = threadIdx.x / G, lane = threadIdx.x % G;
-    const int64_t t = (int64_t)blockIdx.x * NRG + rg;
-    const int64_t npiece = cu.n[NCLASS];
-    const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
-    float4 c[VEC], pre[VEC], row[VEC];
-#pragma unroll
-    for (int j = 0; j < VEC; j++) c[j] = pre[j] = f4_zero();
-    if (t < nshort + npiece) {
-        const bool piece = t >= nshort;
-        const int4 w = piece ? cu.u[NCLASS][t - nshort] : short_unit(cu, t);
-        const int v = w.z, L = w.y & LEN_MASK;
-        const float tv_m = q.m[v], inv_s = 1.f / q.S[v];
-        for (int i = 0; i < L; i++) {
-            const int64_t u = piece ? piece_slot_src(p, w, i) : short_slot_src(p, w, i);
-            const float a = expf(gat_score(q, u, v) - tv_m) * inv_s;
-            gather_row<G, VEC>(rs, msg_off(p, (int)(u - p.first_row)), lane, row);
-#pragma unroll
-            for (int j = 0; j < VEC; j++) c[j] = f4_axpy(a, row[j], c[j]);
-        }
-        if (!piece || w.w < 0) {
-            flush_owner<G, VEC>(p, v, p.cnt[v], c, L, lane, pre, false);
-        } else {
-            const int64_t slot = (int64_t)w.w - p.long_base;
-            float* crow = p.carry + slot * p.d_o;
-#pragma unroll
-            for (int j = 0; j < VEC; j++) {
-                const int col = (j * G + lane) * 4;
-                if (col < p.d_o) *reinterpret_cast<float4*>(crow + col) = c[j];
-            }
-            if (lane == 0) p.carry_cnt[slot] = L;
-        }
-        return;
-    }
-    const int64_t r = t - nshort - npiece;
-    if (r >= p.rows) return;
-    const int64_t v = p.first_row + r;
-    if (p.has_own[v] & OWN_SEGMENT) return;
-    const float a = expf(gat_score(q, v, v) - q.m[v]) / q.S[v];
-    gather_row<G, VEC>(rs, msg_off(p, (int)r), lane, row);
-#pragma unroll
-    for (int j = 0; j < VEC; j++) c[j] = f4_scale(a, row[j]);
-    flush_owner<G, VEC>(p, (int)v, p.cnt[v], c, 1, lane, pre, false);
-}
-
-static void dispatch_gat_aggregate(const ScatterShape& sh, const ScatterParams& p, const ChunkUnits& cu,
-                                   const GatParams& q, int64_t nshort, hipStream_t s) {
-    const int64_t work = nshort + cu.n[NCLASS] + p.rows;
-#define TAURUS_CASE(g, v)                                                                              \
-    if (sh.G == g && sh.VEC == v) {                                                                    \
-        k_gat_aggregate<g, v><<<(unsigned)ceil_div(work, SC_THREADS / g), SC_THREADS, 0, s>>>(p, cu, q, \
-                                                                                              nshort); \
-        TAURUS_CHECK_LAUNCH();                                                                         \
-        return;                                                                                        \
-    }
-    TAURUS_ROW_SHAPES(TAURUS_CASE)
-#undef TAURUS_CASE
-    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
 }
 
 }  // namespace taurus
@@ -1928,7 +1951,7 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
         if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
         return;
     }
-    ScatterParams p;
+    ScatterParams p{};
     p.Y = L->Y;
     p.ystride = L->ncols;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
@@ -1997,6 +2020,9 @@ static void run_gat_passes(taurus_layer* L) {
         p.long_base = idx.list_off[NCLASS][(size_t)k];
         p.first_row = b;
         p.rows = e - b;
+        p.att_t = L->gat_hp + L->d_o + 1;
+        p.att_m = L->gat_m;
+        p.att_s = L->gat_s;
         return p;
     };
     auto units = [&](int64_t k, int64_t& nshort) {
@@ -2034,7 +2060,7 @@ static void run_gat_passes(taurus_layer* L) {
         const ScatterParams p = params(k);
         int64_t nshort = 0;
         const ChunkUnits cu = units(k, nshort);
-        dispatch_gat_aggregate(L->shape, p, cu, q, nshort, s);
+        dispatch_scatter(L->shape, p, cu, s, true);
         const int64_t nfix = idx.list_count(NCLASS + 1, k);
         if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
     }
