@@ -50,8 +50,12 @@ void device_release(void* p, hipStream_t s);
 size_t release_cached(size_t bytes);
 
 // Pinned host buffer of at least `bytes` for the calling thread (reused by
-// its next call).
+// its next call, which first waits for a transfer left in flight by
+// pinned_staging_in_flight).
 void* pinned_staging(size_t bytes);
+// The thread's staging buffer is read by a transfer enqueued on s: the next
+// pinned_staging call waits for it instead of the caller synchronising now.
+void pinned_staging_in_flight(hipStream_t s);
 
 // Small device-to-host reads gathered into one pinned transfer and one
 // stream synchronisation: add() any number, then run().

@@ -113,11 +113,10 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 }
 
 // Chunk-index items.  CSR edge i (source u = the row containing i) becomes
-// key (chunk(u) << vbits | v), value u - chunk(u)*C; a dropped edge gets
-// chunk = nchunks so it sorts after every kept item.
-// Every CSR edge is checked; a propagated one (all of them when mask is
-// null) writes its item at its position among the propagated edges
-// (word_off[w] = propagated edges before mask word w).
+// key (chunk(u) << vbits | v), value u - chunk(u)*C.  Every CSR edge is
+// checked; only a propagated one (all of them when mask is null) writes its
+// item, at its position among the propagated edges (word_off[w] =
+// propagated edges before mask word w).
 __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
                                                     const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
                                                     int64_t C, int vbits, const uint64_t* __restrict__ mask,
@@ -1235,7 +1234,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     // from binary searches and thread ids only); the flags are checked before
     // any kernel indexes by destination.
     const int vbits = std::max(1, bits_for(n - 1));
-    const int cbits = bits_for(nch);
+    const int cbits = bits_for(nch - 1);  // chunk numbers 0 .. nch - 1
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
     SortBuffers sb{{tmp.alloc<uint64_t>(items1, "index keys"), tmp.alloc<uint64_t>(items1, "index keys (ping-pong)")},
                    {tmp.alloc<uint32_t>(items1, "index values"),
@@ -1764,7 +1763,7 @@ static void layer_init(taurus_layer* L) {
     }
 
     // packed weights and bias, one transfer through pinned staging (the
-    // synchronisation at the end keeps the staging buffer until it is done)
+    // staging buffer's next user waits for it)
     std::vector<float> packed32;
     std::vector<uint16_t> packed16;
     size_t wbytes = 0;
@@ -1800,6 +1799,7 @@ static void layer_init(taurus_layer* L) {
     L->bias = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + wbytes);
     if (nattn) L->gat_attn = L->bias + L->d_o;
     TAURUS_HIP(hipMemcpyAsync(L->wpack_any, stage, pbytes, hipMemcpyHostToDevice, s));
+    pinned_staging_in_flight(s);
 
     // output as kernels address it: device memory, or pinned host memory
     // mapped into the device's address space
@@ -1863,8 +1863,7 @@ static void layer_init(taurus_layer* L) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
     }
-    TAURUS_HIP(hipStreamSynchronize(s));
-    L->ms_init = ms_since(t_start);
+    L->ms_init = ms_since(t_start);  // host time; the work stays queued on the stream
 }
 
 // Host-resident chunk (pinned): copy it on the layer's copy stream into one

@@ -216,19 +216,40 @@ void device_release(void* p, hipStream_t s) {
 
 // ------------------------------------------------------------ pinned staging --
 // One pinned host buffer per host thread for small transfers, grown on demand
-// and kept until the process ends.
+// and kept until the process ends.  An asynchronous transfer still reading
+// it is tracked by one event.
+namespace {
+struct Staging {
+    void* buf = nullptr;
+    size_t cap = 0;
+    hipEvent_t busy = nullptr;
+    bool in_flight = false;
+};
+thread_local Staging t_stage;
+}  // namespace
+
 void* pinned_staging(size_t bytes) {
-    static thread_local void* buf = nullptr;
-    static thread_local size_t cap = 0;
-    if (bytes > cap) {
+    Staging& st = t_stage;
+    if (st.in_flight) {
+        TAURUS_HIP(hipEventSynchronize(st.busy));
+        st.in_flight = false;
+    }
+    if (bytes > st.cap) {
         size_t want = std::max<size_t>(bytes, 64 << 10);
         void* p = nullptr;
         TAURUS_HIP(hipHostMalloc(&p, want, hipHostMallocDefault));
-        if (buf) (void)hipHostFree(buf);
-        buf = p;
-        cap = want;
+        if (st.buf) (void)hipHostFree(st.buf);
+        st.buf = p;
+        st.cap = want;
     }
-    return buf;
+    return st.buf;
+}
+
+void pinned_staging_in_flight(hipStream_t s) {
+    Staging& st = t_stage;
+    if (!st.busy) TAURUS_HIP(hipEventCreateWithFlags(&st.busy, hipEventDisableTiming));
+    TAURUS_HIP(hipEventRecord(st.busy, s));
+    st.in_flight = true;
 }
 
 void Readback::add(void* host, const void* dev, size_t bytes) {
@@ -492,8 +513,12 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __res
 // per digit, so wave w's items of digit d follow those of waves < w, and the
 // digit's start within the tile comes from the tile histogram.  The ranked
 // tile is written to LDS in digit order and copied out: LDS slot i of digit
-// d goes to offs[d] + (i - start of d in the tile).
+// d goes to offs[d] + (i - start of d in the tile).  Values take a second
+// trip through the same LDS array after the keys (one array keeps the
+// block's LDS at about 40 KB, four blocks per CU); each thread remembers the
+// digits of the slots it copied out.
 constexpr int RS_WITEMS = RS_TILE / RS_WAVES;   // items per wave
+constexpr int RS_COPY = RS_TILE / RS_THREADS;   // slots each thread copies out
 template <int DBITS>
 __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
@@ -502,7 +527,6 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
     constexpr uint32_t MASK = NB - 1;
     __shared__ uint64_t skey[RS_TILE];
-    __shared__ uint32_t sval[RS_TILE];
     __shared__ uint64_t gbase[NB];
     __shared__ uint32_t dstart[NB];
     __shared__ uint32_t wcnt[RS_WAVES][NB];   // per wave: running count, then its offset within the digit
@@ -578,28 +602,47 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
         }
     }
     __syncthreads();
+    // LDS slot of each item (count or more: out of range, flagged)
 #pragma unroll
     for (int r = 0; r < RS_ITEMS; r++) {
-        if (wbase + r * 64 + lane >= count) continue;
-        const uint32_t d = (uint32_t)((keys[r] >> shift) & MASK);
-        const uint32_t lpos = wcnt[wave][d] + rank[r];
-        if (lpos < (uint32_t)count) {
-            skey[lpos] = keys[r];
-            if (vin) sval[lpos] = vals[r];
-        } else {
-            atomicOr(bad, bad_bit);
+        if (wbase + r * 64 + lane >= count) {
+            rank[r] = RS_TILE;
+            continue;
         }
+        const uint32_t d = (uint32_t)((keys[r] >> shift) & MASK);
+        rank[r] = wcnt[wave][d] + rank[r];
+        if (rank[r] < (uint32_t)count) skey[rank[r]] = keys[r];
+        else atomicOr(bad, bad_bit);
     }
     __syncthreads();
-    for (int i = tid; i < count; i += RS_THREADS) {
-        const uint64_t key = skey[i];
-        const uint32_t d = (uint32_t)((key >> shift) & MASK);
-        const uint64_t pos = gbase[d] + (uint64_t)(i - (int)dstart[d]);
-        if (pos < (uint64_t)n) {
-            kout[pos] = key;
-            if (vin) vout[pos] = sval[i];
-        } else {
-            atomicOr(bad, bad_bit);
+    uint32_t dig[RS_COPY];
+#pragma unroll
+    for (int j = 0; j < RS_COPY; j++) {
+        const int i = j * RS_THREADS + tid;
+        dig[j] = 0;
+        if (i < count) {
+            const uint64_t key = skey[i];
+            const uint32_t d = (uint32_t)((key >> shift) & MASK);
+            dig[j] = d;
+            const uint64_t pos = gbase[d] + (uint64_t)(i - (int)dstart[d]);
+            if (pos < (uint64_t)n) kout[pos] = key;
+            else atomicOr(bad, bad_bit);
+        }
+    }
+    if (!vin) return;
+    __syncthreads();  // every key is out of LDS
+    uint32_t* sval = reinterpret_cast<uint32_t*>(skey);
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; r++)
+        if (rank[r] < (uint32_t)count) sval[rank[r]] = vals[r];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < RS_COPY; j++) {
+        const int i = j * RS_THREADS + tid;
+        if (i < count) {
+            const uint32_t d = dig[j];
+            const uint64_t pos = gbase[d] + (uint64_t)(i - (int)dstart[d]);
+            if (pos < (uint64_t)n) vout[pos] = sval[i];
         }
     }
 }
@@ -618,10 +661,10 @@ static void radix_pass(SortBuffers& b, int64_t n, int shift, int64_t nblocks, ui
 }
 
 // Digit schedule: 8-bit passes, the cheapest per sorted bit here (measured
-// per pass at 20M key-value pairs: 8 bits ~186 us, 9 bits ~237 us, 10 bits
-// ~279 us with hist and scan); one pass fewer with some digits widened to 9
-// or 10 bits when that costs less, e.g. 25 bits as 9 + 8 + 8 instead of four
-// 8-bit passes.  Bits above key_bits are zero in every key sorted here, so a
+// per pass at 20M key-value pairs with hist and scan: 8 bits ~190 us, 9 bits
+// ~240 us; keys alone, 8 bits ~150 us); one pass fewer with some digits
+// widened to 9 or 10 bits when that costs less, e.g. 25 bits as 9 + 8 + 8
+// instead of four 8-bit passes.  Bits above key_bits are zero in every key sorted here, so a
 // pass may cover a few more bits than remain.
 static std::vector<int> digit_schedule(int key_bits) {
     const double cost[11] = {0, 0, 0, 0, 0, 0, 0, 0, 1.0, 1.27, 1.5};
