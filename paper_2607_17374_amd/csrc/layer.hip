@@ -476,19 +476,24 @@ __device__ inline float seg_scale(int agg, int expect) {
 }
 
 // Rows in flight per row-group: 16 slots of up to two float4 per lane, 8 of
-// four.
-__host__ __device__ constexpr int slots_per_round(int vec) { return vec <= 2 ? 16 : 8; }
+// four; half as many in the lean build (twice the waves per SIMD, for
+// chunks with too little work to hide the latency of a batch).
+__host__ __device__ constexpr int slots_per_round(int vec, bool lean = false) {
+    return (vec <= 2 ? 16 : 8) >> (lean ? 1 : 0);
+}
 
 // Units of short class `len` a row-group takes at once: their rows plus
 // one early accumulator row each stay within 20 rows of up to two float4
 // per lane (10 of four), and at most 8 units.
-__host__ __device__ constexpr int batch_units(int vec, int len) {
-    const int k = (vec <= 2 ? 20 : 10) / (len + 1);
+__host__ __device__ constexpr int batch_units(int vec, int len, bool lean = false) {
+    const int k = ((vec <= 2 ? 20 : 10) >> (lean ? 1 : 0)) / (len + 1);
     return k < 1 ? 1 : (k > 8 ? 8 : k);
 }
 
 // vertices per row-group batch of the self pass
-__host__ __device__ constexpr int self_batch_rows(int vec) { return vec <= 2 ? 8 : 4; }
+__host__ __device__ constexpr int self_batch_rows(int vec, bool lean = false) {
+    return (vec <= 2 ? 8 : 4) >> (lean ? 1 : 0);
+}
 
 // Gathers of rows of the chunk transform go through a buffer resource: a
 // slot is the 32-bit byte offset of its row in Y, and an offset past the end
@@ -599,10 +604,10 @@ __device__ inline int rg_pick(const int (&reg)[NREG], int k) {
 // messages (weight sigma_v).  Software-pipelined: the next batch's row
 // offsets and the descriptors after it are requested while this batch's
 // rows are in flight.
-template <int G, int VEC, int LEN, bool ATT>
+template <int G, int VEC, int LEN, bool ATT, bool LEAN>
 __device__ inline void short_batches(const ScatterParams& p, const int4* __restrict__ units, int64_t n, int64_t rot) {
-    constexpr int SLOTS = slots_per_round(VEC);
-    constexpr int K = batch_units(VEC, LEN);                                  // units per batch
+    constexpr int SLOTS = slots_per_round(VEC, LEAN);
+    constexpr int K = batch_units(VEC, LEN, LEAN);                            // units per batch
     constexpr int TS = K * LEN;                                               // slots per batch
     constexpr int RB = TS < SLOTS ? TS : SLOTS;                               // rows per round
     static_assert(TS <= SLOTS || K == 1, "a batch of several units fits one round");
@@ -765,9 +770,9 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
 // shuffles and row-group 0 flushes (or parks the partial row of a hub piece
 // in its carry slot).  The next piece's descriptor is fetched ahead and its
 // offsets are requested while the first round's rows are in flight.
-template <int G, int VEC, bool ATT>
+template <int G, int VEC, bool ATT, bool LEAN>
 __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restrict__ units, int64_t n) {
-    constexpr int SLOTS = slots_per_round(VEC);
+    constexpr int SLOTS = slots_per_round(VEC, LEAN);
     constexpr int NREG = PIECE_LEN / 64;
     const int wave = threadIdx.x >> 6, l64 = threadIdx.x & 63;
     const int rg = l64 / G, lane = l64 % G;
@@ -927,9 +932,9 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
 // arrival each.  A row-group takes K consecutive vertices at a time --
 // consecutive rows of Y and of the accumulators.  These vertices have no
 // other flush in the launch.
-template <int G, int VEC, bool ATT>
+template <int G, int VEC, bool ATT, bool LEAN>
 __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
-    constexpr int K = self_batch_rows(VEC);
+    constexpr int K = self_batch_rows(VEC, LEAN);
     constexpr int KD = (K + G - 1) / G;
     constexpr int NRG = SC_THREADS / G;
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
@@ -979,17 +984,23 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
 // Degree-bucketed scatter of one chunk, persistent: the grid is sized to
 // what the GPU holds at once and walks the wave pieces (longest work
 // first), the short classes from long to short, then the self pass.
-// ATT: GAT's aggregation pass, every slot weighted by its attention.
+// ATT: GAT's aggregation pass, every slot weighted by its attention.  The
+// plain aggregation takes the lean row budget (half the rows in flight per
+// row-group) and runs three waves per SIMD (two for rows of four float4
+// per lane): more row-groups resident hide the dependent loads of a batch
+// better than more rows per row-group do.  GAT's pass keeps the full
+// budget and two waves (its weights need the registers).
 template <int G, int VEC, bool ATT = false>
-__global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(SC_THREADS) __attribute__((amdgpu_waves_per_eu(ATT || VEC > 2 ? 2 : 3)))
 void k_scatter(ScatterParams p, ChunkUnits cu) {
-    wave_pieces<G, VEC, ATT>(p, cu.u[NCLASS], cu.n[NCLASS]);
-    short_batches<G, VEC, 16, ATT>(p, cu.u[4], cu.n[4], cu.rot[4]);
-    short_batches<G, VEC, 8, ATT>(p, cu.u[3], cu.n[3], cu.rot[3]);
-    short_batches<G, VEC, 4, ATT>(p, cu.u[2], cu.n[2], cu.rot[2]);
-    short_batches<G, VEC, 2, ATT>(p, cu.u[1], cu.n[1], cu.rot[1]);
-    short_batches<G, VEC, 1, ATT>(p, cu.u[0], cu.n[0], cu.rot[0]);
-    self_batches<G, VEC, ATT>(p, cu.rot[NCLASS]);
+    constexpr bool LEAN = !ATT;
+    wave_pieces<G, VEC, ATT, LEAN>(p, cu.u[NCLASS], cu.n[NCLASS]);
+    short_batches<G, VEC, 16, ATT, LEAN>(p, cu.u[4], cu.n[4], cu.rot[4]);
+    short_batches<G, VEC, 8, ATT, LEAN>(p, cu.u[3], cu.n[3], cu.rot[3]);
+    short_batches<G, VEC, 4, ATT, LEAN>(p, cu.u[2], cu.n[2], cu.rot[2]);
+    short_batches<G, VEC, 2, ATT, LEAN>(p, cu.u[1], cu.n[1], cu.rot[1]);
+    short_batches<G, VEC, 1, ATT, LEAN>(p, cu.u[0], cu.n[0], cu.rot[0]);
+    self_batches<G, VEC, ATT, LEAN>(p, cu.rot[NCLASS]);
 }
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
@@ -1026,7 +1037,7 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
 // and the persistent grid size.
 struct ScatterShape {
     int G, VEC;
-    int64_t max_blocks;
+    int64_t max_blocks, max_blocks_att;  // workgroups resident at once, plain and GAT builds
 };
 
 static int env_int(const char* name, int dflt) {
@@ -1034,12 +1045,12 @@ static int env_int(const char* name, int dflt) {
     return v && *v ? atoi(v) : dflt;
 }
 
-template <int G, int VEC>
+template <int G, int VEC, bool ATT>
 static int64_t resident_blocks() {
     int dev = 0, cus = 0, per_cu = 0;
     TAURUS_HIP(hipGetDevice(&dev));
     TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    TAURUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_scatter<G, VEC>, SC_THREADS, 0));
+    TAURUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_scatter<G, VEC, ATT>, SC_THREADS, 0));
     return (int64_t)std::max(1, cus) * std::max(1, per_cu);
 }
 
@@ -1060,7 +1071,7 @@ static ScatterShape scatter_shape(int d_o) {
     ScatterShape sh;
     sh.G = g;
     sh.VEC = vec;
-    sh.max_blocks = 0;
+    sh.max_blocks = sh.max_blocks_att = 0;
     return sh;
 }
 
@@ -1072,14 +1083,15 @@ static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, Chu
     const int nrg = SC_THREADS / sh.G;
     // the row-group sequence: wave pieces' row-groups, then the short
     // classes from the longest, then the self pass
+    const bool lean = !att;  // the row budget k_scatter<G, VEC, att> is built with
     int64_t t = cu.n[NCLASS] * (64 / sh.G);
     for (int c = NCLASS - 1; c >= 0; c--) {
         cu.rot[c] = t;
-        t += ceil_div(cu.n[c], batch_units(sh.VEC, class_len(c)));
+        t += ceil_div(cu.n[c], batch_units(sh.VEC, class_len(c), lean));
     }
     cu.rot[NCLASS] = t;
-    t += ceil_div(p.rows, self_batch_rows(sh.VEC));
-    const int64_t blocks = std::max<int64_t>(1, std::min(ceil_div(t, nrg), sh.max_blocks));
+    t += ceil_div(p.rows, self_batch_rows(sh.VEC, lean));
+    const int64_t blocks = std::max<int64_t>(1, std::min(ceil_div(t, nrg), att ? sh.max_blocks_att : sh.max_blocks));
 #define TAURUS_CASE(g, v)                                                         \
     if (sh.G == g && sh.VEC == v) {                                               \
         if (att) k_scatter<g, v, true><<<(unsigned)blocks, SC_THREADS, 0, s>>>(p, cu); \
@@ -1092,9 +1104,9 @@ static void dispatch_scatter(const ScatterShape& sh, const ScatterParams& p, Chu
     fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
 }
 
-static int64_t scatter_resident_blocks(const ScatterShape& sh) {
+static int64_t scatter_resident_blocks(const ScatterShape& sh, bool att) {
 #define TAURUS_CASE(g, v) \
-    if (sh.G == g && sh.VEC == v) return resident_blocks<g, v>();
+    if (sh.G == g && sh.VEC == v) return att ? resident_blocks<g, v, true>() : resident_blocks<g, v, false>();
     TAURUS_ROW_SHAPES(TAURUS_CASE)
 #undef TAURUS_CASE
     fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
@@ -1711,7 +1723,8 @@ static void layer_init(taurus_layer* L) {
     // padded to a multiple of 4
     L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.agg == TAURUS_GAT_ATT ? d.d_out + 4 : d.d_out;
     L->shape = scatter_shape(L->d_o);
-    L->shape.max_blocks = scatter_resident_blocks(L->shape) * std::max(1, env_int("TAURUS_SCATTER_WAVES", 1));
+    L->shape.max_blocks = scatter_resident_blocks(L->shape, false);
+    L->shape.max_blocks_att = scatter_resident_blocks(L->shape, true);
     const int T = 256;
 
     // chunk index: exact layers share the plan's (built here if it is the
