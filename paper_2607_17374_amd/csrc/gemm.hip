@@ -96,8 +96,8 @@ __device__ inline floatx4 mfma16(uint4 a, uint4 b, floatx4 c) {
 // columns for NB = 8); each of its four waves computes 16 rows x all of the
 // group's columns, so every X row is read once per column group (once in
 // all for widths up to 128).  The group's packed weight fragments are staged
-// in LDS one K stage at a time (KS k-blocks), and a wave requests all of its
-// A fragments of the stage before the matrix-core work.
+// in LDS one K stage at a time (PIPE_KS k-blocks), and a wave requests all
+// of its A fragments of the stage before the matrix-core work.
 //   fp32:   k-block = 16 k, fragment = one float4 per lane (4 MFMAs 16x16x4);
 //   16-bit: k-block = 32 k, fragment = eight 16-bit values (one 16x16x32 MFMA).
 template <int DT>
@@ -151,52 +151,82 @@ template <>
 struct GemmOp<TAURUS_F16> : GemmOp16<TAURUS_F16> {};
 
 constexpr int PANEL_ROWS = 64;
-constexpr int PANEL_KS = 4;   // k-blocks per LDS stage
 
-// PANEL_NB: 16-column blocks per workgroup (8 = 128 columns; 4 for narrow outputs)
+// The weights go through two LDS buffers of PIPE_KS k-blocks each: while a
+// stage's products run, the next stage's weight fragments (into registers,
+// then into the other buffer) and A fragments are already in flight, so
+// the workgroups' loads overlap their matrix-core work (all of a chunk's
+// workgroups are resident at once and would otherwise load and multiply in
+// lockstep).  One barrier per stage.  PANEL_NB: 16-column blocks per
+// workgroup (8 = 128 columns; 4 for narrow outputs).
+constexpr int PIPE_KS = 2;
 template <int DT, int PANEL_NB>
 __global__ __launch_bounds__(256) void k_gemm_panel(const void* __restrict__ X, int64_t M, int K,
-                                                    const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP,
-                                                    int Nc, const float* __restrict__ rscale,
-                                                    float* __restrict__ Y) {
+                                                   const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP,
+                                                   int Nc, const float* __restrict__ rscale,
+                                                   float* __restrict__ Y) {
     typedef GemmOp<DT> Op;
     typedef typename Op::frag frag;
-    __shared__ frag sB[PANEL_KS * PANEL_NB * 64];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    constexpr int SF = PIPE_KS * PANEL_NB * 64;  // fragments per stage
+    constexpr int PER = SF / 256;                // of which each thread stages
+    static_assert(SF % 256 == 0, "whole fragments per thread");
+    __shared__ frag sB[2][SF];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int li = lane & 15, lk = lane >> 4;
     const int nb0 = blockIdx.y * PANEL_NB;
-    const int nbs = min(PANEL_NB, NBP - nb0);  // column blocks of this group
+    const int nbs = min(PANEL_NB, NBP - nb0);
     const int64_t row = (int64_t)blockIdx.x * PANEL_ROWS + wave * 16 + li;
     const int KB = (K + Op::KBLK - 1) / Op::KBLK;
+    const int nst = (KB + PIPE_KS - 1) / PIPE_KS;
+    auto load_w = [&](int st, frag (&r)[PER]) {
+#pragma unroll
+        for (int q = 0; q < PER; q++) {
+            const int i = q * 256 + tid;
+            const int kk = i / (PANEL_NB * 64), rr = i - kk * (PANEL_NB * 64), j = rr >> 6, l = rr & 63;
+            const int kb = st * PIPE_KS + kk;
+            r[q] = (kb < KB && j < nbs) ? Wp[((int64_t)kb * NBP + nb0 + j) * 64 + l] : Op::zero();
+        }
+    };
+    auto load_a = [&](int st, frag (&a)[PIPE_KS]) {
+#pragma unroll
+        for (int kk = 0; kk < PIPE_KS; kk++) {
+            const int kb = st * PIPE_KS + kk;
+            const int k = kb * Op::KBLK + (Op::KBLK / 4) * lk;
+            a[kk] = (kb < KB && row < M && k < K) ? Op::load_a(X, row, K, k) : Op::zero();
+        }
+    };
     floatx4 acc[PANEL_NB];
 #pragma unroll
     for (int j = 0; j < PANEL_NB; j++) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int kb0 = 0; kb0 < KB; kb0 += PANEL_KS) {
-        const int ks = min(PANEL_KS, KB - kb0);
-        __syncthreads();  // the previous stage's fragments are no longer read
-        // the whole stage is written (zero fragments past the K or column
-        // range), so every product below is unconditional
-#pragma unroll 2
-        for (int i = threadIdx.x; i < PANEL_KS * PANEL_NB * 64; i += 256) {
-            const int kk = i / (PANEL_NB * 64), r = i - kk * (PANEL_NB * 64), j = r >> 6, l = r & 63;
-            sB[i] = (kk < ks && j < nbs) ? Wp[((int64_t)(kb0 + kk) * NBP + nb0 + j) * 64 + l] : Op::zero();
-        }
-        frag a[PANEL_KS];
+    frag rw[PER], a[PIPE_KS];
+    load_w(0, rw);
+    load_a(0, a);
 #pragma unroll
-        for (int kk = 0; kk < PANEL_KS; kk++) {
-            const int k = (kb0 + kk) * Op::KBLK + (Op::KBLK / 4) * lk;
-            a[kk] = (kk < ks && row < M && k < K) ? Op::load_a(X, row, K, k) : Op::zero();
+    for (int q = 0; q < PER; q++) sB[0][q * 256 + tid] = rw[q];
+    __syncthreads();
+    for (int st = 0; st < nst; st++) {
+        const bool more = st + 1 < nst;
+        frag an[PIPE_KS];
+        if (more) {
+            load_w(st + 1, rw);
+            load_a(st + 1, an);
         }
-        __syncthreads();
 #pragma unroll
-        for (int kk = 0; kk < PANEL_KS; kk++) {
+        for (int kk = 0; kk < PIPE_KS; kk++) {
             frag b[PANEL_NB];
 #pragma unroll
-            for (int j = 0; j < PANEL_NB; j++) b[j] = sB[(kk * PANEL_NB + j) * 64 + lane];
+            for (int j = 0; j < PANEL_NB; j++) b[j] = sB[st & 1][(kk * PANEL_NB + j) * 64 + lane];
             Op::template mma_all<PANEL_NB>(a[kk], b, acc);
         }
+        if (more) {
+            // the other buffer was last read in the previous stage, before its barrier
+#pragma unroll
+            for (int q = 0; q < PER; q++) sB[(st + 1) & 1][q * 256 + tid] = rw[q];
+#pragma unroll
+            for (int kk = 0; kk < PIPE_KS; kk++) a[kk] = an[kk];
+        }
+        __syncthreads();
     }
-    // D fragment: lane l holds rows 4*(l/16) + r, column l%16
     const int64_t rbase = (int64_t)blockIdx.x * PANEL_ROWS + wave * 16 + 4 * lk;
 #pragma unroll
     for (int r = 0; r < 4; r++) {
