@@ -402,6 +402,39 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile_apply(const Tin* __r
     }
 }
 
+// Exclusive scan of a short sequence (the tile sums) by one workgroup that
+// walks it a tile at a time with a running carry: one launch instead of
+// another level of tiles.
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_serial(const uint64_t* __restrict__ in, int64_t n,
+                                                              uint64_t* __restrict__ out) {
+    __shared__ uint64_t stage[SCAN_TILE];
+    uint64_t carry = 0;
+    for (int64_t base = 0; base < n; base += SCAN_TILE) {
+        for (int i = threadIdx.x; i < SCAN_TILE; i += SCAN_THREADS) stage[i] = base + i < n ? in[base + i] : 0;
+        __syncthreads();
+        uint64_t v[SCAN_ITEMS];
+        uint64_t s = 0;
+#pragma unroll
+        for (int j = 0; j < SCAN_ITEMS; j++) {
+            v[j] = stage[threadIdx.x * SCAN_ITEMS + j];
+            s += v[j];
+        }
+        uint64_t total;
+        uint64_t run = block_excl_scan(s, &total) + carry;
+#pragma unroll
+        for (int j = 0; j < SCAN_ITEMS; j++) {
+            stage[threadIdx.x * SCAN_ITEMS + j] = run;
+            run += v[j];
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < SCAN_TILE; i += SCAN_THREADS)
+            if (base + i < n) out[base + i] = stage[i];
+        __syncthreads();  // stage is reloaded for the next tile
+        carry += total;
+    }
+}
+constexpr int64_t SCAN_SERIAL_MAX = 1 << 16;  // tile sums scanned by k_scan_serial
+
 template <typename Tout>
 __global__ void k_write_total(const uint64_t* __restrict__ sums_scanned, const uint64_t* __restrict__ sums,
                               int64_t nb, Tout* __restrict__ out, int64_t n) {
@@ -427,8 +460,8 @@ static void scan_impl(const Tin* in, Tout* out, int64_t n, bool write_total, Are
     uint64_t* sums_scanned = arena.alloc<uint64_t>(nb, "scan block offsets");
     k_scan_tile_sums<Tin><<<(unsigned)nb, SCAN_THREADS, 0, s>>>(in, n, sums);
     TAURUS_CHECK_LAUNCH();
-    if (nb == 1) {
-        k_write_zero<<<1, 64, 0, s>>>(sums_scanned);
+    if (nb <= SCAN_SERIAL_MAX) {
+        k_scan_serial<<<1, SCAN_THREADS, 0, s>>>(sums, nb, sums_scanned);
         TAURUS_CHECK_LAUNCH();
     } else {
         scan_impl<uint64_t, uint64_t>(sums, sums_scanned, nb, false, arena, s);
