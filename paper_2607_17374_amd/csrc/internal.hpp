@@ -61,14 +61,16 @@ void pinned_staging_in_flight(hipStream_t s);
 // stream synchronisation: add() any number, then run().
 class Readback {
 public:
-    void add(void* host, const void* dev, size_t bytes);
+    // count elements of type T; host and device types must match (no
+    // untyped overload, so a mismatch does not compile)
     template <typename T>
     void add(T* host, const T* dev, int64_t count) {
-        add(static_cast<void*>(host), static_cast<const void*>(dev), (size_t)count * sizeof(T));
+        add_bytes(static_cast<void*>(host), static_cast<const void*>(dev), (size_t)count * sizeof(T));
     }
     void run(hipStream_t s);
 
 private:
+    void add_bytes(void* host, const void* dev, size_t bytes);
     struct Item {
         void* host;
         const void* dev;
@@ -125,6 +127,8 @@ void scan_u32_to_u64(const uint32_t* in, uint64_t* out, int64_t n, bool write_to
 // Same for int32 inputs into int64 outputs.
 void scan_i32_to_i64(const int32_t* in, int64_t* out, int64_t n, bool write_total, Arena& arena,
                      hipStream_t s);
+// Same for uint64 inputs.
+void scan_u64(const uint64_t* in, uint64_t* out, int64_t n, bool write_total, Arena& arena, hipStream_t s);
 
 // p[0..n) = v
 void fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

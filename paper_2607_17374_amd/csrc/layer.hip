@@ -167,20 +167,81 @@ __global__ void k_chunk_bounds(const uint64_t* __restrict__ keys, int64_t total,
     offs[j] = lo;
 }
 
-// head[i] = 1 where a new (chunk, destination) segment starts
-// (items past *kept, the dropped edges, get 0)
-__global__ void k_seg_heads(const uint64_t* __restrict__ keys, int64_t n_items, const int64_t* __restrict__ kept,
-                            int32_t* __restrict__ head) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n_items) head[i] = (i < *kept && (i == 0 || keys[i] != keys[i - 1])) ? 1 : 0;
+// Segment heads: item i < kept starts a new (chunk, destination) segment
+// when i = 0 or its key differs from item i-1's.  Items are taken in tiles
+// of HEAD_TILE: k_head_counts counts each tile's heads, and after a scan of
+// the counts k_head_positions writes seg_start[s] = first item of segment
+// s, in item order, and seg_start[P] = items.
+constexpr int HEAD_ITEMS = 16;
+constexpr int HEAD_TILE = 256 * HEAD_ITEMS;
+
+__device__ inline bool seg_head(const uint64_t* keys, int64_t i, int64_t kept) {
+    return i < kept && (i == 0 || keys[i] != keys[i - 1]);
 }
 
-// seg_start[s] = first item of segment s; seg_start[P] = total
-__global__ void k_seg_starts(const int32_t* __restrict__ head, const int64_t* __restrict__ seg_id, int64_t total,
-                             int64_t* __restrict__ seg_start) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < total && head[i]) seg_start[seg_id[i]] = i;
-    if (i == 0) seg_start[seg_id[total]] = total;
+__global__ __launch_bounds__(256) void k_head_counts(const uint64_t* __restrict__ keys,
+                                                     const int64_t* __restrict__ kept,
+                                                     uint64_t* __restrict__ counts) {
+    __shared__ uint32_t wsum[4];
+    const int64_t base = (int64_t)blockIdx.x * HEAD_TILE;
+    const int64_t kp = *kept;
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < HEAD_ITEMS; j++) c += seg_head(keys, base + (int64_t)j * 256 + threadIdx.x, kp) ? 1u : 0u;
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) counts[blockIdx.x] = (uint64_t)wsum[0] + wsum[1] + wsum[2] + wsum[3];
+}
+
+__global__ __launch_bounds__(256) void k_head_positions(const uint64_t* __restrict__ keys, int64_t items,
+                                                        const int64_t* __restrict__ kept,
+                                                        const uint64_t* __restrict__ tile_off, int64_t P,
+                                                        int64_t* __restrict__ seg_start) {
+    __shared__ uint8_t fl[HEAD_TILE];
+    __shared__ uint32_t wsum[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t base = (int64_t)blockIdx.x * HEAD_TILE;
+    const int64_t kp = *kept;
+#pragma unroll
+    for (int j = 0; j < HEAD_ITEMS; j++) fl[j * 256 + tid] = seg_head(keys, base + (int64_t)j * 256 + tid, kp) ? 1 : 0;
+    __syncthreads();
+    // thread t ranks items [t*HEAD_ITEMS, (t+1)*HEAD_ITEMS) of the tile
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < HEAD_ITEMS; j++) c += fl[tid * HEAD_ITEMS + j];
+    uint32_t incl = c;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint64_t pos = tile_off[blockIdx.x] + incl - c;
+    for (int w = 0; w < wave; w++) pos += wsum[w];
+#pragma unroll
+    for (int j = 0; j < HEAD_ITEMS; j++)
+        if (fl[tid * HEAD_ITEMS + j] && pos < (uint64_t)P) seg_start[pos++] = base + tid * HEAD_ITEMS + j;
+    if (blockIdx.x == 0 && tid == 0) seg_start[P] = items;
+}
+
+// chunk_seg[k] = first segment of chunk k: the first segment starting at or
+// after the chunk's first item (every chunk's first item is a head)
+__global__ void k_chunk_segments(const int64_t* __restrict__ chunk_off, int64_t nchunks,
+                                 const int64_t* __restrict__ seg_start, int64_t P,
+                                 int64_t* __restrict__ chunk_seg) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k > nchunks) return;
+    const int64_t target = chunk_off[k];
+    int64_t lo = 0, hi = P;  // seg_start[P] = items >= any target
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if (seg_start[mid] < target) lo = mid + 1;
+        else hi = mid;
+    }
+    chunk_seg[k] = lo;
 }
 
 // work list of a segment: short class 0..NCLASS-1 by slot count, or NCLASS (wave pieces)
@@ -267,16 +328,14 @@ __global__ __launch_bounds__(256) void k_list_totals(const int32_t* __restrict__
 // bases[k] = position in list l (offsets `off`, an exclusive scan of the
 // list's entries per segment) of chunk k's first entry; chunk_seg[k] = the
 // chunk's first segment, chunk_seg[nchunks] = P
+// list l = blockIdx.y: its offsets at off + l * off_stride, its chunk
+// bases at bases + l * (nchunks + 1)
 __global__ void k_list_chunk_bases(const int64_t* __restrict__ chunk_seg, int64_t nchunks,
-                                   const int64_t* __restrict__ off, int64_t* __restrict__ bases) {
+                                   const int64_t* __restrict__ off, int64_t off_stride,
+                                   int64_t* __restrict__ bases) {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k <= nchunks) bases[k] = off[chunk_seg[k]];
-}
-
-__global__ void k_chunk_segments(const int64_t* __restrict__ chunk_off, int64_t nchunks,
-                                 const int64_t* __restrict__ seg_id, int64_t* __restrict__ chunk_seg) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k <= nchunks) chunk_seg[k] = seg_id[chunk_off[k]];
+    const int64_t l = blockIdx.y;
+    if (k <= nchunks) bases[l * (nchunks + 1) + k] = off[l * off_stride + chunk_seg[k]];
 }
 
 // What a unit of segment s says besides its slots: {first item relative to
@@ -306,7 +365,8 @@ __device__ inline SegUnit seg_unit(const uint64_t* keys, const int64_t* seg_star
 }
 
 // Short class l: unit = {first item, slots | NOT_FIRST | SELF_HERE, v, 0} at
-// off[s] (the list's exclusive scan).
+// off[s] (the list's exclusive scan).  l < 0: every short class c at once,
+// at off[c * P + s].
 __global__ void k_emit_short(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start,
                              const int32_t* __restrict__ slots_of, int64_t P, int l, int vbits, int64_t C,
                              const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
@@ -314,9 +374,10 @@ __global__ void k_emit_short(const uint64_t* __restrict__ keys, const int64_t* _
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int slots = slots_of[s];
-    if (seg_class(slots) != l) return;
+    const int c = seg_class(slots);
+    if (l >= 0 ? c != l : c >= NCLASS) return;
     const SegUnit u = seg_unit(keys, seg_start, s, vbits, C, chunk_off, first_chunk);
-    units[off[s]] = make_int4((int)u.rel, slots | u.nf | u.self, u.v, 0);
+    units[l >= 0 ? off[s] : off[(int64_t)c * P + s]] = make_int4((int)u.rel, slots | u.nf | u.self, u.v, 0);
 }
 
 // Longer segments: piece q covers slots [q * PIECE_LEN, ...) of the segment;
@@ -1264,19 +1325,21 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
     k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, items, nch, vbits, doffs);
     TAURUS_CHECK_LAUNCH();
-    int32_t* head = tmp.alloc<int32_t>(items1, "segment heads");
-    int64_t* seg_id = tmp.alloc<int64_t>(items + 1, "segment ids");
-    k_seg_heads<<<(unsigned)ceil_div(items1, T), T, 0, s>>>(keys, items, doffs + nch, head);
+    const int64_t nbt = ceil_div(items1, HEAD_TILE);
+    uint64_t* hcount = tmp.alloc<uint64_t>(nbt, "segment heads per tile");
+    uint64_t* hoff = tmp.alloc<uint64_t>(nbt + 1, "segment heads before each tile");
+    k_head_counts<<<(unsigned)nbt, 256, 0, s>>>(keys, doffs + nch, hcount);
     TAURUS_CHECK_LAUNCH();
-    scan_i32_to_i64(head, seg_id, items, true, tmp, s);
-    int64_t P = 0;
+    scan_u64(hcount, hoff, nbt, true, tmp, s);
+    uint64_t heads = 0;
     {
         Readback rb;
         rb.add(&hbad, bad, 1);
         rb.add(idx->chunk_off.data(), doffs, nch + 1);
-        rb.add(&P, seg_id + items, 1);
+        rb.add(&heads, hoff + nbt, 1);
         rb.run(s);
     }
+    const int64_t P = (int64_t)heads;
     if (hbad & 3) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
     if (hbad & 4) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
     if (hbad & 8) fail(TAURUS_E_DEVICE, "chunk index: radix sort offset out of range");
@@ -1291,13 +1354,13 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     // segments into the work lists, list by list with one count buffer and
     // one offset buffer (two for the wave pieces and their fix-up entries)
     int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
-    k_seg_starts<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(head, seg_id, kept, seg_start);
+    k_head_positions<<<(unsigned)nbt, 256, 0, s>>>(keys, items, doffs + nch, hoff, P, seg_start);
     TAURUS_CHECK_LAUNCH();
     int64_t* chunk_seg = tmp.alloc<int64_t>(nch + 1, "first segment per chunk");
-    k_chunk_segments<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_id, chunk_seg);
+    k_chunk_segments<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_start, P, chunk_seg);
     TAURUS_CHECK_LAUNCH();
-    tmp.free_ptr(head);
-    tmp.free_ptr(seg_id);
+    tmp.free_ptr(hoff);
+    tmp.free_ptr(hcount);
     int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
     fill_i32(first_chunk, n, 0x7fffffff, s);
     int32_t* slots_of = tmp.alloc<int32_t>(P, "segment slots");
@@ -1323,10 +1386,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         TAURUS_CHECK_LAUNCH();
         int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
         scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
-        for (int l = 0; l < NLIST; l++) {
-            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff + (int64_t)l * P, dbases + (int64_t)l * (nch + 1));
-            TAURUS_CHECK_LAUNCH();
-        }
+        k_list_chunk_bases<<<dim3(gC, NLIST), T, 0, s>>>(chunk_seg, nch, loff, P, dbases);
+        TAURUS_CHECK_LAUNCH();
         int64_t total_units = 0;
         {
             Readback rb;
@@ -1336,11 +1397,9 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         }
         if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
         idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
-        for (int l = 0; l < NCLASS; l++) {
-            k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, l, vbits, C, doffs, first_chunk,
-                                          loff + (int64_t)l * P, idx->units);
-            TAURUS_CHECK_LAUNCH();
-        }
+        k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, -1, vbits, C, doffs, first_chunk, loff,
+                                      idx->units);
+        TAURUS_CHECK_LAUNCH();
         k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk,
                                      loff + (int64_t)NCLASS * P, loff + (int64_t)(NCLASS + 1) * P, idx->units,
                                      idx->units, 0);
@@ -1370,7 +1429,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
             k_list_counts<<<gP, T, 0, s>>>(slots_of, P, l, lcnt);
             TAURUS_CHECK_LAUNCH();
             scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
-            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, dbases + (int64_t)l * (nch + 1));
+            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, 0, dbases + (int64_t)l * (nch + 1));
             TAURUS_CHECK_LAUNCH();
             k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, l, vbits, C, doffs, first_chunk, loff,
                                           idx->units + list_base[l]);
@@ -1380,12 +1439,12 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS + 1, lcnt);
         TAURUS_CHECK_LAUNCH();
         scan_i32_to_i64(lcnt, loff_fix, P, true, tmp, s);
-        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff_fix, dbases + (int64_t)(NCLASS + 1) * (nch + 1));
+        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff_fix, 0, dbases + (int64_t)(NCLASS + 1) * (nch + 1));
         TAURUS_CHECK_LAUNCH();
         k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS, lcnt);
         TAURUS_CHECK_LAUNCH();
         scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
-        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, dbases + (int64_t)NCLASS * (nch + 1));
+        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, 0, dbases + (int64_t)NCLASS * (nch + 1));
         TAURUS_CHECK_LAUNCH();
         k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk, loff, loff_fix,
                                      idx->units + list_base[NCLASS], idx->units + list_base[NCLASS + 1],

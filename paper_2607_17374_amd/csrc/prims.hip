@@ -252,7 +252,7 @@ void pinned_staging_in_flight(hipStream_t s) {
     st.in_flight = true;
 }
 
-void Readback::add(void* host, const void* dev, size_t bytes) {
+void Readback::add_bytes(void* host, const void* dev, size_t bytes) {
     items_.push_back({host, dev, bytes, total_});
     total_ += (bytes + 15) & ~(size_t)15;
 }
@@ -483,6 +483,9 @@ void scan_u32_to_u64(const uint32_t* in, uint64_t* out, int64_t n, bool write_to
 void scan_i32_to_i64(const int32_t* in, int64_t* out, int64_t n, bool write_total, Arena& arena,
                      hipStream_t s) {
     scan_impl<int32_t, int64_t>(in, out, n, write_total, arena, s);
+}
+void scan_u64(const uint64_t* in, uint64_t* out, int64_t n, bool write_total, Arena& arena, hipStream_t s) {
+    scan_impl<uint64_t, uint64_t>(in, out, n, write_total, arena, s);
 }
 
 // ---------------------------------------------------------------- radix -----
