@@ -1,0 +1,185 @@
+// Device side of the per-chunk transform on the matrix cores: operand
+// fragments, the MFMA steps and the row-panel body, shared by the transform
+// kernel and the launch that also carries the previous chunk's fix-up.
+// Fragment layouts are described at the top of gemm.hip.
+#pragma once
+
+#include "internal.hpp"
+
+namespace taurus {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+
+template <int DT>
+__device__ inline floatx4 mfma16(uint4 a, uint4 b, floatx4 c) {
+    if constexpr (DT == TAURUS_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                       c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(halfx8, a), __builtin_bit_cast(halfx8, b),
+                                                      c, 0, 0, 0);
+}
+
+// ---------------------------------------------------- row-panel kernel -----
+// A workgroup owns 64 rows and a group of up to NB 16-column blocks (128
+// columns for NB = 8); each of its four waves computes 16 rows x all of the
+// group's columns, so every X row is read once per column group (once in
+// all for widths up to 128).  The group's packed weight fragments are staged
+// in LDS one K stage at a time (PIPE_KS k-blocks), and a wave requests all
+// of its A fragments of the stage before the matrix-core work.
+//   fp32:   k-block = 16 k, fragment = one float4 per lane (4 MFMAs 16x16x4);
+//   16-bit: k-block = 32 k, fragment = eight 16-bit values (one 16x16x32 MFMA).
+template <int DT>
+struct GemmOp;
+template <>
+struct GemmOp<TAURUS_F32> {
+    typedef float4 frag;
+    static constexpr int KBLK = 16;
+    static __device__ inline floatx4 mma(frag a, frag b, floatx4 c) {
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+    }
+    static __device__ inline frag load_a(const void* X, int64_t row, int K, int k) {
+        return *reinterpret_cast<const float4*>(static_cast<const float*>(X) + row * K + k);
+    }
+    static __device__ inline frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    // all NB column blocks of one k-block, component-major: consecutive
+    // products go to different accumulators instead of one dependent chain
+    template <int NB>
+    static __device__ inline void mma_all(frag a, const frag (&b)[NB], floatx4 (&acc)[NB]) {
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[j].x, acc[j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[j].y, acc[j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[j].z, acc[j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[j].w, acc[j], 0, 0, 0);
+    }
+};
+template <int DT>
+struct GemmOp16 {
+    typedef uint4 frag;
+    static constexpr int KBLK = 32;
+    static __device__ inline floatx4 mma(frag a, frag b, floatx4 c) { return mfma16<DT>(a, b, c); }
+    static __device__ inline frag load_a(const void* X, int64_t row, int K, int k) {
+        return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(X) + row * K + k);
+    }
+    static __device__ inline frag zero() { return make_uint4(0, 0, 0, 0); }
+    template <int NB>
+    static __device__ inline void mma_all(frag a, const frag (&b)[NB], floatx4 (&acc)[NB]) {
+#pragma unroll
+        for (int j = 0; j < NB; j++) acc[j] = mfma16<DT>(a, b[j], acc[j]);
+    }
+};
+template <>
+struct GemmOp<TAURUS_BF16> : GemmOp16<TAURUS_BF16> {};
+template <>
+struct GemmOp<TAURUS_F16> : GemmOp16<TAURUS_F16> {};
+
+constexpr int PANEL_ROWS = 64;
+
+// The weights go through two LDS buffers of PIPE_KS k-blocks each: while a
+// stage's products run, the next stage's weight fragments (into registers,
+// then into the other buffer) and A fragments are already in flight, so
+// the workgroups' loads overlap their matrix-core work (all of a chunk's
+// workgroups are resident at once and would otherwise load and multiply in
+// lockstep).  One barrier per stage.  PANEL_NB: 16-column blocks per
+// workgroup (8 = 128 columns; 4 for narrow outputs).  Run by a whole
+// workgroup of 256 threads for the panel (bx, by): rows [64 bx, 64 bx + 64),
+// column blocks [PANEL_NB by, PANEL_NB by + PANEL_NB).  sB is the calling
+// kernel's own LDS array of PanelLds<DT, PANEL_NB> (an array declared here
+// would be one LDS variable shared by every kernel of the file, which the
+// compiler then addresses less directly).
+constexpr int PIPE_KS = 2;
+template <int DT, int PANEL_NB>
+struct PanelLds {
+    static constexpr int SF = PIPE_KS * PANEL_NB * 64;  // fragments per stage
+    typename GemmOp<DT>::frag b[2][SF];
+};
+template <int DT, int PANEL_NB>
+__device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
+                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
+                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
+                                        PanelLds<DT, PANEL_NB>& lds) {
+    typedef GemmOp<DT> Op;
+    typedef typename Op::frag frag;
+    constexpr int SF = PanelLds<DT, PANEL_NB>::SF;
+    constexpr int PER = SF / 256;                // of which each thread stages
+    static_assert(SF % 256 == 0, "whole fragments per thread");
+    auto& sB = lds.b;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int li = lane & 15, lk = lane >> 4;
+    const int nb0 = by * PANEL_NB;
+    const int nbs = min(PANEL_NB, NBP - nb0);
+    const int64_t row = (int64_t)bx * PANEL_ROWS + wave * 16 + li;
+    const int KB = (K + Op::KBLK - 1) / Op::KBLK;
+    const int nst = (KB + PIPE_KS - 1) / PIPE_KS;
+    auto load_w = [&](int st, frag (&r)[PER]) {
+#pragma unroll
+        for (int q = 0; q < PER; q++) {
+            const int i = q * 256 + tid;
+            const int kk = i / (PANEL_NB * 64), rr = i - kk * (PANEL_NB * 64), j = rr >> 6, l = rr & 63;
+            const int kb = st * PIPE_KS + kk;
+            r[q] = (kb < KB && j < nbs) ? Wp[((int64_t)kb * NBP + nb0 + j) * 64 + l] : Op::zero();
+        }
+    };
+    auto load_a = [&](int st, frag (&a)[PIPE_KS]) {
+#pragma unroll
+        for (int kk = 0; kk < PIPE_KS; kk++) {
+            const int kb = st * PIPE_KS + kk;
+            const int k = kb * Op::KBLK + (Op::KBLK / 4) * lk;
+            a[kk] = (kb < KB && row < M && k < K) ? Op::load_a(X, row, K, k) : Op::zero();
+        }
+    };
+    floatx4 acc[PANEL_NB];
+#pragma unroll
+    for (int j = 0; j < PANEL_NB; j++) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    frag rw[PER], a[PIPE_KS];
+    load_w(0, rw);
+    load_a(0, a);
+#pragma unroll
+    for (int q = 0; q < PER; q++) sB[0][q * 256 + tid] = rw[q];
+    __syncthreads();
+    for (int st = 0; st < nst; st++) {
+        const bool more = st + 1 < nst;
+        frag an[PIPE_KS];
+        if (more) {
+            load_w(st + 1, rw);
+            load_a(st + 1, an);
+        }
+#pragma unroll
+        for (int kk = 0; kk < PIPE_KS; kk++) {
+            frag b[PANEL_NB];
+#pragma unroll
+            for (int j = 0; j < PANEL_NB; j++) b[j] = sB[st & 1][(kk * PANEL_NB + j) * 64 + lane];
+            Op::template mma_all<PANEL_NB>(a[kk], b, acc);
+        }
+        if (more) {
+            // the other buffer was last read in the previous stage, before its barrier
+#pragma unroll
+            for (int q = 0; q < PER; q++) sB[(st + 1) & 1][q * 256 + tid] = rw[q];
+#pragma unroll
+            for (int kk = 0; kk < PIPE_KS; kk++) a[kk] = an[kk];
+        }
+        __syncthreads();
+    }
+    const int64_t rbase = (int64_t)bx * PANEL_ROWS + wave * 16 + 4 * lk;
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+        const int64_t orow = rbase + r;
+        if (orow >= M) continue;
+        const float sc = rscale ? rscale[orow] : 1.0f;
+#pragma unroll
+        for (int j = 0; j < PANEL_NB; j++) {
+            const int col = (nb0 + j) * 16 + li;
+            if (j < nbs && col < Nc) Y[orow * Nc + col] = acc[j][r] * sc;
+        }
+    }
+}
+
+}  // namespace taurus

@@ -36,6 +36,7 @@
 #include <mutex>
 
 #include "device.hpp"
+#include "gemm_device.hpp"
 #include "internal.hpp"
 #include "resident.hpp"
 
@@ -49,6 +50,7 @@ void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& pa
 void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
              float* Y, hipStream_t s);
 void gemm_pack_weights_16(const float* W, int K, int Nc, int dtype, std::vector<uint16_t>& packed);
+int gemm_packed_blocks_n(int nc);
 const char* last_error_cstr();
 
 constexpr int SC_THREADS = 256;
@@ -1066,12 +1068,13 @@ void k_scatter(ScatterParams p, ChunkUnits cu) {
 
 // A hub segment's pieces occupy consecutive carry slots; their partial rows
 // (the last one holding the self row of an own-chunk segment) are summed in
-// slot order and flushed.
+// slot order and flushed.  Workgroup blk of the fix-up takes SC_THREADS / G
+// hub segments, one per row-group.
 template <int G, int VEC>
-__global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix) {
+__device__ __attribute__((always_inline)) inline void fixup_rows(const ScatterParams& p, const int4* __restrict__ fix, int64_t nfix, int64_t blk) {
     constexpr int NRG = SC_THREADS / G;
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
-    const int64_t idx = (int64_t)blockIdx.x * NRG + rg;
+    const int64_t idx = blk * NRG + rg;
     if (idx >= nfix) return;
     const int4 f = fix[idx];
     const int v = f.x;
@@ -1090,6 +1093,10 @@ __global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int
         count += p.carry_cnt[first + q];
     }
     flush_owner<G, VEC>(p, v, p.cnt[v], c, count, lane, pre, false);
+}
+template <int G, int VEC>
+__global__ __launch_bounds__(SC_THREADS) void k_fixup(ScatterParams p, const int4* __restrict__ fix, int64_t nfix) {
+    fixup_rows<G, VEC>(p, fix, nfix, blockIdx.x);
 }
 
 // ------------------------------------------------------------- dispatch ---
@@ -1666,6 +1673,12 @@ struct taurus_layer {
     float* Y = nullptr;
     float* carry = nullptr;
     int32_t* carry_cnt = nullptr;
+    // in-core fp32 layers run the fix-up of chunk j inside the transform
+    // launch of the next chunk pushed (or at finalize)
+    bool fuse_fix = false, fix_pending = false;
+    taurus::ScatterParams fix_p{};
+    const int4* fix_list = nullptr;
+    int64_t fix_n = 0;
     uint64_t* mask = nullptr;
     float* gat_hp = nullptr;     // GAT: h' of every vertex, then s, t ([n][ncols])
     float* gat_m = nullptr;      // GAT: per-destination largest score
@@ -1931,6 +1944,7 @@ static void layer_init(taurus_layer* L) {
             fail(TAURUS_E_BUDGET, "residency structures take %lld bytes, above the budget %lld", (long long)total,
                  (long long)d.hbm_budget);
     }
+    L->fuse_fix = !L->res && !L->gat_hp && d.in_dtype == TAURUS_F32;
     if (d.profile) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
@@ -1973,6 +1987,54 @@ static const void* stage_host_chunk(taurus_layer* L, const void* x, int64_t rows
     return L->stage[cur];
 }
 
+// The fp32 transform of one chunk and the fix-up of the chunk pushed before
+// it, in one launch: workgroups [0, gblocks) are the transform's row panels
+// (gx per column group), the rest take the fix-up's hub segments.  Both only
+// follow that earlier chunk's scatter on the stream, and this chunk's
+// scatter follows both; one launch instead of two keeps the fix-up's few
+// workgroups off the critical path.
+static_assert(SC_THREADS == 256, "the transform's workgroups are 256 threads");
+template <int NB, int G, int VEC>
+__global__ __launch_bounds__(256) void k_transform_fixup(const float* __restrict__ X, int64_t M, int K,
+                                                         const float4* __restrict__ Wp, int NBP, int Nc,
+                                                         const float* __restrict__ rscale, float* __restrict__ Y,
+                                                         int gx, int gblocks, ScatterParams p,
+                                                         const int4* __restrict__ fix, int64_t nfix) {
+    __shared__ PanelLds<TAURUS_F32, NB> lds;
+    const int b = (int)blockIdx.x;
+    if (b < gblocks) {
+        gemm_panel_block<TAURUS_F32, NB>(X, M, K, Wp, NBP, Nc, rscale, Y, b % gx, b / gx, lds);
+        return;
+    }
+    fixup_rows<G, VEC>(p, fix, nfix, b - gblocks);
+}
+
+static void transform_with_fixup(const ScatterShape& sh, const float* X, int64_t M, int K, const float* Wp, int Nc,
+                                 const float* rscale, float* Y, const ScatterParams& p, const int4* fix,
+                                 int64_t nfix, hipStream_t s) {
+    const int NBP = gemm_packed_blocks_n(Nc);
+    const int nb = NBP <= 4 ? 4 : 8;
+    const int gx = (int)ceil_div(M, PANEL_ROWS), gy = (int)ceil_div(NBP, nb);
+    const int64_t fblocks = ceil_div(nfix, SC_THREADS / sh.G);
+    const int64_t blocks = (int64_t)gx * gy + fblocks;
+    if (blocks >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "transform of %lld rows is too large", (long long)M);
+    const float4* w = reinterpret_cast<const float4*>(Wp);
+#define TAURUS_CASE(g, v)                                                                                  \
+    if (sh.G == g && sh.VEC == v) {                                                                        \
+        if (nb == 4)                                                                                       \
+            k_transform_fixup<4, g, v><<<(unsigned)blocks, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, gx,  \
+                                                                       gx * gy, p, fix, nfix);             \
+        else                                                                                               \
+            k_transform_fixup<8, g, v><<<(unsigned)blocks, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, gx,  \
+                                                                       gx * gy, p, fix, nfix);             \
+        TAURUS_CHECK_LAUNCH();                                                                             \
+        return;                                                                                            \
+    }
+    TAURUS_ROW_SHAPES(TAURUS_CASE)
+#undef TAURUS_CASE
+    fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
+}
+
 static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int32_t x_on_host) {
     if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
     if (b < 0 || e > L->n || b >= e || b % L->C != 0 || e != std::min(b + L->C, L->n))
@@ -2008,7 +2070,11 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     const float* rscale = L->n_out ? L->n_out + b : nullptr;
     // GAT: the first pass only, into the layer's table of transformed rows
     float* ydst = L->gat_hp ? L->gat_hp + b * (int64_t)L->ncols : L->Y;
-    if (L->d.in_dtype == TAURUS_F32)
+    if (L->d.in_dtype == TAURUS_F32 && L->fix_pending) {
+        transform_with_fixup(L->shape, static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale,
+                             ydst, L->fix_p, L->fix_list, L->fix_n, s);
+        L->fix_pending = false;
+    } else if (L->d.in_dtype == TAURUS_F32)
         gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, ydst, s);
     else
         gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
@@ -2051,7 +2117,14 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     dispatch_scatter(L->shape, p, cu, s);
     if (ev[2]) TAURUS_HIP(hipEventRecord(ev[2], s));
     const int64_t nfix = idx.list_count(NCLASS + 1, k);
-    if (nfix > 0) dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
+    if (nfix > 0 && L->fuse_fix) {
+        L->fix_p = p;
+        L->fix_list = idx.list_at(NCLASS + 1, k);
+        L->fix_n = nfix;
+        L->fix_pending = true;
+    } else if (nfix > 0) {
+        dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
+    }
     if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
     if (L->res) L->res->release(rc, L->cnt, s);
 }
@@ -2142,6 +2215,10 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
     if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
     hipStream_t s = L->s;
     const ChunkIndex& idx = *L->idx;
+    if (L->fix_pending) {  // the last chunk's fix-up
+        dispatch_fixup(L->shape, L->fix_p, L->fix_list, L->fix_n, s);
+        L->fix_pending = false;
+    }
     if (L->gat_hp && !L->gat_done && L->npushed == L->nchunks) run_gat_passes(L);
     Arena tmp(s);
     unsigned long long* dleft = tmp.alloc<unsigned long long>(1, "pending count");
