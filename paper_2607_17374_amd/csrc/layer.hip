@@ -419,10 +419,6 @@ __global__ void k_self_first(const int32_t* __restrict__ first_chunk, int64_t n,
     if (v < n) has_own[v] = (has_own[v] & OWN_SEGMENT) | ((int64_t)first_chunk[v] >= v / C ? SELF_FIRST : 0);
 }
 
-__global__ void k_take_src(const uint32_t* __restrict__ vals, int64_t total, int32_t* __restrict__ src) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < total) src[i] = (int32_t)vals[i];
-}
 
 __global__ __launch_bounds__(256) void k_count_pending(const int2* __restrict__ cnt, int64_t n,
                                                        unsigned long long* __restrict__ left) {
@@ -1317,8 +1313,9 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     const int cbits = bits_for(nch - 1);  // chunk numbers 0 .. nch - 1
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
     SortBuffers sb{{tmp.alloc<uint64_t>(items1, "index keys"), tmp.alloc<uint64_t>(items1, "index keys (ping-pong)")},
-                   {tmp.alloc<uint32_t>(items1, "index values"),
-                    tmp.alloc<uint32_t>(items1, "index values (ping-pong)")},
+                   // the sorted values become the index's item sources
+                   {idx->arena.alloc<uint32_t>(items1, "index values"),
+                    idx->arena.alloc<uint32_t>(items1, "index values (ping-pong)")},
                    0};
     k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits, mask, word_off,
                                                         sb.keys[0], sb.vals[0], bad);
@@ -1326,9 +1323,9 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     if (word_off) tmp.free_ptr(word_off);
     radix_sort_u64(sb, items, vbits + cbits, tmp, s, bad, 8);
     const uint64_t* keys = sb.keys[sb.cur];
-    const uint32_t* vals = sb.vals[sb.cur];
+    uint32_t* vals = sb.vals[sb.cur];
     tmp.free_ptr(sb.keys[1 - sb.cur]);
-    tmp.free_ptr(sb.vals[1 - sb.cur]);
+    idx->arena.free_ptr(sb.vals[1 - sb.cur]);
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
     k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, items, nch, vbits, doffs);
     TAURUS_CHECK_LAUNCH();
@@ -1470,9 +1467,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     }
     for (int64_t k = 0; k < nch; k++)
         idx->max_long_per_chunk = std::max(idx->max_long_per_chunk, idx->list_count(NCLASS, k));
-    idx->item_src = idx->arena.alloc<int32_t>(kept, "item sources");
-    k_take_src<<<(unsigned)ceil_div(kept, T), T, 0, s>>>(vals, kept, idx->item_src);
-    TAURUS_CHECK_LAUNCH();
+    idx->item_src = reinterpret_cast<int32_t*>(vals);  // local source rows, below C < 2^31
     finish();
     return idx;
 }
