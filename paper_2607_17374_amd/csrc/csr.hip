@@ -6,18 +6,31 @@
 
 namespace taurus {
 
-// pack (u, v) into u << vbits | v and flag out-of-range ids and self loops
-__global__ void k_pack_edges(const int32_t* __restrict__ src, const int32_t* __restrict__ dst, int64_t e,
-                             int64_t n, int vbits, uint64_t* __restrict__ keys, int* __restrict__ bad) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= e) return;
-    const int64_t u = src[i], v = dst[i];
-    if (u < 0 || u >= n || v < 0 || v >= n || u == v) {
-        atomicOr(bad, 1);
-        keys[i] = 0;
-        return;
+// pack (u, v) into u << vbits | v and flag out-of-range ids and self loops.
+// Workgroup t packs tile t of RADIX_TILE edges and counts the low 8 bits of
+// its keys, the radix sort's first digit: hist[digit * tiles + t].
+__global__ __launch_bounds__(256) void k_pack_edges(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                                                    int64_t e, int64_t n, int vbits, uint64_t* __restrict__ keys,
+                                                    int* __restrict__ bad, uint32_t* __restrict__ hist,
+                                                    int64_t tiles) {
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * RADIX_TILE;
+    bool flag = false;
+    for (int j = 0; j < RADIX_TILE / 256; j++) {
+        const int64_t i = base + (int64_t)j * 256 + threadIdx.x;
+        if (i >= e) break;
+        const int64_t u = src[i], v = dst[i];
+        uint64_t key = 0;
+        if (u < 0 || u >= n || v < 0 || v >= n || u == v) flag = true;
+        else key = ((uint64_t)u << vbits) | (uint64_t)v;
+        keys[i] = key;
+        atomicAdd(&h[key & 255u], 1u);
     }
-    keys[i] = ((uint64_t)u << vbits) | (uint64_t)v;
+    if (flag) atomicOr(bad, 1);
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
 }
 
 // col_dst from the sorted keys; a key equal to its predecessor is a repeat
@@ -59,9 +72,11 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
     const int T = 256;
     if (e > 0) {
         sb.keys[1] = arena.alloc<uint64_t>(e, "edge keys (ping-pong)");
-        k_pack_edges<<<(unsigned)ceil_div(e, T), T, 0, s>>>(src, dst, e, n, vbits, sb.keys[0], bad);
+        const int64_t tiles = ceil_div(e, RADIX_TILE);
+        uint32_t* hist0 = arena.alloc<uint32_t>(256 * tiles, "first-digit histogram");
+        k_pack_edges<<<(unsigned)tiles, 256, 0, s>>>(src, dst, e, n, vbits, sb.keys[0], bad, hist0, tiles);
         TAURUS_CHECK_LAUNCH();
-        radix_sort_u64(sb, e, 2 * vbits, arena, s, bad, 4);
+        radix_sort_u64(sb, e, 2 * vbits, arena, s, bad, 4, hist0);
         k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, vbits, col_dst, bad);
         TAURUS_CHECK_LAUNCH();
     }

@@ -143,8 +143,13 @@ struct SortBuffers {
     uint32_t* vals[2];  // both null when no values are carried
     int cur;
 };
+// first_hist (optional): counts of bits [0, 8) of the keys in each tile of
+// RADIX_TILE keys, first_hist[digit * tiles + tile], written by the kernel
+// that produced the keys; it replaces the first pass's histogram when that
+// pass sorts an 8-bit digit.
+constexpr int RADIX_TILE = 4096;
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit);
+                    int bad_bit, const uint32_t* first_hist = nullptr);
 
 // In-edges grouped by destination, sources ascending (sample.hip): built once
 // per graph for the fanout sampler.  Complete when build_csc returns.

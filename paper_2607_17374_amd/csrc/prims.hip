@@ -684,11 +684,15 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
 }
 
 template <int DBITS>
-static void radix_pass(SortBuffers& b, int64_t n, int shift, int64_t nblocks, uint32_t* hist, uint64_t* offs,
-                       Arena& arena, hipStream_t s, int* bad, int bad_bit) {
+static void radix_pass(SortBuffers& b, int64_t n, int shift, int64_t nblocks, const uint32_t* pre, uint32_t* hist,
+                       uint64_t* offs, Arena& arena, hipStream_t s, int* bad, int bad_bit) {
     const int c = b.cur;
-    k_radix_hist<DBITS><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
-    TAURUS_CHECK_LAUNCH();
+    if (pre) {  // the tile histogram of this digit came with the keys
+        hist = const_cast<uint32_t*>(pre);
+    } else {
+        k_radix_hist<DBITS><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
+        TAURUS_CHECK_LAUNCH();
+    }
     scan_u32_to_u64(hist, offs, ((int64_t)1 << DBITS) * nblocks, false, arena, s);
     k_radix_scatter<DBITS><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks, hist,
                                                                     offs, b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
@@ -715,8 +719,9 @@ static std::vector<int> digit_schedule(int key_bits) {
     return c < p8 * cost[8] ? w : all8;
 }
 
+static_assert(RS_TILE == RADIX_TILE, "producers of first_hist tile the keys like the sort");
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit) {
+                    int bad_bit, const uint32_t* first_hist) {
     if (n <= 1 || key_bits <= 0) return;
     const int64_t nblocks = ceil_div(n, RS_TILE);
     if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
@@ -726,9 +731,10 @@ void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipSt
     uint64_t* offs = arena.alloc<uint64_t>(((int64_t)1 << wmax) * nblocks, "radix offsets");
     int shift = 0;
     for (int width : widths) {
-        if (width == 8) radix_pass<8>(b, n, shift, nblocks, hist, offs, arena, s, bad, bad_bit);
-        else if (width == 9) radix_pass<9>(b, n, shift, nblocks, hist, offs, arena, s, bad, bad_bit);
-        else radix_pass<10>(b, n, shift, nblocks, hist, offs, arena, s, bad, bad_bit);
+        const uint32_t* pre = shift == 0 && width == 8 ? first_hist : nullptr;
+        if (width == 8) radix_pass<8>(b, n, shift, nblocks, pre, hist, offs, arena, s, bad, bad_bit);
+        else if (width == 9) radix_pass<9>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
+        else radix_pass<10>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
         shift += width;
     }
     arena.free_ptr(offs);
