@@ -202,7 +202,11 @@ typedef struct {
     double ms_index;               /* of which: sampling and chunk-index build (0 when
                                       the plan already held the index)                  */
     double ms_gemm, ms_self, ms_scatter, ms_fixup;  /* ms_self stays 0: the self messages
-                                      run inside the scatter launch, timed in ms_scatter */
+                                      run inside the scatter launch, timed in ms_scatter.
+                                      In-core fp32 layers run a chunk's hub fix-up in the
+                                      next chunk's transform launch (timed in ms_gemm)
+                                      and the last chunk's at finalize (untimed), so
+                                      their ms_fixup stays 0                          */
     int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
     int64_t pool_rows;             /* budgeted layers: accumulator rows of the pool,
                                       hub rows included (0 in core)                     */
