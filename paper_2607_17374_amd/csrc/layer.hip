@@ -83,21 +83,18 @@ __global__ void k_out_norm(const int64_t* __restrict__ row_off, int64_t n, float
 
 // the same for a sampled layer: the out-degree counts u's kept edges (set
 // bits of the layer's mask over its CSR row)
-__global__ void k_out_norm_kept(const int64_t* __restrict__ row_off, const uint64_t* __restrict__ mask, int64_t n,
-                                float* __restrict__ n_out) {
+// Kept out-edges of row u from the kept edges before each CSR position:
+// before(i) = word_off[i / 64] + kept bits of mask word i / 64 below i.
+__global__ void k_out_norm_kept(const int64_t* __restrict__ row_off, const uint64_t* __restrict__ mask,
+                                const uint64_t* __restrict__ word_off, int64_t n, float* __restrict__ n_out) {
     const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (u >= n) return;
-    const int64_t b = row_off[u + 1];
-    int64_t kept = 0;
-    for (int64_t i = row_off[u]; i < b;) {
+    auto before = [&](int64_t i) {
         const int64_t w = i >> 6;
-        const int64_t end = min(b, (w + 1) << 6);
-        const int lo = (int)(i & 63), len = (int)(end - i);
-        uint64_t bits = mask[w] >> lo;
-        if (len < 64) bits &= (1ull << len) - 1;
-        kept += __popcll(bits);
-        i = end;
-    }
+        const int r = (int)(i & 63);
+        return (int64_t)word_off[w] + (r ? __popcll(mask[w] & ((1ull << r) - 1ull)) : 0);
+    };
+    const int64_t kept = before(row_off[u + 1]) - before(row_off[u]);
     n_out[u] = 1.0f / sqrtf((float)(kept + 1));
 }
 
@@ -1835,9 +1832,18 @@ static void layer_init(taurus_layer* L) {
     TAURUS_CHECK_LAUNCH();
     if (d.agg == TAURUS_GCN_SYM) {
         L->n_out = L->arena.alloc<float>(n, "source norms");
-        if (L->mask)
-            k_out_norm_kept<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, L->mask, n, L->n_out);
-        else
+        if (L->mask) {
+            // kept edges before each mask word (words + 1 entries: a row may
+            // end at e, a multiple of 64)
+            const int64_t words = std::max<int64_t>(1, ceil_div(g.e, 64));
+            Arena tmp(s);
+            uint32_t* wcnt = tmp.alloc<uint32_t>(words, "kept edges per mask word");
+            uint64_t* woff = tmp.alloc<uint64_t>(words + 1, "kept edges before each mask word");
+            k_mask_word_counts<<<(unsigned)ceil_div(words, T), T, 0, s>>>(L->mask, words, g.e, wcnt);
+            TAURUS_CHECK_LAUNCH();
+            scan_u32_to_u64(wcnt, woff, words, true, tmp, s);
+            k_out_norm_kept<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, L->mask, woff, n, L->n_out);
+        } else
             k_out_norm<<<(unsigned)ceil_div(n, T), T, 0, s>>>(g.row_off, n, L->n_out);
         TAURUS_CHECK_LAUNCH();
     }
