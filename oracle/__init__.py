@@ -14,6 +14,7 @@ from __future__ import annotations
 import ctypes
 import os
 import subprocess
+from typing import NamedTuple
 
 import numpy as np
 
@@ -91,7 +92,9 @@ def load(path: str):
     L.or_ta_step.restype = None
     L.or_ta_step.argtypes = [i64, vp, vp, vp, vp, vp, vp, vp]
     L.or_reorder_ta.restype = i32
-    L.or_reorder_ta.argtypes = [i64, vp, vp, vp, vp, vp, i32, vp, vp, vp]
+    L.or_reorder_ta.argtypes = [i64, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.or_dispersion.restype = ctypes.c_double
+    L.or_dispersion.argtypes = [i64, vp, vp, vp]
     return L
 
 
@@ -303,19 +306,37 @@ def ta_step(g: Graph, r: np.ndarray):
     return mu, r2
 
 
-def reorder_ta(g: Graph, pi0: np.ndarray | None = None, iterations: int = 5):
-    """Alg. 1 from bootstrap pi0 (identity if None) -> (new_of_old int32[n],
-    spans int64[iterations + 1] (C(pi0), then after each update; 0 past the
-    last update made), updates made).  Each update starts from the current
-    order as positions (r = pi) and ranks the new positions."""
+class TaResult(NamedTuple):
+    """Result of Alg. 1: the order, the real positions it ranks, and per update
+    (index 0 = the bootstrap) the total span C(pi) and the dispersion J(pi)."""
+    pi: np.ndarray          # int32[n], new ID of each vertex
+    positions: np.ndarray   # float64[n], r after the last update made
+    spans: np.ndarray       # int64[iterations + 1]; 0 past the last update made
+    disp: np.ndarray        # float64[iterations + 1]; 0 past the last update made
+    done: int               # updates made
+
+
+def reorder_ta(g: Graph, pi0: np.ndarray | None = None, iterations: int = 5) -> TaResult:
+    """Alg. 1 (Sec. 3.8) from bootstrap pi0 (identity if None): r = pi0 once,
+    then per update mu*, r*, pi = ArgSort(r) (ties by ID), carrying r forward,
+    until pi stops changing or after ``iterations`` updates."""
     pi = np.empty(g.n, np.int32)
+    pos = np.empty(g.n, np.float64)
     spans = np.zeros(iterations + 1, np.int64)
+    disp = np.zeros(iterations + 1, np.float64)
     done = ctypes.c_int(0)
     p0 = None if pi0 is None else np.ascontiguousarray(pi0, np.int32)
     if lib().or_reorder_ta(g.n, _p(g.row_off), _p(g.col_dst), _p(g.in_off), _p(g.in_src), _p(p0), iterations,
-                           _p(pi), _p(spans), ctypes.byref(done)):
+                           _p(pi), _p(pos), _p(spans), _p(disp), ctypes.byref(done)):
         raise MemoryError("or_reorder_ta")
-    return pi, spans, done.value
+    return TaResult(pi, pos, spans, disp, done.value)
+
+
+def dispersion(g: Graph, x: np.ndarray) -> float:
+    """J of Sec. 3.8 for positions x (float64[n], or the ranks of an order) at
+    the centres mu*(x), the self message in every neighbourhood."""
+    x = np.ascontiguousarray(x, np.float64)
+    return float(lib().or_dispersion(g.n, _p(g.in_off), _p(g.in_src), _p(x)))
 
 
 def total_span(g: Graph, pi: np.ndarray) -> int:

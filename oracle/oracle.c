@@ -29,15 +29,19 @@
  *   - the degree/BFS vertex ordering used as a topology-aware bootstrap
  *     (Sec. 3.8 discusses bandwidth-style bootstraps; the exact ordering
  *     rule is a reading of the text and is stated at or_reorder_bfs), the
- *     RCMK bootstrap and the topology-aware reordering of Alg. 1, with the
- *     total span C(pi) and the chunk-level residency profile A(t) (Sec. 3.8);
+ *     RCMK bootstrap and the topology-aware reordering of Alg. 1 (positions
+ *     initialised once from the bootstrap and carried across updates), with
+ *     the total span C(pi), the dispersion J and the chunk-level residency
+ *     profile A(t) (Sec. 3.8);
  *   - a slot-level simulation of a budgeted layer's residency with the
  *     fewest-pending eviction policy (Sec. 3.5.3) and the random, FIFO and
  *     LRU policies it is compared with (Sec. 4).
  *
  * Parity status: every function here is pinned by CPU tests (dense
- * adjacency-matrix products, closed forms, hand-worked small graphs,
- * brute force and the published SplitMix64 outputs); none is unpinned.
+ * adjacency-matrix products, closed forms, hand-worked small graphs -- Alg. 1
+ * worked by hand over two updates among them --, brute force and the
+ * published SplitMix64 outputs); none is unpinned.  The fixture generators
+ * live outside the oracle and have no external generator to match.
  */
 #include <math.h>
 #include <omp.h>
@@ -730,12 +734,10 @@ void or_active_profile(int64_t n, const int64_t* in_off, const int32_t* in_src, 
  *     rows fall short by M, the M candidates (holding a row, not hubs, not
  *     touched by chunk k, still pending) with the smallest (key, ID) are
  *     evicted.  Keys (Sec. 3.5.3 and the policies of the eviction study):
- *       0 fewest pending: min(pending, 16383);
+ *       0 fewest pending: pending(v), the exact count of messages due;
  *       1 random: H(seed, 7, k, v) >> 50;
  *       2 FIFO: the chunk at which v last took a row;
  *       3 LRU: the last chunk that touched v;
- *     chunk numbers >> s, s the smallest shift that fits the chunk count
- *     in 14 bits, then capped at 16383;
  *   - the asking vertices take rows (an evicted one is reloaded), the chunk's
  *     messages arrive, and touched vertices that completed free their rows.
  * Outputs the eviction and reload totals and reloads per vertex.  Returns 0,
@@ -787,9 +789,6 @@ int or_residency_sim(int64_t n, const int64_t* row_off, const int32_t* col_dst, 
     *reloads = 0;
     int rc = free_rows < 0 ? -6 : 0;
     int64_t nch = (n + chunk - 1) / chunk;
-    int cbits = 0;
-    while (cbits < 63 && ((int64_t)1 << cbits) <= nch - 1) cbits++;
-    int shift = cbits > 14 ? cbits - 14 : 0;
     for (int64_t k = 0; k < nch && rc == 0; k++) {
         int64_t b = k * chunk, e = b + chunk < n ? b + chunk : n;
         int64_t nt = 0, nq = 0;
@@ -814,13 +813,12 @@ int or_residency_sim(int64_t n, const int64_t* row_off, const int32_t* col_dst, 
                     uint64_t args[2] = {(uint64_t)k, (uint64_t)v};
                     key = (int64_t)(or_hash(seed, 7, 2, args) >> 50);
                 } else if (policy == 2) {
-                    key = adm[v] >> shift;
+                    key = adm[v];
                 } else if (policy == 3) {
-                    key = mark[v] >> shift;
+                    key = mark[v];
                 } else {
                     key = pend[v];
                 }
-                if (key > 16383) key = 16383;
                 cand[nc].key = key;
                 cand[nc].v = (int32_t)v;
                 nc++;
@@ -862,9 +860,8 @@ int or_residency_sim(int64_t n, const int64_t* row_off, const int32_t* col_dst, 
  * and ranks the vertices by r (Alg. 1).  N(v) holds v's propagated
  * in-neighbours and v itself -- every vertex aggregates a self message, so
  * d(v) = d_in(v) + 1 >= 1 -- hence {v : w in N(v)} = {w} and w's
- * out-neighbours.  Reading taken here: every sum is taken in fp64 in a
- * fixed order, the self term first and then the neighbours in ascending ID,
- * and ArgSort breaks ties by the lower vertex ID.
+ * out-neighbours.  Every sum is taken in fp64, the self term first and then
+ * the neighbours in ascending ID; ArgSort breaks ties by the lower vertex ID.
  *
  * One update: r_in -> mu -> r_out (CSR for the out-neighbours, in-lists for
  * the in-neighbours).
@@ -899,41 +896,81 @@ static int or_pos_cmp(const void* x, const void* y) {
 }
 
 /*
- * Alg. 1 from the bootstrap pi0 (new ID of each vertex; NULL = identity).
- * Each update takes the current order as the positions, r = pi, computes mu*
- * and then r*, and ranks r*: pi = ArgSort(r*).  (Reading taken here: the
- * ordering the sort yields is the position vector of the next update.)  An
- * update that leaves pi unchanged is a fixed point, so the loop stops there
- * and the result equals running every update.  spans[0] = C(pi0) and
- * spans[t] = C(pi) after update t (or_total_span); *done = updates made.
+ * The dispersion J of Sec. 3.8 for positions x, at the centres that
+ * minimise it for those positions:
+ *     mu(v) = (1/d(v)) sum_{u in N(v)} x(u),
+ *     J     = sum_v 1/d(v) sum_{u in N(v)} (x(u) - mu(v))^2,
+ * N(v) = v and its propagated in-neighbours (the self message), d(v) = |N(v)|.
+ * Two plain passes per vertex (centre, then squared deviations), fp64.
+ * Called with x = the ranks of an ordering, this is the J of that ordering.
+ */
+double or_dispersion(int64_t n, const int64_t* in_off, const int32_t* in_src, const double* x) {
+    double total = 0.0;
+#pragma omp parallel for reduction(+ : total) schedule(dynamic, 4096)
+    for (int64_t v = 0; v < n; v++) {
+        double d = (double)(in_off[v + 1] - in_off[v] + 1);
+        double s = x[v];
+        for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) s += x[in_src[k]];
+        double mu = s / d;
+        double q = (x[v] - mu) * (x[v] - mu);
+        for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) q += (x[in_src[k]] - mu) * (x[in_src[k]] - mu);
+        total += q / d;
+    }
+    return total;
+}
+
+/*
+ * Alg. 1 (Sec. 3.8) from the bootstrap order pi0 (new ID of each vertex;
+ * NULL = identity).  The real positions are initialised once, r(v) = pi0(v);
+ * each update then
+ *     1. sets the centres mu = mu*(r) from the current positions,
+ *     2. sets the positions r = r*(mu) from those centres,
+ *     3. ranks the positions, pi = ArgSort(r), ties by the lower vertex ID,
+ * and the loop ends once an update leaves pi unchanged (pi has converged) or
+ * after `iters` updates.  The positions r are carried from one update to the
+ * next; the ranks are only read off them.
+ * Outputs: pi_out (int32[n]); r_out (double[n] or NULL): the positions after
+ * the last update made (pi0 when none); spans[t] (or NULL) = C(pi_t), with
+ * pi_0 the bootstrap (or_total_span); disp[t] (or NULL) = J of the ordering
+ * pi_t, its ranks taken as positions (or_dispersion); *done = updates made.
  * Returns 0, or -3 when out of memory.
  */
 int or_reorder_ta(int64_t n, const int64_t* row_off, const int32_t* col_dst, const int64_t* in_off,
-                  const int32_t* in_src, const int32_t* pi0, int iters, int32_t* pi_out, int64_t* spans,
-                  int* done) {
-    double* r = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
-    double* r2 = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
-    double* mu = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
-    or_pos* pos = (or_pos*)malloc((size_t)(n > 0 ? n : 1) * sizeof(or_pos));
-    if (!r || !r2 || !mu || !pos) return -3;
-    for (int64_t v = 0; v < n; v++) pi_out[v] = pi0 ? pi0[v] : (int32_t)v;
+                  const int32_t* in_src, const int32_t* pi0, int iters, int32_t* pi_out, double* r_out,
+                  int64_t* spans, double* disp, int* done) {
+    size_t nn = (size_t)(n > 0 ? n : 1);
+    double* r = (double*)malloc(nn * sizeof(double));
+    double* r2 = (double*)malloc(nn * sizeof(double));
+    double* mu = (double*)malloc(nn * sizeof(double));
+    double* rank = (double*)malloc(nn * sizeof(double));
+    or_pos* pos = (or_pos*)malloc(nn * sizeof(or_pos));
+    if (!r || !r2 || !mu || !rank || !pos) { free(r); free(r2); free(mu); free(rank); free(pos); return -3; }
+    for (int64_t v = 0; v < n; v++) {
+        pi_out[v] = pi0 ? pi0[v] : (int32_t)v;
+        r[v] = (double)pi_out[v];
+        rank[v] = r[v];
+    }
     if (spans) spans[0] = or_total_span(n, in_off, in_src, pi_out);
+    if (disp) disp[0] = or_dispersion(n, in_off, in_src, rank);
     *done = 0;
     for (int t = 1; t <= iters; t++) {
-        for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];
         or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);
-        for (int64_t v = 0; v < n; v++) { pos[v].r = r2[v]; pos[v].v = (int32_t)v; }
+        memcpy(r, r2, nn * sizeof(double));
+        for (int64_t v = 0; v < n; v++) { pos[v].r = r[v]; pos[v].v = (int32_t)v; }
         qsort(pos, (size_t)n, sizeof(or_pos), or_pos_cmp);
         int changed = 0;
         for (int64_t k = 0; k < n; k++) {
             if (pi_out[pos[k].v] != (int32_t)k) changed = 1;
             pi_out[pos[k].v] = (int32_t)k;
+            rank[pos[k].v] = (double)k;
         }
         *done = t;
         if (spans) spans[t] = or_total_span(n, in_off, in_src, pi_out);
+        if (disp) disp[t] = or_dispersion(n, in_off, in_src, rank);
         if (n >= (1 << 24)) fprintf(stderr, "reorder_ta: update %d of %d done\n", t, iters);
         if (!changed) break;
     }
-    free(r); free(r2); free(mu); free(pos);
+    if (r_out) memcpy(r_out, r, (size_t)n * sizeof(double));
+    free(r); free(r2); free(mu); free(rank); free(pos);
     return 0;
 }

@@ -89,17 +89,37 @@ MUTANTS = {
     "ta_mu_without_self": (
         "double s = r_in[v];",
         "double s = 0.0;",
-        [lambda: P.test_ta_updates_are_the_minimisers(0), P.test_ta_special_cases]),
+        [lambda: P.test_ta_updates_are_the_minimisers(0), P.test_ta_special_cases, lambda: P.test_ta_worked_example(P_GOLDEN)]),
     # Alg. 1: out-neighbour centres not weighted by 1/d
     "ta_r_unweighted": (
         "num += mu[v] / dv;",
         "num += mu[v] / d;",
         [lambda: P.test_ta_updates_are_the_minimisers(0)]),
-    # Alg. 1: real positions carried over instead of the new order
-    "ta_keeps_real_positions": (
-        "for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];\n        or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);",
-        "if (t == 1) for (int64_t v = 0; v < n; v++) r[v] = (double)pi_out[v];\n        or_ta_step(n, row_off, col_dst, in_off, in_src, r, mu, r2);\n        memcpy(r, r2, (size_t)n * sizeof(double));",
-        [lambda: P.test_ta_order_is_a_permutation_with_consistent_spans(0), P.test_ta_updates_compose]),
+    # Alg. 1: each update restarts from the ranks instead of carrying r
+    "ta_resets_positions_to_ranks": (
+        "rank[pos[k].v] = (double)k;\n        }",
+        "rank[pos[k].v] = (double)k;\n        }\n        memcpy(r, rank, nn * sizeof(double));",
+        [lambda: P.test_ta_worked_example(P_GOLDEN), lambda: P.test_ta_positions_follow_dense_operator(0)]),
+    # Alg. 1: the loop runs on after the order has converged
+    "ta_ignores_convergence": (
+        "if (!changed) break;",
+        "(void)changed;",
+        [P.test_ta_special_cases, P.test_ta_stops_when_the_order_converges]),
+    # Alg. 1: ArgSort breaks ties by the higher ID
+    "ta_ties_by_higher_id": (
+        "return (a->v > b->v) - (a->v < b->v);\n}\n\n/*\n * The dispersion",
+        "return (a->v < b->v) - (a->v > b->v);\n}\n\n/*\n * The dispersion",
+        [P.test_ta_special_cases]),
+    # J without the 1/d(v) weight of each destination
+    "dispersion_unweighted": (
+        "total += q / d;",
+        "total += q;",
+        [lambda: P.test_dispersion_is_neighbourhood_variance(0)]),
+    # J's centre without the vertex's own position
+    "dispersion_centre_without_self": (
+        "double s = x[v];",
+        "double s = 0.0;",
+        [lambda: P.test_dispersion_is_neighbourhood_variance(0), lambda: P.test_ta_worked_example(P_GOLDEN)]),
     # RCMK: Cuthill-McKee order not reversed
     "rcm_not_reversed": (
         "new_of_old[queue[i]] = (int32_t)(n - 1 - i);",
@@ -117,8 +137,8 @@ MUTANTS = {
         [P.test_rcm_special_cases, P.test_rcm_matches_scipy]),
     # residency: LRU ranked by admission instead of last use
     "residency_lru_by_admission": (
-        "key = mark[v] >> shift;",
-        "key = adm[v] >> shift;",
+        "key = mark[v];",
+        "key = adm[v];",
         [lambda: P.test_residency_hand_cases("case1")]),
     # residency: the self message not counted in pending
     "residency_no_self_message": (
@@ -133,8 +153,13 @@ MUTANTS = {
     # residency: most pending evicted first
     "residency_most_pending_first": (
         "key = pend[v];",
-        "key = 16383 - (pend[v] < 16383 ? pend[v] : 16383);",
+        "key = -pend[v];",
         [lambda: P.test_residency_hand_cases("case1"), P.test_fewest_pending_reloads_least]),
+    # residency: pending counts capped at 14 bits
+    "residency_pending_capped": (
+        "key = pend[v];",
+        "key = pend[v] < 16383 ? pend[v] : 16383;",
+        [P.test_residency_fewest_pending_is_exact_above_16383]),
     # sampled GCN normalised by the full in-degree
     "gcn_sampled_full_in_degree": (
         "double din_hat = (double)m + 1.0;",

@@ -675,53 +675,162 @@ def test_ta_special_cases():
     g = _g(4, [(0, 1), (1, 2), (2, 3)])
     mu, r = O.ta_step(g, np.arange(4, dtype=np.float64))
     assert np.allclose(mu, [0, 0.5, 1.5, 2.5]) and np.allclose(r, [1 / 6, 1, 2, 2.5])
-    pi, spans, done = O.reorder_ta(g, None, 5)
-    # each of 1, 2, 3 spans itself and its predecessor
-    assert np.array_equal(pi, np.arange(4)) and done == 1 and spans[0] == spans[1] == 3
+    res = O.reorder_ta(g, None, 5)
+    # each of 1, 2, 3 spans itself and its predecessor; the order is unchanged
+    # by the first update, so the loop stops there
+    assert np.array_equal(res.pi, np.arange(4)) and res.done == 1 and res.spans[0] == res.spans[1] == 3
+    assert np.allclose(res.positions, [1 / 6, 1, 2, 2.5])
     # no edges: every vertex is its own neighbourhood, so nothing moves
     g = _g(5, [])
     boot = np.array([3, 0, 4, 1, 2], np.int32)
-    pi, spans, done = O.reorder_ta(g, boot, 5)
-    assert np.array_equal(pi, boot) and done == 1 and spans[0] == 0
+    res = O.reorder_ta(g, boot, 5)
+    assert np.array_equal(res.pi, boot) and res.done == 1 and res.spans[0] == 0 and res.disp[0] == 0
+    assert np.array_equal(res.positions, boot.astype(np.float64))
+    # a reciprocal pair 0 <-> 1 from ranks (2, 0): both centres and both
+    # positions are (2 + 0) / 2 = 1, which the isolated vertex 2 (rank 1)
+    # keeps too; the three-way tie is broken by ID, and the next update
+    # leaves it there
+    g = _g(3, [(0, 1), (1, 0)])
+    res = O.reorder_ta(g, np.array([2, 0, 1], np.int32), 5)
+    assert np.array_equal(res.positions, [1.0, 1.0, 1.0])
+    assert res.pi.tolist() == [0, 1, 2] and res.done == 2
+    # N(0) = N(1) = {0, 1}: ranks {2, 0} span 2 each (variance 1), then
+    # ranks {0, 1} span 1 each (variance 1/4)
+    assert res.spans[:3].tolist() == [4, 2, 2] and res.disp[:3].tolist() == [2.0, 0.5, 0.5]
 
 
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_ta_order_is_a_permutation_with_consistent_spans(seed):
-    rng = np.random.default_rng(seed + 120)
+def _golden_alg1(golden_dir):
+    from fractions import Fraction
+    vals = {}
+    for line in open(f"{golden_dir}/alg1_worked_example.txt"):
+        if line.startswith("#") or not line.strip():
+            continue
+        key, *rest = line.split()
+        vals[key] = rest
+    n = int(vals["n"][0])
+    edges = [tuple(int(x) for x in e.split(",")) for e in vals["edges"]]
+    fr = lambda k: [float(Fraction(x)) for x in vals[k]]
+    it = lambda k: [int(x) for x in vals[k]]
+    return n, edges, fr, it
+
+
+def test_ta_worked_example(golden_dir):
+    """Alg. 1 on the hand-worked graph of tests/golden: the positions are
+    carried across updates, so the second update reverses vertices 0 and 1
+    (restarting from the ranks would leave the order unchanged)."""
+    n, edges, fr, it = _golden_alg1(golden_dir)
+    g = _g(n, edges)
+    one = O.reorder_ta(g, None, 1)
+    assert one.done == 1 and one.pi.tolist() == it("pi1")
+    assert np.allclose(one.positions, fr("r1"), rtol=1e-15, atol=0)
+    two = O.reorder_ta(g, None, 2)
+    assert two.done == 2 and two.pi.tolist() == it("pi2")
+    assert np.allclose(two.positions, fr("r2"), rtol=1e-15, atol=0)
+    assert two.spans.tolist() == it("spans")
+    assert np.allclose(two.disp, fr("disp"), rtol=1e-15, atol=0)
+
+
+def _dense_alg1(n, u, v, pi0, updates):
+    """Alg. 1 as dense linear algebra: with Nm[v, w] = 1 when w is in N(v)
+    (v's in-neighbours and v), d = Nm 1, one update is the linear map
+    r -> (Nm^T D^-1 D^-1 Nm r) / (Nm^T D^-1 1), so the positions after t
+    updates are that map applied t times to the bootstrap ranks."""
+    Nm = np.eye(n)
+    Nm[v, u] = 1.0
+    d = Nm.sum(axis=1)
+    B = (Nm.T @ np.diag(1.0 / d**2) @ Nm) / (Nm.T @ (1.0 / d))[:, None]
+    r = pi0.astype(np.float64)
+    out = []
+    for _ in range(updates):
+        r = B @ r
+        out.append(r.copy())
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_ta_positions_follow_dense_operator(seed):
+    """Positions after t updates equal the dense map applied t times to the
+    bootstrap (the printed loop carries r); the order ranks them, ties by ID;
+    spans and J are those of each update's order."""
+    rng = np.random.default_rng(seed + 140)
+    n = 50
+    _, u, v = random_digraph(rng, n, 0.06, isolated=3)
+    g = O.Graph(n, u, v)
+    boot = rng.permutation(n).astype(np.int32)
+    rs = _dense_alg1(n, u, v, boot, 4)
+    for t in range(1, 5):
+        res = O.reorder_ta(g, boot, t)
+        if res.done < t:
+            break
+        want = rs[t - 1]
+        assert np.allclose(res.positions, want, rtol=1e-12, atol=1e-12 * n)
+        # the order sorts the positions (ties within rounding may go either way)
+        order = np.argsort(res.pi)
+        gaps = np.diff(want[order])
+        assert np.all(gaps > -1e-9 * n), gaps.min()
+        assert res.spans[t] == O.total_span(g, res.pi)
+        ranks = res.pi.astype(np.float64)
+        assert res.disp[t] == pytest.approx(O.dispersion(g, ranks), rel=1e-12)
+
+
+def test_ta_stops_when_the_order_converges():
+    """The loop ends at the first update that leaves pi unchanged, and not
+    before: every earlier update changed the order."""
+    rng = np.random.default_rng(150)
+    stops = []
+    for trial in range(6):
+        n = 12
+        _, u, v = random_digraph(rng, n, 0.15)
+        g = O.Graph(n, u, v)
+        boot = rng.permutation(n).astype(np.int32)
+        full = O.reorder_ta(g, boot, 40)
+        prev = boot
+        for t in range(1, full.done + 1):
+            cur = O.reorder_ta(g, boot, t)
+            assert cur.done == t
+            changed = not np.array_equal(cur.pi, prev)
+            if t < full.done:
+                assert changed, t
+            elif full.done < 40:
+                assert not changed
+            prev = cur.pi
+        stops.append(full.done)
+        if full.done < 40:
+            assert np.array_equal(prev, full.pi)
+            again = O.reorder_ta(g, boot, full.done + 3)
+            assert again.done == full.done and np.array_equal(again.pi, full.pi)
+    # the cases include loops that converge after more than one update
+    assert any(1 < d < 40 for d in stops), stops
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_dispersion_is_neighbourhood_variance(seed):
+    """J = sum_v 1/d(v) sum_{u in N(v)} (x(u) - mu(v))^2 with mu the mean over
+    N(v) is the sum of each neighbourhood's population variance (numpy var)."""
+    rng = np.random.default_rng(seed + 160)
+    n = 40
+    _, u, v = random_digraph(rng, n, 0.1, isolated=2)
+    g = O.Graph(n, u, v)
+    for x in (rng.permutation(n).astype(np.float64), rng.normal(size=n) * 7):
+        want = 0.0
+        for w in range(n):
+            nb = np.concatenate([[w], u[v == w]])
+            want += np.var(x[nb])
+        assert O.dispersion(g, x) == pytest.approx(want, rel=1e-12)
+
+
+def test_ta_order_is_a_permutation_with_consistent_spans():
+    rng = np.random.default_rng(120)
     _, u, v = random_digraph(rng, 60, 0.05, isolated=4)
     g = O.Graph(60, u, v)
     boot = rng.permutation(60).astype(np.int32)
-    pi, spans, done = O.reorder_ta(g, boot, 4)
-    assert np.array_equal(np.sort(pi), np.arange(60))
-    assert spans[0] == O.total_span(g, boot) and spans[done] == O.total_span(g, pi)
-    # each update ranks the positions computed from the previous order, ties by ID
-    prev = boot
-    for _ in range(done):
-        _, r = O.ta_step(g, prev.astype(np.float64))
-        order = np.lexsort((np.arange(60), r))
-        prev = np.empty(60, np.int32)
-        prev[order] = np.arange(60)
-    assert np.array_equal(pi, prev)
-
-
-def test_ta_updates_compose():
-    """An update depends on the current order only, so t updates equal t
-    single updates each started from the last order, and an unchanged order
-    is a fixed point (stopping there loses nothing)."""
-    rng = np.random.default_rng(130)
-    _, u, v = random_digraph(rng, 80, 0.04, isolated=3)
-    g = O.Graph(80, u, v)
-    boot = rng.permutation(80).astype(np.int32)
-    pi, spans, done = O.reorder_ta(g, boot, 8)
-    step, seen = boot, [O.total_span(g, boot)]
-    for _ in range(done):
-        step, sp, d1 = O.reorder_ta(g, step, 1)
-        assert d1 == 1
-        seen.append(int(sp[1]))
-    assert np.array_equal(step, pi) and seen == list(spans[:done + 1])
-    if done < 8:
-        again, _, d = O.reorder_ta(g, pi, 3)
-        assert np.array_equal(again, pi) and d == 1
+    res = O.reorder_ta(g, boot, 4)
+    assert np.array_equal(np.sort(res.pi), np.arange(60))
+    assert res.spans[0] == O.total_span(g, boot) and res.spans[res.done] == O.total_span(g, res.pi)
+    assert res.disp[0] == pytest.approx(O.dispersion(g, boot.astype(np.float64)), rel=1e-12)
+    # the order is the ranks of the returned positions, ties by ID
+    order = np.lexsort((np.arange(60), res.positions))
+    assert np.array_equal(res.pi[order], np.arange(60))
 
 
 def test_ta_lowers_span_on_skewed_rmat():
@@ -734,10 +843,12 @@ def test_ta_lowers_span_on_skewed_rmat():
     src, dst = WL.graph(w)
     g = O.Graph(w.n, src, dst)
     for boot in (None, O.reorder_bfs(g)):
-        pi, spans, done = O.reorder_ta(g, boot, 5)
-        assert done == 5
-        assert spans[1] < spans[0] and spans[5] < 0.75 * spans[0], spans
-        assert spans[5] == O.total_span(g, pi)
+        res = O.reorder_ta(g, boot, 5)
+        assert res.done == 5
+        assert res.spans[1] < res.spans[0] and res.spans[5] < 0.75 * res.spans[0], res.spans
+        assert res.spans[5] == O.total_span(g, res.pi)
+        # J of the order falls with the span (Sec. 3.8 reports the two track)
+        assert res.disp[5] < res.disp[0], res.disp
 
 
 # ---- RCMK bootstrap (Sec. 3.8 bootstraps Alg. 1 with it)
@@ -857,6 +968,41 @@ def test_residency_fifo_readmission():
     g = _g(7, [(0, 3), (1, 6), (5, 3)])
     ev, rl, per = O.residency_sim(g, 1, 2, 0, "fifo")
     assert (ev, rl) == (2, 2) and per.tolist() == [0, 0, 0, 1, 0, 0, 1]
+
+
+def big_pending_graph():
+    """Three destinations whose pending counts are all far above 16,383 when
+    one of them must go.  One source per chunk, a pool of 4 rows, no hubs.
+      chunk 0: vertex 0 sends to A = 1, B = 2, C = 3 (rows: 0, A, B, C);
+               0 has no in-edge, completes and frees its row;
+      chunks 1-3: the self messages of A, B and C (no new rows);
+      chunk 4: vertex 4 sends to 5: rows for 4 and 5, one free, so one of
+               A, B, C is evicted, the fewest pending;
+      chunk 5: 5 completes; chunks 6..: vertices 6.. send to A (20,000 of
+               them), B (the first 17,000) and C (the first 18,000).
+    Before chunk 4, pending = in-degree + 1 (self) - 1 (vertex 0) - 1 (own
+    chunk): A 20,000, B 17,000, C 18,000, so B is the victim; it is reloaded
+    at chunk 6 (two rows free then), and nothing else moves."""
+    src = [0, 0, 0, 4]
+    dst = [1, 2, 3, 5]
+    for j in range(20000):
+        w = 6 + j
+        src.append(w); dst.append(1)
+        if j < 17000:
+            src.append(w); dst.append(2)
+        if j < 18000:
+            src.append(w); dst.append(3)
+    return _g(6 + 20000, list(zip(src, dst)))
+
+
+def test_residency_fewest_pending_is_exact_above_16383():
+    """Sec. 3.5.3 ranks candidates by their exact pending count, however
+    large (a capped count would tie A, B and C and take the lowest ID, A)."""
+    g = big_pending_graph()
+    ev, rl, per = O.residency_sim(g, 1, 4, 0, "pending")
+    want = np.zeros(g.n, np.int32)
+    want[2] = 1
+    assert (ev, rl) == (1, 1) and np.array_equal(per, want), np.nonzero(per)
 
 
 @pytest.mark.parametrize("seed", [0, 1])
