@@ -275,27 +275,37 @@ int taurus_reorder(const taurus_graph* g, int32_t* new_of_old, void* stream);
 int taurus_reorder_rcm(const taurus_graph* g, int32_t* new_of_old, void* stream);
 
 /*
- * Topology-aware reordering (Sec. 3.8, Alg. 1): starting from the bootstrap
- * order pi0 (device int32[n], the new ID of each vertex, a permutation of
- * [0, n); NULL = the identity), up to `iterations` (>= 1) updates each take
- * the current order as positions r = pi and apply the dispersion minimisers
+ * Topology-aware reordering (Sec. 3.8, Alg. 1).  The real positions start
+ * from the bootstrap order, r(v) = pi0(v) (pi0: device int32[n], the new ID
+ * of each vertex, a permutation of [0, n); NULL = the identity), and each of
+ * up to `iterations` (>= 1) updates applies the two minimisers of the
+ * dispersion J (Sec. 3.8) to the current positions,
  *     mu(v) = (1/d(v)) sum_{u in N(v)} r(u)
  *     r(w)  = sum_{v : w in N(v)} mu(v)/d(v) / sum_{v : w in N(v)} 1/d(v)
  * with N(v) = v's in-neighbours plus v itself (the self message) and
- * d(v) = |N(v)|; then new_of_old = the ranks of r, ties by the lower ID.
- * An update that leaves the order unchanged is a fixed point: the loop stops
- * there, with the result of running every update.
- * Sums are fp64 in a fixed order (own term, then neighbours by ascending ID),
- * so the order is the same on every run.  Outputs: new_of_old (device
- * int32[n], written); spans (host int64[iterations + 1] or NULL): the total
- * span C(pi) = sum_v (max - min rank over v and its in-neighbours) of the
- * bootstrap, then after each update made; *updates (host, may be NULL):
- * updates made.
+ * d(v) = |N(v)|, then ranks them, pi = ArgSort(r) with ties by the lower ID.
+ * The positions carry over to the next update; the loop ends once an update
+ * leaves pi unchanged (pi has converged).
+ * Sums are fp64 in a fixed order of the library's own (the same on every
+ * run); they agree with a sequential sum within fp64 rounding, so an order
+ * can differ from one only between positions that close.
+ * Outputs:
+ *   new_of_old  device int32[n], written: the order after the last update;
+ *   positions   device double[n] or NULL: r after the last update made;
+ *   spans       host int64[iterations + 1] or NULL: the total span
+ *               C(pi) = sum_v (max - min rank over N(v)) of the bootstrap,
+ *               then of the order after each update made;
+ *   disp        host double[iterations + 1] or NULL: J of the same orders,
+ *               each order's ranks taken as positions with their optimal
+ *               centres, sum_v 1/d(v) sum_{u in N(v)} (rank(u) - mean)^2;
+ *   *updates    host, may be NULL: updates made.
+ * The caller owns every buffer.  Entries of spans and disp past the last
+ * update made are left as they were.
  * Errors: TAURUS_E_INVALID for a graph that is not a valid CSR, a pi0 that is
  * not a permutation, or iterations < 1.  Returns after the work completed.
  */
 int taurus_reorder_ta(const taurus_graph* g, const int32_t* pi0, int32_t iterations, int32_t* new_of_old,
-                      int64_t* spans, int32_t* updates, void* stream);
+                      double* positions, int64_t* spans, double* disp, int32_t* updates, void* stream);
 
 /*
  * CSR of the relabelled graph: edge (u, v) becomes (new_of_old[u],

@@ -77,7 +77,8 @@ SIGNATURES = {
     "taurus_reorder": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_rcm": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_reorder_ta": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
-                                         ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]),
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]),
     "taurus_relabel_graph": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_permute_rows": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,

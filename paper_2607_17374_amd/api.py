@@ -8,7 +8,7 @@ finalize / sampled_edges / destroy.
 from __future__ import annotations
 
 import ctypes
-from typing import Optional, Sequence
+from typing import NamedTuple, Optional, Sequence
 
 import numpy as np
 import torch
@@ -87,19 +87,31 @@ def reorder_rcm(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, stream=Non
     return out
 
 
+class TaOrder(NamedTuple):
+    """taurus_reorder_ta's outputs: the order and positions on the device, and
+    per update (index 0 = the bootstrap) C(pi) and J(pi) on the host."""
+    pi: torch.Tensor         # int32[n], new ID of each vertex
+    positions: torch.Tensor  # float64[n], r after the last update made
+    spans: np.ndarray        # int64[iterations + 1]
+    disp: np.ndarray         # float64[iterations + 1]
+    done: int                # updates made
+
+
 def reorder_ta(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, pi0: Optional[torch.Tensor] = None,
-               iterations: int = 5, stream=None):
+               iterations: int = 5, stream=None) -> TaOrder:
     """taurus_reorder_ta: topology-aware order (Alg. 1) from bootstrap pi0
-    (identity if None) -> (new_of_old int32[n] on the device, spans
-    int64[iterations + 1] (C(pi0), then after each update), updates made)."""
+    (identity if None)."""
     g = _graph(n, row_off, col_dst)
     out = torch.empty(n, dtype=torch.int32, device=row_off.device)
+    pos = torch.empty(n, dtype=torch.float64, device=row_off.device)
     spans = np.zeros(iterations + 1, dtype=np.int64)
+    disp = np.zeros(iterations + 1, dtype=np.float64)
     done = ctypes.c_int32(0)
     p0 = None if pi0 is None else _dev_ptr(pi0, torch.int32, "pi0")
-    N.check(N.lib().taurus_reorder_ta(ctypes.byref(g), p0, iterations, out.data_ptr(), spans.ctypes.data,
-                                      ctypes.byref(done), _stream_ptr(stream)), "taurus_reorder_ta")
-    return out, spans, done.value
+    N.check(N.lib().taurus_reorder_ta(ctypes.byref(g), p0, iterations, out.data_ptr(), pos.data_ptr(),
+                                      spans.ctypes.data, disp.ctypes.data, ctypes.byref(done),
+                                      _stream_ptr(stream)), "taurus_reorder_ta")
+    return TaOrder(out, pos, spans, disp, done.value)
 
 
 def relabel_graph(n: int, row_off: torch.Tensor, col_dst: torch.Tensor, new_of_old: torch.Tensor, stream=None):

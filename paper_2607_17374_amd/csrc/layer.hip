@@ -2279,8 +2279,8 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
 
 int reorder_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s);
 int reorder_rcm_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s);
-int reorder_ta_impl(const taurus_graph& g, const int32_t* pi0, int iters, int32_t* pi, int64_t* spans,
-                    int32_t* done, hipStream_t s);
+int reorder_ta_impl(const taurus_graph& g, const int32_t* pi0, int iters, int32_t* pi, double* positions,
+                    int64_t* spans, double* disp, int32_t* done, hipStream_t s);
 int relabel_impl(const taurus_graph& g, const int32_t* new_of_old, int64_t* row_off, int32_t* col_dst,
                  hipStream_t s);
 int permute_rows_impl(const void* in, void* out, int64_t n, int64_t row_bytes, const int32_t* new_of_old,
@@ -2375,13 +2375,14 @@ int taurus_reorder_rcm(const taurus_graph* g, int32_t* new_of_old, void* stream)
 }
 
 int taurus_reorder_ta(const taurus_graph* g, const int32_t* pi0, int32_t iterations, int32_t* new_of_old,
-                      int64_t* spans, int32_t* updates, void* stream) {
+                      double* positions, int64_t* spans, double* disp, int32_t* updates, void* stream) {
     return guarded([&] {
         check_graph_args(g);
         if (!new_of_old) fail(TAURUS_E_INVALID, "new_of_old is null");
         if (iterations < 1) fail(TAURUS_E_INVALID, "iterations=%d, at least 1", (int)iterations);
         int32_t done = 0;
-        const int rc = reorder_ta_impl(*g, pi0, iterations, new_of_old, spans, &done, static_cast<hipStream_t>(stream));
+        const int rc = reorder_ta_impl(*g, pi0, iterations, new_of_old, positions, spans, disp, &done,
+                                       static_cast<hipStream_t>(stream));
         if (updates) *updates = done;
         return rc;
     });

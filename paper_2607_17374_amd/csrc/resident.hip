@@ -15,16 +15,18 @@
 //      and without a slot are listed;
 //   2. if the free slots do not cover the list, victims are chosen among
 //      resident, non-hub, still-pending vertices the chunk does not touch,
-//      smallest policy key first, then lowest ID.  Keys (14 bits):
-//        fewest pending: min(pending messages, 16383);
+//      smallest policy key first, then lowest ID.  Keys:
+//        fewest pending: the exact count of pending messages;
 //        random:         the top 14 bits of H(seed, 7, k, v);
 //        FIFO:           the chunk at which v last took a row;
-//        LRU:            the last chunk that sent v a message;
-//      chunk numbers are shifted right until the layer's chunk count fits
-//      14 bits, and values past the last bin share it.  A 16,384-bin
-//      histogram of the keys gives the threshold; ties at the threshold are
-//      ranked by an exclusive scan in vertex order.  The key only decides
-//      which rows move, never the results;
+//        LRU:            the last chunk that sent v a message.
+//      A 16,384-bin histogram gives the threshold bin: pending counts of
+//      16,383 and more share the last bin, and chunk numbers are shifted
+//      right until the layer's chunk count fits 14 bits.  Candidates of a
+//      threshold bin that holds one key value are ranked by an exclusive
+//      scan in vertex order; those of a bin that holds several (the last
+//      pending bin, any shifted chunk bin) are sorted by (exact key, ID).
+//      The key only decides which rows move, never the results;
 //      their rows are written to the pinned host store and their slots freed;
 //   3. listed vertices take free slots; evicted ones copy their row back.
 // After the chunk, touched vertices that completed return their slots.
@@ -73,6 +75,15 @@ struct EvictKeys {
     const int32_t* adm;      // chunk at which v last took a row
 };
 
+// the exact key a coarse bin is refined by
+__device__ inline int64_t res_exact_key(int v, const EvictKeys& e) {
+    switch (e.policy) {
+        case TAURUS_EVICT_FIFO: return max(e.adm[v], 0);
+        case TAURUS_EVICT_LRU: return max(e.dc_mark[v], 0);
+        default: return max(e.cnt[v].x, 0);
+    }
+}
+
 __device__ inline int res_key(int v, int32_t k, const EvictKeys& e) {
     switch (e.policy) {
         case TAURUS_EVICT_RANDOM: {
@@ -105,6 +116,22 @@ __global__ void k_res_tie_flags(int64_t n, int32_t k, int32_t tau, const int32_t
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v >= n) return;
     tie[v] = res_candidate((int)v, k, slot_of, hub, e.dc_mark, e.cnt) && res_key((int)v, k, e) == tau ? 1 : 0;
+}
+
+// the candidates of a coarse threshold bin, keyed (exact key, ID)
+__global__ void k_res_tie_keys(int64_t n, const int32_t* __restrict__ tie, const int64_t* __restrict__ tie_rank,
+                               EvictKeys e, int idbits, uint64_t* __restrict__ keys, uint32_t* __restrict__ ids) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v >= n || !tie[v]) return;
+    const int64_t j = tie_rank[v];
+    keys[j] = ((uint64_t)res_exact_key((int)v, e) << idbits) | (uint64_t)v;
+    ids[j] = (uint32_t)v;
+}
+
+// the sorted position of each coarse-bin candidate becomes its tie rank
+__global__ void k_res_tie_ranks(const uint32_t* __restrict__ order, int64_t m, int64_t* __restrict__ tie_rank) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j < m) tie_rank[order[j]] = j;
 }
 
 __global__ void k_res_victims(int64_t n, int32_t k, int32_t tau, int64_t tie_take,
@@ -346,6 +373,26 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
         TAURUS_CHECK_LAUNCH();
         Arena tmp(s);
         scan_i32_to_i64(tie, tie_rank, n, false, tmp, s);
+        // a bin holding several key values: rank its candidates by (exact key, ID)
+        const bool coarse = (policy == TAURUS_EVICT_PENDING && tau == RES_BINS - 1) ||
+                            ((policy == TAURUS_EVICT_FIFO || policy == TAURUS_EVICT_LRU) && chunk_shift > 0);
+        const int64_t m_tie = (int64_t)hh[(size_t)tau];
+        if (coarse && m_tie > 1) {
+            const int idbits = std::max(1, bits_for(n - 1));
+            SortBuffers sb{{tmp.alloc<uint64_t>(m_tie, "eviction tie keys"),
+                            tmp.alloc<uint64_t>(m_tie, "eviction tie keys (ping-pong)")},
+                           {tmp.alloc<uint32_t>(m_tie, "eviction tie order"),
+                            tmp.alloc<uint32_t>(m_tie, "eviction tie order (ping-pong)")},
+                           0};
+            int* bad = tmp.alloc<int>(1, "sort flag");
+            fill_i32(bad, 1, 0, s);
+            k_res_tie_keys<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, tie, tie_rank, ek, idbits, sb.keys[0],
+                                                                 sb.vals[0]);
+            TAURUS_CHECK_LAUNCH();
+            radix_sort_u64(sb, m_tie, 31 + idbits, tmp, s, bad, 1);
+            k_res_tie_ranks<<<(unsigned)ceil_div(m_tie, T), T, 0, s>>>(sb.vals[sb.cur], m_tie, tie_rank);
+            TAURUS_CHECK_LAUNCH();
+        }
         unsigned long long* vcount = counters + 1;
         fill_i32(reinterpret_cast<int32_t*>(vcount), 2, 0, s);
         k_res_victims<<<(unsigned)ceil_div(n, T), T, 0, s>>>(n, k, tau, M - below, slot_of, hub, ek, tie_rank,

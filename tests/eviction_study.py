@@ -64,8 +64,9 @@ def study(w, check: bool) -> list:
     X = torch.from_numpy(WL.input_features(w)).cuda()
     spec = H.layer_specs(w)[0]
     rcm = T.reorder_rcm(w.n, row_off, col_dst)
-    ta, spans, done = T.reorder_ta(w.n, row_off, col_dst, rcm, 5)
-    say(f"Alg. 1 from RCMK: spans {spans[:done + 1].tolist()}")
+    res_ta = T.reorder_ta(w.n, row_off, col_dst, rcm, 5)
+    ta = res_ta.pi
+    say(f"Alg. 1 from RCMK: spans {res_ta.spans[:res_ta.done + 1].tolist()}")
     out_rows = []
     for order_name, perm in (("generator IDs", None), ("Alg. 1 order", ta)):
         if perm is None:

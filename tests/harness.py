@@ -184,3 +184,117 @@ def oracle_sampled_layers(w: WL.Workload, g, X: np.ndarray, ids: list, keeps: li
             H[need[li - 1]] = rows
             h_dtype = out_dt
     return out
+
+
+# ---- Alg. 1 (Sec. 3.8): GPU positions and orders against the oracle ------
+
+U64 = 2.0 ** -53   # unit roundoff of fp64
+
+
+def _gamma(k):
+    k = np.asarray(k, np.float64)
+    return k * U64 / (1.0 - k * U64)
+
+
+def ta_position_bound(g, updates: int) -> np.ndarray:
+    """Relative error bound rho(w) of the fp64 positions after ``updates``
+    updates of Alg. 1, valid for any summation order (the standard bound
+    gamma(k) = k u / (1 - k u) on a sum of k non-negative terms, errors of
+    non-negative inputs composed multiplicatively).  Per update:
+      centre of v, a sum of d(v) positions then two divisions:
+        1 + rho_q(v) = (1 + max_{N(v)} rho_r)(1 + gamma(d(v)))(1 + u)^2;
+      position of w, a sum over S(w) = {w} + out(w) of those terms divided by
+      a sum of the 1/d(v) (each rounded once):
+        1 + rho_r(w) = (1 + max_{S(w)} rho_q)(1 + gamma(|S(w)|))(1 + u)
+                       / (1 - ((1 + u)(1 + gamma(|S(w)|)) - 1)).
+    Both the GPU and the oracle are within rho(w) r_exact(w), so they differ
+    by at most 2 rho(w) r_exact(w)."""
+    n = g.n
+    din = np.diff(g.in_off).astype(np.int64)
+    dout = np.diff(g.row_off).astype(np.int64)
+    d = din + 1
+    s = dout + 1
+    rho = np.zeros(n)
+
+    def list_max(own, off, idx, lens):
+        # max of own[v] and x[idx[k]] over v's list (lists are contiguous)
+        out = own.copy()
+        if idx.size:
+            nz = lens > 0
+            seg = np.maximum.reduceat(own[idx], off[:-1][nz])
+            out[nz] = np.maximum(out[nz], seg)
+        return out
+
+    for _ in range(updates):
+        m = list_max(rho, g.in_off, g.in_src, din)
+        rq = (1 + m) * (1 + _gamma(d)) * (1 + U64) ** 2 - 1
+        mq = list_max(rq, g.row_off, g.col_dst, dout)
+        den = (1 + U64) * (1 + _gamma(s)) - 1
+        rho = (1 + mq) * (1 + _gamma(s)) * (1 + U64) / (1 - den) - 1
+    return rho
+
+
+def check_ta(g, gpu, ora, tag=""):
+    """Alg. 1 on the GPU (api.TaOrder) against the oracle (oracle.TaResult),
+    both after the same number of updates requested:
+    - the same number of updates made;
+    - positions within the rounding bound of ta_position_bound;
+    - the GPU order ranks its own positions, ties by ID (bit-exact);
+    - the GPU order sorts the oracle's positions except between positions
+      closer than their two bounds (near ties may fall either way), and each
+      vertex it ranks differently from the oracle sits at such a near tie;
+    - C(pi) of the GPU's order equals the oracle's span of that order, J(pi)
+      the oracle's dispersion of it within fp64 rounding; the bootstrap's
+      C and J equal the oracle's.
+    Returns the number of vertices whose rank differs from the oracle's."""
+    import oracle as O
+    n = g.n
+    assert gpu.done == ora.done, (tag, gpu.done, ora.done)
+    pos = gpu.positions.cpu().numpy()
+    pi = gpu.pi.cpu().numpy()
+    rho = ta_position_bound(g, ora.done)
+    tol = 2 * rho / (1 - rho) * np.abs(ora.positions) + 1e-300
+    err = np.abs(pos - ora.positions)
+    assert np.all(err <= tol), (tag, float((err / tol).max()), int(np.argmax(err / tol)))
+    order = np.argsort(pi, kind="stable")
+    assert np.array_equal(np.sort(pi), np.arange(n)), tag
+    assert np.array_equal(order, np.lexsort((np.arange(n), pos))), tag
+    ro = ora.positions[order]
+    slack = tol[order][:-1] + tol[order][1:]
+    gaps = ro[1:] - ro[:-1]
+    assert np.all(gaps >= -slack), (tag, float(gaps.min()))
+    t = ora.done
+    assert gpu.spans[t] == O.total_span(g, pi), tag
+    assert gpu.disp[t] == pytest_approx(O.dispersion(g, pi.astype(np.float64)), 1e-9), tag
+    assert gpu.spans[0] == ora.spans[0] and gpu.disp[0] == pytest_approx(ora.disp[0], 1e-9), tag
+    wrong = np.nonzero(pi != ora.pi)[0]
+    if wrong.size:
+        at_rank = np.empty(n, np.int64)
+        at_rank[ora.pi] = np.arange(n)
+        other = at_rank[pi[wrong]]
+        assert np.all(np.abs(ora.positions[wrong] - ora.positions[other]) <= tol[wrong] + tol[other]), tag
+    return int(wrong.size)
+
+
+def check_ta_updates(g, run_gpu, pi0, iterations, tag=""):
+    """check_ta after every update: run_gpu(t) runs t updates on the GPU.
+    Each prefix must repeat the full run's C and J (the GPU run is
+    deterministic), and every update's order is checked against the oracle's
+    run of that many updates.  Returns the full run and the ranks differing
+    (near ties) after each update."""
+    import oracle as O
+    full = run_gpu(iterations)
+    diffs = []
+    for t in range(1, full.done + 1):
+        got = full if t == full.done else run_gpu(t)
+        assert got.done == t, (tag, t, got.done)
+        assert np.array_equal(got.spans[:t + 1], full.spans[:t + 1]), (tag, t)
+        assert np.array_equal(got.disp[:t + 1], full.disp[:t + 1]), (tag, t)
+        diffs.append(check_ta(g, got, O.reorder_ta(g, pi0, t), f"{tag} after {t}"))
+    assert full.done == O.reorder_ta(g, pi0, iterations).done, tag
+    return full, diffs
+
+
+def pytest_approx(x, rel):
+    import pytest
+    return pytest.approx(x, rel=rel, abs=0)

@@ -182,9 +182,11 @@ def test_reorder_rcm_bit_exact(torch_cuda, case):
 
 @pytest.mark.parametrize("case", range(NCASES))
 @pytest.mark.parametrize("boot", ["identity", "bfs", "rcm"])
-def test_reorder_ta_bit_exact(torch_cuda, case, boot):
-    """Alg. 1 (topology-aware order) against the oracle: the order, the total
-    span after each update and the number of updates are equal."""
+def test_reorder_ta_matches_oracle(torch_cuda, case, boot):
+    """Alg. 1 (topology-aware order) against the oracle: the same number of
+    updates, positions within the fp64 rounding bound, an order that ranks
+    the oracle's positions (near ties aside), and C(pi), J(pi) of each
+    update's order."""
     import oracle as O
     import paper_2607_17374_amd as T
     name, n, src, dst = _cases()[case]
@@ -192,19 +194,56 @@ def test_reorder_ta_bit_exact(torch_cuda, case, boot):
     g = O.Graph(n, src, dst)
     row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(src).cuda(), torch_cuda.from_numpy(dst).cuda())
     p0 = {"identity": lambda: None, "bfs": lambda: O.reorder_bfs(g), "rcm": lambda: O.reorder_rcm(g)}[boot]()
-    pi, spans, done = T.reorder_ta(n, row_off, col_dst, None if p0 is None else torch_cuda.from_numpy(p0).cuda(), 6)
-    want, wspans, wdone = O.reorder_ta(g, p0, 6)
-    assert done == wdone
-    assert np.array_equal(pi.cpu().numpy(), want)
-    assert np.array_equal(spans, wspans)
+    p0d = None if p0 is None else torch_cuda.from_numpy(p0).cuda()
+    got, diffs = H.check_ta_updates(g, lambda t: T.reorder_ta(n, row_off, col_dst, p0d, t), p0, 6,
+                                    f"{name}/{boot}")
+    _note(f"  updates {got.done}, spans {got.spans[:got.done + 1].tolist()}, ranks differing (near ties) {diffs}")
+
+
+def test_reorder_ta_worked_example(torch_cuda):
+    """The two-update example worked by hand (tests/golden): positions carried
+    across updates reverse vertices 0 and 1 in the second update."""
+    import paper_2607_17374_amd as T
+    from tests.test_oracle_pins import _golden_alg1
+    from tests.conftest import ROOT
+    import os
+    n, edges, fr, it = _golden_alg1(os.path.join(ROOT, "tests", "golden"))
+    e = np.array(edges, np.int32)
+    row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(e[:, 0].copy()).cuda(),
+                                   torch_cuda.from_numpy(e[:, 1].copy()).cuda())
+    _note("reorder_ta worked example")
+    got = T.reorder_ta(n, row_off, col_dst, None, 2)
+    assert got.done == 2 and got.pi.cpu().numpy().tolist() == it("pi2")
+    assert np.allclose(got.positions.cpu().numpy(), fr("r2"), rtol=1e-15, atol=0)
+    assert got.spans.tolist() == it("spans")
+    assert np.allclose(got.disp, fr("disp"), rtol=1e-15, atol=0)
+
+
+def test_reorder_ta_hub_pieces(torch_cuda):
+    """Lists long enough to be cut into pieces on the GPU (a hub receiving
+    from and sending to 9,000 vertices, beside a sparse random graph)."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    rng = np.random.default_rng(7)
+    n = 20000
+    u = np.concatenate([rng.integers(1, n, 30000), np.arange(1, 9001), np.zeros(9000, np.int64)])
+    v = np.concatenate([rng.integers(1, n, 30000), np.zeros(9000, np.int64), np.arange(10001, 19001)])
+    src, dst = _simple(n, u, v)
+    _note(f"reorder_ta hub pieces: n={n} e={src.size}")
+    g = O.Graph(n, src, dst)
+    row_off, col_dst = T.build_csr(n, torch_cuda.from_numpy(src).cuda(), torch_cuda.from_numpy(dst).cuda())
+    boot = rng.permutation(n).astype(np.int32)
+    bd = torch_cuda.from_numpy(boot).cuda()
+    got, diffs = H.check_ta_updates(g, lambda t: T.reorder_ta(n, row_off, col_dst, bd, t), boot, 5, "hub pieces")
+    _note(f"  spans {got.spans[:got.done + 1].tolist()}, ranks differing (near ties) {diffs}")
 
 
 def test_reorder_ta_skewed_rmat_model(torch_cuda):
     """C5's recipe (skewed RMAT, random IDs, fp16 GCN) at 1/400 of the
-    vertices: the RCMK order and Alg. 1 from it and from the degree/BFS
-    order, bit-exact with the oracle, each lowering the total span; the
-    model on the Alg. 1 relabelled graph, un-permuted, matches the oracle in
-    the original IDs."""
+    vertices: the RCMK order bit-exact with the oracle, Alg. 1 from it and
+    from the degree/BFS order against the oracle, each lowering the total
+    span; the model on the Alg. 1 relabelled graph, un-permuted, matches the
+    oracle in the original IDs."""
     import oracle as O
     import paper_2607_17374_amd as T
     from paper_2607_17374_amd.api import torch_dtype
@@ -216,12 +255,13 @@ def test_reorder_ta_skewed_rmat_model(torch_cuda):
     row_off, col_dst = H.gpu_graph(w, src, dst)
     rcm = T.reorder_rcm(w.n, row_off, col_dst)
     assert np.array_equal(rcm.cpu().numpy(), O.reorder_rcm(g))
-    for boot in (rcm, T.reorder(w.n, row_off, col_dst)):
-        pi, spans, done = T.reorder_ta(w.n, row_off, col_dst, boot, 5)
-        want, wspans, wdone = O.reorder_ta(g, boot.cpu().numpy(), 5)
-        assert done == wdone and np.array_equal(pi.cpu().numpy(), want) and np.array_equal(spans, wspans)
-        _note(f"  spans {spans[:done + 1].tolist()}")
-        assert spans[done] < spans[0]
+    for bname, boot in (("rcm", rcm), ("bfs", T.reorder(w.n, row_off, col_dst))):
+        got, diffs = H.check_ta_updates(g, lambda t: T.reorder_ta(w.n, row_off, col_dst, boot, t),
+                                        boot.cpu().numpy(), 5, bname)
+        _note(f"  from {bname}: spans {got.spans[:got.done + 1].tolist()}, J {got.disp[:got.done + 1].tolist()}, "
+              f"ranks differing (near ties) {diffs}")
+        assert got.spans[got.done] < got.spans[0] and got.disp[got.done] < got.disp[0]
+    pi = got.pi
     r2, c2 = T.relabel_graph(w.n, row_off, col_dst, pi)
     xh = WL.input_features(w)
     X2 = T.permute_rows(torch.from_numpy(xh.view(np.int16)).cuda().view(torch_dtype(w.feat_dtype)), pi)

@@ -136,6 +136,84 @@ def test_eviction_policies_match_oracle_simulation(torch_cuda, policy):
     assert np.array_equal(hist, np.bincount(np.minimum(per, 63), minlength=64))
 
 
+def big_pending_graph(groups=4, per=4, chunks_per_group=48, chunk=512, seed=3):
+    """16 destinations with 13,500-24,600 in-edges each: chunk k's sources
+    send to the 4 destinations of group k mod 4, destination j keeping each
+    such edge with probability 1 - 0.03 j.  A pool of a few rows beyond one
+    chunk's 516 destinations must evict destinations of the other groups,
+    most of them with 16,383 or more pending messages early on."""
+    rng = np.random.default_rng(seed)
+    nch = groups * chunks_per_group
+    n = nch * chunk
+    nb = groups * per
+    big = (np.arange(nb) * (n // nb) + 7).astype(np.int64)
+    srcs, dsts = [], []
+    for k in range(nch):
+        gi = k % groups
+        u = np.arange(k * chunk, (k + 1) * chunk)
+        for j in range(per):
+            b = big[gi * per + j]
+            keep = rng.random(chunk) < 1.0 - 0.03 * (gi * per + j)
+            uu = u[keep]
+            uu = uu[uu != b]
+            srcs.append(uu)
+            dsts.append(np.full(uu.size, b))
+    return n, chunk, np.concatenate(srcs).astype(np.int32), np.concatenate(dsts).astype(np.int32)
+
+
+def test_fewest_pending_exact_above_histogram_range(torch_cuda):
+    """Fewest-pending eviction ranks candidates by their exact pending count
+    (Sec. 3.5.3) also where the counts pass the kernel's 14-bit histogram:
+    the per-vertex reload histogram and totals equal the oracle's
+    simulation, whose victims differ from those of capped counts on this
+    graph at pools of 518-524 rows."""
+    import oracle as O
+    import paper_2607_17374_amd as T
+    torch = torch_cuda
+    n, chunk, src, dst = big_pending_graph()
+    _note(f"eviction above the histogram range: n={n} e={src.size}")
+    s_d = torch.from_numpy(src).cuda()
+    d_d = torch.from_numpy(dst).cuda()
+    row_off, col_dst = T.build_csr(n, s_d, d_d)
+    rng = np.random.default_rng(11)
+    # wide rows, so that a pool of a few hundred rows is far below the dense
+    # accumulators and the layer runs under its budget
+    d_in, d = 16, 256
+    X = torch.from_numpy(rng.uniform(-1, 1, (n, d_in)).astype(np.float32)).cuda()
+    spec = dict(agg=O.SAGE_MEAN, d_in=d_in, d_out=d,
+                weight_cat=rng.uniform(-0.3, 0.3, (d_in, 2 * d)).astype(np.float32),
+                bias=np.zeros(d, np.float32), relu=False)
+    ref = torch.empty((n, d), dtype=torch.float32, device="cuda")
+    L = T.Layer(n, row_off, col_dst, out=ref, chunk=chunk, **spec)
+    L.push_all(X)
+    st0 = L.finalize()
+    L.destroy()
+    g = O.Graph(n, src, dst)
+    checked = 0
+    budget = H.pool_budget(st0, n, d, d_in, chunk, 520)
+    for attempt in range(4):
+        out = torch.empty_like(ref)
+        L = T.Layer(n, row_off, col_dst, out=out, chunk=chunk, hbm_budget=budget, hub_fraction=0.0,
+                    eviction="pending", **spec)
+        L.push_all(X)
+        st = L.finalize()
+        hist = L.reload_histogram(64)
+        L.destroy()
+        S = st["pool_rows"]
+        _note(f"  budget {budget}: pool {S} rows, {st['evictions']} evictions, {st['reloads']} reloads")
+        assert S > 0, "the layer did not run under its budget"
+        assert torch.equal(out, ref)
+        ev, rl, per = O.residency_sim(g, chunk, S, 0, "pending")
+        assert (st["evictions"], st["reloads"]) == (ev, rl)
+        assert np.array_equal(hist, np.bincount(np.minimum(per, 63), minlength=64))
+        if 518 <= S <= 524 and ev > 0:
+            checked += 1
+            break
+        # move the pool toward 520 rows (each row costs d_out * 4 + 4 bytes, planned with 1/8 room)
+        budget += (520 - S) * (d * 4 + 4) * 9 // 8
+    assert checked > 0
+
+
 def test_host_chunks_and_host_outputs(torch_cuda):
     """Chunks in pinned host memory (staged on the layer's copy stream) and
     outputs written straight into pinned host memory give the device run's
