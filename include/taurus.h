@@ -248,6 +248,26 @@ int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* ds
                      int64_t* row_off, int32_t* col_dst, void* stream);
 
 /*
+ * taurus_build_csr without allocating, for callers that cannot allocate
+ * device memory: code being captured into a HIP graph, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, result and errors as
+ * taurus_build_csr; it calls no hipMalloc, hipFree or other allocating
+ * routine.  Its temporaries live in one fixed device array of
+ * TAURUS_NOALLOC_SCRATCH_BYTES per GPU, which each GPU the library runs on
+ * holds from the first call on it until the process ends.
+ * Limit: e <= TAURUS_NOALLOC_MAX_EDGES; larger inputs return
+ * TAURUS_E_INVALID before any work is enqueued.
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind: calls that overlap on one GPU (other host threads, other streams)
+ * race and must be serialised by the caller.  Returns after the work
+ * completed (it reads back a validity flag into host memory).
+ */
+#define TAURUS_NOALLOC_SCRATCH_BYTES (32ll << 20)
+#define TAURUS_NOALLOC_MAX_EDGES (1ll << 20)
+int taurus_build_csr_noalloc(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                             int32_t* col_dst, void* stream);
+
+/*
  * Degree/BFS vertex ordering (Sec. 3.8: a topology-aware order in which a
  * destination's sources receive nearby ranks, shrinking the span between
  * its first and last message).  new_of_old (device int32[n], written) is

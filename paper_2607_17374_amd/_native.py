@@ -65,6 +65,8 @@ SIGNATURES = {
     "taurus_hash": (ctypes.c_uint64, [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_void_p]),
     "taurus_build_csr": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "taurus_build_csr_noalloc": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "taurus_layer_init": (ctypes.c_int, [ctypes.POINTER(Graph), ctypes.POINTER(LayerDesc),
                                          ctypes.POINTER(ctypes.c_void_p)]),
     "taurus_push_chunk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,

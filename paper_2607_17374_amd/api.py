@@ -66,6 +66,24 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
     return row_off, col_dst
 
 
+NOALLOC_MAX_EDGES = 1 << 20   # TAURUS_NOALLOC_MAX_EDGES
+
+
+def build_csr_noalloc(n: int, src: torch.Tensor, dst: torch.Tensor, row_off: torch.Tensor, col_dst: torch.Tensor,
+                      stream=None) -> None:
+    """taurus_build_csr_noalloc: the CSR build into caller-allocated row_off
+    (int64[n+1]) and col_dst (int32[e]) with no device allocation by the
+    library or by this wrapper; at most NOALLOC_MAX_EDGES edges."""
+    e = src.numel()
+    if row_off.numel() != n + 1 or col_dst.numel() != e:
+        raise ValueError("row_off must hold n + 1 and col_dst e entries")
+    N.check(N.lib().taurus_build_csr_noalloc(n, e, _dev_ptr(src, torch.int32, "src"),
+                                             _dev_ptr(dst, torch.int32, "dst"),
+                                             _dev_ptr(row_off, torch.int64, "row_off"),
+                                             _dev_ptr(col_dst, torch.int32, "col_dst") if e else None,
+                                             _stream_ptr(stream)), "taurus_build_csr_noalloc")
+
+
 def _graph(n: int, row_off: torch.Tensor, col_dst: torch.Tensor) -> N.Graph:
     e = col_dst.numel()
     return N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"), _dev_ptr(col_dst, torch.int32, "col_dst") if e else None)

@@ -2,6 +2,9 @@
 // sources are scanned in vertex order).  Built by a stable radix sort of the
 // (u, v) pairs packed into 64-bit keys; row offsets come from a binary search
 // of each row's first key in the sorted array.
+#include <algorithm>
+#include <mutex>
+
 #include "internal.hpp"
 
 namespace taurus {
@@ -58,13 +61,11 @@ __global__ void k_row_offsets(const uint64_t* __restrict__ keys, int64_t e, int6
     row_off[u] = lo;
 }
 
-int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
-                   int32_t* col_dst, hipStream_t s) {
-    if (n <= 0 || n >= ((int64_t)1 << 31) || e < 0 || e >= ((int64_t)1 << 40))
-        fail(TAURUS_E_INVALID, "taurus_build_csr: n=%lld e=%lld out of range", (long long)n, (long long)e);
-    if (!row_off || (e > 0 && (!src || !dst || !col_dst)))
-        fail(TAURUS_E_INVALID, "taurus_build_csr: null pointer");
-    Arena arena(s);
+// Enqueues the build with every temporary from `arena`; returns the device
+// flag word (bit 0: id out of range or self loop, bit 1: repeat, bit 2:
+// sort inconsistency), to be read after the stream's work.
+static int* enqueue_build_csr(Arena& arena, int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
+                              int64_t* row_off, int32_t* col_dst, hipStream_t s) {
     const int vbits = bits_for(n - 1) > 0 ? bits_for(n - 1) : 1;
     int* bad = arena.alloc<int>(1, "flag");
     fill_i32(bad, 1, 0, s);
@@ -82,13 +83,89 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
     }
     k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);
     TAURUS_CHECK_LAUNCH();
+    return bad;
+}
+
+static void check_build_args(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                             int32_t* col_dst) {
+    if (n <= 0 || n >= ((int64_t)1 << 31) || e < 0 || e >= ((int64_t)1 << 40))
+        fail(TAURUS_E_INVALID, "taurus_build_csr: n=%lld e=%lld out of range", (long long)n, (long long)e);
+    if (!row_off || (e > 0 && (!src || !dst || !col_dst)))
+        fail(TAURUS_E_INVALID, "taurus_build_csr: null pointer");
+}
+
+static void report_build_flags(int hbad) {
+    if (hbad & 1) fail(TAURUS_E_INVALID, "taurus_build_csr: vertex id out of range or self loop");
+    if (hbad & 2) fail(TAURUS_E_INVALID, "taurus_build_csr: repeated edge");
+    if (hbad & 4) fail(TAURUS_E_DEVICE, "taurus_build_csr: radix sort offset out of range");
+}
+
+int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                   int32_t* col_dst, hipStream_t s) {
+    check_build_args(n, e, src, dst, row_off, col_dst);
+    Arena arena(s);
+    int* bad = enqueue_build_csr(arena, n, e, src, dst, row_off, col_dst, s);
     int hbad = 0;
     Readback rb;
     rb.add(&hbad, bad, 1);
     rb.run(s);
-    if (hbad & 1) fail(TAURUS_E_INVALID, "taurus_build_csr: vertex id out of range or self loop");
-    if (hbad & 2) fail(TAURUS_E_INVALID, "taurus_build_csr: repeated edge");
-    if (hbad & 4) fail(TAURUS_E_DEVICE, "taurus_build_csr: radix sort offset out of range");
+    report_build_flags(hbad);
+    return TAURUS_OK;
+}
+
+// ---- the same build without allocating -------------------------------------
+// Its temporaries live in `scratch`, one fixed array per GPU, held from the
+// first call on that GPU until the process ends.  Host code never passes the
+// array's name to a kernel (that is a host-side stand-in): it uses the
+// device address hipGetSymbolAddress returns, looked up once per device.
+__device__ __align__(256) unsigned char scratch[TAURUS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+void* scratch_of_current_device() {
+    int dev = 0;
+    TAURUS_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= MAX_DEVICES) fail(TAURUS_E_DEVICE, "device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t rc = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (rc != hipSuccess || !p)
+            fail(TAURUS_E_DEVICE, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(rc));
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+}  // namespace
+
+// Scratch bytes the build takes for e edges, an upper bound: two key arrays,
+// the first-digit histogram, and per radix pass at most 1,024 buckets of
+// 4-byte counts and 8-byte offsets per tile plus the scan's block sums, each
+// block rounded to 256 bytes.
+int64_t build_csr_scratch_bytes(int64_t e) {
+    const int64_t tiles = ceil_div(std::max<int64_t>(e, 1), RADIX_TILE);
+    const int64_t buckets = 1024 * tiles;
+    const int64_t scan_blocks = ceil_div(buckets, 4096);
+    return 256 + 2 * (8 * std::max<int64_t>(e, 1) + 256) + (1024 * tiles + 256) + (4 * buckets + 256) +
+           (8 * buckets + 256) + 2 * (16 * scan_blocks + 256) + 4096;
+}
+
+int build_csr_noalloc_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                           int32_t* col_dst, hipStream_t s) {
+    check_build_args(n, e, src, dst, row_off, col_dst);
+    if (e > TAURUS_NOALLOC_MAX_EDGES || build_csr_scratch_bytes(e) > TAURUS_NOALLOC_SCRATCH_BYTES)
+        fail(TAURUS_E_INVALID, "taurus_build_csr_noalloc: %lld edges exceed the limit of %lld", (long long)e,
+             (long long)TAURUS_NOALLOC_MAX_EDGES);
+    void* base = scratch_of_current_device();
+    Arena arena(s, base, TAURUS_NOALLOC_SCRATCH_BYTES);
+    int* bad = enqueue_build_csr(arena, n, e, src, dst, row_off, col_dst, s);
+    int hbad = 0;
+    TAURUS_HIP(hipMemcpyAsync(&hbad, bad, sizeof(int), hipMemcpyDeviceToHost, s));
+    TAURUS_HIP(hipStreamSynchronize(s));
+    report_build_flags(hbad);
     return TAURUS_OK;
 }
 

@@ -86,6 +86,12 @@ private:
 class Arena {
 public:
     explicit Arena(hipStream_t s = nullptr, int64_t budget = 0) : stream_(s), budget_(budget) {}
+    // Fixed-region mode: allocations are carved, 256-byte aligned, out of
+    // [region, region + capacity) and never touch the device memory cache;
+    // running out is an error (TAURUS_E_INVALID).  free_ptr gives back the
+    // most recent block only.
+    Arena(hipStream_t s, void* region, int64_t capacity)
+        : stream_(s), region_(static_cast<char*>(region)), capacity_(capacity) {}
     ~Arena() { release(); }
     void set_stream(hipStream_t s) { stream_ = s; }
     Arena(const Arena&) = delete;
@@ -110,6 +116,12 @@ private:
     std::vector<Block> blocks_;
     hipStream_t stream_ = nullptr;
     int64_t budget_ = 0, bytes_ = 0, peak_ = 0;
+    // fixed-region mode: a stack of block starts (offsets), no heap use
+    static constexpr int REGION_STACK = 64;
+    char* region_ = nullptr;
+    int64_t capacity_ = 0, top_ = 0;
+    int64_t starts_[REGION_STACK] = {};
+    int nstarts_ = 0;
 };
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

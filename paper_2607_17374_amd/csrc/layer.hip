@@ -44,6 +44,8 @@ namespace taurus {
 
 int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
                    int32_t* col_dst, hipStream_t s);
+int build_csr_noalloc_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                           int32_t* col_dst, hipStream_t s);
 void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const float* rscale, float* Y,
               hipStream_t s);
 void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& packed);
@@ -2325,6 +2327,18 @@ int taurus_build_csr(int64_t n, int64_t e, const int32_t* src, const int32_t* ds
                      int32_t* col_dst, void* stream) {
     try {
         return build_csr_impl(n, e, src, dst, row_off, col_dst, static_cast<hipStream_t>(stream));
+    } catch (const Failure& f) {
+        return f.status;
+    } catch (const std::exception& x) {
+        set_error("internal error: %s", x.what());
+        return TAURUS_E_DEVICE;
+    }
+}
+
+int taurus_build_csr_noalloc(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
+                             int32_t* col_dst, void* stream) {
+    try {
+        return build_csr_noalloc_impl(n, e, src, dst, row_off, col_dst, static_cast<hipStream_t>(stream));
     } catch (const Failure& f) {
         return f.status;
     } catch (const std::exception& x) {

@@ -271,6 +271,17 @@ void Readback::run(hipStream_t s) {
 // ---------------------------------------------------------------- arena -----
 void* Arena::alloc_bytes(int64_t bytes, const char* what) {
     if (bytes <= 0) bytes = 16;
+    if (region_) {
+        const int64_t start = (top_ + 255) & ~(int64_t)255;
+        if (start + bytes > capacity_ || nstarts_ == REGION_STACK)
+            fail(TAURUS_E_INVALID, "scratch region of %lld bytes cannot hold %lld more bytes for %s",
+                 (long long)capacity_, (long long)bytes, what);
+        starts_[nstarts_++] = top_;
+        top_ = start + bytes;
+        bytes_ = top_;
+        if (bytes_ > peak_) peak_ = bytes_;
+        return region_ + start;
+    }
     const int64_t cls = (int64_t)size_class((size_t)bytes);
     if (budget_ > 0 && bytes_ + cls > budget_)
         fail(TAURUS_E_BUDGET, "allocating %lld bytes for %s exceeds the budget (%lld of %lld in use)",
@@ -292,6 +303,14 @@ void* Arena::alloc_bytes(int64_t bytes, const char* what) {
 }
 
 void Arena::free_ptr(void* p) {
+    if (region_) {
+        // the most recent block only: its start was recorded before alignment
+        if (nstarts_ > 0 && p == region_ + ((starts_[nstarts_ - 1] + 255) & ~(int64_t)255)) {
+            top_ = starts_[--nstarts_];
+            bytes_ = top_;
+        }
+        return;
+    }
     for (size_t i = blocks_.size(); i-- > 0;) {
         if (blocks_[i].p == p) {
             device_release(p, stream_);
@@ -303,6 +322,11 @@ void Arena::free_ptr(void* p) {
 }
 
 void Arena::release() {
+    if (region_) {
+        top_ = bytes_ = 0;
+        nstarts_ = 0;
+        return;
+    }
     for (auto& b : blocks_) device_release(b.p, stream_);
     blocks_.clear();
     bytes_ = 0;

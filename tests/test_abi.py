@@ -69,6 +69,10 @@ def test_invalid_arguments_rejected_before_device_work(native):
     assert L.taurus_finalize(None, None) == native.E_INVALID
     assert L.taurus_sampled_edges(None, None, None) == native.E_INVALID
     assert L.taurus_build_csr(0, 0, None, None, None, None, None) == native.E_INVALID
+    # the allocation-free build refuses more edges than its scratch holds,
+    # before touching any pointer or the device
+    assert L.taurus_build_csr_noalloc(10, (1 << 20) + 1, 8, 8, 8, 8, None) == native.E_INVALID
+    assert "exceed the limit" in native.last_error()
     L.taurus_layer_destroy(None)
     L.taurus_plan_destroy(None)
     hp = ctypes.c_void_p()
