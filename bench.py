@@ -1,21 +1,35 @@
 """Benchmark: layer-wise broadcast GNN inference on one MI355X.
 
-Workload: 2-layer GCN (symmetric normalisation with self loops), exact,
-RMAT(0.57, 0.19, 0.19) graph with 1,000,000 vertices and 20,000,000 edges,
-N(0,1) fp32 features of width 128, layer widths 128 -> 128 -> 64, sources
-streamed in 65,536-vertex chunks.  Inputs (edge list, features) are seeded
-synthetic data resident in HBM before the timed region.
+Default workload (the largest configuration one GPU holds in core):
+sage3-fanout-rmat-100m -- 3-layer GraphSAGE-mean, fanout-sampled (15, 10, 5)
+by hash rank, on an RMAT(0.57, 0.19, 0.19) graph with 100,000,000 vertices
+and 1,600,000,000 edges; N(0,1) bf16 features of width 128 with fp32
+accumulation; layer widths 128 -> 256 -> 256 -> 172; 65,536-vertex source
+chunks.  Inputs (edge list, features) are seeded synthetic data, generated on
+the host and resident in HBM before any timed region.
 
-One step = the whole hot path once: CSR build from the edge list, then for
-each layer init (the chunk index, built by layer 1 and shared with layer 2
-through a plan; pending counts, weights), all chunk pushes (MFMA transform,
-scatter with the self messages and fused finalise, fix-up) and finalize.
+One step = the whole hot path once: the CSR build from the edge list, then
+per layer the in-edge lists (first layer) and the fanout sampler, layer init
+(pending counts, the chunk index of the kept edges, weights), every chunk
+push (MFMA transform, scatter-aggregate with arrival counters, self messages
+and the fused finalise) and finalize, each layer's output feeding the next.
+The CSR build and the layers are timed in two loops of K repetitions each
+(the edge list is freed after the first loop: with it resident, the three
+layers' buffers do not fit in HBM), and a step's time is their sum.
 
-Output: one JSON line.  value = aggregated edges per second per layer
-(sum over layers of the propagated edges / step time) in GTEPS.  roofline =
-the scatter kernel's algorithmic HBM bytes over its HIP-event-timed
-duration, against 8 TB/s.  cpu_baseline = the CPU oracle timed on this
-host over the same workload.
+Output: one JSON line.  value = aggregated edges per second per layer (the
+propagated edges of all layers / step time) in GTEPS.  roofline = the
+scatter kernel's algorithmic HBM bytes over its HIP-event-timed launches,
+against 8 TB/s.  gemm_roofline = the transform's flops over its
+HIP-event-timed launches (a separate untimed pass), against
+min(bf16 MFMA peak, arithmetic intensity x HBM bandwidth).  cpu_baseline =
+the CPU oracle on a bounded sample: its in-lists and sampler over the whole
+graph, and the layer maths for 65,536 seeded destinations plus the 256
+largest in-degrees and up to 256 without in-edges per layer, each layer fed
+the GPU's previous layer; the same sample checks the GPU's outputs.
+
+--workload gcn2-rmat-1m (with --variant) runs the 1M-vertex in-memory
+workloads instead (2-layer GCN / GIN / GAT, exact or sampled).
 """
 from __future__ import annotations
 
@@ -32,6 +46,7 @@ if ROOT not in sys.path:
 METRIC = "aggregated edges/sec per layer (GTEPS) + % HBM/host-link roofline, 1 GPU"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0
 
 
 # Model variants on the same graph and features: (family, fanouts per layer,
@@ -247,8 +262,12 @@ def summarize_profile(trace_dir: str, fetch_dir: str, write_dir: str) -> str:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 3, or 10 for gcn2-rmat-1m)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 1, or 2 for gcn2-rmat-1m)")
+    ap.add_argument("--workload", choices=["sage3-fanout-rmat-100m", "gcn2-rmat-1m"],
+                    default="sage3-fanout-rmat-100m")
+    ap.add_argument("--scale", type=int, default=1,
+                    help="sage3-fanout-rmat-100m only: divide vertices and edges by this (trial runs; not a result)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--full-profile", action="store_true",
@@ -256,7 +275,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy, the reference kernel for HBM byte counters")
     ap.add_argument("--variant", choices=sorted(VARIANTS), default="gcn",
-                    help="model family on the same graph (default: the exact GCN workload)")
+                    help="gcn2-rmat-1m only: model family on the same graph (default: the exact GCN workload)")
     ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="print the profile summary of a kernel-trace run and FETCH_SIZE / WRITE_SIZE runs")
     args = ap.parse_args()
@@ -267,7 +286,16 @@ def main():
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the path has no multi-GPU mode)", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "gcn2-rmat-1m":
+        args.steps = 10 if args.steps is None else args.steps
+        args.warmup = 2 if args.warmup is None else args.warmup
+        return bench_rmat_1m(args)
+    args.steps = 3 if args.steps is None else args.steps
+    args.warmup = 1 if args.warmup is None else args.warmup
+    return bench_sage3_100m(args)
 
+
+def bench_rmat_1m(args):
     import numpy as np
     import torch
     import fixtures as F
@@ -433,6 +461,275 @@ def main():
         "roofline": roofline,
         "gemm_roofline": gemm,
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def sampled_scatter_bytes(st: dict, n: int, d_o: int, out_bytes: int, sage: bool) -> float:
+    """Algorithmic HBM bytes of one layer's scatter launches, from the
+    library's statistics.  Per work unit 16 (its descriptor); per message 4
+    (the source's row code); the chunk transform's rows once -- every
+    vertex's self row and, for GraphSAGE, each source's aggregation row
+    (4 d_o each); one flag byte per vertex (self pass); per flush 12 (counts
+    read and written); the accumulator row read on every flush but a
+    vertex's first and written on every flush but its last (a vertex's first
+    and last flush are one each of its P flushes), and its output row once.
+    Exact when no segment is split into pieces, which holds for fanouts up to
+    15 (a segment then holds at most 15 messages and the self message)."""
+    if st["split_segments"]:
+        raise ValueError("the byte model holds for layers without split segments")
+    P = st["pairs"]
+    units = st["short_units"] + st["wave_units"]
+    y_rows = n * (2 if sage else 1)
+    return (16.0 * units + 4.0 * st["messages"] + 4.0 * d_o * y_rows + 1.0 * n + 12.0 * P
+            + 8.0 * d_o * (P - n) + out_bytes * d_o * n)
+
+
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def destination_sample(seed: int, deg_in, count: int = 65536):
+    """count seeded uniform destinations, the 256 largest in-degrees (ties by
+    lower ID) and up to 256 vertices without in-edges, sorted."""
+    import numpy as np
+    n = deg_in.size
+    rng = np.random.default_rng(seed)
+    uni = rng.choice(n, min(count, n), replace=False)
+    cand = np.argpartition(-deg_in.astype(np.int64), 256)[:512] if n > 512 else np.arange(n)
+    top = cand[np.lexsort((cand, -deg_in[cand].astype(np.int64)))][:256]
+    zero = np.flatnonzero(deg_in == 0)[:256]
+    return np.unique(np.concatenate([uni, top, zero]).astype(np.int64))
+
+
+def bench_sage3_100m(args):
+    import numpy as np
+    import torch
+    import fixtures as F
+    from fixtures import workloads as WL
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    from tests import harness as H
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t_start = time.perf_counter()
+
+    def say(msg):
+        print(f"[bench {time.perf_counter() - t_start:7.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    w = WL.SAGE_FANOUT_RMAT_100M
+    if args.scale > 1:
+        w = w.scaled(n=w.n // args.scale, e=w.e // args.scale)
+    specs = H.layer_specs(w)
+    nl = len(specs)
+    src, dst = WL.graph(w)
+    say(f"{w.name}: edge list {src.size} edges")
+    xh = WL.input_features(w)
+    say("features")
+    X = torch.from_numpy(xh.view(np.int16)).to(dev).view(torch_dtype(w.feat_dtype))
+    src_d = torch.from_numpy(src).to(dev)
+    dst_d = torch.from_numpy(dst).to(dev)
+    # output buffers: layer 1 and layer 3 share one (layer 1's output is dead
+    # once layer 2 has run), layer 2 has its own
+    nbytes = [w.n * s["d_out"] * (4 if s["out_dtype"] == F.F32 else 2) for s in specs]
+    buf_a = torch.empty(max(nbytes[0], nbytes[2]), dtype=torch.uint8, device=dev)
+    buf_b = torch.empty(nbytes[1], dtype=torch.uint8, device=dev)
+
+    def out_view(li):
+        buf = buf_b if li == 1 else buf_a
+        dt = torch_dtype(specs[li]["out_dtype"])
+        return buf[:nbytes[li]].view(dt).view(w.n, specs[li]["d_out"])
+
+    # ---- a1: the CSR build, K timed builds while the edge list is resident
+    for _ in range(args.warmup):
+        row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+        del row_off, col_dst
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+    torch.cuda.synchronize()
+    csr_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    say(f"CSR build {csr_ms:.1f} ms")
+    del src_d, dst_d
+    torch.cuda.empty_cache()
+
+    # ---- a3-a11: sampler and the three layers, K timed passes
+    def layers_pass(profile, hook=None):
+        per = []
+        plan = T.Plan(w.n, row_off, col_dst, w.chunk)
+        h = X
+        for li in range(nl):
+            out = out_view(li)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            L = T.Layer(w.n, row_off, col_dst, out=out, chunk=w.chunk, profile=profile, plan=plan, **specs[li])
+            L.push_all(h)
+            st = L.finalize()
+            torch.cuda.synchronize()
+            st["wall_ms"] = (time.perf_counter() - t0) * 1e3
+            if hook:
+                hook(li, L, out)
+            L.destroy()
+            per.append(st)
+            h = out
+        plan.destroy()
+        return per
+
+    profile = 0 if args.no_profile else 2
+    for _ in range(args.warmup):
+        layers_pass(profile)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    runs = [layers_pass(profile) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    layers_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_step = csr_ms + layers_ms
+    say(f"layers {layers_ms:.1f} ms per pass")
+
+    layers = []
+    sc_bytes = sc_ms = 0.0
+    sc_launches = 0
+    for li in range(nl):
+        sts = [r[li] for r in runs]
+        st = sts[-1]
+        d_o, d_in = specs[li]["d_out"], specs[li]["d_in"]
+        ob = 4 if specs[li]["out_dtype"] == F.F32 else 2
+        wall = float(np.mean([x["wall_ms"] for x in sts]))
+        kb = sampled_scatter_bytes(st, w.n, d_o, ob, sage=True)
+        ms_sc = float(np.mean([x["ms_scatter"] for x in sts]))
+        if profile:
+            sc_bytes += kb * len(sts)
+            sc_ms += sum(x["ms_scatter"] for x in sts)
+            sc_launches += sum(x["launches_scatter"] for x in sts)
+        layers.append({
+            "layer": li + 1, "d_in": d_in, "d_out": d_o, "fanout": specs[li]["fanout"], "edges": st["messages"],
+            "pairs": st["pairs"], "wall_ms": round(wall, 3), "gteps": round(st["messages"] / (wall * 1e-3) / 1e9, 4),
+            "vertices_per_s": round(w.n / (wall * 1e-3), 1),
+            "init_ms": round(float(np.mean([x["ms_init"] for x in sts])), 3),
+            "sample_and_index_ms": round(float(np.mean([x["ms_index"] for x in sts])), 3),
+            "scatter_ms": round(ms_sc, 3), "scatter_algorithmic_gb": round(kb / 1e9, 3),
+            "scatter_gbs": round(kb / (ms_sc * 1e-3) / 1e9, 1) if ms_sc > 0 else None,
+            "short_units": st["short_units"], "wave_units": st["wave_units"],
+        })
+    total_edges = sum(l["edges"] for l in layers)
+    value = total_edges / (ms_step * 1e-3) / 1e9
+    roofline = None
+    if profile and sc_ms > 0:
+        achieved = sc_bytes / (sc_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_scatter",
+                    "avg_launch_us": round(sc_ms * 1e3 / sc_launches, 2),
+                    "bytes_per_launch": round(sc_bytes / sc_launches, 0)}
+
+    # ---- untimed pass with events around every kernel (transform figures),
+    # copying out the rows the oracle sample reads
+    cpu = check = None
+    gemm = None
+    need_rows = {}
+    got_rows = {}
+    ids = keeps = g = None
+    t_or = {}
+    if not args.no_cpu_baseline:
+        import oracle as O
+        t0 = time.perf_counter()
+        g = O.EdgeGraph(w.n, src, dst)
+        t_or["in_lists"] = time.perf_counter() - t0
+        say(f"oracle in-lists {t_or['in_lists']:.1f} s")
+        ids, keeps, kept_in_sample = [], [], []
+        for li in range(1, nl + 1):
+            t0 = time.perf_counter()
+            _, keep_in, m = O.sample(g, w.seed, li, w.fanout(li))
+            t_or[f"sample_{li}"] = time.perf_counter() - t0
+            keeps.append(keep_in)
+            ids.append(destination_sample(w.seed * 1000 + li, g.deg_in))
+            kept_in_sample.append(int(m[ids[-1]].sum()))
+            # rows of layer li's input the oracle reads: the destinations and their kept in-neighbours
+            need_rows[li] = np.unique(np.concatenate([ids[-1], H.in_neighbours(g, ids[-1], keep_in)]))
+            say(f"oracle sampler layer {li}: {t_or[f'sample_{li}']:.1f} s, {len(need_rows[li])} input rows needed")
+
+    def hook(li, L, out):
+        if need_rows:
+            if li + 1 < nl:
+                got_rows[("in", li + 2)] = out.index_select(0, torch.from_numpy(need_rows[li + 2]).to(dev)).cpu()
+            got_rows[("out", li + 1)] = out.index_select(0, torch.from_numpy(ids[li]).to(dev)).cpu()
+
+    per = layers_pass(1, hook)
+    gf = gb = gms = 0.0
+    for li, st in enumerate(per):
+        d_in, d_o = specs[li]["d_in"], specs[li]["d_out"]
+        gf += 2.0 * w.n * d_in * 2 * d_o
+        gb += w.n * d_in * 2.0 + w.n * 2 * d_o * 4.0       # bf16 rows in, fp32 transform rows out
+        gms += st["ms_gemm"]
+        layers[li]["gemm_ms"] = round(st["ms_gemm"], 3)
+    if gms > 0:
+        tf = gf / (gms * 1e-3) / 1e12
+        ai = gf / gb
+        cap = min(BF16_MFMA_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
+        gemm = {"bound": "mfma" if cap >= BF16_MFMA_PEAK_TFLOPS else "hbm", "achieved": round(tf, 2),
+                "peak": round(cap, 1), "unit": "TFLOP/s", "frac": round(tf / cap, 4),
+                "mfma_peak": BF16_MFMA_PEAK_TFLOPS, "ai_flop_per_byte": round(ai, 1),
+                "achieved_gbs": round(gb / (gms * 1e-3) / 1e9, 1), "kernel": "k_gemm_panel (bf16)",
+                "note": "untimed pass with events around every kernel"}
+
+    if need_rows:
+        import oracle as O
+        zs_cmp = []
+        t_layer = {}
+        for li in range(1, nl + 1):
+            p = WL.layer_params(w, li)
+            in_dt, out_dt = w.layer_dtypes(li)
+            if li == 1:
+                Hin = xh
+            else:
+                rows = got_rows[("in", li)]
+                Hin = np.zeros((w.n, rows.shape[1]), np.uint16 if in_dt != F.F32 else np.float32)
+                Hin[need_rows[li]] = rows.view(torch.int16).numpy().view(np.uint16) if in_dt != F.F32 else rows.numpy()
+            t0 = time.perf_counter()
+            z = O.layer(w.agg, g, Hin, in_dt, p.W, p.b, li < nl, keep_in=keeps[li - 1], dst_ids=ids[li - 1])
+            t_layer[li] = time.perf_counter() - t0
+            y = H.to_numpy_f64(got_rows[("out", li)], out_dt)
+            r = H.compare(y, z, H.RTOL[w.feat_dtype])
+            zs_cmp.append({"layer": li, "destinations": int(len(ids[li - 1])), "mismatches": r["n_bad"],
+                           "max_abs": r["max_abs"], "mean_rel": r["mean_rel"]})
+            say(f"oracle layer {li}: {t_layer[li]:.2f} s, mismatches {r['n_bad']} of {len(ids[li - 1])}")
+            del Hin
+        check = zs_cmp
+        t_sample_work = t_or["in_lists"] + sum(t_or[f"sample_{li}"] for li in range(1, nl + 1))
+        t_layers_sample = sum(t_layer.values())
+        t_extrap = t_sample_work + sum(t_layer[li] * w.n / len(ids[li - 1]) for li in range(1, nl + 1))
+        cpu = {"value": round(total_edges / t_extrap / 1e9, 6), "unit": "GTEPS", "cores": O.threads(),
+               "kind": "oracle", "cpu_model": _cpu_model(), "seconds": round(t_sample_work + t_layers_sample, 2),
+               "extrapolated_full_step_s": round(t_extrap, 1),
+               "sample": "in-lists and the fanout sampler of all three layers over the whole graph "
+                         f"({t_sample_work:.1f} s), then the layer maths for 65,536 seeded destinations, the 256 "
+                         "largest in-degrees and up to 256 without in-edges per layer, each fed the GPU's previous "
+                         f"layer ({t_layers_sample:.2f} s); value = all layers' {total_edges / 1e6:.0f}M propagated "
+                         "edges / the full step extrapolated linearly from the sampled destinations (extrapolated)"}
+
+    line = {
+        "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: 3-layer GraphSAGE-mean 128->256->256->172, fanouts (15, 10, 5) by "
+                               "hash rank; RMAT(0.57,0.19,0.19) "
+                               f"{w.n:,} vertices / {w.e:,} edges; N(0,1) bf16 features, fp32 accumulation; "
+                               f"{w.chunk:,}-vertex source chunks; step = CSR build + per layer sampler, chunk "
+                               "index and chunk pushes",
+                   "n": w.n, "e": w.e, "chunk": w.chunk, "csr_ms": round(csr_ms, 3),
+                   "layers_ms": round(layers_ms, 3), **({"scale": f"1/{args.scale}"} if args.scale > 1 else {})},
+        "per_layer": layers,
+        "roofline": roofline,
+        "gemm_roofline": gemm,
+        "cpu_baseline": cpu,
+        "oracle_check": check,
     }
     print(json.dumps(line), flush=True)
 
