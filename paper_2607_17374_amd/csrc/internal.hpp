@@ -160,8 +160,9 @@ struct SortBuffers {
 // that produced the keys; it replaces the first pass's histogram when that
 // pass sorts an 8-bit digit.
 constexpr int RADIX_TILE = 4096;
+// first_bit: sort by bits [first_bit, first_bit + key_bits) only.
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit, const uint32_t* first_hist = nullptr);
+                    int bad_bit, const uint32_t* first_hist = nullptr, int first_bit = 0);
 
 // In-edges grouped by destination, sources ascending (sample.hip): built once
 // per graph for the fanout sampler.  Complete when build_csc returns.
@@ -169,6 +170,8 @@ struct Csc {
     Arena arena;
     int64_t* in_off = nullptr;  // [n+1]
     int32_t* in_src = nullptr;  // [e]
+    int32_t* heavy = nullptr;   // destinations with more than 64 in-edges
+    int64_t nheavy = 0;
     double ms_build = 0;
     explicit Csc(hipStream_t s) : arena(s) {}
     // may be read from other streams than the one it was built on
@@ -181,8 +184,19 @@ struct Csc {
 std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s);
 // row_off monotone from 0 to e and col_dst in [0, n), else TAURUS_E_INVALID (synchronises)
 void validate_csr(const taurus_graph& g, hipStream_t s);
-// mask (device, ceil(e/64) words) = the fanout-k sample of layer `layer`
+// largest fanout a sampled layer takes
+constexpr int FANOUT_MAX = 512;
+// mask (device, ceil(e/64) words, CSR edge order) = the fanout-k sample of
+// layer `layer`
 void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer, int k, uint64_t* mask,
                  hipStream_t s);
+// The kept in-edges of the fanout-k sample as chunk-index items, in CSC
+// order (destinations ascending, sources ascending within one): keys
+// (chunk(u) << vbits | v) in sb.keys[0] (from key_arena, with its ping-pong
+// buffer sb.keys[1]), values u - chunk(u)*C in sb.vals[0] (from val_arena,
+// with sb.vals[1]).  Returns the number kept.  Sets bit 32 of *bad (device)
+// for an in-list the pass could not settle (repeated sources).
+int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, int64_t C, int vbits,
+                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int* bad, hipStream_t s);
 
 }  // namespace taurus

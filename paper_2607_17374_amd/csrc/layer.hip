@@ -113,17 +113,12 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
     }
 }
 
-// Chunk-index items.  CSR edge i (source u = the row containing i) becomes
-// key (chunk(u) << vbits | v), value u - chunk(u)*C.  Every CSR edge is
-// checked; only a propagated one (all of them when mask is null) writes its
-// item, at its position among the propagated edges (word_off[w] =
-// propagated edges before mask word w).
+// Chunk-index items of an exact layer.  CSR edge i (source u = the row
+// containing i) becomes key (chunk(u) << vbits | v), value u - chunk(u)*C.
 __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
                                                     const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
-                                                    int64_t C, int vbits, const uint64_t* __restrict__ mask,
-                                                    const uint64_t* __restrict__ word_off,
-                                                    uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                                    int* __restrict__ bad) {
+                                                    int64_t C, int vbits, uint64_t* __restrict__ keys,
+                                                    uint32_t* __restrict__ vals, int* __restrict__ bad) {
     __shared__ int64_t ro[4][64];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
@@ -131,15 +126,9 @@ __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ 
     const int64_t v = col_dst[i];
     // rows strictly ascending, no self loops (a simple graph)
     if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
-    int64_t pos = i;
-    if (mask) {
-        const uint64_t word = mask[i >> 6];
-        if (!((word >> (i & 63)) & 1ull)) return;
-        pos = (int64_t)word_off[i >> 6] + __popcll(word & ((1ull << (i & 63)) - 1ull));
-    }
     const uint32_t cu = (uint32_t)u / (uint32_t)C;  // u < 2^31 and C < 2^31: 32-bit division
-    keys[pos] = ((uint64_t)cu << vbits) | (uint64_t)v;
-    vals[pos] = (uint32_t)u - cu * (uint32_t)C;
+    keys[i] = ((uint64_t)cu << vbits) | (uint64_t)v;
+    vals[i] = (uint32_t)u - cu * (uint32_t)C;
 }
 
 // propagated edges per mask word (bits at or past e are not edges)
@@ -1240,7 +1229,15 @@ static double ms_since(std::chrono::steady_clock::time_point t0) {
     return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
 }
 
-static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C, const uint64_t* mask,
+// A sampled layer's index (sample != null) takes its items straight from the
+// fanout sampler; an exact layer's from every CSR edge.
+struct SampleReq {
+    const Csc* csc;
+    uint64_t seed;
+    int layer, k;
+};
+
+static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C, const SampleReq* sample,
                                                hipStream_t s, int64_t budget) {
     const auto t_start = std::chrono::steady_clock::now();
     auto idx = std::make_shared<ChunkIndex>(s, budget);
@@ -1248,7 +1245,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     idx->g = g;
     idx->C = C;
     idx->nchunks = ceil_div(n, C);
-    idx->sampled = mask != nullptr;
+    idx->sampled = sample != nullptr;
     const int T = 256;
     const int64_t nch = idx->nchunks;
     Arena tmp(s);
@@ -1284,26 +1281,6 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         return idx;
     }
 
-    // A sampled layer indexes its propagated edges only: their positions
-    // among the CSR edges come from a scan of the mask's per-word counts.
-    int64_t items = e;
-    uint64_t* word_off = nullptr;
-    if (mask) {
-        const int64_t words = ceil_div(e, 64);
-        uint32_t* wcnt = tmp.alloc<uint32_t>(words, "propagated edges per mask word");
-        word_off = tmp.alloc<uint64_t>(words + 1, "propagated edges before each mask word");
-        k_mask_word_counts<<<(unsigned)ceil_div(words, T), T, 0, s>>>(mask, words, e, wcnt);
-        TAURUS_CHECK_LAUNCH();
-        scan_u32_to_u64(wcnt, word_off, words, true, tmp, s);
-        uint64_t total = 0;
-        Readback rb;
-        rb.add(&total, word_off + words, 1);
-        rb.run(s);
-        items = (int64_t)total;
-        tmp.free_ptr(wcnt);
-    }
-    const int64_t items1 = std::max<int64_t>(items, 1);
-
     // Items sorted by (source chunk, destination), stably.  Everything up to
     // the readback below is memory safe on an invalid graph (indices come
     // from binary searches and thread ids only); the flags are checked before
@@ -1311,16 +1288,27 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     const int vbits = std::max(1, bits_for(n - 1));
     const int cbits = bits_for(nch - 1);  // chunk numbers 0 .. nch - 1
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
-    SortBuffers sb{{tmp.alloc<uint64_t>(items1, "index keys"), tmp.alloc<uint64_t>(items1, "index keys (ping-pong)")},
-                   // the sorted values become the index's item sources
-                   {idx->arena.alloc<uint32_t>(items1, "index values"),
-                    idx->arena.alloc<uint32_t>(items1, "index values (ping-pong)")},
-                   0};
-    k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits, mask, word_off,
-                                                        sb.keys[0], sb.vals[0], bad);
-    TAURUS_CHECK_LAUNCH();
-    if (word_off) tmp.free_ptr(word_off);
-    radix_sort_u64(sb, items, vbits + cbits, tmp, s, bad, 8);
+    SortBuffers sb{{nullptr, nullptr}, {nullptr, nullptr}, 0};
+    int64_t items = e;
+    if (sample) {
+        // the sampler's kept in-edges come destination-major with sources
+        // ascending, so a stable sort by the chunk field alone orders them
+        // by (chunk, destination, source)
+        items = sample_items(*sample->csc, n, sample->seed, sample->layer, sample->k, C, vbits, tmp, idx->arena, sb,
+                             bad, s);
+        radix_sort_u64(sb, items, cbits, tmp, s, bad, 8, nullptr, vbits);
+    } else {
+        sb.keys[0] = tmp.alloc<uint64_t>(e, "index keys");
+        sb.keys[1] = tmp.alloc<uint64_t>(e, "index keys (ping-pong)");
+        // the sorted values become the index's item sources
+        sb.vals[0] = idx->arena.alloc<uint32_t>(e, "index values");
+        sb.vals[1] = idx->arena.alloc<uint32_t>(e, "index values (ping-pong)");
+        k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits, sb.keys[0],
+                                                            sb.vals[0], bad);
+        TAURUS_CHECK_LAUNCH();
+        radix_sort_u64(sb, items, vbits + cbits, tmp, s, bad, 8);
+    }
+    const int64_t items1 = std::max<int64_t>(items, 1);
     const uint64_t* keys = sb.keys[sb.cur];
     uint32_t* vals = sb.vals[sb.cur];
     tmp.free_ptr(sb.keys[1 - sb.cur]);
@@ -1346,6 +1334,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     if (hbad & 3) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
     if (hbad & 4) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
     if (hbad & 8) fail(TAURUS_E_DEVICE, "chunk index: radix sort offset out of range");
+    if (hbad & 32) fail(TAURUS_E_INVALID, "sampler: an in-list holds repeated sources");
     const int64_t kept = idx->chunk_off[(size_t)nch];
     idx->kept = kept;
     idx->segments = P;
@@ -1673,7 +1662,8 @@ struct taurus_layer {
     taurus::ScatterParams fix_p{};
     const int4* fix_list = nullptr;
     int64_t fix_n = 0;
-    uint64_t* mask = nullptr;
+    uint64_t* mask = nullptr;    // sampled layers: CSR-order mask, drawn when first needed
+    std::shared_ptr<taurus::Csc> csc;  // sampled layers: the in-edge lists the sample is drawn from
     float* gat_hp = nullptr;     // GAT: h' of every vertex, then s, t ([n][ncols])
     float* gat_m = nullptr;      // GAT: per-destination largest score
     float* gat_s = nullptr;      // GAT: per-destination sum of exp(score - max)
@@ -1760,7 +1750,8 @@ static void validate_desc(const taurus_layer_desc* d) {
     if (d->out_dtype < 0 || d->out_dtype > 2) fail(TAURUS_E_INVALID, "out_dtype %d", d->out_dtype);
     if (!d->weight) fail(TAURUS_E_INVALID, "weight is null");
     if (d->chunk <= 0 || d->chunk >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "chunk %lld", (long long)d->chunk);
-    if (d->fanout < 0 || d->fanout > 64) fail(TAURUS_E_INVALID, "fanout %d outside [0, 64]", d->fanout);
+    if (d->fanout < 0 || d->fanout > FANOUT_MAX)
+        fail(TAURUS_E_INVALID, "fanout %d outside [0, %d]", d->fanout, FANOUT_MAX);
     if (d->fanout > 0 && d->layer < 1) fail(TAURUS_E_INVALID, "layer %d: sampled layers are numbered from 1", d->layer);
     if (!d->out) fail(TAURUS_E_INVALID, "out is null");
     if (d->out_on_host != 0 && d->out_on_host != 1) fail(TAURUS_E_INVALID, "out_on_host=%d", d->out_on_host);
@@ -1812,9 +1803,14 @@ static void layer_init(taurus_layer* L) {
         } else {
             csc = build_csc(g, s);
         }
-        L->mask = L->arena.alloc<uint64_t>(std::max<int64_t>(1, ceil_div(g.e, 64)), "fanout mask");
-        sample_mask(g, *csc, d.seed, d.layer, d.fanout, L->mask, s);
-        L->idx = build_index(g, C, L->mask, s, 0);
+        const SampleReq req{csc.get(), d.seed, d.layer, d.fanout};
+        L->idx = build_index(g, C, &req, s, 0);
+        L->csc = csc;
+        if (d.agg == TAURUS_GCN_SYM) {
+            // the source norms count kept out-edges: the mask in CSR order
+            L->mask = L->arena.alloc<uint64_t>(std::max<int64_t>(1, ceil_div(g.e, 64)), "fanout mask");
+            sample_mask(g, *csc, d.seed, d.layer, d.fanout, L->mask, s);
+        }
     } else if (plan) {
         std::lock_guard<std::mutex> lock(plan->mu);
         if (!plan->idx) {
@@ -2497,6 +2493,10 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
     }
     try {
         const int64_t words = ceil_div(L->g.e, 64);
+        if (L->csc && !L->mask && words > 0) {
+            L->mask = L->arena.alloc<uint64_t>(words, "fanout mask");
+            sample_mask(L->g, *L->csc, L->d.seed, L->d.layer, L->d.fanout, L->mask, L->s);
+        }
         if (L->mask) {
             TAURUS_HIP(hipMemcpyAsync(mask_bits_host, L->mask, (size_t)words * 8, hipMemcpyDeviceToHost, L->s));
             TAURUS_HIP(hipStreamSynchronize(L->s));

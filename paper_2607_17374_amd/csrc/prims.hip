@@ -745,7 +745,7 @@ static std::vector<int> digit_schedule(int key_bits) {
 
 static_assert(RS_TILE == RADIX_TILE, "producers of first_hist tile the keys like the sort");
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit, const uint32_t* first_hist) {
+                    int bad_bit, const uint32_t* first_hist, int first_bit) {
     if (n <= 1 || key_bits <= 0) return;
     const int64_t nblocks = ceil_div(n, RS_TILE);
     if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
@@ -753,7 +753,7 @@ void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipSt
     const int wmax = *std::max_element(widths.begin(), widths.end());
     uint32_t* hist = arena.alloc<uint32_t>(((int64_t)1 << wmax) * nblocks, "radix histogram");
     uint64_t* offs = arena.alloc<uint64_t>(((int64_t)1 << wmax) * nblocks, "radix offsets");
-    int shift = 0;
+    int shift = first_bit;
     for (int width : widths) {
         const uint32_t* pre = shift == 0 && width == 8 ? first_hist : nullptr;
         if (width == 8) radix_pass<8>(b, n, shift, nblocks, pre, hist, offs, arena, s, bad, bad_bit);

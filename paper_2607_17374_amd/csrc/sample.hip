@@ -5,21 +5,26 @@
 //
 // The in-edges of each destination are read from a CSC, built once per
 // graph by a stable radix sort of the CSR edges by destination (sources stay
-// ascending within a destination).  Then, per layer:
-//   1. threshold: for every v with d_in(v) > k a wave finds tau_v, the k-th
-//      smallest rank pair of its in-edges.  The wave takes the in-edges 64
-//      at a time, sorts each batch across its lanes (bitonic network on
-//      (key, u) pairs) and merges it into a running sorted list of the 64
-//      smallest pairs so far; a batch with no pair below the running k-th
-//      smallest is skipped without sorting.  Destinations with more than
-//      512 in-edges are cut into pieces taken by separate waves, whose
-//      k smallest pairs are merged when the last piece is done, so a hub
-//      costs no more wall time than a piece;
-//   2. mask: one pass over the CSR in edge order keeps (u, v) iff its pair is
-//      <= tau_v (tau_v = +inf when d_in(v) <= k); each wave's 64 decisions
-//      form one mask word by ballot, so no atomics are needed.
+// ascending within a destination).  Per layer one pass over the in-lists
+// decides every in-edge and writes the kept ones straight out, in CSC order,
+// at position koff[v] + (kept in-edges of v before it), koff = the exclusive
+// scan of min(d_in, k):
+//   - lists of at most 64 in-edges: 16 lanes per destination hold the whole
+//     list (4 in-edges a lane); an in-edge is kept iff fewer than k pairs of
+//     its list are smaller (every pair is compared with every other by
+//     broadcast within the 16 lanes);
+//   - longer lists: a wave each.  Keys are uniform 64-bit values, so the k
+//     smallest lie below a cutoff that passes about k + 4 sqrt(k) + 16 of
+//     them; the wave counts the keys at or below a cutoff, moves it until
+//     between k and HEAVY_CAP pass (SplitMix64's finaliser is a bijection, so
+//     one destination's keys are distinct and the count rises by one key at
+//     a time: some cutoff always qualifies), gathers those candidates in LDS
+//     and ranks them by pairwise comparison.  Every pair below the k-th
+//     smallest passes any qualifying cutoff, so the kept set is exact.
 // Rank pairs are distinct within a destination (the sources are), so the
-// kept set is unique and the mask is exact.
+// kept set is unique.  The same pass can instead set the kept edges' bits
+// in a CSR-order mask (each kept (u, v) found in row u by binary search),
+// for callers that want the mask.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -51,16 +56,31 @@ void validate_csr(const taurus_graph& g, hipStream_t s) {
     if (hbad) fail(TAURUS_E_INVALID, "graph is not a valid CSR over [0, n) (flags %d)", hbad);
 }
 
-// CSR edge i -> sort key v, value u
+// CSR edge i -> sort key v, value u; flags a row that is not strictly
+// ascending or holds a self loop (bit 16)
 __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
-                                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+                                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                   int* __restrict__ bad) {
     __shared__ int64_t ro[4][64];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
     if (i >= e) return;
-    keys[i] = (uint64_t)col_dst[i];
+    const int32_t v = col_dst[i];
+    if ((int64_t)v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 16);
+    keys[i] = (uint64_t)v;
     vals[i] = (uint32_t)u;
+}
+
+// destinations with more than 64 in-edges (the long-list sampling pass)
+__global__ void k_heavy_flags(const int64_t* __restrict__ in_off, int64_t n, int32_t* __restrict__ flag) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) flag[v] = in_off[v + 1] - in_off[v] > 64 ? 1 : 0;
+}
+__global__ void k_heavy_list(const int32_t* __restrict__ flag, const int64_t* __restrict__ pos, int64_t n,
+                             int32_t* __restrict__ heavy) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n && flag[v]) heavy[pos[v]] = (int32_t)v;
 }
 
 // in_off[v] = first position of the sorted destinations that is >= v
@@ -93,7 +113,7 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
                        {c->arena.alloc<uint32_t>(e, "in-edge sources"),
                         c->arena.alloc<uint32_t>(e, "in-edge sources (ping-pong)")},
                        0};
-        k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0]);
+        k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0], bad);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
         c->in_src = reinterpret_cast<int32_t*>(sb.vals[sb.cur]);
@@ -103,265 +123,294 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
     } else {
         fill_i32(reinterpret_cast<int32_t*>(c->in_off), 2 * (n + 1), 0, s);
     }
+    int32_t* flag = tmp.alloc<int32_t>(n, "long in-list flags");
+    int64_t* pos = tmp.alloc<int64_t>(n + 1, "long in-list positions");
+    k_heavy_flags<<<(unsigned)ceil_div(n, T), T, 0, s>>>(c->in_off, n, flag);
+    TAURUS_CHECK_LAUNCH();
+    scan_i32_to_i64(flag, pos, n, true, tmp, s);
     {
         Readback rb;
         rb.add(&hbad, bad, 1);
+        rb.add(&c->nheavy, pos + n, 1);
         rb.run(s);
     }
+    if (hbad & 16) fail(TAURUS_E_INVALID, "graph rows are not strictly ascending or hold a self loop");
     if (hbad) fail(TAURUS_E_DEVICE, "in-edge sort: radix offset out of range");
+    if (c->nheavy > 0) {
+        c->heavy = c->arena.alloc<int32_t>(c->nheavy, "long in-lists");
+        k_heavy_list<<<(unsigned)ceil_div(n, T), T, 0, s>>>(flag, pos, n, c->heavy);
+        TAURUS_CHECK_LAUNCH();
+    }
     c->ms_build = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
     return c;
 }
 
-// ------------------------------------------------------------- threshold ----
+// --------------------------------------------------------------- sampling ----
 __device__ inline bool pair_less(uint64_t ka, uint32_t ua, uint64_t kb, uint32_t ub) {
     return ka < kb || (ka == kb && ua < ub);
 }
 
-__device__ inline uint64_t shfl64(uint64_t x, int src) {
-    const uint32_t lo = __shfl((uint32_t)x, src, 64), hi = __shfl((uint32_t)(x >> 32), src, 64);
-    return ((uint64_t)hi << 32) | lo;
-}
+constexpr int LIGHT_MAX = 64;     // lists up to this long are ranked in registers
+constexpr int HEAVY_CAP = 1024;   // candidates a wave of the long-list pass holds in LDS
 
-// Compare-exchange with lane ^ stride: keep the smaller pair if keep_min.
-__device__ inline void exchange(uint64_t& k, uint32_t& u, int stride, bool keep_min) {
-    const int lane = threadIdx.x & 63;
-    const uint64_t pk = shfl64(k, lane ^ stride);
-    const uint32_t pu = __shfl(u, lane ^ stride, 64);
-    const bool p_less = pair_less(pk, pu, k, u);
-    if (keep_min == p_less) {
-        k = pk;
-        u = pu;
+// Where the kept in-edges go: chunk-index items at koff[v] + (position among
+// v's kept in-edges) -- key (chunk(u) << vbits | v), value u - chunk(u)*C --
+// or, when mask is set, bit (CSR position of (u, v)) of a CSR-order mask.
+struct SampleOut {
+    uint64_t* keys;
+    uint32_t* vals;
+    const int64_t* koff;
+    int64_t C;
+    int vbits;
+    unsigned long long* mask;
+    const int64_t* row_off;
+    const int32_t* col_dst;
+    int* bad;  // bit SAMPLE_BAD: a list the cutoff search could not settle (repeated sources)
+};
+constexpr int SAMPLE_BAD = 32;
+
+__device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int64_t pos) {
+    if (o.mask) {
+        int64_t lo = o.row_off[u], hi = o.row_off[u + 1];  // (u, v) is an edge: v is in row u
+        while (lo < hi) {
+            const int64_t mid = lo + ((hi - lo) >> 1);
+            if ((int64_t)o.col_dst[mid] < v) lo = mid + 1;
+            else hi = mid;
+        }
+        atomicOr(&o.mask[lo >> 6], 1ull << (lo & 63));
+    } else {
+        const uint32_t cu = u / (uint32_t)o.C;  // u < 2^31 and C < 2^31
+        const int64_t at = o.koff[v] + pos;
+        o.keys[at] = ((uint64_t)cu << o.vbits) | (uint64_t)v;
+        o.vals[at] = u - cu * (uint32_t)o.C;
     }
 }
 
-// Sort the wave's 64 pairs ascending by lane (bitonic network).
-__device__ inline void bitonic_sort64(uint64_t& k, uint32_t& u) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int size = 2; size <= 64; size <<= 1)
-#pragma unroll
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            const bool ascending = (lane & size) == 0 || size == 64;
-            const bool lower = (lane & stride) == 0;
-            exchange(k, u, stride, lower == ascending);
+// Lists of at most LIGHT_MAX in-edges, 16 lanes per destination, four
+// destinations per wave, waves striding over the vertices.  Lane j of a
+// group holds slots j, j + 16, j + 32, j + 48 of its destination's list.
+__global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict__ in_off,
+                                                      const int32_t* __restrict__ in_src, int64_t n, uint64_t seed,
+                                                      int layer, int k, SampleOut o) {
+    const int lane = threadIdx.x & 63, sub = lane & 15, grp = lane >> 4;
+    const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t base = wave * 4; base < n; base += nwaves * 4) {  // uniform over the wave
+        const int64_t v = base + grp;
+        int64_t a = 0, d = 0;
+        if (v < n) {
+            a = in_off[v];
+            d = in_off[v + 1] - a;
         }
-}
-
-// (ck, cu) ascending and (bk, bu) ascending -> the 64 smallest of both,
-// ascending: lane-wise minimum against the reversed batch is bitonic, and a
-// bitonic merge sorts it.
-__device__ inline void merge_smallest(uint64_t& ck, uint32_t& cu, uint64_t bk, uint32_t bu) {
-    const int lane = threadIdx.x & 63;
-    const uint64_t rk = shfl64(bk, 63 - lane);
-    const uint32_t ru = __shfl(bu, 63 - lane, 64);
-    if (pair_less(rk, ru, ck, cu)) {
-        ck = rk;
-        cu = ru;
-    }
+        const bool mine = v < n && d > 0 && d <= LIGHT_MAX;
+        const bool rank = mine && d > k;
+        const uint64_t pre = rank ? sample_prefix(seed, (uint64_t)layer, (uint64_t)v) : 0;
+        uint32_t u[4];
+        uint64_t key[4];
+        bool valid[4];
 #pragma unroll
-    for (int stride = 32; stride > 0; stride >>= 1) exchange(ck, cu, stride, (lane & stride) == 0);
-}
-
-constexpr int SAMPLE_BATCHES = 8;
-// destinations with more in-edges than this are split into pieces of as many
-// in-edges (k_sample_pieces); the others are scanned whole (k_sample_threshold)
-constexpr int64_t SAMPLE_PIECE = 64 * SAMPLE_BATCHES;
-
-// The 64 smallest rank pairs among v's in-edges [a, b) merged into the
-// wave's running list (ck, cu), ascending by lane; pre = v's hash prefix.
-// SAMPLE_BATCHES batches of 64 in-edges are loaded at a time, so a long scan
-// keeps that many loads in flight; a batch with no pair below the running
-// k-th smallest is skipped without sorting.
-__device__ inline void scan_smallest(const int32_t* __restrict__ in_src, int64_t a, int64_t b, uint64_t pre, int k,
-                                     uint64_t& ck, uint32_t& cu) {
-    const int lane = threadIdx.x & 63;
-    for (int64_t base = a; base < b; base += 64 * SAMPLE_BATCHES) {
-        // past the end a lane holds (~0, ~0), which is never below a running
-        // pair and sorts last
-        uint32_t uu[SAMPLE_BATCHES];
-#pragma unroll
-        for (int t = 0; t < SAMPLE_BATCHES; t++) {
-            const int64_t idx = base + t * 64 + lane;
-            uu[t] = idx < b ? (uint32_t)in_src[idx] : ~0u;
+        for (int t = 0; t < 4; t++) {
+            const int sl = t * 16 + sub;
+            valid[t] = mine && sl < d;
+            u[t] = valid[t] ? (uint32_t)in_src[a + sl] : ~0u;
+            key[t] = valid[t] && rank ? sample_key(pre, u[t]) : ~0ull;
         }
+        int below[4] = {0, 0, 0, 0};
+        if (__ballot(rank) != 0) {
+            // every group broadcasts its 64 slots in turn; invalid slots hold
+            // (~0, ~0), which is never below a valid pair
 #pragma unroll
-        for (int t = 0; t < SAMPLE_BATCHES; t++) {
-            if (base + t * 64 >= b) break;  // uniform over the wave
-            const bool valid = base + t * 64 + lane < b;
-            uint32_t u = uu[t];
-            uint64_t key = valid ? sample_key(pre, u) : ~0ull;
-            const uint64_t tk = shfl64(ck, k - 1);
-            const uint32_t tu = __shfl(cu, k - 1, 64);
-            if (__ballot(valid && pair_less(key, u, tk, tu)) == 0) continue;
-            bitonic_sort64(key, u);
-            merge_smallest(ck, cu, key, u);
+            for (int t = 0; t < 4; t++)
+                for (int j = 0; j < 16; j++) {
+                    const uint32_t klo = __shfl((uint32_t)key[t], j, 16), khi = __shfl((uint32_t)(key[t] >> 32), j, 16);
+                    const uint32_t uj = __shfl(u[t], j, 16);
+                    const uint64_t kj = ((uint64_t)khi << 32) | klo;
+#pragma unroll
+                    for (int q = 0; q < 4; q++) below[q] += pair_less(kj, uj, key[q], u[q]) ? 1 : 0;
+                }
+        }
+        // kept slots in slot order (slot = t * 16 + sub): the position among
+        // the destination's kept in-edges counts the kept slots before it
+        int before = 0;
+        const int64_t mk = min(d, (int64_t)k);  // kept in-edges of v (distinct pairs)
+#pragma unroll
+        for (int t = 0; t < 4; t++) {
+            const bool kept = valid[t] && (!rank || below[t] < k);
+            const uint64_t bal = __ballot(kept);
+            const uint32_t g16 = (uint32_t)(bal >> (grp * 16)) & 0xffffu;
+            const int pos = before + __popc(g16 & ((1u << sub) - 1u));
+            if (kept && pos < mk) emit_kept(o, v, u[t], pos);
+            before += __popc(g16);
         }
     }
 }
 
-// destinations per wave of k_sample_threshold: few, so that a run of
-// mid-degree destinations (natural RMAT IDs cluster them) is spread over
-// many waves
-constexpr int SAMPLE_DPW = 8;
-
-// One wave per SAMPLE_DPW consecutive destinations; those with k < d_in <=
-// SAMPLE_PIECE are scanned one after another by the whole wave.
-__global__ __launch_bounds__(256) void k_sample_threshold(const int64_t* __restrict__ in_off,
-                                                          const int32_t* __restrict__ in_src, int64_t n,
-                                                          uint64_t seed, int layer, int k,
-                                                          uint64_t* __restrict__ thr_key,
-                                                          uint32_t* __restrict__ thr_u) {
-    const int lane = threadIdx.x & 63;
-    const int64_t v0 = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6) * SAMPLE_DPW;
-    if (v0 >= n) return;  // uniform over the wave
-    const int64_t myv = v0 + lane;
-    int64_t b = 0, d = 0;
-    if (lane < SAMPLE_DPW && myv < n) {
-        b = in_off[myv];
-        d = in_off[myv + 1] - b;
+// Lists longer than LIGHT_MAX (heavy[0 .. nheavy)), a wave each; the four
+// waves of a workgroup keep their candidates in separate LDS slices.
+__global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict__ in_off,
+                                                      const int32_t* __restrict__ in_src,
+                                                      const int32_t* __restrict__ heavy, int64_t nheavy,
+                                                      uint64_t seed, int layer, int k, SampleOut o) {
+    __shared__ uint64_t ckey[4][HEAVY_CAP];
+    __shared__ uint32_t cu[4][HEAVY_CAP];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t h = wave; h < nheavy; h += nwaves) {  // uniform over the wave
+        const int64_t v = heavy[h];
+        const int64_t a = in_off[v], d = in_off[v + 1] - a;
         if (d <= k) {  // every in-edge is kept
-            thr_key[myv] = ~0ull;
-            thr_u[myv] = ~0u;
+            for (int64_t sl = lane; sl < d; sl += 64) emit_kept(o, v, (uint32_t)in_src[a + sl], sl);
+            continue;
         }
-    }
-    uint64_t todo = __ballot(lane < SAMPLE_DPW && myv < n && d > k && d <= SAMPLE_PIECE);
-    while (todo) {
-        const int j = __ffsll((unsigned long long)todo) - 1;
-        todo &= todo - 1;
-        const int64_t v = v0 + j;
-        const int64_t vb = (int64_t)shfl64((uint64_t)b, j), vd = (int64_t)shfl64((uint64_t)d, j);
-        uint64_t ck = ~0ull;
-        uint32_t cu = ~0u;
-        scan_smallest(in_src, vb, vb + vd, sample_prefix(seed, (uint64_t)layer, (uint64_t)v), k, ck, cu);
-        if (lane == k - 1) {
-            thr_key[v] = ck;
-            thr_u[v] = cu;
-        }
-    }
-}
-
-// The destination whose in-edges hold CSC position pos (0 <= pos < e): the
-// largest v with in_off[v] <= pos, found by the whole wave (every lane with
-// the same pos) with a 64-ary search: each round the lanes probe 64 evenly
-// spaced offsets, and since in_off is non-decreasing the probes that pass
-// form a prefix of the lanes.
-__device__ inline int64_t covering(const int64_t* __restrict__ in_off, int64_t n, int64_t pos) {
-    const int lane = threadIdx.x & 63;
-    int64_t lo = 0, hi = n - 1;  // the answer lies in [lo, hi]
-    while (hi - lo >= 64) {
-        const int64_t step = (hi - lo + 63) / 64;
-        const int64_t q = min(lo + (int64_t)(lane + 1) * step, hi);
-        const int c = __popcll(__ballot(in_off[q] <= pos));
-        const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
-        lo = min(lo + (int64_t)c * step, hi);
-        hi = nhi;
-    }
-    const bool ok = lo + lane <= hi && in_off[lo + lane] <= pos;
-    return lo + __popcll(__ballot(ok)) - 1;
-}
-
-// Destinations with more than SAMPLE_PIECE in-edges.  One wave per piece of
-// SAMPLE_PIECE consecutive CSC positions.  A piece meets at most two such
-// destinations: the one holding its first position (slot 0) and one starting
-// inside it, which then holds its last position (slot 1).  For each, the
-// wave writes the k smallest pairs of its part of the piece to
-// piece_key/piece_u[(p * 2 + slot) * k + i]; the last piece of a destination
-// to finish (a counter per destination, behind a device-scope fence) merges
-// the destination's pieces in order and writes its threshold.
-__global__ __launch_bounds__(256) void k_sample_pieces(const int64_t* __restrict__ in_off,
-                                                       const int32_t* __restrict__ in_src, int64_t n, int64_t e,
-                                                       uint64_t seed, int layer, int k,
-                                                       uint64_t* __restrict__ piece_key,
-                                                       uint32_t* __restrict__ piece_u, int32_t* __restrict__ done,
-                                                       uint64_t* __restrict__ thr_key,
-                                                       uint32_t* __restrict__ thr_u) {
-    const int lane = threadIdx.x & 63;
-    const int64_t p = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-    if (p >= (e + SAMPLE_PIECE - 1) / SAMPLE_PIECE) return;  // uniform over the wave
-    const int64_t start = p * SAMPLE_PIECE, end = min(e, start + SAMPLE_PIECE);
-    const int64_t va = covering(in_off, n, start), vz = covering(in_off, n, end - 1);
-    for (int slot = 0; slot < 2; slot++) {
-        if (slot == 1 && vz == va) break;
-        const int64_t v = slot == 0 ? va : vz;
-        const int64_t vb = in_off[v], ve = in_off[v + 1];
-        if (ve - vb <= SAMPLE_PIECE) continue;
         const uint64_t pre = sample_prefix(seed, (uint64_t)layer, (uint64_t)v);
-        uint64_t ck = ~0ull;
-        uint32_t cu = ~0u;
-        scan_smallest(in_src, max(vb, start), min(ve, end), pre, k, ck, cu);
-        const int64_t r = (p * 2 + slot) * k;
-        if (lane < k) {
-            piece_key[r + lane] = ck;
-            piece_u[r + lane] = cu;
+        auto count = [&](uint64_t cut) {
+            int64_t c = 0;
+            for (int64_t sl = lane; sl - lane < d; sl += 64) {
+                const bool in = sl < d && sample_key(pre, (uint32_t)in_src[a + sl]) <= cut;
+                c += __popcll(__ballot(in));
+            }
+            return c;
+        };
+        // cutoff: about k + 4 sqrt(k) + 16 keys of d pass; then widen or
+        // narrow until k <= count <= HEAVY_CAP
+        const double want = (double)k + 4.0 * sqrt((double)k) + 16.0;
+        uint64_t cut = want >= (double)d ? ~0ull : (uint64_t)(want / (double)d * 18446744073709551616.0);
+        bool have_lo = false, have_hi = false;
+        uint64_t lo = 0, hi = 0;  // count(lo) < k, count(hi) > HEAVY_CAP
+        int64_t cnt = count(cut);
+        int rounds = 0;
+        while ((cnt < k || cnt > HEAVY_CAP) && ++rounds <= 200) {
+            if (cnt < k) {
+                lo = cut;
+                have_lo = true;
+            } else {
+                hi = cut;
+                have_hi = true;
+            }
+            if (!have_hi) cut = cut > (~0ull >> 1) ? ~0ull : 2 * cut + 1;
+            else if (!have_lo) cut = cut >> 1;
+            else cut = lo + ((hi - lo) >> 1);
+            cnt = count(cut);
         }
-        __threadfence();
-        const int64_t p0 = vb / SAMPLE_PIECE, p1 = (ve - 1) / SAMPLE_PIECE;
-        int last = 0;
-        if (lane == 0) last = atomicAdd(&done[v], 1) == (int)(p1 - p0) ? 1 : 0;
-        if (__shfl(last, 0, 64) == 0) continue;
-        __threadfence();
-        ck = ~0ull;
-        cu = ~0u;
-        for (int64_t q = p0; q <= p1; q++) {
-            // v holds the first position of every piece but possibly p0
-            const int64_t rq = (q * 2 + ((q == p0 && vb != q * SAMPLE_PIECE) ? 1 : 0)) * k;
-            const uint64_t bk = lane < k ? piece_key[rq + lane] : ~0ull;
-            const uint32_t bu = lane < k ? piece_u[rq + lane] : ~0u;
-            merge_smallest(ck, cu, bk, bu);
+        if (cnt < k || cnt > HEAVY_CAP) {  // only repeated sources make the count jump past the window
+            if (lane == 0) atomicOr(o.bad, SAMPLE_BAD);
+            continue;
         }
-        if (lane == k - 1) {
-            thr_key[v] = ck;
-            thr_u[v] = cu;
+        // candidates in CSC order (sources ascending)
+        int64_t m = 0;
+        for (int64_t sl = lane; sl - lane < d; sl += 64) {
+            uint32_t uu = 0;
+            uint64_t kk = ~0ull;
+            bool in = false;
+            if (sl < d) {
+                uu = (uint32_t)in_src[a + sl];
+                kk = sample_key(pre, uu);
+                in = kk <= cut;
+            }
+            const uint64_t bal = __ballot(in);
+            if (in) {
+                const int64_t at = m + __popcll(bal & lt);
+                ckey[w][at] = kk;
+                cu[w][at] = uu;
+            }
+            m += __popcll(bal);
         }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        // rank each candidate among all; keep the k smallest, in candidate order
+        int64_t before = 0;
+        for (int64_t i0 = 0; i0 < m; i0 += 64) {
+            const int64_t i = i0 + lane;
+            bool kept = false;
+            uint32_t ui = 0;
+            if (i < m) {
+                const uint64_t ki = ckey[w][i];
+                ui = cu[w][i];
+                int r = 0;
+                for (int64_t j = 0; j < m && r < k; j++) r += pair_less(ckey[w][j], cu[w][j], ki, ui) ? 1 : 0;
+                kept = r < k;
+            }
+            const uint64_t bal = __ballot(kept);
+            const int64_t pos = before + __popcll(bal & lt);
+            if (kept && pos < k) emit_kept(o, v, ui, pos);
+            before += __popcll(bal);
+        }
+        // the slice is rewritten by this wave's next destination
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
 }
 
-// ------------------------------------------------------------------ mask ----
-__global__ __launch_bounds__(256) void k_sample_mask(const int64_t* __restrict__ row_off,
-                                                     const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
-                                                     uint64_t seed, int layer,
-                                                     const uint64_t* __restrict__ thr_key,
-                                                     const uint32_t* __restrict__ thr_u,
-                                                     uint64_t* __restrict__ mask) {
-    __shared__ int64_t ro[4][64];
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
-    bool keep = false;
-    if (i < e) {
-        const int32_t v = col_dst[i];
-        const uint64_t key = sample_key(sample_prefix(seed, (uint64_t)layer, (uint64_t)v), (uint64_t)u);
-        keep = !pair_less(thr_key[v], thr_u[v], key, (uint32_t)u);
+static void sample_pass(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, const SampleOut& o,
+                        hipStream_t s) {
+    if (k < 1 || k > FANOUT_MAX) fail(TAURUS_E_INVALID, "fanout %d outside [1, %d]", k, FANOUT_MAX);
+    int dev = 0, cus = 0;
+    TAURUS_HIP(hipGetDevice(&dev));
+    TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    const int64_t grid_light = std::min<int64_t>(ceil_div(n, 16), (int64_t)cus * 32);
+    k_sample_light<<<(unsigned)std::max<int64_t>(1, grid_light), 256, 0, s>>>(csc.in_off, csc.in_src, n, seed, layer,
+                                                                             k, o);
+    TAURUS_CHECK_LAUNCH();
+    if (csc.nheavy > 0) {
+        const int64_t grid_heavy = std::min<int64_t>(ceil_div(csc.nheavy, 4), (int64_t)cus * 12);
+        k_sample_heavy<<<(unsigned)grid_heavy, 256, 0, s>>>(csc.in_off, csc.in_src, csc.heavy, csc.nheavy, seed,
+                                                          layer, k, o);
+        TAURUS_CHECK_LAUNCH();
     }
-    const uint64_t word = __ballot(keep);
-    const int64_t i0 = i - lane;
-    if (lane == 0 && i0 < e) mask[i0 >> 6] = word;
+}
+
+// kept per destination, min(d_in(v), k)
+__global__ void k_sample_counts(const int64_t* __restrict__ in_off, int64_t n, int k, int32_t* __restrict__ m) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) m[v] = (int32_t)min(in_off[v + 1] - in_off[v], (int64_t)k);
+}
+
+int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, int64_t C, int vbits,
+                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int* bad, hipStream_t s) {
+    if (k < 1 || k > FANOUT_MAX) fail(TAURUS_E_INVALID, "fanout %d outside [1, %d]", k, FANOUT_MAX);
+    Arena tmp(s);
+    int32_t* m = tmp.alloc<int32_t>(n, "kept per destination");
+    int64_t* koff = tmp.alloc<int64_t>(n + 1, "kept before each destination");
+    k_sample_counts<<<(unsigned)ceil_div(n, 256), 256, 0, s>>>(csc.in_off, n, k, m);
+    TAURUS_CHECK_LAUNCH();
+    scan_i32_to_i64(m, koff, n, true, tmp, s);
+    int64_t kept = 0;
+    {
+        Readback rb;
+        rb.add(&kept, koff + n, 1);
+        rb.run(s);
+    }
+    const int64_t k1 = std::max<int64_t>(kept, 1);
+    sb.keys[0] = key_arena.alloc<uint64_t>(k1, "index keys");
+    sb.keys[1] = key_arena.alloc<uint64_t>(k1, "index keys (ping-pong)");
+    sb.vals[0] = val_arena.alloc<uint32_t>(k1, "index values");
+    sb.vals[1] = val_arena.alloc<uint32_t>(k1, "index values (ping-pong)");
+    sb.cur = 0;
+    if (kept > 0)
+        sample_pass(csc, n, seed, layer, k,
+                    SampleOut{sb.keys[0], sb.vals[0], koff, C, vbits, nullptr, nullptr, nullptr, bad}, s);
+    return kept;
 }
 
 void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer, int k, uint64_t* mask,
                  hipStream_t s) {
-    const int64_t n = g.n, e = g.e;
-    if (e == 0) return;
-    if (k < 1 || k > 64) fail(TAURUS_E_INVALID, "fanout %d outside [1, 64]", k);
+    const int64_t words = ceil_div(g.e, 64);
+    if (words == 0) return;
+    fill_i32(reinterpret_cast<int32_t*>(mask), 2 * words, 0, s);
     Arena tmp(s);
-    uint64_t* thr_key = tmp.alloc<uint64_t>(n, "sampling thresholds");
-    uint32_t* thr_u = tmp.alloc<uint32_t>(n, "sampling thresholds (sources)");
-    const int64_t pieces = ceil_div(e, SAMPLE_PIECE);
-    uint64_t* piece_key = tmp.alloc<uint64_t>(pieces * 2 * k, "piece pairs");
-    uint32_t* piece_u = tmp.alloc<uint32_t>(pieces * 2 * k, "piece pairs (sources)");
-    int32_t* done = tmp.alloc<int32_t>(n, "pieces done");
-    fill_i32(done, n, 0, s);
-    k_sample_pieces<<<(unsigned)ceil_div(pieces, 4), 256, 0, s>>>(csc.in_off, csc.in_src, n, e, seed, layer, k,
-                                                                 piece_key, piece_u, done, thr_key, thr_u);
-    TAURUS_CHECK_LAUNCH();
-    const int64_t waves = ceil_div(n, SAMPLE_DPW);
-    k_sample_threshold<<<(unsigned)ceil_div(waves, 4), 256, 0, s>>>(csc.in_off, csc.in_src, n, seed, layer, k, thr_key,
-                                                                   thr_u);
-    TAURUS_CHECK_LAUNCH();
-    k_sample_mask<<<(unsigned)ceil_div(e, 256), 256, 0, s>>>(g.row_off, g.col_dst, n, e, seed, layer, thr_key, thr_u,
-                                                            mask);
-    TAURUS_CHECK_LAUNCH();
+    int* bad = tmp.alloc<int>(1, "sampler flag");
+    fill_i32(bad, 1, 0, s);
+    sample_pass(csc, g.n, seed, layer, k,
+                SampleOut{nullptr, nullptr, nullptr, 1, 1, reinterpret_cast<unsigned long long*>(mask), g.row_off,
+                          g.col_dst, bad},
+                s);
+    int hbad = 0;
+    Readback rb;
+    rb.add(&hbad, bad, 1);
+    rb.run(s);
+    if (hbad) fail(TAURUS_E_INVALID, "sampler: an in-list holds repeated sources");
 }
 
 }  // namespace taurus

@@ -59,7 +59,7 @@ def _gpu_mask(torch, n, row_off, col_dst, k, layer, seed, plan=None, chunk=1024)
     return words, kept
 
 
-@pytest.mark.parametrize("k", [1, 5, 15, 64])
+@pytest.mark.parametrize("k", [1, 5, 15, 64, 65, 300, 512])
 def test_sampler_mask_bit_exact(torch_cuda, k):
     import oracle as O
     import paper_2607_17374_amd as T
@@ -200,7 +200,7 @@ def test_sampling_error_paths(torch_cuda):
     row_off, col_dst = H.gpu_graph(w)
     spec = H.layer_specs(w)[0]
     out = torch.empty((w.n, spec["d_out"]), dtype=torch.float32, device="cuda")
-    for bad in (dict(fanout=65), dict(fanout=-1), dict(fanout=5, agg=7, weight_cat=np.zeros((64, 64), np.float32)),
+    for bad in (dict(fanout=513), dict(fanout=-1), dict(fanout=5, agg=7, weight_cat=np.zeros((64, 64), np.float32)),
                 dict(fanout=5, layer=0), dict(in_dtype=F.BF16, d_in=60, weight_cat=np.zeros((60, 128), np.float32))):
         with pytest.raises(T.TaurusError) as ex:
             T.Layer(w.n, row_off, col_dst, out=out, chunk=1024, **dict(spec, **bad))
