@@ -88,10 +88,11 @@ public:
     explicit Arena(hipStream_t s = nullptr, int64_t budget = 0) : stream_(s), budget_(budget) {}
     // Fixed-region mode: allocations are carved, 256-byte aligned, out of
     // [region, region + capacity) and never touch the device memory cache;
-    // running out is an error (TAURUS_E_INVALID).  free_ptr gives back the
-    // most recent block only.
-    Arena(hipStream_t s, void* region, int64_t capacity)
-        : stream_(s), region_(static_cast<char*>(region)), capacity_(capacity) {}
+    // running out is an error (TAURUS_E_INVALID), or, with fallback, a
+    // request that does not fit comes from the cache as usual.  free_ptr
+    // gives back the most recent block of the region only.
+    Arena(hipStream_t s, void* region, int64_t capacity, bool fallback = false)
+        : stream_(s), region_(static_cast<char*>(region)), capacity_(capacity), fallback_(fallback) {}
     ~Arena() { release(); }
     void set_stream(hipStream_t s) { stream_ = s; }
     Arena(const Arena&) = delete;
@@ -120,6 +121,7 @@ private:
     static constexpr int REGION_STACK = 64;
     char* region_ = nullptr;
     int64_t capacity_ = 0, top_ = 0;
+    bool fallback_ = false;
     int64_t starts_[REGION_STACK] = {};
     int nstarts_ = 0;
 };
@@ -181,7 +183,8 @@ struct Csc {
         arena.release();
     }
 };
-std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s);
+// scratch (optional): where the sort's temporaries go
+std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scratch = nullptr);
 // row_off monotone from 0 to e and col_dst in [0, n), else TAURUS_E_INVALID (synchronises)
 void validate_csr(const taurus_graph& g, hipStream_t s);
 // largest fanout a sampled layer takes

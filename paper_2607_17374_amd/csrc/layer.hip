@@ -1237,8 +1237,9 @@ struct SampleReq {
     int layer, k;
 };
 
+// scratch (optional): where the build's temporaries go
 static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C, const SampleReq* sample,
-                                               hipStream_t s, int64_t budget) {
+                                               hipStream_t s, int64_t budget, Arena* scratch = nullptr) {
     const auto t_start = std::chrono::steady_clock::now();
     auto idx = std::make_shared<ChunkIndex>(s, budget);
     const int64_t n = g.n, e = g.e;
@@ -1248,7 +1249,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     idx->sampled = sample != nullptr;
     const int T = 256;
     const int64_t nch = idx->nchunks;
-    Arena tmp(s);
+    Arena own(s);
+    Arena& tmp = scratch ? *scratch : own;
     auto finish = [&]() {
         TAURUS_HIP(hipEventCreateWithFlags(&idx->ready, hipEventDisableTiming));
         TAURUS_HIP(hipEventRecord(idx->ready, s));
@@ -1790,21 +1792,33 @@ static void layer_init(taurus_layer* L) {
     taurus_plan* plan = const_cast<taurus_plan*>(d.plan);
     if (plan && (!same_graph(plan->g, g) || plan->chunk != C))
         fail(TAURUS_E_INVALID, "plan was built for another graph or chunk size");
+    // Without a budget the accumulators are dense: they are allocated first
+    // and, until the first chunk arrives (their rows are logically zero
+    // while nothing has arrived and are never cleared), hold the temporaries
+    // of the in-edge lists and the chunk index, so that those take no memory
+    // of their own.
+    std::unique_ptr<Arena> scratch;
+    if (d.hbm_budget == 0) {
+        const int64_t acc_elems = n * (int64_t)d.d_out;
+        L->acc = L->arena.alloc<float>(acc_elems, "accumulators");
+        scratch = std::make_unique<Arena>(s, L->acc, acc_elems * 4, true);
+    }
     const auto t_index = std::chrono::steady_clock::now();
     if (d.fanout > 0) {
         std::shared_ptr<Csc> csc;
         if (plan) {
             std::lock_guard<std::mutex> lock(plan->mu);
             if (!plan->csc) {
-                plan->csc = build_csc(g, s);
+                plan->csc = build_csc(g, s, scratch.get());
                 plan->ms_build += plan->csc->ms_build;
             }
             csc = plan->csc;
         } else {
-            csc = build_csc(g, s);
+            csc = build_csc(g, s, scratch.get());
         }
+        if (scratch) scratch->release();
         const SampleReq req{csc.get(), d.seed, d.layer, d.fanout};
-        L->idx = build_index(g, C, &req, s, 0);
+        L->idx = build_index(g, C, &req, s, 0, scratch.get());
         L->csc = csc;
         if (d.agg == TAURUS_GCN_SYM) {
             // the source norms count kept out-edges: the mask in CSR order
@@ -1814,14 +1828,15 @@ static void layer_init(taurus_layer* L) {
     } else if (plan) {
         std::lock_guard<std::mutex> lock(plan->mu);
         if (!plan->idx) {
-            plan->idx = build_index(g, C, nullptr, s, 0);
+            plan->idx = build_index(g, C, nullptr, s, 0, scratch.get());
             plan->ms_build += plan->idx->ms_build;
         }
         L->idx = plan->idx;
         L->idx->wait_ready(s);
     } else {
-        L->idx = build_index(g, C, nullptr, s, 0);
+        L->idx = build_index(g, C, nullptr, s, 0, scratch.get());
     }
+    if (scratch) scratch->release();
     L->ms_index = ms_since(t_index);
     const ChunkIndex& idx = *L->idx;
 
@@ -1919,7 +1934,9 @@ static void layer_init(taurus_layer* L) {
     const int64_t row_bytes = (int64_t)L->d_o * 4;
     const int64_t index_bytes = L->idx->arena.bytes();
     const int64_t dense = n * row_bytes;
-    if (d.hbm_budget == 0 || L->arena.bytes() + index_bytes + dense + (dense >> 3) <= d.hbm_budget) {
+    if (L->acc) {
+        // allocated before the index (no budget)
+    } else if (L->arena.bytes() + index_bytes + dense + (dense >> 3) <= d.hbm_budget) {
         L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
     } else {
         const int64_t staging = 2 * std::min(C, n) * (int64_t)d.d_in * (d.in_dtype == TAURUS_F32 ? 4 : 2) * 9 / 8;

@@ -273,14 +273,15 @@ void* Arena::alloc_bytes(int64_t bytes, const char* what) {
     if (bytes <= 0) bytes = 16;
     if (region_) {
         const int64_t start = (top_ + 255) & ~(int64_t)255;
-        if (start + bytes > capacity_ || nstarts_ == REGION_STACK)
+        if (start + bytes <= capacity_ && nstarts_ < REGION_STACK) {
+            starts_[nstarts_++] = top_;
+            top_ = start + bytes;
+            if (top_ > peak_) peak_ = top_;
+            return region_ + start;
+        }
+        if (!fallback_)
             fail(TAURUS_E_INVALID, "scratch region of %lld bytes cannot hold %lld more bytes for %s",
                  (long long)capacity_, (long long)bytes, what);
-        starts_[nstarts_++] = top_;
-        top_ = start + bytes;
-        bytes_ = top_;
-        if (bytes_ > peak_) peak_ = bytes_;
-        return region_ + start;
     }
     const int64_t cls = (int64_t)size_class((size_t)bytes);
     if (budget_ > 0 && bytes_ + cls > budget_)
@@ -303,12 +304,9 @@ void* Arena::alloc_bytes(int64_t bytes, const char* what) {
 }
 
 void Arena::free_ptr(void* p) {
-    if (region_) {
+    if (region_ && static_cast<char*>(p) >= region_ && static_cast<char*>(p) < region_ + capacity_) {
         // the most recent block only: its start was recorded before alignment
-        if (nstarts_ > 0 && p == region_ + ((starts_[nstarts_ - 1] + 255) & ~(int64_t)255)) {
-            top_ = starts_[--nstarts_];
-            bytes_ = top_;
-        }
+        if (nstarts_ > 0 && p == region_ + ((starts_[nstarts_ - 1] + 255) & ~(int64_t)255)) top_ = starts_[--nstarts_];
         return;
     }
     for (size_t i = blocks_.size(); i-- > 0;) {
@@ -323,9 +321,8 @@ void Arena::free_ptr(void* p) {
 
 void Arena::release() {
     if (region_) {
-        top_ = bytes_ = 0;
+        top_ = 0;
         nstarts_ = 0;
-        return;
     }
     for (auto& b : blocks_) device_release(b.p, stream_);
     blocks_.clear();

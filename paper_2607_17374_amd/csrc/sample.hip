@@ -97,13 +97,14 @@ __global__ void k_csc_offsets(const uint64_t* __restrict__ keys, int64_t e, int6
     in_off[v] = lo;
 }
 
-std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s) {
+std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scratch) {
     const auto t0 = std::chrono::steady_clock::now();
     auto c = std::make_shared<Csc>(s);
     const int64_t n = g.n, e = g.e;
     const int T = 256;
     validate_csr(g, s);
-    Arena tmp(s);
+    Arena own(s);
+    Arena& tmp = scratch ? *scratch : own;
     int* bad = tmp.alloc<int>(1, "sort flag");
     fill_i32(bad, 1, 0, s);
     int hbad = 0;
