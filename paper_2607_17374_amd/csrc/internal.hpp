@@ -197,9 +197,12 @@ void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer
 // order (destinations ascending, sources ascending within one): keys
 // (chunk(u) << vbits | v) in sb.keys[0] (from key_arena, with its ping-pong
 // buffer sb.keys[1]), values u - chunk(u)*C in sb.vals[0] (from val_arena,
-// with sb.vals[1]).  Returns the number kept.  Sets bit 32 of *bad (device)
-// for an in-list the pass could not settle (repeated sources).
+// with sb.vals[1]).  Also m[v] = min(d_in(v), k) and first_chunk[v] = the
+// chunk of v's smallest kept source (left as it was when none is kept).
+// Returns the number kept.  Sets bit 32 of *bad (device) for an in-list
+// the pass could not settle (repeated sources).
 int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, int64_t C, int vbits,
-                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int* bad, hipStream_t s);
+                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int32_t* m, int32_t* first_chunk, int* bad,
+                     hipStream_t s);
 
 }  // namespace taurus

@@ -217,23 +217,6 @@ __global__ __launch_bounds__(256) void k_head_positions(const uint64_t* __restri
     if (blockIdx.x == 0 && tid == 0) seg_start[P] = items;
 }
 
-// chunk_seg[k] = first segment of chunk k: the first segment starting at or
-// after the chunk's first item (every chunk's first item is a head)
-__global__ void k_chunk_segments(const int64_t* __restrict__ chunk_off, int64_t nchunks,
-                                 const int64_t* __restrict__ seg_start, int64_t P,
-                                 int64_t* __restrict__ chunk_seg) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k > nchunks) return;
-    const int64_t target = chunk_off[k];
-    int64_t lo = 0, hi = P;  // seg_start[P] = items >= any target
-    while (lo < hi) {
-        const int64_t mid = lo + ((hi - lo) >> 1);
-        if (seg_start[mid] < target) lo = mid + 1;
-        else hi = mid;
-    }
-    chunk_seg[k] = lo;
-}
-
 // work list of a segment: short class 0..NCLASS-1 by slot count, or NCLASS (wave pieces)
 __device__ inline int seg_class(int64_t slots) {
 #pragma unroll
@@ -253,6 +236,9 @@ __device__ inline int64_t seg_slots(int64_t len, uint32_t v, uint32_t chunk, int
 // destination's first chunk, mark a segment from the destination's own chunk
 // (OWN_SEGMENT; it carries the self message) and record the segment's slot
 // count.
+// (COUNTED: the message counts and first chunks are known already, as for
+// a sampled layer)
+template <bool COUNTED>
 __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
                                int vbits, int64_t C, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
                                int32_t* __restrict__ slots_of, uint8_t* __restrict__ has_own,
@@ -262,70 +248,16 @@ __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t*
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
     const uint64_t v = keys[b] & (((uint64_t)1 << vbits) - 1);
     const uint32_t chunk = (uint32_t)(keys[b] >> vbits);
-    atomicAdd(&m[v], (int)len);
-    atomicMin(&first_chunk[v], (int)chunk);
+    if (!COUNTED) {
+        atomicAdd(&m[v], (int)len);
+        atomicMin(&first_chunk[v], (int)chunk);
+    }
     const int64_t slots = seg_slots(len, (uint32_t)v, chunk, C);
     if (slots > len) {
         has_own[v] = OWN_SEGMENT;
         atomicAdd(own_count, 1ull);
     }
     slots_of[s] = (int32_t)slots;
-}
-
-// entries segment s adds to work list l: 1 in its short class, its pieces in
-// the wave list, 1 in the fix-up list when cut into several pieces
-__device__ inline int list_entries(int l, int64_t slots) {
-    const int cls = seg_class(slots);
-    if (l < NCLASS) return cls == l ? 1 : 0;
-    const int pieces = cls == NCLASS ? (int)((slots + PIECE_LEN - 1) / PIECE_LEN) : 0;
-    return l == NCLASS ? pieces : (pieces > 1 ? 1 : 0);
-}
-
-__global__ void k_list_counts(const int32_t* __restrict__ slots_of, int64_t P, int l, int32_t* __restrict__ cnt) {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s < P) cnt[s] = list_entries(l, slots_of[s]);
-}
-
-// all lists at once: cnt[l * P + s] = entries of segment s in list l
-__global__ void k_list_counts_all(const int32_t* __restrict__ slots_of, int64_t P, int32_t* __restrict__ cnt) {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= P) return;
-    const int64_t slots = slots_of[s];
-#pragma unroll
-    for (int l = 0; l < NLIST; l++) cnt[(int64_t)l * P + s] = list_entries(l, slots);
-}
-
-// totals[l] += entries of every segment in list l (one block-level sum per
-// list, then one atomic per block and list)
-__global__ __launch_bounds__(256) void k_list_totals(const int32_t* __restrict__ slots_of, int64_t P,
-                                                     unsigned long long* __restrict__ totals) {
-    __shared__ unsigned long long part[NLIST];
-    if (threadIdx.x < NLIST) part[threadIdx.x] = 0;
-    __syncthreads();
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s < P) {
-        const int64_t slots = slots_of[s];
-#pragma unroll
-        for (int l = 0; l < NLIST; l++) {
-            const int c = list_entries(l, slots);
-            if (c) atomicAdd(&part[l], (unsigned long long)c);
-        }
-    }
-    __syncthreads();
-    if (threadIdx.x < NLIST && part[threadIdx.x]) atomicAdd(&totals[threadIdx.x], part[threadIdx.x]);
-}
-
-// bases[k] = position in list l (offsets `off`, an exclusive scan of the
-// list's entries per segment) of chunk k's first entry; chunk_seg[k] = the
-// chunk's first segment, chunk_seg[nchunks] = P
-// list l = blockIdx.y: its offsets at off + l * off_stride, its chunk
-// bases at bases + l * (nchunks + 1)
-__global__ void k_list_chunk_bases(const int64_t* __restrict__ chunk_seg, int64_t nchunks,
-                                   const int64_t* __restrict__ off, int64_t off_stride,
-                                   int64_t* __restrict__ bases) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t l = blockIdx.y;
-    if (k <= nchunks) bases[l * (nchunks + 1) + k] = off[l * off_stride + chunk_seg[k]];
 }
 
 // What a unit of segment s says besides its slots: {first item relative to
@@ -354,49 +286,112 @@ __device__ inline SegUnit seg_unit(const uint64_t* keys, const int64_t* seg_star
     return u;
 }
 
-// Short class l: unit = {first item, slots | NOT_FIRST | SELF_HERE, v, 0} at
-// off[s] (the list's exclusive scan).  l < 0: every short class c at once,
-// at off[c * P + s].
-__global__ void k_emit_short(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start,
-                             const int32_t* __restrict__ slots_of, int64_t P, int l, int vbits, int64_t C,
-                             const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
-                             const int64_t* __restrict__ off, int4* __restrict__ units) {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= P) return;
-    const int slots = slots_of[s];
-    const int c = seg_class(slots);
-    if (l >= 0 ? c != l : c >= NCLASS) return;
-    const SegUnit u = seg_unit(keys, seg_start, s, vbits, C, chunk_off, first_chunk);
-    units[l >= 0 ? off[s] : off[(int64_t)c * P + s]] = make_int4((int)u.rel, slots | u.nf | u.self, u.v, 0);
+// ---- work lists by tiles of segments ----
+constexpr int LT_THREADS = 256, LT_PER = 16, LT_TILE = LT_THREADS * LT_PER;
+
+// entries segment s adds to every list
+__device__ inline void seg_entries(int64_t slots, int64_t (&c)[NLIST]) {
+    const int cls = seg_class(slots);
+    if (cls < NCLASS) {
+        c[cls] += 1;
+    } else {
+        const int64_t pieces = (slots + PIECE_LEN - 1) / PIECE_LEN;
+        c[NCLASS] += pieces;
+        c[NCLASS + 1] += pieces > 1 ? 1 : 0;
+    }
 }
 
-// Longer segments: piece q covers slots [q * PIECE_LEN, ...) of the segment;
-// the self slot is the segment's last slot, so SELF_HERE goes on its last
-// piece.  A piece = {first item, slots | flags, v, slot}, slot = its position
-// in the work-list buffer (base + its position in the wave list) when the
-// segment has several pieces (a hub: its partial row goes to the carry
-// buffer), else -1.  A hub also gets a fix-up entry {v, buffer position of
-// its first piece, pieces, 0} at fix_off[s].
-__global__ void k_emit_long(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start,
-                            const int32_t* __restrict__ slots_of, int64_t P, int vbits, int64_t C,
-                            const int64_t* __restrict__ chunk_off, const int32_t* __restrict__ first_chunk,
-                            const int64_t* __restrict__ off, const int64_t* __restrict__ fix_off,
-                            int4* __restrict__ units, int4* __restrict__ fix, int base) {
-    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= P) return;
-    const int64_t slots = slots_of[s];
-    if (seg_class(slots) != NCLASS) return;
-    const SegUnit u = seg_unit(keys, seg_start, s, vbits, C, chunk_off, first_chunk);
-    const int pieces = (int)((slots + PIECE_LEN - 1) / PIECE_LEN);
-    const int64_t first = off[s];
-    for (int q = 0; q < pieces; q++) {
-        const int64_t o = (int64_t)q * PIECE_LEN;
-        const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
-        const int self = q == pieces - 1 ? u.self : 0;
-        units[first + q] =
-            make_int4((int)(u.rel + o), plen | u.nf | self, u.v, pieces > 1 ? base + (int)(first + q) : -1);
+// tile_cnt[l * ntiles + t] = entries the segments of tile t add to list l;
+// thread j of a tile takes its segments j * LT_PER .. j * LT_PER + LT_PER - 1
+__global__ __launch_bounds__(LT_THREADS) void k_list_tile_counts(const int32_t* __restrict__ slots_of, int64_t P,
+                                                                int64_t ntiles, uint64_t* __restrict__ tile_cnt) {
+    __shared__ int64_t part[LT_THREADS / 64][NLIST];
+    int64_t c[NLIST] = {};
+    const int64_t s0 = (int64_t)blockIdx.x * LT_TILE + (int64_t)threadIdx.x * LT_PER;
+    for (int j = 0; j < LT_PER; j++)
+        if (s0 + j < P) seg_entries(slots_of[s0 + j], c);
+#pragma unroll
+    for (int l = 0; l < NLIST; l++)
+        for (int m = 32; m >= 1; m >>= 1) c[l] += __shfl_xor(c[l], m, 64);
+    if ((threadIdx.x & 63) == 0)
+        for (int l = 0; l < NLIST; l++) part[threadIdx.x >> 6][l] = c[l];
+    __syncthreads();
+    if (threadIdx.x < NLIST) {
+        int64_t t = 0;
+        for (int w = 0; w < LT_THREADS / 64; w++) t += part[w][threadIdx.x];
+        tile_cnt[(int64_t)threadIdx.x * ntiles + blockIdx.x] = (uint64_t)t;
     }
-    if (pieces > 1) fix[fix_off[s]] = make_int4(u.v, base + (int)first, pieces, 0);
+}
+
+// Units of tile t's segments, in segment order within each list, from the
+// tile's positions tile_off[l * ntiles + t] (absolute in the work-list
+// buffer).  A segment that starts a chunk also writes, for that chunk and
+// any empty chunks before it, each list's position there:
+// dbases[l * (nchunks + 1) + k]; the last segment writes the list ends for
+// the chunks after it and for k = nchunks.
+__global__ __launch_bounds__(LT_THREADS) void k_list_emit(const uint64_t* __restrict__ keys,
+                                                         const int64_t* __restrict__ seg_start,
+                                                         const int32_t* __restrict__ slots_of, int64_t P,
+                                                         int64_t ntiles, const uint64_t* __restrict__ tile_off,
+                                                         int vbits, int64_t C, const int64_t* __restrict__ chunk_off,
+                                                         const int32_t* __restrict__ first_chunk, int64_t nchunks,
+                                                         int4* __restrict__ units, int64_t* __restrict__ dbases) {
+    __shared__ int64_t wsum[LT_THREADS / 64][NLIST];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t s0 = (int64_t)blockIdx.x * LT_TILE + (int64_t)threadIdx.x * LT_PER;
+    int64_t c[NLIST] = {};
+    for (int j = 0; j < LT_PER; j++)
+        if (s0 + j < P) seg_entries(slots_of[s0 + j], c);
+    // exclusive prefix of c over the block's threads, per list
+    int64_t base[NLIST];
+#pragma unroll
+    for (int l = 0; l < NLIST; l++) {
+        int64_t x = c[l];
+        for (int m = 1; m < 64; m <<= 1) {
+            const int64_t y = __shfl_up(x, m, 64);
+            if (lane >= m) x += y;
+        }
+        base[l] = x - c[l];
+        if (lane == 63) wsum[w][l] = x;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int l = 0; l < NLIST; l++) {
+        int64_t before = (int64_t)tile_off[(int64_t)l * ntiles + blockIdx.x];
+        for (int q = 0; q < w; q++) before += wsum[q][l];
+        base[l] += before;
+    }
+    if (s0 >= P) return;
+    int64_t prev = s0 == 0 ? -1 : (int64_t)(keys[seg_start[s0 - 1]] >> vbits);
+    for (int j = 0; j < LT_PER && s0 + j < P; j++) {
+        const int64_t sg = s0 + j;
+        const int64_t b = seg_start[sg];
+        const int64_t chunk = (int64_t)(keys[b] >> vbits);
+        for (int64_t k = prev + 1; k <= chunk; k++)
+            for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = base[l];
+        prev = chunk;
+        const SegUnit u = seg_unit(keys, seg_start, sg, vbits, C, chunk_off, first_chunk);
+        const int64_t slots = slots_of[sg];
+        const int cls = seg_class(slots);
+        if (cls < NCLASS) {
+            units[base[cls]++] = make_int4((int)u.rel, (int)slots | u.nf | u.self, u.v, 0);
+        } else {
+            const int pieces = (int)((slots + PIECE_LEN - 1) / PIECE_LEN);
+            const int64_t first = base[NCLASS];
+            for (int q = 0; q < pieces; q++) {
+                const int64_t o = (int64_t)q * PIECE_LEN;
+                const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
+                const int self = q == pieces - 1 ? u.self : 0;
+                units[first + q] = make_int4((int)(u.rel + o), plen | u.nf | self, u.v, pieces > 1 ? (int)(first + q) : -1);
+            }
+            base[NCLASS] += pieces;
+            if (pieces > 1) units[base[NCLASS + 1]++] = make_int4(u.v, (int)first, pieces, 0);
+        }
+    }
+    if (s0 + LT_PER >= P) {  // the thread holding the last segment
+        for (int64_t k = prev + 1; k <= nchunks; k++)
+            for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = base[l];
+    }
 }
 
 // SELF_FIRST: v's own chunk is no later than its first message chunk, so
@@ -1271,8 +1266,10 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     // flags: 1, 2 invalid CSR; 4 unsorted row or self loop; 8 sort inconsistency
     int* bad = tmp.alloc<int>(1, "graph flag");
     fill_i32(bad, 1, 0, s);
-    k_validate_graph<<<(unsigned)ceil_div(std::max(n, e), T), T, 0, s>>>(g.row_off, g.col_dst, n, e, bad);
-    TAURUS_CHECK_LAUNCH();
+    if (!sample) {  // a sampled layer's in-edge lists were built from a validated CSR
+        k_validate_graph<<<(unsigned)ceil_div(std::max(n, e), T), T, 0, s>>>(g.row_off, g.col_dst, n, e, bad);
+        TAURUS_CHECK_LAUNCH();
+    }
     int hbad = 0;
     if (e == 0) {  // no messages: the self passes do all the work
         Readback rb;
@@ -1292,12 +1289,14 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
     SortBuffers sb{{nullptr, nullptr}, {nullptr, nullptr}, 0};
     int64_t items = e;
+    int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
+    fill_i32(first_chunk, n, 0x7fffffff, s);
     if (sample) {
         // the sampler's kept in-edges come destination-major with sources
         // ascending, so a stable sort by the chunk field alone orders them
         // by (chunk, destination, source)
         items = sample_items(*sample->csc, n, sample->seed, sample->layer, sample->k, C, vbits, tmp, idx->arena, sb,
-                             bad, s);
+                             idx->m, first_chunk, bad, s);
         radix_sort_u64(sb, items, cbits, tmp, s, bad, 8, nullptr, vbits);
     } else {
         sb.keys[0] = tmp.alloc<uint64_t>(e, "index keys");
@@ -1350,109 +1349,53 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     int64_t* seg_start = tmp.alloc<int64_t>(P + 1, "segment starts");
     k_head_positions<<<(unsigned)nbt, 256, 0, s>>>(keys, items, doffs + nch, hoff, P, seg_start);
     TAURUS_CHECK_LAUNCH();
-    int64_t* chunk_seg = tmp.alloc<int64_t>(nch + 1, "first segment per chunk");
-    k_chunk_segments<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(doffs, nch, seg_start, P, chunk_seg);
-    TAURUS_CHECK_LAUNCH();
     tmp.free_ptr(hoff);
     tmp.free_ptr(hcount);
-    int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
-    fill_i32(first_chunk, n, 0x7fffffff, s);
     int32_t* slots_of = tmp.alloc<int32_t>(P, "segment slots");
-    k_seg_classify<<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m, first_chunk,
-                                                          slots_of, idx->has_own, idx->own_count);
+    if (sample)
+        k_seg_classify<true><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m, first_chunk,
+                                                                    slots_of, idx->has_own, idx->own_count);
+    else
+        k_seg_classify<false><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m,
+                                                                     first_chunk, slots_of, idx->has_own,
+                                                                     idx->own_count);
     TAURUS_CHECK_LAUNCH();
     k_self_first<<<(unsigned)ceil_div(n, T), T, 0, s>>>(first_chunk, n, C, idx->has_own);
     TAURUS_CHECK_LAUNCH();
-    // Unit positions: one exclusive scan over all lists (P * NLIST counts,
-    // positions absolute in the work-list buffer), or, when those arrays
-    // would be large, list by list with one count buffer and one offset
-    // buffer (two for the wave pieces and their fix-up entries).  Both give
-    // the same lists.
-    const int lean_env = env_int("TAURUS_INDEX_LEAN", -1);
-    const bool lean = lean_env >= 0 ? lean_env != 0 : P * NLIST * 12 > ((int64_t)1 << 30);
-    const unsigned gP = (unsigned)ceil_div(P, T), gC = (unsigned)ceil_div(nch + 1, T);
-    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list bases");
-    std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);
+    // Unit positions: per tile of LT_TILE segments, the entries each list
+    // takes (one pass), an exclusive scan over all lists' tiles one list
+    // after another (the lists' buffer positions), then each tile writes its
+    // units and its chunks' first positions (a second pass).
+    const int64_t ntiles = ceil_div(P, LT_TILE);
+    uint64_t* tile_cnt = tmp.alloc<uint64_t>(ntiles * NLIST, "list entries per tile");
+    uint64_t* tile_off = tmp.alloc<uint64_t>(ntiles * NLIST + 1, "list positions per tile");
+    k_list_tile_counts<<<(unsigned)ntiles, LT_THREADS, 0, s>>>(slots_of, P, ntiles, tile_cnt);
+    TAURUS_CHECK_LAUNCH();
+    scan_u64(tile_cnt, tile_off, ntiles * NLIST, true, tmp, s);
     int64_t list_base[NLIST + 1] = {0};
-    if (!lean) {
-        int32_t* lcnt = tmp.alloc<int32_t>(P * NLIST, "list counts");
-        k_list_counts_all<<<gP, T, 0, s>>>(slots_of, P, lcnt);
-        TAURUS_CHECK_LAUNCH();
-        int64_t* loff = tmp.alloc<int64_t>(P * NLIST + 1, "list offsets");
-        scan_i32_to_i64(lcnt, loff, P * NLIST, true, tmp, s);
-        k_list_chunk_bases<<<dim3(gC, NLIST), T, 0, s>>>(chunk_seg, nch, loff, P, dbases);
-        TAURUS_CHECK_LAUNCH();
-        int64_t total_units = 0;
-        {
-            Readback rb;
-            rb.add(bases.data(), dbases, (nch + 1) * NLIST);
-            rb.add(&total_units, loff + P * NLIST, 1);
-            rb.run(s);
-        }
-        if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
-        idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
-        k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, -1, vbits, C, doffs, first_chunk, loff,
-                                      idx->units);
-        TAURUS_CHECK_LAUNCH();
-        k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk,
-                                     loff + (int64_t)NCLASS * P, loff + (int64_t)(NCLASS + 1) * P, idx->units,
-                                     idx->units, 0);
-        TAURUS_CHECK_LAUNCH();
+    {
+        uint64_t lb[NLIST + 1] = {};
+        Readback rb;
+        for (int l = 0; l < NLIST; l++) rb.add(&lb[l], tile_off + (int64_t)l * ntiles, 1);
+        rb.add(&lb[NLIST], tile_off + ntiles * NLIST, 1);
+        rb.run(s);
+        for (int l = 0; l <= NLIST; l++) list_base[l] = (int64_t)lb[l];
+    }
+    const int64_t total_units = list_base[NLIST];
+    if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
+    idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
+    int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list positions");
+    k_list_emit<<<(unsigned)ntiles, LT_THREADS, 0, s>>>(keys, seg_start, slots_of, P, ntiles, tile_off, vbits, C,
+                                                       doffs, first_chunk, nch, idx->units, dbases);
+    TAURUS_CHECK_LAUNCH();
+    {
+        std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);
+        Readback rb;
+        rb.add(bases.data(), dbases, (nch + 1) * NLIST);
+        rb.run(s);
         for (int l = 0; l < NLIST; l++) {
             for (int64_t k = 0; k <= nch; k++) idx->list_off[l][(size_t)k] = bases[(size_t)l * (nch + 1) + (size_t)k];
-            idx->n_list[l] = idx->list_off[l][(size_t)nch] - idx->list_off[l][0];
-        }
-    } else {
-        unsigned long long* dtot = tmp.alloc<unsigned long long>(NLIST, "list totals");
-        fill_i32(reinterpret_cast<int32_t*>(dtot), 2 * NLIST, 0, s);
-        k_list_totals<<<gP, T, 0, s>>>(slots_of, P, dtot);
-        TAURUS_CHECK_LAUNCH();
-        unsigned long long tot[NLIST] = {};
-        {
-            Readback rb;
-            rb.add(tot, dtot, NLIST);
-            rb.run(s);
-        }
-        for (int l = 0; l < NLIST; l++) list_base[l + 1] = list_base[l] + (int64_t)tot[l];
-        const int64_t total_units = list_base[NLIST];
-        if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
-        idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
-        int32_t* lcnt = tmp.alloc<int32_t>(P, "list counts");
-        int64_t* loff = tmp.alloc<int64_t>(P + 1, "list offsets");
-        for (int l = 0; l < NCLASS; l++) {
-            k_list_counts<<<gP, T, 0, s>>>(slots_of, P, l, lcnt);
-            TAURUS_CHECK_LAUNCH();
-            scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
-            k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, 0, dbases + (int64_t)l * (nch + 1));
-            TAURUS_CHECK_LAUNCH();
-            k_emit_short<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, l, vbits, C, doffs, first_chunk, loff,
-                                          idx->units + list_base[l]);
-            TAURUS_CHECK_LAUNCH();
-        }
-        int64_t* loff_fix = tmp.alloc<int64_t>(P + 1, "fix-up list offsets");
-        k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS + 1, lcnt);
-        TAURUS_CHECK_LAUNCH();
-        scan_i32_to_i64(lcnt, loff_fix, P, true, tmp, s);
-        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff_fix, 0, dbases + (int64_t)(NCLASS + 1) * (nch + 1));
-        TAURUS_CHECK_LAUNCH();
-        k_list_counts<<<gP, T, 0, s>>>(slots_of, P, NCLASS, lcnt);
-        TAURUS_CHECK_LAUNCH();
-        scan_i32_to_i64(lcnt, loff, P, true, tmp, s);
-        k_list_chunk_bases<<<gC, T, 0, s>>>(chunk_seg, nch, loff, 0, dbases + (int64_t)NCLASS * (nch + 1));
-        TAURUS_CHECK_LAUNCH();
-        k_emit_long<<<gP, T, 0, s>>>(keys, seg_start, slots_of, P, vbits, C, doffs, first_chunk, loff, loff_fix,
-                                     idx->units + list_base[NCLASS], idx->units + list_base[NCLASS + 1],
-                                     (int)list_base[NCLASS]);
-        TAURUS_CHECK_LAUNCH();
-        {
-            Readback rb;
-            rb.add(bases.data(), dbases, (nch + 1) * NLIST);
-            rb.run(s);
-        }
-        for (int l = 0; l < NLIST; l++) {
-            for (int64_t k = 0; k <= nch; k++)
-                idx->list_off[l][(size_t)k] = list_base[l] + bases[(size_t)l * (nch + 1) + (size_t)k];
-            idx->n_list[l] = (int64_t)tot[l];
+            idx->n_list[l] = list_base[l + 1] - list_base[l];
         }
     }
     for (int64_t k = 0; k < nch; k++)

@@ -153,6 +153,7 @@ __device__ inline bool pair_less(uint64_t ka, uint32_t ua, uint64_t kb, uint32_t
 
 constexpr int LIGHT_MAX = 64;     // lists up to this long are ranked in registers
 constexpr int HEAVY_CAP = 1024;   // candidates a wave of the long-list pass holds in LDS
+constexpr int REG_MAX = 512;      // long lists up to this length are held in registers
 
 // Where the kept in-edges go: chunk-index items at koff[v] + (position among
 // v's kept in-edges) -- key (chunk(u) << vbits | v), value u - chunk(u)*C --
@@ -167,6 +168,7 @@ struct SampleOut {
     const int64_t* row_off;
     const int32_t* col_dst;
     int* bad;  // bit SAMPLE_BAD: a list the cutoff search could not settle (repeated sources)
+    int32_t* first_chunk;  // items mode: chunk of v's first kept source (its smallest), or null
 };
 constexpr int SAMPLE_BAD = 32;
 
@@ -184,6 +186,7 @@ __device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int6
         const int64_t at = o.koff[v] + pos;
         o.keys[at] = ((uint64_t)cu << o.vbits) | (uint64_t)v;
         o.vals[at] = u - cu * (uint32_t)o.C;
+        if (pos == 0 && o.first_chunk) o.first_chunk[v] = (int32_t)cu;
     }
 }
 
@@ -217,18 +220,22 @@ __global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict_
             key[t] = valid[t] && rank ? sample_key(pre, u[t]) : ~0ull;
         }
         int below[4] = {0, 0, 0, 0};
-        if (__ballot(rank) != 0) {
-            // every group broadcasts its 64 slots in turn; invalid slots hold
-            // (~0, ~0), which is never below a valid pair
+        // registers holding slots of a list to rank, over the wave
+        const int tn = (__ballot(rank) != 0) + (__ballot(rank && d > 16) != 0) + (__ballot(rank && d > 32) != 0) +
+                       (__ballot(rank && d > 48) != 0);
+        // every group broadcasts its slots in turn; invalid slots hold
+        // (~0, ~0), which is never below a valid pair
 #pragma unroll
-            for (int t = 0; t < 4; t++)
-                for (int j = 0; j < 16; j++) {
-                    const uint32_t klo = __shfl((uint32_t)key[t], j, 16), khi = __shfl((uint32_t)(key[t] >> 32), j, 16);
-                    const uint32_t uj = __shfl(u[t], j, 16);
-                    const uint64_t kj = ((uint64_t)khi << 32) | klo;
+        for (int t = 0; t < 4; t++) {
+            if (t >= tn) break;  // uniform over the wave
+            for (int j = 0; j < 16; j++) {
+                const uint32_t klo = __shfl((uint32_t)key[t], j, 16), khi = __shfl((uint32_t)(key[t] >> 32), j, 16);
+                const uint32_t uj = __shfl(u[t], j, 16);
+                const uint64_t kj = ((uint64_t)khi << 32) | klo;
 #pragma unroll
-                    for (int q = 0; q < 4; q++) below[q] += pair_less(kj, uj, key[q], u[q]) ? 1 : 0;
-                }
+                for (int q = 0; q < 4; q++)
+                    if (q < tn) below[q] += pair_less(kj, uj, key[q], u[q]) ? 1 : 0;
+            }
         }
         // kept slots in slot order (slot = t * 16 + sub): the position among
         // the destination's kept in-edges counts the kept slots before it
@@ -266,8 +273,26 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
             continue;
         }
         const uint64_t pre = sample_prefix(seed, (uint64_t)layer, (uint64_t)v);
+        // lists of up to REG_MAX in-edges are read once into registers
+        const bool in_regs = d <= REG_MAX;
+        uint64_t rk[REG_MAX / 64];
+        uint32_t ru[REG_MAX / 64];
+        if (in_regs) {
+#pragma unroll
+            for (int t = 0; t < REG_MAX / 64; t++) {
+                const int64_t sl = t * 64 + lane;
+                ru[t] = sl < d ? (uint32_t)in_src[a + sl] : ~0u;
+            }
+#pragma unroll
+            for (int t = 0; t < REG_MAX / 64; t++) rk[t] = (int64_t)t * 64 + lane < d ? sample_key(pre, ru[t]) : ~0ull;
+        }
         auto count = [&](uint64_t cut) {
             int64_t c = 0;
+            if (in_regs) {
+#pragma unroll
+                for (int t = 0; t < REG_MAX / 64; t++) c += __popcll(__ballot((int64_t)t * 64 + lane < d && rk[t] <= cut));
+                return c;
+            }
             for (int64_t sl = lane; sl - lane < d; sl += 64) {
                 const bool in = sl < d && sample_key(pre, (uint32_t)in_src[a + sl]) <= cut;
                 c += __popcll(__ballot(in));
@@ -301,15 +326,7 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
         }
         // candidates in CSC order (sources ascending)
         int64_t m = 0;
-        for (int64_t sl = lane; sl - lane < d; sl += 64) {
-            uint32_t uu = 0;
-            uint64_t kk = ~0ull;
-            bool in = false;
-            if (sl < d) {
-                uu = (uint32_t)in_src[a + sl];
-                kk = sample_key(pre, uu);
-                in = kk <= cut;
-            }
+        auto gather = [&](bool in, uint64_t kk, uint32_t uu) {
             const uint64_t bal = __ballot(in);
             if (in) {
                 const int64_t at = m + __popcll(bal & lt);
@@ -317,6 +334,20 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
                 cu[w][at] = uu;
             }
             m += __popcll(bal);
+        };
+        if (in_regs) {
+#pragma unroll
+            for (int t = 0; t < REG_MAX / 64; t++) gather((int64_t)t * 64 + lane < d && rk[t] <= cut, rk[t], ru[t]);
+        } else {
+            for (int64_t sl = lane; sl - lane < d; sl += 64) {
+                uint32_t uu = 0;
+                uint64_t kk = ~0ull;
+                if (sl < d) {
+                    uu = (uint32_t)in_src[a + sl];
+                    kk = sample_key(pre, uu);
+                }
+                gather(sl < d && kk <= cut, kk, uu);
+            }
         }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -369,14 +400,13 @@ __global__ void k_sample_counts(const int64_t* __restrict__ in_off, int64_t n, i
 }
 
 int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, int64_t C, int vbits,
-                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int* bad, hipStream_t s) {
+                     Arena& key_arena, Arena& val_arena, SortBuffers& sb, int32_t* m, int32_t* first_chunk, int* bad,
+                     hipStream_t s) {
     if (k < 1 || k > FANOUT_MAX) fail(TAURUS_E_INVALID, "fanout %d outside [1, %d]", k, FANOUT_MAX);
-    Arena tmp(s);
-    int32_t* m = tmp.alloc<int32_t>(n, "kept per destination");
-    int64_t* koff = tmp.alloc<int64_t>(n + 1, "kept before each destination");
+    int64_t* koff = key_arena.alloc<int64_t>(n + 1, "kept before each destination");
     k_sample_counts<<<(unsigned)ceil_div(n, 256), 256, 0, s>>>(csc.in_off, n, k, m);
     TAURUS_CHECK_LAUNCH();
-    scan_i32_to_i64(m, koff, n, true, tmp, s);
+    scan_i32_to_i64(m, koff, n, true, key_arena, s);
     int64_t kept = 0;
     {
         Readback rb;
@@ -391,7 +421,8 @@ int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k,
     sb.cur = 0;
     if (kept > 0)
         sample_pass(csc, n, seed, layer, k,
-                    SampleOut{sb.keys[0], sb.vals[0], koff, C, vbits, nullptr, nullptr, nullptr, bad}, s);
+                    SampleOut{sb.keys[0], sb.vals[0], koff, C, vbits, nullptr, nullptr, nullptr, bad, first_chunk},
+                    s);
     return kept;
 }
 
@@ -405,7 +436,7 @@ void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer
     fill_i32(bad, 1, 0, s);
     sample_pass(csc, g.n, seed, layer, k,
                 SampleOut{nullptr, nullptr, nullptr, 1, 1, reinterpret_cast<unsigned long long*>(mask), g.row_off,
-                          g.col_dst, bad},
+                          g.col_dst, bad, nullptr},
                 s);
     int hbad = 0;
     Readback rb;
