@@ -268,6 +268,8 @@ def main():
                     default="sage3-fanout-rmat-100m")
     ap.add_argument("--scale", type=int, default=1,
                     help="sage3-fanout-rmat-100m only: divide vertices and edges by this (trial runs; not a result)")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="sage3-fanout-rmat-100m only: source chunk size (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--full-profile", action="store_true",
@@ -527,6 +529,9 @@ def bench_sage3_100m(args):
     w = WL.SAGE_FANOUT_RMAT_100M
     if args.scale > 1:
         w = w.scaled(n=w.n // args.scale, e=w.e // args.scale)
+    if args.chunk > 0:
+        import dataclasses
+        w = dataclasses.replace(w, chunk=args.chunk)
     specs = H.layer_specs(w)
     nl = len(specs)
     src, dst = WL.graph(w)
@@ -541,6 +546,16 @@ def bench_sage3_100m(args):
     nbytes = [w.n * s["d_out"] * (4 if s["out_dtype"] == F.F32 else 2) for s in specs]
     buf_a = torch.empty(max(nbytes[0], nbytes[2]), dtype=torch.uint8, device=dev)
     buf_b = torch.empty(nbytes[1], dtype=torch.uint8, device=dev)
+
+    if args.copy_calibration:
+        # a plain streaming kernel of known size for the byte counters:
+        # neg reads 1 GiB and writes 1 GiB
+        ca = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        cb = torch.empty_like(ca)
+        for _ in range(3):
+            torch.neg(ca, out=cb)
+        del ca, cb
+        torch.cuda.synchronize()
 
     def out_view(li):
         buf = buf_b if li == 1 else buf_a
@@ -661,7 +676,7 @@ def bench_sage3_100m(args):
                 got_rows[("in", li + 2)] = out.index_select(0, torch.from_numpy(need_rows[li + 2]).to(dev)).cpu()
             got_rows[("out", li + 1)] = out.index_select(0, torch.from_numpy(ids[li]).to(dev)).cpu()
 
-    per = layers_pass(1, hook)
+    per = layers_pass(1, hook) if (need_rows or not args.no_profile) else []
     gf = gb = gms = 0.0
     for li, st in enumerate(per):
         d_in, d_o = specs[li]["d_in"], specs[li]["d_out"]

@@ -104,11 +104,13 @@ typedef struct {
  *                in_dtype the weights are rounded to that type at init.
  *   bias         HOST fp32 [d_out], or NULL for no bias; copied at init.
  *   fanout       0 = exact inference (every in-edge propagates); k in
- *                [1, 64] keeps for each destination v its min(d_in(v), k)
+ *                [1, 512] keeps for each destination v its min(d_in(v), k)
  *                in-edges whose rank key (H(seed, 4, layer, v, u), u) is
  *                smallest, where H is the SplitMix64-based counter hash of
- *                taurus_hash() (GraphSAGE layers only: the sampled GCN
- *                normalisation is not defined here).
+ *                taurus_hash() (Sec. 3.9, sampling-based inference).  Every
+ *                family samples the same way; a sampled GCN layer normalises
+ *                by the sampled graph's degrees, (kept out-degree(u) + 1) on
+ *                the source side and (|M(v)| + 1) on the destination side.
  *   layer        1-based layer number (only feeds the sampling hash).
  *   seed         sampling seed.
  *   chunk        source-chunk size C in vertices (> 0).  Chunk j covers
@@ -372,19 +374,28 @@ int taurus_plan_create(const taurus_graph* g, int64_t chunk, void* stream, tauru
 void taurus_plan_destroy(taurus_plan* plan);
 
 /*
- * Create the state of one layer: copies the weights, computes degrees and
- * normalisers, draws the fanout mask (fanout > 0), builds or takes the
- * per-chunk destination index, and sets every vertex's pending-message count
- * to |M(v)| + 1 (the self message counts as one arrival).  *out receives the
- * handle.  Blocks until the index is built.
+ * Create the state of one layer (Sec. 3.4: one pending-message count per
+ * vertex, O(|V|) state; Sec. 3.9 for the sampled message set M(v)): copies
+ * the weights, computes degrees and normalisers, draws the fanout sample
+ * (fanout > 0), builds or takes the per-chunk destination index, and sets
+ * every vertex's pending-message count to |M(v)| + 1 (the self message
+ * counts as one arrival).  Without a budget the dense accumulators are
+ * allocated first and hold the index build's temporaries until the first
+ * push.  *out receives the handle.  Blocks until the index is built.
+ * Errors: TAURUS_E_INVALID for bad arguments or a graph that is not a valid
+ * simple CSR; TAURUS_E_BUDGET when the budget cannot hold the layer;
+ * TAURUS_E_OOM / TAURUS_E_DEVICE from the runtime.  On error *out is NULL.
  */
 int taurus_layer_init(const taurus_graph* g, const taurus_layer_desc* d, taurus_layer** out);
 
 /*
- * Stream one source chunk through the layer (Sec. 3.3-3.6): transform the
- * chunk's rows, push their messages to the destinations and finalise every
- * destination whose last message arrives.  [src_begin, src_end) must be a
- * whole chunk: src_begin = j*chunk, src_end = min(src_begin + chunk, n).
+ * Stream one source chunk through the layer (Sec. 3.1 broadcast along
+ * out-edges; Secs. 3.3-3.6): transform the chunk's rows, push their messages
+ * to the destinations and finalise every destination whose last message
+ * arrives.  [src_begin, src_end) must be a whole chunk: src_begin = j*chunk,
+ * src_end = min(src_begin + chunk, n), because the destination index (which
+ * destinations a chunk's sources reach, grouped into work units) is built
+ * per chunk at init; other ranges return TAURUS_E_INVALID.
  * x points at the chunk's rows (row src_begin first), row-major
  * [src_end - src_begin][d_in] of in_dtype: device memory if x_on_host = 0,
  * pinned host memory if x_on_host = 1 (copied on the layer's own copy
@@ -398,8 +409,10 @@ int taurus_push_chunk(taurus_layer* L, int64_t src_begin, int64_t src_end, const
                       int32_t x_on_host);
 
 /*
- * Wait for the layer's work, check that every destination completed and fill
- * *stats (may be NULL).  Returns TAURUS_E_INCOMPLETE (with the count in
+ * Wait for the layer's work, check that every destination completed (Sec.
+ * 3.6: a vertex graduates once its pending count reaches zero, its output
+ * row written by the flush that completes it) and fill *stats (may be
+ * NULL).  Returns TAURUS_E_INCOMPLETE (with the count in
  * stats->pending_left) if some destination still has pending messages, e.g.
  * because a chunk was never pushed.  After TAURUS_OK every row of desc.out
  * holds its final value.
@@ -407,11 +420,14 @@ int taurus_push_chunk(taurus_layer* L, int64_t src_begin, int64_t src_end, const
 int taurus_finalize(taurus_layer* L, taurus_stats* stats);
 
 /*
- * Copy the layer's propagated-edge mask to host memory: bit i of
- * mask_bits_host[i / 64] (least significant bit first) is set if CSR edge i
- * propagates in this layer (all ones for exact layers).  mask_bits_host has
- * ceil(e/64) words; *n_kept receives the number of set bits (may be NULL).
- * Synchronises the layer's stream.
+ * Copy the layer's propagated-edge mask to host memory (Sec. 3.9: the
+ * incoming edges the fanout sample keeps): bit i of mask_bits_host[i / 64]
+ * (least significant bit first) is set if CSR edge i propagates in this
+ * layer (all ones for exact layers).  mask_bits_host has ceil(e/64) words;
+ * *n_kept receives the number of set bits (may be NULL).  A sampled layer
+ * draws the CSR-order mask on the first call (the same selection as the
+ * layer's index), which takes ceil(e/64) words of device memory until
+ * destroy.  Synchronises the layer's stream.
  */
 int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_kept);
 

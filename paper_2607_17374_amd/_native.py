@@ -15,7 +15,9 @@ LIB_PATH = os.path.join(_HERE, "libtaurus.so")
 
 OK, E_INVALID, E_OOM, E_DEVICE, E_STATE, E_INCOMPLETE, E_BUDGET = 0, -1, -2, -3, -4, -5, -6
 F32, BF16, F16 = 0, 1, 2
-SAGE_MEAN, GCN_SYM = 0, 1
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
+EVICT_PENDING, EVICT_RANDOM, EVICT_FIFO, EVICT_LRU = 0, 1, 2, 3
+NOALLOC_SCRATCH_BYTES, NOALLOC_MAX_EDGES = 32 << 20, 1 << 20
 
 STATUS_NAMES = {OK: "OK", E_INVALID: "E_INVALID", E_OOM: "E_OOM", E_DEVICE: "E_DEVICE",
                 E_STATE: "E_STATE", E_INCOMPLETE: "E_INCOMPLETE", E_BUDGET: "E_BUDGET"}

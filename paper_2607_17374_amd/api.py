@@ -66,7 +66,7 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None):
     return row_off, col_dst
 
 
-NOALLOC_MAX_EDGES = 1 << 20   # TAURUS_NOALLOC_MAX_EDGES
+NOALLOC_MAX_EDGES = N.NOALLOC_MAX_EDGES
 
 
 def build_csr_noalloc(n: int, src: torch.Tensor, dst: torch.Tensor, row_off: torch.Tensor, col_dst: torch.Tensor,
@@ -182,7 +182,7 @@ def alloc_device(shape, dtype, device) -> torch.Tensor:
 
 
 # eviction policies of a budgeted layer (taurus_eviction)
-EVICTION = {"pending": 0, "random": 1, "fifo": 2, "lru": 3}
+EVICTION = {"pending": N.EVICT_PENDING, "random": N.EVICT_RANDOM, "fifo": N.EVICT_FIFO, "lru": N.EVICT_LRU}
 
 
 class Plan:

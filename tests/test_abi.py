@@ -38,6 +38,37 @@ def test_library_exports_every_declared_symbol(native):
         assert name in native.SIGNATURES, f"binding lacks {name}"
 
 
+def header_constants():
+    """TAURUS_* constants of the header's enums and #defines -> values."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    vals = {}
+    for name, val in re.findall(r"\b(TAURUS_[A-Z0-9_]+)\s*=\s*(-?\d+)", text):
+        vals[name] = int(val)
+    for name, a, b in re.findall(r"#define\s+(TAURUS_[A-Z0-9_]+)\s+\((\d+)ll\s*<<\s*(\d+)\)", text):
+        vals[name] = int(a) << int(b)
+    return vals
+
+
+def test_binding_constants_match_header(native):
+    vals = header_constants()
+    for name, val in vals.items():
+        short = name[len("TAURUS_"):]
+        if short in ("OK",) or hasattr(native, short):
+            assert getattr(native, short) == val, name
+        else:
+            raise AssertionError(f"binding lacks {name}")
+
+
+def test_binding_signatures_match_header(native):
+    """Each declared function takes as many arguments in the binding as in
+    the header."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for name, params in re.findall(r"\b(taurus_[a-z_0-9]+)\s*\(([^)]*)\)\s*;", text):
+        params = params.strip()
+        n = 0 if params in ("", "void") else params.count(",") + 1
+        assert len(native.SIGNATURES[name][1]) == n, name
+
+
 def test_binding_structs_match_header_layout(native):
     # field order and sizes as declared in taurus.h (x86-64 alignment)
     assert ctypes.sizeof(native.Graph) == 32
