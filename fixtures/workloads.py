@@ -15,7 +15,7 @@ import numpy as np
 from . import F32, BF16, F16, UNIFORM, NORMAL
 from . import rmat_edges, features, weights, bias, round16
 
-SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT, GIN_MLP = 0, 1, 2, 3, 4
 
 
 @dataclass(frozen=True)
@@ -116,6 +116,10 @@ class LayerParams:
     W: np.ndarray             # fp32 (rows d_out), values already rounded to the storage dtype
     b: np.ndarray             # fp32 [d_out]
     attn: np.ndarray | None = None   # GAT: [2][d_out] fp32, row 0 source, row 1 destination
+    # GIN with a perceptron apply: W is its first layer [d_h][d_in] and b its
+    # bias; W2 [d_out][d_h] and b2 [d_out] the second layer
+    W2: np.ndarray | None = None
+    b2: np.ndarray | None = None
 
     @property
     def W_agg(self):
@@ -135,13 +139,22 @@ class LayerParams:
 def layer_params(w: Workload, layer: int) -> LayerParams:
     d_in, d_out = w.dims[layer - 1], w.dims[layer]
     cols = 2 * d_in if w.agg == SAGE_MEAN else d_in
+    # GIN's perceptron: hidden width d_out, its first layer d_in -> d_out
+    # here and its second layer d_out -> d_out from the layer number + 100
     W = weights(w.seed, layer, d_out, cols, fan_in=cols, fan_out=d_out)
     if w.feat_dtype != F32:
         from . import bits_to_float
         W = bits_to_float(round16(W, w.feat_dtype), w.feat_dtype).reshape(W.shape)
     b = bias(w.seed, layer, d_out, fan_in=cols)
+    W2 = b2 = None
+    if w.agg == GIN_MLP:
+        W2 = weights(w.seed, 100 + layer, d_out, d_out, fan_in=d_out, fan_out=d_out)
+        if w.feat_dtype != F32:
+            from . import bits_to_float
+            W2 = bits_to_float(round16(W2, w.feat_dtype), w.feat_dtype).reshape(W2.shape)
+        b2 = bias(w.seed, 100 + layer, d_out, fan_in=d_out)
     attn = None
     if w.agg == GAT_ATT:
         from . import attention
         attn = attention(w.seed, layer, d_out)
-    return LayerParams(layer, w.agg, d_in, d_out, W, b, attn)
+    return LayerParams(layer, w.agg, d_in, d_out, W, b, attn, W2, b2)

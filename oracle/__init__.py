@@ -23,7 +23,7 @@ _SO = os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "oracle.c")
 
 F32, BF16, F16 = 0, 1, 2
-SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT, GIN_MLP = 0, 1, 2, 3, 4
 
 
 def build(force: bool = True) -> str:
@@ -93,6 +93,8 @@ def load(path: str):
     L.or_ta_step.argtypes = [i64, vp, vp, vp, vp, vp, vp, vp]
     L.or_reorder_ta.restype = i32
     L.or_reorder_ta.argtypes = [i64, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+    L.or_gin_mlp_layer.restype = i32
+    L.or_gin_mlp_layer.argtypes = [i64, vp, vp, vp, vp, i32, i64, vp, vp, i64, vp, vp, i64, i32, i64, vp, vp]
     L.or_dispersion.restype = ctypes.c_double
     L.or_dispersion.argtypes = [i64, vp, vp, vp]
     return L
@@ -238,6 +240,30 @@ def layer(agg: int, g: Graph, H: np.ndarray, h_dtype: int, W: np.ndarray, b: np.
                         count, _p(ids), _p(out))
     if rc:
         raise RuntimeError(f"or_layer: {rc}")
+    return out
+
+
+def gin_mlp_layer(g, H: np.ndarray, h_dtype: int, W1: np.ndarray, b1: np.ndarray | None, W2: np.ndarray,
+                  b2: np.ndarray | None, relu: bool, keep_in: np.ndarray | None = None,
+                  dst_ids: np.ndarray | None = None) -> np.ndarray:
+    """GIN layer with a two-layer perceptron apply function (eps = 0) in fp64
+    for ``dst_ids`` (all if None): W1 [d_h][d_in], W2 [d_out][d_h]."""
+    H = np.ascontiguousarray(H)
+    d_in = H.shape[1]
+    W1 = np.ascontiguousarray(W1, np.float64)
+    W2 = np.ascontiguousarray(W2, np.float64)
+    d_h, d_out = W1.shape[0], W2.shape[0]
+    assert W1.shape[1] == d_in and W2.shape[1] == d_h
+    c1 = None if b1 is None else np.ascontiguousarray(b1, np.float64)
+    c2 = None if b2 is None else np.ascontiguousarray(b2, np.float64)
+    ids = None if dst_ids is None else np.ascontiguousarray(dst_ids, np.int64)
+    count = g.n if ids is None else ids.size
+    out = np.empty((count, d_out), np.float64)
+    kin = None if keep_in is None else np.ascontiguousarray(keep_in, np.uint8)
+    rc = lib().or_gin_mlp_layer(g.n, _p(g.in_off), _p(g.in_src), _p(kin), _p(H), h_dtype, d_in, _p(W1), _p(c1),
+                                d_h, _p(W2), _p(c2), d_out, int(relu), count, _p(ids), _p(out))
+    if rc:
+        raise RuntimeError(f"or_gin_mlp_layer: {rc}")
     return out
 
 

@@ -23,8 +23,9 @@
  *   - fanout sampling: up to k incoming edges kept per vertex, per layer
  *     (Sec. 3.9, "Sampling-based Inference"), ranked by a counter-based
  *     hash;
- *   - GIN (GINConv with a linear apply function, sum aggregation) and
- *     single-head GATConv (Sec. 3.9, "GATConv"; Sec. 4.1 evaluates both);
+ *   - GIN (GINConv, sum aggregation, with a linear or a two-layer
+ *     perceptron apply function) and single-head GATConv (Sec. 3.9,
+ *     "GATConv"; Sec. 4.1 evaluates both);
  *     sampled GCN layers take the sampled graph's degrees;
  *   - the degree/BFS vertex ordering used as a topology-aware bootstrap
  *     (Sec. 3.8 discusses bandwidth-style bootstraps; the exact ordering
@@ -444,6 +445,55 @@ int or_layer(int agg, int64_t n, const int64_t* in_off, const int32_t* in_src,
             for (int64_t o = 0; o < d_out; o++) {
                 double z = bias ? bias[o] : 0.0;
                 for (int64_t j = 0; j < cols; j++) z += W[o * cols + j] * a[j];
+                if (relu && z < 0.0) z = 0.0;
+                out[i * d_out + o] = z;
+            }
+        }
+        free(a);
+    }
+    return bad ? -3 : 0;
+}
+
+/*
+ * GINConv with a two-layer perceptron as its apply function and eps = 0
+ * (Sec. 4.1 evaluates GINConv; the perceptron is the standard GIN update):
+ *     a    = h_v + sum_{u in M(v)} h_u                    (sum aggregation)
+ *     t    = ReLU(W1 a + b1)                              (W1: d_h x d_in)
+ *     z    = W2 t + b2                                    (W2: d_out x d_h)
+ * Output: out[i][j] = ReLU(z_j) if relu else z_j, for v = dst_ids[i] (all
+ * vertices when dst_ids is NULL).  keep_in selects the propagated in-edges
+ * (NULL = all).  b1, b2 may be NULL (zero).  Returns 0, or -3 when out of
+ * memory.
+ */
+int or_gin_mlp_layer(int64_t n, const int64_t* in_off, const int32_t* in_src, const uint8_t* keep_in,
+                     const void* H, int h_dtype, int64_t d_in, const double* W1, const double* b1, int64_t d_h,
+                     const double* W2, const double* b2, int64_t d_out, int relu, int64_t n_dst,
+                     const int64_t* dst_ids, double* out) {
+    int64_t count = dst_ids ? n_dst : n;
+    int bad = 0;
+#pragma omp parallel
+    {
+        double* a = (double*)malloc((size_t)(d_in + d_h) * sizeof(double));
+        double* t = a ? a + d_in : NULL;
+        if (!a) bad = 1;
+#pragma omp for schedule(dynamic, 256)
+        for (int64_t i = 0; i < count; i++) {
+            if (!a) continue;
+            int64_t v = dst_ids ? dst_ids[i] : i;
+            for (int64_t j = 0; j < d_in; j++) a[j] = or_load(H, h_dtype, v * d_in + j);
+            for (int64_t k = in_off[v]; k < in_off[v + 1]; k++) {
+                if (keep_in && !keep_in[k]) continue;
+                int64_t u = in_src[k];
+                for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, u * d_in + j);
+            }
+            for (int64_t h = 0; h < d_h; h++) {
+                double x = b1 ? b1[h] : 0.0;
+                for (int64_t j = 0; j < d_in; j++) x += W1[h * d_in + j] * a[j];
+                t[h] = x > 0.0 ? x : 0.0;
+            }
+            for (int64_t o = 0; o < d_out; o++) {
+                double z = b2 ? b2[o] : 0.0;
+                for (int64_t h = 0; h < d_h; h++) z += W2[o * d_h + h] * t[h];
                 if (relu && z < 0.0) z = 0.0;
                 out[i * d_out + o] = z;
             }

@@ -170,6 +170,16 @@ MUTANTS = {
         "for (int64_t j = 0; j < d_in; j++) a[j] += or_load(H, h_dtype, v * d_in + j);\n            }",
         "(void)0;\n            }",
         [lambda: P.test_gin_matches_dense(False)]),
+    # GIN with a perceptron: hidden ReLU dropped
+    "gin_mlp_no_hidden_relu": (
+        "t[h] = x > 0.0 ? x : 0.0;",
+        "t[h] = x;",
+        [lambda: P.test_gin_mlp_matches_dense(False)]),
+    # GIN with a perceptron: the second layer's weight transposed
+    "gin_mlp_w2_transposed": (
+        "for (int64_t h = 0; h < d_h; h++) z += W2[o * d_h + h] * t[h];",
+        "for (int64_t h = 0; h < d_h; h++) z += W2[h * d_out + o] * t[h];",
+        [lambda: P.test_gin_mlp_matches_dense(False)]),
     # GAT without the self message in the softmax
     "gat_no_self_message": (
         "for (int64_t k = in_off[v] - 1; k < in_off[v + 1]; k++) {",

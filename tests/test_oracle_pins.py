@@ -249,6 +249,41 @@ def test_gin_matches_dense(sampled):
     np.testing.assert_allclose(z, 0.5 * (np.diff(g.in_off)[:, None] + 1) * np.ones((1, d_in)), rtol=0, atol=0)
 
 
+@pytest.mark.parametrize("sampled", [False, True])
+def test_gin_mlp_matches_dense(sampled):
+    """GIN with a two-layer perceptron apply function: ReLU(((A^T + I) H) W1^T
+    + b1) W2^T + b2 as dense matrix products (numpy), exact and sampled;
+    identity second layer and zero bias reduce it to ReLU of the linear GIN."""
+    rng = np.random.default_rng(28)
+    n, d_in, d_h, d_out = 80, 6, 9, 5
+    A, u, v = random_digraph(rng, n, 0.09, isolated=3)
+    g = O.Graph(n, u, v)
+    H32 = rng.standard_normal((n, d_in)).astype(np.float32)
+    W1, b1 = rng.standard_normal((d_h, d_in)), rng.standard_normal(d_h)
+    W2, b2 = rng.standard_normal((d_out, d_h)), rng.standard_normal(d_out)
+    keep_in, A_used = None, A
+    if sampled:
+        words, keep_in, _ = O.sample(g, 6, 2, 3)
+        bits = O.mask_bits(words, g.e)
+        A_used = np.zeros_like(A)
+        A_used[np.repeat(np.arange(n), np.diff(g.row_off))[bits], g.col_dst[bits]] = True
+    agg = (A_used.astype(np.float64) + np.eye(n)).T @ H32.astype(np.float64)
+    for relu in (False, True):
+        want = np.maximum(agg @ W1.T + b1, 0) @ W2.T + b2
+        if relu:
+            want = np.maximum(want, 0)
+        got = O.gin_mlp_layer(g, H32, O.F32, W1, b1, W2, b2, relu, keep_in=keep_in)
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    # W2 = I, no biases: ReLU of the linear GIN with W1
+    z = O.gin_mlp_layer(g, H32, O.F32, W1, None, np.eye(d_h), None, False, keep_in=keep_in)
+    lin = O.layer(O.GIN_SUM, g, H32, O.F32, W1, None, True, keep_in=keep_in)
+    np.testing.assert_allclose(z, lin, rtol=1e-13, atol=1e-13)
+    # subset of destinations equals rows of the full result
+    ids = np.array([0, 5, 17, n - 1], np.int64)
+    sub = O.gin_mlp_layer(g, H32, O.F32, W1, b1, W2, b2, True, keep_in=keep_in, dst_ids=ids)
+    np.testing.assert_array_equal(sub, O.gin_mlp_layer(g, H32, O.F32, W1, b1, W2, b2, True, keep_in=keep_in)[ids])
+
+
 def test_subset_of_destinations_equals_rows_of_full():
     rng = np.random.default_rng(8)
     n = 70
