@@ -47,8 +47,8 @@ MUTANTS = {
         [lambda: P.test_sage_matches_dense(1, False)]),
     # activation applied the wrong way round
     "relu_flipped": (
-        "if (relu && z < 0.0) z = 0.0;",
-        "if (relu && z > 0.0) z = 0.0;",
+        "z += W[o * cols + j] * a[j];\n                if (relu && z < 0.0) z = 0.0;",
+        "z += W[o * cols + j] * a[j];\n                if (relu && z > 0.0) z = 0.0;",
         [lambda: P.test_sage_matches_dense(0, True)]),
     # sampler keeps the largest keys
     "sampler_keeps_largest": (
