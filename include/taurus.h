@@ -63,11 +63,17 @@ typedef enum {
                              d^ = degree + 1 (one self loop per vertex); a sampled layer uses the
                              degrees of its sampled graph: kept out-edges, d^_in(v) = |M(v)| + 1 */
     TAURUS_GIN_SUM = 2,   /* GINConv, linear apply, eps = 0: z_v = W (h_v + sum_{u in M(v)} h_u) + b */
-    TAURUS_GAT_ATT = 3    /* GATConv, one head (Sec. 3.9): h' = W h, e_uv = LeakyReLU(a^T [h'_u || h'_v]),
+    TAURUS_GAT_ATT = 3,   /* GATConv, one head (Sec. 3.9): h' = W h, e_uv = LeakyReLU(a^T [h'_u || h'_v]),
                              slope 0.2, alpha = softmax of e over M(v) + {v},
                              z_v = sum alpha_uv h'_u + b; needs desc.attn; in core (hbm_budget 0).
                              The pushes transform (pass 1); finalize runs the softmax statistics
                              (pass 2) and the aggregation (pass 3) over every chunk            */
+    TAURUS_GIN_MLP = 4    /* GINConv with a two-layer perceptron apply (Sec. 4.1), eps = 0:
+                             t_v = ReLU(W1 (h_v + sum_{u in M(v)} h_u) + b1), z_v = W2 t_v + b2.
+                             W1 goes before the aggregation (linearity); a destination's t_v is
+                             formed when it completes, and each chunk's completed rows then take
+                             W2 on the matrix cores (the graduation transform, Sec. 3.6).  Needs
+                             desc.d_hidden and desc.weight2; in core (hbm_budget 0)            */
 } taurus_agg;
 
 /*
@@ -147,9 +153,15 @@ typedef struct {
  *                transformed source row, row 1 (a_dst) the destination's;
  *                read at init.  NULL for the other families.
  *   eviction     TAURUS_EVICT_* policy of a budgeted layer (ignored in core).
- *                Victims are ranked by a 14-bit key: pending counts past
- *                16383 share the last bin, and chunk numbers are shifted
- *                right until the layer's chunk count fits 14 bits.
+ *                Victims are ranked by their exact key (pending count,
+ *                admission chunk or last chunk), ties by the lower ID.
+ *   d_hidden     TAURUS_GIN_MLP layers: the perceptron's hidden width (a
+ *                positive multiple of 4, at most 1024); ignored otherwise.
+ *   weight2      TAURUS_GIN_MLP layers: HOST fp32 [d_hidden][d_out], the
+ *                perceptron's second layer (z = t W2); weight is then its
+ *                first layer [d_in][d_hidden] and bias b1 [d_hidden] (or
+ *                NULL).  Copied at init.  NULL otherwise.
+ *   bias2        TAURUS_GIN_MLP layers: HOST fp32 [d_out] or NULL.
  *   plan         NULL, or a plan made for this graph (same n, e, row_off,
  *                col_dst pointers) and this chunk size: an exact layer
  *                (fanout = 0) then shares the plan's chunk index, and a
@@ -173,6 +185,9 @@ typedef struct {
     const taurus_plan* plan;
     int32_t eviction;
     const float* attn;
+    int32_t d_hidden;
+    const float* weight2;
+    const float* bias2;
 } taurus_layer_desc;
 
 typedef struct taurus_layer taurus_layer;

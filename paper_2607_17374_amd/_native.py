@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_HERE, "libtaurus.so")
 
 OK, E_INVALID, E_OOM, E_DEVICE, E_STATE, E_INCOMPLETE, E_BUDGET = 0, -1, -2, -3, -4, -5, -6
 F32, BF16, F16 = 0, 1, 2
-SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT = 0, 1, 2, 3
+SAGE_MEAN, GCN_SYM, GIN_SUM, GAT_ATT, GIN_MLP = 0, 1, 2, 3, 4
 EVICT_PENDING, EVICT_RANDOM, EVICT_FIFO, EVICT_LRU = 0, 1, 2, 3
 NOALLOC_SCRATCH_BYTES, NOALLOC_MAX_EDGES = 32 << 20, 1 << 20
 
@@ -42,7 +42,8 @@ class LayerDesc(ctypes.Structure):
                 ("chunk", ctypes.c_int64), ("hbm_budget", ctypes.c_int64), ("hub_fraction", ctypes.c_double),
                 ("out", ctypes.c_void_p), ("out_on_host", ctypes.c_int32),
                 ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p),
-                ("eviction", ctypes.c_int32), ("attn", ctypes.c_void_p)]
+                ("eviction", ctypes.c_int32), ("attn", ctypes.c_void_p), ("d_hidden", ctypes.c_int32),
+                ("weight2", ctypes.c_void_p), ("bias2", ctypes.c_void_p)]
 
 
 class Stats(ctypes.Structure):

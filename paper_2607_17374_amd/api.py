@@ -224,7 +224,8 @@ class Layer:
                  in_dtype: int = N.F32, out_dtype: int = N.F32, relu: bool = False, fanout: int = 0,
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
                  hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None,
-                 eviction: str = "pending", attn: Optional[np.ndarray] = None):
+                 eviction: str = "pending", attn: Optional[np.ndarray] = None, d_hidden: int = 0,
+                 weight2: Optional[np.ndarray] = None, bias2: Optional[np.ndarray] = None):
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
@@ -232,6 +233,18 @@ class Layer:
         self._w = np.ascontiguousarray(weight_cat, dtype=np.float32)
         self._b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
         self._a = None if attn is None else np.ascontiguousarray(attn, dtype=np.float32).reshape(2, d_out)
+        self._w2 = None if weight2 is None else np.ascontiguousarray(weight2, dtype=np.float32)
+        self._b2 = None if bias2 is None else np.ascontiguousarray(bias2, dtype=np.float32)
+        # the library reads these host arrays at init with the sizes the
+        # descriptor implies: a short array would be read past its end
+        width = 2 * d_out if agg == N.SAGE_MEAN else d_hidden if agg == N.GIN_MLP else d_out
+        sizes = [(self._w, d_in * width, "weight_cat"), (self._b, width, "bias"),
+                 (self._a, 2 * d_out if agg == N.GAT_ATT else None, "attn"),
+                 (self._w2, d_hidden * d_out if agg == N.GIN_MLP else None, "weight2"),
+                 (self._b2, d_out if agg == N.GIN_MLP else None, "bias2")]
+        for arr, want, name in sizes:
+            if arr is not None and want is not None and arr.size != want:
+                raise ValueError(f"{name} has {arr.size} values; this layer needs {want}")
         self.out = out
         out_ptr, out_on_host = _buf_ptr(out, _TORCH_DTYPE[out_dtype], "out")
         self.n, self.d_in, self.d_out, self.chunk, self.in_dtype = n, d_in, d_out, chunk, in_dtype
@@ -242,7 +255,9 @@ class Layer:
             hub_fraction=hub_fraction, out=out_ptr, out_on_host=out_on_host,
             stream=_stream_ptr(stream), profile=int(profile), plan=plan.handle if plan is not None else None,
             eviction=EVICTION[eviction] if isinstance(eviction, str) else int(eviction),
-            attn=None if self._a is None else self._a.ctypes.data)
+            attn=None if self._a is None else self._a.ctypes.data, d_hidden=d_hidden,
+            weight2=None if self._w2 is None else self._w2.ctypes.data,
+            bias2=None if self._b2 is None else self._b2.ctypes.data)
         self._keep = (row_off, col_dst, plan)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")

@@ -101,11 +101,14 @@ struct PanelLds {
     static constexpr int SF = PIPE_KS * PANEL_NB * 64;  // fragments per stage
     typename GemmOp<DT>::frag b[2][SF];
 };
-template <int DT, int PANEL_NB>
-__device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
-                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
-                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
-                                        PanelLds<DT, PANEL_NB>& lds) {
+// The body with the row mapping and the epilogue as parameters: logical row
+// r of the panel reads row arow(r) of X; for each row r < M the epilogue's
+// row(r) returns a per-row writer w, and w(col, value) stores each product
+// of that row, column col < Nc.
+template <int DT, int PANEL_NB, class ARow, class Epi>
+__device__ __attribute__((always_inline)) inline void gemm_panel_core(const void* __restrict__ X, int64_t M, int K,
+                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc, int bx,
+                                        int by, PanelLds<DT, PANEL_NB>& lds, ARow arow, Epi epi) {
     typedef GemmOp<DT> Op;
     typedef typename Op::frag frag;
     constexpr int SF = PanelLds<DT, PANEL_NB>::SF;
@@ -133,7 +136,7 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_block(const voi
         for (int kk = 0; kk < PIPE_KS; kk++) {
             const int kb = st * PIPE_KS + kk;
             const int k = kb * Op::KBLK + (Op::KBLK / 4) * lk;
-            a[kk] = (kb < KB && row < M && k < K) ? Op::load_a(X, row, K, k) : Op::zero();
+            a[kk] = (kb < KB && row < M && k < K) ? Op::load_a(X, arow(row), K, k) : Op::zero();
         }
     };
     floatx4 acc[PANEL_NB];
@@ -173,13 +176,34 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_block(const voi
     for (int r = 0; r < 4; r++) {
         const int64_t orow = rbase + r;
         if (orow >= M) continue;
-        const float sc = rscale ? rscale[orow] : 1.0f;
+        auto w = epi.row(orow);
 #pragma unroll
         for (int j = 0; j < PANEL_NB; j++) {
             const int col = (nb0 + j) * 16 + li;
-            if (j < nbs && col < Nc) Y[orow * Nc + col] = acc[j][r] * sc;
+            if (j < nbs && col < Nc) w(col, acc[j][r]);
         }
     }
+}
+
+// Y = X W (rows scaled by rscale when given), rows [64 bx, 64 bx + 64) and
+// column blocks [PANEL_NB by, PANEL_NB by + PANEL_NB)
+struct ScaledRows {
+    const float* rscale;
+    float* Y;
+    int Nc;
+    __device__ inline auto row(int64_t r) const {
+        const float sc = rscale ? rscale[r] : 1.0f;
+        float* y = Y + r * Nc;
+        return [=](int col, float v) { y[col] = v * sc; };
+    }
+};
+template <int DT, int PANEL_NB>
+__device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
+                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
+                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
+                                        PanelLds<DT, PANEL_NB>& lds) {
+    gemm_panel_core<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, bx, by, lds, [](int64_t r) { return r; },
+                                  ScaledRows{rscale, Y, Nc});
 }
 
 }  // namespace taurus

@@ -445,6 +445,11 @@ struct ScatterParams {
     const float* att_t;
     const float* att_m;
     const float* att_s;
+    // GIN with a perceptron (agg TAURUS_GIN_MLP): a completing destination's
+    // hidden row ReLU(acc + b1) replaces its accumulator row and v is
+    // appended to ready_ids for the graduation transform
+    int32_t* ready_ids;
+    unsigned int* ready_count;
 };
 
 struct ChunkUnits {        // this chunk's slice of the short classes and wave units
@@ -598,7 +603,21 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
 #pragma unroll
         for (int j = 0; j < VEC; j++) t[j] = f4_add(a[j], t[j]);
     }
-    if (left == 0) {
+    if (left == 0 && p.agg == TAURUS_GIN_MLP) {
+        float* arow = acc_row(p, v);
+#pragma unroll
+        for (int j = 0; j < VEC; j++) {
+            const int col = (j * G + lane) * 4;
+            if (col < p.d_o) {
+                const float4 b = *reinterpret_cast<const float4*>(p.bias + col);
+                float4 z = f4_add(t[j], b);
+                z.x = fmaxf(z.x, 0.f); z.y = fmaxf(z.y, 0.f);
+                z.z = fmaxf(z.z, 0.f); z.w = fmaxf(z.w, 0.f);
+                *reinterpret_cast<float4*>(arow + col) = z;
+            }
+        }
+        if (lane == 0) p.ready_ids[atomicAdd(p.ready_count, 1u)] = v;
+    } else if (left == 0) {
         const float phi = p.agg == 1 ? 1.0f / sqrtf((float)pe.y) : 1.0f;
 #pragma unroll
         for (int j = 0; j < VEC; j++) {
@@ -1172,6 +1191,53 @@ static void dispatch_fixup(const ScatterShape& sh, const ScatterParams& p, const
     fail(TAURUS_E_INVALID, "unsupported row shape G=%d VEC=%d", sh.G, sh.VEC);
 }
 
+// ---------------------------------------------- graduation transform (GIN) --
+// A GIN layer with a perceptron apply leaves each completed destination's
+// hidden row t_v = ReLU(acc_v + b1) in its accumulator row and its ID in
+// the chunk's ready list.  After the chunk's flushes, the ready rows take the
+// perceptron's second layer on the matrix cores: out[v] = act(t_v W2 + b2),
+// written in the output type (Sec. 3.6 transforms graduated vertices in
+// batches).  The workgroups stride over the row panels of however many rows
+// the chunk made ready (read from device memory), so the launch needs no
+// count from the host.
+
+__device__ inline void store_out1(void* out, int dtype, int64_t idx, float z) {
+    if (dtype == 0) static_cast<float*>(out)[idx] = z;
+    else static_cast<uint16_t*>(out)[idx] = (uint16_t)(dtype == 1 ? f32_to_bf16_bits(z) : f32_to_f16_bits(z));
+}
+
+struct GradRows {
+    const int32_t* ids;
+    const float* b2;
+    void* out;
+    int d_out, dtype, relu;
+    __device__ inline auto row(int64_t r) const {
+        const int64_t base = (int64_t)ids[r] * d_out;
+        return [=](int col, float x) {
+            float z = x + (b2 ? b2[col] : 0.0f);
+            if (relu) z = fmaxf(z, 0.0f);
+            store_out1(out, dtype, base + col, z);
+        };
+    }
+};
+
+constexpr int GRAD_NB = 8;   // 16-column blocks per workgroup (128 columns)
+
+__global__ __launch_bounds__(256) void k_graduate(const float* __restrict__ hidden, int d_h,
+                                                  const float4* __restrict__ w2p, int nbp, int d_out,
+                                                  const int32_t* __restrict__ ids,
+                                                  const unsigned int* __restrict__ count,
+                                                  const float* __restrict__ b2, void* out, int dtype, int relu) {
+    __shared__ PanelLds<TAURUS_F32, GRAD_NB> lds;
+    const int64_t M = *count;
+    const int64_t ngy = (nbp + GRAD_NB - 1) / GRAD_NB;
+    const int64_t tiles = (M + PANEL_ROWS - 1) / PANEL_ROWS * ngy;
+    const GradRows epi{ids, b2, out, d_out, dtype, relu};
+    for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x)  // uniform over the workgroup
+        gemm_panel_core<TAURUS_F32, GRAD_NB>(hidden, M, d_h, w2p, nbp, d_out, (int)(t / ngy), (int)(t % ngy), lds,
+                                             [=](int64_t r) { return (int64_t)ids[r]; }, epi);
+}
+
 // ------------------------------------------------------------- chunk index --
 
 // The structures a layer streams over, fixed by (graph, chunk size, edge
@@ -1615,6 +1681,13 @@ struct taurus_layer {
     float* gat_carry = nullptr;  // GAT: per hub piece {max, sum}
     const float* gat_attn = nullptr;  // GAT: a_src then a_dst on the device
     bool gat_done = false;       // GAT: passes 2 and 3 have run
+    // GIN with a perceptron: the second layer (packed for the matrix cores)
+    // and its bias, the chunk's ready list and its length
+    float* w2pack = nullptr;
+    float* bias2 = nullptr;
+    int32_t* ready_ids = nullptr;
+    unsigned int* ready_count = nullptr;
+    int grad_blocks = 0;
     void* wpack_any = nullptr;  // packed weights (fp32 or 16-bit fragments)
     void* out_dev = nullptr;    // desc.out as kernels address it
     std::unique_ptr<taurus::Residency> res;  // accumulator pool under a budget (null: dense rows)
@@ -1681,8 +1754,14 @@ namespace taurus {
 static void validate_desc(const taurus_layer_desc* d) {
     if (!d) fail(TAURUS_E_INVALID, "null descriptor");
     if (d->agg != TAURUS_SAGE_MEAN && d->agg != TAURUS_GCN_SYM && d->agg != TAURUS_GIN_SUM &&
-        d->agg != TAURUS_GAT_ATT)
+        d->agg != TAURUS_GAT_ATT && d->agg != TAURUS_GIN_MLP)
         fail(TAURUS_E_INVALID, "unknown agg %d", d->agg);
+    if (d->agg == TAURUS_GIN_MLP) {
+        if (d->d_hidden <= 0 || d->d_hidden % 4 || d->d_hidden > 1024)
+            fail(TAURUS_E_INVALID, "d_hidden=%d: a positive multiple of 4, at most 1024", d->d_hidden);
+        if (!d->weight2) fail(TAURUS_E_INVALID, "a GIN perceptron layer needs weight2");
+        if (d->hbm_budget != 0) fail(TAURUS_E_INVALID, "GIN perceptron layers run in core (hbm_budget 0)");
+    }
     if (d->agg == TAURUS_GAT_ATT && !d->attn) fail(TAURUS_E_INVALID, "a GAT layer needs its attention vectors");
     if (d->agg == TAURUS_GAT_ATT && d->hbm_budget != 0)
         fail(TAURUS_E_INVALID, "GAT layers run in core (hbm_budget must be 0)");
@@ -1720,10 +1799,11 @@ static void layer_init(taurus_layer* L) {
     L->n = n;
     L->C = C;
     L->nchunks = ceil_div(n, C);
-    L->d_o = d.d_out;
+    // accumulator width: the perceptron's hidden width for GIN_MLP
+    L->d_o = d.agg == TAURUS_GIN_MLP ? d.d_hidden : d.d_out;
     // GraphSAGE: [W_agg | W_self]; GAT: W and the two attention columns,
     // padded to a multiple of 4
-    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.agg == TAURUS_GAT_ATT ? d.d_out + 4 : d.d_out;
+    L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.agg == TAURUS_GAT_ATT ? d.d_out + 4 : L->d_o;
     L->shape = scatter_shape(L->d_o);
     L->shape.max_blocks = scatter_resident_blocks(L->shape, false);
     L->shape.max_blocks_att = scatter_resident_blocks(L->shape, true);
@@ -1742,7 +1822,7 @@ static void layer_init(taurus_layer* L) {
     // of their own.
     std::unique_ptr<Arena> scratch;
     if (d.hbm_budget == 0) {
-        const int64_t acc_elems = n * (int64_t)d.d_out;
+        const int64_t acc_elems = n * (int64_t)L->d_o;
         L->acc = L->arena.alloc<float>(acc_elems, "accumulators");
         scratch = std::make_unique<Arena>(s, L->acc, acc_elems * 4, true);
     }
@@ -1829,17 +1909,31 @@ static void layer_init(taurus_layer* L) {
     wbytes = (wbytes + 255) / 256 * 256;
     // bias, then (GAT) the attention vectors a_src, a_dst
     const int nattn = d.agg == TAURUS_GAT_ATT ? 2 * L->d_o : 0;
-    const size_t pbytes = wbytes + (size_t)(L->d_o + nattn) * 4;
+    // GIN with a perceptron: its second layer (fp32, packed) and bias after
+    std::vector<float> packed2;
+    if (d.agg == TAURUS_GIN_MLP) gemm_pack_weights_f32(d.weight2, d.d_hidden, d.d_out, packed2);
+    const size_t w2off = (wbytes + (size_t)(L->d_o + nattn) * 4 + 255) / 256 * 256;
+    const size_t pbytes = packed2.empty() ? wbytes + (size_t)(L->d_o + nattn) * 4
+                                          : w2off + packed2.size() * 4 + (size_t)d.d_out * 4;
     char* stage = static_cast<char*>(pinned_staging(pbytes));
     if (!packed32.empty()) std::memcpy(stage, packed32.data(), packed32.size() * 4);
     if (!packed16.empty()) std::memcpy(stage, packed16.data(), packed16.size() * 2);
     float* sbias = reinterpret_cast<float*>(stage + wbytes);
     for (int j = 0; j < L->d_o; j++) sbias[j] = d.bias ? d.bias[j] : 0.0f;
     for (int j = 0; j < nattn; j++) sbias[L->d_o + j] = d.attn[j];
+    if (!packed2.empty()) {
+        std::memcpy(stage + w2off, packed2.data(), packed2.size() * 4);
+        float* sb2 = reinterpret_cast<float*>(stage + w2off + packed2.size() * 4);
+        for (int j = 0; j < d.d_out; j++) sb2[j] = d.bias2 ? d.bias2[j] : 0.0f;
+    }
     L->wpack_any = L->arena.alloc_bytes((int64_t)pbytes, "packed weights and bias");
     L->wpack = static_cast<float*>(L->wpack_any);
     L->bias = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + wbytes);
     if (nattn) L->gat_attn = L->bias + L->d_o;
+    if (!packed2.empty()) {
+        L->w2pack = reinterpret_cast<float*>(static_cast<char*>(L->wpack_any) + w2off);
+        L->bias2 = L->w2pack + packed2.size();
+    }
     TAURUS_HIP(hipMemcpyAsync(L->wpack_any, stage, pbytes, hipMemcpyHostToDevice, s));
     pinned_staging_in_flight(s);
 
@@ -1903,7 +1997,29 @@ static void layer_init(taurus_layer* L) {
             fail(TAURUS_E_BUDGET, "residency structures take %lld bytes, above the budget %lld", (long long)total,
                  (long long)d.hbm_budget);
     }
-    L->fuse_fix = !L->res && !L->gat_hp && d.in_dtype == TAURUS_F32;
+    if (d.agg == TAURUS_GIN_MLP) {
+        // ready list: a push completes at most the destinations it touches
+        // (its own rows and one per list entry)
+        int64_t max_dc = 0;
+        for (int64_t k = 0; k < L->nchunks; k++) {
+            int64_t t = std::min(C, n - k * C);
+            for (int l = 0; l < NLIST; l++) t += idx.list_count(l, k);
+            max_dc = std::max(max_dc, t);
+        }
+        max_dc = std::min(max_dc, n);
+        L->ready_ids = L->arena.alloc<int32_t>(max_dc, "ready list");
+        L->ready_count = L->arena.alloc<unsigned int>(1, "ready count");
+        fill_i32(reinterpret_cast<int32_t*>(L->ready_count), 1, 0, s);
+        int dev = 0, cus = 0;
+        TAURUS_HIP(hipGetDevice(&dev));
+        TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        const int64_t ngy = ceil_div(gemm_packed_blocks_n(d.d_out), GRAD_NB);
+        L->grad_blocks = (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(max_dc, PANEL_ROWS) * ngy,
+                                                                     2 * (int64_t)std::max(1, cus)));
+    }
+    // the perceptron's graduation reads every flush of the chunk, the
+    // fix-up's included, so its fix-up is not deferred
+    L->fuse_fix = !L->res && !L->gat_hp && d.in_dtype == TAURUS_F32 && d.agg != TAURUS_GIN_MLP;
     if (d.profile) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
@@ -2068,6 +2184,8 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.long_base = idx.list_off[NCLASS][(size_t)k];
     p.first_row = b;
     p.rows = e - b;
+    p.ready_ids = L->ready_ids;
+    p.ready_count = L->ready_count;
     ChunkUnits cu;
     for (int l = 0; l <= NCLASS; l++) {
         cu.u[l] = idx.list_at(l, k);
@@ -2083,6 +2201,15 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
         L->fix_pending = true;
     } else if (nfix > 0) {
         dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
+    }
+    if (L->ready_ids) {
+        k_graduate<<<(unsigned)L->grad_blocks, 256, 0, s>>>(L->acc, L->d_o,
+                                                             reinterpret_cast<const float4*>(L->w2pack),
+                                                             gemm_packed_blocks_n(L->d.d_out), L->d.d_out,
+                                                             L->ready_ids, L->ready_count, L->bias2, L->out_dev,
+                                                             L->d.out_dtype, L->d.relu);
+        TAURUS_CHECK_LAUNCH();
+        fill_i32(reinterpret_cast<int32_t*>(L->ready_count), 1, 0, s);
     }
     if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
     if (L->res) L->res->release(rc, L->cnt, s);

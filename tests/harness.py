@@ -41,10 +41,13 @@ def layer_specs(w: WL.Workload, fanouts=None):
     for li in range(1, w.layers + 1):
         p = WL.layer_params(w, li)
         in_dt, out_dt = w.layer_dtypes(li)
+        extra = {}
+        if w.agg == WL.GIN_MLP:   # the perceptron's second layer, row-major [d_hidden][d_out]
+            extra = dict(d_hidden=p.d_out, weight2=np.ascontiguousarray(p.W2.T, np.float32), bias2=p.b2)
         specs.append(dict(agg=w.agg, d_in=p.d_in, d_out=p.d_out, weight_cat=p.weight_cat(), bias=p.b,
                           in_dtype=in_dt, out_dtype=out_dt, relu=li < w.layers,
                           fanout=(fanouts[li - 1] if fanouts else w.fanout(li)), layer=li, seed=w.seed,
-                          attn=p.attn))
+                          attn=p.attn, **extra))
     return specs
 
 
@@ -53,6 +56,8 @@ def oracle_layer(w: WL.Workload, p, g, H, h_dtype, relu, keep_in=None, dst_ids=N
     import oracle as O
     if w.agg == WL.GAT_ATT:
         return O.gat_layer(g, H, h_dtype, p.W, p.attn, p.b, relu, keep_in=keep_in, dst_ids=dst_ids)
+    if w.agg == WL.GIN_MLP:
+        return O.gin_mlp_layer(g, H, h_dtype, p.W, p.b, p.W2, p.b2, relu, keep_in=keep_in, dst_ids=dst_ids)
     return O.layer(w.agg, g, H, h_dtype, p.W, p.b, relu, keep_in=keep_in, dst_ids=dst_ids)
 
 
