@@ -141,9 +141,36 @@ def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int, sage: bool) -> dict
 
 
 # ---------------------------------------------------------------- profiles --
-PROFILE = os.path.join(ROOT, "profiles", "k_scatter_gcn2-rmat-1m.md")
+PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "layer.hip")
 GIB_KIB = float(1 << 20)
+WORKLOADS = ("sage3-fanout-rmat-100m", "gcn2-rmat-1m")
+
+
+def profile_path(workload: str) -> str:
+    return os.path.join(PROFILE_DIR, f"k_scatter_{workload}.md")
+
+
+def profile_commands(workload: str) -> list:
+    """The commands whose output a workload's profile summary digests, run
+    from the repository root (counter runs profile the scatter, the
+    transform and the calibration copy only)."""
+    tag = "c3" if workload == WORKLOADS[0] else "c2"
+    base = "python3 bench.py" + ("" if workload == WORKLOADS[0] else f" --workload {workload}")
+    timed = " --steps 3 --warmup 1" if workload == WORKLOADS[0] else " --steps 10 --warmup 2"
+    once = " --steps 1 --warmup 0 --no-cpu-baseline --no-profile --copy-calibration"
+    sel = '--kernel-include-regex "k_scatter|k_gemm_panel|k_transform_fixup|neg"'
+    mfma = ("SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES "
+            "SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE")
+    return [
+        f"rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_{tag} -o {tag} -- "
+        f"{base}{timed} --no-cpu-baseline",
+        f"rocprofv3 --pmc FETCH_SIZE {sel} --output-format csv -d gpurun_out/pmc_fetch_{tag} -o p -- {base}{once}",
+        f"rocprofv3 --pmc WRITE_SIZE {sel} --output-format csv -d gpurun_out/pmc_write_{tag} -o p -- {base}{once}",
+        f"rocprofv3 --pmc {mfma} {sel} --output-format csv -d gpurun_out/pmc_mfma_{tag} -o p -- {base}{once}",
+        f"python3 bench.py --summarize-profile {workload} gpurun_out/prof_{tag} gpurun_out/pmc_fetch_{tag} "
+        f"gpurun_out/pmc_write_{tag} gpurun_out/pmc_mfma_{tag}",
+    ]
 
 
 # the scatter kernels and their launch dispatch: the part of KERNEL_SOURCE
@@ -166,15 +193,16 @@ def source_digest() -> str:
     return h.hexdigest()
 
 
-def profiled_traffic():
-    """HBM bytes per k_scatter launch from the committed counter summary, or
-    None when there is none or the kernel source changed since it was taken."""
+def profiled_traffic(workload: str):
+    """HBM bytes per k_scatter launch from the workload's committed counter
+    summary, or None when there is none or the kernel source changed since
+    it was taken."""
     try:
-        text = open(PROFILE).read()
+        text = open(profile_path(workload)).read()
     except OSError:
         return None
     vals = dict(line.strip().split(": ", 1) for line in text.splitlines()
-                if line.startswith("    ") and ": " in line)
+                if line.startswith("    ") and ": " in line and not line.strip().startswith(("rocprofv3", "python3")))
     if vals.get("source_sha256") != source_digest():
         return None
     try:
@@ -203,26 +231,34 @@ def _counter_means(d: str, counter: str) -> dict:
     return {k: (n, t / n) for k, (n, t) in acc.items()}
 
 
-def summarize_profile(trace_dir: str, fetch_dir: str, write_dir: str) -> str:
+def _pick(d: dict, pred):
+    """(dispatches, dispatch-weighted mean) over the kernels whose name passes pred."""
+    ks = [k for k in d if pred(k)]
+    n = sum(d[k][0] for k in ks)
+    return n, (sum(d[k][0] * d[k][1] for k in ks) / n if n else float("nan"))
+
+
+WORKLOAD_TITLE = {
+    WORKLOADS[0]: "sage3-fanout-rmat-100m (3-layer GraphSAGE-mean 128->256->256->172, fanouts (15, 10, 5), "
+                  "RMAT 100M vertices / 1.6B edges, bf16 features, 65,536-vertex chunks)",
+    WORKLOADS[1]: "gcn2-rmat-1m (2-layer GCN 128->128->64, RMAT 1M vertices / 20M edges, fp32, "
+                  "65,536-vertex chunks)",
+}
+
+
+def summarize_profile(workload: str, trace_dir: str, fetch_dir: str, write_dir: str, mfma_dir: str = None) -> str:
     import csv
     import glob
     stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
     if not stats:
         raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
     rows = list(csv.DictReader(open(stats[0])))
-    out = ["# k_scatter on gcn2-rmat-1m (2-layer GCN 128->128->64, RMAT 1M vertices / 20M edges, "
-           "65,536-vertex chunks)", "",
-           "Commands, from the repository root on one MI355X:", "",
-           "    rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_gcn -o gcn -- "
-           "python3 bench.py --steps 10 --warmup 2 --no-cpu-baseline",
-           "    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o p -- "
-           "python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --no-profile --copy-calibration",
-           "    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o p -- "
-           "python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --no-profile --copy-calibration",
-           "    python3 bench.py --summarize-profile gpurun_out/prof_gcn gpurun_out/pmc_fetch gpurun_out/pmc_write",
-           "", "## Kernel time (--kernel-trace --stats, 12 steps)", "",
-           "| kernel | calls | total ms | average us | % |", "|---|---|---|---|---|"]
-    for r in rows[:16]:
+    out = [f"# k_scatter on {WORKLOAD_TITLE[workload]}", "",
+           "Commands, from the repository root on one MI355X (counter runs one at a time):", ""]
+    out += ["    " + c for c in profile_commands(workload)]
+    out += ["", "## Kernel time (--kernel-trace --stats, every pass of the run)", "",
+            "| kernel | calls | total ms | average us | % |", "|---|---|---|---|---|"]
+    for r in rows[:20]:
         out.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
     sc = [r for r in rows if "k_scatter<" in r["Name"]]
@@ -230,25 +266,42 @@ def summarize_profile(trace_dir: str, fetch_dir: str, write_dir: str) -> str:
     tot_ns = sum(float(r["TotalDurationNs"]) for r in sc)
     fetch = _counter_means(fetch_dir, "FETCH_SIZE")
     write = _counter_means(write_dir, "WRITE_SIZE")
-
-    def pick(d, pred):
-        ks = [k for k in d if pred(k)]
-        n = sum(d[k][0] for k in ks)
-        return n, (sum(d[k][0] * d[k][1] for k in ks) / n if n else float("nan"))
-
-    _, f_cal = pick(fetch, lambda k: "neg_kernel" in k)
-    _, w_cal = pick(write, lambda k: "neg_kernel" in k)
-    nf, f_sc = pick(fetch, lambda k: "k_scatter<" in k)
-    nw, w_sc = pick(write, lambda k: "k_scatter<" in k)
+    _, f_cal = _pick(fetch, lambda k: "neg_kernel" in k)
+    _, w_cal = _pick(write, lambda k: "neg_kernel" in k)
+    nf, f_sc = _pick(fetch, lambda k: "k_scatter<" in k)
+    nw, w_sc = _pick(write, lambda k: "k_scatter<" in k)
     ff, fw = GIB_KIB / f_cal, GIB_KIB / w_cal
     traffic = (f_sc * ff + w_sc * fw) * 1024.0
-    out += ["", "## HBM traffic of k_scatter (--pmc, one counter per run)", "",
+    out += ["", "## HBM traffic (--pmc, one counter per run)", "",
             f"Calibration: torch neg over 1 GiB (1,048,576 KiB read and written) reads FETCH_SIZE "
             f"{f_cal:.0f} KiB and WRITE_SIZE {w_cal:.0f} KiB per dispatch, so the factors are "
             f"{ff:.3f} (fetch) and {fw:.3f} (write).", "",
-            f"k_scatter, mean over {nf} / {nw} dispatches (both layers): FETCH_SIZE {f_sc:.0f} KiB, "
-            f"WRITE_SIZE {w_sc:.0f} KiB per dispatch; scaled: {traffic / 1e6:.1f} MB per launch.", "",
-            "Machine-readable (bench.py reports traffic only while the kernel source digest matches):", "",
+            f"k_scatter, mean over {nf} / {nw} dispatches (all layers): FETCH_SIZE {f_sc:.0f} KiB, "
+            f"WRITE_SIZE {w_sc:.0f} KiB per dispatch; scaled: {traffic / 1e6:.1f} MB per launch."]
+    gemm_pred = lambda k: "k_gemm_panel" in k or "k_transform_fixup" in k
+    ng, f_g = _pick(fetch, gemm_pred)
+    _, w_g = _pick(write, gemm_pred)
+    if ng:
+        out += ["", f"Transform (k_gemm_panel / k_transform_fixup), mean over {ng} dispatches: FETCH_SIZE "
+                    f"{f_g:.0f} KiB, WRITE_SIZE {w_g:.0f} KiB per dispatch; scaled: "
+                    f"{(f_g * ff + w_g * fw) * 1024.0 / 1e6:.1f} MB per launch."]
+    if mfma_dir:
+        gt = [r for r in rows if gemm_pred(r["Name"])]
+        g_calls = sum(int(r["Calls"]) for r in gt)
+        g_us = sum(float(r["TotalDurationNs"]) for r in gt) / max(g_calls, 1) / 1e3
+        mops = {c: _pick(_counter_means(mfma_dir, c), gemm_pred) for c in
+                ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_VALU_MFMA_BUSY_CYCLES",
+                 "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE")}
+        flops = 512.0 * sum(v[1] for k, v in mops.items() if "MOPS" in k and v[0])
+        busy, cu_busy = mops["SQ_VALU_MFMA_BUSY_CYCLES"][1], mops["SQ_BUSY_CU_CYCLES"][1]
+        out += ["", "## Matrix cores in the transform (--pmc)", "",
+                f"Mean per dispatch over {mops['SQ_INSTS_VALU_MFMA_MOPS_BF16'][0]} dispatches:",
+                "", "| counter | mean per dispatch |", "|---|---|"]
+        out += [f"| {k} | {v[1]:.4g} |" for k, v in mops.items()]
+        out += ["", f"MFMA work from the counters: 512 x MOPS = {flops / 1e9:.3f} GFLOP per dispatch; over the "
+                    f"traced mean duration {g_us:.2f} us that is {flops / (g_us * 1e-6) / 1e12:.1f} TFLOP/s.  "
+                    f"Matrix-core busy cycles over CU busy cycles: {busy / cu_busy:.3f}."]
+    out += ["", "Machine-readable (bench.py reports traffic only while the kernel source digest matches):", "",
             "    kernel: k_scatter",
             f"    launches: {calls}",
             f"    avg_launch_us: {tot_ns / max(calls, 1) / 1e3:.2f}",
@@ -264,8 +317,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default 3, or 10 for gcn2-rmat-1m)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 1, or 2 for gcn2-rmat-1m)")
-    ap.add_argument("--workload", choices=["sage3-fanout-rmat-100m", "gcn2-rmat-1m"],
-                    default="sage3-fanout-rmat-100m")
+    ap.add_argument("--workload", choices=WORKLOADS, default=WORKLOADS[0])
     ap.add_argument("--scale", type=int, default=1,
                     help="sage3-fanout-rmat-100m only: divide vertices and edges by this (trial runs; not a result)")
     ap.add_argument("--chunk", type=int, default=0,
@@ -278,10 +330,13 @@ def main():
                     help="first run a plain 1 GiB device copy, the reference kernel for HBM byte counters")
     ap.add_argument("--variant", choices=sorted(VARIANTS), default="gcn",
                     help="gcn2-rmat-1m only: model family on the same graph (default: the exact GCN workload)")
-    ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
-                    help="print the profile summary of a kernel-trace run and FETCH_SIZE / WRITE_SIZE runs")
+    ap.add_argument("--summarize-profile", nargs="+", metavar="ARG",
+                    help="WORKLOAD TRACE_DIR FETCH_DIR WRITE_DIR [MFMA_DIR]: print the profile summary of a "
+                         "kernel-trace run and FETCH_SIZE / WRITE_SIZE (and matrix-core counter) runs")
     args = ap.parse_args()
     if args.summarize_profile:
+        if len(args.summarize_profile) not in (4, 5) or args.summarize_profile[0] not in WORKLOADS:
+            raise SystemExit("--summarize-profile WORKLOAD TRACE_DIR FETCH_DIR WRITE_DIR [MFMA_DIR]")
         print(summarize_profile(*args.summarize_profile))
         return
     if args.gpus != 1:
@@ -427,7 +482,7 @@ def bench_rmat_1m(args):
         byt, ms_, nlaunch = tot["scatter"]
         achieved = byt / (ms_ * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(), "kernel": "k_scatter",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic("gcn2-rmat-1m"), "kernel": "k_scatter",
                     "avg_launch_us": round(ms_ * 1e3 / nlaunch, 2), "bytes_per_launch": round(byt / nlaunch, 0),
                     "model_check": model_ok}
     gemm = None
@@ -640,7 +695,9 @@ def bench_sage3_100m(args):
     if profile and sc_ms > 0:
         achieved = sc_bytes / (sc_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_scatter",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None if args.scale > 1 or args.chunk > 0 else profiled_traffic(w.name),
+                    "kernel": "k_scatter",
                     "avg_launch_us": round(sc_ms * 1e3 / sc_launches, 2),
                     "bytes_per_launch": round(sc_bytes / sc_launches, 0)}
 

@@ -237,8 +237,9 @@ class Layer:
         self._b2 = None if bias2 is None else np.ascontiguousarray(bias2, dtype=np.float32)
         # the library reads these host arrays at init with the sizes the
         # descriptor implies: a short array would be read past its end
-        width = 2 * d_out if agg == N.SAGE_MEAN else d_hidden if agg == N.GIN_MLP else d_out
-        sizes = [(self._w, d_in * width, "weight_cat"), (self._b, width, "bias"),
+        hidden = d_hidden if agg == N.GIN_MLP else d_out       # accumulator width
+        width = 2 * d_out if agg == N.SAGE_MEAN else hidden     # transform columns
+        sizes = [(self._w, d_in * width, "weight_cat"), (self._b, hidden, "bias"),
                  (self._a, 2 * d_out if agg == N.GAT_ATT else None, "attn"),
                  (self._w2, d_hidden * d_out if agg == N.GIN_MLP else None, "weight2"),
                  (self._b2, d_out if agg == N.GIN_MLP else None, "bias2")]
