@@ -195,7 +195,9 @@ void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer
                  hipStream_t s);
 // The kept in-edges of the fanout-k sample as chunk-index items, in CSC
 // order (destinations ascending, sources ascending within one): keys
-// (chunk(u) << vbits | v) in sb.keys[0] (from key_arena, with its ping-pong
+// (chunk(u) << (vbits + 1) | nf << vbits | v) in sb.keys[0], nf = 1 when
+// chunk(u) is after the earlier of v's own chunk and the chunk of v's
+// smallest kept source (from key_arena, with its ping-pong
 // buffer sb.keys[1]), values u - chunk(u)*C in sb.vals[0] (from val_arena,
 // with sb.vals[1]).  Also m[v] = min(d_in(v), k) and first_chunk[v] = the
 // chunk of v's smallest kept source (left as it was when none is kept).

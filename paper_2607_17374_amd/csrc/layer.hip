@@ -142,12 +142,13 @@ __global__ void k_mask_word_counts(const uint64_t* __restrict__ mask, int64_t wo
     cnt[w] = (uint32_t)__popcll(m);
 }
 
-// offs[j] = first sorted position whose chunk field is >= j, j in [0, nchunks]
-__global__ void k_chunk_bounds(const uint64_t* __restrict__ keys, int64_t total, int64_t nchunks, int vbits,
+// offs[j] = first sorted position whose chunk field (bits kshift and up) is
+// >= j, j in [0, nchunks]
+__global__ void k_chunk_bounds(const uint64_t* __restrict__ keys, int64_t total, int64_t nchunks, int kshift,
                                int64_t* __restrict__ offs) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (j > nchunks) return;
-    const uint64_t target = (uint64_t)j << vbits;
+    const uint64_t target = (uint64_t)j << kshift;
     int64_t lo = 0, hi = total;
     while (lo < hi) {
         const int64_t mid = lo + ((hi - lo) >> 1);
@@ -240,14 +241,15 @@ __device__ inline int64_t seg_slots(int64_t len, uint32_t v, uint32_t chunk, int
 // a sampled layer)
 template <bool COUNTED>
 __global__ void k_seg_classify(const uint64_t* __restrict__ keys, const int64_t* __restrict__ seg_start, int64_t P,
-                               int vbits, int64_t C, int32_t* __restrict__ m, int32_t* __restrict__ first_chunk,
+                               int vbits, int kshift, int64_t C, int32_t* __restrict__ m,
+                               int32_t* __restrict__ first_chunk,
                                int32_t* __restrict__ slots_of, uint8_t* __restrict__ has_own,
                                unsigned long long* __restrict__ own_count) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= P) return;
     const int64_t b = seg_start[s], len = seg_start[s + 1] - b;
     const uint64_t v = keys[b] & (((uint64_t)1 << vbits) - 1);
-    const uint32_t chunk = (uint32_t)(keys[b] >> vbits);
+    const uint32_t chunk = (uint32_t)(keys[b] >> kshift);
     if (!COUNTED) {
         atomicAdd(&m[v], (int)len);
         atomicMin(&first_chunk[v], (int)chunk);
@@ -272,16 +274,22 @@ struct SegUnit {
     int64_t rel;
     int nf, v, self;
 };
-__device__ inline SegUnit seg_unit(const uint64_t* keys, const int64_t* seg_start, int64_t s, int vbits, int64_t C,
-                                   const int64_t* chunk_off, const int32_t* first_chunk) {
+// Keys are (chunk << kshift | v); with kshift = vbits + 1 (sampled layers)
+// bit vbits says the segment is not v's first flush, otherwise it comes
+// from first_chunk.
+__device__ inline SegUnit seg_unit(const uint64_t* keys, const int64_t* seg_start, int64_t s, int vbits, int kshift,
+                                   int64_t C, const int64_t* chunk_off, const int32_t* first_chunk) {
     const int64_t b = seg_start[s];
     const uint64_t key = keys[b];
     SegUnit u;
     u.v = (int)(key & (((uint64_t)1 << vbits) - 1));
-    const int chunk = (int)(key >> vbits);
+    const int chunk = (int)(key >> kshift);
     u.rel = b - chunk_off[chunk];
     const int own_chunk = (int)((uint32_t)u.v / (uint32_t)C);
-    u.nf = chunk != min(first_chunk[u.v], own_chunk) ? NOT_FIRST : 0;
+    if (kshift > vbits)
+        u.nf = (key >> vbits) & 1 ? NOT_FIRST : 0;
+    else
+        u.nf = chunk != min(first_chunk[u.v], own_chunk) ? NOT_FIRST : 0;
     u.self = own_chunk == chunk ? SELF_HERE : 0;
     return u;
 }
@@ -301,15 +309,15 @@ __device__ inline void seg_entries(int64_t slots, int64_t (&c)[NLIST]) {
     }
 }
 
-// tile_cnt[l * ntiles + t] = entries the segments of tile t add to list l;
-// thread j of a tile takes its segments j * LT_PER .. j * LT_PER + LT_PER - 1
+// tile_cnt[l * ntiles + t] = entries the segments of tile t add to list l
+// (the tile's segments in LT_PER rounds of LT_THREADS consecutive ones)
 __global__ __launch_bounds__(LT_THREADS) void k_list_tile_counts(const int32_t* __restrict__ slots_of, int64_t P,
                                                                 int64_t ntiles, uint64_t* __restrict__ tile_cnt) {
     __shared__ int64_t part[LT_THREADS / 64][NLIST];
     int64_t c[NLIST] = {};
-    const int64_t s0 = (int64_t)blockIdx.x * LT_TILE + (int64_t)threadIdx.x * LT_PER;
+    const int64_t s0 = (int64_t)blockIdx.x * LT_TILE + threadIdx.x;
     for (int j = 0; j < LT_PER; j++)
-        if (s0 + j < P) seg_entries(slots_of[s0 + j], c);
+        if (s0 + j * LT_THREADS < P) seg_entries(slots_of[s0 + j * LT_THREADS], c);
 #pragma unroll
     for (int l = 0; l < NLIST; l++)
         for (int m = 32; m >= 1; m >>= 1) c[l] += __shfl_xor(c[l], m, 64);
@@ -325,72 +333,106 @@ __global__ __launch_bounds__(LT_THREADS) void k_list_tile_counts(const int32_t* 
 
 // Units of tile t's segments, in segment order within each list, from the
 // tile's positions tile_off[l * ntiles + t] (absolute in the work-list
-// buffer).  A segment that starts a chunk also writes, for that chunk and
-// any empty chunks before it, each list's position there:
+// buffer).  The tile is taken in LT_PER rounds of LT_THREADS consecutive
+// segments, one per thread, so reads and each list's writes are
+// contiguous over the threads; a round's positions are a workgroup prefix
+// of the entries its segments add (ballots for the one-entry lists, a scan
+// for the wave pieces).  A segment that starts a chunk also writes, for
+// that chunk and any empty chunks before it, each list's position there:
 // dbases[l * (nchunks + 1) + k]; the last segment writes the list ends for
 // the chunks after it and for k = nchunks.
 __global__ __launch_bounds__(LT_THREADS) void k_list_emit(const uint64_t* __restrict__ keys,
                                                          const int64_t* __restrict__ seg_start,
                                                          const int32_t* __restrict__ slots_of, int64_t P,
                                                          int64_t ntiles, const uint64_t* __restrict__ tile_off,
-                                                         int vbits, int64_t C, const int64_t* __restrict__ chunk_off,
+                                                         int vbits, int kshift, int64_t C,
+                                                         const int64_t* __restrict__ chunk_off,
                                                          const int32_t* __restrict__ first_chunk, int64_t nchunks,
                                                          int4* __restrict__ units, int64_t* __restrict__ dbases) {
-    __shared__ int64_t wsum[LT_THREADS / 64][NLIST];
+    constexpr int NW = LT_THREADS / 64;
+    __shared__ int64_t wsum[2][NW][NLIST];   // per round parity: entries of each wave
+    __shared__ int64_t run[NLIST];           // list positions before the current round
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int64_t s0 = (int64_t)blockIdx.x * LT_TILE + (int64_t)threadIdx.x * LT_PER;
-    int64_t c[NLIST] = {};
-    for (int j = 0; j < LT_PER; j++)
-        if (s0 + j < P) seg_entries(slots_of[s0 + j], c);
-    // exclusive prefix of c over the block's threads, per list
-    int64_t base[NLIST];
+    const uint64_t lt = (1ull << lane) - 1ull;
+    if (threadIdx.x < NLIST) run[threadIdx.x] = (int64_t)tile_off[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    const int64_t t0 = (int64_t)blockIdx.x * LT_TILE;
+    for (int r = 0; r < LT_PER; r++) {
+        const int64_t sg = t0 + (int64_t)r * LT_THREADS + threadIdx.x;
+        if (t0 + (int64_t)r * LT_THREADS >= P) break;  // uniform over the workgroup
+        const int par = r & 1;
+        const bool here = sg < P;
+        const int64_t slots = here ? slots_of[sg] : 0;
+        const int cls = here ? seg_class(slots) : -1;
+        const int64_t pieces = cls == NCLASS ? (slots + PIECE_LEN - 1) / PIECE_LEN : 0;
+        // this thread's entries before it in the wave, per list
+        int64_t pre[NLIST];
 #pragma unroll
-    for (int l = 0; l < NLIST; l++) {
-        int64_t x = c[l];
-        for (int m = 1; m < 64; m <<= 1) {
-            const int64_t y = __shfl_up(x, m, 64);
-            if (lane >= m) x += y;
+        for (int l = 0; l < NCLASS; l++) {
+            const uint64_t bal = __ballot(cls == l);
+            pre[l] = __popcll(bal & lt);
+            if (lane == 0) wsum[par][w][l] = __popcll(bal);
         }
-        base[l] = x - c[l];
-        if (lane == 63) wsum[w][l] = x;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int l = 0; l < NLIST; l++) {
-        int64_t before = (int64_t)tile_off[(int64_t)l * ntiles + blockIdx.x];
-        for (int q = 0; q < w; q++) before += wsum[q][l];
-        base[l] += before;
-    }
-    if (s0 >= P) return;
-    int64_t prev = s0 == 0 ? -1 : (int64_t)(keys[seg_start[s0 - 1]] >> vbits);
-    for (int j = 0; j < LT_PER && s0 + j < P; j++) {
-        const int64_t sg = s0 + j;
-        const int64_t b = seg_start[sg];
-        const int64_t chunk = (int64_t)(keys[b] >> vbits);
-        for (int64_t k = prev + 1; k <= chunk; k++)
-            for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = base[l];
-        prev = chunk;
-        const SegUnit u = seg_unit(keys, seg_start, sg, vbits, C, chunk_off, first_chunk);
-        const int64_t slots = slots_of[sg];
-        const int cls = seg_class(slots);
-        if (cls < NCLASS) {
-            units[base[cls]++] = make_int4((int)u.rel, (int)slots | u.nf | u.self, u.v, 0);
-        } else {
-            const int pieces = (int)((slots + PIECE_LEN - 1) / PIECE_LEN);
-            const int64_t first = base[NCLASS];
-            for (int q = 0; q < pieces; q++) {
-                const int64_t o = (int64_t)q * PIECE_LEN;
-                const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
-                const int self = q == pieces - 1 ? u.self : 0;
-                units[first + q] = make_int4((int)(u.rel + o), plen | u.nf | self, u.v, pieces > 1 ? (int)(first + q) : -1);
+        {
+            const uint64_t bal = __ballot(pieces > 1);
+            pre[NCLASS + 1] = __popcll(bal & lt);
+            if (lane == 0) wsum[par][w][NCLASS + 1] = __popcll(bal);
+        }
+        int64_t x = pieces;
+        if (__ballot(pieces > 0)) {  // uniform over the wave
+            for (int m = 1; m < 64; m <<= 1) {
+                const int64_t y = __shfl_up(x, m, 64);
+                if (lane >= m) x += y;
             }
-            base[NCLASS] += pieces;
-            if (pieces > 1) units[base[NCLASS + 1]++] = make_int4(u.v, (int)first, pieces, 0);
         }
-    }
-    if (s0 + LT_PER >= P) {  // the thread holding the last segment
-        for (int64_t k = prev + 1; k <= nchunks; k++)
-            for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = base[l];
+        pre[NCLASS] = x - pieces;
+        if (lane == 63) wsum[par][w][NCLASS] = x;
+        __syncthreads();
+#pragma unroll
+        for (int l = 0; l < NLIST; l++) {
+            int64_t before = run[l];
+            for (int q = 0; q < w; q++) before += wsum[par][q][l];
+            pre[l] += before;
+        }
+        if (here) {
+            const int64_t b = seg_start[sg];
+            const int64_t chunk = (int64_t)(keys[b] >> kshift);
+            const int64_t prev = sg == 0 ? -1 : (int64_t)(keys[seg_start[sg - 1]] >> kshift);
+            for (int64_t k = prev + 1; k <= chunk; k++)
+                for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = pre[l];
+            const SegUnit u = seg_unit(keys, seg_start, sg, vbits, kshift, C, chunk_off, first_chunk);
+            if (cls < NCLASS) {
+                units[pre[cls]] = make_int4((int)u.rel, (int)slots | u.nf | u.self, u.v, 0);
+            } else {
+                const int64_t first = pre[NCLASS];
+                for (int q = 0; q < (int)pieces; q++) {
+                    const int64_t o = (int64_t)q * PIECE_LEN;
+                    const int plen = (int)min((int64_t)PIECE_LEN, slots - o);
+                    const int self = q == pieces - 1 ? u.self : 0;
+                    units[first + q] =
+                        make_int4((int)(u.rel + o), plen | u.nf | self, u.v, pieces > 1 ? (int)(first + q) : -1);
+                }
+                if (pieces > 1) units[pre[NCLASS + 1]] = make_int4(u.v, (int)first, (int)pieces, 0);
+            }
+            if (sg == P - 1) {  // list ends for the chunks after the last segment's
+                int64_t end[NLIST];
+                for (int l = 0; l < NLIST; l++) end[l] = pre[l];
+                if (cls < NCLASS) end[cls] += 1;
+                else {
+                    end[NCLASS] += pieces;
+                    end[NCLASS + 1] += pieces > 1 ? 1 : 0;
+                }
+                for (int64_t k = chunk + 1; k <= nchunks; k++)
+                    for (int l = 0; l < NLIST; l++) dbases[(int64_t)l * (nchunks + 1) + k] = end[l];
+            }
+        }
+        // every thread has read run: add the round's totals (wsum[par] is
+        // next written two rounds on, after the next round's barriers)
+        __syncthreads();
+        if (threadIdx.x < NLIST) {
+            int64_t t = 0;
+            for (int q = 0; q < NW; q++) t += wsum[par][q][threadIdx.x];
+            run[threadIdx.x] += t;
+        }
     }
 }
 
@@ -1352,7 +1394,9 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     // any kernel indexes by destination.
     const int vbits = std::max(1, bits_for(n - 1));
     const int cbits = bits_for(nch - 1);  // chunk numbers 0 .. nch - 1
-    if (vbits + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
+    // the sampler's keys carry the not-first-flush bit between the fields
+    const int kshift = sample ? vbits + 1 : vbits;
+    if (kshift + cbits > 64) fail(TAURUS_E_INVALID, "index key does not fit 64 bits");
     SortBuffers sb{{nullptr, nullptr}, {nullptr, nullptr}, 0};
     int64_t items = e;
     int32_t* first_chunk = tmp.alloc<int32_t>(n, "first chunk per vertex");
@@ -1363,7 +1407,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         // by (chunk, destination, source)
         items = sample_items(*sample->csc, n, sample->seed, sample->layer, sample->k, C, vbits, tmp, idx->arena, sb,
                              idx->m, first_chunk, bad, s);
-        radix_sort_u64(sb, items, cbits, tmp, s, bad, 8, nullptr, vbits);
+        radix_sort_u64(sb, items, cbits, tmp, s, bad, 8, nullptr, kshift);
     } else {
         sb.keys[0] = tmp.alloc<uint64_t>(e, "index keys");
         sb.keys[1] = tmp.alloc<uint64_t>(e, "index keys (ping-pong)");
@@ -1381,7 +1425,7 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     tmp.free_ptr(sb.keys[1 - sb.cur]);
     idx->arena.free_ptr(sb.vals[1 - sb.cur]);
     int64_t* doffs = tmp.alloc<int64_t>(nch + 1, "chunk offsets");
-    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, items, nch, vbits, doffs);
+    k_chunk_bounds<<<(unsigned)ceil_div(nch + 1, T), T, 0, s>>>(keys, items, nch, kshift, doffs);
     TAURUS_CHECK_LAUNCH();
     const int64_t nbt = ceil_div(items1, HEAD_TILE);
     uint64_t* hcount = tmp.alloc<uint64_t>(nbt, "segment heads per tile");
@@ -1419,10 +1463,11 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     tmp.free_ptr(hcount);
     int32_t* slots_of = tmp.alloc<int32_t>(P, "segment slots");
     if (sample)
-        k_seg_classify<true><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m, first_chunk,
-                                                                    slots_of, idx->has_own, idx->own_count);
+        k_seg_classify<true><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, kshift, C, idx->m,
+                                                                    first_chunk, slots_of, idx->has_own,
+                                                                    idx->own_count);
     else
-        k_seg_classify<false><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, C, idx->m,
+        k_seg_classify<false><<<(unsigned)ceil_div(P, T), T, 0, s>>>(keys, seg_start, P, vbits, kshift, C, idx->m,
                                                                      first_chunk, slots_of, idx->has_own,
                                                                      idx->own_count);
     TAURUS_CHECK_LAUNCH();
@@ -1451,8 +1496,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
     if (total_units >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "too many work units");
     idx->units = idx->arena.alloc<int4>(std::max<int64_t>(1, total_units), "work lists");
     int64_t* dbases = tmp.alloc<int64_t>((nch + 1) * NLIST, "chunk list positions");
-    k_list_emit<<<(unsigned)ntiles, LT_THREADS, 0, s>>>(keys, seg_start, slots_of, P, ntiles, tile_off, vbits, C,
-                                                       doffs, first_chunk, nch, idx->units, dbases);
+    k_list_emit<<<(unsigned)ntiles, LT_THREADS, 0, s>>>(keys, seg_start, slots_of, P, ntiles, tile_off, vbits,
+                                                       kshift, C, doffs, first_chunk, nch, idx->units, dbases);
     TAURUS_CHECK_LAUNCH();
     {
         std::vector<int64_t> bases((size_t)(nch + 1) * NLIST);

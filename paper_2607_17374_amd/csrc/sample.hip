@@ -172,7 +172,8 @@ struct SampleOut {
 };
 constexpr int SAMPLE_BAD = 32;
 
-__device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int64_t pos) {
+// fcu: chunk of v's smallest kept source (items mode)
+__device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int64_t pos, uint32_t fcu) {
     if (o.mask) {
         int64_t lo = o.row_off[u], hi = o.row_off[u + 1];  // (u, v) is an edge: v is in row u
         while (lo < hi) {
@@ -184,7 +185,10 @@ __device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int6
     } else {
         const uint32_t cu = u / (uint32_t)o.C;  // u < 2^31 and C < 2^31
         const int64_t at = o.koff[v] + pos;
-        o.keys[at] = ((uint64_t)cu << o.vbits) | (uint64_t)v;
+        // not the destination's first flush: a chunk after the earlier of
+        // its first kept source's chunk and its own chunk
+        const uint64_t nf = cu != min(fcu, (uint32_t)v / (uint32_t)o.C) ? 1 : 0;
+        o.keys[at] = ((uint64_t)cu << (o.vbits + 1)) | (nf << o.vbits) | (uint64_t)v;
         o.vals[at] = u - cu * (uint32_t)o.C;
         if (pos == 0 && o.first_chunk) o.first_chunk[v] = (int32_t)cu;
     }
@@ -241,13 +245,21 @@ __global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict_
         // the destination's kept in-edges counts the kept slots before it
         int before = 0;
         const int64_t mk = min(d, (int64_t)k);  // kept in-edges of v (distinct pairs)
+        // the smallest kept source (slot order is source order)
+        uint32_t umin = ~0u;
+#pragma unroll
+        for (int t = 0; t < 4; t++)
+            if (valid[t] && (!rank || below[t] < k)) umin = min(umin, u[t]);
+#pragma unroll
+        for (int x = 8; x >= 1; x >>= 1) umin = min(umin, (uint32_t)__shfl_xor(umin, x, 16));
+        const uint32_t fcu = umin / (uint32_t)o.C;
 #pragma unroll
         for (int t = 0; t < 4; t++) {
             const bool kept = valid[t] && (!rank || below[t] < k);
             const uint64_t bal = __ballot(kept);
             const uint32_t g16 = (uint32_t)(bal >> (grp * 16)) & 0xffffu;
             const int pos = before + __popc(g16 & ((1u << sub) - 1u));
-            if (kept && pos < mk) emit_kept(o, v, u[t], pos);
+            if (kept && pos < mk) emit_kept(o, v, u[t], pos, fcu);
             before += __popc(g16);
         }
     }
@@ -261,6 +273,7 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
                                                       uint64_t seed, int layer, int k, SampleOut o) {
     __shared__ uint64_t ckey[4][HEAVY_CAP];
     __shared__ uint32_t cu[4][HEAVY_CAP];
+    __shared__ uint64_t kbits[4][HEAVY_CAP / 64];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const uint64_t lt = (1ull << lane) - 1ull;
     const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -268,8 +281,9 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
     for (int64_t h = wave; h < nheavy; h += nwaves) {  // uniform over the wave
         const int64_t v = heavy[h];
         const int64_t a = in_off[v], d = in_off[v + 1] - a;
-        if (d <= k) {  // every in-edge is kept
-            for (int64_t sl = lane; sl < d; sl += 64) emit_kept(o, v, (uint32_t)in_src[a + sl], sl);
+        if (d <= k) {  // every in-edge is kept; the first is the smallest
+            const uint32_t fcu = (uint32_t)in_src[a] / (uint32_t)o.C;
+            for (int64_t sl = lane; sl < d; sl += 64) emit_kept(o, v, (uint32_t)in_src[a + sl], sl, fcu);
             continue;
         }
         const uint64_t pre = sample_prefix(seed, (uint64_t)layer, (uint64_t)v);
@@ -351,22 +365,33 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
         }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        // rank each candidate among all; keep the k smallest, in candidate order
-        int64_t before = 0;
+        // rank each candidate among all; keep the k smallest, in candidate
+        // order.  The kept flags go to LDS first: the first kept candidate
+        // (the smallest kept source) decides every kept item's key.
+        uint32_t fcu = ~0u;
         for (int64_t i0 = 0; i0 < m; i0 += 64) {
             const int64_t i = i0 + lane;
             bool kept = false;
-            uint32_t ui = 0;
             if (i < m) {
                 const uint64_t ki = ckey[w][i];
-                ui = cu[w][i];
+                const uint32_t ui = cu[w][i];
                 int r = 0;
                 for (int64_t j = 0; j < m && r < k; j++) r += pair_less(ckey[w][j], cu[w][j], ki, ui) ? 1 : 0;
                 kept = r < k;
             }
             const uint64_t bal = __ballot(kept);
+            if (lane == 0) kbits[w][i0 >> 6] = bal;
+            if (bal && fcu == ~0u) fcu = cu[w][i0 + __builtin_ctzll(bal)] / (uint32_t)o.C;
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        int64_t before = 0;
+        for (int64_t i0 = 0; i0 < m; i0 += 64) {
+            const int64_t i = i0 + lane;
+            const uint64_t bal = kbits[w][i0 >> 6];
+            const bool kept = (bal >> lane) & 1;
             const int64_t pos = before + __popcll(bal & lt);
-            if (kept && pos < k) emit_kept(o, v, ui, pos);
+            if (kept && pos < k) emit_kept(o, v, cu[w][i], pos, fcu);
             before += __popcll(bal);
         }
         // the slice is rewritten by this wave's next destination
