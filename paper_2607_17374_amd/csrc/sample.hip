@@ -9,18 +9,21 @@
 // decides every in-edge and writes the kept ones straight out, in CSC order,
 // at position koff[v] + (kept in-edges of v before it), koff = the exclusive
 // scan of min(d_in, k):
-//   - lists of at most 64 in-edges: 16 lanes per destination hold the whole
-//     list (4 in-edges a lane); an in-edge is kept iff fewer than k pairs of
-//     its list are smaller (every pair is compared with every other by
-//     broadcast within the 16 lanes);
+//   - lists of at most min(k, 64) in-edges are kept whole: a wave copies the
+//     lists of 64 consecutive destinations in-edge-parallel;
+//   - lists of k+1 .. 64 in-edges (collected by that pass): 16 lanes per
+//     destination hold the whole list (4 in-edges a lane); an in-edge is
+//     kept iff fewer than k pairs of its list are smaller (every pair is
+//     compared with every other by broadcast within the 16 lanes);
 //   - longer lists: a wave each.  Keys are uniform 64-bit values, so the k
 //     smallest lie below a cutoff that passes about k + 4 sqrt(k) + 16 of
 //     them; the wave counts the keys at or below a cutoff, moves it until
-//     between k and HEAVY_CAP pass (SplitMix64's finaliser is a bijection, so
-//     one destination's keys are distinct and the count rises by one key at
-//     a time: some cutoff always qualifies), gathers those candidates in LDS
-//     and ranks them by pairwise comparison.  Every pair below the k-th
-//     smallest passes any qualifying cutoff, so the kept set is exact.
+//     between k and a cap (256 or 1024) pass (SplitMix64's finaliser is a
+//     bijection, so one destination's keys are distinct and the count rises
+//     by one key at a time: some cutoff always qualifies), gathers those
+//     candidates in LDS and ranks them by pairwise comparison.  Every pair
+//     below the k-th smallest passes any qualifying cutoff, so the kept set
+//     is exact.
 // Rank pairs are distinct within a destination (the sources are), so the
 // kept set is unique.  The same pass can instead set the kept edges' bits
 // in a CSR-order mask (each kept (u, v) found in row u by binary search),
@@ -152,7 +155,11 @@ __device__ inline bool pair_less(uint64_t ka, uint32_t ua, uint64_t kb, uint32_t
 }
 
 constexpr int LIGHT_MAX = 64;     // lists up to this long are ranked in registers
-constexpr int HEAVY_CAP = 1024;   // candidates a wave of the long-list pass holds in LDS
+// candidates a wave of the long-list pass holds in LDS: 256 while the
+// cutoff's target k + 4 sqrt(k) + 16 stays well inside it (k <= 128), else
+// 1024 (fewer workgroups fit a CU)
+constexpr int HEAVY_CAP = 1024;
+constexpr int HEAVY_CAP_SMALL = 256, HEAVY_SMALL_K = 128;
 constexpr int REG_MAX = 512;      // long lists up to this length are held in registers
 
 // Where the kept in-edges go: chunk-index items at koff[v] + (position among
@@ -172,8 +179,10 @@ struct SampleOut {
 };
 constexpr int SAMPLE_BAD = 32;
 
-// fcu: chunk of v's smallest kept source (items mode)
-__device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int64_t pos, uint32_t fcu) {
+// Kept in-edge (u, v) at item position `at` (items mode: koff[v] + its
+// position among v's kept in-edges; `first` when that position is 0).
+// fcu: chunk of v's smallest kept source.
+__device__ inline void emit_item(const SampleOut& o, int64_t v, uint32_t u, int64_t at, bool first, uint32_t fcu) {
     if (o.mask) {
         int64_t lo = o.row_off[u], hi = o.row_off[u + 1];  // (u, v) is an edge: v is in row u
         while (lo < hi) {
@@ -184,33 +193,119 @@ __device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int6
         atomicOr(&o.mask[lo >> 6], 1ull << (lo & 63));
     } else {
         const uint32_t cu = u / (uint32_t)o.C;  // u < 2^31 and C < 2^31
-        const int64_t at = o.koff[v] + pos;
         // not the destination's first flush: a chunk after the earlier of
         // its first kept source's chunk and its own chunk
         const uint64_t nf = cu != min(fcu, (uint32_t)v / (uint32_t)o.C) ? 1 : 0;
         o.keys[at] = ((uint64_t)cu << (o.vbits + 1)) | (nf << o.vbits) | (uint64_t)v;
         o.vals[at] = u - cu * (uint32_t)o.C;
-        if (pos == 0 && o.first_chunk) o.first_chunk[v] = (int32_t)cu;
+        if (first && o.first_chunk) o.first_chunk[v] = (int32_t)cu;
     }
 }
 
-// Lists of at most LIGHT_MAX in-edges, 16 lanes per destination, four
-// destinations per wave, waves striding over the vertices.  Lane j of a
-// group holds slots j, j + 16, j + 32, j + 48 of its destination's list.
-__global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict__ in_off,
-                                                      const int32_t* __restrict__ in_src, int64_t n, uint64_t seed,
-                                                      int layer, int k, SampleOut o) {
-    const int lane = threadIdx.x & 63, sub = lane & 15, grp = lane >> 4;
+__device__ inline void emit_kept(const SampleOut& o, int64_t v, uint32_t u, int64_t pos, uint32_t fcu) {
+    emit_item(o, v, u, o.mask ? 0 : o.koff[v] + pos, pos == 0, fcu);
+}
+
+// Lists of 1 .. min(k, LIGHT_MAX) in-edges, kept whole, and the
+// destinations whose lists need ranking (k < d_in <= LIGHT_MAX) noted in
+// rank_list.  A wave takes 64 consecutive destinations, a lane each; their
+// kept in-edges are copied in-edge-parallel (item t of the wave's run goes
+// to the lane whose running count first exceeds t), so the in-lists are
+// read and the items written contiguously.
+__global__ __launch_bounds__(256) void k_sample_short(const int64_t* __restrict__ in_off,
+                                                      const int32_t* __restrict__ in_src, int64_t n, int k,
+                                                      SampleOut o, int32_t* __restrict__ rank_list,
+                                                      unsigned int* __restrict__ rank_count) {
+    // destinations to rank wait in a per-wave LDS buffer and leave it 64 at
+    // a time, so the shared list count takes one atomic per 64 of them
+    __shared__ int32_t rbuf[4][128];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t lt = (1ull << lane) - 1ull;
     const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-    for (int64_t base = wave * 4; base < n; base += nwaves * 4) {  // uniform over the wave
-        const int64_t v = base + grp;
+    const int64_t cmax = min((int64_t)k, (int64_t)LIGHT_MAX);
+    auto flush = [&](int cnt) {  // the first cnt buffered entries to the list
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        unsigned int at = 0;
+        if (lane == 0) at = atomicAdd(rank_count, (unsigned int)cnt);
+        at = __shfl(at, 0);
+        if (lane < cnt) rank_list[at + lane] = rbuf[w][lane];
+    };
+    int rn = 0;  // buffered entries (uniform over the wave)
+    for (int64_t v0 = wave * 64; v0 < n; v0 += nwaves * 64) {  // uniform over the wave
+        const int64_t v = v0 + lane;
         int64_t a = 0, d = 0;
         if (v < n) {
             a = in_off[v];
             d = in_off[v + 1] - a;
         }
-        const bool mine = v < n && d > 0 && d <= LIGHT_MAX;
+        const bool rank = d > k && d <= LIGHT_MAX;
+        const uint64_t rb = __ballot(rank);
+        if (rb) {
+            if (rank) rbuf[w][rn + __popcll(rb & lt)] = (int32_t)v;
+            rn += __popcll(rb);
+            if (rn >= 64) {
+                flush(64);
+                const int32_t rest = lane + 64 < rn ? rbuf[w][lane + 64] : 0;
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+                if (lane + 64 < rn) rbuf[w][lane] = rest;
+                rn -= 64;
+            }
+        }
+        const int cnt = d > 0 && d <= cmax ? (int)d : 0;
+        int incl = cnt;
+#pragma unroll
+        for (int m = 1; m < 64; m <<= 1) {
+            const int y = __shfl_up(incl, m, 64);
+            if (lane >= m) incl += y;
+        }
+        const int total = __shfl(incl, 63);
+        // a kept list's first in-edge is its smallest source
+        const uint32_t fcu = cnt ? (uint32_t)in_src[a] / (uint32_t)o.C : 0u;
+        const int64_t ko = cnt && !o.mask ? o.koff[v] : 0;
+        for (int t0 = 0; t0 < total; t0 += 64) {  // uniform over the wave
+            const int t = t0 + lane;
+            // owner: the first lane whose running count exceeds t
+            int lo = 0, hi = 63;
+#pragma unroll
+            for (int q = 0; q < 6; q++) {
+                const int mid = (lo + hi) >> 1;
+                const int x = __shfl(incl, mid);
+                if (x > t) hi = mid;
+                else lo = mid + 1;
+            }
+            const int pos = t - (__shfl(incl, lo) - __shfl(cnt, lo));
+            const int64_t al = __shfl(a, lo), kl = __shfl(ko, lo);
+            const uint32_t fl = __shfl(fcu, lo);
+            if (t < total) emit_item(o, v0 + lo, (uint32_t)in_src[al + pos], kl + pos, pos == 0, fl);
+        }
+    }
+    if (rn > 0) flush(rn);
+}
+
+// Lists of k < d_in <= LIGHT_MAX in-edges (rank_list[0 .. *rank_count)),
+// 16 lanes per destination, four destinations per wave, waves striding
+// over the list.  Lane j of a group holds slots j, j + 16, j + 32, j + 48
+// of its destination's list.
+__global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict__ in_off,
+                                                      const int32_t* __restrict__ in_src,
+                                                      const int32_t* __restrict__ rank_list,
+                                                      const unsigned int* __restrict__ rank_count, uint64_t seed,
+                                                      int layer, int k, SampleOut o) {
+    const int lane = threadIdx.x & 63, sub = lane & 15, grp = lane >> 4;
+    const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    const int64_t nr = *rank_count;
+    for (int64_t base = wave * 4; base < nr; base += nwaves * 4) {  // uniform over the wave
+        const int64_t v = base + grp < nr ? (int64_t)rank_list[base + grp] : -1;
+        int64_t a = 0, d = 0;
+        if (v >= 0) {
+            a = in_off[v];
+            d = in_off[v + 1] - a;
+        }
+        const bool mine = v >= 0 && d > 0 && d <= LIGHT_MAX;
         const bool rank = mine && d > k;
         const uint64_t pre = rank ? sample_prefix(seed, (uint64_t)layer, (uint64_t)v) : 0;
         uint32_t u[4];
@@ -267,13 +362,14 @@ __global__ __launch_bounds__(256) void k_sample_light(const int64_t* __restrict_
 
 // Lists longer than LIGHT_MAX (heavy[0 .. nheavy)), a wave each; the four
 // waves of a workgroup keep their candidates in separate LDS slices.
+template <int CAP>
 __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict__ in_off,
                                                       const int32_t* __restrict__ in_src,
                                                       const int32_t* __restrict__ heavy, int64_t nheavy,
                                                       uint64_t seed, int layer, int k, SampleOut o) {
-    __shared__ uint64_t ckey[4][HEAVY_CAP];
-    __shared__ uint32_t cu[4][HEAVY_CAP];
-    __shared__ uint64_t kbits[4][HEAVY_CAP / 64];
+    __shared__ uint64_t ckey[4][CAP];
+    __shared__ uint32_t cu[4][CAP];
+    __shared__ uint64_t kbits[4][CAP / 64];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const uint64_t lt = (1ull << lane) - 1ull;
     const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -300,28 +396,55 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
 #pragma unroll
             for (int t = 0; t < REG_MAX / 64; t++) rk[t] = (int64_t)t * 64 + lane < d ? sample_key(pre, ru[t]) : ~0ull;
         }
-        auto count = [&](uint64_t cut) {
+        // Count the keys at or below cut; with gather, also write those
+        // candidates to LDS in CSC order (sources ascending) while they fit.
+        // Longer lists stream through in blocks of REG_MAX, all of a
+        // block's loads in flight before its keys are hashed.
+        auto scan = [&](uint64_t cut, bool gather) {
             int64_t c = 0;
+            auto take = [&](bool in, uint64_t kk, uint32_t uu) {
+                const uint64_t bal = __ballot(in);
+                if (gather && in) {
+                    const int64_t at = c + __popcll(bal & lt);
+                    if (at < CAP) {
+                        ckey[w][at] = kk;
+                        cu[w][at] = uu;
+                    }
+                }
+                c += __popcll(bal);
+            };
             if (in_regs) {
 #pragma unroll
-                for (int t = 0; t < REG_MAX / 64; t++) c += __popcll(__ballot((int64_t)t * 64 + lane < d && rk[t] <= cut));
+                for (int t = 0; t < REG_MAX / 64; t++) take((int64_t)t * 64 + lane < d && rk[t] <= cut, rk[t], ru[t]);
                 return c;
             }
-            for (int64_t sl = lane; sl - lane < d; sl += 64) {
-                const bool in = sl < d && sample_key(pre, (uint32_t)in_src[a + sl]) <= cut;
-                c += __popcll(__ballot(in));
+            for (int64_t b0 = 0; b0 < d; b0 += REG_MAX) {  // uniform over the wave
+                uint32_t uu[REG_MAX / 64];
+#pragma unroll
+                for (int t = 0; t < REG_MAX / 64; t++) {
+                    const int64_t sl = b0 + t * 64 + lane;
+                    uu[t] = sl < d ? (uint32_t)in_src[a + sl] : 0u;
+                }
+#pragma unroll
+                for (int t = 0; t < REG_MAX / 64; t++) {
+                    const bool ok = b0 + t * 64 + lane < d;
+                    const uint64_t kk = ok ? sample_key(pre, uu[t]) : ~0ull;
+                    take(ok && kk <= cut, kk, uu[t]);
+                }
             }
             return c;
         };
-        // cutoff: about k + 4 sqrt(k) + 16 keys of d pass; then widen or
-        // narrow until k <= count <= HEAVY_CAP
+        // cutoff: about k + 4 sqrt(k) + 16 keys of d pass, gathering on the
+        // way; if the count falls outside [k, CAP], widen or narrow the
+        // cutoff by counting alone, then gather once more
         const double want = (double)k + 4.0 * sqrt((double)k) + 16.0;
         uint64_t cut = want >= (double)d ? ~0ull : (uint64_t)(want / (double)d * 18446744073709551616.0);
         bool have_lo = false, have_hi = false;
-        uint64_t lo = 0, hi = 0;  // count(lo) < k, count(hi) > HEAVY_CAP
-        int64_t cnt = count(cut);
+        uint64_t lo = 0, hi = 0;  // count(lo) < k, count(hi) > CAP
+        int64_t cnt = scan(cut, true);
+        bool gathered = true;
         int rounds = 0;
-        while ((cnt < k || cnt > HEAVY_CAP) && ++rounds <= 200) {
+        while ((cnt < k || cnt > CAP) && ++rounds <= 200) {
             if (cnt < k) {
                 lo = cut;
                 have_lo = true;
@@ -332,37 +455,15 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
             if (!have_hi) cut = cut > (~0ull >> 1) ? ~0ull : 2 * cut + 1;
             else if (!have_lo) cut = cut >> 1;
             else cut = lo + ((hi - lo) >> 1);
-            cnt = count(cut);
+            cnt = scan(cut, false);
+            gathered = false;
         }
-        if (cnt < k || cnt > HEAVY_CAP) {  // only repeated sources make the count jump past the window
+        if (cnt < k || cnt > CAP) {  // only repeated sources make the count jump past the window
             if (lane == 0) atomicOr(o.bad, SAMPLE_BAD);
             continue;
         }
-        // candidates in CSC order (sources ascending)
-        int64_t m = 0;
-        auto gather = [&](bool in, uint64_t kk, uint32_t uu) {
-            const uint64_t bal = __ballot(in);
-            if (in) {
-                const int64_t at = m + __popcll(bal & lt);
-                ckey[w][at] = kk;
-                cu[w][at] = uu;
-            }
-            m += __popcll(bal);
-        };
-        if (in_regs) {
-#pragma unroll
-            for (int t = 0; t < REG_MAX / 64; t++) gather((int64_t)t * 64 + lane < d && rk[t] <= cut, rk[t], ru[t]);
-        } else {
-            for (int64_t sl = lane; sl - lane < d; sl += 64) {
-                uint32_t uu = 0;
-                uint64_t kk = ~0ull;
-                if (sl < d) {
-                    uu = (uint32_t)in_src[a + sl];
-                    kk = sample_key(pre, uu);
-                }
-                gather(sl < d && kk <= cut, kk, uu);
-            }
-        }
+        if (!gathered) scan(cut, true);
+        const int64_t m = cnt;
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         // rank each candidate among all; keep the k smallest, in candidate
@@ -401,19 +502,34 @@ __global__ __launch_bounds__(256) void k_sample_heavy(const int64_t* __restrict_
 }
 
 static void sample_pass(const Csc& csc, int64_t n, uint64_t seed, int layer, int k, const SampleOut& o,
-                        hipStream_t s) {
+                        Arena& tmp, hipStream_t s) {
     if (k < 1 || k > FANOUT_MAX) fail(TAURUS_E_INVALID, "fanout %d outside [1, %d]", k, FANOUT_MAX);
+    if (n >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "sampler: %lld vertices exceed 2^31", (long long)n);
     int dev = 0, cus = 0;
     TAURUS_HIP(hipGetDevice(&dev));
     TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    const int64_t grid_light = std::min<int64_t>(ceil_div(n, 16), (int64_t)cus * 32);
-    k_sample_light<<<(unsigned)std::max<int64_t>(1, grid_light), 256, 0, s>>>(csc.in_off, csc.in_src, n, seed, layer,
-                                                                             k, o);
+    int32_t* rank_list = tmp.alloc<int32_t>(std::max<int64_t>(1, n), "short lists to rank");
+    unsigned int* rank_count = tmp.alloc<unsigned int>(1, "short lists to rank: count");
+    fill_i32(reinterpret_cast<int32_t*>(rank_count), 1, 0, s);
+    const int64_t grid_short = std::min<int64_t>(ceil_div(n, 256), (int64_t)cus * 32);
+    k_sample_short<<<(unsigned)std::max<int64_t>(1, grid_short), 256, 0, s>>>(csc.in_off, csc.in_src, n, k, o,
+                                                                             rank_list, rank_count);
     TAURUS_CHECK_LAUNCH();
+    if (k < LIGHT_MAX) {  // else every list of at most LIGHT_MAX in-edges is kept whole
+        k_sample_light<<<(unsigned)cus * 32, 256, 0, s>>>(csc.in_off, csc.in_src, rank_list, rank_count, seed, layer,
+                                                          k, o);
+        TAURUS_CHECK_LAUNCH();
+    }
     if (csc.nheavy > 0) {
-        const int64_t grid_heavy = std::min<int64_t>(ceil_div(csc.nheavy, 4), (int64_t)cus * 12);
-        k_sample_heavy<<<(unsigned)grid_heavy, 256, 0, s>>>(csc.in_off, csc.in_src, csc.heavy, csc.nheavy, seed,
-                                                          layer, k, o);
+        if (k <= HEAVY_SMALL_K) {
+            const int64_t grid = std::min<int64_t>(ceil_div(csc.nheavy, 4), (int64_t)cus * 32);
+            k_sample_heavy<HEAVY_CAP_SMALL><<<(unsigned)grid, 256, 0, s>>>(csc.in_off, csc.in_src, csc.heavy,
+                                                                          csc.nheavy, seed, layer, k, o);
+        } else {
+            const int64_t grid = std::min<int64_t>(ceil_div(csc.nheavy, 4), (int64_t)cus * 12);
+            k_sample_heavy<HEAVY_CAP><<<(unsigned)grid, 256, 0, s>>>(csc.in_off, csc.in_src, csc.heavy, csc.nheavy,
+                                                                    seed, layer, k, o);
+        }
         TAURUS_CHECK_LAUNCH();
     }
 }
@@ -447,7 +563,7 @@ int64_t sample_items(const Csc& csc, int64_t n, uint64_t seed, int layer, int k,
     if (kept > 0)
         sample_pass(csc, n, seed, layer, k,
                     SampleOut{sb.keys[0], sb.vals[0], koff, C, vbits, nullptr, nullptr, nullptr, bad, first_chunk},
-                    s);
+                    key_arena, s);
     return kept;
 }
 
@@ -462,7 +578,7 @@ void sample_mask(const taurus_graph& g, const Csc& csc, uint64_t seed, int layer
     sample_pass(csc, g.n, seed, layer, k,
                 SampleOut{nullptr, nullptr, nullptr, 1, 1, reinterpret_cast<unsigned long long*>(mask), g.row_off,
                           g.col_dst, bad, nullptr},
-                s);
+                tmp, s);
     int hbad = 0;
     Readback rb;
     rb.add(&hbad, bad, 1);
