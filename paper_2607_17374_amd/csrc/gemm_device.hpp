@@ -105,10 +105,11 @@ struct PanelLds {
 // r of the panel reads row arow(r) of X; for each row r < M the epilogue's
 // row(r) returns a per-row writer w, and w(col, value) stores each product
 // of that row, column col < Nc.
-template <int DT, int PANEL_NB, class ARow, class Epi>
-__device__ __attribute__((always_inline)) inline void gemm_panel_core(const void* __restrict__ X, int64_t M, int K,
-                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc, int bx,
-                                        int by, PanelLds<DT, PANEL_NB>& lds, ARow arow, Epi epi) {
+template <int DT, int PANEL_NB, class ARow>
+__device__ __attribute__((always_inline)) inline void gemm_panel_compute(const void* __restrict__ X, int64_t M,
+                                        int K, const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int bx,
+                                        int by, PanelLds<DT, PANEL_NB>& lds, ARow arow,
+                                        floatx4 (&acc)[PANEL_NB]) {
     typedef GemmOp<DT> Op;
     typedef typename Op::frag frag;
     constexpr int SF = PanelLds<DT, PANEL_NB>::SF;
@@ -139,7 +140,6 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_core(const void
             a[kk] = (kb < KB && row < M && k < K) ? Op::load_a(X, arow(row), K, k) : Op::zero();
         }
     };
-    floatx4 acc[PANEL_NB];
 #pragma unroll
     for (int j = 0; j < PANEL_NB; j++) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
     frag rw[PER], a[PIPE_KS];
@@ -171,7 +171,20 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_core(const void
         }
         __syncthreads();
     }
-    const int64_t rbase = (int64_t)bx * PANEL_ROWS + wave * 16 + 4 * lk;
+}
+
+// The panel with a per-element epilogue: lane (li, lk) of wave w holds rows
+// 64 bx + 16 w + 4 lk + r (r = 0..3) of column 16 (PANEL_NB by + j) + li in
+// acc[j][r].
+template <int DT, int PANEL_NB, class ARow, class Epi>
+__device__ __attribute__((always_inline)) inline void gemm_panel_core(const void* __restrict__ X, int64_t M, int K,
+                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc, int bx,
+                                        int by, PanelLds<DT, PANEL_NB>& lds, ARow arow, Epi epi) {
+    floatx4 acc[PANEL_NB];
+    gemm_panel_compute<DT, PANEL_NB>(X, M, K, Wp, NBP, bx, by, lds, arow, acc);
+    const int lane = threadIdx.x & 63, li = lane & 15, lk = lane >> 4;
+    const int nb0 = by * PANEL_NB, nbs = min(PANEL_NB, NBP - nb0);
+    const int64_t rbase = (int64_t)bx * PANEL_ROWS + (threadIdx.x >> 6) * 16 + 4 * lk;
 #pragma unroll
     for (int r = 0; r < 4; r++) {
         const int64_t orow = rbase + r;
@@ -186,24 +199,53 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_core(const void
 }
 
 // Y = X W (rows scaled by rscale when given), rows [64 bx, 64 bx + 64) and
-// column blocks [PANEL_NB by, PANEL_NB by + PANEL_NB)
-struct ScaledRows {
-    const float* rscale;
-    float* Y;
-    int Nc;
-    __device__ inline auto row(int64_t r) const {
-        const float sc = rscale ? rscale[r] : 1.0f;
-        float* y = Y + r * Nc;
-        return [=](int col, float v) { y[col] = v * sc; };
-    }
-};
+// column blocks [PANEL_NB by, PANEL_NB by + PANEL_NB).  The products go
+// through LDS (the weight buffers are free once the last stage is done): a
+// 64 x 16 PANEL_NB fp32 tile, written in the matrix cores' layout and read
+// back row-major, so that each wave stores whole 16-byte pieces of
+// consecutive columns (two full 512-byte rows per store for 128 columns)
+// instead of 64-byte pieces of four rows.  Columns are XOR-swizzled by 16
+// with bit 2 of the row, so the four row groups of a store into the tile
+// fall on distinct bank halves.
 template <int DT, int PANEL_NB>
 __device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
                                         const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
                                         const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
                                         PanelLds<DT, PANEL_NB>& lds) {
-    gemm_panel_core<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, bx, by, lds, [](int64_t r) { return r; },
-                                  ScaledRows{rscale, Y, Nc});
+    constexpr int TW = PANEL_NB * 16;  // tile width (fp32 columns)
+    static_assert(sizeof(lds.b) >= (size_t)PANEL_ROWS * TW * 4, "the weight buffers hold the output tile");
+    floatx4 acc[PANEL_NB];
+    gemm_panel_compute<DT, PANEL_NB>(X, M, K, Wp, NBP, bx, by, lds, [](int64_t r) { return r; }, acc);
+    // every wave is past the last stage's barrier: the buffers are free
+    float* tile = reinterpret_cast<float*>(&lds.b[0][0]);
+    const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lk = lane >> 4;
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+        const int row = (tid >> 6) * 16 + 4 * lk + r;
+        const int sw = ((row >> 2) & 1) << 4;
+#pragma unroll
+        for (int j = 0; j < PANEL_NB; j++) tile[row * TW + ((j * 16 + li) ^ sw)] = acc[j][r];
+    }
+    __syncthreads();
+    const int c0 = by * TW;  // first column of the group
+    constexpr int Q = TW / 4;  // float4 per tile row
+#pragma unroll
+    for (int i = 0; i < PANEL_ROWS * Q / 256; i++) {
+        const int q = i * 256 + tid, row = q / Q, c = (q % Q) * 4;
+        const int64_t grow = (int64_t)bx * PANEL_ROWS + row;
+        const int col = c0 + c;
+        if (grow >= M || col >= Nc) continue;
+        const int sw = ((row >> 2) & 1) << 4;
+        float4 v = *reinterpret_cast<const float4*>(tile + row * TW + (c ^ sw));
+        if (rscale) {
+            const float sc = rscale[grow];
+            v.x *= sc;
+            v.y *= sc;
+            v.z *= sc;
+            v.w *= sc;
+        }
+        *reinterpret_cast<float4*>(Y + grow * Nc + col) = v;
+    }
 }
 
 }  // namespace taurus
