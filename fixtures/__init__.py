@@ -26,7 +26,7 @@ def build(force: bool = True) -> str:
     """Compile fixgen.c into libfixgen.so (host code, gcc + OpenMP)."""
     if force or not os.path.exists(_SO):
         tmp = _SO + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall",
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-Wall",
                                "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _SO)
     return _SO
@@ -49,6 +49,8 @@ def lib():
         L.fx_rmat.argtypes = [u64, i64, i64, dbl, dbl, dbl, vp, vp]
         L.fx_features.restype = None
         L.fx_features.argtypes = [u64, i32, i64, i64, i64, i32, vp]
+        L.fx_fill_features.restype = i32
+        L.fx_fill_features.argtypes = [vp, i64, i64, vp]
         L.fx_features_rows.restype = None
         L.fx_features_rows.argtypes = [u64, i32, i64, vp, i64, i32, vp]
         L.fx_weights.restype = None
@@ -95,6 +97,20 @@ def features(seed: int, dist: int, v0: int, v1: int, d: int, dtype: int = F32) -
     out = np.empty((v1 - v0, d), np_dtype(dtype))
     lib().fx_features(seed, dist, v0, v1, d, dtype, _p(out))
     return out
+
+
+class FillCtx(ctypes.Structure):
+    """Context of fx_fill_features (the chunk-loader fill callback)."""
+    _fields_ = [("seed", ctypes.c_uint64), ("dist", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("d", ctypes.c_int64), ("threads", ctypes.c_int32)]
+
+
+def feature_fill(seed: int, dist: int, d: int, dtype: int = F32, threads: int = 0):
+    """(function address, context) of the native fill callback that writes the
+    same rows as features(); keep the context alive while it is used."""
+    ctx = FillCtx(seed & (2**64 - 1), dist, dtype, d, threads)
+    fn = ctypes.cast(lib().fx_fill_features, ctypes.c_void_p).value
+    return fn, ctx
 
 
 def features_rows(seed: int, dist: int, ids: np.ndarray, d: int, dtype: int = F32) -> np.ndarray:

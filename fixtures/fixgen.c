@@ -195,9 +195,39 @@ static inline float fx_feature(uint64_t seed, int dist, uint64_t v, uint64_t j) 
     return (float)z;
 }
 
+/*
+ * One fp32 row of dist 0 from the row prefix hv = H(seed, 2, v): the same
+ * values as fx_feature, written so that the compiler vectorises it (x =
+ * top 24 bits; x * 2^-23 - 1 = (x - 2^23) * 2^-23 is exact in fp32).  A
+ * copy built for AVX-512 (64-bit vector multiplies) is used where the host
+ * has it.
+ */
+#define FX_UNIFORM_ROW_BODY                                                      \
+    for (int64_t j = 0; j < d; j++) {                                            \
+        uint64_t z = hv + FX_GAMMA + (uint64_t)j;                                \
+        z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;                             \
+        z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;                             \
+        z ^= z >> 31;                                                            \
+        row[j] = (float)((int32_t)(z >> 40) - 8388608) * 0x1.0p-23f;             \
+    }
+__attribute__((target("avx512f,avx512dq,avx512vl")))
+static void fx_uniform_row_avx512(uint64_t hv, int64_t d, float* row) { FX_UNIFORM_ROW_BODY }
+static void fx_uniform_row_plain(uint64_t hv, int64_t d, float* row) { FX_UNIFORM_ROW_BODY }
+static void fx_uniform_row(uint64_t hv, int64_t d, float* row) {
+    static int wide = -1;
+    if (wide < 0) wide = __builtin_cpu_supports("avx512dq") && __builtin_cpu_supports("avx512vl") ? 1 : 0;
+    if (wide) fx_uniform_row_avx512(hv, d, row);
+    else fx_uniform_row_plain(hv, d, row);
+}
+
 void fx_features(uint64_t seed, int dist, int64_t v0, int64_t v1, int64_t d, int out_dtype, void* out) {
+    const uint64_t s2 = fx_step(seed, 2);
 #pragma omp parallel for schedule(static)
     for (int64_t v = v0; v < v1; v++) {
+        if (dist == 0 && out_dtype == 0) {
+            fx_uniform_row(fx_step(s2, (uint64_t)v), d, (float*)out + (v - v0) * d);
+            continue;
+        }
         for (int64_t j = 0; j < d; j++) {
             float f = fx_feature(seed, dist, (uint64_t)v, (uint64_t)j);
             int64_t o = (v - v0) * d + j;
@@ -206,6 +236,44 @@ void fx_features(uint64_t seed, int dist, int64_t v0, int64_t v1, int64_t d, int
             else ((uint16_t*)out)[o] = fx_f32_to_f16(f);
         }
     }
+}
+
+/*
+ * The same rows as fx_features, as a chunk-loader fill callback: ctx is an
+ * fx_fill_ctx, rows [v0, v1) go to out.  The row's hash prefix
+ * H(seed, 2, v) is taken once per row (the values are fx_features' exactly);
+ * rows are spread over ctx->threads OpenMP threads (0: the runtime's
+ * default).  Returns 0.
+ */
+typedef struct {
+    uint64_t seed;
+    int32_t dist;
+    int32_t out_dtype;
+    int64_t d;
+    int32_t threads;
+} fx_fill_ctx;
+
+int fx_fill_features(void* ctx_, int64_t v0, int64_t v1, void* out) {
+    const fx_fill_ctx* ctx = (const fx_fill_ctx*)ctx_;
+    const uint64_t s2 = fx_step(ctx->seed, 2);
+    const int64_t d = ctx->d;
+    const int nt = ctx->threads > 0 ? ctx->threads : omp_get_max_threads();
+#pragma omp parallel for schedule(static) num_threads(nt)
+    for (int64_t v = v0; v < v1; v++) {
+        const uint64_t hv = fx_step(s2, (uint64_t)v);
+        const int64_t o = (v - v0) * d;
+        if (ctx->dist == 0 && ctx->out_dtype == 0) {
+            fx_uniform_row(hv, d, (float*)out + o);
+            continue;
+        }
+        for (int64_t j = 0; j < d; j++) {
+            float f = fx_feature(ctx->seed, ctx->dist, (uint64_t)v, (uint64_t)j);
+            if (ctx->out_dtype == 0) ((float*)out)[o + j] = f;
+            else if (ctx->out_dtype == 1) ((uint16_t*)out)[o + j] = fx_f32_to_bf16(f);
+            else ((uint16_t*)out)[o + j] = fx_f32_to_f16(f);
+        }
+    }
+    return 0;
 }
 
 /* Rows listed in `ids` (any order), for sampled checks at large sizes. */

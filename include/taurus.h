@@ -456,6 +456,48 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
  */
 int taurus_layer_reload_histogram(taurus_layer* L, int64_t* counts, int32_t bins);
 
+/*
+ * Chunk loader (Sec. 3.3, Graph Reader: a dedicated reader keeps chunks
+ * coming while earlier ones copy and compute; Sec. 3.6, copies overlap
+ * compute on separate streams).  The loader fills chunks on host threads,
+ * each into one buffer of a ring of pinned host buffers, while the calling
+ * thread pushes them in ascending order (taurus_push_chunk with
+ * x_on_host = 1: copy on the layer's copy stream, then the chunk's work),
+ * so generation or reading, the host-to-device copy and the compute of
+ * different chunks overlap.
+ *
+ * fill(ctx, begin, end, dst) writes rows [begin, end) of the layer's input,
+ * row-major [end - begin][d_in] of desc.in_dtype, into dst (pinned host
+ * memory owned by the loader) and returns 0, or nonzero to stop the layer.
+ * It is called from `threads` loader threads at once (1 .. 64), for
+ * different chunks, and must be safe for that.  `ring` pinned buffers of
+ * one chunk each (threads + 1 .. 256; 0 picks 2 * threads) hold chunks
+ * being filled, filled and waiting, or copying; the ring is allocated per
+ * call and freed before return.
+ *
+ * Pushes every chunk of the layer; no chunk may have been pushed before
+ * (TAURUS_E_STATE).  Returns when the last chunk is queued and every copy
+ * out of the ring is done (the layer's work may still run; call
+ * taurus_finalize).  stats (may be NULL) receives the loader's times.
+ * Errors: TAURUS_E_INVALID for bad arguments or a fill that returned
+ * nonzero (the message names the chunk and the value; the handle is then
+ * poisoned, as are push errors after work started); TAURUS_E_OOM when the
+ * ring cannot be allocated.
+ */
+typedef int (*taurus_fill_fn)(void* ctx, int64_t begin, int64_t end, void* dst);
+
+typedef struct {
+    int64_t chunks;          /* chunks filled and pushed                          */
+    int64_t bytes;           /* host bytes filled (= bytes copied to the device)  */
+    double fill_seconds;     /* time inside fill, summed over the loader threads  */
+    double wait_seconds;     /* the pushing thread waiting for a filled chunk     */
+    double push_seconds;     /* the pushing thread inside taurus_push_chunk       */
+    double wall_seconds;     /* the whole call                                    */
+} taurus_stream_stats;
+
+int taurus_stream_layer(taurus_layer* L, taurus_fill_fn fill, void* ctx, int32_t threads, int32_t ring,
+                        taurus_stream_stats* stats);
+
 /* Release everything the layer allocated.  NULL is ignored. */
 void taurus_layer_destroy(taurus_layer* L);
 

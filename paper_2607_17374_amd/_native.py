@@ -62,6 +62,19 @@ class Stats(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class StreamStats(ctypes.Structure):
+    _fields_ = [("chunks", ctypes.c_int64), ("bytes", ctypes.c_int64), ("fill_seconds", ctypes.c_double),
+                ("wait_seconds", ctypes.c_double), ("push_seconds", ctypes.c_double),
+                ("wall_seconds", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+# the loader's fill callback: int fill(void* ctx, int64_t begin, int64_t end, void* dst)
+FILL_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p)
+
+
 # every function the header declares, with its C signature
 SIGNATURES = {
     "taurus_last_error": (ctypes.c_char_p, []),
@@ -75,6 +88,8 @@ SIGNATURES = {
     "taurus_push_chunk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                          ctypes.c_int32]),
     "taurus_finalize": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(Stats)]),
+    "taurus_stream_layer": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.POINTER(StreamStats)]),
     "taurus_sampled_edges": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]),
     "taurus_layer_destroy": (None, [ctypes.c_void_p]),
     "taurus_layer_reload_histogram": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]),

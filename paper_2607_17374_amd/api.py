@@ -276,6 +276,21 @@ class Layer:
             b, e = j * self.chunk, min((j + 1) * self.chunk, self.n)
             self.push_chunk(b, e, x[b:e])
 
+    def stream(self, fill, ctx=None, threads: int = 2, ring: int = 0) -> dict:
+        """taurus_stream_layer: the library's loader fills every chunk through
+        fill (a C function address, or an N.FILL_FN callback) on `threads`
+        host threads into a ring of pinned buffers and pushes them in order.
+        ctx: a ctypes object (passed by address), an int address or None.
+        Returns the loader's times."""
+        fn = fill if isinstance(fill, int) else ctypes.cast(fill, ctypes.c_void_p).value
+        if ctx is None or isinstance(ctx, int):
+            cp = ctx
+        else:
+            cp = ctypes.addressof(ctx)
+        st = N.StreamStats()
+        N.check(N.lib().taurus_stream_layer(self._h, fn, cp, threads, ring, ctypes.byref(st)), "taurus_stream_layer")
+        return st.as_dict()
+
     def finalize(self) -> dict:
         st = N.Stats()
         rc = N.lib().taurus_finalize(self._h, ctypes.byref(st))

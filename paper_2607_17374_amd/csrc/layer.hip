@@ -31,9 +31,12 @@
 // of one chunk are disjoint, kernels of one layer are stream ordered), so
 // accumulators are updated with plain loads and stores, no atomics.
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <condition_variable>
 #include <memory>
 #include <mutex>
+#include <thread>
 
 #include "device.hpp"
 #include "gemm_device.hpp"
@@ -2416,6 +2419,132 @@ int relabel_impl(const taurus_graph& g, const int32_t* new_of_old, int64_t* row_
 int permute_rows_impl(const void* in, void* out, int64_t n, int64_t row_bytes, const int32_t* new_of_old,
                       int inverse, hipStream_t s);
 
+// ------------------------------------------------------------ loader -----
+// Chunk j is filled into ring buffer j % R by whichever loader thread takes
+// it (threads take chunks in ascending order), once the chunk R before it
+// has left that buffer.  The calling thread pushes chunk j once it is
+// filled; push_chunk(j) returns only after chunk j - 1's copy to the device
+// is done (stage_host_chunk), which releases chunk j - 1's buffer.
+struct HostRing {
+    void* p = nullptr;
+    ~HostRing() {
+        if (p) (void)hipHostFree(p);
+    }
+};
+
+static void stream_layer(taurus_layer* L, taurus_fill_fn fill, void* ctx, int threads, int ring,
+                         taurus_stream_stats* st) {
+    const auto t0 = std::chrono::steady_clock::now();
+    if (L->poisoned) fail(TAURUS_E_STATE, "layer handle is poisoned by an earlier failure");
+    if (!fill) fail(TAURUS_E_INVALID, "fill is null");
+    if (threads < 1 || threads > 64) fail(TAURUS_E_INVALID, "threads=%d outside [1, 64]", threads);
+    if (ring == 0) ring = 2 * threads;
+    if (ring < threads + 1 || ring > 256) fail(TAURUS_E_INVALID, "ring=%d outside [threads + 1, 256]", ring);
+    if (L->npushed != 0) fail(TAURUS_E_STATE, "the loader pushes every chunk; %lld were pushed before",
+                              (long long)L->npushed);
+    const int64_t nch = L->nchunks, C = L->C;
+    const size_t row = (size_t)L->d.d_in * (L->d.in_dtype == TAURUS_F32 ? 4 : 2);
+    const size_t slot = (size_t)std::min(C, L->n) * row;
+    HostRing buf;
+    if (hipHostMalloc(&buf.p, std::max<size_t>(1, slot) * (size_t)ring, hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        buf.p = nullptr;
+        fail(TAURUS_E_OOM, "pinned ring of %d x %zu bytes", ring, slot);
+    }
+    auto at = [&](int64_t j) { return static_cast<char*>(buf.p) + (size_t)(j % ring) * slot; };
+
+    std::mutex m;
+    std::condition_variable cv;
+    int64_t next = 0;                         // next chunk a loader thread takes
+    int64_t released = 0;                     // chunks [0, released) have left the ring
+    std::vector<int64_t> ready((size_t)ring, -1);  // chunk filled into each buffer
+    bool stop = false;
+    int64_t bad_chunk = -1;
+    int bad_rc = 0;
+    std::atomic<int64_t> fill_ns{0};
+    auto worker = [&]() {
+        for (;;) {
+            int64_t j;
+            {
+                std::unique_lock<std::mutex> lk(m);
+                cv.wait(lk, [&] { return stop || next >= nch || released > next - ring; });
+                if (stop || next >= nch) return;
+                j = next++;
+            }
+            const int64_t b = j * C, e = std::min(b + C, L->n);
+            const auto f0 = std::chrono::steady_clock::now();
+            const int rc = fill(ctx, b, e, at(j));
+            fill_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - f0)
+                           .count();
+            std::lock_guard<std::mutex> lk(m);
+            if (rc != 0) {
+                if (bad_chunk < 0) {
+                    bad_chunk = j;
+                    bad_rc = rc;
+                }
+                stop = true;
+            } else {
+                ready[(size_t)(j % ring)] = j;
+            }
+            cv.notify_all();
+        }
+    };
+    std::vector<std::thread> pool;
+    auto halt = [&]() {
+        {
+            std::lock_guard<std::mutex> lk(m);
+            stop = true;
+        }
+        cv.notify_all();
+        for (auto& t : pool) t.join();
+        pool.clear();
+    };
+    double wait_s = 0, push_s = 0;
+    try {
+        for (int i = 0; i < threads; i++) pool.emplace_back(worker);
+        for (int64_t j = 0; j < nch; j++) {
+            const auto w0 = std::chrono::steady_clock::now();
+            {
+                std::unique_lock<std::mutex> lk(m);
+                cv.wait(lk, [&] { return stop || ready[(size_t)(j % ring)] == j; });
+                if (ready[(size_t)(j % ring)] != j) break;  // a fill failed
+            }
+            const auto p0 = std::chrono::steady_clock::now();
+            wait_s += std::chrono::duration<double>(p0 - w0).count();
+            push_chunk(L, j * C, std::min(j * C + C, L->n), at(j), 1);
+            push_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - p0).count();
+            {  // chunk j - 1's copy is done: its buffer is free
+                std::lock_guard<std::mutex> lk(m);
+                if (j > 0) ready[(size_t)((j - 1) % ring)] = -1;
+                released = j;
+            }
+            cv.notify_all();
+        }
+        // the last chunk's copy leaves the ring before the ring is freed
+        for (int i = 0; i < 2; i++)
+            if (L->stage_used[i]) TAURUS_HIP(hipEventSynchronize(L->h2d_done[i]));
+    } catch (...) {
+        halt();
+        // copies from the ring may still be queued: let them finish before
+        // the ring is freed
+        if (L->copy_stream) (void)hipStreamSynchronize(L->copy_stream);
+        throw;
+    }
+    halt();
+    if (bad_chunk >= 0) {
+        L->poisoned = true;
+        fail(TAURUS_E_INVALID, "fill returned %d for chunk %lld", bad_rc, (long long)bad_chunk);
+    }
+    if (st) {
+        st->chunks = nch;
+        st->bytes = (int64_t)row * L->n;
+        st->fill_seconds = (double)fill_ns.load() * 1e-9;
+        st->wait_seconds = wait_s;
+        st->push_seconds = push_s;
+        st->wall_seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    }
+}
+
 // Runs an entry point's body: library failures become their status, any
 // other exception TAURUS_E_DEVICE; nothing crosses the C boundary.
 template <typename F>
@@ -2597,6 +2726,26 @@ int taurus_push_chunk(taurus_layer* L, int64_t src_begin, int64_t src_end, const
         if (f.status == TAURUS_E_OOM || f.status == TAURUS_E_DEVICE || f.status == TAURUS_E_BUDGET)
             L->poisoned = true;
         return f.status;
+    }
+}
+
+int taurus_stream_layer(taurus_layer* L, taurus_fill_fn fill, void* ctx, int32_t threads, int32_t ring,
+                        taurus_stream_stats* stats) {
+    if (!L) {
+        set_error("null layer handle");
+        return TAURUS_E_INVALID;
+    }
+    try {
+        stream_layer(L, fill, ctx, threads, ring, stats);
+        return TAURUS_OK;
+    } catch (const Failure& f) {
+        if (f.status == TAURUS_E_OOM || f.status == TAURUS_E_DEVICE || f.status == TAURUS_E_BUDGET)
+            L->poisoned = true;
+        return f.status;
+    } catch (const std::exception& x) {
+        L->poisoned = true;
+        set_error("internal error: %s", x.what());
+        return TAURUS_E_DEVICE;
     }
 }
 
