@@ -144,7 +144,8 @@ def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int, sage: bool) -> dict
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "layer.hip")
 GIB_KIB = float(1 << 20)
-WORKLOADS = ("sage3-fanout-rmat-100m", "gcn2-rmat-1m")
+WORKLOADS = ("sage3-fanout-rmat-100m", "gcn2-rmat-1m", "sage2-ooc-rmat-269m")
+LINK_PEAK_GBS = 64.0      # PCIe Gen5 x16, per direction
 
 
 def profile_path(workload: str) -> str:
@@ -319,10 +320,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 1, or 2 for gcn2-rmat-1m)")
     ap.add_argument("--workload", choices=WORKLOADS, default=WORKLOADS[0])
     ap.add_argument("--scale", type=int, default=1,
-                    help="sage3-fanout-rmat-100m only: divide vertices and edges by this (trial runs; not a result)")
+                    help="divide vertices and edges by this: trial runs of sage3-fanout-rmat-100m (not a result); "
+                         "sage2-ooc-rmat-269m needs 16 or more (its pinned host memory)")
     ap.add_argument("--chunk", type=int, default=0,
                     help="sage3-fanout-rmat-100m only: source chunk size (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--loader-threads", type=int, default=2,
+                    help="sage2-ooc-rmat-269m: loader threads (each fill spreads a chunk over the host cores)")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--full-profile", action="store_true",
                     help="events around every kernel (adds the transform's MFMA roofline; more events in the stream)")
@@ -335,7 +339,7 @@ def main():
                          "kernel-trace run and FETCH_SIZE / WRITE_SIZE (and matrix-core counter) runs")
     args = ap.parse_args()
     if args.summarize_profile:
-        if len(args.summarize_profile) not in (4, 5) or args.summarize_profile[0] not in WORKLOADS:
+        if len(args.summarize_profile) not in (4, 5) or args.summarize_profile[0] not in WORKLOADS[:2]:
             raise SystemExit("--summarize-profile WORKLOAD TRACE_DIR FETCH_DIR WRITE_DIR [MFMA_DIR]")
         print(summarize_profile(*args.summarize_profile))
         return
@@ -347,6 +351,13 @@ def main():
         args.steps = 10 if args.steps is None else args.steps
         args.warmup = 2 if args.warmup is None else args.warmup
         return bench_rmat_1m(args)
+    if args.workload == "sage2-ooc-rmat-269m":
+        args.steps = 2 if args.steps is None else args.steps
+        args.warmup = 1 if args.warmup is None else args.warmup
+        if args.scale < 16:
+            raise SystemExit("sage2-ooc-rmat-269m: --scale 16 or more (pinned host memory: at 1/16 both layers' "
+                             "outputs and the store for evicted rows already take 43 GB)")
+        return bench_ooc(args)
     args.steps = 3 if args.steps is None else args.steps
     args.warmup = 1 if args.warmup is None else args.warmup
     return bench_sage3_100m(args)
@@ -800,6 +811,194 @@ def bench_sage3_100m(args):
         "per_layer": layers,
         "roofline": roofline,
         "gemm_roofline": gemm,
+        "cpu_baseline": cpu,
+        "oracle_check": check,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def pinned_copy_gbs(dev, gib: int = 4) -> float:
+    """Plain pinned host-to-device copy rate (GB/s), the measured link ceiling."""
+    import torch
+    from paper_2607_17374_amd.api import alloc_pinned
+    h = alloc_pinned((gib << 30,), torch.uint8)
+    d = torch.empty(gib << 30, dtype=torch.uint8, device=dev)
+    d.copy_(h, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        d.copy_(h, non_blocking=True)
+    torch.cuda.synchronize()
+    rate = 3 * (gib << 30) / (time.perf_counter() - t0) / 1e9
+    del h, d
+    torch.cuda.empty_cache()
+    return rate
+
+
+def bench_ooc(args):
+    """sage2-ooc-rmat-269m at 1/scale: 2-layer GraphSAGE-mean 512 -> 256 ->
+    128 (fp32, U[-1, 1) features) on RMAT with 1% resident hubs, the
+    accumulators under the HBM budget scaled with the graph (eviction to
+    pinned host memory), 131,072-vertex chunks.  Layer 1's input is never
+    resident anywhere: the library's loader fills each chunk with the seeded
+    generator on host threads into a ring of pinned buffers while earlier
+    chunks copy and compute.  Layer 1 writes its output to pinned host
+    memory, which layer 2 streams back in (and writes its own there).  One
+    step = CSR build + both layers; roofline = the host link: the bytes
+    layer 1 moves over it per second of its streaming, against 64 GB/s."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import fixtures as F
+    from fixtures import workloads as WL
+    import paper_2607_17374_amd as T
+    from tests import harness as H
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t_start = time.perf_counter()
+
+    def say(msg):
+        print(f"[bench {time.perf_counter() - t_start:7.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    base = WL.SAGE_OOC_RMAT_269M
+    w = base.scaled(base.n // args.scale, base.e // args.scale, name=f"{base.name}-div{args.scale}")
+    w = dataclasses.replace(w, hbm_budget=base.hbm_budget // args.scale)
+    specs = H.layer_specs(w)
+    link = pinned_copy_gbs(dev)
+    say(f"pinned host-to-device copy {link:.1f} GB/s")
+    src, dst = WL.graph(w)
+    say(f"{w.name}: edge list {src.size} edges")
+    src_d = torch.from_numpy(src).to(dev)
+    dst_d = torch.from_numpy(dst).to(dev)
+    for _ in range(args.warmup):
+        row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+        del row_off, col_dst
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+    torch.cuda.synchronize()
+    csr_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    del src_d, dst_d
+    torch.cuda.empty_cache()
+    say(f"CSR build {csr_ms:.1f} ms")
+    outs = [T.api.alloc_pinned((w.n, sp["d_out"]), torch.float32) for sp in specs]
+    say("pinned outputs")
+    fill_fn, fill_ctx = F.feature_fill(w.seed, w.feat_dist, w.dims[0], F.F32)
+
+    def one_pass():
+        per = []
+        plan = T.Plan(w.n, row_off, col_dst, w.chunk)
+        for li, sp in enumerate(specs):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            L = T.Layer(w.n, row_off, col_dst, out=outs[li], chunk=w.chunk, plan=plan, hbm_budget=w.hbm_budget,
+                        hub_fraction=w.hub_fraction, **sp)
+            t1 = time.perf_counter()
+            if li == 0:
+                ls = L.stream(fill_fn, fill_ctx, threads=args.loader_threads)
+            else:
+                ls = None
+                L.push_all(outs[li - 1])
+            t2 = time.perf_counter()
+            st = L.finalize()
+            torch.cuda.synchronize()
+            t3 = time.perf_counter()
+            L.destroy()
+            st.update(init_s=t1 - t0, push_s=t2 - t1, layer_s=t3 - t0, stream_s=t3 - t1, loader=ls)
+            per.append(st)
+        plan.destroy()
+        return per
+
+    for _ in range(args.warmup):
+        one_pass()
+    t0 = time.perf_counter()
+    runs = [one_pass() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    layers_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_step = csr_ms + layers_ms
+    say(f"layers {layers_ms:.1f} ms per pass")
+    layers = []
+    for li in range(len(specs)):
+        sts = [r[li] for r in runs]
+        st = sts[-1]
+        mean = lambda k: float(np.mean([x[k] for x in sts]))
+        d = {"layer": li + 1, "d_in": specs[li]["d_in"], "d_out": specs[li]["d_out"], "edges": st["messages"],
+             "wall_ms": round(mean("layer_s") * 1e3, 1), "init_ms": round(mean("init_s") * 1e3, 1),
+             "gteps": round(st["messages"] / mean("layer_s") / 1e9, 4),
+             "h2d_gb": round(st["h2d_bytes"] / 1e9, 2), "d2h_gb": round(st["d2h_bytes"] / 1e9, 2),
+             "h2d_gbs": round(st["h2d_bytes"] / mean("stream_s") / 1e9, 2),
+             "d2h_gbs": round(st["d2h_bytes"] / mean("stream_s") / 1e9, 2),
+             "evictions": st["evictions"], "reloads": st["reloads"], "hub_message_share": st["hub_message_share"],
+             "device_gb": round(st["device_bytes"] / 1e9, 2), "input": "loader" if li == 0 else "pinned host"}
+        if st["loader"]:
+            lw = float(np.mean([x["loader"]["wall_seconds"] for x in sts]))
+            d["loader"] = {k: round(float(np.mean([x["loader"][k] for x in sts])), 3)
+                           for k in ("fill_seconds", "wait_seconds", "push_seconds", "wall_seconds")}
+            d["generator_gbs"] = round(st["loader"]["bytes"] / (d["loader"]["fill_seconds"] / args.loader_threads)
+                                       / 1e9, 2)
+            d["loader_gbs"] = round(st["loader"]["bytes"] / lw / 1e9, 2)
+        layers.append(d)
+    total_edges = sum(l["edges"] for l in layers)
+    value = total_edges / (ms_step * 1e-3) / 1e9
+    l1 = runs[-1][0]
+    stream_s = float(np.mean([r[0]["stream_s"] for r in runs]))
+    achieved = l1["h2d_bytes"] / stream_s / 1e9
+    waited = layers[0]["loader"]["wait_seconds"]
+    roofline = {"bound": "host-link", "achieved": round(achieved, 2), "peak": LINK_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / LINK_PEAK_GBS, 4), "traffic": None, "kernel": "host-to-device chunk copies",
+                "measured_pinned_copy_gbs": round(link, 2), "frac_of_measured": round(achieved / link, 4),
+                "d2h_gbs": layers[0]["d2h_gbs"],
+                "note": "layer 1: every chunk generated on host threads and copied while earlier chunks compute; "
+                        f"the pushing thread waited {waited:.2f} s of {stream_s:.2f} s for the generator"}
+
+    check = cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as O
+        t0 = time.perf_counter()
+        g = O.EdgeGraph(w.n, src, dst)
+        t_lists = time.perf_counter() - t0
+        del src, dst
+        ids = [destination_sample(w.seed * 1000 + li, g.deg_in) for li in range(1, w.layers + 1)]
+        need1 = np.unique(np.concatenate([ids[0], ids[1], H.in_neighbours(g, ids[1])]))
+        need0 = np.unique(np.concatenate([need1, H.in_neighbours(g, need1)]))
+        X = np.zeros((w.n, w.dims[0]), np.float32)      # only the rows the oracle reads are touched
+        X[need0] = F.features_rows(w.seed, w.feat_dist, need0, w.dims[0])
+        say(f"oracle in-lists {t_lists:.1f} s; {need0.size} input rows")
+        t0 = time.perf_counter()
+        zs = H.oracle_sampled_layers(w, g, X, ids)
+        t_or = time.perf_counter() - t0
+        check = []
+        for li, z in enumerate(zs, start=1):
+            y = outs[li - 1].numpy()[ids[li - 1]].astype(np.float64)
+            r = H.compare(y, z, H.RTOL[F.F32])
+            check.append({"layer": li, "destinations": int(len(ids[li - 1])), "mismatches": r["n_bad"],
+                          "max_abs": r["max_abs"], "mean_rel": r["mean_rel"]})
+            say(f"oracle layer {li}: mismatches {r['n_bad']} of {len(ids[li - 1])}")
+        rows = need0.size + need1.size
+        t_extrap = t_lists + t_or * (w.n * w.layers) / rows
+        cpu = {"value": round(total_edges / t_extrap / 1e9, 6), "unit": "GTEPS", "cores": O.threads(),
+               "kind": "oracle", "cpu_model": _cpu_model(), "seconds": round(t_lists + t_or, 2),
+               "extrapolated_full_step_s": round(t_extrap, 1),
+               "sample": f"in-lists over the whole graph ({t_lists:.1f} s), then both layers at {rows} rows (the "
+                         "65,536 seeded destinations, the 256 largest in-degrees and up to 256 without in-edges per "
+                         f"layer, and the layer-1 rows layer 2 reads) ({t_or:.2f} s); value = both layers' "
+                         f"{total_edges / 1e6:.0f}M edges / the step extrapolated linearly in rows (extrapolated)"}
+
+    line = {
+        "metric": METRIC, "value": round(value, 4), "unit": "GTEPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: 2-layer GraphSAGE-mean 512->256->128, fp32, U[-1,1) features; "
+                               f"RMAT(0.57,0.19,0.19) {w.n:,} vertices / {w.e:,} edges; {w.chunk:,}-vertex chunks; "
+                               f"HBM budget {w.hbm_budget / 1e9:.0f} GB with 1% resident hubs; layer-1 chunks "
+                               "generated on host threads by the library's loader, outputs in pinned host memory; "
+                               "step = CSR build + both layers",
+                   "n": w.n, "e": w.e, "chunk": w.chunk, "scale": f"1/{args.scale}", "csr_ms": round(csr_ms, 3),
+                   "layers_ms": round(layers_ms, 3), "loader_threads": args.loader_threads},
+        "per_layer": layers,
+        "roofline": roofline,
         "cpu_baseline": cpu,
         "oracle_check": check,
     }

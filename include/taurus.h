@@ -236,8 +236,10 @@ typedef struct {
  * hands cached blocks of the current device back to the runtime, smallest
  * first, until at least `bytes` bytes are freed (bytes <= 0: all of them),
  * for a caller whose own allocation ran out of memory.  Blocks in use are
- * not touched.  Synchronises the device.  Returns the bytes freed, or a
- * negative status.
+ * not touched.  Large pinned host buffers (budgeted layers' stores for
+ * evicted rows, the chunk loader's rings) are cached the same way; this
+ * call frees every cached one of them too.  Synchronises the device.
+ * Returns the device bytes freed, or a negative status.
  */
 int64_t taurus_release_cached_memory(int64_t bytes);
 
@@ -472,8 +474,9 @@ int taurus_layer_reload_histogram(taurus_layer* L, int64_t* counts, int32_t bins
  * It is called from `threads` loader threads at once (1 .. 64), for
  * different chunks, and must be safe for that.  `ring` pinned buffers of
  * one chunk each (threads + 1 .. 256; 0 picks 2 * threads) hold chunks
- * being filled, filled and waiting, or copying; the ring is allocated per
- * call and freed before return.
+ * being filled, filled and waiting, or copying; the ring comes from the
+ * library's cache of pinned host buffers (taurus_release_cached_memory)
+ * and goes back to it before return.
  *
  * Pushes every chunk of the layer; no chunk may have been pushed before
  * (TAURUS_E_STATE).  Returns when the last chunk is queued and every copy

@@ -181,6 +181,32 @@ def alloc_device(shape, dtype, device) -> torch.Tensor:
         return torch.empty(shape, dtype=dtype, device=device)
 
 
+_hip = None
+
+
+def alloc_pinned(shape, dtype) -> torch.Tensor:
+    """Pinned host tensor of exactly this size (hipHostMalloc; torch's pinned
+    allocator rounds large blocks up to a power of two, which matters where
+    pinned memory is capped).  Freed when the last tensor viewing it goes."""
+    import weakref
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipHostMalloc.restype = ctypes.c_int
+        _hip.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t, ctypes.c_uint]
+        _hip.hipHostFree.restype = ctypes.c_int
+        _hip.hipHostFree.argtypes = [ctypes.c_void_p]
+    nbytes = max(1, int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size())
+    p = ctypes.c_void_p()
+    rc = _hip.hipHostMalloc(ctypes.byref(p), nbytes, 0)
+    if rc != 0 or not p.value:
+        raise MemoryError(f"hipHostMalloc({nbytes}) failed ({rc})")
+    buf = (ctypes.c_uint8 * nbytes).from_address(p.value)
+    weakref.finalize(buf, _hip.hipHostFree, p.value)
+    t = torch.frombuffer(buf, dtype=torch.uint8)
+    return t[:nbytes].view(dtype).view(shape) if shape else t.view(dtype)
+
+
 # eviction policies of a budgeted layer (taurus_eviction)
 EVICTION = {"pending": N.EVICT_PENDING, "random": N.EVICT_RANDOM, "fifo": N.EVICT_FIFO, "lru": N.EVICT_LRU}
 

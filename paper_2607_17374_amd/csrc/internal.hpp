@@ -49,6 +49,13 @@ void device_release(void* p, hipStream_t s);
 // until at least `bytes` are freed (0: all); returns the bytes freed
 size_t release_cached(size_t bytes);
 
+// Large pinned host buffers from a process-wide cache: a block of at least
+// `bytes` (*cap receives its size), given back with pinned_return(p, cap)
+// once nothing reads it; release_pinned frees every cached block.
+void* pinned_acquire(size_t bytes, size_t* cap);
+void pinned_return(void* p, size_t cap);
+size_t release_pinned();
+
 // Pinned host buffer of at least `bytes` for the calling thread (reused by
 // its next call, which first waits for a transfer left in flight by
 // pinned_staging_in_flight).

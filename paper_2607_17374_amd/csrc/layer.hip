@@ -2425,11 +2425,10 @@ int permute_rows_impl(const void* in, void* out, int64_t n, int64_t row_bytes, c
 // has left that buffer.  The calling thread pushes chunk j once it is
 // filled; push_chunk(j) returns only after chunk j - 1's copy to the device
 // is done (stage_host_chunk), which releases chunk j - 1's buffer.
-struct HostRing {
+struct HostRing {  // from the pinned block cache
     void* p = nullptr;
-    ~HostRing() {
-        if (p) (void)hipHostFree(p);
-    }
+    size_t cap = 0;
+    ~HostRing() { pinned_return(p, cap); }
 };
 
 static void stream_layer(taurus_layer* L, taurus_fill_fn fill, void* ctx, int threads, int ring,
@@ -2446,11 +2445,7 @@ static void stream_layer(taurus_layer* L, taurus_fill_fn fill, void* ctx, int th
     const size_t row = (size_t)L->d.d_in * (L->d.in_dtype == TAURUS_F32 ? 4 : 2);
     const size_t slot = (size_t)std::min(C, L->n) * row;
     HostRing buf;
-    if (hipHostMalloc(&buf.p, std::max<size_t>(1, slot) * (size_t)ring, hipHostMallocDefault) != hipSuccess) {
-        (void)hipGetLastError();
-        buf.p = nullptr;
-        fail(TAURUS_E_OOM, "pinned ring of %d x %zu bytes", ring, slot);
-    }
+    buf.p = pinned_acquire(std::max<size_t>(1, slot) * (size_t)ring, &buf.cap);
     auto at = [&](int64_t j) { return static_cast<char*>(buf.p) + (size_t)(j % ring) * slot; };
 
     std::mutex m;
@@ -2794,6 +2789,7 @@ int taurus_sampled_edges(taurus_layer* L, uint64_t* mask_bits_host, int64_t* n_k
 
 int64_t taurus_release_cached_memory(int64_t bytes) {
     try {
+        release_pinned();
         return (int64_t)release_cached(bytes <= 0 ? 0 : (size_t)bytes);
     } catch (const Failure& f) {
         return f.status;

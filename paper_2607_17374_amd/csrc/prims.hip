@@ -214,6 +214,64 @@ void device_release(void* p, hipStream_t s) {
     c.free_lists[{info.dev, info.cls}].push_back(FreeBlock{p, s});
 }
 
+// ---------------------------------------------------------- pinned blocks --
+// Large pinned host buffers (the residency store for evicted rows, the chunk
+// loader's ring) come from a cache as device memory does: pinning tens of
+// GB costs seconds, and the next layer usually needs the same size.  A
+// request takes the smallest free block at least as large.
+namespace {
+struct PinnedCache {
+    std::mutex mu;
+    std::multimap<size_t, void*> free;
+};
+PinnedCache& pinned_cache() {
+    static PinnedCache* c = new PinnedCache;  // outlives every static destructor
+    return *c;
+}
+}  // namespace
+
+void* pinned_acquire(size_t bytes, size_t* cap) {
+    bytes = std::max<size_t>(bytes, 1);
+    {
+        PinnedCache& c = pinned_cache();
+        std::lock_guard<std::mutex> g(c.mu);
+        auto it = c.free.lower_bound(bytes);
+        if (it != c.free.end()) {
+            void* p = it->second;
+            *cap = it->first;
+            c.free.erase(it);
+            return p;
+        }
+    }
+    void* p = nullptr;
+    const hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        fail(TAURUS_E_OOM, "pinned host allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+    }
+    *cap = bytes;
+    return p;
+}
+
+void pinned_return(void* p, size_t cap) {
+    if (!p) return;
+    PinnedCache& c = pinned_cache();
+    std::lock_guard<std::mutex> g(c.mu);
+    c.free.emplace(cap, p);
+}
+
+size_t release_pinned() {
+    PinnedCache& c = pinned_cache();
+    std::lock_guard<std::mutex> g(c.mu);
+    size_t total = 0;
+    for (auto& kv : c.free) {
+        (void)hipHostFree(kv.second);
+        total += kv.first;
+    }
+    c.free.clear();
+    return total;
+}
+
 // ------------------------------------------------------------ pinned staging --
 // One pinned host buffer per host thread for small transfers, grown on demand
 // and kept until the process ends.  An asynchronous transfer still reading

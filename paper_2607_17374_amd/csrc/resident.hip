@@ -319,13 +319,13 @@ Residency::Residency(hipStream_t s, int64_t n_, int d_o_, int64_t slots, int64_t
     rb.run(s);
     hub_share = messages > 0 ? (double)hub_msgs / (double)messages : 0.0;
     // host store for evicted rows: pinned, written and read by kernels only
-    TAURUS_HIP(hipHostMalloc(&store_host, (size_t)n * d_o * sizeof(float), hipHostMallocDefault));
+    store_host = static_cast<float*>(pinned_acquire((size_t)n * d_o * sizeof(float), &store_cap));
     TAURUS_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&store_dev), store_host, 0));
 }
 
 Residency::~Residency() {
     (void)hipDeviceSynchronize();
-    if (store_host) (void)hipHostFree(store_host);
+    pinned_return(store_host, store_cap);
 }
 
 void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream_t s) {

@@ -60,7 +60,8 @@ private:
     unsigned int* hist = nullptr;
     unsigned long long* counters = nullptr;  // [0] listed, [1] victims, [2] reloads, [3] hub messages
     int32_t *free_list = nullptr, *free_top = nullptr;
-    float* store_host = nullptr;  // pinned [n][d_o]
+    float* store_host = nullptr;  // pinned [n][d_o] (from the pinned block cache)
+    size_t store_cap = 0;
     float* store_dev = nullptr;   // the same memory as seen by kernels
 };
 
