@@ -247,6 +247,66 @@ WORKLOAD_TITLE = {
 }
 
 
+OOC_PROFILE_SCALE = 16
+
+
+def copy_profile_command() -> str:
+    return ("rocprofv3 --memory-copy-trace --kernel-trace --stats --output-format csv -d gpurun_out/prof_c4 -o c4 -- "
+            f"python3 bench.py --workload {WORKLOADS[2]} --scale {OOC_PROFILE_SCALE} --steps 2 --warmup 1 "
+            "--no-cpu-baseline")
+
+
+def summarize_copies(trace_dir: str) -> str:
+    """Host-link summary of the out-of-core bench from a memory-copy trace:
+    each layer's chunk copies run on that layer's own copy stream, so the
+    streams in order of their first copy alternate layer 1, layer 2 (one
+    pair per pass); each streams the layer's whole input once."""
+    import csv
+    import glob
+    from fixtures import workloads as WL
+    base = WL.SAGE_OOC_RMAT_269M
+    n = base.n // OOC_PROFILE_SCALE
+    tr = glob.glob(os.path.join(trace_dir, "**", "*memory_copy_trace.csv"), recursive=True)
+    ks = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not tr or not ks:
+        raise SystemExit(f"no memory-copy trace or kernel stats under {trace_dir}")
+    rows = [r for r in csv.DictReader(open(tr[0])) if r["Direction"] == "MEMORY_COPY_HOST_TO_DEVICE"]
+    by = {}
+    for r in rows:
+        by.setdefault(r["Stream_Id"], []).append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    copy_streams = sorted((v for k, v in by.items() if k != "0"), key=lambda v: min(a for a, _ in v))
+    out = [f"# Host link on {WORKLOADS[2]} at 1/{OOC_PROFILE_SCALE} ({n:,} vertices, {base.e // OOC_PROFILE_SCALE:,} "
+           "edges, 131,072-vertex chunks)", "",
+           "Command, from the repository root on one MI355X:", "", "    " + copy_profile_command(),
+           f"    python3 bench.py --summarize-copies gpurun_out/prof_c4", "",
+           "Layer 1's chunks are filled by the library's loader (the seeded generator on host threads) and copied "
+           "on layer 1's copy stream; layer 2 streams layer 1's output back from pinned host memory on its own "
+           "copy stream.  Each stream carries its layer's whole input once (n x d_in x 4 bytes).  Engine rate = "
+           "bytes / summed copy durations; effective rate = bytes / (first copy start to last copy end).  "
+           "Nominal link: 64 GB/s per direction (PCIe Gen5 x16).", "",
+           "| pass | layer | copies | GB | summed copy ms | engine GB/s | span ms | effective GB/s | of 64 GB/s |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for k, v in enumerate(copy_streams):
+        layer = k % 2 + 1
+        d_in = base.dims[layer - 1]
+        gb = n * d_in * 4 / 1e9
+        busy = sum(b - a for a, b in v) / 1e6
+        span = (max(b for _, b in v) - min(a for a, _ in v)) / 1e6
+        out.append(f"| {k // 2 + 1}{' (warm-up)' if k < 2 else ''} | {layer} | {len(v)} | {gb:.2f} | {busy:.1f} | "
+                   f"{gb / busy * 1e3:.1f} | {span:.1f} | {gb / span * 1e3:.1f} | {gb / span * 1e3 / 64:.3f} |")
+    cal = sorted(by.get("0", []), key=lambda t: t[1] - t[0], reverse=True)[:3]
+    if cal:
+        ms = sum(b - a for a, b in cal) / len(cal) / 1e6
+        out += ["", f"Plain pinned copy of 4 GiB on the default stream (the bench's link calibration), mean of "
+                    f"{len(cal)}: {ms:.1f} ms = {(4 << 30) / ms / 1e6:.1f} GB/s."]
+    krow = list(csv.DictReader(open(ks[0])))
+    out += ["", "## Kernel time (same run)", "", "| kernel | calls | total ms | average us |", "|---|---|---|---|"]
+    for r in krow[:12]:
+        out.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} |")
+    return "\n".join(out)
+
+
 def summarize_profile(workload: str, trace_dir: str, fetch_dir: str, write_dir: str, mfma_dir: str = None) -> str:
     import csv
     import glob
@@ -337,7 +397,12 @@ def main():
     ap.add_argument("--summarize-profile", nargs="+", metavar="ARG",
                     help="WORKLOAD TRACE_DIR FETCH_DIR WRITE_DIR [MFMA_DIR]: print the profile summary of a "
                          "kernel-trace run and FETCH_SIZE / WRITE_SIZE (and matrix-core counter) runs")
+    ap.add_argument("--summarize-copies", metavar="TRACE_DIR",
+                    help="print the host-link summary of a memory-copy trace of the out-of-core bench")
     args = ap.parse_args()
+    if args.summarize_copies:
+        print(summarize_copies(args.summarize_copies))
+        return
     if args.summarize_profile:
         if len(args.summarize_profile) not in (4, 5) or args.summarize_profile[0] not in WORKLOADS[:2]:
             raise SystemExit("--summarize-profile WORKLOAD TRACE_DIR FETCH_DIR WRITE_DIR [MFMA_DIR]")
