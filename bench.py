@@ -144,7 +144,7 @@ def kernel_bytes(fm: dict, n: int, d_o: int, out_bytes: int, sage: bool) -> dict
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_17374_amd", "csrc", "layer.hip")
 GIB_KIB = float(1 << 20)
-WORKLOADS = ("sage3-fanout-rmat-100m", "gcn2-rmat-1m", "sage2-ooc-rmat-269m")
+WORKLOADS = ("sage3-fanout-rmat-100m", "gcn2-rmat-1m", "sage2-ooc-rmat-269m", "gcn2-skew-rmat-50m")
 LINK_PEAK_GBS = 64.0      # PCIe Gen5 x16, per direction
 
 
@@ -214,6 +214,7 @@ def profiled_traffic(workload: str):
 
 def _short_name(name: str) -> str:
     import re
+    name = name.replace("(anonymous namespace)::", "")
     return re.sub(r"\(.*", "", name).replace("void ", "").strip()
 
 
@@ -304,6 +305,46 @@ def summarize_copies(trace_dir: str) -> str:
     for r in krow[:12]:
         out.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
                    f"{float(r['AverageNs']) / 1e3:.1f} |")
+    return "\n".join(out)
+
+
+def c5_profile_command() -> str:
+    return ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_c5 -o c5 -- "
+            f"python3 bench.py --workload {WORKLOADS[3]} --steps 1 --warmup 1")
+
+
+def summarize_reorder(trace_dir: str) -> str:
+    """Kernel-time summary of the reordered skewed GCN bench: every
+    kernel, and the Alg. 1 kernels (k_ta_*) and the degree/BFS kernels
+    grouped."""
+    import csv
+    import glob
+    ks = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not ks:
+        raise SystemExit(f"no kernel stats under {trace_dir}")
+    rows = list(csv.DictReader(open(ks[0])))
+    out = [f"# Reordering kernels (Alg. 1, degree/BFS, RCMK) on {WORKLOADS[3]} (50M vertices, 1B edges, "
+           "random IDs)", "",
+           "Command, from the repository root on one MI355X:", "", "    " + c5_profile_command(),
+           "    python3 bench.py --summarize-reorder gpurun_out/prof_c5", "",
+           "The run makes two steps (one warm-up) of: CSR build, degree/BFS order, Alg. 1 from it (5 updates), "
+           "relabel, both GCN layers; then each ordering once on its own (degree/BFS and RCMK, Alg. 1 from each "
+           "with 5 updates), with the layers in each.  Alg. 1 therefore runs 4 times (20 updates), the degree/BFS "
+           "order 3 times and RCMK once.", ""]
+    ta = ("k_sum_short", "k_sum_piece", "k_sum_combine", "k_rank_short", "k_rank_piece", "k_rank_combine",
+          "k_sum_terms", "k_ta_")
+    groups = {"Alg. 1 kernels (sums, ranks, positions; its position sort is counted with the radix sorts)":
+              lambda k: any(x in k for x in ta),
+              "radix sorts (CSR builds, relabelling, Alg. 1's position sort, indexes)": lambda k: "k_radix" in k}
+    out += ["| group | calls | total ms |", "|---|---|---|"]
+    for g, pred in groups.items():
+        sel = [r for r in rows if pred(r["Name"])]
+        out.append(f"| {g} | {sum(int(r['Calls']) for r in sel)} | "
+                   f"{sum(float(r['TotalDurationNs']) for r in sel) / 1e6:.1f} |")
+    out += ["", "| kernel | calls | total ms | average us | % |", "|---|---|---|---|---|"]
+    for r in rows[:40]:
+        out.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['Percentage']):.1f} |")
     return "\n".join(out)
 
 
@@ -399,7 +440,12 @@ def main():
                          "kernel-trace run and FETCH_SIZE / WRITE_SIZE (and matrix-core counter) runs")
     ap.add_argument("--summarize-copies", metavar="TRACE_DIR",
                     help="print the host-link summary of a memory-copy trace of the out-of-core bench")
+    ap.add_argument("--summarize-reorder", metavar="TRACE_DIR",
+                    help="print the kernel summary of a trace of the reordered skewed GCN bench")
     args = ap.parse_args()
+    if args.summarize_reorder:
+        print(summarize_reorder(args.summarize_reorder))
+        return
     if args.summarize_copies:
         print(summarize_copies(args.summarize_copies))
         return
@@ -416,6 +462,10 @@ def main():
         args.steps = 10 if args.steps is None else args.steps
         args.warmup = 2 if args.warmup is None else args.warmup
         return bench_rmat_1m(args)
+    if args.workload == "gcn2-skew-rmat-50m":
+        args.steps = 3 if args.steps is None else args.steps
+        args.warmup = 1 if args.warmup is None else args.warmup
+        return bench_c5(args)
     if args.workload == "sage2-ooc-rmat-269m":
         args.steps = 2 if args.steps is None else args.steps
         args.warmup = 1 if args.warmup is None else args.warmup
@@ -878,6 +928,139 @@ def bench_sage3_100m(args):
         "gemm_roofline": gemm,
         "cpu_baseline": cpu,
         "oracle_check": check,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_c5(args):
+    """gcn2-skew-rmat-50m: 2-layer GCN 256 -> 256 -> 64 (fp16 storage, fp32
+    accumulation) on a skewed RMAT(0.65, 0.15, 0.15) graph with 50M vertices
+    and 1B edges in random vertex IDs, reordered before the layers.  One
+    step = CSR build + degree/BFS order + Alg. 1 (5 updates of the
+    topology-aware order from it) + relabelling the graph and permuting the
+    features + both layers in the new IDs.  Beside the step: each ordering
+    (random IDs, degree/BFS, RCMK, Alg. 1 from either) timed on its own with
+    the layers' time in that order, its total edge span C(pi) and
+    dispersion J(pi)."""
+    import numpy as np
+    import torch
+    from fixtures import workloads as WL
+    import paper_2607_17374_amd as T
+    from paper_2607_17374_amd.api import torch_dtype
+    from tests import harness as H
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t_start = time.perf_counter()
+
+    def say(msg):
+        print(f"[bench {time.perf_counter() - t_start:7.1f}s] {msg}", file=sys.stderr, flush=True)
+
+    w = WL.GCN_SKEW_RMAT_50M
+    if args.scale > 1:
+        w = w.scaled(w.n // args.scale, w.e // args.scale)
+    specs = H.layer_specs(w)
+    src, dst = WL.graph(w)
+    say(f"{w.name}: edge list {src.size} edges (random IDs)")
+    xh = WL.input_features(w)
+    X = torch.from_numpy(xh.view(np.int16)).to(dev).view(torch_dtype(w.feat_dtype))
+    del xh
+    src_d = torch.from_numpy(src).to(dev)
+    dst_d = torch.from_numpy(dst).to(dev)
+    del src, dst
+    outs = [T.alloc_device((w.n, sp["d_out"]), torch_dtype(sp["out_dtype"]), dev) for sp in specs]
+
+    def sync_ms(t0):
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3
+
+    def layers(row_off, col_dst, x):
+        t0 = time.perf_counter()
+        plan = T.Plan(w.n, row_off, col_dst, w.chunk)
+        h = x
+        for li, sp in enumerate(specs):
+            L = T.Layer(w.n, row_off, col_dst, out=outs[li], chunk=w.chunk, plan=plan, **sp)
+            L.push_all(h)
+            L.finalize()
+            L.destroy()
+            h = outs[li]
+        plan.destroy()
+        return sync_ms(t0)
+
+    def step():
+        t = {}
+        t0 = time.perf_counter()
+        row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+        t["csr_ms"] = sync_ms(t0)
+        t0 = time.perf_counter()
+        pi0 = T.reorder(w.n, row_off, col_dst)
+        t["bfs_ms"] = sync_ms(t0)
+        t0 = time.perf_counter()
+        ta = T.reorder_ta(w.n, row_off, col_dst, pi0, 5)
+        t["alg1_ms"] = sync_ms(t0)
+        t0 = time.perf_counter()
+        r2, c2 = T.relabel_graph(w.n, row_off, col_dst, ta.pi)
+        x2 = T.permute_rows(X, ta.pi)
+        t["relabel_ms"] = sync_ms(t0)
+        del row_off, col_dst
+        t["layers_ms"] = layers(r2, c2, x2)
+        return t, ta
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    runs = [step() for _ in range(args.steps)]
+    ms_step = sync_ms(t0) / args.steps
+    phases = {k: round(float(np.mean([r[0][k] for r in runs])), 2) for k in runs[0][0]}
+    ta = runs[-1][1]
+    say(f"step {ms_step:.1f} ms: {phases}")
+
+    # each ordering on its own: its time, the layers' time in it, C(pi), J(pi)
+    row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
+    orders = []
+    ident = torch.arange(w.n, dtype=torch.int32, device=dev)
+    base = T.reorder_ta(w.n, row_off, col_dst, ident, 1)   # index 0: C and J of the identity
+    orders.append({"order": "random IDs", "order_ms": 0.0, "span": int(base.spans[0]), "J": float(base.disp[0]),
+                   "layers_ms": round(layers(row_off, col_dst, X), 1)})
+    for label, fn in (("degree/BFS", T.reorder), ("RCMK", T.reorder_rcm)):
+        t0 = time.perf_counter()
+        pi = fn(w.n, row_off, col_dst)
+        o_ms = sync_ms(t0)
+        t0 = time.perf_counter()
+        got = T.reorder_ta(w.n, row_off, col_dst, pi, 5)
+        ta_ms = sync_ms(t0)
+        for name, perm, ms, sp, dj in ((label, pi, o_ms, int(got.spans[0]), float(got.disp[0])),
+                                       (f"Alg. 1 from {label} (5 updates)", got.pi, o_ms + ta_ms,
+                                        int(got.spans[got.done]), float(got.disp[got.done]))):
+            r2, c2 = T.relabel_graph(w.n, row_off, col_dst, perm)
+            x2 = T.permute_rows(X, perm)
+            orders.append({"order": name, "order_ms": round(ms, 1), "span": sp, "J": dj,
+                           "layers_ms": round(layers(r2, c2, x2), 1)})
+            if name.startswith("Alg. 1"):
+                orders[-1]["alg1_ms"] = round(ta_ms, 1)
+                orders[-1]["updates"] = int(got.done)
+                orders[-1]["spans_per_update"] = [int(x) for x in got.spans[:got.done + 1]]
+                orders[-1]["J_per_update"] = [float(x) for x in got.disp[:got.done + 1]]
+            del r2, c2, x2
+            torch.cuda.empty_cache()
+        say(f"{label}: {orders[-2]} / {orders[-1]['order']} {orders[-1]['order_ms']} ms")
+    edges = 2 * w.e
+    line = {
+        "metric": METRIC, "value": round(edges / (ms_step * 1e-3) / 1e9, 4), "unit": "GTEPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: 2-layer GCN 256->256->64, fp16 storage, fp32 accumulation; skewed "
+                               f"RMAT(0.65,0.15,0.15) {w.n:,} vertices / {w.e:,} edges in random IDs; "
+                               f"{w.chunk:,}-vertex chunks; step = CSR build + degree/BFS order + Alg. 1 "
+                               "(5 updates) + relabel + both layers",
+                   "n": w.n, "e": w.e, "chunk": w.chunk, "phases_ms": phases,
+                   **({"scale": f"1/{args.scale}"} if args.scale > 1 else {})},
+        "alg1": {"updates": int(ta.done), "spans": [int(x) for x in ta.spans[:ta.done + 1]],
+                 "J": [float(x) for x in ta.disp[:ta.done + 1]], "ms": phases["alg1_ms"]},
+        "orders": orders,
+        "roofline": None,
+        "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
 

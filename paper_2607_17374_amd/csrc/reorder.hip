@@ -101,9 +101,22 @@ __global__ void k_label_jump(const uint32_t* __restrict__ order, int64_t n, int3
     }
 }
 
+// size[l] = vertices labelled l.  Lanes of a wave with the same label add
+// once (a giant component would otherwise put nearly every vertex's atomic
+// on one counter): the first remaining lane's label is matched by ballot,
+// that lane adds the matches, and the rest go round again.
 __global__ void k_tree_sizes(const int32_t* __restrict__ label, int64_t n, int32_t* __restrict__ size) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (v < n) atomicAdd(&size[label[v]], 1);
+    const int lane = threadIdx.x & 63;
+    const int32_t l = v < n ? label[v] : -1;
+    uint64_t left = __ballot(v < n);
+    while (left) {  // uniform over the wave
+        const int lead = __builtin_ctzll(left);
+        const int32_t ll = __shfl(l, lead);
+        const uint64_t same = __ballot(v < n && l == ll);
+        if (lane == lead) atomicAdd(&size[ll], (int)__popcll(same));
+        left &= ~same;
+    }
 }
 
 // roots: pos = the first slot of their tree; they form the first frontier
