@@ -166,34 +166,51 @@ __global__ __launch_bounds__(256) void k_res_evict(const int32_t* __restrict__ v
 
 // one wave per listed vertex: take slot free_list[top - 1 - j] at chunk k;
 // reload if evicted
-__global__ __launch_bounds__(256) void k_res_assign(const int32_t* __restrict__ need, int64_t nn, int d_o,
-                                                    const int32_t* __restrict__ free_list, int64_t top, int32_t k,
+// A wave per listed destination (waves stride over the list): take the
+// free slot top - 1 - j, reloading the row if it was evicted.  nn and top
+// come from the host (nn_dev null) or from device memory (the listed count
+// and the free-list top), for a launch sized for the most the chunk can
+// list.
+__global__ __launch_bounds__(256) void k_res_assign(const int32_t* __restrict__ need, int64_t nn,
+                                                    const unsigned long long* __restrict__ nn_dev, int d_o,
+                                                    const int32_t* __restrict__ free_list, int64_t top,
+                                                    const int32_t* __restrict__ top_dev, int32_t k,
                                                     float* __restrict__ pool, const float* __restrict__ store,
                                                     int32_t* __restrict__ slot_of, uint8_t* __restrict__ evicted,
                                                     int32_t* __restrict__ want, int32_t* __restrict__ adm,
                                                     int32_t* __restrict__ reloads_of,
                                                     unsigned long long* __restrict__ reloads) {
-    const int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
-    if (j >= nn) return;
-    const int v = need[j];
-    const int32_t s = free_list[top - 1 - j];
-    if (evicted[v]) {
-        const float4* src = reinterpret_cast<const float4*>(store + (int64_t)v * d_o);
-        float4* dst = reinterpret_cast<float4*>(pool + (int64_t)s * d_o);
-        for (int q = lane; q < d_o / 4; q += 64) dst[q] = src[q];
+    if (nn_dev) {
+        nn = (int64_t)*nn_dev;
+        top = *top_dev;
     }
-    __builtin_amdgcn_wave_barrier();
-    if (lane == 0) {
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t j = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6; j < nn; j += nw) {  // uniform
+        const int v = need[j];
+        const int32_t s = free_list[top - 1 - j];
         if (evicted[v]) {
-            evicted[v] = 0;
-            reloads_of[v] += 1;
-            atomicAdd(reloads, 1ull);
+            const float4* src = reinterpret_cast<const float4*>(store + (int64_t)v * d_o);
+            float4* dst = reinterpret_cast<float4*>(pool + (int64_t)s * d_o);
+            for (int q = lane; q < d_o / 4; q += 64) dst[q] = src[q];
         }
-        slot_of[v] = s;
-        adm[v] = k;
-        want[v] = 0;
+        __builtin_amdgcn_wave_barrier();
+        if (lane == 0) {
+            if (evicted[v]) {
+                evicted[v] = 0;
+                reloads_of[v] += 1;
+                atomicAdd(reloads, 1ull);
+            }
+            slot_of[v] = s;
+            adm[v] = k;
+            want[v] = 0;
+        }
     }
+}
+
+// free-list top after a device-counted assignment: *top -= listed
+__global__ void k_res_take(int32_t* __restrict__ top, const unsigned long long* __restrict__ listed) {
+    *top -= (int32_t)*listed;
 }
 
 // touched vertices that completed give their slot back (hub slots stay)
@@ -309,6 +326,7 @@ Residency::Residency(hipStream_t s, int64_t n_, int d_o_, int64_t slots, int64_t
     TAURUS_CHECK_LAUNCH();
     k_res_set<<<1, 1, 0, s>>>(free_top, (int32_t)(S - H));
     TAURUS_CHECK_LAUNCH();
+    free_lb = S - H;
     unsigned long long hub_msgs = 0;
     if (H > 0) {
         k_sum_hub_messages<<<nb, T, 0, s>>>(m, hub, n, counters + 3);
@@ -336,6 +354,21 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
     k_res_collect<<<(unsigned)ceil_div(std::max<int64_t>(total, 1), T), T, 0, s>>>(c, total, k, slot_of, cnt, dc_mark,
                                                                                   want, need, need_count);
     TAURUS_CHECK_LAUNCH();
+    // the chunk lists at most `total` destinations: with at least that many
+    // slots surely free, assign them without a readback
+    const int64_t grid_cap = 4096;  // workgroups of four waves, striding over the list
+    if (total <= free_lb) {
+        if (total > 0) {
+            k_res_assign<<<(unsigned)std::min<int64_t>(ceil_div(total, 4), grid_cap), T, 0, s>>>(
+                need, 0, need_count, d_o, free_list, 0, free_top, k, pool, store_dev, slot_of, evicted, want, adm,
+                reloads_of, counters + 2);
+            TAURUS_CHECK_LAUNCH();
+            k_res_take<<<1, 1, 0, s>>>(free_top, need_count);
+            TAURUS_CHECK_LAUNCH();
+        }
+        free_lb -= total;
+        return;
+    }
     unsigned long long nn = 0;
     int32_t top = 0;
     {
@@ -413,13 +446,14 @@ void Residency::prepare(const ResChunk& c, int32_t k, const int2* cnt, hipStream
         top += (int32_t)M;
     }
     if (nn > 0) {
-        k_res_assign<<<(unsigned)ceil_div((int64_t)nn * 64, T), T, 0, s>>>(need, (int64_t)nn, d_o, free_list, top, k,
-                                                                         pool, store_dev, slot_of, evicted, want,
-                                                                         adm, reloads_of, counters + 2);
+        k_res_assign<<<(unsigned)std::min<int64_t>(ceil_div((int64_t)nn, 4), grid_cap), T, 0, s>>>(
+            need, (int64_t)nn, nullptr, d_o, free_list, top, nullptr, k, pool, store_dev, slot_of, evicted, want,
+            adm, reloads_of, counters + 2);
         TAURUS_CHECK_LAUNCH();
         k_res_set<<<1, 1, 0, s>>>(free_top, top - (int32_t)nn);
         TAURUS_CHECK_LAUNCH();
     }
+    free_lb = (int64_t)top - (int64_t)nn;  // exact here
 }
 
 void Residency::release(const ResChunk& c, const int2* cnt, hipStream_t s) {

@@ -63,6 +63,11 @@ private:
     float* store_host = nullptr;  // pinned [n][d_o] (from the pinned block cache)
     size_t store_cap = 0;
     float* store_dev = nullptr;   // the same memory as seen by kernels
+    // a lower bound of the free slots, kept on the host: a chunk that
+    // touches at most this many destinations needs no eviction, so its slots
+    // are assigned without reading anything back (releases only raise the
+    // true count)
+    int64_t free_lb = 0;
 };
 
 }  // namespace taurus
