@@ -198,25 +198,21 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_core(const void
     }
 }
 
-// Y = X W (rows scaled by rscale when given), rows [64 bx, 64 bx + 64) and
-// column blocks [PANEL_NB by, PANEL_NB by + PANEL_NB).  The products go
-// through LDS (the weight buffers are free once the last stage is done): a
-// 64 x 16 PANEL_NB fp32 tile, written in the matrix cores' layout and read
-// back row-major, so that each wave stores whole 16-byte pieces of
-// consecutive columns (two full 512-byte rows per store for 128 columns)
-// instead of 64-byte pieces of four rows.  Columns are XOR-swizzled by 16
-// with bit 2 of the row, so the four row groups of a store into the tile
-// fall on distinct bank halves.
+// The products of one panel leave through LDS (the weight buffers are free
+// once the last stage is done): a 64 x 16 PANEL_NB fp32 tile, written in
+// the matrix cores' layout and read back row-major, so that each wave
+// stores whole 16-byte pieces of consecutive columns (two full 512-byte
+// rows per store for 128 columns) instead of 64-byte pieces of four rows.
+// Columns are XOR-swizzled by 16 with bit 2 of the row, so the four row
+// groups of a store into the tile fall on distinct bank halves.  Rows are
+// scaled by rscale when given.  Ends with the tile read: a caller that
+// writes the buffers again first passes a barrier.
 template <int DT, int PANEL_NB>
-__device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
-                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
-                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
-                                        PanelLds<DT, PANEL_NB>& lds) {
+__device__ __attribute__((always_inline)) inline void store_panel_staged(const floatx4 (&acc)[PANEL_NB],
+                                        PanelLds<DT, PANEL_NB>& lds, int64_t M, int Nc,
+                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by) {
     constexpr int TW = PANEL_NB * 16;  // tile width (fp32 columns)
     static_assert(sizeof(lds.b) >= (size_t)PANEL_ROWS * TW * 4, "the weight buffers hold the output tile");
-    floatx4 acc[PANEL_NB];
-    gemm_panel_compute<DT, PANEL_NB>(X, M, K, Wp, NBP, bx, by, lds, [](int64_t r) { return r; }, acc);
-    // every wave is past the last stage's barrier: the buffers are free
     float* tile = reinterpret_cast<float*>(&lds.b[0][0]);
     const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lk = lane >> 4;
 #pragma unroll
@@ -246,6 +242,19 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_block(const voi
         }
         *reinterpret_cast<float4*>(Y + grow * Nc + col) = v;
     }
+}
+
+// Y = X W, rows [64 bx, 64 bx + 64) and column blocks [PANEL_NB by,
+// PANEL_NB by + PANEL_NB), through the staged store.
+template <int DT, int PANEL_NB>
+__device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
+                                        const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
+                                        const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
+                                        PanelLds<DT, PANEL_NB>& lds) {
+    floatx4 acc[PANEL_NB];
+    gemm_panel_compute<DT, PANEL_NB>(X, M, K, Wp, NBP, bx, by, lds, [](int64_t r) { return r; }, acc);
+    // every wave is past the last stage's barrier: the buffers are free
+    store_panel_staged<DT, PANEL_NB>(acc, lds, M, Nc, rscale, Y, bx, by);
 }
 
 }  // namespace taurus
