@@ -159,11 +159,14 @@ void fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 // is keys[cur] (vals[cur]); on return cur names the buffer holding the
 // result.  An internal inconsistency sets bit `bad_bit` of *bad (device
 // memory); the caller reads it at its next synchronisation.
-struct SortBuffers {
-    uint64_t* keys[2];
+template <class K>
+struct SortBuffersT {
+    K* keys[2];
     uint32_t* vals[2];  // both null when no values are carried
     int cur;
 };
+using SortBuffers = SortBuffersT<uint64_t>;
+using SortBuffers32 = SortBuffersT<uint32_t>;
 // first_hist (optional): counts of bits [0, 8) of the keys in each tile of
 // RADIX_TILE keys, first_hist[digit * tiles + tile], written by the kernel
 // that produced the keys; it replaces the first pass's histogram when that
@@ -172,6 +175,8 @@ constexpr int RADIX_TILE = 4096;
 // first_bit: sort by bits [first_bit, first_bit + key_bits) only.
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
                     int bad_bit, const uint32_t* first_hist = nullptr, int first_bit = 0);
+// The same for 32-bit keys (key_bits <= 32): half the key traffic per pass.
+void radix_sort_u32(SortBuffers32& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad, int bad_bit);
 
 // In-edges grouped by destination, sources ascending (sample.hip): built once
 // per graph for the fanout sampler.  Complete when build_csc returns.

@@ -592,8 +592,8 @@ __device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
 
 // Per tile: count of each digit (LDS atomics; the tile's loads are issued
 // before any of them).  hist[b * nblocks + tile].
-template <int DBITS>
-__global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __restrict__ keys, int64_t n,
+template <int DBITS, class K>
+__global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const K* __restrict__ keys, int64_t n,
                                                            int shift, int64_t nblocks,
                                                            uint32_t* __restrict__ hist) {
     constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
@@ -634,14 +634,14 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const uint64_t* __res
 // digits of the slots it copied out.
 constexpr int RS_WITEMS = RS_TILE / RS_WAVES;   // items per wave
 constexpr int RS_COPY = RS_TILE / RS_THREADS;   // slots each thread copies out
-template <int DBITS>
+template <int DBITS, class K>
 __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
-    const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
+    const K* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
     int64_t nblocks, const uint32_t* __restrict__ hist, const uint64_t* __restrict__ offs,
-    uint64_t* __restrict__ kout, uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
+    K* __restrict__ kout, uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
     constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
     constexpr uint32_t MASK = NB - 1;
-    __shared__ uint64_t skey[RS_TILE];
+    __shared__ K skey[RS_TILE];
     __shared__ uint64_t gbase[NB];
     __shared__ uint32_t dstart[NB];
     __shared__ uint32_t wcnt[RS_WAVES][NB];   // per wave: running count, then its offset within the digit
@@ -652,7 +652,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const int wbase = wave * RS_WITEMS;
 
     // request the wave's items first
-    uint64_t keys[RS_ITEMS];
+    K keys[RS_ITEMS];
     uint32_t vals[RS_ITEMS];
 #pragma unroll
     for (int r = 0; r < RS_ITEMS; r++) {
@@ -736,7 +736,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
         const int i = j * RS_THREADS + tid;
         dig[j] = 0;
         if (i < count) {
-            const uint64_t key = skey[i];
+            const K key = skey[i];
             const uint32_t d = (uint32_t)((key >> shift) & MASK);
             dig[j] = d;
             const uint64_t pos = gbase[d] + (uint64_t)(i - (int)dstart[d]);
@@ -762,19 +762,20 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     }
 }
 
-template <int DBITS>
-static void radix_pass(SortBuffers& b, int64_t n, int shift, int64_t nblocks, const uint32_t* pre, uint32_t* hist,
-                       uint64_t* offs, Arena& arena, hipStream_t s, int* bad, int bad_bit) {
+template <int DBITS, class K>
+static void radix_pass(SortBuffersT<K>& b, int64_t n, int shift, int64_t nblocks, const uint32_t* pre,
+                       uint32_t* hist, uint64_t* offs, Arena& arena, hipStream_t s, int* bad, int bad_bit) {
     const int c = b.cur;
     if (pre) {  // the tile histogram of this digit came with the keys
         hist = const_cast<uint32_t*>(pre);
     } else {
-        k_radix_hist<DBITS><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
+        k_radix_hist<DBITS, K><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
         TAURUS_CHECK_LAUNCH();
     }
     scan_u32_to_u64(hist, offs, ((int64_t)1 << DBITS) * nblocks, false, arena, s);
-    k_radix_scatter<DBITS><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks, hist,
-                                                                    offs, b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
+    k_radix_scatter<DBITS, K><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks,
+                                                                       hist, offs, b.keys[1 - c], b.vals[1 - c], bad,
+                                                                       bad_bit);
     TAURUS_CHECK_LAUNCH();
     b.cur = 1 - c;
 }
@@ -799,8 +800,9 @@ static std::vector<int> digit_schedule(int key_bits) {
 }
 
 static_assert(RS_TILE == RADIX_TILE, "producers of first_hist tile the keys like the sort");
-void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit, const uint32_t* first_hist, int first_bit) {
+template <class K>
+static void radix_sort_impl(SortBuffersT<K>& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
+                            int bad_bit, const uint32_t* first_hist, int first_bit) {
     if (n <= 1 || key_bits <= 0) return;
     const int64_t nblocks = ceil_div(n, RS_TILE);
     if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
@@ -810,14 +812,25 @@ void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipSt
     uint64_t* offs = arena.alloc<uint64_t>(((int64_t)1 << wmax) * nblocks, "radix offsets");
     int shift = first_bit;
     for (int width : widths) {
+        if (shift >= (int)(8 * sizeof(K))) break;  // the remaining bits are zero in every key
         const uint32_t* pre = shift == 0 && width == 8 ? first_hist : nullptr;
-        if (width == 8) radix_pass<8>(b, n, shift, nblocks, pre, hist, offs, arena, s, bad, bad_bit);
-        else if (width == 9) radix_pass<9>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
-        else radix_pass<10>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
+        if (width == 8) radix_pass<8, K>(b, n, shift, nblocks, pre, hist, offs, arena, s, bad, bad_bit);
+        else if (width == 9) radix_pass<9, K>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
+        else radix_pass<10, K>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
         shift += width;
     }
     arena.free_ptr(offs);
     arena.free_ptr(hist);
+}
+
+void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
+                    int bad_bit, const uint32_t* first_hist, int first_bit) {
+    radix_sort_impl<uint64_t>(b, n, key_bits, arena, s, bad, bad_bit, first_hist, first_bit);
+}
+
+void radix_sort_u32(SortBuffers32& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad, int bad_bit) {
+    if (key_bits > 32) fail(TAURUS_E_INVALID, "32-bit radix sort of %d-bit keys", key_bits);
+    radix_sort_impl<uint32_t>(b, n, key_bits, arena, s, bad, bad_bit, nullptr, 0);
 }
 
 }  // namespace taurus

@@ -63,7 +63,7 @@ void validate_csr(const taurus_graph& g, hipStream_t s) {
 // ascending or holds a self loop (bit 16)
 __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
-                                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                   uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
                                                    int* __restrict__ bad) {
     __shared__ int64_t ro[4][64];
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ r
     if (i >= e) return;
     const int32_t v = col_dst[i];
     if ((int64_t)v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 16);
-    keys[i] = (uint64_t)v;
+    keys[i] = (uint32_t)v;
     vals[i] = (uint32_t)u;
 }
 
@@ -88,13 +88,13 @@ __global__ void k_heavy_list(const int32_t* __restrict__ flag, const int64_t* __
 
 // in_off[v] = first position of the sorted destinations that is >= v
 // (binary search; no atomics, so hubs cost nothing extra), v in [0, n]
-__global__ void k_csc_offsets(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int64_t* __restrict__ in_off) {
+__global__ void k_csc_offsets(const uint32_t* __restrict__ keys, int64_t e, int64_t n, int64_t* __restrict__ in_off) {
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v > n) return;
     int64_t lo = 0, hi = e;
     while (lo < hi) {
         const int64_t mid = lo + ((hi - lo) >> 1);
-        if (keys[mid] < (uint64_t)v) lo = mid + 1;
+        if ((int64_t)keys[mid] < v) lo = mid + 1;
         else hi = mid;
     }
     in_off[v] = lo;
@@ -113,13 +113,13 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scra
     int hbad = 0;
     c->in_off = c->arena.alloc<int64_t>(n + 1, "in-edge offsets");
     if (e > 0) {
-        SortBuffers sb{{tmp.alloc<uint64_t>(e, "csc keys"), tmp.alloc<uint64_t>(e, "csc keys (ping-pong)")},
+        SortBuffers32 sb{{tmp.alloc<uint32_t>(e, "csc keys"), tmp.alloc<uint32_t>(e, "csc keys (ping-pong)")},
                        {c->arena.alloc<uint32_t>(e, "in-edge sources"),
                         c->arena.alloc<uint32_t>(e, "in-edge sources (ping-pong)")},
                        0};
         k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0], bad);
         TAURUS_CHECK_LAUNCH();
-        radix_sort_u64(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
+        radix_sort_u32(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
         c->in_src = reinterpret_cast<int32_t*>(sb.vals[sb.cur]);
         c->arena.free_ptr(sb.vals[1 - sb.cur]);
         k_csc_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, c->in_off);
