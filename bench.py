@@ -59,6 +59,10 @@ VARIANTS = {
     "gat": (3, (), "2-layer single-head GAT 128->128->64 (LeakyReLU 0.2), exact: transform, softmax statistics "
                    "and aggregation passes"),
     "gat-sampled": (3, (10, 5), "2-layer single-head GAT 128->128->64, fanouts (10, 5)"),
+    "gin-mlp": (4, (), "2-layer GIN 128->128->64 with a two-layer perceptron apply (hidden = output width, "
+                       "eps = 0), exact: W1 before aggregation, ReLU(+b1) at completion, W2 on each chunk's "
+                       "completed rows"),
+    "gin-mlp-sampled": (4, (10, 5), "2-layer GIN with perceptron apply, fanouts (10, 5)"),
 }
 
 
@@ -565,7 +569,7 @@ def bench_rmat_1m(args):
     for li in range(nl):
         sts = [r[2][li] for r in runs]
         d_o, d_in = specs[li]["d_out"], specs[li]["d_in"]
-        ncols = d_o  # GCN and GIN transform width
+        ncols = d_o  # GCN and GIN transform width (GIN's perceptron: W1, then W2 at graduation)
         wall = float(np.mean([s["wall_ms"] for s in sts]))
         st = sts[-1]
         kb = kernel_bytes(fm, w.n, d_o, 4, sage=False)
@@ -579,7 +583,9 @@ def bench_rmat_1m(args):
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
         ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
               for k in ("gemm", "scatter", "fixup", "init", "index")}
-        if profile and not sampled and agg != WL.GAT_ATT:   # GAT aggregates in its own passes
+        # GAT aggregates in its own passes; GIN's perceptron writes a completed
+        # row into its accumulator row instead of the output, the same bytes
+        if profile and not sampled and agg != WL.GAT_ATT:
             for k in tot:
                 tot[k][0] += kb[k] * len(sts)
                 tot[k][1] += sum(s[f"ms_{k}"] for s in sts)

@@ -491,10 +491,8 @@ struct ScatterParams {
     const float* att_m;
     const float* att_s;
     // GIN with a perceptron (agg TAURUS_GIN_MLP): a completing destination's
-    // hidden row ReLU(acc + b1) replaces its accumulator row and v is
-    // appended to ready_ids for the graduation transform
-    int32_t* ready_ids;
-    unsigned int* ready_count;
+    // hidden row ReLU(acc + b1) replaces its accumulator row; the chunk's
+    // graduation transform reads it from there
 };
 
 struct ChunkUnits {        // this chunk's slice of the short classes and wave units
@@ -661,7 +659,6 @@ __device__ inline void flush_owner(const ScatterParams& p, int v, int2 pe, const
                 *reinterpret_cast<float4*>(arow + col) = z;
             }
         }
-        if (lane == 0) p.ready_ids[atomicAdd(p.ready_count, 1u)] = v;
     } else if (left == 0) {
         const float phi = p.agg == 1 ? 1.0f / sqrtf((float)pe.y) : 1.0f;
 #pragma unroll
@@ -1238,13 +1235,14 @@ static void dispatch_fixup(const ScatterShape& sh, const ScatterParams& p, const
 
 // ---------------------------------------------- graduation transform (GIN) --
 // A GIN layer with a perceptron apply leaves each completed destination's
-// hidden row t_v = ReLU(acc_v + b1) in its accumulator row and its ID in
-// the chunk's ready list.  After the chunk's flushes, the ready rows take the
-// perceptron's second layer on the matrix cores: out[v] = act(t_v W2 + b2),
-// written in the output type (Sec. 3.6 transforms graduated vertices in
-// batches).  The workgroups stride over the row panels of however many rows
-// the chunk made ready (read from device memory), so the launch needs no
-// count from the host.
+// hidden row t_v = ReLU(acc_v + b1) in its accumulator row.  After the
+// chunk's flushes, the rows that completed in it take the perceptron's
+// second layer on the matrix cores: out[v] = act(t_v W2 + b2), written in
+// the output type (Sec. 3.6 transforms graduated vertices in batches).
+// Which rows those are is fixed by the chunk index (the last chunk that
+// carries a message to v), so the lists are built once per layer and the
+// scatter keeps no list of its own: a shared counter bumped by every
+// completing destination serialises the scatter's waves.
 
 __device__ inline void store_out1(void* out, int dtype, int64_t idx, float z) {
     if (dtype == 0) static_cast<float*>(out)[idx] = z;
@@ -1268,19 +1266,59 @@ struct GradRows {
 
 constexpr int GRAD_NB = 8;   // 16-column blocks per workgroup (128 columns)
 
+// The graduation transform of one chunk: out[ids[r]] = act(hidden[ids[r]] W2
+// + b2) for the M destinations that complete in it.
 __global__ __launch_bounds__(256) void k_graduate(const float* __restrict__ hidden, int d_h,
                                                   const float4* __restrict__ w2p, int nbp, int d_out,
-                                                  const int32_t* __restrict__ ids,
-                                                  const unsigned int* __restrict__ count,
+                                                  const int32_t* __restrict__ ids, int64_t M,
                                                   const float* __restrict__ b2, void* out, int dtype, int relu) {
     __shared__ PanelLds<TAURUS_F32, GRAD_NB> lds;
-    const int64_t M = *count;
     const int64_t ngy = (nbp + GRAD_NB - 1) / GRAD_NB;
     const int64_t tiles = (M + PANEL_ROWS - 1) / PANEL_ROWS * ngy;
     const GradRows epi{ids, b2, out, d_out, dtype, relu};
     for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x)  // uniform over the workgroup
         gemm_panel_core<TAURUS_F32, GRAD_NB>(hidden, M, d_h, w2p, nbp, d_out, (int)(t / ngy), (int)(t % ngy), lds,
                                              [=](int64_t r) { return (int64_t)ids[r]; }, epi);
+}
+
+// The chunk a destination completes in is the last chunk that carries one
+// of its messages: its own chunk (the self message) or a later one holding
+// one of its segments.  k_own_chunk starts lc[v] at v's own chunk (and ids
+// at the identity); k_unit_chunks raises it to the chunk of every work-list
+// entry naming v, whose entries of chunk k sit at [offs[k], offs[k + 1]).
+__global__ __launch_bounds__(256) void k_own_chunk(uint32_t* __restrict__ lc, uint32_t* __restrict__ ids, int64_t n,
+                                                   int64_t C) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v < n) {
+        lc[v] = (uint32_t)(v / C);
+        ids[v] = (uint32_t)v;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_unit_chunks(const int4* __restrict__ units, const int64_t* __restrict__ offs,
+                                                     int64_t nch, uint32_t* __restrict__ lc) {
+    const int64_t i = offs[0] + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= offs[nch]) return;
+    int64_t lo = 0, hi = nch - 1;  // the last chunk k with offs[k] <= i
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (offs[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    atomicMax(&lc[units[i].z], (uint32_t)lo);
+}
+
+// off[k] = the first position of chunk number k in the ascending key[0, n)
+// (n >= 1), off[nch] = n
+__global__ __launch_bounds__(256) void k_chunk_starts(const uint32_t* __restrict__ key, int64_t n, int64_t nch,
+                                                      int64_t* __restrict__ off) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int64_t k = key[i];
+    const int64_t prev = i == 0 ? -1 : (int64_t)key[i - 1];
+    for (int64_t j = prev + 1; j <= k; j++) off[j] = i;
+    if (i == n - 1)
+        for (int64_t j = k + 1; j <= nch; j++) off[j] = n;
 }
 
 // ------------------------------------------------------------- chunk index --
@@ -1730,11 +1768,12 @@ struct taurus_layer {
     const float* gat_attn = nullptr;  // GAT: a_src then a_dst on the device
     bool gat_done = false;       // GAT: passes 2 and 3 have run
     // GIN with a perceptron: the second layer (packed for the matrix cores)
-    // and its bias, the chunk's ready list and its length
+    // and its bias; the destinations grouped by the chunk they complete in
+    // (comp_ids), chunk k's at [comp_off[k], comp_off[k + 1])
     float* w2pack = nullptr;
     float* bias2 = nullptr;
-    int32_t* ready_ids = nullptr;
-    unsigned int* ready_count = nullptr;
+    int32_t* comp_ids = nullptr;
+    std::vector<int64_t> comp_off;
     int grad_blocks = 0;
     void* wpack_any = nullptr;  // packed weights (fp32 or 16-bit fragments)
     void* out_dev = nullptr;    // desc.out as kernels address it
@@ -1798,6 +1837,54 @@ taurus_layer::~taurus_layer() {
 }
 
 namespace taurus {
+
+// Graduation lists of a GIN layer with a perceptron: the vertices grouped
+// (stably) by the chunk they complete in, built once from the chunk index,
+// so that a push knows the rows it hands to W2 without the scatter keeping
+// a list.  Temporaries come from tmp.
+static void build_completion_lists(taurus_layer* L, const ChunkIndex& idx, Arena& tmp, hipStream_t s) {
+    const int T = 256;
+    const int64_t n = L->n, nch = L->nchunks;
+    SortBuffers32 sb{{tmp.alloc<uint32_t>(n, "completing chunks"), tmp.alloc<uint32_t>(n, "completing chunks (ping-pong)")},
+                     {tmp.alloc<uint32_t>(n, "completing vertices"),
+                      tmp.alloc<uint32_t>(n, "completing vertices (ping-pong)")},
+                     0};
+    k_own_chunk<<<(unsigned)ceil_div(n, T), T, 0, s>>>(sb.keys[0], sb.vals[0], n, L->C);
+    TAURUS_CHECK_LAUNCH();
+    // the short classes' and the wave units' positions per chunk (the
+    // fix-up list names hubs that the wave units name too)
+    constexpr int NL = NCLASS + 1;
+    const size_t obytes = (size_t)NL * (size_t)(nch + 1) * sizeof(int64_t);
+    int64_t* stage = static_cast<int64_t*>(pinned_staging(obytes));
+    for (int l = 0; l < NL; l++)
+        for (int64_t k = 0; k <= nch; k++) stage[(size_t)l * (nch + 1) + (size_t)k] = idx.list_off[l][(size_t)k];
+    int64_t* offs = tmp.alloc<int64_t>((int64_t)NL * (nch + 1), "work-list positions");
+    TAURUS_HIP(hipMemcpyAsync(offs, stage, obytes, hipMemcpyHostToDevice, s));
+    pinned_staging_in_flight(s);
+    for (int l = 0; l < NL; l++) {
+        const int64_t cnt = idx.list_off[l][(size_t)nch] - idx.list_off[l][0];
+        if (cnt <= 0) continue;
+        k_unit_chunks<<<(unsigned)ceil_div(cnt, T), T, 0, s>>>(idx.units, offs + (int64_t)l * (nch + 1), nch,
+                                                               sb.keys[0]);
+        TAURUS_CHECK_LAUNCH();
+    }
+    int* bad = tmp.alloc<int>(1, "sort flag");
+    fill_i32(bad, 1, 0, s);
+    radix_sort_u32(sb, n, std::max(1, bits_for(nch - 1)), tmp, s, bad, 0);
+    int64_t* off = tmp.alloc<int64_t>(nch + 1, "graduation list positions");
+    k_chunk_starts<<<(unsigned)ceil_div(n, T), T, 0, s>>>(sb.keys[sb.cur], n, nch, off);
+    TAURUS_CHECK_LAUNCH();
+    L->comp_ids = L->arena.alloc<int32_t>(n, "graduation lists");
+    TAURUS_HIP(hipMemcpyAsync(L->comp_ids, sb.vals[sb.cur], (size_t)n * 4, hipMemcpyDeviceToDevice, s));
+    L->comp_off.assign((size_t)nch + 1, 0);
+    int hbad = 0;
+    Readback rb;
+    rb.add(L->comp_off.data(), off, nch + 1);
+    rb.add(&hbad, bad, 1);
+    rb.run(s);
+    if (hbad || L->comp_off[0] != 0 || L->comp_off[(size_t)nch] != n)
+        fail(TAURUS_E_DEVICE, "graduation lists are inconsistent (flags %d)", hbad);
+}
 
 static void validate_desc(const taurus_layer_desc* d) {
     if (!d) fail(TAURUS_E_INVALID, "null descriptor");
@@ -2046,24 +2133,15 @@ static void layer_init(taurus_layer* L) {
                  (long long)d.hbm_budget);
     }
     if (d.agg == TAURUS_GIN_MLP) {
-        // ready list: a push completes at most the destinations it touches
-        // (its own rows and one per list entry)
-        int64_t max_dc = 0;
-        for (int64_t k = 0; k < L->nchunks; k++) {
-            int64_t t = std::min(C, n - k * C);
-            for (int l = 0; l < NLIST; l++) t += idx.list_count(l, k);
-            max_dc = std::max(max_dc, t);
-        }
-        max_dc = std::min(max_dc, n);
-        L->ready_ids = L->arena.alloc<int32_t>(max_dc, "ready list");
-        L->ready_count = L->arena.alloc<unsigned int>(1, "ready count");
-        fill_i32(reinterpret_cast<int32_t*>(L->ready_count), 1, 0, s);
+        // the accumulators are not in use yet: their memory holds the
+        // temporaries here too
+        Arena own(s);
+        build_completion_lists(L, idx, scratch ? *scratch : own, s);
+        if (scratch) scratch->release();
         int dev = 0, cus = 0;
         TAURUS_HIP(hipGetDevice(&dev));
         TAURUS_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-        const int64_t ngy = ceil_div(gemm_packed_blocks_n(d.d_out), GRAD_NB);
-        L->grad_blocks = (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(max_dc, PANEL_ROWS) * ngy,
-                                                                     2 * (int64_t)std::max(1, cus)));
+        L->grad_blocks = 2 * std::max(1, cus);   // at most two workgroups per compute unit
     }
     // the perceptron's graduation reads every flush of the chunk, the
     // fix-up's included, so its fix-up is not deferred
@@ -2232,8 +2310,6 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.long_base = idx.list_off[NCLASS][(size_t)k];
     p.first_row = b;
     p.rows = e - b;
-    p.ready_ids = L->ready_ids;
-    p.ready_count = L->ready_count;
     ChunkUnits cu;
     for (int l = 0; l <= NCLASS; l++) {
         cu.u[l] = idx.list_at(l, k);
@@ -2250,14 +2326,17 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     } else if (nfix > 0) {
         dispatch_fixup(L->shape, p, idx.list_at(NCLASS + 1, k), nfix, s);
     }
-    if (L->ready_ids) {
-        k_graduate<<<(unsigned)L->grad_blocks, 256, 0, s>>>(L->acc, L->d_o,
-                                                             reinterpret_cast<const float4*>(L->w2pack),
-                                                             gemm_packed_blocks_n(L->d.d_out), L->d.d_out,
-                                                             L->ready_ids, L->ready_count, L->bias2, L->out_dev,
-                                                             L->d.out_dtype, L->d.relu);
-        TAURUS_CHECK_LAUNCH();
-        fill_i32(reinterpret_cast<int32_t*>(L->ready_count), 1, 0, s);
+    if (L->comp_ids) {
+        // the destinations that completed in this chunk's scatter and fix-up
+        const int64_t c0 = L->comp_off[(size_t)k], M = L->comp_off[(size_t)k + 1] - c0;
+        const int nbp = gemm_packed_blocks_n(L->d.d_out);
+        const int64_t tiles = ceil_div(M, PANEL_ROWS) * ceil_div(nbp, GRAD_NB);
+        if (tiles > 0) {
+            k_graduate<<<(unsigned)std::min<int64_t>(tiles, L->grad_blocks), 256, 0, s>>>(
+                L->acc, L->d_o, reinterpret_cast<const float4*>(L->w2pack), nbp, L->d.d_out, L->comp_ids + c0, M,
+                L->bias2, L->out_dev, L->d.out_dtype, L->d.relu);
+            TAURUS_CHECK_LAUNCH();
+        }
     }
     if (ev[3]) TAURUS_HIP(hipEventRecord(ev[3], s));
     if (L->res) L->res->release(rc, L->cnt, s);
