@@ -82,9 +82,9 @@ template <int DT, int PANEL_NB>
 __global__ __launch_bounds__(256) void k_gemm_panel(const void* __restrict__ X, int64_t M, int K,
                                                     const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP,
                                                     int Nc, const float* __restrict__ rscale,
-                                                    float* __restrict__ Y) {
+                                                    float* __restrict__ Y, int stream) {
     __shared__ PanelLds<DT, PANEL_NB> lds;
-    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, blockIdx.y, lds);
+    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, blockIdx.y, lds, stream != 0);
 }
 
 template <int DT>
@@ -92,12 +92,13 @@ static void launch_panel(const void* X, int64_t M, int K, const void* Wp, int Nc
                          hipStream_t s) {
     const int NBP = gemm_packed_blocks_n(Nc);
     const auto* w = static_cast<const typename GemmOp<DT>::frag*>(Wp);
+    const int stream = transform_streams(M, Nc) ? 1 : 0;
     if (NBP <= 4) {
         dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), 1);
-        k_gemm_panel<DT, 4><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y);
+        k_gemm_panel<DT, 4><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream);
     } else {
         dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), (unsigned)ceil_div(NBP, 8));
-        k_gemm_panel<DT, 8><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y);
+        k_gemm_panel<DT, 8><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream);
     }
     TAURUS_CHECK_LAUNCH();
 }

@@ -604,12 +604,16 @@ __device__ inline uint32_t self_off(const ScatterParams& p, int r) {
     return (uint32_t)r * (uint32_t)(p.ystride * 4) + (uint32_t)p.self_col * 4u;
 }
 
+// Row at byte offset off (NO_ROW: zeros); qv = float4 per row that hold
+// values: the lanes past them (a width that does not fill the row-group's
+// G * VEC float4) load nothing, so a narrow row costs only its own bytes.
 template <int G, int VEC>
-__device__ inline void gather_row(__amdgpu_buffer_rsrc_t rs, uint32_t off, int lane, float4 (&r)[VEC]) {
+__device__ inline void gather_row(__amdgpu_buffer_rsrc_t rs, uint32_t off, int lane, int qv, float4 (&r)[VEC]) {
     const uint32_t o = off + (uint32_t)lane * 16u;
 #pragma unroll
     for (int j = 0; j < VEC; j++) {
-        const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(rs, o, j * G * 16, 0);
+        const uint32_t oj = (j * G + lane < qv) ? o : NO_ROW;
+        const u32x4_t q = __builtin_amdgcn_raw_buffer_load_b128(rs, oj, j * G * 16, 0);
         r[j] = make_float4(__uint_as_float(q.x), __uint_as_float(q.y), __uint_as_float(q.z), __uint_as_float(q.w));
     }
 }
@@ -723,6 +727,7 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
     int64_t b = phase_first((int64_t)blockIdx.x * NRG + rg, rot, stride);
     if (b >= nb) return;  // the whole row-group
     const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    const int qv = p.d_o >> 2;  // float4 of a row that hold values
 
     // descriptor k of batch bb in lane k % G, register k / G; an empty unit
     // has no slots and v = -1
@@ -785,7 +790,7 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
             for (int j = 0; j < TS; j++) sw[j] = __shfl(wt[j / G], j % G, G);
         }
 #pragma unroll
-        for (int j = 0; j < RB; j++) gather_row<G, VEC>(rs, so[j], lane, rows[j]);
+        for (int j = 0; j < RB; j++) gather_row<G, VEC>(rs, so[j], lane, qv, rows[j]);
         int2 pe_l[KD];
 #pragma unroll
         for (int q = 0; q < KD; q++) pe_l[q] = dv[q] >= 0 ? p.cnt[dv[q]] : make_int2(0, 0);
@@ -830,7 +835,7 @@ __device__ inline void short_batches(const ScatterParams& p, const int4* __restr
                 const int j = k * LEN + i;
                 if (j >= RB && j % RB == 0) {  // next round (a single-unit batch)
 #pragma unroll
-                    for (int jj = 0; jj < RB; jj++) gather_row<G, VEC>(rs, so[j + jj], lane, rows[jj]);
+                    for (int jj = 0; jj < RB; jj++) gather_row<G, VEC>(rs, so[j + jj], lane, qv, rows[jj]);
                 }
                 if constexpr (ATT) {
 #pragma unroll
@@ -883,6 +888,7 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
     int64_t un = (int64_t)blockIdx.x * (SC_THREADS / 64) + wave;
     if (un >= n) return;  // the whole wave
     const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    const int qv = p.d_o >> 2;  // float4 of a row that hold values
     auto load_offsets = [&](int4 w, uint32_t (&cr)[NREG], float (&wt)[NREG]) {
         const int items = (w.y & LEN_MASK) - ((w.y & SELF_HERE) ? 1 : 0);
 #pragma unroll
@@ -907,7 +913,7 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
         float4 pre[VEC], srow[VEC];
         const bool have_pre = flush && rg == 0 && (w.y & NOT_FIRST);
         if (have_pre) load_acc_row<G, VEC>(p, v, lane, pre);
-        gather_row<G, VEC>(rs, self && rg == 0 ? self_off(p, (int)((int64_t)v - p.first_row)) : NO_ROW, lane, srow);
+        gather_row<G, VEC>(rs, self && rg == 0 ? self_off(p, (int)((int64_t)v - p.first_row)) : NO_ROW, lane, qv, srow);
         const bool more = un1 < n;
         uint32_t ncr[NREG];
         float nwt[NREG];
@@ -924,7 +930,7 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
         auto round = [&](const uint32_t (&o)[SLOTS], const float (&ow)[SLOTS]) {
             float4 rows[SLOTS][VEC];
 #pragma unroll
-            for (int k = 0; k < SLOTS; k++) gather_row<G, VEC>(rs, o[k], lane, rows[k]);
+            for (int k = 0; k < SLOTS; k++) gather_row<G, VEC>(rs, o[k], lane, qv, rows[k]);
 #pragma unroll
             for (int k = 0; k < SLOTS; k++)
 #pragma unroll
@@ -1044,6 +1050,7 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
     const int64_t nrg = (int64_t)gridDim.x * NRG;
     const int64_t stride = nrg * K;
     const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
+    const int qv = p.d_o >> 2;  // float4 of a row that hold values
     for (int64_t r0 = phase_first((int64_t)blockIdx.x * NRG + rg, rot, nrg) * K; r0 < p.rows; r0 += stride) {
         int fl[KD];
         int2 pe_l[KD];
@@ -1064,7 +1071,7 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
         for (int k = 0; k < K; k++) {
             f[k] = rg_pick<G, KD>(fl, k);
             const bool todo = !(f[k] & OWN_SEGMENT);
-            gather_row<G, VEC>(rs, todo ? self_off(p, (int)(r0 + k)) : NO_ROW, lane, rows[k]);
+            gather_row<G, VEC>(rs, todo ? self_off(p, (int)(r0 + k)) : NO_ROW, lane, qv, rows[k]);
             if (todo && !(f[k] & SELF_FIRST)) load_acc_row<G, VEC>(p, (int)(p.first_row + r0 + k), lane, pre[k]);
         }
 #pragma unroll
@@ -1744,6 +1751,7 @@ struct taurus_layer {
     bool poisoned = false;
     int64_t n = 0, C = 0, nchunks = 0;
     int d_o = 0, ncols = 0;
+    int ystride = 0;  // row stride of the chunk transform Y (floats)
     taurus::ScatterShape shape{};
     int2* cnt = nullptr;
     float* n_out = nullptr;
@@ -1939,6 +1947,10 @@ static void layer_init(taurus_layer* L) {
     // GraphSAGE: [W_agg | W_self]; GAT: W and the two attention columns,
     // padded to a multiple of 4
     L->ncols = d.agg == TAURUS_SAGE_MEAN ? 2 * d.d_out : d.agg == TAURUS_GAT_ATT ? d.d_out + 4 : L->d_o;
+    // Y rows padded to whole 128-byte lines (the padding columns hold the
+    // zero-padded weights' products): the transform then writes whole lines
+    // and a gathered row starts on a line
+    L->ystride = d.agg == TAURUS_GAT_ATT ? L->ncols : (L->ncols + 31) / 32 * 32;
     L->shape = scatter_shape(L->d_o);
     L->shape.max_blocks = scatter_resident_blocks(L->shape, false);
     L->shape.max_blocks_att = scatter_resident_blocks(L->shape, true);
@@ -2085,8 +2097,8 @@ static void layer_init(taurus_layer* L) {
 
     // working buffers
     // the scatter addresses Y with 32-bit byte offsets
-    if (std::min<int64_t>(C, n) * (int64_t)L->ncols * 4 > (int64_t)0x7f000000)
-        fail(TAURUS_E_INVALID, "chunk %lld x %d transform columns exceeds 2 GiB of fp32", (long long)C, L->ncols);
+    if (std::min<int64_t>(C, n) * (int64_t)L->ystride * 4 > (int64_t)0x7f000000)
+        fail(TAURUS_E_INVALID, "chunk %lld x %d transform columns exceeds 2 GiB of fp32", (long long)C, L->ystride);
     if (d.agg == TAURUS_GAT_ATT) {
         L->gat_hp = L->arena.alloc<float>(n * (int64_t)L->ncols, "GAT transformed rows and scores");
         L->gat_m = L->arena.alloc<float>(n, "GAT largest scores");
@@ -2094,7 +2106,7 @@ static void layer_init(taurus_layer* L) {
         fill_i32(reinterpret_cast<int32_t*>(L->gat_s), n, 0, s);
         L->gat_carry = L->arena.alloc<float>(2 * std::max<int64_t>(1, idx.max_long_per_chunk), "GAT piece statistics");
     } else {
-        L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ncols, "chunk transform");
+        L->Y = L->arena.alloc<float>(std::min<int64_t>(C, n) * (int64_t)L->ystride, "chunk transform");
     }
     const int64_t carry_rows = std::max<int64_t>(1, idx.max_long_per_chunk);
     L->carry = L->arena.alloc<float>(carry_rows * L->d_o, "hub piece carries");
@@ -2199,12 +2211,12 @@ template <int NB, int G, int VEC>
 __global__ __launch_bounds__(256) void k_transform_fixup(const float* __restrict__ X, int64_t M, int K,
                                                          const float4* __restrict__ Wp, int NBP, int Nc,
                                                          const float* __restrict__ rscale, float* __restrict__ Y,
-                                                         int gx, int gblocks, ScatterParams p,
+                                                         int gx, int gblocks, int stream, ScatterParams p,
                                                          const int4* __restrict__ fix, int64_t nfix) {
     __shared__ PanelLds<TAURUS_F32, NB> lds;
     const int b = (int)blockIdx.x;
     if (b < gblocks) {
-        gemm_panel_block<TAURUS_F32, NB>(X, M, K, Wp, NBP, Nc, rscale, Y, b % gx, b / gx, lds);
+        gemm_panel_block<TAURUS_F32, NB>(X, M, K, Wp, NBP, Nc, rscale, Y, b % gx, b / gx, lds, stream != 0);
         return;
     }
     fixup_rows<G, VEC>(p, fix, nfix, b - gblocks);
@@ -2220,14 +2232,15 @@ static void transform_with_fixup(const ScatterShape& sh, const float* X, int64_t
     const int64_t blocks = (int64_t)gx * gy + fblocks;
     if (blocks >= ((int64_t)1 << 31)) fail(TAURUS_E_INVALID, "transform of %lld rows is too large", (long long)M);
     const float4* w = reinterpret_cast<const float4*>(Wp);
+    const int stream = transform_streams(M, Nc) ? 1 : 0;
 #define TAURUS_CASE(g, v)                                                                                  \
     if (sh.G == g && sh.VEC == v) {                                                                        \
         if (nb == 4)                                                                                       \
             k_transform_fixup<4, g, v><<<(unsigned)blocks, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, gx,  \
-                                                                       gx * gy, p, fix, nfix);             \
+                                                                       gx * gy, stream, p, fix, nfix);     \
         else                                                                                               \
             k_transform_fixup<8, g, v><<<(unsigned)blocks, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, gx,  \
-                                                                       gx * gy, p, fix, nfix);             \
+                                                                       gx * gy, stream, p, fix, nfix);     \
         TAURUS_CHECK_LAUNCH();                                                                             \
         return;                                                                                            \
     }
@@ -2272,14 +2285,14 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     // GAT: the first pass only, into the layer's table of transformed rows
     float* ydst = L->gat_hp ? L->gat_hp + b * (int64_t)L->ncols : L->Y;
     if (L->d.in_dtype == TAURUS_F32 && L->fix_pending) {
-        transform_with_fixup(L->shape, static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale,
+        transform_with_fixup(L->shape, static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ystride, rscale,
                              ydst, L->fix_p, L->fix_list, L->fix_n, s);
         L->fix_pending = false;
     } else if (L->d.in_dtype == TAURUS_F32)
-        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ncols, rscale, ydst, s);
+        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ystride, rscale, ydst, s);
     else
         gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
-                static_cast<const uint16_t*>(L->wpack_any), L->ncols, rscale, ydst, s);
+                static_cast<const uint16_t*>(L->wpack_any), L->ystride, rscale, ydst, s);
     if (x_on_host) TAURUS_HIP(hipEventRecord(L->gemm_done[(L->host_pushes - 1) & 1], s));
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
     if (L->gat_hp) {  // the attention terms of the chunk's rows; passes 2 and 3 run at finalize
@@ -2291,9 +2304,9 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     }
     ScatterParams p{};
     p.Y = L->Y;
-    p.ystride = L->ncols;
+    p.ystride = L->ystride;
     p.self_col = L->d.agg == TAURUS_SAGE_MEAN ? L->d_o : 0;
-    p.y_bytes = (int)(std::min(L->C, L->n) * (int64_t)L->ncols * 4);
+    p.y_bytes = (int)(std::min(L->C, L->n) * (int64_t)L->ystride * 4);
     p.src = idx.item_src ? idx.item_src + idx.chunk_off[(size_t)k] : nullptr;
     p.has_own = idx.has_own;
     p.cnt = L->cnt;
