@@ -11,7 +11,7 @@ namespace taurus {
 
 // pack (u, v) into u << vbits | v and flag out-of-range ids and self loops.
 // Workgroup t packs tile t of RADIX_TILE edges and counts the low 8 bits of
-// its keys, the radix sort's first digit: hist[digit * tiles + t].
+// its keys, the radix sort's first digit: hist[t * 256 + digit].
 __global__ __launch_bounds__(256) void k_pack_edges(const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
                                                     int64_t e, int64_t n, int vbits, uint64_t* __restrict__ keys,
                                                     int* __restrict__ bad, uint32_t* __restrict__ hist,
@@ -33,7 +33,7 @@ __global__ __launch_bounds__(256) void k_pack_edges(const int32_t* __restrict__ 
     }
     if (flag) atomicOr(bad, 1);
     __syncthreads();
-    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
+    hist[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
 }
 
 // col_dst from the sorted keys; a key equal to its predecessor is a repeat
@@ -143,14 +143,16 @@ void* scratch_of_current_device() {
 
 // Scratch bytes the build takes for e edges, an upper bound: two key arrays,
 // the first-digit histogram, and per radix pass at most 1,024 buckets of
-// 4-byte counts and 8-byte offsets per tile plus the scan's block sums, each
-// block rounded to 256 bytes.
+// 4-byte counts per tile, plus the offset computation's per-group counts and
+// offsets (at most ceil(sqrt(tiles)) groups) and digit totals, each block
+// rounded to 256 bytes.
 int64_t build_csr_scratch_bytes(int64_t e) {
     const int64_t tiles = ceil_div(std::max<int64_t>(e, 1), RADIX_TILE);
     const int64_t buckets = 1024 * tiles;
-    const int64_t scan_blocks = ceil_div(buckets, 4096);
+    int64_t groups = 1;
+    while (groups * groups < tiles) groups++;
     return 256 + 2 * (8 * std::max<int64_t>(e, 1) + 256) + (1024 * tiles + 256) + (4 * buckets + 256) +
-           (8 * buckets + 256) + 2 * (16 * scan_blocks + 256) + 4096;
+           2 * (8 * 1024 * groups + 256) + (8 * 1024 + 256) + 4096;
 }
 
 int build_csr_noalloc_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,

@@ -168,13 +168,13 @@ struct SortBuffersT {
 using SortBuffers = SortBuffersT<uint64_t>;
 using SortBuffers32 = SortBuffersT<uint32_t>;
 // first_hist (optional): counts of bits [0, 8) of the keys in each tile of
-// RADIX_TILE keys, first_hist[digit * tiles + tile], written by the kernel
+// RADIX_TILE keys, first_hist[tile * 256 + digit], written by the kernel
 // that produced the keys; it replaces the first pass's histogram when that
 // pass sorts an 8-bit digit.
 constexpr int RADIX_TILE = 4096;
 // first_bit: sort by bits [first_bit, first_bit + key_bits) only.
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit, const uint32_t* first_hist = nullptr, int first_bit = 0);
+                    int bad_bit, uint32_t* first_hist = nullptr, int first_bit = 0);
 // The same for 32-bit keys (key_bits <= 32): half the key traffic per pass.
 void radix_sort_u32(SortBuffers32& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad, int bad_bit);
 

@@ -591,7 +591,9 @@ __device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
 }
 
 // Per tile: count of each digit (LDS atomics; the tile's loads are issued
-// before any of them).  hist[b * nblocks + tile].
+// before any of them).  hist[tile * NB + b]: a tile's counts are one
+// contiguous row, written and later read whole (a digit-major layout puts
+// each count of a tile on its own cache line).
 template <int DBITS, class K>
 __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const K* __restrict__ keys, int64_t n,
                                                            int shift, int64_t nblocks,
@@ -616,8 +618,148 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_hist(const K* __restrict__
 #pragma unroll
     for (int q = 0; q < Q; q++) {
         const int bkt = q * RS_THREADS + threadIdx.x;
-        hist[(int64_t)bkt * nblocks + blockIdx.x] = h[bkt];
+        hist[(int64_t)blockIdx.x * NB + bkt] = h[bkt];
     }
+}
+
+// The global position of a tile's first item of digit d is (items of
+// digits < d) + (items of digit d in tiles before this one).  From the
+// tile-major histogram, over groups of `gt` consecutive tiles, it is kept as
+// a group base gb[group * NB + d] (64-bit) plus the tile's offset within its
+// group, written over the tile's count (32-bit: a group holds fewer than
+// 2^32 items), in three steps:
+//   k_radix_group_sums: per group, each digit's count;
+//   k_radix_digit_scan: per digit, the exclusive prefix of those counts over
+//     the groups, and the digit's total (a workgroup per 64 digits, its four
+//     waves taking a quarter of the groups each);
+//   k_radix_offsets: per group, the digits' bases (an exclusive scan of the
+//     totals) plus the group's prefix into gb, then the group's tiles one
+//     after another, each count replaced by the running offset.
+template <int DBITS>
+__global__ __launch_bounds__(RS_THREADS) void k_radix_group_sums(const uint32_t* __restrict__ hist, int64_t nblocks,
+                                                                 int64_t gt, uint64_t* __restrict__ gsum) {
+    constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
+    const int64_t t0 = (int64_t)blockIdx.x * gt, t1 = min(t0 + gt, nblocks);
+    uint64_t acc[Q] = {};
+    int64_t t = t0;
+    for (; t + 4 <= t1; t += 4) {  // four rows' loads in flight
+        uint32_t x[4][Q];
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+#pragma unroll
+            for (int q = 0; q < Q; q++) x[u][q] = hist[(t + u) * NB + q * RS_THREADS + threadIdx.x];
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+#pragma unroll
+            for (int q = 0; q < Q; q++) acc[q] += x[u][q];
+    }
+    for (; t < t1; t++)
+#pragma unroll
+        for (int q = 0; q < Q; q++) acc[q] += hist[t * NB + q * RS_THREADS + threadIdx.x];
+#pragma unroll
+    for (int q = 0; q < Q; q++) gsum[(int64_t)blockIdx.x * NB + q * RS_THREADS + threadIdx.x] = acc[q];
+}
+
+template <int DBITS>
+__global__ __launch_bounds__(RS_THREADS) void k_radix_digit_scan(const uint64_t* __restrict__ gsum, int64_t ng,
+                                                                 uint64_t* __restrict__ gscan,
+                                                                 uint64_t* __restrict__ tot) {
+    constexpr int NB = 1 << DBITS;
+    __shared__ uint64_t wpart[RS_WAVES][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int d = blockIdx.x * 64 + lane;  // NB is a multiple of 64
+    const int64_t per = (ng + RS_WAVES - 1) / RS_WAVES;
+    const int64_t g0 = min((int64_t)wave * per, ng), g1 = min(g0 + per, ng);
+    uint64_t sum = 0;
+    for (int64_t g = g0; g < g1; g++) sum += gsum[g * NB + d];
+    wpart[wave][lane] = sum;
+    __syncthreads();
+    uint64_t run = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < RS_WAVES; w++) {
+        if (w < wave) run += wpart[w][lane];
+        all += wpart[w][lane];
+    }
+    for (int64_t g = g0; g < g1; g++) {
+        gscan[g * NB + d] = run;
+        run += gsum[g * NB + d];
+    }
+    if (wave == 0) tot[d] = all;
+}
+
+template <int DBITS>
+__global__ __launch_bounds__(RS_THREADS) void k_radix_offsets(uint32_t* __restrict__ hist, int64_t nblocks,
+                                                              int64_t gt, const uint64_t* __restrict__ gscan,
+                                                              const uint64_t* __restrict__ tot,
+                                                              uint64_t* __restrict__ gb) {
+    constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
+    __shared__ uint64_t wsum[RS_WAVES];
+    __shared__ uint64_t base[NB];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // digit bases: thread t owns digits [t*Q, t*Q + Q)
+    uint64_t own = 0, tq[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        tq[q] = tot[tid * Q + q];
+        own += tq[q];
+    }
+    uint64_t incl = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint64_t y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint64_t b = incl - own;
+#pragma unroll
+    for (int w = 0; w < RS_WAVES; w++)
+        if (w < wave) b += wsum[w];
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        base[tid * Q + q] = b;
+        b += tq[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        const int64_t i = (int64_t)blockIdx.x * NB + q * RS_THREADS + tid;
+        gb[i] = base[q * RS_THREADS + tid] + gscan[i];
+    }
+    const int64_t t0 = (int64_t)blockIdx.x * gt, t1 = min(t0 + gt, nblocks);
+    uint32_t run[Q] = {};
+    int64_t t = t0;
+    for (; t + 4 <= t1; t += 4) {  // four rows' loads in flight
+        uint32_t x[4][Q];
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+#pragma unroll
+            for (int q = 0; q < Q; q++) x[u][q] = hist[(t + u) * NB + q * RS_THREADS + tid];
+#pragma unroll
+        for (int u = 0; u < 4; u++)
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+                hist[(t + u) * NB + q * RS_THREADS + tid] = run[q];
+                run[q] += x[u][q];
+            }
+    }
+    for (; t < t1; t++)
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+            const int64_t i = t * NB + q * RS_THREADS + tid;
+            const uint32_t x = hist[i];
+            hist[i] = run[q];
+            run[q] += x;
+        }
+}
+
+// tiles per group of the offset computation: about the square root of the
+// tile count, so that the per-digit scan over groups and each group's walk
+// over its tiles are about equally long
+static int64_t radix_group_tiles(int64_t nblocks) {
+    int64_t g = 1;
+    while (g * g < nblocks) g++;
+    return g;
 }
 
 // Scatter one tile stably, staged through LDS so that each digit's items
@@ -637,7 +779,7 @@ constexpr int RS_COPY = RS_TILE / RS_THREADS;   // slots each thread copies out
 template <int DBITS, class K>
 __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const K* __restrict__ kin, const uint32_t* __restrict__ vin, int64_t n, int shift,
-    int64_t nblocks, const uint32_t* __restrict__ hist, const uint64_t* __restrict__ offs,
+    const uint32_t* __restrict__ rel, const uint64_t* __restrict__ gb, int64_t gt,
     K* __restrict__ kout, uint32_t* __restrict__ vout, int* __restrict__ bad, int bad_bit) {
     constexpr int NB = 1 << DBITS, Q = NB / RS_THREADS;
     constexpr uint32_t MASK = NB - 1;
@@ -651,7 +793,14 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     const int count = (int)min((int64_t)RS_TILE, n - tile0);
     const int wbase = wave * RS_WITEMS;
 
-    // request the wave's items first
+    // the tile's global offsets (its group's base plus its offset within
+    // the group; thread t owning buckets [t*Q, t*Q + Q)) are requested first
+    uint64_t go[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        const int d = tid * Q + q;
+        go[q] = gb[(int64_t)(blockIdx.x / gt) * NB + d] + rel[(int64_t)blockIdx.x * NB + d];
+    }
     K keys[RS_ITEMS];
     uint32_t vals[RS_ITEMS];
 #pragma unroll
@@ -664,32 +813,9 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
     for (int w = 0; w < RS_WAVES; w++)
 #pragma unroll
         for (int q = 0; q < Q; q++) wcnt[w][q * RS_THREADS + tid] = 0;
-    // digit starts within the tile: exclusive scan of the tile histogram,
-    // thread t owning buckets [t*Q, t*Q + Q)
-    uint32_t hq[Q], own = 0;
 #pragma unroll
-    for (int q = 0; q < Q; q++) {
-        hq[q] = hist[(int64_t)(tid * Q + q) * nblocks + blockIdx.x];
-        gbase[tid * Q + q] = offs[(int64_t)(tid * Q + q) * nblocks + blockIdx.x];
-        own += hq[q];
-    }
-    uint32_t incl = own;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += y;
-    }
-    if (lane == 63) wsum[wave] = incl;
+    for (int q = 0; q < Q; q++) gbase[tid * Q + q] = go[q];
     __syncthreads();
-    uint32_t run = incl - own;
-#pragma unroll
-    for (int w = 0; w < RS_WAVES; w++)
-        if (w < wave) run += wsum[w];
-#pragma unroll
-    for (int q = 0; q < Q; q++) {
-        dstart[tid * Q + q] = run;
-        run += hq[q];
-    }
 
     // rank within the wave (no block barrier: the counters are the wave's own)
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -704,17 +830,42 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
         if (valid && (peers & lt_mask) == 0) wcnt[wave][d] = runc + (uint32_t)__popcll(peers);
     }
     __syncthreads();
-    // per digit: offsets of the waves within the tile's run of that digit
+    // the tile's count of each digit is the sum of the waves' counts; the
+    // digits' starts within the tile are their exclusive scan
+    uint32_t hq[Q], own = 0;
 #pragma unroll
     for (int q = 0; q < Q; q++) {
-        const int bkt = q * RS_THREADS + tid;
-        uint32_t acc = dstart[bkt];
+        hq[q] = 0;
+#pragma unroll
+        for (int w = 0; w < RS_WAVES; w++) hq[q] += wcnt[w][tid * Q + q];
+        own += hq[q];
+    }
+    uint32_t incl = own;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t run = incl - own;
+#pragma unroll
+    for (int w = 0; w < RS_WAVES; w++)
+        if (w < wave) run += wsum[w];
+    // per digit: the start of the digit in the tile and the waves' offsets
+    // within its run (thread t's own digits: no other thread reads them here)
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        const int bkt = tid * Q + q;
+        dstart[bkt] = run;
+        uint32_t acc = run;
 #pragma unroll
         for (int w = 0; w < RS_WAVES; w++) {
             const uint32_t c = wcnt[w][bkt];
             wcnt[w][bkt] = acc;
             acc += c;
         }
+        run += hq[q];
     }
     __syncthreads();
     // LDS slot of each item (count or more: out of range, flagged)
@@ -763,20 +914,33 @@ __global__ __launch_bounds__(RS_THREADS) void k_radix_scatter(
 }
 
 template <int DBITS, class K>
-static void radix_pass(SortBuffersT<K>& b, int64_t n, int shift, int64_t nblocks, const uint32_t* pre,
-                       uint32_t* hist, uint64_t* offs, Arena& arena, hipStream_t s, int* bad, int bad_bit) {
+static void radix_pass(SortBuffersT<K>& b, int64_t n, int shift, int64_t nblocks, uint32_t* pre, uint32_t* hist,
+                       Arena& arena, hipStream_t s, int* bad, int bad_bit) {
+    constexpr int NB = 1 << DBITS;
     const int c = b.cur;
     if (pre) {  // the tile histogram of this digit came with the keys
-        hist = const_cast<uint32_t*>(pre);
+        hist = pre;
     } else {
         k_radix_hist<DBITS, K><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], n, shift, nblocks, hist);
         TAURUS_CHECK_LAUNCH();
     }
-    scan_u32_to_u64(hist, offs, ((int64_t)1 << DBITS) * nblocks, false, arena, s);
-    k_radix_scatter<DBITS, K><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, nblocks,
-                                                                       hist, offs, b.keys[1 - c], b.vals[1 - c], bad,
-                                                                       bad_bit);
+    const int64_t gt = radix_group_tiles(nblocks), ng = ceil_div(nblocks, gt);
+    uint64_t* gsum = arena.alloc<uint64_t>(ng * NB, "radix group counts");
+    uint64_t* gscan = arena.alloc<uint64_t>(ng * NB, "radix group offsets");
+    uint64_t* tot = arena.alloc<uint64_t>(NB, "radix digit totals");
+    k_radix_group_sums<DBITS><<<(unsigned)ng, RS_THREADS, 0, s>>>(hist, nblocks, gt, gsum);
     TAURUS_CHECK_LAUNCH();
+    k_radix_digit_scan<DBITS><<<NB / 64, RS_THREADS, 0, s>>>(gsum, ng, gscan, tot);
+    TAURUS_CHECK_LAUNCH();
+    uint64_t* gb = gsum;  // the group counts are read once, by the digit scan
+    k_radix_offsets<DBITS><<<(unsigned)ng, RS_THREADS, 0, s>>>(hist, nblocks, gt, gscan, tot, gb);
+    TAURUS_CHECK_LAUNCH();
+    k_radix_scatter<DBITS, K><<<(unsigned)nblocks, RS_THREADS, 0, s>>>(b.keys[c], b.vals[c], n, shift, hist, gb, gt,
+                                                                       b.keys[1 - c], b.vals[1 - c], bad, bad_bit);
+    TAURUS_CHECK_LAUNCH();
+    arena.free_ptr(tot);
+    arena.free_ptr(gscan);
+    arena.free_ptr(gsum);
     b.cur = 1 - c;
 }
 
@@ -802,29 +966,27 @@ static std::vector<int> digit_schedule(int key_bits) {
 static_assert(RS_TILE == RADIX_TILE, "producers of first_hist tile the keys like the sort");
 template <class K>
 static void radix_sort_impl(SortBuffersT<K>& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                            int bad_bit, const uint32_t* first_hist, int first_bit) {
+                            int bad_bit, uint32_t* first_hist, int first_bit) {
     if (n <= 1 || key_bits <= 0) return;
     const int64_t nblocks = ceil_div(n, RS_TILE);
     if (nblocks > 0x7fffffff) fail(TAURUS_E_INVALID, "radix sort of %lld items is too large", (long long)n);
     const std::vector<int> widths = digit_schedule(key_bits);
     const int wmax = *std::max_element(widths.begin(), widths.end());
     uint32_t* hist = arena.alloc<uint32_t>(((int64_t)1 << wmax) * nblocks, "radix histogram");
-    uint64_t* offs = arena.alloc<uint64_t>(((int64_t)1 << wmax) * nblocks, "radix offsets");
     int shift = first_bit;
     for (int width : widths) {
         if (shift >= (int)(8 * sizeof(K))) break;  // the remaining bits are zero in every key
-        const uint32_t* pre = shift == 0 && width == 8 ? first_hist : nullptr;
-        if (width == 8) radix_pass<8, K>(b, n, shift, nblocks, pre, hist, offs, arena, s, bad, bad_bit);
-        else if (width == 9) radix_pass<9, K>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
-        else radix_pass<10, K>(b, n, shift, nblocks, nullptr, hist, offs, arena, s, bad, bad_bit);
+        uint32_t* pre = shift == 0 && width == 8 ? first_hist : nullptr;
+        if (width == 8) radix_pass<8, K>(b, n, shift, nblocks, pre, hist, arena, s, bad, bad_bit);
+        else if (width == 9) radix_pass<9, K>(b, n, shift, nblocks, nullptr, hist, arena, s, bad, bad_bit);
+        else radix_pass<10, K>(b, n, shift, nblocks, nullptr, hist, arena, s, bad, bad_bit);
         shift += width;
     }
-    arena.free_ptr(offs);
     arena.free_ptr(hist);
 }
 
 void radix_sort_u64(SortBuffers& b, int64_t n, int key_bits, Arena& arena, hipStream_t s, int* bad,
-                    int bad_bit, const uint32_t* first_hist, int first_bit) {
+                    int bad_bit, uint32_t* first_hist, int first_bit) {
     radix_sort_impl<uint64_t>(b, n, key_bits, arena, s, bad, bad_bit, first_hist, first_bit);
 }
 
