@@ -25,6 +25,89 @@ __host__ __device__ inline uint64_t sample_prefix(uint64_t seed, uint64_t layer,
 }
 __host__ __device__ inline uint64_t sample_key(uint64_t prefix, uint64_t u) { return mix64(prefix + SM64_GAMMA + u); }
 
+// Row of CSR edge t for a whole wave (every lane passes the same t): the
+// largest u in [0, n) with row_off[u] <= t, by a 64-ary search (every lane
+// probes at once, ~log64(n) dependent loads).  All probes stay in [0, n].
+// Every lane of the wave must call it (it uses ballots).
+__device__ inline int64_t wave_row_of(const int64_t* __restrict__ row_off, int64_t n, int64_t t) {
+    const int lane = threadIdx.x & 63;
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 64) {
+        const int64_t step = (hi - lo + 63) >> 6;
+        const int64_t p = min(lo + (int64_t)(lane + 1) * step, hi);
+        const int k = __popcll(__ballot(row_off[p] <= t));
+        const int64_t nlo = lo + (int64_t)k * step;
+        hi = min(nlo + step, hi);
+        lo = nlo;
+    }
+    {
+        const int64_t p = lo + lane + 1;
+        const int k = __popcll(__ballot(p <= hi && row_off[p] <= t));
+        lo += k;
+    }
+    return min(lo, n - 1);
+}
+
+// Rows of a workgroup's tile of CSR edges [i0, i1) (i0 < i1 <= e), for
+// kernels that take TILE consecutive edges per workgroup: two waves find the
+// rows ua and ub of the first and last edge (wave_row_of); when the tile
+// spans at most ROWS rows, their starts go to `ro` in LDS (relative to i0,
+// clamped to [-1, TILE + 1]) and each edge finds its row there by binary
+// search, else (many empty rows) by binary search of row_off between ua and
+// ub.  (Finding each thread's first row once and walking forward over its
+// consecutive edges, recorded per edge in LDS, measured slower.)  Memory
+// safe on invalid offsets (rows stay in [0, n)).  Called by the whole
+// workgroup (it has barriers); `ro` holds ROWS + 1 entries.
+struct TileRows {
+    int64_t ua, ub, nr;
+    bool staged;
+};
+template <int ROWS, int TILE>
+__device__ inline TileRows tile_rows(const int64_t* __restrict__ row_off, int64_t n, int64_t i0, int64_t i1,
+                                     int32_t* ro, int64_t* bnd) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (wave < 2) {
+        const int64_t u = wave_row_of(row_off, n, wave == 0 ? i0 : i1 - 1);
+        if (lane == 0) bnd[wave] = u;
+    }
+    __syncthreads();
+    TileRows t;
+    t.ua = bnd[0];
+    t.ub = bnd[1];
+    t.nr = t.ub - t.ua + 1;
+    t.staged = t.nr >= 1 && t.nr <= ROWS;
+    if (t.staged)
+        for (int64_t j = threadIdx.x; j <= t.nr; j += blockDim.x) {  // j = nr: the end of the last row
+            const int64_t x = row_off[t.ua + j] - i0;
+            ro[j] = (int32_t)max(min(x, (int64_t)TILE + 1), (int64_t)-1);
+        }
+    __syncthreads();
+    return t;
+}
+// Row of edge i of the tile; `later`: i is not the first edge of its row.
+__device__ inline int64_t tile_row_of(const TileRows& t, const int64_t* __restrict__ row_off, const int32_t* ro,
+                                      int64_t i0, int64_t i, bool& later) {
+    if (t.staged) {
+        const int32_t li = (int32_t)(i - i0);
+        int a = 0, z = (int)t.nr;  // the last row start at or before li
+        while (z - a > 1) {
+            const int mid = (a + z) >> 1;
+            if (ro[mid] <= li) a = mid;
+            else z = mid;
+        }
+        later = ro[a] < li && i > 0;
+        return t.ua + a;
+    }
+    int64_t a = t.ua, z = max(t.ub + 1, t.ua + 1);
+    while (z - a > 1) {
+        const int64_t mid = (a + z) >> 1;
+        if (row_off[mid] <= i) a = mid;
+        else z = mid;
+    }
+    later = i > row_off[a];
+    return a;
+}
+
 // Row (source) of CSR edge i = lane's edge, for all 64 lanes of a wave whose
 // first edge is i0 = i - lane.  The wave finds the row u0 of i0 with a 64-ary
 // search (every lane probes at once, ~log64(n) dependent loads instead of
@@ -38,22 +121,7 @@ __host__ __device__ inline uint64_t sample_key(uint64_t prefix, uint64_t u) { re
 __device__ inline int64_t wave_edge_row(const int64_t* __restrict__ row_off, int64_t n, int64_t i,
                                         int64_t* ro) {
     const int lane = threadIdx.x & 63;
-    const int64_t i0 = i - lane;
-    int64_t lo = 0, hi = n;
-    while (hi - lo > 64) {
-        const int64_t step = (hi - lo + 63) >> 6;
-        const int64_t p = min(lo + (int64_t)(lane + 1) * step, hi);
-        const int k = __popcll(__ballot(row_off[p] <= i0));
-        const int64_t nlo = lo + (int64_t)k * step;
-        hi = min(nlo + step, hi);
-        lo = nlo;
-    }
-    {
-        const int64_t p = lo + lane + 1;
-        const int k = __popcll(__ballot(p <= hi && row_off[p] <= i0));
-        lo += k;
-    }
-    const int64_t u0 = min(lo, n - 1);
+    const int64_t u0 = wave_row_of(row_off, n, i - lane);
     const int64_t q = u0 + 1 + lane;
     ro[lane] = q <= n ? row_off[q] : INT64_MAX;
     __builtin_amdgcn_wave_barrier();

@@ -118,20 +118,32 @@ __global__ void k_validate_graph(const int64_t* __restrict__ row_off, const int3
 
 // Chunk-index items of an exact layer.  CSR edge i (source u = the row
 // containing i) becomes key (chunk(u) << vbits | v), value u - chunk(u)*C.
+// A workgroup takes MI_TILE consecutive edges and finds their rows through
+// tile_rows.
+constexpr int MI_ITEMS = 16, MI_TILE = 256 * MI_ITEMS, MI_ROWS = 8192;
 __global__ __launch_bounds__(256) void k_make_items(const int64_t* __restrict__ row_off,
                                                     const int32_t* __restrict__ col_dst, int64_t e, int64_t n,
                                                     int64_t C, int vbits, uint64_t* __restrict__ keys,
                                                     uint32_t* __restrict__ vals, int* __restrict__ bad) {
-    __shared__ int64_t ro[4][64];
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
-    if (i >= e) return;
-    const int64_t v = col_dst[i];
-    // rows strictly ascending, no self loops (a simple graph)
-    if (v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 4);
-    const uint32_t cu = (uint32_t)u / (uint32_t)C;  // u < 2^31 and C < 2^31: 32-bit division
-    keys[i] = ((uint64_t)cu << vbits) | (uint64_t)v;
-    vals[i] = (uint32_t)u - cu * (uint32_t)C;
+    __shared__ int32_t ro[MI_ROWS + 1];
+    __shared__ int64_t bnd[2];
+    const int64_t i0 = (int64_t)blockIdx.x * MI_TILE, i1 = min(i0 + MI_TILE, e);
+    const TileRows t = tile_rows<MI_ROWS, MI_TILE>(row_off, n, i0, i1, ro, bnd);
+    bool flag = false;
+#pragma unroll 4
+    for (int r = 0; r < MI_ITEMS; r++) {
+        const int64_t i = i0 + (int64_t)r * 256 + threadIdx.x;
+        if (i >= i1) break;
+        bool later;
+        const int64_t u = tile_row_of(t, row_off, ro, i0, i, later);
+        const int64_t v = col_dst[i];
+        // rows strictly ascending, no self loops (a simple graph)
+        if (v == u || (later && col_dst[i - 1] >= v)) flag = true;
+        const uint32_t cu = (uint32_t)u / (uint32_t)C;  // u < 2^31 and C < 2^31: 32-bit division
+        keys[i] = ((uint64_t)cu << vbits) | (uint64_t)v;
+        vals[i] = (uint32_t)u - cu * (uint32_t)C;
+    }
+    if (flag) atomicOr(bad, 4);
 }
 
 // propagated edges per mask word (bits at or past e are not edges)
@@ -1462,8 +1474,8 @@ static std::shared_ptr<ChunkIndex> build_index(const taurus_graph& g, int64_t C,
         // the sorted values become the index's item sources
         sb.vals[0] = idx->arena.alloc<uint32_t>(e, "index values");
         sb.vals[1] = idx->arena.alloc<uint32_t>(e, "index values (ping-pong)");
-        k_make_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits, sb.keys[0],
-                                                            sb.vals[0], bad);
+        k_make_items<<<(unsigned)ceil_div(e, MI_TILE), 256, 0, s>>>(g.row_off, g.col_dst, e, n, C, vbits,
+                                                                    sb.keys[0], sb.vals[0], bad);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, items, vbits + cbits, tmp, s, bad, 8);
     }

@@ -60,19 +60,30 @@ void validate_csr(const taurus_graph& g, hipStream_t s) {
 }
 
 // CSR edge i -> sort key v, value u; flags a row that is not strictly
-// ascending or holds a self loop (bit 16)
+// ascending or holds a self loop (bit 16).  A workgroup takes CI_TILE
+// consecutive edges and finds their rows through tile_rows.
+constexpr int CI_ITEMS = 16, CI_TILE = 256 * CI_ITEMS, CI_ROWS = 8192;
 __global__ __launch_bounds__(256) void k_csc_items(const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
                                                    uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
                                                    int* __restrict__ bad) {
-    __shared__ int64_t ro[4][64];
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
-    if (i >= e) return;
-    const int32_t v = col_dst[i];
-    if ((int64_t)v == u || (i > row_off[u] && col_dst[i - 1] >= v)) atomicOr(bad, 16);
-    keys[i] = (uint32_t)v;
-    vals[i] = (uint32_t)u;
+    __shared__ int32_t ro[CI_ROWS + 1];
+    __shared__ int64_t bnd[2];
+    const int64_t i0 = (int64_t)blockIdx.x * CI_TILE, i1 = min(i0 + CI_TILE, e);
+    const TileRows t = tile_rows<CI_ROWS, CI_TILE>(row_off, n, i0, i1, ro, bnd);
+    bool flag = false;
+#pragma unroll 4
+    for (int r = 0; r < CI_ITEMS; r++) {
+        const int64_t i = i0 + (int64_t)r * 256 + threadIdx.x;
+        if (i >= i1) break;
+        bool later;
+        const int64_t u = tile_row_of(t, row_off, ro, i0, i, later);
+        const int32_t v = col_dst[i];
+        if ((int64_t)v == u || (later && col_dst[i - 1] >= v)) flag = true;
+        keys[i] = (uint32_t)v;
+        vals[i] = (uint32_t)u;
+    }
+    if (flag) atomicOr(bad, 16);
 }
 
 // destinations with more than 64 in-edges (the long-list sampling pass)
@@ -117,7 +128,8 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scra
                        {c->arena.alloc<uint32_t>(e, "in-edge sources"),
                         c->arena.alloc<uint32_t>(e, "in-edge sources (ping-pong)")},
                        0};
-        k_csc_items<<<(unsigned)ceil_div(e, T), T, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0], sb.vals[0], bad);
+        k_csc_items<<<(unsigned)ceil_div(e, CI_TILE), 256, 0, s>>>(g.row_off, g.col_dst, n, e, sb.keys[0],
+                                                                  sb.vals[0], bad);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u32(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
         c->in_src = reinterpret_cast<int32_t*>(sb.vals[sb.cur]);
