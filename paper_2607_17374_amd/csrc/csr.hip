@@ -36,14 +36,25 @@ __global__ __launch_bounds__(256) void k_pack_edges(const int32_t* __restrict__ 
     hist[(int64_t)blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
 }
 
-// col_dst from the sorted keys; a key equal to its predecessor is a repeat
-__global__ void k_unpack_cols(const uint64_t* __restrict__ keys, int64_t e, int vbits,
-                              int32_t* __restrict__ col_dst, int* __restrict__ bad) {
+// col_dst from the sorted keys; a key equal to its predecessor is a repeat.
+// Also the row offsets: edge i is the first of every row after its
+// predecessor's up to its own (row_off[w] = i for those w), and the last
+// edge ends the rows after it (row_off[w] = e up to w = n).  Sources of the
+// sorted keys are below n (an out-of-range id was packed as key 0 and
+// flagged), so every write stays in [0, n].
+__global__ void k_unpack_cols(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
+                              int32_t* __restrict__ col_dst, int64_t* __restrict__ row_off, int* __restrict__ bad) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= e) return;
     const uint64_t k = keys[i];
     col_dst[i] = (int32_t)(k & (((uint64_t)1 << vbits) - 1));
-    if (i > 0 && keys[i - 1] == k) atomicOr(bad, 2);
+    const uint64_t kp = i > 0 ? keys[i - 1] : 0;
+    if (i > 0 && kp == k) atomicOr(bad, 2);
+    const int64_t u = min((int64_t)(k >> vbits), n - 1);
+    const int64_t up = i > 0 ? min((int64_t)(kp >> vbits), n - 1) : -1;
+    for (int64_t w = up + 1; w <= u; w++) row_off[w] = i;
+    if (i == e - 1)
+        for (int64_t w = u + 1; w <= n; w++) row_off[w] = e;
 }
 
 // row_off[u] = first position whose source is >= u (binary search), u in [0, n]
@@ -78,11 +89,12 @@ static int* enqueue_build_csr(Arena& arena, int64_t n, int64_t e, const int32_t*
         k_pack_edges<<<(unsigned)tiles, 256, 0, s>>>(src, dst, e, n, vbits, sb.keys[0], bad, hist0, tiles);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, e, 2 * vbits, arena, s, bad, 4, hist0);
-        k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, vbits, col_dst, bad);
+        k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, col_dst, row_off, bad);
+        TAURUS_CHECK_LAUNCH();
+    } else {
+        k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);
         TAURUS_CHECK_LAUNCH();
     }
-    k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);
-    TAURUS_CHECK_LAUNCH();
     return bad;
 }
 
