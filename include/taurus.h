@@ -168,6 +168,14 @@ typedef struct {
  *                sampled layer its in-edge lists, instead of building its
  *                own.  A plan with another graph or chunk size is
  *                TAURUS_E_INVALID.
+ *   setup_stream NULL, or a hipStream_t for the work taurus_layer_init
+ *                enqueues (in-edge lists, sampling, chunk index, weights,
+ *                counters): it then runs beside whatever `stream` still has
+ *                queued, such as an earlier layer's chunks, instead of after
+ *                it, and `stream` waits for it before this layer's first
+ *                kernel there.  The caller guarantees that the graph, the
+ *                plan and host arrays are ready as seen from setup_stream.
+ *                All later calls use `stream`.
  */
 typedef struct {
     int32_t agg, d_in, d_out, in_dtype, out_dtype, relu;
@@ -188,6 +196,7 @@ typedef struct {
     int32_t d_hidden;
     const float* weight2;
     const float* bias2;
+    void* setup_stream;
 } taurus_layer_desc;
 
 typedef struct taurus_layer taurus_layer;

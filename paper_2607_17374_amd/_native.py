@@ -43,7 +43,7 @@ class LayerDesc(ctypes.Structure):
                 ("out", ctypes.c_void_p), ("out_on_host", ctypes.c_int32),
                 ("stream", ctypes.c_void_p), ("profile", ctypes.c_int32), ("plan", ctypes.c_void_p),
                 ("eviction", ctypes.c_int32), ("attn", ctypes.c_void_p), ("d_hidden", ctypes.c_int32),
-                ("weight2", ctypes.c_void_p), ("bias2", ctypes.c_void_p)]
+                ("weight2", ctypes.c_void_p), ("bias2", ctypes.c_void_p), ("setup_stream", ctypes.c_void_p)]
 
 
 class Stats(ctypes.Structure):

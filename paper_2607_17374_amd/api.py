@@ -251,7 +251,11 @@ class Layer:
                  layer: int = 1, seed: int = 0, chunk: int = 65536, hbm_budget: int = 0,
                  hub_fraction: float = 0.0, stream=None, profile: int = 0, plan: "Plan" = None,
                  eviction: str = "pending", attn: Optional[np.ndarray] = None, d_hidden: int = 0,
-                 weight2: Optional[np.ndarray] = None, bias2: Optional[np.ndarray] = None):
+                 weight2: Optional[np.ndarray] = None, bias2: Optional[np.ndarray] = None,
+                 setup_stream=None):
+        """setup_stream: a torch stream for the work the init enqueues (it
+        then overlaps what `stream` still has queued, such as an earlier
+        layer's chunks); the graph and plan must be ready on it."""
         self._h = ctypes.c_void_p()
         e = col_dst.numel()
         self.graph = N.Graph(n, e, _dev_ptr(row_off, torch.int64, "row_off"),
@@ -284,8 +288,9 @@ class Layer:
             eviction=EVICTION[eviction] if isinstance(eviction, str) else int(eviction),
             attn=None if self._a is None else self._a.ctypes.data, d_hidden=d_hidden,
             weight2=None if self._w2 is None else self._w2.ctypes.data,
-            bias2=None if self._b2 is None else self._b2.ctypes.data)
-        self._keep = (row_off, col_dst, plan)
+            bias2=None if self._b2 is None else self._b2.ctypes.data,
+            setup_stream=None if setup_stream is None else setup_stream.cuda_stream)
+        self._keep = (row_off, col_dst, plan, setup_stream)
         N.check(N.lib().taurus_layer_init(ctypes.byref(self.graph), ctypes.byref(self.desc),
                                           ctypes.byref(self._h)), "taurus_layer_init")
 

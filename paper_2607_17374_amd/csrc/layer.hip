@@ -1787,6 +1787,7 @@ struct taurus_layer {
     float* gat_carry = nullptr;  // GAT: per hub piece {max, sum}
     const float* gat_attn = nullptr;  // GAT: a_src then a_dst on the device
     bool gat_done = false;       // GAT: passes 2 and 3 have run
+    bool acc_deferred = false;   // dense accumulators allocated by the first push
     // GIN with a perceptron: the second layer (packed for the matrix cores)
     // and its bias; the destinations grouped by the chunk they complete in
     // (comp_ids), chunk k's at [comp_off[k], comp_off[k + 1])
@@ -1947,7 +1948,10 @@ static bool same_graph(const taurus_graph& a, const taurus_graph& b) {
 
 static void layer_init(taurus_layer* L) {
     const auto t_start = std::chrono::steady_clock::now();
-    hipStream_t s = L->s;
+    // the set-up work goes to desc.setup_stream when given (the layer's
+    // stream waits for it at the end), else to the layer's stream
+    hipStream_t s = L->d.setup_stream ? static_cast<hipStream_t>(L->d.setup_stream) : L->s;
+    L->arena.set_stream(s);
     const taurus_graph& g = L->g;
     const taurus_layer_desc& d = L->d;
     const int64_t n = g.n, C = d.chunk;
@@ -1979,8 +1983,12 @@ static void layer_init(taurus_layer* L) {
     // while nothing has arrived and are never cleared), hold the temporaries
     // of the in-edge lists and the chunk index, so that those take no memory
     // of their own.
+    // With a set-up stream the dense accumulators wait for the first push
+    // instead (the layer before, whose chunks the set-up overlaps, may hold
+    // its own until then), and the index takes memory of its own meanwhile.
     std::unique_ptr<Arena> scratch;
-    if (d.hbm_budget == 0) {
+    const bool defer_acc = d.hbm_budget == 0 && s != L->s;
+    if (d.hbm_budget == 0 && !defer_acc) {
         const int64_t acc_elems = n * (int64_t)L->d_o;
         L->acc = L->arena.alloc<float>(acc_elems, "accumulators");
         scratch = std::make_unique<Arena>(s, L->acc, acc_elems * 4, true);
@@ -2132,6 +2140,8 @@ static void layer_init(taurus_layer* L) {
     const int64_t dense = n * row_bytes;
     if (L->acc) {
         // allocated before the index (no budget)
+    } else if (defer_acc) {
+        L->acc_deferred = true;
     } else if (L->arena.bytes() + index_bytes + dense + (dense >> 3) <= d.hbm_budget) {
         L->acc = L->arena.alloc<float>(n * (int64_t)L->d_o, "accumulators");
     } else {
@@ -2173,6 +2183,17 @@ static void layer_init(taurus_layer* L) {
     if (d.profile) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
+    }
+    if (s != L->s) {
+        // the layer's stream takes up the layer's memory and work from here
+        hipEvent_t ready = nullptr;
+        TAURUS_HIP(hipEventCreateWithFlags(&ready, hipEventDisableTiming));
+        const hipError_t rc1 = hipEventRecord(ready, s);
+        const hipError_t rc2 = rc1 == hipSuccess ? hipStreamWaitEvent(L->s, ready, 0) : rc1;
+        (void)hipEventDestroy(ready);  // released once the wait has been satisfied
+        TAURUS_HIP(rc2);
+        L->arena.set_stream(L->s);
+        if (L->res) L->res->arena.set_stream(L->s);
     }
     L->ms_init = ms_since(t_start);  // host time; the work stays queued on the stream
 }
@@ -2270,6 +2291,10 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     if (x_on_host != 0 && x_on_host != 1) fail(TAURUS_E_INVALID, "x_on_host=%d", x_on_host);
     const int64_t k = b / L->C;
     if (L->pushed[(size_t)k]) fail(TAURUS_E_STATE, "chunk %lld pushed twice", (long long)k);
+    if (L->acc_deferred) {
+        L->acc = L->arena.alloc<float>(L->n * (int64_t)L->d_o, "accumulators");
+        L->acc_deferred = false;
+    }
     const ChunkIndex& idx = *L->idx;
     hipStream_t s = L->s;
     if (x_on_host) x = stage_host_chunk(L, x, e - b);

@@ -77,7 +77,8 @@ def test_binding_structs_match_header_layout(native):
     assert native.LayerDesc.plan.offset == 112 and native.LayerDesc.eviction.offset == 120
     assert native.LayerDesc.attn.offset == 128 and native.LayerDesc.d_hidden.offset == 136
     assert native.LayerDesc.weight2.offset == 144 and native.LayerDesc.bias2.offset == 152
-    assert ctypes.sizeof(native.LayerDesc) == 160
+    assert native.LayerDesc.setup_stream.offset == 160
+    assert ctypes.sizeof(native.LayerDesc) == 168
     assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 2 * 8
 
 
