@@ -82,6 +82,36 @@ def test_binding_structs_match_header_layout(native):
     assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 2 * 8
 
 
+def test_binding_structs_match_compiled_header(native, tmp_path):
+    """Every field offset and struct size of the binding's structures equals
+    what a C compiler makes of include/taurus.h."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"taurus_graph": native.Graph, "taurus_layer_desc": native.LayerDesc,
+               "taurus_stats": native.Stats, "taurus_stream_stats": native.StreamStats}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", f'#include "{HEADER}"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'    printf("{cname} sizeof %zu\\n", sizeof({cname}));')
+        for field, _ in py._fields_:
+            lines.append(f'    printf("{cname} {field} %zu\\n", offsetof({cname}, {field}));')
+    lines += ["    return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c11", "-o", str(exe), str(src)], check=True, capture_output=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.splitlines():
+        cname, field, value = line.split()
+        got[(cname, field)] = int(value)
+    for cname, py in structs.items():
+        assert got[(cname, "sizeof")] == ctypes.sizeof(py), cname
+        for field, _ in py._fields_:
+            assert got[(cname, field)] == getattr(py, field).offset, (cname, field)
+
+
 def test_hash_matches_published_splitmix64(golden_dir):
     from paper_2607_17374_amd.api import hash_u64
     G = 0x9e3779b97f4a7c15
