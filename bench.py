@@ -516,7 +516,7 @@ def bench_rmat_1m(args):
     fm = flush_model(src, dst, w.n, w.chunk)
     setup = torch.cuda.Stream()
 
-    def step():
+    def step(prof):
         t0 = time.perf_counter()
         row_off, col_dst = T.build_csr(w.n, src_d, dst_d)
         t_csr = time.perf_counter() - t0
@@ -530,7 +530,7 @@ def bench_rmat_1m(args):
             # a later layer is set up on a stream of its own, beside the
             # previous layer's queued chunks
             t = time.perf_counter()
-            L = T.Layer(w.n, row_off, col_dst, out=outs[li], chunk=w.chunk, profile=profile, plan=plan,
+            L = T.Layer(w.n, row_off, col_dst, out=outs[li], chunk=w.chunk, profile=prof, plan=plan,
                         setup_stream=setup if li > 0 else None, **specs[li])
             return L, time.perf_counter() - t
 
@@ -538,8 +538,7 @@ def bench_rmat_1m(args):
         for li in range(len(specs)):
             tl = time.perf_counter()
             L.push_all(h)
-            # the next layer's set-up is host work that overlaps this layer's
-            # queued chunks (its kernels run after them on the same stream)
+            # the next layer's set-up runs beside this layer's queued chunks
             nxt = make(li + 1) if li + 1 < len(specs) else None
             st = L.finalize()
             L.destroy()
@@ -555,10 +554,12 @@ def bench_rmat_1m(args):
         return t_csr * 1e3, t_plan * 1e3, per
 
     for _ in range(args.warmup):
-        step()
+        step(profile)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    runs = [step() for _ in range(args.steps)]
+    # per-kernel events in the first timed step only: each event pair costs
+    # about 6 us of the step
+    runs = [step(profile if i == 0 else 0) for i in range(args.steps)]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = elapsed * 1e3 / args.steps
@@ -584,18 +585,20 @@ def bench_rmat_1m(args):
         if not all(checks):
             model_ok = False
             print(f"warning: layer {li + 1} work counts differ from the flush model: {checks}", file=sys.stderr)
-        ms = {k: float(np.mean([s[f"ms_{k}"] for s in sts]))
-              for k in ("gemm", "scatter", "fixup", "init", "index")}
+        prof = sts[:1] if profile else []  # the step with events
+        timed = ("gemm", "scatter", "fixup")
+        ms = {k: float(np.mean([s[f"ms_{k}"] for s in (prof if k in timed else sts)])) if (prof or k not in timed)
+              else 0.0 for k in ("gemm", "scatter", "fixup", "init", "index")}
         # GAT aggregates in its own passes; GIN's perceptron writes a completed
         # row into its accumulator row instead of the output, the same bytes
-        if profile and not sampled and agg != WL.GAT_ATT:
+        if prof and not sampled and agg != WL.GAT_ATT:
             for k in tot:
-                tot[k][0] += kb[k] * len(sts)
-                tot[k][1] += sum(s[f"ms_{k}"] for s in sts)
-                tot[k][2] += sum(s[f"launches_{k}"] for s in sts)
-        if profile:
-            gemm_flops += 2.0 * w.n * d_in * ncols * len(sts)
-            gemm_ms += sum(s["ms_gemm"] for s in sts)
+                tot[k][0] += kb[k] * len(prof)
+                tot[k][1] += sum(s[f"ms_{k}"] for s in prof)
+                tot[k][2] += sum(s[f"launches_{k}"] for s in prof)
+        if prof:
+            gemm_flops += 2.0 * w.n * d_in * ncols * len(prof)
+            gemm_ms += sum(s["ms_gemm"] for s in prof)
         layers.append({
             "layer": li + 1, "d_in": d_in, "d_out": d_o, "edges": st["messages"], "pairs": st["pairs"],
             "wall_ms": round(wall, 3), "gteps": round(st["messages"] / (wall * 1e-3) / 1e9, 3),
@@ -798,7 +801,9 @@ def bench_sage3_100m(args):
         layers_pass(profile)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    runs = [layers_pass(profile) for _ in range(args.steps)]
+    # events around the scatter launches in the first timed pass only: each
+    # event pair costs about 6 us of the step
+    runs = [layers_pass(profile if i == 0 else 0) for i in range(args.steps)]
     torch.cuda.synchronize()
     layers_ms = (time.perf_counter() - t0) * 1e3 / args.steps
     ms_step = csr_ms + layers_ms
@@ -814,11 +819,12 @@ def bench_sage3_100m(args):
         ob = 4 if specs[li]["out_dtype"] == F.F32 else 2
         wall = float(np.mean([x["wall_ms"] for x in sts]))
         kb = sampled_scatter_bytes(st, w.n, d_o, ob, sage=True)
-        ms_sc = float(np.mean([x["ms_scatter"] for x in sts]))
-        if profile:
-            sc_bytes += kb * len(sts)
-            sc_ms += sum(x["ms_scatter"] for x in sts)
-            sc_launches += sum(x["launches_scatter"] for x in sts)
+        prof = sts[:1] if profile else []  # the pass with events
+        ms_sc = float(np.mean([x["ms_scatter"] for x in prof])) if prof else 0.0
+        if prof:
+            sc_bytes += kb * len(prof)
+            sc_ms += sum(x["ms_scatter"] for x in prof)
+            sc_launches += sum(x["launches_scatter"] for x in prof)
         layers.append({
             "layer": li + 1, "d_in": d_in, "d_out": d_o, "fanout": specs[li]["fanout"], "edges": st["messages"],
             "pairs": st["pairs"], "wall_ms": round(wall, 3), "gteps": round(st["messages"] / (wall * 1e-3) / 1e9, 4),
