@@ -37,11 +37,16 @@ __global__ __launch_bounds__(256) void k_pack_edges(const int32_t* __restrict__ 
 }
 
 // col_dst from the sorted keys; a key equal to its predecessor is a repeat.
-// Also the row offsets: edge i is the first of every row after its
-// predecessor's up to its own (row_off[w] = i for those w), and the last
-// edge ends the rows after it (row_off[w] = e up to w = n).  Sources of the
-// sorted keys are below n (an out-of-range id was packed as key 0 and
-// flagged), so every write stays in [0, n].
+// Also the row offsets (row_off filled with -1 beforehand): edge i is the
+// first of its row u when its predecessor's row up differs, so row_off[u] =
+// i, and so is every empty row between up and u when there are at most
+// GAP_INLINE of them; the last edge ends the rows after it (row_off[w] = e,
+// w up to n) the same way.  Longer runs of empty rows stay -1 for
+// k_row_offsets_fill (a thread looping over millions of them, as after a
+// relabelling that puts the vertices without out-edges last, took 0.5 s).
+// Sources of the sorted keys are below n (an out-of-range id was packed as
+// key 0 and flagged), so every write stays in [0, n].
+constexpr int64_t GAP_INLINE = 16;
 __global__ void k_unpack_cols(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
                               int32_t* __restrict__ col_dst, int64_t* __restrict__ row_off, int* __restrict__ bad) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -52,24 +57,40 @@ __global__ void k_unpack_cols(const uint64_t* __restrict__ keys, int64_t e, int6
     if (i > 0 && kp == k) atomicOr(bad, 2);
     const int64_t u = min((int64_t)(k >> vbits), n - 1);
     const int64_t up = i > 0 ? min((int64_t)(kp >> vbits), n - 1) : -1;
-    for (int64_t w = up + 1; w <= u; w++) row_off[w] = i;
-    if (i == e - 1)
-        for (int64_t w = u + 1; w <= n; w++) row_off[w] = e;
+    if (up < u) {
+        row_off[u] = i;
+        if (u - up <= GAP_INLINE)
+            for (int64_t w = up + 1; w < u; w++) row_off[w] = i;
+    }
+    if (i == e - 1) {
+        row_off[n] = e;
+        if (n - u <= GAP_INLINE)
+            for (int64_t w = u + 1; w < n; w++) row_off[w] = e;
+    }
 }
 
 // row_off[u] = first position whose source is >= u (binary search), u in [0, n]
-__global__ void k_row_offsets(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
-                              int64_t* __restrict__ row_off) {
-    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (u > n) return;
-    const uint64_t target = (uint64_t)u << vbits;
+__device__ inline int64_t first_key_at_least(const uint64_t* __restrict__ keys, int64_t e, uint64_t target) {
     int64_t lo = 0, hi = e;
     while (lo < hi) {
         const int64_t mid = lo + ((hi - lo) >> 1);
         if (keys[mid] < target) lo = mid + 1;
         else hi = mid;
     }
-    row_off[u] = lo;
+    return lo;
+}
+__global__ void k_row_offsets(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
+                              int64_t* __restrict__ row_off) {
+    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (u > n) return;
+    row_off[u] = first_key_at_least(keys, e, (uint64_t)u << vbits);
+}
+// the rows k_unpack_cols left at -1 (long runs of empty rows)
+__global__ void k_row_offsets_fill(const uint64_t* __restrict__ keys, int64_t e, int64_t n, int vbits,
+                                   int64_t* __restrict__ row_off) {
+    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (u > n || row_off[u] >= 0) return;
+    row_off[u] = first_key_at_least(keys, e, (uint64_t)u << vbits);
 }
 
 // Enqueues the build with every temporary from `arena`; returns the device
@@ -89,7 +110,10 @@ static int* enqueue_build_csr(Arena& arena, int64_t n, int64_t e, const int32_t*
         k_pack_edges<<<(unsigned)tiles, 256, 0, s>>>(src, dst, e, n, vbits, sb.keys[0], bad, hist0, tiles);
         TAURUS_CHECK_LAUNCH();
         radix_sort_u64(sb, e, 2 * vbits, arena, s, bad, 4, hist0);
+        fill_i32(reinterpret_cast<int32_t*>(row_off), 2 * (n + 1), -1, s);
         k_unpack_cols<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, col_dst, row_off, bad);
+        TAURUS_CHECK_LAUNCH();
+        k_row_offsets_fill<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);
         TAURUS_CHECK_LAUNCH();
     } else {
         k_row_offsets<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, vbits, row_off);

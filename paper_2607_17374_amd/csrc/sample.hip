@@ -97,19 +97,42 @@ __global__ void k_heavy_list(const int32_t* __restrict__ flag, const int64_t* __
     if (v < n && flag[v]) heavy[pos[v]] = (int32_t)v;
 }
 
-// in_off from the sorted destinations (e >= 1): position i is the first of
-// every destination after its predecessor's up to its own (in_off[w] = i
-// for those w), and the last position ends the destinations after it
-// (in_off[w] = e up to w = n).  Destinations are below n (the CSR was
-// checked), clamped so that every write stays in [0, n].
+// in_off from the sorted destinations (e >= 1; in_off filled with -1
+// beforehand), as the CSR build's row offsets: position i starts its
+// destination v when its predecessor's destination differs, and so every
+// empty destination in between when there are at most CSC_GAP_INLINE; the
+// last position ends the rest the same way.  Longer runs stay -1 for
+// k_csc_offsets_fill.  Destinations are below n (the CSR was checked),
+// clamped so that every write stays in [0, n].
+constexpr int64_t CSC_GAP_INLINE = 16;
 __global__ void k_csc_offsets(const uint32_t* __restrict__ keys, int64_t e, int64_t n, int64_t* __restrict__ in_off) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= e) return;
     const int64_t v = min((int64_t)keys[i], n - 1);
     const int64_t vp = i > 0 ? min((int64_t)keys[i - 1], n - 1) : -1;
-    for (int64_t w = vp + 1; w <= v; w++) in_off[w] = i;
-    if (i == e - 1)
-        for (int64_t w = v + 1; w <= n; w++) in_off[w] = e;
+    if (vp < v) {
+        in_off[v] = i;
+        if (v - vp <= CSC_GAP_INLINE)
+            for (int64_t w = vp + 1; w < v; w++) in_off[w] = i;
+    }
+    if (i == e - 1) {
+        in_off[n] = e;
+        if (n - v <= CSC_GAP_INLINE)
+            for (int64_t w = v + 1; w < n; w++) in_off[w] = e;
+    }
+}
+// the destinations k_csc_offsets left at -1: first position >= v (binary search)
+__global__ void k_csc_offsets_fill(const uint32_t* __restrict__ keys, int64_t e, int64_t n,
+                                   int64_t* __restrict__ in_off) {
+    const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (v > n || in_off[v] >= 0) return;
+    int64_t lo = 0, hi = e;
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if ((int64_t)keys[mid] < v) lo = mid + 1;
+        else hi = mid;
+    }
+    in_off[v] = lo;
 }
 
 std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scratch) {
@@ -135,7 +158,10 @@ std::shared_ptr<Csc> build_csc(const taurus_graph& g, hipStream_t s, Arena* scra
         radix_sort_u32(sb, e, std::max(1, bits_for(n - 1)), tmp, s, bad, 8);
         c->in_src = reinterpret_cast<int32_t*>(sb.vals[sb.cur]);
         c->arena.free_ptr(sb.vals[1 - sb.cur]);
+        fill_i32(reinterpret_cast<int32_t*>(c->in_off), 2 * (n + 1), -1, s);
         k_csc_offsets<<<(unsigned)ceil_div(e, T), T, 0, s>>>(sb.keys[sb.cur], e, n, c->in_off);
+        TAURUS_CHECK_LAUNCH();
+        k_csc_offsets_fill<<<(unsigned)ceil_div(n + 1, T), T, 0, s>>>(sb.keys[sb.cur], e, n, c->in_off);
         TAURUS_CHECK_LAUNCH();
     } else {
         fill_i32(reinterpret_cast<int32_t*>(c->in_off), 2 * (n + 1), 0, s);
