@@ -25,6 +25,23 @@ __host__ __device__ inline uint64_t sample_prefix(uint64_t seed, uint64_t layer,
 }
 __host__ __device__ inline uint64_t sample_key(uint64_t prefix, uint64_t u) { return mix64(prefix + SM64_GAMMA + u); }
 
+// Slot in a list of length *count for each lane that appends one entry
+// (want): the wave's appending lanes take consecutive slots with a single
+// atomic, so a list that grows by millions of entries does not serialise on
+// its counter.  Lanes that do not append get 0 and must ignore it.  Call from
+// every active lane that may append.
+template <class C>
+__device__ inline C wave_append(bool want, C* count) {
+    const uint64_t b = __ballot(want);
+    if (!b) return 0;
+    const int lane = threadIdx.x & 63;
+    const int lead = __builtin_ctzll(b);
+    C base = 0;
+    if (lane == lead) base = atomicAdd(count, (C)__popcll(b));
+    base = __shfl(base, lead);
+    return base + (C)__popcll(b & ((1ull << lane) - 1ull));
+}
+
 // Row of CSR edge t for a whole wave (every lane passes the same t): the
 // largest u in [0, n) with row_off[u] <= t, by a 64-ary search (every lane
 // probes at once, ~log64(n) dependent loads).  All probes stay in [0, n].

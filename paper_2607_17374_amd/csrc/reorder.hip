@@ -127,10 +127,13 @@ __global__ void k_roots(const int32_t* __restrict__ label, const int32_t* __rest
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v >= n) return;
     const int32_t r = rank[v];
-    if (label[v] != r) return;
-    pos[v] = (int32_t)off[r];
-    next[r] = 1;
-    frontier[atomicAdd(count, 1ull)] = (int32_t)v;
+    const bool root = label[v] == r;
+    if (root) {
+        pos[v] = (int32_t)off[r];
+        next[r] = 1;
+    }
+    const unsigned long long at = wave_append(root, count);
+    if (root) frontier[at] = (int32_t)v;
 }
 
 // One wave per frontier vertex x: each unvisited neighbour w (x's search
@@ -148,9 +151,13 @@ __global__ __launch_bounds__(256) void k_expand(const int32_t* __restrict__ fron
     const int32_t px = pos[x], lx = label[x];
     for (int64_t k = in_off[x] + lane; k < in_off[x + 1]; k += 64) {
         const int32_t w = in_src[k];
-        if (pos[w] >= 0 || label[w] != lx) continue;
-        atomicMin(&claim[w], px);
-        if (atomicExch(&listed[w], 1) == 0) cand[atomicAdd(count, 1ull)] = w;
+        bool add = false;
+        if (pos[w] < 0 && label[w] == lx) {
+            atomicMin(&claim[w], px);
+            add = atomicExch(&listed[w], 1) == 0;
+        }
+        const unsigned long long at = wave_append(add, count);
+        if (add) cand[at] = w;
     }
 }
 

@@ -57,7 +57,9 @@ __global__ void k_res_collect(ResChunk c, int64_t total, int32_t k, const int32_
     if (t >= total) return;
     const int v = dest_of(c, t);
     dc_mark[v] = k;
-    if (slot_of[v] < 0 && cnt[v].x > 0 && atomicExch(&want[v], 1) == 0) need[atomicAdd(need_count, 1ull)] = v;
+    const bool add = slot_of[v] < 0 && cnt[v].x > 0 && atomicExch(&want[v], 1) == 0;
+    const unsigned long long at = wave_append(add, need_count);
+    if (add) need[at] = v;
 }
 
 __device__ inline bool res_candidate(int v, int32_t k, const int32_t* slot_of, const uint8_t* hub,
@@ -141,7 +143,9 @@ __global__ void k_res_victims(int64_t n, int32_t k, int32_t tau, int64_t tie_tak
     const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (v >= n || !res_candidate((int)v, k, slot_of, hub, e.dc_mark, e.cnt)) return;
     const int b = res_key((int)v, k, e);
-    if (b < tau || (b == tau && tie_rank[v] < tie_take)) victims[atomicAdd(count, 1ull)] = (int32_t)v;
+    const bool add = b < tau || (b == tau && tie_rank[v] < tie_take);
+    const unsigned long long at = wave_append(add, count);
+    if (add) victims[at] = (int32_t)v;
 }
 
 // one wave per victim: row to the host store, slot back to the free list
@@ -222,7 +226,8 @@ __global__ void k_res_release(ResChunk c, int64_t total, const int2* __restrict_
     const int v = dest_of(c, t);
     if (cnt[v].x != 0 || hub[v]) return;
     const int32_t s = atomicExch(&slot_of[v], -1);
-    if (s >= 0) free_list[atomicAdd(free_top, 1)] = s;
+    const int32_t at = wave_append(s >= 0, free_top);
+    if (s >= 0) free_list[at] = s;
 }
 
 __global__ void k_res_set(int32_t* __restrict__ p, int32_t v) { *p = v; }
