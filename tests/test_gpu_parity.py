@@ -36,7 +36,10 @@ def _random_simple_graph(rng, n, e):
 
 # ------------------------------------------------------------------ CSR ----
 
-@pytest.mark.parametrize("n,e,seed", [(1, 0, 0), (5, 0, 1), (37, 200, 2), (1000, 20000, 3), (70000, 400000, 4)])
+# the last case is sparse: runs of hundreds of empty rows between edges, the
+# row offsets of long runs filled by the build's second pass
+@pytest.mark.parametrize("n,e,seed", [(1, 0, 0), (5, 0, 1), (37, 200, 2), (1000, 20000, 3), (70000, 400000, 4),
+                                      (1 << 20, 30000, 6)])
 def test_csr_random_bit_exact(torch_cuda, n, e, seed):
     import oracle as O
     _note(f"csr random n={n} e={e} seed={seed}")
@@ -264,6 +267,28 @@ def test_edgeless_and_isolated(torch_cuda):
     row_off, col_dst = H.gpu_graph(w, src, dst)
     outs, _ = H.gpu_model(w, row_off, col_dst)
     _check_model(w, outs, zs, "edgeless")
+
+
+@pytest.mark.parametrize("fanouts", [(), (3, 2)], ids=["exact", "sampled"])
+def test_sparse_graph_models(torch_cuda, fanouts):
+    """A graph far sparser than a tile of 4,096 edges is rows (1M vertices,
+    30K edges): the item kernels find rows by searching row_off between a
+    tile's first and last rows, and the CSR and in-edge offsets fill long
+    runs of empty rows in their second pass.  Both GraphSAGE layers, exact
+    and sampled, equal the oracle."""
+    import dataclasses
+    _note(f"sparse graph fanouts={fanouts}")
+    rng = np.random.default_rng(11)
+    n, e = 1 << 20, 30000
+    src, dst = _random_simple_graph(rng, n, e)
+    w = dataclasses.replace(WL.SAGE_RMAT_4K.scaled(n, len(src), chunk=65536), fanouts=fanouts,
+                            name=f"sparse-{len(fanouts)}")
+    _, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    outs, stats = H.gpu_model(w, row_off, col_dst)
+    _check_model(w, outs, zs, w.name)
+    for st in stats:
+        assert st["pending_left"] == 0 and st["completed"] == w.n
 
 
 # --------------------------------------------------------- error paths -----
