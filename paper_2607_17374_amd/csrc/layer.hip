@@ -600,9 +600,9 @@ __host__ __device__ constexpr int self_batch_rows(int vec, bool lean = false) {
 // Gathers of rows of the chunk transform go through a buffer resource: a
 // slot is the 32-bit byte offset of its row in Y, and an offset past the end
 // of Y (NO_ROW, an empty slot) reads as zeros, so no load is predicated.  A
-// lane reads columns (j*G + lane)*4 .. +3 of the row for j < VEC; columns at
-// or past d_o (widths that do not fill G*VEC float4) hold neighbouring data
-// and are never stored.
+// lane reads columns (j*G + lane)*4 .. +3 of the row for j < VEC; a lane
+// whose columns are at or past d_o (widths that do not fill G*VEC float4)
+// takes NO_ROW's offset instead and reads zeros.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 constexpr uint32_t NO_ROW = 0x7fffff00u;   // > any y_bytes; NO_ROW + a row's bytes stays below 2^32
 
