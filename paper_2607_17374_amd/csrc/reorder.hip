@@ -60,31 +60,43 @@ __global__ void k_ranks(const uint32_t* __restrict__ order, int64_t n, int32_t* 
 }
 
 // label[u] = min(label[u], label[v]) over edges (u, v): u reaches all v
-// reaches.  Edges of one row are contiguous, so each wave reduces runs of
-// equal u with shuffles first and issues one atomic per run.
+// reaches.  A workgroup takes LE_TILE consecutive edges (rows found through
+// tile_rows), 64 consecutive ones per wave at a time; edges of one row are
+// contiguous, so each wave reduces runs of equal u with shuffles first and
+// issues one atomic per run.
+constexpr int LE_ITEMS = 16, LE_TILE = 256 * LE_ITEMS, LE_ROWS = 8192;
 __global__ __launch_bounds__(256) void k_label_edges(const int64_t* __restrict__ row_off,
                                                      const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
                                                      int32_t* __restrict__ label, int* __restrict__ changed) {
-    __shared__ int64_t ro[4][64];
+    __shared__ int32_t ro[LE_ROWS + 1];
+    __shared__ int64_t bnd[2];
     const int lane = threadIdx.x & 63;
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
-    const bool valid = i < e;
-    int32_t m = valid ? label[col_dst[i]] : INT32_MAX;
-    // inclusive segmented minimum over lanes with the same u
+    const int64_t i0 = (int64_t)blockIdx.x * LE_TILE, i1 = min(i0 + LE_TILE, e);
+    const TileRows t = tile_rows<LE_ROWS, LE_TILE>(row_off, n, i0, i1, ro, bnd);
+    bool any = false;
+    for (int r = 0; r < LE_ITEMS; r++) {
+        if (i0 + (int64_t)r * 256 >= i1) break;  // uniform over the workgroup
+        const int64_t i = i0 + (int64_t)r * 256 + threadIdx.x;
+        const bool valid = i < i1;
+        bool later;
+        const int64_t u = valid ? tile_row_of(t, row_off, ro, i0, i, later) : -1;
+        int32_t m = valid ? label[col_dst[i]] : INT32_MAX;
+        // inclusive segmented minimum over lanes with the same u
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int32_t om = __shfl_up(m, d, 64);
-        const int64_t ou = __shfl_up(u, d, 64);
-        if (lane >= d && ou == u) m = min(m, om);
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t om = __shfl_up(m, d, 64);
+            const int64_t ou = __shfl_up(u, d, 64);
+            if (lane >= d && ou == u) m = min(m, om);
+        }
+        const int64_t nu = __shfl_down(u, 1, 64);
+        const bool next_valid = __shfl_down((int)valid, 1, 64) != 0;
+        const bool last = valid && (lane == 63 || !next_valid || nu != u);
+        if (last && m < label[u]) {
+            atomicMin(&label[u], m);
+            any = true;
+        }
     }
-    const int64_t nu = __shfl_down(u, 1, 64);
-    const bool next_valid = __shfl_down((int)valid, 1, 64) != 0;
-    const bool last = valid && (lane == 63 || !next_valid || nu != u);
-    if (last && m < label[u]) {
-        atomicMin(&label[u], m);
-        *changed = 1;
-    }
+    if (any) *changed = 1;
 }
 
 // shortcut: v reaches the root of rank label[v], hence everything that root
@@ -250,7 +262,7 @@ static void search_order(int64_t n, const Search& sp, int32_t* new_of_old, hipSt
         if (iter > 4 * n + 8) fail(TAURUS_E_DEVICE, "reorder: owner labels did not converge");
         fill_i32(flag, 1, 0, s);
         if (e > 0) {
-            k_label_edges<<<blocks(e), T, 0, s>>>(sp.reach_off, sp.reach_adj, n, e, label, flag);
+            k_label_edges<<<(unsigned)ceil_div(e, LE_TILE), T, 0, s>>>(sp.reach_off, sp.reach_adj, n, e, label, flag);
             TAURUS_CHECK_LAUNCH();
         }
         k_label_jump<<<blocks(n), T, 0, s>>>(order, n, label, flag);
@@ -430,16 +442,25 @@ int reorder_rcm_impl(const taurus_graph& g, int32_t* new_of_old, hipStream_t s) 
 }
 
 // ------------------------------------------------------------- relabel -----
+// edge i of the CSR in the new numbering; LE_TILE edges per workgroup, rows
+// found through tile_rows
 __global__ __launch_bounds__(256) void k_relabel_edges(const int64_t* __restrict__ row_off,
                                                        const int32_t* __restrict__ col_dst, int64_t n, int64_t e,
                                                        const int32_t* __restrict__ new_of_old,
                                                        int32_t* __restrict__ src, int32_t* __restrict__ dst) {
-    __shared__ int64_t ro[4][64];
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t u = wave_edge_row(row_off, n, i, ro[threadIdx.x >> 6]);
-    if (i >= e) return;
-    src[i] = new_of_old[u];
-    dst[i] = new_of_old[col_dst[i]];
+    __shared__ int32_t ro[LE_ROWS + 1];
+    __shared__ int64_t bnd[2];
+    const int64_t i0 = (int64_t)blockIdx.x * LE_TILE, i1 = min(i0 + LE_TILE, e);
+    const TileRows t = tile_rows<LE_ROWS, LE_TILE>(row_off, n, i0, i1, ro, bnd);
+#pragma unroll 4
+    for (int r = 0; r < LE_ITEMS; r++) {
+        const int64_t i = i0 + (int64_t)r * 256 + threadIdx.x;
+        if (i >= i1) break;
+        bool later;
+        const int64_t u = tile_row_of(t, row_off, ro, i0, i, later);
+        src[i] = new_of_old[u];
+        dst[i] = new_of_old[col_dst[i]];
+    }
 }
 
 __global__ void k_check_perm(const int32_t* __restrict__ p, int64_t n, int32_t* __restrict__ seen,
@@ -472,8 +493,8 @@ int relabel_impl(const taurus_graph& g, const int32_t* new_of_old, int64_t* row_
     int32_t* src = tmp.alloc<int32_t>(std::max<int64_t>(1, g.e), "relabelled sources");
     int32_t* dst = tmp.alloc<int32_t>(std::max<int64_t>(1, g.e), "relabelled destinations");
     if (g.e > 0) {
-        k_relabel_edges<<<(unsigned)ceil_div(g.e, 256), 256, 0, s>>>(g.row_off, g.col_dst, g.n, g.e, new_of_old, src,
-                                                                     dst);
+        k_relabel_edges<<<(unsigned)ceil_div(g.e, LE_TILE), 256, 0, s>>>(g.row_off, g.col_dst, g.n, g.e, new_of_old,
+                                                                         src, dst);
         TAURUS_CHECK_LAUNCH();
     }
     return build_csr_impl(g.n, g.e, src, dst, row_off, col_dst, s);
