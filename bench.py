@@ -669,15 +669,39 @@ def sampled_scatter_bytes(st: dict, n: int, d_o: int, out_bytes: int, sage: bool
     read and written); the accumulator row read on every flush but a
     vertex's first and written on every flush but its last (a vertex's first
     and last flush are one each of its P flushes), and its output row once.
+    In-core GraphSAGE layers take the self messages of the A vertices
+    without a segment from their own chunk in the transform (A =
+    self_in_transform, of which self_fresh found nothing accumulated and
+    self_last completed the vertex, counted in a profiled run): the scatter
+    then reads no self row for them and only updates their counts (12), and
+    the transform_self_bytes of those flushes leave its total.
     Exact when no segment is split into pieces, which holds for fanouts up to
     15 (a segment then holds at most 15 messages and the self message)."""
     if st["split_segments"]:
         raise ValueError("the byte model holds for layers without split segments")
     P = st["pairs"]
+    A = st.get("self_in_transform", 0)
+    if A and not (st["self_fresh"] or st["self_last"]):
+        raise ValueError("the self-message counts are taken in profiled runs only")
     units = st["short_units"] + st["wave_units"]
-    y_rows = n * (2 if sage else 1)
+    y_rows = n * (2 if sage else 1) - A
     return (16.0 * units + 4.0 * st["messages"] + 4.0 * d_o * y_rows + 1.0 * n + 12.0 * P
-            + 8.0 * d_o * (P - n) + out_bytes * d_o * n)
+            + 8.0 * d_o * (P - n) + out_bytes * d_o * n - transform_self_bytes(st, d_o, out_bytes, counts=False))
+
+
+def transform_self_bytes(st: dict, d_o: int, out_bytes: int, counts: bool = True) -> float:
+    """Accumulator and output bytes of the self messages an in-core
+    GraphSAGE layer's transform takes (none otherwise): each reads the row
+    (4 d_o) unless it found nothing accumulated, and writes it (4 d_o) or,
+    as the vertex's last arrival, the output row (out_bytes d_o); with
+    counts, also each such vertex's flag byte and counts (9) that the
+    transform reads."""
+    A = st.get("self_in_transform", 0)
+    if not A:
+        return 0.0
+    fresh, last = st["self_fresh"], st["self_last"]
+    return (4.0 * d_o * (A - fresh) + 4.0 * d_o * (A - last) + out_bytes * d_o * last
+            + (9.0 * A if counts else 0.0))
 
 
 def _cpu_model() -> str:
@@ -818,8 +842,8 @@ def bench_sage3_100m(args):
         d_o, d_in = specs[li]["d_out"], specs[li]["d_in"]
         ob = 4 if specs[li]["out_dtype"] == F.F32 else 2
         wall = float(np.mean([x["wall_ms"] for x in sts]))
-        kb = sampled_scatter_bytes(st, w.n, d_o, ob, sage=True)
-        prof = sts[:1] if profile else []  # the pass with events
+        prof = sts[:1] if profile else []  # the pass with events (and the self-message counts)
+        kb = sampled_scatter_bytes(prof[0], w.n, d_o, ob, sage=True) if prof else None
         ms_sc = float(np.mean([x["ms_scatter"] for x in prof])) if prof else 0.0
         if prof:
             sc_bytes += kb * len(prof)
@@ -831,8 +855,9 @@ def bench_sage3_100m(args):
             "vertices_per_s": round(w.n / (wall * 1e-3), 1),
             "init_ms": round(float(np.mean([x["ms_init"] for x in sts])), 3),
             "sample_and_index_ms": round(float(np.mean([x["ms_index"] for x in sts])), 3),
-            "scatter_ms": round(ms_sc, 3), "scatter_algorithmic_gb": round(kb / 1e9, 3),
-            "scatter_gbs": round(kb / (ms_sc * 1e-3) / 1e9, 1) if ms_sc > 0 else None,
+            "scatter_ms": round(ms_sc, 3), "scatter_algorithmic_gb": round(kb / 1e9, 3) if kb else None,
+            "scatter_gbs": round(kb / (ms_sc * 1e-3) / 1e9, 1) if ms_sc > 0 and kb else None,
+            "self_in_transform": st["self_in_transform"],
             "short_units": st["short_units"], "wave_units": st["wave_units"],
         })
     total_edges = sum(l["edges"] for l in layers)
@@ -884,7 +909,12 @@ def bench_sage3_100m(args):
     for li, st in enumerate(per):
         d_in, d_o = specs[li]["d_in"], specs[li]["d_out"]
         gf += 2.0 * w.n * d_in * 2 * d_o
-        gb += w.n * d_in * 2.0 + w.n * 2 * d_o * 4.0       # bf16 rows in, fp32 transform rows out
+        # bf16 rows in, fp32 transform rows out (the self half only for the
+        # vertices whose self message is a segment slot), and the self
+        # messages the transform takes
+        A = st["self_in_transform"]
+        ob = 4 if specs[li]["out_dtype"] == F.F32 else 2
+        gb += w.n * d_in * 2.0 + (2 * w.n - A) * d_o * 4.0 + transform_self_bytes(st, d_o, ob)
         gms += st["ms_gemm"]
         layers[li]["gemm_ms"] = round(st["ms_gemm"], 3)
     if gms > 0:

@@ -228,15 +228,25 @@ typedef struct {
     double ms_index;               /* of which: sampling and chunk-index build (0 when
                                       the plan already held the index)                  */
     double ms_gemm, ms_self, ms_scatter, ms_fixup;  /* ms_self stays 0: the self messages
-                                      run inside the scatter launch, timed in ms_scatter.
-                                      In-core fp32 layers run a chunk's hub fix-up in the
-                                      next chunk's transform launch (timed in ms_gemm)
+                                      run inside the scatter launch, timed in ms_scatter,
+                                      or, for in-core GraphSAGE layers, those of vertices
+                                      without a segment from their own chunk inside the
+                                      transform, timed in ms_gemm.
+                                      In-core fp32 GCN and linear-apply GIN layers run a
+                                      chunk's hub fix-up in the next chunk's transform
+                                      launch (timed in ms_gemm)
                                       and the last chunk's at finalize (untimed), so
                                       their ms_fixup stays 0                          */
     int64_t launches_gemm, launches_self, launches_scatter, launches_fixup;
     int64_t pool_rows;             /* budgeted layers: accumulator rows of the pool,
                                       hub rows included (0 in core)                     */
     int64_t hub_rows;              /* of which resident hub rows                        */
+    int64_t self_in_transform;     /* in-core GraphSAGE layers: self messages added by
+                                      the chunk transforms (vertices without a segment
+                                      from their own chunk), 0 otherwise; counted in
+                                      pairs                                             */
+    int64_t self_fresh, self_last; /* of those, when desc.profile != 0 (else 0): found
+                                      nothing accumulated yet / completed the vertex    */
 } taurus_stats;
 
 /*

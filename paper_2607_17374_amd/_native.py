@@ -56,7 +56,8 @@ class Stats(ctypes.Structure):
         ("ms_self", ctypes.c_double), ("ms_scatter", ctypes.c_double), ("ms_fixup", ctypes.c_double),
         ("launches_gemm", ctypes.c_int64), ("launches_self", ctypes.c_int64),
         ("launches_scatter", ctypes.c_int64), ("launches_fixup", ctypes.c_int64),
-        ("pool_rows", ctypes.c_int64), ("hub_rows", ctypes.c_int64)]
+        ("pool_rows", ctypes.c_int64), ("hub_rows", ctypes.c_int64),
+        ("self_in_transform", ctypes.c_int64), ("self_fresh", ctypes.c_int64), ("self_last", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

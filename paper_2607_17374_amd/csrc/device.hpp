@@ -1,10 +1,45 @@
-// Device helpers shared by the chunk index and the fanout sampler.
+// Device helpers shared by the kernel files: the sampler's hash, wave
+// appends, searches for the CSR row of an edge, the chunk index's per-vertex
+// flags and output-row stores.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
 namespace taurus {
+
+// Per-vertex flags of a layer's chunk index.
+constexpr uint8_t OWN_SEGMENT = 1;  // v has a segment from its own chunk
+constexpr uint8_t SELF_FIRST = 2;   // no message to v comes from an earlier chunk
+
+// fp32 to bf16 bits, round to nearest even (a NaN stays a quiet NaN)
+__device__ inline uint32_t f32_to_bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ inline uint32_t f32_to_f16_bits(float f) {
+    const _Float16 h = (_Float16)f;  // v_cvt_f16_f32, round to nearest even
+    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+
+// Four consecutive output values at element idx of out, stored as dtype
+// (0 fp32, 1 bf16, 2 fp16).
+__device__ inline void store_out4(void* out, int dtype, int64_t idx, float4 z) {
+    if (dtype == 0) {
+        *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = z;
+    } else {
+        uint2 p;
+        if (dtype == 1) {
+            p.x = f32_to_bf16_bits(z.x) | (f32_to_bf16_bits(z.y) << 16);
+            p.y = f32_to_bf16_bits(z.z) | (f32_to_bf16_bits(z.w) << 16);
+        } else {
+            p.x = f32_to_f16_bits(z.x) | (f32_to_f16_bits(z.y) << 16);
+            p.y = f32_to_f16_bits(z.z) | (f32_to_f16_bits(z.w) << 16);
+        }
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + idx) = p;
+    }
+}
 
 // SplitMix64 finaliser and increment (Steele, Lea and Flood, OOPSLA 2014).
 constexpr uint64_t SM64_GAMMA = 0x9e3779b97f4a7c15ULL;

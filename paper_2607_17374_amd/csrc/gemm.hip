@@ -82,38 +82,41 @@ template <int DT, int PANEL_NB>
 __global__ __launch_bounds__(256) void k_gemm_panel(const void* __restrict__ X, int64_t M, int K,
                                                     const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP,
                                                     int Nc, const float* __restrict__ rscale,
-                                                    float* __restrict__ Y, int stream) {
+                                                    float* __restrict__ Y, int stream, SelfFlush sf) {
     __shared__ PanelLds<DT, PANEL_NB> lds;
-    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, blockIdx.y, lds, stream != 0);
+    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, blockIdx.y, lds, stream != 0, sf);
 }
 
 template <int DT>
 static void launch_panel(const void* X, int64_t M, int K, const void* Wp, int Nc, const float* rscale, float* Y,
-                         hipStream_t s) {
+                         const SelfFlush* sf, hipStream_t s) {
     const int NBP = gemm_packed_blocks_n(Nc);
     const auto* w = static_cast<const typename GemmOp<DT>::frag*>(Wp);
     const int stream = transform_streams(M, Nc) ? 1 : 0;
+    const SelfFlush f = sf ? *sf : SelfFlush{};
+    if (f.own && (rscale || f.self_col + f.d_o > Nc || f.self_col % 4 || f.d_o % 4))
+        fail(TAURUS_E_INVALID, "self messages in the transform need unscaled rows and a self half inside Y");
     if (NBP <= 4) {
         dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), 1);
-        k_gemm_panel<DT, 4><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream);
+        k_gemm_panel<DT, 4><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream, f);
     } else {
         dim3 grid((unsigned)ceil_div(M, PANEL_ROWS), (unsigned)ceil_div(NBP, 8));
-        k_gemm_panel<DT, 8><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream);
+        k_gemm_panel<DT, 8><<<grid, 256, 0, s>>>(X, M, K, w, NBP, Nc, rscale, Y, stream, f);
     }
     TAURUS_CHECK_LAUNCH();
 }
 
 void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const float* rscale, float* Y,
-              hipStream_t s) {
+              const SelfFlush* sf, hipStream_t s) {
     if (M <= 0) return;
-    launch_panel<TAURUS_F32>(X, M, K, Wp, Nc, rscale, Y, s);
+    launch_panel<TAURUS_F32>(X, M, K, Wp, Nc, rscale, Y, sf, s);
 }
 
 void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
-             float* Y, hipStream_t s) {
+             float* Y, const SelfFlush* sf, hipStream_t s) {
     if (M <= 0) return;
-    if (dtype == TAURUS_BF16) launch_panel<TAURUS_BF16>(X, M, K, Wp, Nc, rscale, Y, s);
-    else launch_panel<TAURUS_F16>(X, M, K, Wp, Nc, rscale, Y, s);
+    if (dtype == TAURUS_BF16) launch_panel<TAURUS_BF16>(X, M, K, Wp, Nc, rscale, Y, sf, s);
+    else launch_panel<TAURUS_F16>(X, M, K, Wp, Nc, rscale, Y, sf, s);
 }
 
 }  // namespace taurus

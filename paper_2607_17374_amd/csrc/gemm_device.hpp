@@ -4,6 +4,7 @@
 // Fragment layouts are described at the top of gemm.hip.
 #pragma once
 
+#include "device.hpp"
 #include "internal.hpp"
 
 namespace taurus {
@@ -206,6 +207,39 @@ __device__ __attribute__((always_inline)) inline void gemm_panel_core(const void
     }
 }
 
+// GraphSAGE self messages taken by the chunk's transform (in-core layers).
+// Vertex v = first_row + r of the chunk whose self message is not a slot of
+// a segment from its own chunk (no OWN_SEGMENT) receives W_self h_v straight
+// from the products of its self-half columns [self_col, self_col + d_o),
+// with weight 1 as in a flush: added to its accumulator row (or written as
+// the row when nothing has arrived yet), or, when it is v's last arrival,
+// finalised into its output row as act(acc + b).  Y then holds only the
+// aggregation half of such rows.  The counts are only read here (a row's
+// columns are split over several workgroups): the scatter that follows
+// takes the self arrival off.  own == nullptr: every row goes to Y.
+struct SelfFlush {
+    const uint8_t* own;   // per vertex: chunk-index flags
+    const int2* cnt;      // per vertex: {pending, expected}
+    float* acc;           // [n][d_o] fp32 accumulator rows
+    void* out;            // [n][d_o] output rows in out_dtype
+    const float* bias;    // [d_o]
+    int64_t first_row;    // first vertex of the chunk
+    int self_col, d_o, relu, out_dtype;
+};
+
+// A column group [c0, c0 + tw) of the products that holds self-half columns.
+__device__ inline bool self_group(const SelfFlush& sf, int c0, int tw) {
+    return sf.own && c0 < sf.self_col + sf.d_o && c0 + tw > sf.self_col;
+}
+
+// What a panel's self messages need to know of its 64 rows, one bit per row
+// (the same in every wave of the workgroup): the row's self message is taken
+// here (no OWN_SEGMENT), nothing has been accumulated for it yet, and it is
+// the row's last arrival.
+struct SelfRows {
+    uint64_t take, fresh, last;
+};
+
 // The products of one panel leave through LDS (the weight buffers are free
 // once the last stage is done): a 64 x 16 PANEL_NB fp32 tile, written in
 // the matrix cores' layout and read back row-major, so that each wave
@@ -221,11 +255,35 @@ template <int DT, int PANEL_NB>
 __device__ __attribute__((always_inline)) inline void store_panel_staged(const floatx4 (&acc)[PANEL_NB],
                                         PanelLds<DT, PANEL_NB>& lds, int64_t M, int Nc,
                                         const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
-                                        bool stream) {
+                                        bool stream, const SelfFlush& sf, const SelfRows& sr) {
     constexpr int TW = PANEL_NB * 16;  // tile width (fp32 columns)
     static_assert(sizeof(lds.b) >= (size_t)PANEL_ROWS * TW * 4, "the weight buffers hold the output tile");
     float* tile = reinterpret_cast<float*>(&lds.b[0][0]);
     const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lk = lane >> 4;
+    const int c0 = by * TW;  // first column of the group
+    constexpr int Q = TW / 4;  // float4 per tile row
+    constexpr int IT = PANEL_ROWS * Q / 256;  // float4 per thread
+    // Thread tid stores float4 i of the tile at row (256 i + tid) / Q, column
+    // 4 ((256 i + tid) % Q) of the group.  A group with self-half columns
+    // (GraphSAGE: rows are not scaled) requests the accumulator pieces its
+    // self messages need before the tile goes through LDS, so that their
+    // loads overlap the staging.
+    const bool selfs = self_group(sf, c0, TW);
+    auto takes = [&](int row, int col) {
+        return col >= sf.self_col && col < sf.self_col + sf.d_o && ((sr.take >> row) & 1);
+    };
+    float4 prev[IT];
+    if (selfs) {
+#pragma unroll
+        for (int i = 0; i < IT; i++) {
+            const int q = i * 256 + tid, row = q / Q, c = (q % Q) * 4;
+            const int64_t grow = (int64_t)bx * PANEL_ROWS + row;
+            const int col = c0 + c;
+            prev[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (grow < M && col < Nc && takes(row, col) && !((sr.fresh >> row) & 1))
+                prev[i] = *reinterpret_cast<const float4*>(sf.acc + (sf.first_row + grow) * sf.d_o + (col - sf.self_col));
+        }
+    }
 #pragma unroll
     for (int r = 0; r < 4; r++) {
         const int row = (tid >> 6) * 16 + 4 * lk + r;
@@ -234,42 +292,78 @@ __device__ __attribute__((always_inline)) inline void store_panel_staged(const f
         for (int j = 0; j < PANEL_NB; j++) tile[row * TW + ((j * 16 + li) ^ sw)] = acc[j][r];
     }
     __syncthreads();
-    const int c0 = by * TW;  // first column of the group
-    constexpr int Q = TW / 4;  // float4 per tile row
+    auto put = [&](float* dst, float4 v) {
+        if (stream)
+            __builtin_nontemporal_store(floatx4{v.x, v.y, v.z, v.w}, reinterpret_cast<floatx4*>(dst));
+        else
+            *reinterpret_cast<float4*>(dst) = v;
+    };
 #pragma unroll
-    for (int i = 0; i < PANEL_ROWS * Q / 256; i++) {
+    for (int i = 0; i < IT; i++) {
         const int q = i * 256 + tid, row = q / Q, c = (q % Q) * 4;
         const int64_t grow = (int64_t)bx * PANEL_ROWS + row;
         const int col = c0 + c;
         if (grow >= M || col >= Nc) continue;
         const int sw = ((row >> 2) & 1) << 4;
-        float4 v = *reinterpret_cast<const float4*>(tile + row * TW + (c ^ sw));
-        if (rscale) {
-            const float sc = rscale[grow];
-            v.x *= sc;
-            v.y *= sc;
-            v.z *= sc;
-            v.w *= sc;
+        float4 x = *reinterpret_cast<const float4*>(tile + row * TW + (c ^ sw));
+        if (!selfs || !takes(row, col)) {
+            if (rscale) {
+                const float sc = rscale[grow];
+                x.x *= sc;
+                x.y *= sc;
+                x.z *= sc;
+                x.w *= sc;
+            }
+            put(Y + grow * Nc + col, x);
+            continue;
         }
-        float* dst = Y + grow * Nc + col;
-        if (stream)
-            __builtin_nontemporal_store(floatx4{v.x, v.y, v.z, v.w}, reinterpret_cast<floatx4*>(dst));
-        else
-            *reinterpret_cast<float4*>(dst) = v;
+        // v's self message: add, or finalise on its last arrival
+        const int64_t v = sf.first_row + grow;
+        const int ac = col - sf.self_col;
+        const float4 t = make_float4(x.x + prev[i].x, x.y + prev[i].y, x.z + prev[i].z, x.w + prev[i].w);
+        if ((sr.last >> row) & 1) {
+            const float4 b = *reinterpret_cast<const float4*>(sf.bias + ac);
+            float4 z = make_float4(t.x + b.x, t.y + b.y, t.z + b.z, t.w + b.w);
+            if (sf.relu) {
+                z.x = fmaxf(z.x, 0.f); z.y = fmaxf(z.y, 0.f);
+                z.z = fmaxf(z.z, 0.f); z.w = fmaxf(z.w, 0.f);
+            }
+            store_out4(sf.out, sf.out_dtype, v * sf.d_o + ac, z);
+        } else {
+            put(sf.acc + v * sf.d_o + ac, t);
+        }
     }
 }
 
 // Y = X W, rows [64 bx, 64 bx + 64) and column blocks [PANEL_NB by,
-// PANEL_NB by + PANEL_NB), through the staged store.
+// PANEL_NB by + PANEL_NB), through the staged store (with the self
+// messages sf takes).
 template <int DT, int PANEL_NB>
 __device__ __attribute__((always_inline)) inline void gemm_panel_block(const void* __restrict__ X, int64_t M, int K,
                                         const typename GemmOp<DT>::frag* __restrict__ Wp, int NBP, int Nc,
                                         const float* __restrict__ rscale, float* __restrict__ Y, int bx, int by,
-                                        PanelLds<DT, PANEL_NB>& lds, bool stream) {
+                                        PanelLds<DT, PANEL_NB>& lds, bool stream, const SelfFlush& sf) {
+    // a group with self messages: lane l of every wave reads row l's flag
+    // and counts, and the wave turns them into SelfRows (uniform, so they
+    // hold no vector registers through the products); the epilogue then
+    // waits on the accumulator rows alone
+    SelfRows sr{0, 0, 0};
+    if (self_group(sf, by * PANEL_NB * 16, PANEL_NB * 16)) {
+        const int64_t r = (int64_t)bx * PANEL_ROWS + (threadIdx.x & 63);
+        uint32_t fl = OWN_SEGMENT;
+        int2 pe = make_int2(0, 0);
+        if (r < M) {
+            fl = sf.own[sf.first_row + r];
+            pe = sf.cnt[sf.first_row + r];
+        }
+        sr.take = __ballot(!(fl & OWN_SEGMENT));
+        sr.fresh = __ballot(pe.x == pe.y);
+        sr.last = __ballot(pe.x == 1);
+    }
     floatx4 acc[PANEL_NB];
     gemm_panel_compute<DT, PANEL_NB>(X, M, K, Wp, NBP, bx, by, lds, [](int64_t r) { return r; }, acc);
     // every wave is past the last stage's barrier: the buffers are free
-    store_panel_staged<DT, PANEL_NB>(acc, lds, M, Nc, rscale, Y, bx, by, stream);
+    store_panel_staged<DT, PANEL_NB>(acc, lds, M, Nc, rscale, Y, bx, by, stream, sf, sr);
 }
 
 }  // namespace taurus

@@ -50,10 +50,10 @@ int build_csr_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst,
 int build_csr_noalloc_impl(int64_t n, int64_t e, const int32_t* src, const int32_t* dst, int64_t* row_off,
                            int32_t* col_dst, hipStream_t s);
 void gemm_f32(const float* X, int64_t M, int K, const float* Wp, int Nc, const float* rscale, float* Y,
-              hipStream_t s);
+              const SelfFlush* sf, hipStream_t s);
 void gemm_pack_weights_f32(const float* W, int K, int Nc, std::vector<float>& packed);
 void gemm_16(const uint16_t* X, int dtype, int64_t M, int K, const uint16_t* Wp, int Nc, const float* rscale,
-             float* Y, hipStream_t s);
+             float* Y, const SelfFlush* sf, hipStream_t s);
 void gemm_pack_weights_16(const float* W, int K, int Nc, int dtype, std::vector<uint16_t>& packed);
 int gemm_packed_blocks_n(int nc);
 const char* last_error_cstr();
@@ -65,9 +65,8 @@ constexpr int NOT_FIRST = 1 << 30;                  // unit.y flags (see seg_uni
 constexpr int SELF_HERE = 1 << 29;
 constexpr int LEN_MASK = SELF_HERE - 1;
 constexpr int NLIST = NCLASS + 2;                   // short classes, wave units, fix-up entries
+constexpr int TALLY_SLOTS = 64;                     // spread of the self-message tallies
 static_assert(RES_LISTS == NCLASS + 1, "residency walks the short classes and the wave units");
-constexpr uint8_t OWN_SEGMENT = 1;                  // per-vertex flags: v has a segment from its own chunk
-constexpr uint8_t SELF_FIRST = 2;                   //   no message to v comes from an earlier chunk
 
 // most slots of a segment in short class c: 1, 2, 4, 8, 16
 __host__ __device__ constexpr int class_len(int c) { return 1 << c; }
@@ -505,6 +504,13 @@ struct ScatterParams {
     // GIN with a perceptron (agg TAURUS_GIN_MLP): a completing destination's
     // hidden row ReLU(acc + b1) replaces its accumulator row; the chunk's
     // graduation transform reads it from there
+    // self_done: the chunk's transform took the self messages of the
+    // vertices without a segment here (SelfFlush); the self pass only takes
+    // their arrival off the count, and, with self_tally set, counts how many
+    // of those self messages found nothing accumulated and how many were the
+    // last arrival ([TALLY_SLOTS][2], summed at finalize)
+    int self_done;
+    unsigned long long* self_tally;
 };
 
 struct ChunkUnits {        // this chunk's slice of the short classes and wave units
@@ -531,32 +537,6 @@ __device__ inline float4 f4_axpy(float s, float4 a, float4 b) {
     return make_float4(fmaf(s, a.x, b.x), fmaf(s, a.y, b.y), fmaf(s, a.z, b.z), fmaf(s, a.w, b.w));
 }
 __device__ inline float4 f4_scale(float s, float4 a) { return make_float4(s * a.x, s * a.y, s * a.z, s * a.w); }
-
-__device__ inline uint32_t f32_to_bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-__device__ inline uint32_t f32_to_f16_bits(float f) {
-    const _Float16 h = (_Float16)f;  // v_cvt_f16_f32, round to nearest even
-    return (uint32_t)__builtin_bit_cast(uint16_t, h);
-}
-
-__device__ inline void store_out4(void* out, int dtype, int64_t idx, float4 z) {
-    if (dtype == 0) {
-        *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = z;
-    } else {
-        uint2 p;
-        if (dtype == 1) {
-            p.x = f32_to_bf16_bits(z.x) | (f32_to_bf16_bits(z.y) << 16);
-            p.y = f32_to_bf16_bits(z.z) | (f32_to_bf16_bits(z.w) << 16);
-        } else {
-            p.x = f32_to_f16_bits(z.x) | (f32_to_f16_bits(z.y) << 16);
-            p.y = f32_to_f16_bits(z.z) | (f32_to_f16_bits(z.w) << 16);
-        }
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + idx) = p;
-    }
-}
 
 __device__ inline float* acc_row(const ScatterParams& p, int v) {
     return p.acc + (int64_t)(p.slot ? p.slot[v] : v) * p.d_o;
@@ -1052,7 +1032,8 @@ __device__ inline void wave_pieces(const ScatterParams& p, const int4* __restric
 // chunk (the others take their self message in their segment's flush): one
 // arrival each.  A row-group takes K consecutive vertices at a time --
 // consecutive rows of Y and of the accumulators.  These vertices have no
-// other flush in the launch.
+// other flush in the launch.  When the transform has already added their
+// self rows (self_done), only the counts are updated.
 template <int G, int VEC, bool ATT, bool LEAN>
 __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
     constexpr int K = self_batch_rows(VEC, LEAN);
@@ -1061,6 +1042,35 @@ __device__ inline void self_batches(const ScatterParams& p, int64_t rot) {
     const int rg = threadIdx.x / G, lane = threadIdx.x % G;
     const int64_t nrg = (int64_t)gridDim.x * NRG;
     const int64_t stride = nrg * K;
+    if (!ATT && p.self_done) {
+        int fresh = 0, last = 0;
+        for (int64_t r0 = phase_first((int64_t)blockIdx.x * NRG + rg, rot, nrg) * K; r0 < p.rows; r0 += stride) {
+#pragma unroll
+            for (int q = 0; q < KD; q++) {
+                const int k = q * G + lane;
+                const int64_t v = p.first_row + r0 + k;
+                if (k < K && r0 + k < p.rows && !(p.has_own[v] & OWN_SEGMENT)) {
+                    const int2 pe = p.cnt[v];
+                    fresh += pe.x == pe.y;
+                    last += pe.x == 1;
+                    p.cnt[v].x = pe.x - 1;
+                }
+            }
+        }
+        if (p.self_tally) {
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) {
+                fresh += __shfl_xor(fresh, o);
+                last += __shfl_xor(last, o);
+            }
+            if ((threadIdx.x & 63) == 0 && (fresh | last)) {
+                unsigned long long* t = p.self_tally + 2 * (blockIdx.x % TALLY_SLOTS);
+                atomicAdd(t, (unsigned long long)fresh);
+                atomicAdd(t + 1, (unsigned long long)last);
+            }
+        }
+        return;
+    }
     const __amdgpu_buffer_rsrc_t rs = y_rsrc(p);
     const int qv = p.d_o >> 2;  // float4 of a row that hold values
     for (int64_t r0 = phase_first((int64_t)blockIdx.x * NRG + rg, rot, nrg) * K; r0 < p.rows; r0 += stride) {
@@ -1773,9 +1783,14 @@ struct taurus_layer {
     float* Y = nullptr;
     float* carry = nullptr;
     int32_t* carry_cnt = nullptr;
-    // in-core fp32 layers run the fix-up of chunk j inside the transform
-    // launch of the next chunk pushed (or at finalize)
+    // in-core fp32 GCN and linear-apply GIN layers run the fix-up of chunk j
+    // inside the transform launch of the next chunk pushed (or at finalize)
     bool fuse_fix = false, fix_pending = false;
+    // in-core GraphSAGE layers: each chunk's transform takes the self
+    // messages of the vertices without a segment from their own chunk
+    // (SelfFlush), so those rows' self halves never pass through Y
+    bool self_in_transform = false;
+    unsigned long long* self_tally = nullptr;  // profiled layers: [TALLY_SLOTS][2]
     taurus::ScatterParams fix_p{};
     const int4* fix_list = nullptr;
     int64_t fix_n = 0;
@@ -2179,7 +2194,15 @@ static void layer_init(taurus_layer* L) {
     }
     // the perceptron's graduation reads every flush of the chunk, the
     // fix-up's included, so its fix-up is not deferred
-    L->fuse_fix = !L->res && !L->gat_hp && d.in_dtype == TAURUS_F32 && d.agg != TAURUS_GIN_MLP;
+    // The transform of a chunk that takes self messages must not run beside
+    // the previous chunk's fix-up, which may flush the same rows
+    L->self_in_transform = d.agg == TAURUS_SAGE_MEAN && !L->res;
+    L->fuse_fix = !L->res && !L->gat_hp && d.in_dtype == TAURUS_F32 && d.agg != TAURUS_GIN_MLP &&
+                  !L->self_in_transform;
+    if (L->self_in_transform && d.profile) {
+        L->self_tally = L->arena.alloc<unsigned long long>(2 * TALLY_SLOTS, "self-message tallies");
+        fill_i32(reinterpret_cast<int32_t*>(L->self_tally), 4 * TALLY_SLOTS, 0, s);
+    }
     if (d.profile) {
         L->events.assign((size_t)L->nchunks * EV_PER_CHUNK, nullptr);
         for (auto& ev : L->events) ev = timing_event_acquire();
@@ -2249,7 +2272,8 @@ __global__ __launch_bounds__(256) void k_transform_fixup(const float* __restrict
     __shared__ PanelLds<TAURUS_F32, NB> lds;
     const int b = (int)blockIdx.x;
     if (b < gblocks) {
-        gemm_panel_block<TAURUS_F32, NB>(X, M, K, Wp, NBP, Nc, rscale, Y, b % gx, b / gx, lds, stream != 0);
+        gemm_panel_block<TAURUS_F32, NB>(X, M, K, Wp, NBP, Nc, rscale, Y, b % gx, b / gx, lds, stream != 0,
+                                         SelfFlush{});
         return;
     }
     fixup_rows<G, VEC>(p, fix, nfix, b - gblocks);
@@ -2321,15 +2345,29 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     const float* rscale = L->n_out ? L->n_out + b : nullptr;
     // GAT: the first pass only, into the layer's table of transformed rows
     float* ydst = L->gat_hp ? L->gat_hp + b * (int64_t)L->ncols : L->Y;
+    SelfFlush sf{};
+    if (L->self_in_transform) {
+        sf.own = idx.has_own;
+        sf.cnt = L->cnt;
+        sf.acc = L->acc;
+        sf.out = L->out_dev;
+        sf.bias = L->bias;
+        sf.first_row = b;
+        sf.self_col = L->d_o;
+        sf.d_o = L->d_o;
+        sf.relu = L->d.relu;
+        sf.out_dtype = L->d.out_dtype;
+    }
+    const SelfFlush* sfp = L->self_in_transform ? &sf : nullptr;
     if (L->d.in_dtype == TAURUS_F32 && L->fix_pending) {
         transform_with_fixup(L->shape, static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ystride, rscale,
                              ydst, L->fix_p, L->fix_list, L->fix_n, s);
         L->fix_pending = false;
     } else if (L->d.in_dtype == TAURUS_F32)
-        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ystride, rscale, ydst, s);
+        gemm_f32(static_cast<const float*>(x), e - b, L->d.d_in, L->wpack, L->ystride, rscale, ydst, sfp, s);
     else
         gemm_16(static_cast<const uint16_t*>(x), L->d.in_dtype, e - b, L->d.d_in,
-                static_cast<const uint16_t*>(L->wpack_any), L->ystride, rscale, ydst, s);
+                static_cast<const uint16_t*>(L->wpack_any), L->ystride, rscale, ydst, sfp, s);
     if (x_on_host) TAURUS_HIP(hipEventRecord(L->gemm_done[(L->host_pushes - 1) & 1], s));
     if (ev[1]) TAURUS_HIP(hipEventRecord(ev[1], s));
     if (L->gat_hp) {  // the attention terms of the chunk's rows; passes 2 and 3 run at finalize
@@ -2360,6 +2398,8 @@ static void push_chunk(taurus_layer* L, int64_t b, int64_t e, const void* x, int
     p.long_base = idx.list_off[NCLASS][(size_t)k];
     p.first_row = b;
     p.rows = e - b;
+    p.self_done = L->self_in_transform ? 1 : 0;
+    p.self_tally = L->self_tally;
     ChunkUnits cu;
     for (int l = 0; l <= NCLASS; l++) {
         cu.u[l] = idx.list_at(l, k);
@@ -2489,9 +2529,11 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
     k_count_pending<<<(unsigned)ceil_div(L->n, 256), 256, 0, s>>>(L->cnt, L->n, dleft);
     TAURUS_CHECK_LAUNCH();
     unsigned long long left = 0, own = 0;
+    std::vector<unsigned long long> tally(L->self_tally ? 2 * TALLY_SLOTS : 0);
     Readback rb;
     rb.add(&left, dleft, 1);
     rb.add(&own, idx.own_count, 1);
+    if (L->self_tally) rb.add(tally.data(), L->self_tally, 2 * TALLY_SLOTS);
     rb.run(s);
     if (st) {
         std::memset(st, 0, sizeof(*st));
@@ -2500,6 +2542,11 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         st->messages = idx.kept;
         st->self_terms = L->n;
         st->pairs = idx.segments + L->n - (int64_t)own;  // own-chunk segments carry their vertex's self message
+        if (L->self_in_transform) st->self_in_transform = L->n - (int64_t)own;
+        for (int i = 0; i < (int)tally.size(); i += 2) {
+            st->self_fresh += (int64_t)tally[(size_t)i];
+            st->self_last += (int64_t)tally[(size_t)i + 1];
+        }
         st->pending_left = (int64_t)left;
         st->completed = L->n - (int64_t)left;
         st->chunks = L->nchunks;

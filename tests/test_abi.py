@@ -79,7 +79,7 @@ def test_binding_structs_match_header_layout(native):
     assert native.LayerDesc.weight2.offset == 144 and native.LayerDesc.bias2.offset == 152
     assert native.LayerDesc.setup_stream.offset == 160
     assert ctypes.sizeof(native.LayerDesc) == 168
-    assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 2 * 8
+    assert ctypes.sizeof(native.Stats) == 17 * 8 + 7 * 8 + 4 * 8 + 5 * 8
 
 
 def test_binding_structs_match_compiled_header(native, tmp_path):

@@ -149,6 +149,47 @@ def test_chunk_order_invariance(torch_cuda):
     _check_model(w, outs, zs, "shuffled")
 
 
+def _expected_self_counts(src, dst, n, chunk, order):
+    """Vertices without an in-edge from their own chunk (their self message
+    is taken by the transform), and of those the ones whose self message
+    comes before / after every other message when chunks are pushed in
+    `order`: counted from the edge list."""
+    pos = np.empty(len(order), np.int64)
+    pos[np.asarray(order)] = np.arange(len(order))
+    own_pos = pos[np.arange(n) // chunk]
+    msg_pos = pos[src.astype(np.int64) // chunk]
+    own_seg = np.zeros(n, bool)
+    own_seg[dst[msg_pos == own_pos[dst]]] = True
+    first = np.full(n, len(order), np.int64)
+    last = np.full(n, -1, np.int64)
+    np.minimum.at(first, dst, msg_pos)
+    np.maximum.at(last, dst, msg_pos)
+    alone = ~own_seg
+    return (int(alone.sum()), int((alone & (first > own_pos)).sum()), int((alone & (last < own_pos)).sum()))
+
+
+@pytest.mark.parametrize("order", ["ascending", "shuffled"])
+def test_sage_self_messages_in_transform(torch_cuda, order):
+    """In-core GraphSAGE: the transform takes the self messages of vertices
+    with no in-edge from their own chunk; outputs match the oracle and the
+    layer's counts of those messages (all, into an empty row, completing the
+    vertex) match the edge list."""
+    w = WL.SAGE_RMAT_4K
+    chunk = 256
+    nch = w.n // chunk
+    seq = list(range(nch)) if order == "ascending" else [int(c) for c in np.random.default_rng(5).permutation(nch)]
+    _note(f"self messages in the transform, chunk {chunk}, order {order}")
+    src, dst = WL.graph(w)
+    _, zs = H.oracle_model(w, src, dst)
+    row_off, col_dst = H.gpu_graph(w, src, dst)
+    outs, stats = H.gpu_model(w, row_off, col_dst, chunk=chunk, order=seq, profile=True)
+    _check_model(w, outs, zs, f"chunk {chunk} {order}")
+    want = _expected_self_counts(src, dst, w.n, chunk, seq)
+    assert want[0] > 0 and want[1] > 0 and want[2] > 0, want
+    for st in stats:
+        assert (st["self_in_transform"], st["self_fresh"], st["self_last"]) == want
+
+
 def test_gcn_scaled_workload(torch_cuda):
     w = WL.GCN_RMAT_1M.scaled(30000, 400000, chunk=4096)
     _note(f"layers {w.name}")
