@@ -84,7 +84,12 @@ __global__ __launch_bounds__(256) void k_gemm_panel(const void* __restrict__ X, 
                                                     int Nc, const float* __restrict__ rscale,
                                                     float* __restrict__ Y, int stream, SelfFlush sf) {
     __shared__ PanelLds<DT, PANEL_NB> lds;
-    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, blockIdx.y, lds, stream != 0, sf);
+    // With self messages the column groups start at the first one holding
+    // self-half columns: those workgroups wait on accumulator rows, and
+    // dispatched first they overlap the purely streaming groups that follow
+    // instead of forming the launch's tail.
+    const int by = sf.own ? (int)((blockIdx.y + sf.self_col / (PANEL_NB * 16)) % gridDim.y) : (int)blockIdx.y;
+    gemm_panel_block<DT, PANEL_NB>(X, M, K, Wp, NBP, Nc, rscale, Y, blockIdx.x, by, lds, stream != 0, sf);
 }
 
 template <int DT>
