@@ -681,7 +681,7 @@ def sampled_scatter_bytes(st: dict, n: int, d_o: int, out_bytes: int, sage: bool
         raise ValueError("the byte model holds for layers without split segments")
     P = st["pairs"]
     A = st.get("self_in_transform", 0)
-    if A and not (st["self_fresh"] or st["self_last"]):
+    if A and min(st["self_fresh"], st["self_last"]) < 0:
         raise ValueError("the self-message counts are taken in profiled runs only")
     units = st["short_units"] + st["wave_units"]
     y_rows = n * (2 if sage else 1) - A

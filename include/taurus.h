@@ -245,8 +245,9 @@ typedef struct {
                                       the chunk transforms (vertices without a segment
                                       from their own chunk), 0 otherwise; counted in
                                       pairs                                             */
-    int64_t self_fresh, self_last; /* of those, when desc.profile != 0 (else 0): found
-                                      nothing accumulated yet / completed the vertex    */
+    int64_t self_fresh, self_last; /* of those, when desc.profile != 0: found nothing
+                                      accumulated yet / completed the vertex (-1 when
+                                      not counted, 0 for other layers)                  */
 } taurus_stats;
 
 /*

@@ -2542,7 +2542,10 @@ static int finalize(taurus_layer* L, taurus_stats* st) {
         st->messages = idx.kept;
         st->self_terms = L->n;
         st->pairs = idx.segments + L->n - (int64_t)own;  // own-chunk segments carry their vertex's self message
-        if (L->self_in_transform) st->self_in_transform = L->n - (int64_t)own;
+        if (L->self_in_transform) {
+            st->self_in_transform = L->n - (int64_t)own;
+            st->self_fresh = st->self_last = L->self_tally ? 0 : -1;  // -1: not counted
+        }
         for (int i = 0; i < (int)tally.size(); i += 2) {
             st->self_fresh += (int64_t)tally[(size_t)i];
             st->self_last += (int64_t)tally[(size_t)i + 1];

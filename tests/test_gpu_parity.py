@@ -188,6 +188,9 @@ def test_sage_self_messages_in_transform(torch_cuda, order):
     assert want[0] > 0 and want[1] > 0 and want[2] > 0, want
     for st in stats:
         assert (st["self_in_transform"], st["self_fresh"], st["self_last"]) == want
+    # without profiling the counts are not taken
+    _, stats = H.gpu_model(w, row_off, col_dst, chunk=chunk, order=seq)
+    assert all((st["self_in_transform"], st["self_fresh"], st["self_last"]) == (want[0], -1, -1) for st in stats)
 
 
 def test_gcn_scaled_workload(torch_cuda):
