@@ -19,6 +19,9 @@
 //   2. self pass: every vertex of the chunk adds its self row (the vertex's
 //      own message: the W_self half for GraphSAGE, its normalised row for
 //      GCN) to its accumulator -- a streaming pass over consecutive rows;
+//      a vertex with a segment from its own chunk takes it in that
+//      segment's flush instead, and in-core GraphSAGE layers add the others'
+//      in the transform (step 1), leaving the pass only their counts;
 //   3. scatter: per unit, the sum of its source rows scaled once by
 //      1/|M(v)| (the per-message normalisation of Sec. 3.4 applied to the
 //      segment sum) is added to v's fp32 accumulator; the pending count
